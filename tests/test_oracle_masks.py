@@ -1,0 +1,93 @@
+"""Pins the oracle's Case-III mask draw (Sec. 3.1): statistics, exact
+thresholds, the counter layout, determinism and stream independence."""
+import numpy as np
+import pytest
+
+from oracle import masks
+from oracle.philox import philox4x64
+
+
+def test_threshold_exact():
+    assert masks.drop_threshold(0.0) == 0
+    assert masks.drop_threshold(0.5) == 1 << 63
+    assert masks.drop_threshold(0.25) == 1 << 62
+    assert masks.drop_threshold(0.75) == 3 << 62
+    # 0.3 is not dyadic: floor of the exact binary64 value times 2^64
+    from fractions import Fraction
+    assert masks.drop_threshold(0.3) == (Fraction(0.3) * (1 << 64)).__floor__()
+    assert masks.drop_threshold(np.nextafter(1.0, 0.0)) == (1 << 64) - (1 << 11)
+    for bad in (-0.1, 1.0, 1.5):
+        with pytest.raises(ValueError):
+            masks.drop_threshold(bad)
+
+
+def test_counter_layout_brute_force():
+    seed, step, stream, T, K = 1234567, 3, 6, 5, 11
+    u = masks.uniform_words(seed, step, stream, T, K)
+    for t in range(T):
+        for k in range(K):
+            blk = philox4x64(np.array([k // 4, t, stream, step], dtype=np.uint64),
+                             (np.uint64(seed), np.uint64(0)))
+            assert u[t, k] == blk[k % 4]
+
+
+@pytest.mark.parametrize("p", [0.3, 0.5, 0.65, 0.7])
+def test_drop_fraction(p):
+    T, K = 1000, 1000
+    m = masks.keep_mask(42, 0, 2, T, K, p)
+    n = T * K
+    drop = n - int(m.sum())
+    sigma = np.sqrt(n * p * (1 - p))
+    assert abs(drop - n * p) < 5 * sigma
+    # each time step varies (Case-III randomised in time)
+    assert len({m[t].tobytes() for t in range(20)}) == 20
+
+
+def test_p_zero_keeps_all():
+    m = masks.keep_mask(1, 0, 0, 7, 33, 0.0)
+    assert m.all()
+
+
+def test_drop_decision_matches_threshold():
+    seed, step, stream, T, K, p = 99, 1, 4, 6, 50, 0.5
+    u = masks.uniform_words(seed, step, stream, T, K)
+    m = masks.keep_mask(seed, step, stream, T, K, p)
+    # p = 0.5: dropped iff the top bit of the word is clear
+    assert np.array_equal(m, (u >> np.uint64(63)).astype(np.uint8))
+
+
+def test_determinism_and_fresh_steps():
+    a = masks.keep_mask(5, 0, 0, 10, 100, 0.5)
+    b = masks.keep_mask(5, 0, 0, 10, 100, 0.5)
+    c = masks.keep_mask(5, 1, 0, 10, 100, 0.5)
+    assert np.array_equal(a, b)
+    assert not np.array_equal(a, c)
+
+
+def test_streams_independent():
+    T, K = 200, 1000
+    a = masks.keep_mask(7, 0, masks.nr_stream(0), T, K, 0.5).astype(np.float64).ravel()
+    b = masks.keep_mask(7, 0, masks.rh_stream(0, 0), T, K, 0.5).astype(np.float64).ravel()
+    c = masks.keep_mask(7, 0, masks.rh_stream(0, 1), T, K, 0.5).astype(np.float64).ravel()
+    n = a.size
+    for x, y in ((a, b), (a, c), (b, c)):
+        r = np.corrcoef(x, y)[0, 1]
+        assert abs(r) < 5 / np.sqrt(n)
+
+
+def test_keep_lists():
+    m = masks.keep_mask(3, 0, 0, 9, 37, 0.6)
+    lists, counts = masks.keep_lists(m)
+    for t in range(9):
+        assert np.all(np.diff(lists[t]) > 0)
+        assert counts[t] == m[t].sum()
+        assert np.all(m[t][lists[t]] == 1)
+
+
+def test_stream_ids_distinct():
+    ids = set()
+    for l in range(4):
+        ids.add(masks.nr_stream(l))
+        for d in range(2):
+            ids.add(masks.rh_stream(l, d))
+    assert len(ids) == 12
