@@ -1,0 +1,196 @@
+/*
+ * lstm_sd.h -- C ABI of a structured-dropout LSTM training step for AMD
+ * Instinct MI355X (gfx950).
+ *
+ * The method (Sec. 3 of "Structured in Space, Randomized in Time: Leveraging
+ * Dropout in RNNs for Efficient Training"): dropout masks are drawn per
+ * neuron and per time step and shared by every row of the batch (Case-III,
+ * Sec. 3.1).  A dropped input or recurrent neuron is then a whole row of the
+ * contraction dimension of the gate products (Eq. 1-4), so the forward
+ * products run on compacted operands (Sec. 3.2, FP paragraph), the input
+ * gradients of Eq. 10 are computed only for kept columns (BP paragraph) and
+ * the weight gradients of Eq. 11 only for kept rows (WG paragraph).
+ *
+ * Conventions shared by every entry point
+ *   - L layers, D directions (1 or 2), input dim I, hidden H, batch B,
+ *     sequence length T.  K_in(l) = I for l = 0, D*H above.
+ *   - Row-vector convention of Eq. 1-4: gate pre-activations a = x W + h U + b
+ *     with the 4H gate columns ordered i | f | g | o.
+ *   - W[l*D+d] is [K_in(l)][4H] and U[l*D+d] is [H][4H], row-major
+ *     ("K-major": a dropped input neuron k is the whole row k).
+ *     b[l*D+d] is [4H] float.
+ *   - Sequences are time-major: x is [T][B][I], y is [T][B][D*H].
+ *   - dtype 0: every tensor is float32.  dtype 1: x, W, U and h0 are
+ *     bfloat16 (raw 16-bit words); products accumulate in float32; c0, b, y,
+ *     hT, cT, dy and every gradient stay float32.
+ *   - Inverted dropout: a kept value is scaled by s = 1/(1-p) (s = 1 when
+ *     p = 0).  The non-recurrent (NR) mask of layer l multiplies that
+ *     layer's input (shared by both directions); the recurrent (RH) mask of
+ *     (l, d) multiplies only the copy of h_prev that enters U.  The cell
+ *     state is never dropped.
+ *   - compact = 1 skips dropped rows/columns (the method); compact = 0 runs
+ *     the same kernels over every row with the mask applied as a
+ *     multiplier (the dense baseline).  Both give the same result up to
+ *     floating-point summation order.
+ *   - Optional per-row lengths [B] (int32, device): rows freeze h and c and
+ *     output 0 from t = lengths[b] on; lengths outside [0, T] are clamped.
+ *
+ * Ownership and synchronisation
+ *   The caller owns every buffer.  All pointers named "device" are device
+ *   memory of the current HIP device, 16-byte aligned.  The library
+ *   allocates nothing.  Every call only enqueues work on `stream` (a
+ *   hipStream_t; NULL = the default stream) and returns; nothing inside a
+ *   call waits for the device, so calls can be captured into a HIP graph.
+ *   Calls that share a mask, reserve or workspace buffer must be ordered on
+ *   one stream.
+ *
+ * Errors
+ *   Every int-returning entry point returns LSTM_SD_OK (0) or a negative
+ *   code and then leaves a message for lstm_sd_last_error().  Arguments are
+ *   validated before any device work is enqueued.
+ */
+#ifndef LSTM_SD_H
+#define LSTM_SD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LSTM_SD_OK            0
+#define LSTM_SD_EINVAL       -1   /* null required pointer, bad dimension, p outside [0,1) */
+#define LSTM_SD_EUNSUPPORTED -2   /* dtype or a size beyond the library's limits */
+#define LSTM_SD_EHIP         -3   /* HIP launch/runtime error; message has the HIP error string */
+#define LSTM_SD_EWORKSPACE   -4   /* a buffer is smaller than its size query returned */
+
+#define LSTM_SD_DTYPE_F32  0
+#define LSTM_SD_DTYPE_BF16 1
+
+/* Limits: every K dimension (I, D*H, H) is at most LSTM_SD_MAX_K. */
+#define LSTM_SD_MAX_K 2048
+
+typedef struct {
+    int32_t num_layers;   /* L >= 1 */
+    int32_t input_dim;    /* I >= 1 */
+    int32_t hidden;       /* H >= 1 */
+    int32_t batch;        /* B >= 1 */
+    int32_t seq_len;      /* T >= 1 */
+    int32_t num_dirs;     /* D in {1, 2} */
+    int32_t dtype;        /* LSTM_SD_DTYPE_F32 or LSTM_SD_DTYPE_BF16 */
+    int32_t compact;      /* 1 = skip dropped rows (method), 0 = dense baseline */
+    double p_nr;          /* non-recurrent dropout rate, [0, 1) */
+    double p_rh;          /* recurrent dropout rate, [0, 1) */
+} lstm_sd_dims;
+
+/* Host arrays of L*D device pointers, index l*D + d. */
+typedef struct {
+    const void* const* W;    /* [K_in(l)][4H], dtype */
+    const void* const* U;    /* [H][4H], dtype */
+    const float* const* b;   /* [4H] */
+} lstm_sd_weights;
+
+/* Host arrays of L*D device pointers, index l*D + d; float32, overwritten. */
+typedef struct {
+    float* const* dW;        /* [K_in(l)][4H] */
+    float* const* dU;        /* [H][4H] */
+    float* const* db;        /* [4H] */
+} lstm_sd_grads;
+
+/* Byte offsets of the parts of a mask buffer (all relative to its start).
+ * Sites: the NR site of layer l is site l; the RH site of (l, d) is site
+ * L + l*D + d.  Site s has K(s) neurons (K_in(l) for NR, H for RH); rows are
+ * padded to kmax entries.
+ *   mask  uint8 [sites][T][kmax]  1 = kept, 0 = dropped
+ *   keep  int32 [sites][T][kmax]  ascending kept indices (compact = 1) or
+ *                                 0..K(s)-1 (compact = 0); entries past the
+ *                                 count are unspecified
+ *   pos   int32 [sites][T][kmax]  inverse of keep: position of neuron k in
+ *                                 keep, or -1 if k is not listed
+ *   count int32 [sites][T]        number of listed entries */
+typedef struct {
+    int32_t sites;
+    int32_t kmax;
+    int32_t seq_len;
+    int32_t reserved;
+    size_t mask_off, keep_off, pos_off, count_off, total_bytes;
+} lstm_sd_mask_layout;
+
+int         lstm_sd_version(void);
+const char* lstm_sd_last_error(void);
+
+/* Size queries; return 0 (and set the error) for invalid dims. */
+size_t lstm_sd_mask_bytes(const lstm_sd_dims* dims);
+size_t lstm_sd_reserve_bytes(const lstm_sd_dims* dims);
+size_t lstm_sd_workspace_bytes(const lstm_sd_dims* dims);
+int    lstm_sd_mask_layout_get(const lstm_sd_dims* dims, lstm_sd_mask_layout* out);
+
+/* Draw the Case-III masks of every site for one training step (Sec. 3.1:
+ * structured within the batch, fresh at every time step) and build the keep
+ * lists ("matrix compaction", Sec. 4).  Neuron k of a site with stream id
+ * `sid` at time t is dropped iff the 64-bit word number k%4 of
+ * Philox4x64-10(key = (seed, 0), counter = (k/4, t, sid, step)) is below
+ * floor(p * 2^64).  Stream ids: NR of layer l = 4l; RH of (l, d) = 4l+2+d.
+ * mask_buf: device, lstm_sd_mask_bytes(dims) bytes. */
+int lstm_sd_mask_generate(const lstm_sd_dims* dims, uint64_t seed, uint64_t step,
+                          void* mask_buf, size_t mask_bytes, void* stream);
+
+/* Rebuild keep, pos and count from the mask bytes already in mask_buf
+ * (written by the caller, e.g. to force a pattern). */
+int lstm_sd_mask_compact(const lstm_sd_dims* dims, void* mask_buf, size_t mask_bytes,
+                         void* stream);
+
+/* Forward unroll, Eq. 1-6 with the masks of mask_buf.
+ *   x        device [T][B][I], dtype
+ *   lengths  device [B] int32, or NULL (every row has length T)
+ *   h0       device [L*D][B][H], dtype;  c0 device [L*D][B][H] float
+ *   y        device [T][B][D*H] float: top layer output (0 at padded steps)
+ *   hT, cT   device [L*D][B][H] float: state after the last valid step
+ *   reserve  device, lstm_sd_reserve_bytes(dims): activations kept for
+ *            lstm_sd_backward
+ *   workspace device, lstm_sd_workspace_bytes(dims) */
+int lstm_sd_forward(const lstm_sd_dims* dims, const lstm_sd_weights* w,
+                    const void* x, const int32_t* lengths,
+                    const void* h0, const float* c0,
+                    const void* mask_buf, size_t mask_bytes,
+                    float* y, float* hT, float* cT,
+                    void* reserve, size_t reserve_bytes,
+                    void* workspace, size_t workspace_bytes, void* stream);
+
+/* Back-propagation through time, Eq. 7-11, for the forward pass that filled
+ * `reserve` (same dims, weights, x, lengths, h0, c0 and masks).
+ *   dy       device [T][B][D*H] float: dLoss/dy
+ *   dhT, dcT device [L*D][B][H] float, or NULL for zero
+ *   dx       device [T][B][I] float, or NULL to skip the input gradient of
+ *            layer 0; dropped columns are written as exact zeros
+ *   dh0, dc0 device [L*D][B][H] float
+ *   g        gradients, overwritten (rows of never-kept neurons are 0) */
+int lstm_sd_backward(const lstm_sd_dims* dims, const lstm_sd_weights* w,
+                     const void* x, const int32_t* lengths,
+                     const void* h0, const float* c0,
+                     const void* mask_buf, size_t mask_bytes,
+                     const void* reserve, size_t reserve_bytes,
+                     const float* dy, const float* dhT, const float* dcT,
+                     float* dx, float* dh0, float* dc0, const lstm_sd_grads* g,
+                     void* workspace, size_t workspace_bytes, void* stream);
+
+/* Mean-squared-error loss of y against target over valid (t, b) and all
+ * D*H features, and its gradient: loss = sum (y-target)^2 / N,
+ * dy = 2 (y - target) / N at valid positions and 0 elsewhere, with N =
+ * (number of valid (t, b)) * D*H.  A loss of the workloads, not of the
+ * paper (its tasks need datasets).
+ *   y, target  device [T][B][D*H] float;  lengths device [B] or NULL
+ *   dy         device [T][B][D*H] float (written)
+ *   loss       device float[1] (written)
+ *   workspace  device, lstm_sd_workspace_bytes(dims); only its last 16 KiB
+ *              are used, so the same buffer can be shared with the step. */
+int lstm_sd_mse_grad(const lstm_sd_dims* dims, const float* y, const float* target,
+                     const int32_t* lengths, float* dy, float* loss,
+                     void* workspace, size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LSTM_SD_H */

@@ -1,0 +1,204 @@
+"""ctypes binding of liblstm_sd.so (C ABI in include/lstm_sd.h).
+
+Argument marshalling only: every step of the computation runs in the
+library's HIP kernels.  Functions keep the C names; device buffers are passed
+as torch tensors (their data pointers are handed to the library) and the
+stream defaults to torch's current stream.  A missing library raises: there
+is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+from . import build as _build
+
+LIB_PATH = _build.LIB
+
+OK, EINVAL, EUNSUPPORTED, EHIP, EWORKSPACE = 0, -1, -2, -3, -4
+DTYPE_F32, DTYPE_BF16 = 0, 1
+MAX_K = 2048
+
+
+class lstm_sd_dims(ctypes.Structure):
+    _fields_ = [("num_layers", ctypes.c_int32), ("input_dim", ctypes.c_int32),
+                ("hidden", ctypes.c_int32), ("batch", ctypes.c_int32),
+                ("seq_len", ctypes.c_int32), ("num_dirs", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("compact", ctypes.c_int32),
+                ("p_nr", ctypes.c_double), ("p_rh", ctypes.c_double)]
+
+
+class lstm_sd_weights(ctypes.Structure):
+    _fields_ = [("W", ctypes.POINTER(ctypes.c_void_p)), ("U", ctypes.POINTER(ctypes.c_void_p)),
+                ("b", ctypes.POINTER(ctypes.c_void_p))]
+
+
+class lstm_sd_grads(ctypes.Structure):
+    _fields_ = [("dW", ctypes.POINTER(ctypes.c_void_p)), ("dU", ctypes.POINTER(ctypes.c_void_p)),
+                ("db", ctypes.POINTER(ctypes.c_void_p))]
+
+
+class lstm_sd_mask_layout(ctypes.Structure):
+    _fields_ = [("sites", ctypes.c_int32), ("kmax", ctypes.c_int32), ("seq_len", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("mask_off", ctypes.c_size_t),
+                ("keep_off", ctypes.c_size_t), ("pos_off", ctypes.c_size_t),
+                ("count_off", ctypes.c_size_t), ("total_bytes", ctypes.c_size_t)]
+
+
+_P = ctypes.c_void_p
+_SZ = ctypes.c_size_t
+_DIMS = ctypes.POINTER(lstm_sd_dims)
+
+# name -> (restype, argtypes); the header's declarations
+SIGNATURES = {
+    "lstm_sd_version": (ctypes.c_int, []),
+    "lstm_sd_last_error": (ctypes.c_char_p, []),
+    "lstm_sd_mask_bytes": (_SZ, [_DIMS]),
+    "lstm_sd_reserve_bytes": (_SZ, [_DIMS]),
+    "lstm_sd_workspace_bytes": (_SZ, [_DIMS]),
+    "lstm_sd_mask_layout_get": (ctypes.c_int, [_DIMS, ctypes.POINTER(lstm_sd_mask_layout)]),
+    "lstm_sd_mask_generate": (ctypes.c_int, [_DIMS, ctypes.c_uint64, ctypes.c_uint64, _P, _SZ, _P]),
+    "lstm_sd_mask_compact": (ctypes.c_int, [_DIMS, _P, _SZ, _P]),
+    "lstm_sd_forward": (ctypes.c_int, [_DIMS, ctypes.POINTER(lstm_sd_weights), _P, _P, _P, _P, _P, _SZ,
+                                       _P, _P, _P, _P, _SZ, _P, _SZ, _P]),
+    "lstm_sd_backward": (ctypes.c_int, [_DIMS, ctypes.POINTER(lstm_sd_weights), _P, _P, _P, _P, _P, _SZ,
+                                        _P, _SZ, _P, _P, _P, _P, _P, _P, ctypes.POINTER(lstm_sd_grads),
+                                        _P, _SZ, _P]),
+    "lstm_sd_mse_grad": (ctypes.c_int, [_DIMS, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+}
+
+_lib = None
+
+
+def load(path: str = LIB_PATH):
+    """Load the library (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with paper_2106_12089_amd.build.build() "
+                           "(no fallback implementation exists)")
+    lib = ctypes.CDLL(path)
+    for name, (res, args) in SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+class LstmSdError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"lstm_sd error {code}: {msg}")
+        self.code = code
+
+
+def _check(rc):
+    if rc != OK:
+        raise LstmSdError(rc, load().lstm_sd_last_error().decode())
+    return rc
+
+
+def make_dims(num_layers, input_dim, hidden, batch, seq_len, num_dirs=1, dtype=DTYPE_BF16,
+              compact=1, p_nr=0.0, p_rh=0.0) -> lstm_sd_dims:
+    return lstm_sd_dims(num_layers, input_dim, hidden, batch, seq_len, num_dirs, dtype, compact,
+                        float(p_nr), float(p_rh))
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is not None:
+        return stream if isinstance(stream, int) else stream.cuda_stream
+    import torch
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _ptr_array(ts):
+    arr = (ctypes.c_void_p * len(ts))(*[_ptr(t) for t in ts])
+    return arr
+
+
+# --- size queries -----------------------------------------------------------
+def lstm_sd_version() -> int:
+    return load().lstm_sd_version()
+
+
+def lstm_sd_last_error() -> str:
+    return load().lstm_sd_last_error().decode()
+
+
+def lstm_sd_mask_bytes(dims) -> int:
+    n = load().lstm_sd_mask_bytes(ctypes.byref(dims))
+    if n == 0:
+        raise LstmSdError(EINVAL, lstm_sd_last_error())
+    return n
+
+
+def lstm_sd_reserve_bytes(dims) -> int:
+    n = load().lstm_sd_reserve_bytes(ctypes.byref(dims))
+    if n == 0:
+        raise LstmSdError(EINVAL, lstm_sd_last_error())
+    return n
+
+
+def lstm_sd_workspace_bytes(dims) -> int:
+    n = load().lstm_sd_workspace_bytes(ctypes.byref(dims))
+    if n == 0:
+        raise LstmSdError(EINVAL, lstm_sd_last_error())
+    return n
+
+
+def lstm_sd_mask_layout_get(dims) -> lstm_sd_mask_layout:
+    out = lstm_sd_mask_layout()
+    _check(load().lstm_sd_mask_layout_get(ctypes.byref(dims), ctypes.byref(out)))
+    return out
+
+
+# --- device calls -------------------------------------------------------------
+def lstm_sd_mask_generate(dims, seed, step, mask_buf, stream=None):
+    _check(load().lstm_sd_mask_generate(ctypes.byref(dims), ctypes.c_uint64(seed & (2**64 - 1)),
+                                        ctypes.c_uint64(step), _ptr(mask_buf),
+                                        mask_buf.numel() * mask_buf.element_size(), _stream(stream)))
+
+
+def lstm_sd_mask_compact(dims, mask_buf, stream=None):
+    _check(load().lstm_sd_mask_compact(ctypes.byref(dims), _ptr(mask_buf),
+                                       mask_buf.numel() * mask_buf.element_size(), _stream(stream)))
+
+
+def _nbytes(t):
+    return t.numel() * t.element_size()
+
+
+def lstm_sd_forward(dims, W, U, b, x, lengths, h0, c0, mask_buf, y, hT, cT, reserve, workspace,
+                    stream=None):
+    keep = (_ptr_array(W), _ptr_array(U), _ptr_array(b))
+    w = lstm_sd_weights(keep[0], keep[1], keep[2])
+    _check(load().lstm_sd_forward(ctypes.byref(dims), ctypes.byref(w), _ptr(x), _ptr(lengths), _ptr(h0),
+                                  _ptr(c0), _ptr(mask_buf), _nbytes(mask_buf), _ptr(y), _ptr(hT), _ptr(cT),
+                                  _ptr(reserve), _nbytes(reserve), _ptr(workspace), _nbytes(workspace),
+                                  _stream(stream)))
+
+
+def lstm_sd_backward(dims, W, U, b, x, lengths, h0, c0, mask_buf, reserve, dy, dhT, dcT, dx, dh0, dc0,
+                     dW, dU, db, workspace, stream=None):
+    keep = (_ptr_array(W), _ptr_array(U), _ptr_array(b), _ptr_array(dW), _ptr_array(dU), _ptr_array(db))
+    w = lstm_sd_weights(keep[0], keep[1], keep[2])
+    g = lstm_sd_grads(keep[3], keep[4], keep[5])
+    _check(load().lstm_sd_backward(ctypes.byref(dims), ctypes.byref(w), _ptr(x), _ptr(lengths), _ptr(h0),
+                                   _ptr(c0), _ptr(mask_buf), _nbytes(mask_buf), _ptr(reserve),
+                                   _nbytes(reserve), _ptr(dy), _ptr(dhT), _ptr(dcT), _ptr(dx), _ptr(dh0),
+                                   _ptr(dc0), ctypes.byref(g), _ptr(workspace), _nbytes(workspace),
+                                   _stream(stream)))
+
+
+def lstm_sd_mse_grad(dims, y, target, lengths, dy, loss, workspace, stream=None):
+    _check(load().lstm_sd_mse_grad(ctypes.byref(dims), _ptr(y), _ptr(target), _ptr(lengths), _ptr(dy),
+                                   _ptr(loss), _ptr(workspace), _nbytes(workspace), _stream(stream)))

@@ -1,0 +1,451 @@
+// C ABI of the structured-dropout LSTM step: validation, buffer layout and
+// the launch sequence of forward and backward.
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+
+#include "../../include/lstm_sd.h"
+#include "device.h"
+#include "kernels.h"
+#include "plan.h"
+
+namespace lsd {
+
+void launch_mask_build(const MaskArgs& a, int sites, hipStream_t st);
+template <typename T> void launch_fx(const FxArgs& a, hipStream_t st);
+template <typename T> void launch_step(const StepArgs& a, int D, hipStream_t st);
+template <typename T> void launch_bwd_pw(const BwdPwArgs& a, int D, hipStream_t st);
+template <typename T> void launch_bwd_dh(const DhArgs& a, int D, int H, hipStream_t st);
+template <typename T> void launch_dx(const DxArgs& a, int K, hipStream_t st);
+template <typename T> void launch_wgrad(const WgArgs& a, hipStream_t st);
+template <typename T> void launch_fwd_init(const void*, const float*, float*, float*, long, hipStream_t);
+void launch_bwd_init(const float*, const float*, float*, float*, long, hipStream_t);
+void launch_bwd_final(const FinalArgs& a, int D, hipStream_t st);
+void launch_expand(const float*, int, const SiteView&, float*, int, int, int, hipStream_t);
+void launch_db(const float*, float*, int, int, hipStream_t);
+void launch_mse(const float*, const float*, const int32_t*, float*, float*, int, float*, int, int, int,
+                hipStream_t);
+int setup_kernel_attributes();
+
+static thread_local std::string g_err;
+
+static int fail(int code, const std::string& msg) {
+    g_err = msg;
+    return code;
+}
+
+static float inv_keep(double p) { return p > 0.0 ? (float)(1.0 / (1.0 - p)) : 1.0f; }
+
+int make_plan(const lstm_sd_dims* d, Plan* p, const char** why) {
+    if (!d) { *why = "dims is NULL"; return LSTM_SD_EINVAL; }
+    if (d->num_layers < 1 || d->input_dim < 1 || d->hidden < 1 || d->batch < 1 || d->seq_len < 1) {
+        *why = "dimensions must be >= 1"; return LSTM_SD_EINVAL;
+    }
+    if (d->num_dirs != 1 && d->num_dirs != 2) { *why = "num_dirs must be 1 or 2"; return LSTM_SD_EINVAL; }
+    if (!(d->p_nr >= 0.0 && d->p_nr < 1.0) || !(d->p_rh >= 0.0 && d->p_rh < 1.0)) {
+        *why = "dropout rates must be in [0, 1)"; return LSTM_SD_EINVAL;
+    }
+    if (d->compact != 0 && d->compact != 1) { *why = "compact must be 0 or 1"; return LSTM_SD_EINVAL; }
+    if (d->dtype != LSTM_SD_DTYPE_F32 && d->dtype != LSTM_SD_DTYPE_BF16) {
+        *why = "dtype must be 0 (f32) or 1 (bf16)"; return LSTM_SD_EUNSUPPORTED;
+    }
+    if (d->num_layers > 16) { *why = "at most 16 layers"; return LSTM_SD_EUNSUPPORTED; }
+    const long kin1 = (long)d->num_dirs * d->hidden;
+    if (d->input_dim > LSTM_SD_MAX_K || kin1 > LSTM_SD_MAX_K || d->hidden > LSTM_SD_MAX_K) {
+        *why = "input_dim, hidden and num_dirs*hidden must be <= LSTM_SD_MAX_K"; return LSTM_SD_EUNSUPPORTED;
+    }
+    if ((long)d->batch * d->seq_len > (1L << 24) || d->batch > 65536 || d->seq_len > 65535) {
+        *why = "batch*seq_len too large"; return LSTM_SD_EUNSUPPORTED;
+    }
+    Plan& q = *p;
+    q.L = d->num_layers; q.I = d->input_dim; q.H = d->hidden; q.B = d->batch; q.T = d->seq_len;
+    q.D = d->num_dirs; q.dtype = d->dtype; q.compact = d->compact;
+    q.p_nr = d->p_nr; q.p_rh = d->p_rh;
+    q.s_nr = inv_keep(d->p_nr); q.s_rh = inv_keep(d->p_rh);
+    q.esize = d->dtype == LSTM_SD_DTYPE_BF16 ? 2 : 4;
+    q.G = 4 * q.H;
+    q.sites = q.L + q.L * q.D;
+    q.kin_max = q.L > 1 ? (q.I > q.D * q.H ? q.I : q.D * q.H) : q.I;
+    q.kmax = q.kin_max > q.H ? q.kin_max : q.H;
+
+    const size_t A = 256, T = q.T, B = q.B, H = q.H, G = q.G, D = q.D;
+    size_t off = 0;
+    q.m_mask = off;  off = align_up(off + (size_t)q.sites * T * q.kmax, A);
+    q.m_keep = off;  off = align_up(off + (size_t)q.sites * T * q.kmax * 4, A);
+    q.m_pos = off;   off = align_up(off + (size_t)q.sites * T * q.kmax * 4, A);
+    q.m_count = off; off = align_up(off + (size_t)q.sites * T * 4, A);
+    q.m_total = off;
+
+    off = 0;
+    q.r_gates = off; off = align_up(off + T * B * G * 4, A);
+    q.r_c = off;     off = align_up(off + T * B * H * 4, A);
+    q.r_hrec = off;  off = align_up(off + T * B * H * q.esize, A);
+    q.r_dir_bytes = off;
+    q.r_ybuf_base = (size_t)q.L * q.D * q.r_dir_bytes;
+    q.r_ybuf_bytes = align_up(T * B * D * H * q.esize, A);
+    q.r_total = q.r_ybuf_base + (size_t)(q.L - 1) * q.r_ybuf_bytes;
+
+    size_t fwd = align_up(D * T * B * G * 4, A);
+    q.w_gx = 0;
+    off = 0;
+    q.w_da = off;     off = align_up(off + D * T * B * G * q.esize, A);
+    q.w_dbpart = off; off = align_up(off + D * T * G * 4, A);
+    q.w_dhrec = off;  off = align_up(off + D * 2 * B * H * 4, A);
+    q.w_dc = off;     off = align_up(off + D * B * H * 4, A);
+    q.w_dhc = off;    off = align_up(off + D * B * H * 4, A);
+    q.w_dxc = off;    off = align_up(off + 2 * T * B * (size_t)q.kin_max * 4, A);
+    q.w_bwd_end = off;
+    size_t body = fwd > off ? fwd : off;
+    q.w_loss = align_up(body, A);
+    q.w_total = q.w_loss + 16384;
+    return LSTM_SD_OK;
+}
+
+static int hip_check(const char* where) {
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return fail(LSTM_SD_EHIP, std::string(where) + ": " + hipGetErrorString(e));
+    return LSTM_SD_OK;
+}
+
+static SiteView site_view(const Plan& P, const void* mbuf, int s) {
+    const char* m = (const char*)mbuf;
+    SiteView v;
+    v.mask = (const uint8_t*)(m + P.mask_at(s, 0));
+    v.keep = (const int32_t*)(m + P.keep_at(s, 0));
+    v.pos = (const int32_t*)(m + P.pos_at(s, 0));
+    v.count = (const int32_t*)(m + P.count_at(s));
+    v.kmax = P.kmax;
+    return v;
+}
+
+static uint64_t threshold64(double p) {
+    // floor(p * 2^64), exact: p = mant * 2^exp with a 53-bit integer mantissa
+    if (p <= 0.0) return 0;
+    int e;
+    double m = frexp(p, &e);                 // p = m * 2^e, 0.5 <= m < 1
+    uint64_t mant = (uint64_t)ldexp(m, 53);  // exact
+    int sh = e + 64 - 53;                    // p * 2^64 = mant * 2^sh
+    if (sh >= 0) return sh >= 64 ? 0 : (mant << sh);
+    return -sh >= 64 ? 0 : (mant >> (-sh));
+}
+
+static int do_masks(const lstm_sd_dims* dims, uint64_t seed, uint64_t step, void* mbuf, size_t mbytes,
+                    void* stream, int generate) {
+    Plan P;
+    const char* why = nullptr;
+    int rc = make_plan(dims, &P, &why);
+    if (rc) return fail(rc, why);
+    if (!mbuf) return fail(LSTM_SD_EINVAL, "mask_buf is NULL");
+    if (mbytes < P.m_total) return fail(LSTM_SD_EWORKSPACE, "mask_bytes smaller than lstm_sd_mask_bytes()");
+    MaskArgs a;
+    memset(&a, 0, sizeof(a));
+    char* m = (char*)mbuf;
+    a.mask = (uint8_t*)(m + P.m_mask);
+    a.keep = (int32_t*)(m + P.m_keep);
+    a.pos = (int32_t*)(m + P.m_pos);
+    a.count = (int32_t*)(m + P.m_count);
+    a.T = P.T; a.kmax = P.kmax; a.compact = P.compact; a.generate = generate;
+    a.seed = seed; a.step = step;
+    for (int s = 0; s < P.sites; ++s) {
+        a.K[s] = P.site_k(s);
+        a.sid[s] = P.stream_id(s);
+        a.thr[s] = threshold64(s < P.L ? P.p_nr : P.p_rh);
+    }
+    launch_mask_build(a, P.sites, (hipStream_t)stream);
+    return hip_check("mask kernel launch");
+}
+
+template <typename E>
+static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, const int32_t* lengths,
+                        const void* h0, const float* c0, const void* mbuf, float* y, float* hT, float* cT,
+                        void* reserve, void* ws, hipStream_t st) {
+    const int L = P.L, D = P.D, T = P.T, B = P.B, H = P.H, G = P.G;
+    char* R = (char*)reserve;
+    char* W = (char*)ws;
+    launch_fwd_init<E>(h0, c0, hT, cT, (long)L * D * B * H, st);
+    for (int l = 0; l < L; ++l) {
+        const int kin = P.kin(l);
+        const void* X = l == 0 ? x : (const void*)(R + P.rybuf(l - 1));
+        for (int d = 0; d < D; ++d) {
+            FxArgs f;
+            f.X = X; f.ldx = kin;
+            f.W = w->W[l * D + d];
+            f.bias = w->b[l * D + d];
+            f.site = site_view(P, mbuf, P.site_nr(l));
+            f.Gx = (float*)(W + P.w_gx) + (size_t)d * T * B * G;
+            f.B = B; f.N = G; f.T = T; f.s = P.s_nr;
+            launch_fx<E>(f, st);
+        }
+        for (int s = 0; s < T; ++s) {
+            StepArgs a;
+            memset(&a, 0, sizeof(a));
+            a.lengths = lengths; a.B = B; a.H = H; a.ldy = D * H; a.s = P.s_rh;
+            for (int d = 0; d < D; ++d) {
+                const int k = l * D + d;
+                const int t = d == 0 ? s : T - 1 - s;
+                const int tp = d == 0 ? t - 1 : t + 1;
+                char* rd = R + P.rdir(l, d);
+                StepDir& sd = a.d[d];
+                sd.t = t;
+                sd.hprev = s == 0 ? (const void*)((const char*)h0 + (size_t)k * B * H * P.esize)
+                                  : (const void*)(rd + P.r_hrec + (size_t)tp * B * H * P.esize);
+                sd.U = w->U[k];
+                sd.gx = (const float*)(W + P.w_gx) + ((size_t)d * T + t) * B * G;
+                SiteView sv = site_view(P, mbuf, P.site_rh(l, d));
+                sd.mask = sv.mask + (size_t)t * P.kmax;
+                sd.keep = sv.keep + (size_t)t * P.kmax;
+                sd.count = sv.count + t;
+                sd.gates = (float*)(rd + P.r_gates) + (size_t)t * B * G;
+                sd.cres = (float*)(rd + P.r_c) + (size_t)t * B * H;
+                sd.hrec = rd + P.r_hrec + (size_t)t * B * H * P.esize;
+                sd.hT = hT + (size_t)k * B * H;
+                sd.cT = cT + (size_t)k * B * H;
+                sd.y = (l == L - 1) ? y + (size_t)t * B * D * H + d * H : nullptr;
+                sd.ybuf = (l < L - 1) ? (void*)(R + P.rybuf(l) + ((size_t)t * B * D * H + d * H) * P.esize)
+                                      : nullptr;
+            }
+            launch_step<E>(a, D, st);
+        }
+    }
+    return hip_check("forward launch");
+}
+
+template <typename E>
+static int backward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, const int32_t* lengths,
+                         const void* h0, const float* c0, const void* mbuf, const void* reserve,
+                         const float* dy, const float* dhT, const float* dcT, float* dx, float* dh0,
+                         float* dc0, const lstm_sd_grads* g, void* ws, hipStream_t st) {
+    const int L = P.L, D = P.D, T = P.T, B = P.B, H = P.H, G = P.G;
+    const char* R = (const char*)reserve;
+    char* W = (char*)ws;
+    for (int l = L - 1; l >= 0; --l) {
+        const int kin = P.kin(l);
+        float* dhc = (float*)(W + P.w_dhc);
+        float* dcs = (float*)(W + P.w_dc);
+        launch_bwd_init(dhT ? dhT + (size_t)l * D * B * H : nullptr, dcT ? dcT + (size_t)l * D * B * H : nullptr,
+                        dhc, dcs, (long)D * B * H, st);
+        float* dhrec = (float*)(W + P.w_dhrec);               // [D][2][B][H]
+        float* dxc_above = (float*)(W + P.w_dxc) + (size_t)((l + 1) & 1) * T * B * P.kin_max;
+        float* dxc_here = (float*)(W + P.w_dxc) + (size_t)(l & 1) * T * B * P.kin_max;
+        for (int s = 0; s < T; ++s) {
+            BwdPwArgs a;
+            memset(&a, 0, sizeof(a));
+            a.lengths = lengths; a.B = B; a.H = H; a.ldy = D * H;
+            a.lddx = l + 1 < L ? P.kin(l + 1) : 0;
+            DhArgs h;
+            memset(&h, 0, sizeof(h));
+            h.B = B; h.G = G; h.ldo = H; h.s = P.s_rh;
+            for (int d = 0; d < D; ++d) {
+                const int k = l * D + d;
+                const int t = d == 0 ? T - 1 - s : s;         // BP order: reverse of FP order
+                const int tn = d == 0 ? t + 1 : t - 1;        // step processed just before
+                const int tp = d == 0 ? t - 1 : t + 1;        // forward predecessor
+                const char* rd = R + P.rdir(l, d);
+                BwdPwDir& pd = a.d[d];
+                pd.t = t;
+                pd.gates = (const float*)(rd + P.r_gates) + (size_t)t * B * G;
+                pd.cres = (const float*)(rd + P.r_c) + (size_t)t * B * H;
+                pd.cprev = s == T - 1 ? c0 + (size_t)k * B * H : (const float*)(rd + P.r_c) + (size_t)tp * B * H;
+                if (l == L - 1) {
+                    pd.dy = dy + (size_t)t * B * D * H + d * H;
+                } else {
+                    SiteView sv = site_view(P, mbuf, P.site_nr(l + 1));
+                    pd.dxc = dxc_above + (size_t)t * B * a.lddx;
+                    pd.dxpos = sv.pos + (size_t)t * P.kmax + d * H;
+                }
+                if (s > 0) {
+                    SiteView sv = site_view(P, mbuf, P.site_rh(l, d));
+                    pd.dhrec = dhrec + ((size_t)d * 2 + (s & 1)) * B * H;
+                    pd.rhpos = sv.pos + (size_t)tn * P.kmax;
+                }
+                pd.dhc = dhc + (size_t)d * B * H;
+                pd.dcs = dcs + (size_t)d * B * H;
+                pd.da = W + P.w_da + ((size_t)d * T + t) * B * G * P.esize;
+                pd.dbpart = (float*)(W + P.w_dbpart) + ((size_t)d * T + t) * G;
+
+                SiteView rv = site_view(P, mbuf, P.site_rh(l, d));
+                DhDir& hd = h.d[d];
+                hd.da = pd.da;
+                hd.Wk = w->U[k];
+                hd.mask = rv.mask + (size_t)t * P.kmax;
+                hd.keep = rv.keep + (size_t)t * P.kmax;
+                hd.count = rv.count + t;
+                hd.out = dhrec + ((size_t)d * 2 + ((s + 1) & 1)) * B * H;
+            }
+            launch_bwd_pw<E>(a, D, st);
+            launch_bwd_dh<E>(h, D, H, st);
+        }
+        {
+            FinalArgs f;
+            memset(&f, 0, sizeof(f));
+            f.B = B; f.H = H;
+            for (int d = 0; d < D; ++d) {
+                const int k = l * D + d;
+                const int t0 = d == 0 ? 0 : T - 1;
+                SiteView rv = site_view(P, mbuf, P.site_rh(l, d));
+                f.d[d].dhrec = dhrec + ((size_t)d * 2 + (T & 1)) * B * H;
+                f.d[d].rhpos = rv.pos + (size_t)t0 * P.kmax;
+                f.d[d].dhc = dhc + (size_t)d * B * H;
+                f.d[d].dcs = dcs + (size_t)d * B * H;
+                f.d[d].dh0 = dh0 + (size_t)k * B * H;
+                f.d[d].dc0 = dc0 + (size_t)k * B * H;
+            }
+            launch_bwd_final(f, D, st);
+        }
+        const SiteView nv = site_view(P, mbuf, P.site_nr(l));
+        if (l > 0 || dx) {
+            DxArgs a;
+            memset(&a, 0, sizeof(a));
+            for (int d = 0; d < D; ++d) {
+                a.da[d] = W + P.w_da + (size_t)d * T * B * G * P.esize;
+                a.W[d] = w->W[l * D + d];
+            }
+            a.site = nv; a.out = dxc_here; a.D = D; a.B = B; a.G = G; a.ldo = kin; a.T = T; a.s = P.s_nr;
+            launch_dx<E>(a, kin, st);
+            if (l == 0) launch_expand(dxc_here, kin, nv, dx, B, kin, T, st);
+        }
+        const void* X = l == 0 ? x : (const void*)(R + P.rybuf(l - 1));
+        for (int d = 0; d < D; ++d) {
+            const int k = l * D + d;
+            const char* rd = R + P.rdir(l, d);
+            WgArgs a;
+            memset(&a, 0, sizeof(a));
+            a.act = X; a.act_tstride = (long)B * kin; a.act_ld = kin;
+            a.act_first = nullptr; a.t_first = -1; a.act_shift = 0;
+            a.da = W + P.w_da + (size_t)d * T * B * G * P.esize;
+            a.site = nv; a.dW = g->dW[k]; a.K = kin; a.B = B; a.G = G; a.T = T; a.s = P.s_nr;
+            launch_wgrad<E>(a, st);
+
+            WgArgs u = a;
+            u.act = rd + P.r_hrec; u.act_tstride = (long)B * H; u.act_ld = H;
+            u.act_first = (const char*)h0 + (size_t)k * B * H * P.esize;
+            u.t_first = d == 0 ? 0 : T - 1;
+            u.act_shift = d == 0 ? -1 : 1;
+            u.site = site_view(P, mbuf, P.site_rh(l, d));
+            u.dW = g->dU[k]; u.K = H; u.s = P.s_rh;
+            launch_wgrad<E>(u, st);
+
+            launch_db((const float*)(W + P.w_dbpart) + (size_t)d * T * G, g->db[k], G, T, st);
+        }
+    }
+    return hip_check("backward launch");
+}
+
+}  // namespace lsd
+
+using namespace lsd;
+
+extern "C" {
+
+int lstm_sd_version(void) { return 1; }
+
+const char* lstm_sd_last_error(void) { return g_err.c_str(); }
+
+size_t lstm_sd_mask_bytes(const lstm_sd_dims* dims) {
+    Plan P; const char* why = nullptr;
+    int rc = make_plan(dims, &P, &why);
+    if (rc) { fail(rc, why); return 0; }
+    return P.m_total;
+}
+
+size_t lstm_sd_reserve_bytes(const lstm_sd_dims* dims) {
+    Plan P; const char* why = nullptr;
+    int rc = make_plan(dims, &P, &why);
+    if (rc) { fail(rc, why); return 0; }
+    return P.r_total;
+}
+
+size_t lstm_sd_workspace_bytes(const lstm_sd_dims* dims) {
+    Plan P; const char* why = nullptr;
+    int rc = make_plan(dims, &P, &why);
+    if (rc) { fail(rc, why); return 0; }
+    return P.w_total;
+}
+
+int lstm_sd_mask_layout_get(const lstm_sd_dims* dims, lstm_sd_mask_layout* out) {
+    Plan P; const char* why = nullptr;
+    int rc = make_plan(dims, &P, &why);
+    if (rc) return fail(rc, why);
+    if (!out) return fail(LSTM_SD_EINVAL, "out is NULL");
+    out->sites = P.sites; out->kmax = P.kmax; out->seq_len = P.T; out->reserved = 0;
+    out->mask_off = P.m_mask; out->keep_off = P.m_keep; out->pos_off = P.m_pos;
+    out->count_off = P.m_count; out->total_bytes = P.m_total;
+    return LSTM_SD_OK;
+}
+
+int lstm_sd_mask_generate(const lstm_sd_dims* dims, uint64_t seed, uint64_t step, void* mask_buf,
+                          size_t mask_bytes, void* stream) {
+    return do_masks(dims, seed, step, mask_buf, mask_bytes, stream, 1);
+}
+
+int lstm_sd_mask_compact(const lstm_sd_dims* dims, void* mask_buf, size_t mask_bytes, void* stream) {
+    return do_masks(dims, 0, 0, mask_buf, mask_bytes, stream, 0);
+}
+
+int lstm_sd_forward(const lstm_sd_dims* dims, const lstm_sd_weights* w, const void* x, const int32_t* lengths,
+                    const void* h0, const float* c0, const void* mask_buf, size_t mask_bytes, float* y,
+                    float* hT, float* cT, void* reserve, size_t reserve_bytes, void* workspace,
+                    size_t workspace_bytes, void* stream) {
+    Plan P; const char* why = nullptr;
+    int rc = make_plan(dims, &P, &why);
+    if (rc) return fail(rc, why);
+    if (!w || !w->W || !w->U || !w->b) return fail(LSTM_SD_EINVAL, "weights is NULL");
+    for (int k = 0; k < P.L * P.D; ++k)
+        if (!w->W[k] || !w->U[k] || !w->b[k]) return fail(LSTM_SD_EINVAL, "a weight pointer is NULL");
+    if (!x || !h0 || !c0 || !mask_buf || !y || !hT || !cT || !reserve || !workspace)
+        return fail(LSTM_SD_EINVAL, "a required pointer is NULL");
+    if (mask_bytes < P.m_total) return fail(LSTM_SD_EWORKSPACE, "mask_bytes smaller than lstm_sd_mask_bytes()");
+    if (reserve_bytes < P.r_total) return fail(LSTM_SD_EWORKSPACE, "reserve_bytes smaller than lstm_sd_reserve_bytes()");
+    if (workspace_bytes < P.w_total) return fail(LSTM_SD_EWORKSPACE, "workspace_bytes smaller than lstm_sd_workspace_bytes()");
+    if (setup_kernel_attributes()) return fail(LSTM_SD_EHIP, "hipFuncSetAttribute failed");
+    hipStream_t st = (hipStream_t)stream;
+    if (P.dtype == LSTM_SD_DTYPE_BF16)
+        return forward_impl<bf16>(P, w, x, lengths, h0, c0, mask_buf, y, hT, cT, reserve, workspace, st);
+    return forward_impl<float>(P, w, x, lengths, h0, c0, mask_buf, y, hT, cT, reserve, workspace, st);
+}
+
+int lstm_sd_backward(const lstm_sd_dims* dims, const lstm_sd_weights* w, const void* x, const int32_t* lengths,
+                     const void* h0, const float* c0, const void* mask_buf, size_t mask_bytes,
+                     const void* reserve, size_t reserve_bytes, const float* dy, const float* dhT,
+                     const float* dcT, float* dx, float* dh0, float* dc0, const lstm_sd_grads* g,
+                     void* workspace, size_t workspace_bytes, void* stream) {
+    Plan P; const char* why = nullptr;
+    int rc = make_plan(dims, &P, &why);
+    if (rc) return fail(rc, why);
+    if (!w || !w->W || !w->U || !w->b) return fail(LSTM_SD_EINVAL, "weights is NULL");
+    if (!g || !g->dW || !g->dU || !g->db) return fail(LSTM_SD_EINVAL, "grads is NULL");
+    for (int k = 0; k < P.L * P.D; ++k) {
+        if (!w->W[k] || !w->U[k] || !w->b[k]) return fail(LSTM_SD_EINVAL, "a weight pointer is NULL");
+        if (!g->dW[k] || !g->dU[k] || !g->db[k]) return fail(LSTM_SD_EINVAL, "a gradient pointer is NULL");
+    }
+    if (!x || !h0 || !c0 || !mask_buf || !reserve || !dy || !dh0 || !dc0 || !workspace)
+        return fail(LSTM_SD_EINVAL, "a required pointer is NULL");
+    if (mask_bytes < P.m_total) return fail(LSTM_SD_EWORKSPACE, "mask_bytes smaller than lstm_sd_mask_bytes()");
+    if (reserve_bytes < P.r_total) return fail(LSTM_SD_EWORKSPACE, "reserve_bytes smaller than lstm_sd_reserve_bytes()");
+    if (workspace_bytes < P.w_total) return fail(LSTM_SD_EWORKSPACE, "workspace_bytes smaller than lstm_sd_workspace_bytes()");
+    if (setup_kernel_attributes()) return fail(LSTM_SD_EHIP, "hipFuncSetAttribute failed");
+    hipStream_t st = (hipStream_t)stream;
+    if (P.dtype == LSTM_SD_DTYPE_BF16)
+        return backward_impl<bf16>(P, w, x, lengths, h0, c0, mask_buf, reserve, dy, dhT, dcT, dx, dh0, dc0, g,
+                                   workspace, st);
+    return backward_impl<float>(P, w, x, lengths, h0, c0, mask_buf, reserve, dy, dhT, dcT, dx, dh0, dc0, g,
+                                workspace, st);
+}
+
+int lstm_sd_mse_grad(const lstm_sd_dims* dims, const float* y, const float* target, const int32_t* lengths,
+                     float* dy, float* loss, void* workspace, size_t workspace_bytes, void* stream) {
+    Plan P; const char* why = nullptr;
+    int rc = make_plan(dims, &P, &why);
+    if (rc) return fail(rc, why);
+    if (!y || !target || !dy || !loss || !workspace) return fail(LSTM_SD_EINVAL, "a required pointer is NULL");
+    if (workspace_bytes < P.w_total) return fail(LSTM_SD_EWORKSPACE, "workspace_bytes smaller than lstm_sd_workspace_bytes()");
+    float* partial = (float*)((char*)workspace + P.w_loss);
+    launch_mse(y, target, lengths, dy, partial, 1024, loss, P.T, P.B, P.D * P.H, (hipStream_t)stream);
+    return hip_check("mse launch");
+}
+
+}  // extern "C"

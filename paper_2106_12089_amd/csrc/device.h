@@ -1,0 +1,94 @@
+// Device helpers for gfx950: bfloat16 conversion, 16x16x32 MFMA tiles on
+// 8-element fragments, Philox4x64-10 and LSTM activations.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace lsd {
+
+typedef uint16_t bf16;   // raw bfloat16 bits
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef short s16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float bf2f(bf16 h) { return __uint_as_float((uint32_t)h << 16); }
+
+// float -> bfloat16, round to nearest even (finite inputs)
+__device__ __forceinline__ bf16 f2bf(float f) {
+    uint32_t u = __float_as_uint(f);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (bf16)(u >> 16);
+}
+
+template <typename T> __device__ __forceinline__ float to_f32(T v);
+template <> __device__ __forceinline__ float to_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ float to_f32<bf16>(bf16 v) { return bf2f(v); }
+
+template <typename T> __device__ __forceinline__ T from_f32(float v);
+template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ bf16 from_f32<bf16>(float v) { return f2bf(v); }
+
+template <typename T> __device__ __forceinline__ T zero_val() { return (T)0; }
+
+// An MFMA operand fragment: 8 consecutive contraction elements of one row
+// (A) or one column (B) held by one lane.  For the 16x16 tile, lane l holds
+// row/column l%16 and contraction elements 8*(l/16) .. 8*(l/16)+7 of a
+// 32-long contraction chunk.  The contraction order inside a chunk only has
+// to agree between A and B, so the fp32 path issues the 4-deep fp32 MFMA
+// once per fragment slot.
+template <typename T> struct Frag { T v[8]; };
+
+__device__ __forceinline__ void mma_16x16x32(const Frag<bf16>& a, const Frag<bf16>& b, f32x4_t& c) {
+    s16x8_t av, bv;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) { av[e] = (short)a.v[e]; bv[e] = (short)b.v[e]; }
+    c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, av),
+                                                __builtin_bit_cast(bf16x8_t, bv), c, 0, 0, 0);
+}
+
+__device__ __forceinline__ void mma_16x16x32(const Frag<float>& a, const Frag<float>& b, f32x4_t& c) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.v[e], b.v[e], c, 0, 0, 0);
+}
+
+// Output element r (0..3) of lane l of a 16x16 accumulator sits at
+// row 4*(l/16) + r, column l%16.
+__device__ __forceinline__ int acc_row(int lane, int r) { return 4 * (lane >> 4) + r; }
+__device__ __forceinline__ int acc_col(int lane) { return lane & 15; }
+
+// ---------------------------------------------------------------------------
+// Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC'11)
+struct u64x4 { uint64_t x[4]; };
+
+__device__ __forceinline__ u64x4 philox4x64_10(u64x4 c, uint64_t k0, uint64_t k1) {
+    const uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
+    const uint64_t W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        uint64_t lo0 = M0 * c.x[0], hi0 = __umul64hi(M0, c.x[0]);
+        uint64_t lo1 = M1 * c.x[2], hi1 = __umul64hi(M1, c.x[2]);
+        u64x4 n;
+        n.x[0] = hi1 ^ c.x[1] ^ k0;
+        n.x[1] = lo1;
+        n.x[2] = hi0 ^ c.x[3] ^ k1;
+        n.x[3] = lo0;
+        c = n;
+        k0 += W0;
+        k1 += W1;
+    }
+    return c;
+}
+
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float sigmoidf_(float z) { return 1.0f / (1.0f + __expf(-z)); }
+__device__ __forceinline__ float tanhf_(float z) {
+    // tanh z = 2 sigmoid(2z) - 1, written to stay accurate for small |z|
+    float a = fabsf(z);
+    float e = __expf(-2.0f * a);
+    float t = (1.0f - e) / (1.0f + e);
+    return copysignf(t, z);
+}
+
+}  // namespace lsd

@@ -1,0 +1,120 @@
+"""Device-resident state of one LSTM training step driven through the C ABI.
+
+PyTorch only allocates device memory here and supplies the stream; every
+computation is a call into liblstm_sd.so.
+"""
+from __future__ import annotations
+
+from typing import Optional
+
+import numpy as np
+import torch
+
+from . import binding as B_
+
+
+class Session:
+    """Buffers and calls for one (config, dropout mode) pair.
+
+    wl:      a workload (x, W, U, b, h0, c0, target, lengths as numpy arrays)
+    p_nr, p_rh: dropout rates of the two sites; compact: 1 = method, 0 = dense
+    """
+
+    def __init__(self, wl, p_nr: float, p_rh: float, compact: int, device: str = "cuda:0",
+                 loss: Optional[str] = None):
+        cfg = wl.cfg
+        self.cfg, self.wl = cfg, wl
+        self.device = torch.device(device)
+        self.L, self.D, self.H = cfg.num_layers, cfg.num_dirs, cfg.hidden
+        self.T, self.B, self.I = wl.x.shape[0], wl.x.shape[1], wl.x.shape[2]
+        self.bf16 = cfg.dtype == "bf16"
+        self.loss_kind = loss or cfg.loss
+        dt = torch.bfloat16 if self.bf16 else torch.float32
+        self.dims = B_.make_dims(self.L, self.I, self.H, self.B, self.T, self.D,
+                                 B_.DTYPE_BF16 if self.bf16 else B_.DTYPE_F32, compact, p_nr, p_rh)
+        dev = self.device
+        f = lambda a, t=torch.float32: torch.from_numpy(np.ascontiguousarray(a)).to(dev).to(t)
+        self.W = [f(w, dt) for w in wl.W]
+        self.U = [f(u, dt) for u in wl.U]
+        self.b = [f(v) for v in wl.b]
+        self.x = f(wl.x, dt)
+        self.h0 = f(wl.h0, dt)
+        self.c0 = f(wl.c0)
+        self.target = f(wl.target)
+        self.lengths = None if wl.lengths is None else f(wl.lengths, torch.int32)
+        u8 = torch.uint8
+        self.mask_buf = torch.zeros(B_.lstm_sd_mask_bytes(self.dims), dtype=u8, device=dev)
+        self.reserve = torch.zeros(B_.lstm_sd_reserve_bytes(self.dims), dtype=u8, device=dev)
+        self.workspace = torch.zeros(B_.lstm_sd_workspace_bytes(self.dims), dtype=u8, device=dev)
+        F = self.D * self.H
+        z = lambda *s: torch.zeros(*s, dtype=torch.float32, device=dev)
+        self.y = z(self.T, self.B, F)
+        self.hT = z(self.L * self.D, self.B, self.H)
+        self.cT = z(self.L * self.D, self.B, self.H)
+        self.dy = z(self.T, self.B, F)
+        self.loss = z(1)
+        self.dx = z(self.T, self.B, self.I)
+        self.dh0 = z(self.L * self.D, self.B, self.H)
+        self.dc0 = z(self.L * self.D, self.B, self.H)
+        self.dW = [z(*w.shape) for w in self.W]
+        self.dU = [z(*u.shape) for u in self.U]
+        self.db = [z(*v.shape) for v in self.b]
+        if self.loss_kind == "sum":
+            self.dy.fill_(1.0)      # d(sum y)/dy, constant
+
+    # -- calls ---------------------------------------------------------------
+    def masks(self, seed: int, step: int):
+        B_.lstm_sd_mask_generate(self.dims, seed, step, self.mask_buf)
+
+    def masks_compact(self):
+        B_.lstm_sd_mask_compact(self.dims, self.mask_buf)
+
+    def forward(self):
+        B_.lstm_sd_forward(self.dims, self.W, self.U, self.b, self.x, self.lengths, self.h0, self.c0,
+                           self.mask_buf, self.y, self.hT, self.cT, self.reserve, self.workspace)
+
+    def loss_grad(self):
+        if self.loss_kind == "mse":
+            B_.lstm_sd_mse_grad(self.dims, self.y, self.target, self.lengths, self.dy, self.loss,
+                                self.workspace)
+
+    def backward(self, dy=None, dhT=None, dcT=None, want_dx=True):
+        B_.lstm_sd_backward(self.dims, self.W, self.U, self.b, self.x, self.lengths, self.h0, self.c0,
+                            self.mask_buf, self.reserve, self.dy if dy is None else dy, dhT, dcT,
+                            self.dx if want_dx else None, self.dh0, self.dc0, self.dW, self.dU, self.db,
+                            self.workspace)
+
+    def step(self, seed: int, step: int):
+        self.masks(seed, step)
+        self.forward()
+        self.loss_grad()
+        self.backward()
+
+    # -- host views (tests) -------------------------------------------------------
+    def mask_views(self):
+        """Decode the mask buffer: (mask, keep, pos, count) numpy arrays with
+        shapes [sites][T][kmax] (x3) and [sites][T]."""
+        lay = B_.lstm_sd_mask_layout_get(self.dims)
+        raw = self.mask_buf.cpu().numpy()
+        S, T, K = lay.sites, lay.seq_len, lay.kmax
+        mask = raw[lay.mask_off:lay.mask_off + S * T * K].reshape(S, T, K)
+        keep = raw[lay.keep_off:lay.keep_off + S * T * K * 4].view(np.int32).reshape(S, T, K)
+        pos = raw[lay.pos_off:lay.pos_off + S * T * K * 4].view(np.int32).reshape(S, T, K)
+        count = raw[lay.count_off:lay.count_off + S * T * 4].view(np.int32).reshape(S, T)
+        return mask, keep, pos, count
+
+    def write_masks(self, mask_u8: np.ndarray):
+        """Overwrite the mask bytes ([sites][T][kmax]) and rebuild keep lists."""
+        lay = B_.lstm_sd_mask_layout_get(self.dims)
+        flat = torch.from_numpy(np.ascontiguousarray(mask_u8, dtype=np.uint8).ravel()).to(self.device)
+        self.mask_buf[lay.mask_off:lay.mask_off + flat.numel()].copy_(flat)
+        self.masks_compact()
+
+    def site_k(self, s):
+        return (self.I if s == 0 else self.D * self.H) if s < self.L else self.H
+
+    def outputs(self):
+        g = lambda t: t.detach().float().cpu().numpy().astype(np.float64)
+        return dict(y=g(self.y), hT=g(self.hT), cT=g(self.cT), dx=g(self.dx), dh0=g(self.dh0),
+                    dc0=g(self.dc0), dW=[g(t) for t in self.dW], dU=[g(t) for t in self.dU],
+                    db=[g(t) for t in self.db], loss=float(self.loss.item()), dy=g(self.dy))

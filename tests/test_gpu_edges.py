@@ -1,0 +1,142 @@
+"""Edge cases of the HIP path against the oracle: ragged sizes that are not
+multiples of any tile, a single row and step, zero-length rows, rates of 0,
+forced mask patterns (a neuron never kept, a step with everything dropped,
+everything kept) and the dense/compact equivalence."""
+import dataclasses
+
+import numpy as np
+import pytest
+
+import workloads
+from tests._parity import TOL, compare, oracle_step, say, site_list
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+def make(name, **kw):
+    base = workloads.get_config("tiny")
+    cfg = dataclasses.replace(base, name=name, **kw)
+    return cfg, workloads.make_workload(cfg)
+
+
+def run_both(cfg, wl, p_nr, p_rh, compact, forced=None, dhT=False):
+    from paper_2106_12089_amd.session import Session
+    from oracle import masks as om
+    s = Session(wl, p_nr, p_rh, compact)
+    s.masks(cfg.mask_seed, 0)
+    m_nr, m_rh = om.all_masks(cfg.mask_seed, 0, cfg.num_layers, cfg.num_dirs, cfg.seq_len, cfg.k_in,
+                              cfg.hidden, p_nr, p_rh)
+    if forced is not None:
+        m_nr, m_rh = forced(m_nr, m_rh)
+        mask, _, _, _ = s.mask_views()
+        mask = mask.copy()
+        for i, m in enumerate(site_list(cfg, m_nr, m_rh)):
+            mask[i, :, :m.shape[1]] = m
+        s.write_masks(mask)
+    s.forward()
+    s.loss_grad()
+    s.backward()
+    torch.cuda.synchronize()
+    gpu = s.outputs()
+    ref = oracle_step(wl, p_nr, p_rh, m_nr, m_rh)
+    return gpu, ref, m_nr, m_rh
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", [
+    dict(num_layers=2, num_dirs=2, input_dim=37, hidden=45, batch=19, seq_len=3),
+    dict(num_layers=1, num_dirs=1, input_dim=5, hidden=3, batch=1, seq_len=1),
+    dict(num_layers=3, num_dirs=1, input_dim=70, hidden=33, batch=35, seq_len=5),
+    dict(num_layers=1, num_dirs=2, input_dim=129, hidden=100, batch=70, seq_len=4),
+])
+@pytest.mark.parametrize("mode", ["nrrh", "nrrh_dense"])
+def test_ragged_shapes(shape, dtype, mode):
+    cfg, wl = make("ragged", dtype=dtype, loss="mse", **shape)
+    compact = 0 if mode.endswith("dense") else 1
+    say(f"[gpu] ragged {shape} {dtype} {mode}")
+    gpu, ref, _, _ = run_both(cfg, wl, 0.5, 0.5, compact)
+    errs = compare(gpu, ref)
+    assert max(errs.values()) <= TOL[dtype], errs
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_lengths_with_zero_rows(dtype):
+    cfg, wl = make("lens", dtype=dtype, loss="mse", num_layers=2, num_dirs=2, input_dim=24, hidden=20,
+                   batch=6, seq_len=7, min_len=0)
+    wl.lengths[:] = np.array([7, 0, 3, 1, 6, 0], dtype=np.int32)
+    valid = np.arange(cfg.seq_len)[:, None] < wl.lengths[None, :]
+    wl.x[~valid] = 0.0
+    say(f"[gpu] lengths {dtype}")
+    gpu, ref, _, _ = run_both(cfg, wl, 0.5, 0.5, 1)
+    errs = compare(gpu, ref)
+    assert max(errs.values()) <= TOL[dtype], errs
+    assert np.all(gpu["y"][~valid] == 0.0)
+
+
+def test_rate_zero_is_plain_lstm():
+    cfg, wl = make("p0", dtype="f32", loss="mse")
+    say("[gpu] p = 0")
+    gpu, ref, m_nr, _ = run_both(cfg, wl, 0.0, 0.0, 1)
+    assert all(m.all() for m in m_nr)
+    errs = compare(gpu, ref)
+    assert max(errs.values()) <= TOL["f32"], errs
+
+
+@pytest.mark.parametrize("compact", [1, 0])
+def test_forced_patterns(compact):
+    cfg, wl = make("forced", dtype="f32", loss="mse", num_layers=2, input_dim=40, hidden=24, batch=5,
+                   seq_len=6)
+
+    def force(m_nr, m_rh):
+        m_nr = [m.copy() for m in m_nr]
+        m_rh = [[m.copy() for m in r] for r in m_rh]
+        m_nr[0][:, 7] = 0          # never kept: zero dW row
+        m_nr[1][:, 3] = 0
+        m_rh[1][0][:, 5] = 0       # never kept: zero dU row
+        m_nr[0][2, :] = 0          # everything dropped at t = 2
+        m_rh[0][0][4, :] = 0
+        m_nr[1][1, :] = 1          # everything kept at t = 1
+        return m_nr, m_rh
+
+    say(f"[gpu] forced patterns compact={compact}")
+    gpu, ref, m_nr, m_rh = run_both(cfg, wl, 0.5, 0.5, compact, forced=force)
+    errs = compare(gpu, ref)
+    assert max(errs.values()) <= TOL["f32"], errs
+    assert np.all(gpu["dW"][0][7] == 0.0)
+    assert np.all(gpu["dW"][1][3] == 0.0)
+    assert np.all(gpu["dU"][1][5] == 0.0)
+    assert np.all(gpu["dx"][2] == 0.0)
+
+
+def test_dense_equals_compact():
+    cfg = workloads.get_config("lm_medium")
+    wl = workloads.make_workload(cfg)
+    from paper_2106_12089_amd.session import Session
+    say("[gpu] dense vs compact lm_medium")
+    outs = []
+    for compact in (1, 0):
+        s = Session(wl, 0.5, 0.5, compact)
+        s.step(cfg.mask_seed, 1)
+        torch.cuda.synchronize()
+        outs.append(s.outputs())
+    errs = compare(outs[0], outs[1])
+    assert max(errs.values()) <= 1e-2, errs
+
+
+def test_mse_kernel_matches_oracle():
+    from oracle import lstm
+    from paper_2106_12089_amd.session import Session
+    cfg = workloads.get_config("seq2seq_enc")
+    wl = workloads.make_workload(cfg)
+    s = Session(wl, 0.3, 0.0, 1)
+    say("[gpu] mse kernel")
+    y = np.random.default_rng(0).normal(size=s.y.shape).astype(np.float32)
+    valid = np.arange(cfg.seq_len)[:, None] < wl.lengths[None, :]
+    y[~valid] = 0.0
+    s.y.copy_(torch.from_numpy(y))
+    s.loss_grad()
+    torch.cuda.synchronize()
+    loss, dy = lstm.loss_mse(y, wl.target, wl.lengths)
+    assert abs(s.loss.item() - loss) / loss < 1e-5
+    assert np.allclose(s.dy.cpu().numpy(), dy, rtol=1e-5, atol=1e-9)

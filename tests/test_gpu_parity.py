@@ -1,0 +1,127 @@
+"""Parity of the HIP path (through the C ABI) with the float64 oracle on the
+seeded workloads, at the workloads' full sizes, in every dropout mode.
+
+Bar: masks, keep lists and counts bit-exact; every output and gradient
+within a normwise relative error of 1e-4 (fp32 path) or 2e-2 (bf16 MFMA
+path); structurally zero entries exactly zero.  The stress shape is checked
+on a sample of batch rows: the GPU runs the full batch, the gradient of a
+loss that only sees the sampled rows is fed to both sides, and the oracle
+runs on those rows alone (rows are independent under batch-shared masks)."""
+import numpy as np
+import pytest
+
+import workloads
+from tests._parity import (TOL, compare, mode_rates, oracle_masks, oracle_step, say, site_list)
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+MODES = ["nr", "nrrh", "nr_dense", "nrrh_dense"]
+CASES = [(c, p) for c in ("tiny", "lm_medium", "lm_large", "seq2seq_enc", "tagger", "stress")
+         for p in workloads.get_config(c).p_values]
+
+_WL = {}
+
+
+def workload(name):
+    if name not in _WL:
+        _WL[name] = workloads.make_workload(workloads.get_config(name))
+    return _WL[name]
+
+
+def check_masks(sess, cfg, m_nr, m_rh, compact):
+    mask, keep, pos, count = sess.mask_views()
+    for s, ref in enumerate(site_list(cfg, m_nr, m_rh)):
+        K = ref.shape[1]
+        assert np.array_equal(mask[s, :, :K], ref), f"mask site {s}"
+        for t in range(ref.shape[0]):
+            if compact:
+                kl = np.nonzero(ref[t])[0]
+                assert count[s, t] == len(kl)
+                assert np.array_equal(keep[s, t, :len(kl)], kl)
+                p = np.full(K, -1)
+                p[kl] = np.arange(len(kl))
+                assert np.array_equal(pos[s, t, :K], p)
+            else:
+                assert count[s, t] == K
+                assert np.array_equal(keep[s, t, :K], np.arange(K))
+
+
+@pytest.mark.parametrize("mode", MODES)
+@pytest.mark.parametrize("name,p", CASES)
+def test_step_parity(name, p, mode):
+    from paper_2106_12089_amd.session import Session
+    cfg = workloads.get_config(name)
+    wl = workload(name)
+    p_nr, p_rh, compact = mode_rates(cfg, mode, p)
+    say(f"[gpu] {name} p={p} mode={mode}")
+    sess = Session(wl, p_nr, p_rh, compact)
+    sess.masks(cfg.mask_seed, 0)
+    m_nr, m_rh = oracle_masks(cfg, p_nr, p_rh)
+    torch.cuda.synchronize()
+    check_masks(sess, cfg, m_nr, m_rh, compact)
+    tol = TOL[cfg.dtype]
+    sess.forward()
+    if name == "stress":
+        rows = np.array([0, 37, 101, 255])
+        sub = workloads.slice_rows(wl, rows)
+        ref = oracle_step(sub, p_nr, p_rh, m_nr, m_rh)     # dy = MSE gradient over the sampled rows
+        dy_full = np.zeros((cfg.seq_len, cfg.batch, cfg.num_dirs * cfg.hidden), dtype=np.float32)
+        dy_full[:, rows] = ref["dy"]
+        sess.backward(dy=torch.from_numpy(dy_full).cuda())
+        torch.cuda.synchronize()
+        gpu = sess.outputs()
+        errs = compare(gpu, ref, keys=("y", "hT", "cT"), rows=rows)
+        # the input and state gradients are zero outside the sampled rows
+        for k in ("dx", "dh0", "dc0"):
+            a = gpu[k]
+            errs[k] = float(np.linalg.norm(a[:, rows] - ref[k]) / np.linalg.norm(ref[k]))
+            others = np.setdiff1d(np.arange(cfg.batch), rows)
+            assert np.all(a[:, others] == 0.0), k
+    else:
+        sess.loss_grad()
+        sess.backward()
+        torch.cuda.synchronize()
+        gpu = sess.outputs()
+        ref = oracle_step(wl, p_nr, p_rh, m_nr, m_rh)
+        errs = compare(gpu, ref)
+        if ref["loss"] is not None and cfg.loss == "mse":
+            errs["loss"] = abs(gpu["loss"] - ref["loss"]) / abs(ref["loss"])
+    say("   errs max", max(errs.values()), {k: f"{v:.2e}" for k, v in errs.items()})
+    bad = {k: v for k, v in errs.items() if not v <= tol}
+    assert not bad, bad
+    # output sparsity (Eq. 10): dropped input columns get exactly zero gradient
+    dx = gpu["dx"]
+    drop = m_nr[0] == 0
+    for t in range(cfg.seq_len):
+        assert np.all(dx[t][:, drop[t]] == 0.0)
+
+
+def test_determinism():
+    from paper_2106_12089_amd.session import Session
+    cfg = workloads.get_config("lm_medium")
+    wl = workload("lm_medium")
+    say("[gpu] determinism lm_medium nrrh")
+    outs = []
+    for _ in range(2):
+        s = Session(wl, 0.5, 0.5, 1)
+        s.step(cfg.mask_seed, 3)
+        torch.cuda.synchronize()
+        outs.append(s.outputs())
+    for k in ("y", "hT", "cT", "dx", "dh0", "dc0"):
+        assert np.array_equal(outs[0][k], outs[1][k]), k
+    for k in ("dW", "dU", "db"):
+        for a, b in zip(outs[0][k], outs[1][k]):
+            assert np.array_equal(a, b), k
+
+
+def test_fresh_masks_per_step():
+    from paper_2106_12089_amd.session import Session
+    cfg = workloads.get_config("tiny")
+    wl = workload("tiny")
+    say("[gpu] masks at step 5")
+    s = Session(wl, 0.5, 0.5, 1)
+    s.masks(cfg.mask_seed, 5)
+    torch.cuda.synchronize()
+    m_nr, m_rh = oracle_masks(cfg, 0.5, 0.5, step=5)
+    check_masks(s, cfg, m_nr, m_rh, 1)
