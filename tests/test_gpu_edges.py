@@ -91,12 +91,12 @@ def test_forced_patterns(compact):
     def force(m_nr, m_rh):
         m_nr = [m.copy() for m in m_nr]
         m_rh = [[m.copy() for m in r] for r in m_rh]
+        m_nr[1][1, :] = 1          # everything kept at t = 1 (but neuron 3, below)
         m_nr[0][:, 7] = 0          # never kept: zero dW row
         m_nr[1][:, 3] = 0
         m_rh[1][0][:, 5] = 0       # never kept: zero dU row
         m_nr[0][2, :] = 0          # everything dropped at t = 2
         m_rh[0][0][4, :] = 0
-        m_nr[1][1, :] = 1          # everything kept at t = 1
         return m_nr, m_rh
 
     say(f"[gpu] forced patterns compact={compact}")
