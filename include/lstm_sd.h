@@ -108,13 +108,16 @@ typedef struct {
  *                                 count are unspecified
  *   pos   int32 [sites][T][kmax]  inverse of keep: position of neuron k in
  *                                 keep, or -1 if k is not listed
- *   count int32 [sites][T]        number of listed entries */
+ *   count int32 [sites][T]        number of listed entries
+ *   drop  int32 [sites][T][kmax]  ascending dropped indices (compact = 1);
+ *                                 empty when compact = 0
+ *   dcount int32 [sites][T]       number of entries of drop */
 typedef struct {
     int32_t sites;
     int32_t kmax;
     int32_t seq_len;
     int32_t reserved;
-    size_t mask_off, keep_off, pos_off, count_off, total_bytes;
+    size_t mask_off, keep_off, pos_off, count_off, drop_off, dcount_off, total_bytes;
 } lstm_sd_mask_layout;
 
 int         lstm_sd_version(void);

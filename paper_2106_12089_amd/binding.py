@@ -42,7 +42,8 @@ class lstm_sd_mask_layout(ctypes.Structure):
     _fields_ = [("sites", ctypes.c_int32), ("kmax", ctypes.c_int32), ("seq_len", ctypes.c_int32),
                 ("reserved", ctypes.c_int32), ("mask_off", ctypes.c_size_t),
                 ("keep_off", ctypes.c_size_t), ("pos_off", ctypes.c_size_t),
-                ("count_off", ctypes.c_size_t), ("total_bytes", ctypes.c_size_t)]
+                ("count_off", ctypes.c_size_t), ("drop_off", ctypes.c_size_t),
+                ("dcount_off", ctypes.c_size_t), ("total_bytes", ctypes.c_size_t)]
 
 
 _P = ctypes.c_void_p

@@ -16,17 +16,17 @@
 namespace lsd {
 
 void launch_mask_build(const MaskArgs& a, int sites, hipStream_t st);
+template <typename T> void launch_transpose(const TransArgs& a, int N, hipStream_t st);
 template <typename T> void launch_fx(const FxArgs& a, hipStream_t st);
 template <typename T> void launch_step(const StepArgs& a, int D, hipStream_t st);
-template <typename T> void launch_bwd_pw(const BwdPwArgs& a, int D, hipStream_t st);
-template <typename T> void launch_bwd_dh(const DhArgs& a, int D, int H, hipStream_t st);
+template <typename T> void launch_bwd(const BwdArgs& a, int D, hipStream_t st);
 template <typename T> void launch_dx(const DxArgs& a, int K, hipStream_t st);
-template <typename T> void launch_wgrad(const WgArgs& a, hipStream_t st);
+template <typename T> void launch_wgrad(const WgArgs& a, int ts, hipStream_t st);
 template <typename T> void launch_fwd_init(const void*, const float*, float*, float*, long, hipStream_t);
+void launch_wreduce(const float* part, float* dW, long n, int ts, hipStream_t st);
 void launch_bwd_init(const float*, const float*, float*, float*, long, hipStream_t);
-void launch_bwd_final(const FinalArgs& a, int D, hipStream_t st);
 void launch_expand(const float*, int, const SiteView&, float*, int, int, int, hipStream_t);
-void launch_db(const float*, float*, int, int, hipStream_t);
+void launch_db(const float*, float*, int, int, int, hipStream_t);
 void launch_mse(const float*, const float*, const int32_t*, float*, float*, int, float*, int, int, int,
                 hipStream_t);
 int setup_kernel_attributes();
@@ -68,39 +68,59 @@ int make_plan(const lstm_sd_dims* d, Plan* p, const char** why) {
     q.s_nr = inv_keep(d->p_nr); q.s_rh = inv_keep(d->p_rh);
     q.esize = d->dtype == LSTM_SD_DTYPE_BF16 ? 2 : 4;
     q.G = 4 * q.H;
+    q.BP = (q.B + 31) / 32 * 32;
+    q.MGc = (q.B + 63) / 64;
     q.sites = q.L + q.L * q.D;
     q.kin_max = q.L > 1 ? (q.I > q.D * q.H ? q.I : q.D * q.H) : q.I;
     q.kmax = q.kin_max > q.H ? q.kin_max : q.H;
+    {
+        const int ncol = (q.G + 15) / 16;
+        int ts = (512 + ncol - 1) / ncol;
+        if (ts > 8) ts = 8;
+        if (ts > q.T) ts = q.T;
+        if (ts < 1) ts = 1;
+        const int tper = (q.T + ts - 1) / ts;
+        q.ts = (q.T + tper - 1) / tper;
+    }
 
-    const size_t A = 256, T = q.T, B = q.B, H = q.H, G = q.G, D = q.D;
+    const size_t A = 256, T = q.T, B = q.B, H = q.H, G = q.G, D = q.D, BP = q.BP, es = q.esize;
+    const size_t S = q.sites, KM = q.kmax;
     size_t off = 0;
-    q.m_mask = off;  off = align_up(off + (size_t)q.sites * T * q.kmax, A);
-    q.m_keep = off;  off = align_up(off + (size_t)q.sites * T * q.kmax * 4, A);
-    q.m_pos = off;   off = align_up(off + (size_t)q.sites * T * q.kmax * 4, A);
-    q.m_count = off; off = align_up(off + (size_t)q.sites * T * 4, A);
+    q.m_mask = off;   off = align_up(off + S * T * KM, A);
+    q.m_keep = off;   off = align_up(off + S * T * KM * 4, A);
+    q.m_pos = off;    off = align_up(off + S * T * KM * 4, A);
+    q.m_count = off;  off = align_up(off + S * T * 4, A);
+    q.m_drop = off;   off = align_up(off + S * T * KM * 4, A);
+    q.m_dcount = off; off = align_up(off + S * T * 4, A);
     q.m_total = off;
 
     off = 0;
     q.r_gates = off; off = align_up(off + T * B * G * 4, A);
     q.r_c = off;     off = align_up(off + T * B * H * 4, A);
-    q.r_hrec = off;  off = align_up(off + T * B * H * q.esize, A);
+    q.r_hrecT = off; off = align_up(off + T * H * BP * es, A);
     q.r_dir_bytes = off;
-    q.r_ybuf_base = (size_t)q.L * q.D * q.r_dir_bytes;
-    q.r_ybuf_bytes = align_up(T * B * D * H * q.esize, A);
+    off = (size_t)q.L * D * q.r_dir_bytes;
+    q.r_xT = off;    off = align_up(off + T * (size_t)q.I * BP * es, A);
+    q.r_h0T = off;   off = align_up(off + (size_t)q.L * D * H * BP * es, A);
+    q.r_ybuf_base = off;
+    q.r_ybufT_off = align_up(T * B * D * H * es, A);
+    q.r_ybuf_bytes = q.r_ybufT_off + align_up(T * D * H * BP * es, A);
     q.r_total = q.r_ybuf_base + (size_t)(q.L - 1) * q.r_ybuf_bytes;
 
-    size_t fwd = align_up(D * T * B * G * 4, A);
-    q.w_gx = 0;
     off = 0;
-    q.w_da = off;     off = align_up(off + D * T * B * G * q.esize, A);
-    q.w_dbpart = off; off = align_up(off + D * T * G * 4, A);
-    q.w_dhrec = off;  off = align_up(off + D * 2 * B * H * 4, A);
+    q.w_gx = off;   off = align_up(off + D * T * B * G * 4, A);
+    q.w_hrec = off; off = align_up(off + D * 2 * B * H * es, A);
+    const size_t fwd = off;
+    off = 0;
+    q.w_da = off;     off = align_up(off + D * T * B * G * es, A);
+    q.w_daT = off;    off = align_up(off + D * T * G * BP * es, A);
+    q.w_dbpart = off; off = align_up(off + D * T * (size_t)q.MGc * G * 4, A);
     q.w_dc = off;     off = align_up(off + D * B * H * 4, A);
     q.w_dhc = off;    off = align_up(off + D * B * H * 4, A);
     q.w_dxc = off;    off = align_up(off + 2 * T * B * (size_t)q.kin_max * 4, A);
-    q.w_bwd_end = off;
-    size_t body = fwd > off ? fwd : off;
-    q.w_loss = align_up(body, A);
+    q.w_wpart = off;  off = align_up(off + (q.ts > 1 ? (size_t)q.ts * KM * G * 4 : 0), A);
+    const size_t bwd = off;
+    q.w_loss = align_up(fwd > bwd ? fwd : bwd, A);
     q.w_total = q.w_loss + 16384;
     return LSTM_SD_OK;
 }
@@ -113,22 +133,25 @@ static int hip_check(const char* where) {
 
 static SiteView site_view(const Plan& P, const void* mbuf, int s) {
     const char* m = (const char*)mbuf;
+    const size_t row = (size_t)s * P.T * P.kmax;
     SiteView v;
-    v.mask = (const uint8_t*)(m + P.mask_at(s, 0));
-    v.keep = (const int32_t*)(m + P.keep_at(s, 0));
-    v.pos = (const int32_t*)(m + P.pos_at(s, 0));
-    v.count = (const int32_t*)(m + P.count_at(s));
+    v.mask = (const uint8_t*)(m + P.m_mask) + row;
+    v.keep = (const int32_t*)(m + P.m_keep) + row;
+    v.pos = (const int32_t*)(m + P.m_pos) + row;
+    v.count = (const int32_t*)(m + P.m_count) + (size_t)s * P.T;
+    v.drop = (const int32_t*)(m + P.m_drop) + row;
+    v.dcount = (const int32_t*)(m + P.m_dcount) + (size_t)s * P.T;
     v.kmax = P.kmax;
     return v;
 }
 
 static uint64_t threshold64(double p) {
-    // floor(p * 2^64), exact: p = mant * 2^exp with a 53-bit integer mantissa
+    // floor(p * 2^64), exact: p = mant * 2^(e-53) with a 53-bit integer mantissa
     if (p <= 0.0) return 0;
     int e;
-    double m = frexp(p, &e);                 // p = m * 2^e, 0.5 <= m < 1
-    uint64_t mant = (uint64_t)ldexp(m, 53);  // exact
-    int sh = e + 64 - 53;                    // p * 2^64 = mant * 2^sh
+    const double m = frexp(p, &e);                 // p = m * 2^e, 0.5 <= m < 1
+    const uint64_t mant = (uint64_t)ldexp(m, 53);  // exact
+    const int sh = e + 64 - 53;                    // p * 2^64 = mant * 2^sh
     if (sh >= 0) return sh >= 64 ? 0 : (mant << sh);
     return -sh >= 64 ? 0 : (mant >> (-sh));
 }
@@ -148,6 +171,8 @@ static int do_masks(const lstm_sd_dims* dims, uint64_t seed, uint64_t step, void
     a.keep = (int32_t*)(m + P.m_keep);
     a.pos = (int32_t*)(m + P.m_pos);
     a.count = (int32_t*)(m + P.m_count);
+    a.drop = (int32_t*)(m + P.m_drop);
+    a.dcount = (int32_t*)(m + P.m_dcount);
     a.T = P.T; a.kmax = P.kmax; a.compact = P.compact; a.generate = generate;
     a.seed = seed; a.step = step;
     for (int s = 0; s < P.sites; ++s) {
@@ -163,10 +188,18 @@ template <typename E>
 static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, const int32_t* lengths,
                         const void* h0, const float* c0, const void* mbuf, float* y, float* hT, float* cT,
                         void* reserve, void* ws, hipStream_t st) {
-    const int L = P.L, D = P.D, T = P.T, B = P.B, H = P.H, G = P.G;
+    const int L = P.L, D = P.D, T = P.T, B = P.B, H = P.H, G = P.G, BP = P.BP;
+    const size_t es = P.esize;
     char* R = (char*)reserve;
     char* W = (char*)ws;
     launch_fwd_init<E>(h0, c0, hT, cT, (long)L * D * B * H, st);
+    {
+        TransArgs t;
+        t.src = x; t.dst = R + P.r_xT; t.B = B; t.K = P.I; t.BP = BP;
+        launch_transpose<E>(t, T, st);
+        t.src = h0; t.dst = R + P.r_h0T; t.K = H;
+        launch_transpose<E>(t, L * D, st);
+    }
     for (int l = 0; l < L; ++l) {
         const int kin = P.kin(l);
         const void* X = l == 0 ? x : (const void*)(R + P.rybuf(l - 1));
@@ -177,36 +210,40 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
             f.bias = w->b[l * D + d];
             f.site = site_view(P, mbuf, P.site_nr(l));
             f.Gx = (float*)(W + P.w_gx) + (size_t)d * T * B * G;
-            f.B = B; f.N = G; f.T = T; f.s = P.s_nr;
+            f.B = B; f.G = G; f.T = T; f.dense = !P.compact; f.s = P.s_nr;
             launch_fx<E>(f, st);
         }
         for (int s = 0; s < T; ++s) {
             StepArgs a;
             memset(&a, 0, sizeof(a));
-            a.lengths = lengths; a.B = B; a.H = H; a.ldy = D * H; a.s = P.s_rh;
+            a.lengths = lengths; a.B = B; a.H = H; a.ldy = D * H; a.BP = BP; a.dense = !P.compact; a.s = P.s_rh;
             for (int d = 0; d < D; ++d) {
                 const int k = l * D + d;
                 const int t = d == 0 ? s : T - 1 - s;
-                const int tp = d == 0 ? t - 1 : t + 1;
                 char* rd = R + P.rdir(l, d);
+                char* hrec2 = W + P.w_hrec + (size_t)d * 2 * B * H * es;
                 StepDir& sd = a.d[d];
                 sd.t = t;
-                sd.hprev = s == 0 ? (const void*)((const char*)h0 + (size_t)k * B * H * P.esize)
-                                  : (const void*)(rd + P.r_hrec + (size_t)tp * B * H * P.esize);
+                sd.hprev = s == 0 ? (const void*)((const char*)h0 + (size_t)k * B * H * es)
+                                  : (const void*)(hrec2 + (size_t)((s - 1) & 1) * B * H * es);
+                sd.hrec = hrec2 + (size_t)(s & 1) * B * H * es;
+                sd.hrecT = rd + P.r_hrecT + (size_t)t * H * BP * es;
                 sd.U = w->U[k];
                 sd.gx = (const float*)(W + P.w_gx) + ((size_t)d * T + t) * B * G;
-                SiteView sv = site_view(P, mbuf, P.site_rh(l, d));
+                const SiteView sv = site_view(P, mbuf, P.site_rh(l, d));
                 sd.mask = sv.mask + (size_t)t * P.kmax;
                 sd.keep = sv.keep + (size_t)t * P.kmax;
                 sd.count = sv.count + t;
                 sd.gates = (float*)(rd + P.r_gates) + (size_t)t * B * G;
                 sd.cres = (float*)(rd + P.r_c) + (size_t)t * B * H;
-                sd.hrec = rd + P.r_hrec + (size_t)t * B * H * P.esize;
                 sd.hT = hT + (size_t)k * B * H;
                 sd.cT = cT + (size_t)k * B * H;
-                sd.y = (l == L - 1) ? y + (size_t)t * B * D * H + d * H : nullptr;
-                sd.ybuf = (l < L - 1) ? (void*)(R + P.rybuf(l) + ((size_t)t * B * D * H + d * H) * P.esize)
-                                      : nullptr;
+                if (l == L - 1) {
+                    sd.y = y + (size_t)t * B * D * H + d * H;
+                } else {
+                    sd.ybuf = R + P.rybuf(l) + ((size_t)t * B * D * H + d * H) * es;
+                    sd.ybufT = R + P.rybufT(l) + ((size_t)t * D * H + d * H) * BP * es;
+                }
             }
             launch_step<E>(a, D, st);
         }
@@ -215,121 +252,113 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
 }
 
 template <typename E>
-static int backward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, const int32_t* lengths,
-                         const void* h0, const float* c0, const void* mbuf, const void* reserve,
+static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t* lengths,
+                         const float* c0, const void* mbuf, const void* reserve,
                          const float* dy, const float* dhT, const float* dcT, float* dx, float* dh0,
                          float* dc0, const lstm_sd_grads* g, void* ws, hipStream_t st) {
-    const int L = P.L, D = P.D, T = P.T, B = P.B, H = P.H, G = P.G;
+    const int L = P.L, D = P.D, T = P.T, B = P.B, H = P.H, G = P.G, BP = P.BP;
+    const size_t es = P.esize;
     const char* R = (const char*)reserve;
     char* W = (char*)ws;
+    const int nkt = (H + 15) / 16;
     for (int l = L - 1; l >= 0; --l) {
         const int kin = P.kin(l);
         float* dhc = (float*)(W + P.w_dhc);
         float* dcs = (float*)(W + P.w_dc);
         launch_bwd_init(dhT ? dhT + (size_t)l * D * B * H : nullptr, dcT ? dcT + (size_t)l * D * B * H : nullptr,
                         dhc, dcs, (long)D * B * H, st);
-        float* dhrec = (float*)(W + P.w_dhrec);               // [D][2][B][H]
         float* dxc_above = (float*)(W + P.w_dxc) + (size_t)((l + 1) & 1) * T * B * P.kin_max;
         float* dxc_here = (float*)(W + P.w_dxc) + (size_t)(l & 1) * T * B * P.kin_max;
-        for (int s = 0; s < T; ++s) {
-            BwdPwArgs a;
+        // T pointwise steps plus one final pass (recurrent gradient of h0)
+        for (int s = 0; s <= T; ++s) {
+            const bool final_pass = s == T;
+            BwdArgs a;
             memset(&a, 0, sizeof(a));
-            a.lengths = lengths; a.B = B; a.H = H; a.ldy = D * H;
+            a.lengths = lengths; a.B = B; a.H = H; a.BP = BP; a.ldy = D * H;
             a.lddx = l + 1 < L ? P.kin(l + 1) : 0;
-            DhArgs h;
-            memset(&h, 0, sizeof(h));
-            h.B = B; h.G = G; h.ldo = H; h.s = P.s_rh;
+            a.nkt = nkt; a.has_next = s > 0; a.final_pass = final_pass; a.dense = !P.compact; a.s = P.s_rh;
             for (int d = 0; d < D; ++d) {
                 const int k = l * D + d;
-                const int t = d == 0 ? T - 1 - s : s;         // BP order: reverse of FP order
-                const int tn = d == 0 ? t + 1 : t - 1;        // step processed just before
-                const int tp = d == 0 ? t - 1 : t + 1;        // forward predecessor
+                const int t = final_pass ? -1 : (d == 0 ? T - 1 - s : s);   // BP order: reverse of FP
+                const int tn = d == 0 ? T - s : s - 1;                        // step processed just before
+                const int tp = d == 0 ? t - 1 : t + 1;                        // forward predecessor of t
                 const char* rd = R + P.rdir(l, d);
-                BwdPwDir& pd = a.d[d];
-                pd.t = t;
-                pd.gates = (const float*)(rd + P.r_gates) + (size_t)t * B * G;
-                pd.cres = (const float*)(rd + P.r_c) + (size_t)t * B * H;
-                pd.cprev = s == T - 1 ? c0 + (size_t)k * B * H : (const float*)(rd + P.r_c) + (size_t)tp * B * H;
-                if (l == L - 1) {
-                    pd.dy = dy + (size_t)t * B * D * H + d * H;
-                } else {
-                    SiteView sv = site_view(P, mbuf, P.site_nr(l + 1));
-                    pd.dxc = dxc_above + (size_t)t * B * a.lddx;
-                    pd.dxpos = sv.pos + (size_t)t * P.kmax + d * H;
-                }
+                const SiteView rv = site_view(P, mbuf, P.site_rh(l, d));
+                BwdDir& bd = a.d[d];
+                bd.t = t;
+                bd.U = w->U[k];
+                bd.dhc = dhc + (size_t)d * B * H;
+                bd.dcs = dcs + (size_t)d * B * H;
                 if (s > 0) {
-                    SiteView sv = site_view(P, mbuf, P.site_rh(l, d));
-                    pd.dhrec = dhrec + ((size_t)d * 2 + (s & 1)) * B * H;
-                    pd.rhpos = sv.pos + (size_t)tn * P.kmax;
+                    bd.da_next = W + P.w_da + ((size_t)d * T + tn) * B * G * es;
+                    bd.nmask = rv.mask + (size_t)tn * P.kmax;
+                    bd.nkeep = rv.keep + (size_t)tn * P.kmax;
+                    bd.ncount = rv.count + tn;
+                    bd.ndrop = rv.drop + (size_t)tn * P.kmax;
+                    bd.ndcount = rv.dcount + tn;
                 }
-                pd.dhc = dhc + (size_t)d * B * H;
-                pd.dcs = dcs + (size_t)d * B * H;
-                pd.da = W + P.w_da + ((size_t)d * T + t) * B * G * P.esize;
-                pd.dbpart = (float*)(W + P.w_dbpart) + ((size_t)d * T + t) * G;
-
-                SiteView rv = site_view(P, mbuf, P.site_rh(l, d));
-                DhDir& hd = h.d[d];
-                hd.da = pd.da;
-                hd.Wk = w->U[k];
-                hd.mask = rv.mask + (size_t)t * P.kmax;
-                hd.keep = rv.keep + (size_t)t * P.kmax;
-                hd.count = rv.count + t;
-                hd.out = dhrec + ((size_t)d * 2 + ((s + 1) & 1)) * B * H;
+                if (final_pass) {
+                    bd.dh0 = dh0 + (size_t)k * B * H;
+                    bd.dc0 = dc0 + (size_t)k * B * H;
+                    continue;
+                }
+                bd.gates = (const float*)(rd + P.r_gates) + (size_t)t * B * G;
+                bd.cres = (const float*)(rd + P.r_c) + (size_t)t * B * H;
+                bd.cprev = s == T - 1 ? c0 + (size_t)k * B * H : (const float*)(rd + P.r_c) + (size_t)tp * B * H;
+                if (l == L - 1) {
+                    bd.dy = dy + (size_t)t * B * D * H + d * H;
+                } else {
+                    const SiteView sv = site_view(P, mbuf, P.site_nr(l + 1));
+                    bd.dxc = dxc_above + (size_t)t * B * a.lddx;
+                    bd.dxpos = sv.pos + (size_t)t * P.kmax + d * H;
+                }
+                bd.da = W + P.w_da + ((size_t)d * T + t) * B * G * es;
+                bd.daT = W + P.w_daT + ((size_t)d * T + t) * G * BP * es;
+                bd.dbpart = (float*)(W + P.w_dbpart) + ((size_t)d * T + t) * P.MGc * G;
             }
-            launch_bwd_pw<E>(a, D, st);
-            launch_bwd_dh<E>(h, D, H, st);
-        }
-        {
-            FinalArgs f;
-            memset(&f, 0, sizeof(f));
-            f.B = B; f.H = H;
-            for (int d = 0; d < D; ++d) {
-                const int k = l * D + d;
-                const int t0 = d == 0 ? 0 : T - 1;
-                SiteView rv = site_view(P, mbuf, P.site_rh(l, d));
-                f.d[d].dhrec = dhrec + ((size_t)d * 2 + (T & 1)) * B * H;
-                f.d[d].rhpos = rv.pos + (size_t)t0 * P.kmax;
-                f.d[d].dhc = dhc + (size_t)d * B * H;
-                f.d[d].dcs = dcs + (size_t)d * B * H;
-                f.d[d].dh0 = dh0 + (size_t)k * B * H;
-                f.d[d].dc0 = dc0 + (size_t)k * B * H;
-            }
-            launch_bwd_final(f, D, st);
+            launch_bwd<E>(a, D, st);
         }
         const SiteView nv = site_view(P, mbuf, P.site_nr(l));
         if (l > 0 || dx) {
             DxArgs a;
             memset(&a, 0, sizeof(a));
             for (int d = 0; d < D; ++d) {
-                a.da[d] = W + P.w_da + (size_t)d * T * B * G * P.esize;
+                a.da[d] = W + P.w_da + (size_t)d * T * B * G * es;
                 a.W[d] = w->W[l * D + d];
             }
-            a.site = nv; a.out = dxc_here; a.D = D; a.B = B; a.G = G; a.ldo = kin; a.T = T; a.s = P.s_nr;
+            a.site = nv; a.out = dxc_here; a.D = D; a.B = B; a.G = G; a.ldo = kin; a.T = T;
+            a.dense = !P.compact; a.s = P.s_nr;
             launch_dx<E>(a, kin, st);
             if (l == 0) launch_expand(dxc_here, kin, nv, dx, B, kin, T, st);
         }
-        const void* X = l == 0 ? x : (const void*)(R + P.rybuf(l - 1));
+        const void* XT = l == 0 ? (const void*)(R + P.r_xT) : (const void*)(R + P.rybufT(l - 1));
+        const int tper = (T + P.ts - 1) / P.ts;
+        float* wpart = (float*)(W + P.w_wpart);
         for (int d = 0; d < D; ++d) {
             const int k = l * D + d;
             const char* rd = R + P.rdir(l, d);
             WgArgs a;
             memset(&a, 0, sizeof(a));
-            a.act = X; a.act_tstride = (long)B * kin; a.act_ld = kin;
-            a.act_first = nullptr; a.t_first = -1; a.act_shift = 0;
-            a.da = W + P.w_da + (size_t)d * T * B * G * P.esize;
-            a.site = nv; a.dW = g->dW[k]; a.K = kin; a.B = B; a.G = G; a.T = T; a.s = P.s_nr;
-            launch_wgrad<E>(a, st);
+            a.actT = XT; a.tstride = (long)kin * BP; a.actT_first = nullptr; a.t_first = -1; a.shift = 0;
+            a.daT = W + P.w_daT + (size_t)d * T * G * BP * es;
+            a.site = nv; a.K = kin; a.B = B; a.BP = BP; a.G = G; a.T = T; a.tper = tper;
+            a.dense = !P.compact; a.s = P.s_nr;
+            a.out = P.ts > 1 ? wpart : g->dW[k];
+            launch_wgrad<E>(a, P.ts, st);
+            if (P.ts > 1) launch_wreduce(wpart, g->dW[k], (long)kin * G, P.ts, st);
 
             WgArgs u = a;
-            u.act = rd + P.r_hrec; u.act_tstride = (long)B * H; u.act_ld = H;
-            u.act_first = (const char*)h0 + (size_t)k * B * H * P.esize;
+            u.actT = rd + P.r_hrecT; u.tstride = (long)H * BP;
+            u.actT_first = R + P.r_h0T + (size_t)k * H * BP * es;
             u.t_first = d == 0 ? 0 : T - 1;
-            u.act_shift = d == 0 ? -1 : 1;
+            u.shift = d == 0 ? -1 : 1;
             u.site = site_view(P, mbuf, P.site_rh(l, d));
-            u.dW = g->dU[k]; u.K = H; u.s = P.s_rh;
-            launch_wgrad<E>(u, st);
+            u.K = H; u.s = P.s_rh;
+            u.out = P.ts > 1 ? wpart : g->dU[k];
+            launch_wgrad<E>(u, P.ts, st);
+            if (P.ts > 1) launch_wreduce(wpart, g->dU[k], (long)H * G, P.ts, st);
 
-            launch_db((const float*)(W + P.w_dbpart) + (size_t)d * T * G, g->db[k], G, T, st);
+            launch_db((const float*)(W + P.w_dbpart) + (size_t)d * T * P.MGc * G, g->db[k], G, T, P.MGc, st);
         }
     }
     return hip_check("backward launch");
@@ -373,7 +402,8 @@ int lstm_sd_mask_layout_get(const lstm_sd_dims* dims, lstm_sd_mask_layout* out) 
     if (!out) return fail(LSTM_SD_EINVAL, "out is NULL");
     out->sites = P.sites; out->kmax = P.kmax; out->seq_len = P.T; out->reserved = 0;
     out->mask_off = P.m_mask; out->keep_off = P.m_keep; out->pos_off = P.m_pos;
-    out->count_off = P.m_count; out->total_bytes = P.m_total;
+    out->count_off = P.m_count; out->drop_off = P.m_drop; out->dcount_off = P.m_dcount;
+    out->total_bytes = P.m_total;
     return LSTM_SD_OK;
 }
 
@@ -430,9 +460,9 @@ int lstm_sd_backward(const lstm_sd_dims* dims, const lstm_sd_weights* w, const v
     if (setup_kernel_attributes()) return fail(LSTM_SD_EHIP, "hipFuncSetAttribute failed");
     hipStream_t st = (hipStream_t)stream;
     if (P.dtype == LSTM_SD_DTYPE_BF16)
-        return backward_impl<bf16>(P, w, x, lengths, h0, c0, mask_buf, reserve, dy, dhT, dcT, dx, dh0, dc0, g,
+        return backward_impl<bf16>(P, w, lengths, c0, mask_buf, reserve, dy, dhT, dcT, dx, dh0, dc0, g,
                                    workspace, st);
-    return backward_impl<float>(P, w, x, lengths, h0, c0, mask_buf, reserve, dy, dhT, dcT, dx, dh0, dc0, g,
+    return backward_impl<float>(P, w, lengths, c0, mask_buf, reserve, dy, dhT, dcT, dx, dh0, dc0, g,
                                 workspace, st);
 }
 

@@ -1,4 +1,4 @@
-// Kernel argument blocks and launchers shared by the host driver.
+// Kernel argument blocks shared by the host driver and the kernels.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -13,6 +13,8 @@ struct MaskArgs {
     int32_t* keep;
     int32_t* pos;
     int32_t* count;
+    int32_t* drop;
+    int32_t* dcount;
     int T, kmax, compact, generate;
     uint64_t seed, step;
     int K[MAX_SITES];
@@ -20,118 +22,122 @@ struct MaskArgs {
     uint64_t thr[MAX_SITES];
 };
 
-// Mask rows of one site: row t starts at +t*kmax (mask, keep, pos), count[t].
+// Mask rows of one site: row t starts at +t*kmax (mask, keep, pos, drop),
+// count[t], dcount[t].
 struct SiteView {
     const uint8_t* mask;
     const int32_t* keep;
     const int32_t* pos;
     const int32_t* count;
+    const int32_t* drop;
+    const int32_t* dcount;
     int kmax;
 };
 
-// Gathered-K forward product of one layer/direction, all t in one launch:
-//   Gx[t][b][n] = s * sum_{j < count_t} X[t][b][keep_t[j]] * W[keep_t[j]][n] + bias[n]
+// src [N][B][K] -> dst [N][K][BP] (BP >= B; rows b >= B written as zero)
+struct TransArgs {
+    const void* src;
+    void* dst;
+    int B, K, BP;
+};
+
+// Forward input product of one layer/direction, all t in one launch:
+//   Gx[t][b][n] = s * sum_{j < count_t} X[t][b][keep_t[j]] W[keep_t[j]][n] + bias[n]
 struct FxArgs {
-    const void* X;  int ldx;            // X + (t*B + b)*ldx
-    const void* W;                      // [K][N]
+    const void* X; int ldx;             // X + (t*B + b)*ldx
+    const void* W;                      // [K][G]
     const float* bias;
     SiteView site;
-    float* Gx;                          // [T][B][N]
-    int B, N, T;
+    float* Gx;                          // [T][B][G]
+    int B, G, T, dense;
     float s;
 };
 
 // One recurrent forward step, per direction (grid.z = direction).
 struct StepDir {
-    const void* hprev;                  // [B][H] rows of h_{prev} (dtype)
+    const void* hprev;                  // [B][H] row-major h_prev (dtype)
     const void* U;                      // [H][4H]
-    const float* gx;                    // [B][4H] for this t
+    const float* gx;                    // [B][4H] at t
     const uint8_t* mask;                // RH site row at t
     const int32_t* keep;
-    const int32_t* count;               // points at count_t
+    const int32_t* count;               // -> count_t
     float* gates;                       // [B][4H]
     float* cres;                        // [B][H]
-    void* hrec;                         // [B][H] dtype
+    void* hrec;                         // [B][H] row-major h_t (dtype)
+    void* hrecT;                        // [H][BP] h_t transposed (dtype)
     float* hT;                          // [B][H] fp32 state, in place
     float* cT;                          // [B][H] fp32 state, in place
     float* y;                           // top layer output rows + d*H, or null
-    void* ybuf;                         // inter-layer output rows + d*H, or null
+    void* ybuf;                         // inter-layer output rows + d*H (ld ldy), or null
+    void* ybufT;                        // inter-layer output transposed rows + d*H (ld BP), or null
     int t;
 };
 struct StepArgs {
     StepDir d[2];
     const int32_t* lengths;
-    int B, H, ldy;
+    int B, H, ldy, BP, dense;
     float s;
 };
 
-// Backward pointwise of one step (Eq. 7-9 and the activation derivatives).
-struct BwdPwDir {
-    const float* gates;                 // [B][4H] at t
+// One backward step of BPTT for one direction: the output-sparse recurrent
+// gradient of the step processed before (Eq. 10) for the kept units, then
+// the pointwise backward (Eq. 7-9 and activation derivatives) at t.
+struct BwdDir {
+    // recurrent gradient from the previously processed step (has_next)
+    const void* da_next;                // [B][G] dtype
+    const uint8_t* nmask;               // RH mask row of that step
+    const int32_t* nkeep;               // kept units of that step
+    const int32_t* ncount;
+    const int32_t* ndrop;               // dropped units of that step
+    const int32_t* ndcount;
+    const void* U;                      // [H][G]
+    // pointwise at t
+    const float* gates;                 // [B][G]
     const float* cres;                  // c_t [B][H]
-    const float* cprev;                 // c_{prev} [B][H] (reserve or c0)
-    const float* dy;                    // full rows + d*H (top layer), or null
-    const float* dxc;                   // compacted rows of the layer above, or null
-    const int32_t* dxpos;               // NR pos row of the layer above at t (offset by d*H)
-    const float* dhrec;                 // compacted recurrent gradient, or null
-    const int32_t* rhpos;               // RH pos row of the step it came from
+    const float* cprev;                 // c_prev [B][H]
+    const float* dy;                    // top layer: rows + d*H (ld ldy), or null
+    const float* dxc;                   // layer above: compacted rows (ld lddx), or null
+    const int32_t* dxpos;               // NR pos row of the layer above at t, + d*H
     float* dhc;                         // [B][H] pass-through carry, in place
-    float* dcs;                         // [B][H] cell gradient carry, in place
-    void* da;                           // [B][4H] dtype
-    float* dbpart;                      // [4H] for this t
+    float* dcs;                         // [B][H] cell-gradient carry, in place
+    void* da;                           // [B][G] dtype (row-major)
+    void* daT;                          // [G][BP] dtype (transposed)
+    float* dbpart;                      // [MG][G] for this t
+    float* dh0;                         // final pass: [B][H]
+    float* dc0;
     int t;
 };
-struct BwdPwArgs {
-    BwdPwDir d[2];
+struct BwdArgs {
+    BwdDir d[2];
     const int32_t* lengths;
-    int B, H, ldy, lddx;
-};
-
-// Gathered-N backward product: out[b][j] = s * m * sum_n DA[b][n] * Wt[keep[j]][n]
-// (for the recurrent step: one t, grid.z = direction; for dX: grid.z = t and
-// the directions are summed).
-struct DhDir {
-    const void* da;                     // [B][G] rows (dtype)
-    const void* Wk;                     // [K][G] weight with the gathered rows
-    const uint8_t* mask;
-    const int32_t* keep;
-    const int32_t* count;
-    float* out;                         // [B][ldo] compacted output
-};
-struct DhArgs {
-    DhDir d[2];
-    int B, G, ldo;
+    int B, H, BP, ldy, lddx, nkt, has_next, final_pass, dense;
     float s;
 };
 
+// Output-sparse input gradient, all t, summed over directions:
+//   out[t][b][j] = s * m * sum_d sum_n DA_d[t][b][n] W_d[keep_t[j]][n]
 struct DxArgs {
-    const void* da[2];                  // DA_d base [T][B][G]
+    const void* da[2];                  // DA_d [T][B][G]
     const void* W[2];                   // [K][G]
     SiteView site;
     float* out;                         // [T][B][ldo]
-    int D, B, G, ldo, T;
+    int D, B, G, ldo, T, dense;
     float s;
 };
 
-// Row-scatter weight gradient of one layer/direction:
-//   dW[keep_t[j]][n] += s * sum_b act_t[b][keep_t[j]] * DA[t][b][n]
+// Row-scatter weight gradient of one layer/direction, t in [t0, t1) per
+// workgroup row of the grid:
+//   dW[keep_t[j]][n] += s * sum_b actT_t[keep_t[j]][b] DAT_t[n][b]
 struct WgArgs {
-    const void* act;                    // activations: act + t*act_tstride, rows ld act_ld
-    long act_tstride; int act_ld;
-    const void* act_first;              // if non-null, replaces act at t == t_first
-    int t_first; int act_shift;         // act index for t is t + act_shift (h_prev indexing)
-    const void* da;                     // [T][B][G]
+    const void* actT;                   // actT + (t + shift)*tstride: [K][BP]
+    long tstride;
+    const void* actT_first;             // replaces actT at t == t_first (if non-null)
+    int t_first, shift;
+    const void* daT;                    // [T][G][BP]
     SiteView site;
-    float* dW;                          // [K][G]
-    int K, B, G, T;
+    float* out;                         // [TS][K][G] partials (or dW when TS == 1)
+    int K, B, BP, G, T, tper, dense;
     float s;
 };
-
-// Final step of a layer's backward pass.
-struct FinalDir {
-    const float* dhrec; const int32_t* rhpos; const float* dhc; const float* dcs;
-    float* dh0; float* dc0;
-};
-struct FinalArgs { FinalDir d[2]; int B, H; };
 
 }  // namespace lsd

@@ -1,10 +1,15 @@
-// HIP kernels (gfx950, wave64) of the structured-dropout LSTM step.
+// HIP kernels (gfx950, wave64) of the structured-dropout LSTM training step.
 //
-// Every product runs on MFMA 16x16x32 tiles (bf16 inputs, fp32 accumulate;
-// the fp32 path issues the fp32 MFMA).  Operands are gathered by the keep
-// lists while they are loaded, so dropped rows of the contraction are never
-// read or multiplied (compact mode); in dense mode the keep lists are the
-// identity and the mask zeroes the dropped operands instead.
+// Every product runs on MFMA 16x16x32 tiles (bf16 inputs with fp32
+// accumulation; the fp32 path issues the fp32 MFMA).  Operands are gathered
+// through the keep lists while they are loaded, so the dropped rows of a
+// contraction are never read or multiplied (compact mode).  In dense mode
+// the keep lists are the identity and the mask zeroes the dropped operands.
+//
+// Layouts (B = batch, BP = B rounded up to 32, G = 4H):
+//   row-major activations [B][K]        forward products (gather along K)
+//   transposed activations [K][BP]      weight gradients (contiguous in b)
+//   DA [B][G] and DA^T [G][BP]          backward products / weight gradients
 #include <hip/hip_runtime.h>
 
 #include "device.h"
@@ -14,16 +19,34 @@
 namespace lsd {
 
 // ---------------------------------------------------------------------------
-// Masks (Sec. 3.1, Case-III) and compaction into keep lists.
+// Vector loads of 4 consecutive elements (8-byte aligned for bf16, 16 for f32)
+__device__ __forceinline__ void ld4(const bf16* p, bf16* o) {
+    const uint2 v = *(const uint2*)p;
+    o[0] = (bf16)(v.x & 0xffffu); o[1] = (bf16)(v.x >> 16);
+    o[2] = (bf16)(v.y & 0xffffu); o[3] = (bf16)(v.y >> 16);
+}
+__device__ __forceinline__ void ld4(const float* p, float* o) {
+    const float4 v = *(const float4*)p;
+    o[0] = v.x; o[1] = v.y; o[2] = v.z; o[3] = v.w;
+}
+template <typename T>
+__device__ __forceinline__ void zero4(T* o) {
+    o[0] = o[1] = o[2] = o[3] = zero_val<T>();
+}
+
+// ---------------------------------------------------------------------------
+// Masks (Sec. 3.1, Case-III) and their compaction into keep/drop lists.
 // grid (T, sites), block 256.
 __global__ void __launch_bounds__(256) k_mask_build(MaskArgs a) {
     const int t = blockIdx.x, s = blockIdx.y, tid = threadIdx.x;
     const int K = a.K[s];
     __shared__ uint8_t sm[LSTM_SD_MAX_K];
-    __shared__ int wsum[4];
-    uint8_t* mrow = a.mask + ((size_t)s * a.T + t) * a.kmax;
-    int32_t* krow = a.keep + ((size_t)s * a.T + t) * a.kmax;
-    int32_t* prow = a.pos + ((size_t)s * a.T + t) * a.kmax;
+    __shared__ int wsum[4], wdrop[4];
+    const size_t row = ((size_t)s * a.T + t) * a.kmax;
+    uint8_t* mrow = a.mask + row;
+    int32_t* krow = a.keep + row;
+    int32_t* prow = a.pos + row;
+    int32_t* drow = a.drop + row;
     if (a.generate) {
         const uint64_t thr = a.thr[s];
         for (int q = tid; q < (K + 3) / 4; q += blockDim.x) {
@@ -32,12 +55,12 @@ __global__ void __launch_bounds__(256) k_mask_build(MaskArgs a) {
             c.x[1] = (uint64_t)t;
             c.x[2] = (uint64_t)a.sid[s];
             c.x[3] = a.step;
-            u64x4 r = philox4x64_10(c, a.seed, 0ull);
+            const u64x4 r = philox4x64_10(c, a.seed, 0ull);
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                int k = 4 * q + e;
+                const int k = 4 * q + e;
                 if (k < K) {
-                    uint8_t kept = (thr == 0 || r.x[e] >= thr) ? 1 : 0;
+                    const uint8_t kept = (thr == 0 || r.x[e] >= thr) ? 1 : 0;
                     sm[k] = kept;
                     mrow[k] = kept;
                 }
@@ -49,187 +72,329 @@ __global__ void __launch_bounds__(256) k_mask_build(MaskArgs a) {
     __syncthreads();
     if (!a.compact) {
         for (int k = tid; k < K; k += blockDim.x) { krow[k] = k; prow[k] = k; }
-        if (tid == 0) a.count[(size_t)s * a.T + t] = K;
+        if (tid == 0) {
+            a.count[(size_t)s * a.T + t] = K;
+            a.dcount[(size_t)s * a.T + t] = 0;
+        }
         return;
     }
     const int lane = tid & 63, w = tid >> 6;
-    int base = 0;
+    int base = 0, dbase = 0;
     for (int k0 = 0; k0 < K; k0 += 256) {
         const int k = k0 + tid;
         const int f = (k < K) ? sm[k] : 0;
+        const int g = (k < K) ? 1 - f : 0;
         const unsigned long long bal = __ballot(f);
-        const int pre = __popcll(bal & ((1ull << lane) - 1ull));
-        if (lane == 0) wsum[w] = __popcll(bal);
+        const unsigned long long dbal = __ballot(g);
+        const unsigned long long below = (1ull << lane) - 1ull;
+        const int pre = __popcll(bal & below), dpre = __popcll(dbal & below);
+        if (lane == 0) { wsum[w] = __popcll(bal); wdrop[w] = __popcll(dbal); }
         __syncthreads();
-        int off = base;
-        for (int i = 0; i < w; ++i) off += wsum[i];
+        int off = base, doff = dbase;
+        for (int i = 0; i < w; ++i) { off += wsum[i]; doff += wdrop[i]; }
         const int tot = wsum[0] + wsum[1] + wsum[2] + wsum[3];
+        const int dtot = wdrop[0] + wdrop[1] + wdrop[2] + wdrop[3];
         if (k < K) {
             if (f) { krow[off + pre] = k; prow[k] = off + pre; }
-            else prow[k] = -1;
+            else { drow[doff + dpre] = k; prow[k] = -1; }
         }
         base += tot;
+        dbase += dtot;
         __syncthreads();
     }
-    if (tid == 0) a.count[(size_t)s * a.T + t] = base;
+    if (tid == 0) {
+        a.count[(size_t)s * a.T + t] = base;
+        a.dcount[(size_t)s * a.T + t] = dbase;
+    }
 }
 
 // ---------------------------------------------------------------------------
-// FP input product, all t (Eq. 1-4, first term; Sec. 3.2 FP input sparsity).
-// grid (ceil(N/64), ceil(B/32), T), block 256: WG tile 32 rows x 64 cols,
-// wave w owns columns 16w..16w+15 and both 16-row tiles.
+// src [N][B][K] -> dst [N][K][BP], zero rows b in [B, BP).
+// grid (ceil(K/32), BP/32, N), block (32, 8).
+template <typename T>
+__global__ void __launch_bounds__(256) k_transpose(TransArgs a) {
+    __shared__ T tile[32][33];
+    const int n = blockIdx.z;
+    const int k0 = blockIdx.x * 32, b0 = blockIdx.y * 32;
+    const T* src = (const T*)a.src + (size_t)n * a.B * a.K;
+    T* dst = (T*)a.dst + (size_t)n * a.K * a.BP;
+    for (int i = threadIdx.y; i < 32; i += 8) {
+        const int b = b0 + i, k = k0 + threadIdx.x;
+        tile[i][threadIdx.x] = (b < a.B && k < a.K) ? src[(size_t)b * a.K + k] : zero_val<T>();
+    }
+    __syncthreads();
+    for (int i = threadIdx.y; i < 32; i += 8) {
+        const int k = k0 + i, b = b0 + threadIdx.x;
+        if (k < a.K) dst[(size_t)k * a.BP + b] = tile[threadIdx.x][i];
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Forward input product, all t (Eq. 1-4 first term; Sec. 3.2, FP input
+// sparsity: the dropped columns of x and rows of W are skipped).
+// grid (ceil(G/64), ceil(B/64), T), block 256: wave w owns 16 columns and up
+// to 4 row tiles; the keep row of t is staged in LDS.
 template <typename T>
 __global__ void __launch_bounds__(256) k_fx(FxArgs a) {
+    __shared__ int kidx[LSTM_SD_MAX_K];
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int t = blockIdx.z;
-    const int m0 = blockIdx.y * 32;
+    const int m0 = blockIdx.y * 64;
     const int n = blockIdx.x * 64 + w * 16 + (lane & 15);
+    const bool nok = n < a.G;
     const int g8 = 8 * (lane >> 4);
     const T* X = (const T*)a.X + (size_t)t * a.B * a.ldx;
     const T* W = (const T*)a.W;
-    const uint8_t* mrow = a.site.mask + (size_t)t * a.site.kmax;
     const int32_t* krow = a.site.keep + (size_t)t * a.site.kmax;
+    const uint8_t* mrow = a.site.mask + (size_t)t * a.site.kmax;
     const int cnt = a.site.count[t];
-    f32x4_t acc0 = {0, 0, 0, 0}, acc1 = {0, 0, 0, 0};
-    const int r0 = m0 + (lane & 15), r1 = r0 + 16;
+    for (int j = threadIdx.x; j < cnt; j += blockDim.x) {
+        const int k = krow[j];
+        kidx[j] = (a.dense && !mrow[k]) ? -1 : k;
+    }
+    __syncthreads();
+    const int mtiles = min(4, (a.B - m0 + 15) / 16);
+    f32x4_t acc[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[i] = f32x4_t{0, 0, 0, 0};
     for (int kc = 0; kc < cnt; kc += 32) {
-        Frag<T> fa0, fa1, fb;
+        int kk[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
             const int j = kc + g8 + e;
-            T va0 = zero_val<T>(), va1 = zero_val<T>(), vb = zero_val<T>();
-            if (j < cnt) {
-                const int k = krow[j];
-                if (mrow[k]) {
-                    if (r0 < a.B) va0 = X[(size_t)r0 * a.ldx + k];
-                    if (r1 < a.B) va1 = X[(size_t)r1 * a.ldx + k];
-                }
-                if (n < a.N) vb = W[(size_t)k * a.N + n];
-            }
-            fa0.v[e] = va0; fa1.v[e] = va1; fb.v[e] = vb;
+            kk[e] = j < cnt ? kidx[j] : -1;
         }
-        mma_16x16x32(fa0, fb, acc0);
-        mma_16x16x32(fa1, fb, acc1);
+        Frag<T> fb;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) fb.v[e] = (kk[e] >= 0 && nok) ? W[(size_t)kk[e] * a.G + n] : zero_val<T>();
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) {
+            if (mt < mtiles) {
+                const int row = m0 + mt * 16 + (lane & 15);
+                const bool rok = row < a.B;
+                Frag<T> fa;
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    fa.v[e] = (kk[e] >= 0 && rok) ? X[(size_t)row * a.ldx + kk[e]] : zero_val<T>();
+                mma_16x16x32(fa, fb, acc[mt]);
+            }
+        }
     }
-    if (n < a.N) {
+    if (nok) {
         const float bn = a.bias[n];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            int row = m0 + acc_row(lane, r);
-            if (row < a.B) a.Gx[((size_t)t * a.B + row) * a.N + n] = a.s * acc0[r] + bn;
-            row += 16;
-            if (row < a.B) a.Gx[((size_t)t * a.B + row) * a.N + n] = a.s * acc1[r] + bn;
-        }
+        for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int row = m0 + mt * 16 + acc_row(lane, r);
+                if (mt < mtiles && row < a.B) a.Gx[((size_t)t * a.B + row) * a.G + n] = a.s * acc[mt][r] + bn;
+            }
     }
 }
 
 // ---------------------------------------------------------------------------
-// One recurrent forward step (Eq. 1-6), fused with the gate pointwise.
-// grid (ceil(H/4), 1, D), block 256.  A workgroup owns 4 hidden units and
-// therefore the 16 gate columns {g*H + u}; the contraction over the kept
-// recurrent neurons is split over the 4 waves and reduced in LDS.
-template <typename T>
-__global__ void __launch_bounds__(256) k_step(StepArgs a) {
+// One recurrent forward step (Eq. 1-6) fused with the gate pointwise.
+// grid (ceil(H/(4NT)), ceil(B/(64/NT)), D), block 1024 (16 waves).  A
+// workgroup owns 4*NT hidden units, i.e. NT 16-column tiles holding the
+// four gates of 4 units each, for 64/NT batch rows; the contraction over
+// the kept recurrent neurons is split over the 16 waves and reduced in LDS.
+template <typename T, int NT>
+__global__ void __launch_bounds__(1024) k_step(StepArgs a) {
+    constexpr int MG = 64 / NT, MT = MG / 16, UPW = 4 * NT;
+    __shared__ int kidx[LSTM_SD_MAX_K];
+    __shared__ float red[16][MG][16 * NT + 1];
     const StepDir& D = a.d[blockIdx.z];
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int H = a.H, G = 4 * H, B = a.B;
-    const int u0 = blockIdx.x * 4;
-    const int c = lane & 15;                        // tile column
-    const int ucol = u0 + (c & 3);
-    const int gcol = (c >> 2) * H + ucol;           // gate column in [0, 4H)
-    const bool colok = ucol < H;
+    const int u0 = blockIdx.x * UPW;
+    const int m0 = blockIdx.y * MG;
     const int g8 = 8 * (lane >> 4);
     const T* hp = (const T*)D.hprev;
     const T* U = (const T*)D.U;
     const int cnt = *D.count;
-    __shared__ float red[4][64][17];
-    for (int mg = 0; mg < B; mg += 64) {
+    for (int j = threadIdx.x; j < cnt; j += blockDim.x) {
+        const int k = D.keep[j];
+        kidx[j] = (a.dense && !D.mask[k]) ? -1 : k;
+    }
+    __syncthreads();
+    int gcol[NT];
+    bool cok[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+        const int c = lane & 15;
+        const int unit = u0 + 4 * nt + (c & 3);
+        cok[nt] = unit < H;
+        gcol[nt] = (c >> 2) * H + unit;
+    }
+    f32x4_t acc[MT][NT];
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int j = 0; j < NT; ++j) acc[i][j] = f32x4_t{0, 0, 0, 0};
+    for (int kc = 32 * w; kc < cnt; kc += 32 * 16) {
+        int kk[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int j = kc + g8 + e;
+            kk[e] = j < cnt ? kidx[j] : -1;
+        }
+        Frag<T> fb[NT];
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                fb[nt].v[e] = (kk[e] >= 0 && cok[nt]) ? U[(size_t)kk[e] * G + gcol[nt]] : zero_val<T>();
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            const int row = m0 + mt * 16 + (lane & 15);
+            const bool rok = row < B;
+            Frag<T> fa;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) fa.v[e] = (kk[e] >= 0 && rok) ? hp[(size_t)row * H + kk[e]] : zero_val<T>();
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) mma_16x16x32(fa, fb[nt], acc[mt][nt]);
+        }
+    }
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) red[w][mt * 16 + acc_row(lane, r)][nt * 16 + (lane & 15)] = acc[mt][nt][r];
+    __syncthreads();
+    if (threadIdx.x < MG * UPW) {
+        const int rr = threadIdx.x / UPW, uu = threadIdx.x % UPW;
+        const int b = m0 + rr, u = u0 + uu;
+        if (b < B && u < H) {
+            const int nt = uu >> 2, cu = uu & 3;
+            float pre[4];
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int cc = nt * 16 + g * 4 + cu;
+                float v = 0.f;
+#pragma unroll
+                for (int i = 0; i < 16; ++i) v += red[i][rr][cc];
+                pre[g] = a.s * v + D.gx[(size_t)b * G + g * H + u];
+            }
+            const float ig = 1.0f / (1.0f + expf(-pre[0]));
+            const float fg = 1.0f / (1.0f + expf(-pre[1]));
+            const float gg = tanhf(pre[2]);
+            const float og = 1.0f / (1.0f + expf(-pre[3]));
+            const float cp = D.cT[(size_t)b * H + u];
+            const float cn = fg * cp + ig * gg;
+            const float hn = og * tanhf(cn);
+            const bool valid = (a.lengths == nullptr) || (D.t < a.lengths[b]);
+            float* gt = D.gates + (size_t)b * G;
+            gt[u] = ig; gt[H + u] = fg; gt[2 * H + u] = gg; gt[3 * H + u] = og;
+            D.cres[(size_t)b * H + u] = valid ? cn : cp;
+            const T hv = valid ? from_f32<T>(hn) : hp[(size_t)b * H + u];
+            ((T*)D.hrec)[(size_t)b * H + u] = hv;
+            ((T*)D.hrecT)[(size_t)u * a.BP + b] = hv;
+            if (valid) {
+                D.cT[(size_t)b * H + u] = cn;
+                D.hT[(size_t)b * H + u] = hn;
+            }
+            if (D.y) D.y[(size_t)b * a.ldy + u] = valid ? hn : 0.0f;
+            if (D.ybuf) {
+                const T yv = valid ? from_f32<T>(hn) : zero_val<T>();
+                ((T*)D.ybuf)[(size_t)b * a.ldy + u] = yv;
+                ((T*)D.ybufT)[(size_t)u * a.BP + b] = yv;
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// One BPTT step (per direction, grid.z).  grid (nkt + ceil(H/16),
+// ceil(B/64), D), block 1024 (16 waves).
+//   * workgroups x < nkt own 16 units kept at the previously processed step:
+//     they first form the output-sparse recurrent gradient of those units,
+//     dh_rec[b][u] = s * m * sum_n DA_next[b][n] U[u][n] (Eq. 10), with the
+//     contraction over 4H split across the 16 waves;
+//   * the other workgroups own 16 units dropped at that step (no product).
+// Every workgroup then runs the pointwise backward of its units at t.  In
+// the final pass (after the last step) it writes dh0 and dc0 instead.
+template <typename T>
+__global__ void __launch_bounds__(1024) k_bwd(BwdArgs a) {
+    __shared__ float red[16][64][17];
+    __shared__ int units[16];
+    const BwdDir& D = a.d[blockIdx.z];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int H = a.H, G = 4 * H, B = a.B;
+    const int m0 = blockIdx.y * 64;
+    const bool kept_tile = a.has_next && (int)blockIdx.x < a.nkt;
+    int j0, nlist;
+    const int32_t* list;
+    if (kept_tile) {
+        j0 = blockIdx.x * 16; nlist = *D.ncount; list = D.nkeep;
+    } else {
+        j0 = (blockIdx.x - (a.has_next ? a.nkt : 0)) * 16;
+        if (a.has_next) { nlist = *D.ndcount; list = D.ndrop; }
+        else { nlist = H; list = nullptr; }
+    }
+    if (j0 >= nlist) return;
+    if (threadIdx.x < 16) {
+        const int j = j0 + threadIdx.x;
+        units[threadIdx.x] = j < nlist ? (list ? list[j] : j) : -1;
+    }
+    __syncthreads();
+    if (kept_tile) {
+        const int ul = units[lane & 15];
+        const int g8 = 8 * (lane >> 4);
+        const T* DA = (const T*)D.da_next;
+        const T* U = (const T*)D.U;
         f32x4_t acc[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) acc[i] = f32x4_t{0, 0, 0, 0};
-        for (int kc = 32 * w; kc < cnt; kc += 128) {
+        const int mtiles = min(4, (B - m0 + 15) / 16);
+        for (int nc = 32 * w; nc < G; nc += 32 * 16) {
             Frag<T> fb;
-            int kk[8];
-            bool kv[8];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int j = kc + g8 + e;
-                kv[e] = j < cnt;
-                kk[e] = kv[e] ? D.keep[j] : 0;
-                if (kv[e] && !D.mask[kk[e]]) kv[e] = false;
-                fb.v[e] = (kv[e] && colok) ? U[(size_t)kk[e] * G + gcol] : zero_val<T>();
+            for (int h = 0; h < 2; ++h) {
+                const int n = nc + g8 + 4 * h;
+                if (ul >= 0 && n < G) ld4(U + (size_t)ul * G + n, fb.v + 4 * h);
+                else zero4(fb.v + 4 * h);
             }
 #pragma unroll
             for (int mt = 0; mt < 4; ++mt) {
-                const int row = mg + mt * 16 + (lane & 15);
-                if (mg + mt * 16 >= B) break;
-                Frag<T> fa;
+                if (mt < mtiles) {
+                    const int row = m0 + mt * 16 + (lane & 15);
+                    Frag<T> fa;
 #pragma unroll
-                for (int e = 0; e < 8; ++e)
-                    fa.v[e] = (kv[e] && row < B) ? hp[(size_t)row * H + kk[e]] : zero_val<T>();
-                mma_16x16x32(fa, fb, acc[mt]);
+                    for (int h = 0; h < 2; ++h) {
+                        const int n = nc + g8 + 4 * h;
+                        if (row < B && n < G) ld4(DA + (size_t)row * G + n, fa.v + 4 * h);
+                        else zero4(fa.v + 4 * h);
+                    }
+                    mma_16x16x32(fa, fb, acc[mt]);
+                }
             }
         }
 #pragma unroll
         for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) red[w][mt * 16 + acc_row(lane, r)][c] = acc[mt][r];
-        __syncthreads();
-        // pointwise: thread -> (row, unit)
-        {
-            const int rr = threadIdx.x >> 2, uu = threadIdx.x & 3;
-            const int b = mg + rr, u = u0 + uu;
-            if (b < B && u < H) {
-                float pre[4];
-#pragma unroll
-                for (int g = 0; g < 4; ++g) {
-                    const int cc = g * 4 + uu;
-                    float v = red[0][rr][cc] + red[1][rr][cc] + red[2][rr][cc] + red[3][rr][cc];
-                    pre[g] = a.s * v + D.gx[(size_t)b * G + g * H + u];
-                }
-                const float ig = 1.0f / (1.0f + expf(-pre[0]));
-                const float fg = 1.0f / (1.0f + expf(-pre[1]));
-                const float gg = tanhf(pre[2]);
-                const float og = 1.0f / (1.0f + expf(-pre[3]));
-                const float cp = D.cT[(size_t)b * H + u];
-                const float cn = fg * cp + ig * gg;
-                const float hn = og * tanhf(cn);
-                const bool valid = (a.lengths == nullptr) || (D.t < a.lengths[b]);
-                float* gt = D.gates + (size_t)b * G;
-                gt[u] = ig; gt[H + u] = fg; gt[2 * H + u] = gg; gt[3 * H + u] = og;
-                D.cres[(size_t)b * H + u] = valid ? cn : cp;
-                ((T*)D.hrec)[(size_t)b * H + u] = valid ? from_f32<T>(hn) : hp[(size_t)b * H + u];
-                if (valid) {
-                    D.cT[(size_t)b * H + u] = cn;
-                    D.hT[(size_t)b * H + u] = hn;
-                }
-                if (D.y) D.y[(size_t)b * a.ldy + u] = valid ? hn : 0.0f;
-                if (D.ybuf) ((T*)D.ybuf)[(size_t)b * a.ldy + u] = valid ? from_f32<T>(hn) : zero_val<T>();
-            }
-        }
-        __syncthreads();
+            for (int r = 0; r < 4; ++r) red[w][mt * 16 + acc_row(lane, r)][lane & 15] = acc[mt][r];
     }
-}
-
-// ---------------------------------------------------------------------------
-// Backward pointwise of one step (Eq. 7-9 plus the activation derivatives),
-// and the per-step bias-gradient partial sum over the batch.
-// grid (ceil(H/16), 1, D), block 256: thread -> unit tid%16, rows tid/16 + 16i.
-template <typename T>
-__global__ void __launch_bounds__(256) k_bwd_pw(BwdPwArgs a) {
-    const BwdPwDir& D = a.d[blockIdx.z];
-    const int H = a.H, G = 4 * H, B = a.B;
-    const int uu = threadIdx.x & 15, rg = threadIdx.x >> 4;
-    const int u = blockIdx.x * 16 + uu;
-    float dbs[4] = {0, 0, 0, 0};
-    if (u < H) {
-        for (int b = rg; b < B; b += 16) {
+    __syncthreads();
+    // pointwise: thread -> (row rr, unit slot i)
+    const int rr = threadIdx.x >> 4, i = threadIdx.x & 15;
+    const int b = m0 + rr;
+    const int u = units[i];
+    float da4[4] = {0.f, 0.f, 0.f, 0.f};
+    if (b < B && u >= 0) {
+        float dh = D.dhc[(size_t)b * H + u];
+        if (kept_tile) {
+            float v = 0.f;
+#pragma unroll
+            for (int q = 0; q < 16; ++q) v += red[q][rr][i];
+            const float sc = (a.dense && !D.nmask[u]) ? 0.0f : a.s;
+            dh += sc * v;
+        }
+        if (a.final_pass) {
+            D.dh0[(size_t)b * H + u] = dh;
+            D.dc0[(size_t)b * H + u] = D.dcs[(size_t)b * H + u];
+        } else {
             const bool valid = (a.lengths == nullptr) || (D.t < a.lengths[b]);
-            float dh = D.dhc[(size_t)b * H + u];
-            if (D.dhrec) {
-                const int p = D.rhpos[u];
-                if (p >= 0) dh += D.dhrec[(size_t)b * H + p];
-            }
             if (valid) {
                 if (D.dy) dh += D.dy[(size_t)b * a.ldy + u];
                 if (D.dxc) {
@@ -237,198 +402,187 @@ __global__ void __launch_bounds__(256) k_bwd_pw(BwdPwArgs a) {
                     if (p >= 0) dh += D.dxc[(size_t)b * a.lddx + p];
                 }
             }
-            const float* gt = D.gates + (size_t)b * G;
-            float da0 = 0.f, da1 = 0.f, da2 = 0.f, da3 = 0.f;
             const float dcin = D.dcs[(size_t)b * H + u];
             if (valid) {
+                const float* gt = D.gates + (size_t)b * G;
                 const float ig = gt[u], fg = gt[H + u], gg = gt[2 * H + u], og = gt[3 * H + u];
                 const float ct = D.cres[(size_t)b * H + u];
                 const float cp = D.cprev[(size_t)b * H + u];
                 const float tc = tanhf(ct);
-                const float dout = dh * tc;                           // Eq. 7
-                const float dc = dh * og * (1.0f - tc * tc) + dcin;   // Eq. 7
-                const float df = dc * cp, di = dc * gg, dg = dc * ig; // Eq. 8-9
-                da0 = di * ig * (1.0f - ig);
-                da1 = df * fg * (1.0f - fg);
-                da2 = dg * (1.0f - gg * gg);
-                da3 = dout * og * (1.0f - og);
-                D.dcs[(size_t)b * H + u] = dc * fg;                   // Eq. 8
+                const float dout = dh * tc;                            // Eq. 7
+                const float dc = dh * og * (1.0f - tc * tc) + dcin;    // Eq. 7
+                da4[0] = dc * gg * ig * (1.0f - ig);                   // Eq. 9, sigmoid'
+                da4[1] = dc * cp * fg * (1.0f - fg);                   // Eq. 8, sigmoid'
+                da4[2] = dc * ig * (1.0f - gg * gg);                   // Eq. 9, tanh'
+                da4[3] = dout * og * (1.0f - og);                      // Eq. 7, sigmoid'
+                D.dcs[(size_t)b * H + u] = dc * fg;                    // Eq. 8
                 D.dhc[(size_t)b * H + u] = 0.0f;
             } else {
-                D.dhc[(size_t)b * H + u] = dh;                        // frozen row
+                D.dhc[(size_t)b * H + u] = dh;                         // frozen row: pass through
             }
             T* dar = (T*)D.da + (size_t)b * G;
-            dar[u] = from_f32<T>(da0);
-            dar[H + u] = from_f32<T>(da1);
-            dar[2 * H + u] = from_f32<T>(da2);
-            dar[3 * H + u] = from_f32<T>(da3);
-            dbs[0] += da0; dbs[1] += da1; dbs[2] += da2; dbs[3] += da3;
+            T* dat = (T*)D.daT;
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const T v = from_f32<T>(da4[g]);
+                dar[g * H + u] = v;
+                dat[(size_t)(g * H + u) * a.BP + b] = v;
+            }
         }
     }
-    __shared__ float red[16][4][16];
+    if (a.final_pass) return;
+    // bias-gradient partial over this workgroup's rows: reuse red
+    __syncthreads();
 #pragma unroll
-    for (int g = 0; g < 4; ++g) red[rg][g][uu] = dbs[g];
+    for (int g = 0; g < 4; ++g) red[g][rr][i] = da4[g];
     __syncthreads();
     if (threadIdx.x < 64) {
         const int g = threadIdx.x >> 4, q = threadIdx.x & 15;
-        const int uq = blockIdx.x * 16 + q;
-        if (uq < H) {
+        const int uq = units[q];
+        if (uq >= 0) {
             float s = 0.f;
-            for (int i = 0; i < 16; ++i) s += red[i][g][q];
-            D.dbpart[g * H + uq] = s;
+            for (int r = 0; r < 64; ++r) s += red[g][r][q];
+            D.dbpart[(size_t)blockIdx.y * G + g * H + uq] = s;
         }
     }
 }
 
 // ---------------------------------------------------------------------------
-// Output-sparse recurrent gradient of one step (Eq. 10, Sec. 3.2 BP):
-//   dhrec[b][j] = s * m * sum_n DA[b][n] U[keep[j]][n], j < count.
-// grid (ceil(H/64), ceil(B/32), D), block 256; tile 32 rows x 64 kept columns.
-template <typename T>
-__global__ void __launch_bounds__(256) k_bwd_dh(DhArgs a) {
-    const DhDir& D = a.d[blockIdx.z];
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int cnt = *D.count;
-    const int j0 = blockIdx.x * 64;
-    if (j0 >= cnt) return;
-    const int m0 = blockIdx.y * 32;
-    const int j = j0 + w * 16 + (lane & 15);
-    const int g8 = 8 * (lane >> 4);
-    const T* DA = (const T*)D.da;
-    const T* Wk = (const T*)D.Wk;
-    const int k = (j < cnt) ? D.keep[j] : -1;
-    const int r0 = m0 + (lane & 15), r1 = r0 + 16;
-    f32x4_t acc0 = {0, 0, 0, 0}, acc1 = {0, 0, 0, 0};
-    for (int nc = 0; nc < a.G; nc += 32) {
-        Frag<T> fa0, fa1, fb;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const int n = nc + g8 + e;
-            const bool nv = n < a.G;
-            fa0.v[e] = (nv && r0 < a.B) ? DA[(size_t)r0 * a.G + n] : zero_val<T>();
-            fa1.v[e] = (nv && r1 < a.B) ? DA[(size_t)r1 * a.G + n] : zero_val<T>();
-            fb.v[e] = (nv && k >= 0) ? Wk[(size_t)k * a.G + n] : zero_val<T>();
-        }
-        mma_16x16x32(fa0, fb, acc0);
-        mma_16x16x32(fa1, fb, acc1);
-    }
-    // columns of this lane's outputs: j (acc_col = lane & 15)
-    if (j < cnt) {
-        const float sc = D.mask[k] ? a.s : 0.0f;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            int row = m0 + acc_row(lane, r);
-            if (row < a.B) D.out[(size_t)row * a.ldo + j] = sc * acc0[r];
-            row += 16;
-            if (row < a.B) D.out[(size_t)row * a.ldo + j] = sc * acc1[r];
-        }
-    }
-}
-
-// ---------------------------------------------------------------------------
-// Output-sparse input gradient, all t (Eq. 10), summed over directions:
-//   dxc[t][b][j] = s * m * sum_d sum_n DA_d[t][b][n] W_d[keep_t[j]][n].
-// grid (ceil(Kmax/64), ceil(B/32), T), block 256.
+// Output-sparse input gradient, all t (Eq. 10), summed over directions.
+// grid (ceil(K/16), T, ceil(B/64)), block 256: 16 kept columns per
+// workgroup, the contraction over 4H split over the 4 waves.
 template <typename T>
 __global__ void __launch_bounds__(256) k_dx(DxArgs a) {
+    __shared__ float red[4][64][17];
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int t = blockIdx.z;
+    const int t = blockIdx.y;
     const int cnt = a.site.count[t];
-    const int j0 = blockIdx.x * 64;
+    const int j0 = blockIdx.x * 16;
     if (j0 >= cnt) return;
-    const int m0 = blockIdx.y * 32;
-    const int j = j0 + w * 16 + (lane & 15);
+    const int m0 = blockIdx.z * 64;
+    const int j = j0 + (lane & 15);
     const int g8 = 8 * (lane >> 4);
     const int32_t* krow = a.site.keep + (size_t)t * a.site.kmax;
     const uint8_t* mrow = a.site.mask + (size_t)t * a.site.kmax;
     const int k = (j < cnt) ? krow[j] : -1;
-    const int r0 = m0 + (lane & 15), r1 = r0 + 16;
-    f32x4_t acc0 = {0, 0, 0, 0}, acc1 = {0, 0, 0, 0};
+    const int mtiles = min(4, (a.B - m0 + 15) / 16);
+    f32x4_t acc[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[i] = f32x4_t{0, 0, 0, 0};
     for (int d = 0; d < a.D; ++d) {
         const T* DA = (const T*)a.da[d] + (size_t)t * a.B * a.G;
         const T* Wk = (const T*)a.W[d];
-        for (int nc = 0; nc < a.G; nc += 32) {
-            Frag<T> fa0, fa1, fb;
+        for (int nc = 32 * w; nc < a.G; nc += 128) {
+            Frag<T> fb;
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int n = nc + g8 + e;
-                const bool nv = n < a.G;
-                fa0.v[e] = (nv && r0 < a.B) ? DA[(size_t)r0 * a.G + n] : zero_val<T>();
-                fa1.v[e] = (nv && r1 < a.B) ? DA[(size_t)r1 * a.G + n] : zero_val<T>();
-                fb.v[e] = (nv && k >= 0) ? Wk[(size_t)k * a.G + n] : zero_val<T>();
+            for (int h = 0; h < 2; ++h) {
+                const int n = nc + g8 + 4 * h;
+                if (k >= 0 && n < a.G) ld4(Wk + (size_t)k * a.G + n, fb.v + 4 * h);
+                else zero4(fb.v + 4 * h);
             }
-            mma_16x16x32(fa0, fb, acc0);
-            mma_16x16x32(fa1, fb, acc1);
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt) {
+                if (mt < mtiles) {
+                    const int row = m0 + mt * 16 + (lane & 15);
+                    Frag<T> fa;
+#pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        const int n = nc + g8 + 4 * h;
+                        if (row < a.B && n < a.G) ld4(DA + (size_t)row * a.G + n, fa.v + 4 * h);
+                        else zero4(fa.v + 4 * h);
+                    }
+                    mma_16x16x32(fa, fb, acc[mt]);
+                }
+            }
         }
     }
-    if (j < cnt) {
-        const float sc = mrow[k] ? a.s : 0.0f;
-        float* out = a.out + (size_t)t * a.B * a.ldo;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            int row = m0 + acc_row(lane, r);
-            if (row < a.B) out[(size_t)row * a.ldo + j] = sc * acc0[r];
-            row += 16;
-            if (row < a.B) out[(size_t)row * a.ldo + j] = sc * acc1[r];
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) red[w][mt * 16 + acc_row(lane, r)][lane & 15] = acc[mt][r];
+    __syncthreads();
+    float* out = a.out + (size_t)t * a.B * a.ldo;
+    for (int q = threadIdx.x; q < 64 * 16; q += 256) {
+        const int rr = q >> 4, c = q & 15;
+        const int row = m0 + rr, jj = j0 + c;
+        if (row < a.B && jj < cnt) {
+            const int kk = krow[jj];
+            const float sc = (a.dense && !mrow[kk]) ? 0.0f : a.s;
+            out[(size_t)row * a.ldo + jj] = sc * (red[0][rr][c] + red[1][rr][c] + red[2][rr][c] + red[3][rr][c]);
         }
     }
 }
 
 // ---------------------------------------------------------------------------
-// Row-sparse weight gradient (Eq. 11, Sec. 3.2 WG), summed over t.
-// grid (ceil(G/16)), block 256, dynamic LDS K*16 floats: a workgroup owns 16
-// columns of dW for every row and accumulates in LDS; at each t the kept
-// rows are processed in 16-row tiles (distinct rows per tile, so waves never
-// collide), and rows never kept stay exactly zero.
+// Row-sparse weight gradient (Eq. 11; Sec. 3.2 WG).  grid (ceil(G/16), TS),
+// block 512, dynamic LDS K*16 floats.  A workgroup owns 16 columns of the
+// gradient for every row and the time steps [ts*tper, ts*tper + tper); at each
+// t the kept rows are processed in 16-row tiles (distinct rows per tile, so
+// waves never touch the same LDS row), and never-kept rows stay zero.
 template <typename T>
-__global__ void __launch_bounds__(256) k_wgrad(WgArgs a) {
+__global__ void __launch_bounds__(512) k_wgrad(WgArgs a) {
     extern __shared__ float acc_lds[];   // [K][16]
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int n0 = blockIdx.x * 16;
     const int col = lane & 15;
     const int n = n0 + col;
+    const bool nok = n < a.G;
     const int g8 = 8 * (lane >> 4);
     for (int i = threadIdx.x; i < a.K * 16; i += blockDim.x) acc_lds[i] = 0.0f;
     __syncthreads();
-    const T* DAall = (const T*)a.da;
-    for (int t = 0; t < a.T; ++t) {
+    const int t0 = blockIdx.y * a.tper;
+    const int t1 = min(a.T, t0 + a.tper);
+    for (int t = t0; t < t1; ++t) {
         const int cnt = a.site.count[t];
         const int32_t* krow = a.site.keep + (size_t)t * a.site.kmax;
         const uint8_t* mrow = a.site.mask + (size_t)t * a.site.kmax;
-        const T* act;
-        if (a.act_first && t == a.t_first) act = (const T*)a.act_first;
-        else act = (const T*)a.act + (long)(t + a.act_shift) * a.act_tstride;
-        const T* DA = DAall + (size_t)t * a.B * a.G;
-        for (int jt = w; jt * 16 < cnt; jt += 4) {
-            const int j = jt * 16 + (lane & 15);        // A row of this lane
+        const T* act = (a.actT_first && t == a.t_first) ? (const T*)a.actT_first
+                                                        : (const T*)a.actT + (long)(t + a.shift) * a.tstride;
+        const T* DAT = (const T*)a.daT + (size_t)t * a.G * a.BP;
+        for (int jt = w; jt * 16 < cnt; jt += 8) {
+            const int j = jt * 16 + (lane & 15);
             int k = -1;
-            if (j < cnt) { k = krow[j]; if (!mrow[k]) k = -1; }
+            if (j < cnt) {
+                k = krow[j];
+                if (a.dense && !mrow[k]) k = -1;
+            }
             f32x4_t acc = {0, 0, 0, 0};
             for (int bc = 0; bc < a.B; bc += 32) {
                 Frag<T> fa, fb;
 #pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const int b = bc + g8 + e;
-                    const bool bv = b < a.B;
-                    fa.v[e] = (bv && k >= 0) ? act[(size_t)b * a.act_ld + k] : zero_val<T>();
-                    fb.v[e] = (bv && n < a.G) ? DA[(size_t)b * a.G + n] : zero_val<T>();
+                for (int h = 0; h < 2; ++h) {
+                    const int b = bc + g8 + 4 * h;
+                    if (k >= 0) ld4(act + (size_t)k * a.BP + b, fa.v + 4 * h);
+                    else zero4(fa.v + 4 * h);
+                    if (nok) ld4(DAT + (size_t)n * a.BP + b, fb.v + 4 * h);
+                    else zero4(fb.v + 4 * h);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (b + e >= a.B) { fa.v[4 * h + e] = zero_val<T>(); fb.v[4 * h + e] = zero_val<T>(); }
                 }
                 mma_16x16x32(fa, fb, acc);
             }
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int jr = jt * 16 + acc_row(lane, r);
-                if (jr < cnt) {
-                    const int kr = krow[jr];
-                    acc_lds[kr * 16 + col] += a.s * acc[r];
-                }
+                if (jr < cnt) acc_lds[krow[jr] * 16 + col] += a.s * acc[r];
             }
         }
         __syncthreads();
     }
+    float* out = a.out + (size_t)blockIdx.y * a.K * a.G;
     for (int i = threadIdx.x; i < a.K * 16; i += blockDim.x) {
         const int kr = i >> 4, cc = i & 15;
-        if (n0 + cc < a.G) a.dW[(size_t)kr * a.G + n0 + cc] = acc_lds[i];
+        if (n0 + cc < a.G) out[(size_t)kr * a.G + n0 + cc] = acc_lds[i];
+    }
+}
+
+// dW = sum over ts of the partials
+__global__ void k_wreduce(const float* part, float* dW, long n, int ts) {
+    for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < n; i += (long)gridDim.x * blockDim.x) {
+        float s = 0.f;
+        for (int q = 0; q < ts; ++q) s += part[(size_t)q * n + i];
+        dW[i] = s;
     }
 }
 
@@ -444,27 +598,11 @@ __global__ void k_fwd_init(const T* h0, const float* c0, float* hT, float* cT, l
     }
 }
 
-// carries <- dhT/dcT slices (or zero) for D directions of one layer
+// carries <- dhT/dcT slices (or zero)
 __global__ void k_bwd_init(const float* dhT, const float* dcT, float* dhc, float* dcs, long n) {
     for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < n; i += (long)gridDim.x * blockDim.x) {
         dhc[i] = dhT ? dhT[i] : 0.0f;
         dcs[i] = dcT ? dcT[i] : 0.0f;
-    }
-}
-
-// dh0 = (expanded last recurrent gradient) + carry, dc0 = cell carry
-__global__ void k_bwd_final(FinalArgs a) {
-    const FinalDir& D = a.d[blockIdx.y];
-    const long n = (long)a.B * a.H;
-    for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < n; i += (long)gridDim.x * blockDim.x) {
-        const int b = (int)(i / a.H), u = (int)(i % a.H);
-        float v = D.dhc[i];
-        if (D.dhrec) {
-            const int p = D.rhpos[u];
-            if (p >= 0) v += D.dhrec[(size_t)b * a.H + p];
-        }
-        D.dh0[i] = v;
-        D.dc0[i] = D.dcs[i];
     }
 }
 
@@ -480,12 +618,13 @@ __global__ void k_expand(const float* dxc, int ldc, SiteView site, float* dx, in
     }
 }
 
-// db[n] = sum_t dbpart[t][n]
-__global__ void k_db(const float* dbpart, float* db, int G, int T) {
+// db[n] = sum over t and row groups of dbpart[t][g][n]
+__global__ void k_db(const float* dbpart, float* db, int G, int T, int ng) {
     const int n = blockIdx.x * blockDim.x + threadIdx.x;
     if (n >= G) return;
     float s = 0.f;
-    for (int t = 0; t < T; ++t) s += dbpart[(size_t)t * G + n];
+    for (int t = 0; t < T; ++t)
+        for (int g = 0; g < ng; ++g) s += dbpart[((size_t)t * ng + g) * G + n];
     db[n] = s;
 }
 
@@ -551,31 +690,39 @@ static inline int nblk(long n, int bs, int cap = 4096) {
 void launch_mask_build(const MaskArgs& a, int sites, hipStream_t st) {
     hipLaunchKernelGGL(k_mask_build, dim3(a.T, sites), dim3(256), 0, st, a);
 }
-
+template <typename T>
+void launch_transpose(const TransArgs& a, int N, hipStream_t st) {
+    hipLaunchKernelGGL(k_transpose<T>, dim3((a.K + 31) / 32, a.BP / 32, N), dim3(32, 8), 0, st, a);
+}
 template <typename T>
 void launch_fx(const FxArgs& a, hipStream_t st) {
-    hipLaunchKernelGGL(k_fx<T>, dim3((a.N + 63) / 64, (a.B + 31) / 32, a.T), dim3(256), 0, st, a);
+    hipLaunchKernelGGL(k_fx<T>, dim3((a.G + 63) / 64, (a.B + 63) / 64, a.T), dim3(256), 0, st, a);
 }
 template <typename T>
 void launch_step(const StepArgs& a, int D, hipStream_t st) {
-    hipLaunchKernelGGL(k_step<T>, dim3((a.H + 3) / 4, 1, D), dim3(256), 0, st, a);
+    if (a.H > 1024) {
+        hipLaunchKernelGGL((k_step<T, 2>), dim3((a.H + 7) / 8, (a.B + 31) / 32, D), dim3(1024), 0, st, a);
+    } else {
+        hipLaunchKernelGGL((k_step<T, 1>), dim3((a.H + 3) / 4, (a.B + 63) / 64, D), dim3(1024), 0, st, a);
+    }
 }
 template <typename T>
-void launch_bwd_pw(const BwdPwArgs& a, int D, hipStream_t st) {
-    hipLaunchKernelGGL(k_bwd_pw<T>, dim3((a.H + 15) / 16, 1, D), dim3(256), 0, st, a);
-}
-template <typename T>
-void launch_bwd_dh(const DhArgs& a, int D, int H, hipStream_t st) {
-    hipLaunchKernelGGL(k_bwd_dh<T>, dim3((H + 63) / 64, (a.B + 31) / 32, D), dim3(256), 0, st, a);
+void launch_bwd(const BwdArgs& a, int D, hipStream_t st) {
+    const int ndt = (a.H + 15) / 16;
+    const int nx = (a.has_next ? a.nkt : 0) + ndt;
+    hipLaunchKernelGGL(k_bwd<T>, dim3(nx, (a.B + 63) / 64, D), dim3(1024), 0, st, a);
 }
 template <typename T>
 void launch_dx(const DxArgs& a, int K, hipStream_t st) {
-    hipLaunchKernelGGL(k_dx<T>, dim3((K + 63) / 64, (a.B + 31) / 32, a.T), dim3(256), 0, st, a);
+    hipLaunchKernelGGL(k_dx<T>, dim3((K + 15) / 16, a.T, (a.B + 63) / 64), dim3(256), 0, st, a);
 }
 template <typename T>
-void launch_wgrad(const WgArgs& a, hipStream_t st) {
-    size_t lds = (size_t)a.K * 16 * sizeof(float);
-    hipLaunchKernelGGL(k_wgrad<T>, dim3((a.G + 15) / 16), dim3(256), lds, st, a);
+void launch_wgrad(const WgArgs& a, int ts, hipStream_t st) {
+    const size_t lds = (size_t)a.K * 16 * sizeof(float);
+    hipLaunchKernelGGL(k_wgrad<T>, dim3((a.G + 15) / 16, ts), dim3(512), lds, st, a);
+}
+void launch_wreduce(const float* part, float* dW, long n, int ts, hipStream_t st) {
+    hipLaunchKernelGGL(k_wreduce, dim3(nblk(n, 256, 8192)), dim3(256), 0, st, part, dW, n, ts);
 }
 template <typename T>
 void launch_fwd_init(const void* h0, const float* c0, float* hT, float* cT, long n, hipStream_t st) {
@@ -584,14 +731,11 @@ void launch_fwd_init(const void* h0, const float* c0, float* hT, float* cT, long
 void launch_bwd_init(const float* dhT, const float* dcT, float* dhc, float* dcs, long n, hipStream_t st) {
     hipLaunchKernelGGL(k_bwd_init, dim3(nblk(n, 256)), dim3(256), 0, st, dhT, dcT, dhc, dcs, n);
 }
-void launch_bwd_final(const FinalArgs& a, int D, hipStream_t st) {
-    hipLaunchKernelGGL(k_bwd_final, dim3(nblk((long)a.B * a.H, 256), D), dim3(256), 0, st, a);
-}
 void launch_expand(const float* dxc, int ldc, const SiteView& s, float* dx, int B, int K, int T, hipStream_t st) {
     hipLaunchKernelGGL(k_expand, dim3(nblk((long)T * B * K, 256)), dim3(256), 0, st, dxc, ldc, s, dx, B, K, T);
 }
-void launch_db(const float* dbpart, float* db, int G, int T, hipStream_t st) {
-    hipLaunchKernelGGL(k_db, dim3((G + 255) / 256), dim3(256), 0, st, dbpart, db, G, T);
+void launch_db(const float* dbpart, float* db, int G, int T, int ng, hipStream_t st) {
+    hipLaunchKernelGGL(k_db, dim3((G + 255) / 256), dim3(256), 0, st, dbpart, db, G, T, ng);
 }
 void launch_mse(const float* y, const float* tg, const int32_t* lengths, float* dy, float* partial, int np,
                 float* loss, int T, int B, int F, hipStream_t st) {
@@ -610,19 +754,15 @@ int setup_kernel_attributes() {
     return 0;
 }
 
-template void launch_fx<float>(const FxArgs&, hipStream_t);
-template void launch_fx<bf16>(const FxArgs&, hipStream_t);
-template void launch_step<float>(const StepArgs&, int, hipStream_t);
-template void launch_step<bf16>(const StepArgs&, int, hipStream_t);
-template void launch_bwd_pw<float>(const BwdPwArgs&, int, hipStream_t);
-template void launch_bwd_pw<bf16>(const BwdPwArgs&, int, hipStream_t);
-template void launch_bwd_dh<float>(const DhArgs&, int, int, hipStream_t);
-template void launch_bwd_dh<bf16>(const DhArgs&, int, int, hipStream_t);
-template void launch_dx<float>(const DxArgs&, int, hipStream_t);
-template void launch_dx<bf16>(const DxArgs&, int, hipStream_t);
-template void launch_wgrad<float>(const WgArgs&, hipStream_t);
-template void launch_wgrad<bf16>(const WgArgs&, hipStream_t);
-template void launch_fwd_init<float>(const void*, const float*, float*, float*, long, hipStream_t);
-template void launch_fwd_init<bf16>(const void*, const float*, float*, float*, long, hipStream_t);
+#define LSD_INST(T)                                                                         \
+    template void launch_transpose<T>(const TransArgs&, int, hipStream_t);                  \
+    template void launch_fx<T>(const FxArgs&, hipStream_t);                                 \
+    template void launch_step<T>(const StepArgs&, int, hipStream_t);                        \
+    template void launch_bwd<T>(const BwdArgs&, int, hipStream_t);                          \
+    template void launch_dx<T>(const DxArgs&, int, hipStream_t);                            \
+    template void launch_wgrad<T>(const WgArgs&, int, hipStream_t);                         \
+    template void launch_fwd_init<T>(const void*, const float*, float*, float*, long, hipStream_t);
+LSD_INST(float)
+LSD_INST(bf16)
 
 }  // namespace lsd

@@ -16,21 +16,25 @@ struct Plan {
     float s_nr, s_rh;     // 1/(1-p) computed in double, rounded to float
     int esize;            // bytes per element of x/W/U/h copies
     int G;                // 4H
+    int BP;               // batch rounded up to 32 (transposed copies)
+    int MGc;              // number of 64-row groups of the batch
     int sites, kmax, kin_max;
+    int ts;               // time splits of the weight-gradient kernel
 
     // mask buffer
-    size_t m_mask, m_keep, m_pos, m_count, m_total;
+    size_t m_mask, m_keep, m_pos, m_count, m_drop, m_dcount, m_total;
 
-    // reserve: per (l, d) block, then per-layer inter-layer outputs
-    size_t r_gates, r_c, r_hrec, r_dir_bytes;   // offsets inside one (l,d) block
-    size_t r_ybuf_base, r_ybuf_bytes;           // ybuf for layers 0..L-2
+    // reserve
+    size_t r_gates, r_c, r_hrecT, r_dir_bytes;  // inside one (l, d) block
+    size_t r_xT, r_h0T;                         // layer-0 input and h0, transposed
+    size_t r_ybuf_base, r_ybuf_bytes;           // per layer l < L-1: ybuf then ybufT
+    size_t r_ybufT_off;                         // offset of ybufT inside a layer block
     size_t r_total;
 
     // workspace
-    size_t w_gx;                                // forward: D x [T][B][4H] f32
-    size_t w_da, w_dbpart, w_dhrec, w_dc, w_dhc, w_dxc, w_bwd_end;
-    size_t w_loss;                              // last 16 KiB: loss partials
-    size_t w_total;
+    size_t w_gx, w_hrec;                        // forward
+    size_t w_da, w_daT, w_dbpart, w_dc, w_dhc, w_dxc, w_wpart;  // backward
+    size_t w_loss, w_total;
 
     int kin(int l) const { return l == 0 ? I : D * H; }
     int site_nr(int l) const { return l; }
@@ -41,15 +45,9 @@ struct Plan {
         int r = s - L, l = r / D, d = r % D;
         return 4 * l + 2 + d;
     }
-
-    // mask buffer accessors (byte offsets)
-    size_t mask_at(int s, int t) const { return m_mask + ((size_t)s * T + t) * kmax; }
-    size_t keep_at(int s, int t) const { return m_keep + ((size_t)s * T + t) * kmax * 4; }
-    size_t pos_at(int s, int t) const { return m_pos + ((size_t)s * T + t) * kmax * 4; }
-    size_t count_at(int s) const { return m_count + (size_t)s * T * 4; }
-
     size_t rdir(int l, int d) const { return (size_t)(l * D + d) * r_dir_bytes; }
     size_t rybuf(int l) const { return r_ybuf_base + (size_t)l * r_ybuf_bytes; }
+    size_t rybufT(int l) const { return rybuf(l) + r_ybufT_off; }
 };
 
 // Returns 0 and fills `p`, or a negative LSTM_SD_* code with a message.

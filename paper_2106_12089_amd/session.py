@@ -92,16 +92,19 @@ class Session:
 
     # -- host views (tests) -------------------------------------------------------
     def mask_views(self):
-        """Decode the mask buffer: (mask, keep, pos, count) numpy arrays with
-        shapes [sites][T][kmax] (x3) and [sites][T]."""
+        """Decode the mask buffer: (mask, keep, pos, count, drop, dcount) numpy
+        arrays with shapes [sites][T][kmax] or [sites][T]."""
         lay = B_.lstm_sd_mask_layout_get(self.dims)
         raw = self.mask_buf.cpu().numpy()
         S, T, K = lay.sites, lay.seq_len, lay.kmax
+        i32 = lambda off, n: raw[off:off + n * 4].view(np.int32)
         mask = raw[lay.mask_off:lay.mask_off + S * T * K].reshape(S, T, K)
-        keep = raw[lay.keep_off:lay.keep_off + S * T * K * 4].view(np.int32).reshape(S, T, K)
-        pos = raw[lay.pos_off:lay.pos_off + S * T * K * 4].view(np.int32).reshape(S, T, K)
-        count = raw[lay.count_off:lay.count_off + S * T * 4].view(np.int32).reshape(S, T)
-        return mask, keep, pos, count
+        keep = i32(lay.keep_off, S * T * K).reshape(S, T, K)
+        pos = i32(lay.pos_off, S * T * K).reshape(S, T, K)
+        count = i32(lay.count_off, S * T).reshape(S, T)
+        drop = i32(lay.drop_off, S * T * K).reshape(S, T, K)
+        dcount = i32(lay.dcount_off, S * T).reshape(S, T)
+        return mask, keep, pos, count, drop, dcount
 
     def write_masks(self, mask_u8: np.ndarray):
         """Overwrite the mask bytes ([sites][T][kmax]) and rebuild keep lists."""

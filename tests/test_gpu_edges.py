@@ -29,7 +29,7 @@ def run_both(cfg, wl, p_nr, p_rh, compact, forced=None, dhT=False):
                               cfg.hidden, p_nr, p_rh)
     if forced is not None:
         m_nr, m_rh = forced(m_nr, m_rh)
-        mask, _, _, _ = s.mask_views()
+        mask = s.mask_views()[0]
         mask = mask.copy()
         for i, m in enumerate(site_list(cfg, m_nr, m_rh)):
             mask[i, :, :m.shape[1]] = m

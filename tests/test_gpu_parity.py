@@ -30,7 +30,7 @@ def workload(name):
 
 
 def check_masks(sess, cfg, m_nr, m_rh, compact):
-    mask, keep, pos, count = sess.mask_views()
+    mask, keep, pos, count, drop, dcount = sess.mask_views()
     for s, ref in enumerate(site_list(cfg, m_nr, m_rh)):
         K = ref.shape[1]
         assert np.array_equal(mask[s, :, :K], ref), f"mask site {s}"
@@ -42,9 +42,13 @@ def check_masks(sess, cfg, m_nr, m_rh, compact):
                 p = np.full(K, -1)
                 p[kl] = np.arange(len(kl))
                 assert np.array_equal(pos[s, t, :K], p)
+                dl = np.nonzero(ref[t] == 0)[0]
+                assert dcount[s, t] == len(dl)
+                assert np.array_equal(drop[s, t, :len(dl)], dl)
             else:
                 assert count[s, t] == K
                 assert np.array_equal(keep[s, t, :K], np.arange(K))
+                assert dcount[s, t] == 0
 
 
 @pytest.mark.parametrize("mode", MODES)
