@@ -1,6 +1,6 @@
 """Benchmark of one structured-dropout LSTM training step on one MI355X.
 
-A step is one pass of the whole path on one batch of synthetic input that
+A step is one pass of the whole path over one batch of synthetic input that
 is already resident in HBM: draw the Case-III masks and build the keep lists
 (fresh masks every step), forward unroll, MSE loss gradient, BPTT with the
 weight gradients.  The workload is the 2-layer, 650-unit language-model
@@ -8,12 +8,17 @@ shape (batch 20, 35 steps, bf16 storage with fp32 accumulation, structured
 dropout p = 0.5 on the non-recurrent inputs).  Prints one JSON line.
 
   value      effective TFLOP/s: algorithmic FLOPs of the step (products over
-             the actually kept rows, 3 products per gate GEMM) / step time
-  speedup    same kernels run dense (compact = 0) / method
+             the rows actually kept, three products per gate GEMM) / step time
+  speedup    the same kernels run dense (compact = 0) / the method
+  roofline   the kernel with the largest share of the step, its algorithmic
+             bytes (or FLOPs) per launch over its average launch duration,
+             measured with HIP events on its own stream in a second timed
+             pass of the same workload
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -26,86 +31,184 @@ sys.path.insert(0, ROOT)
 
 WORKLOAD = "lm_medium"
 METRIC = "LSTM fwd+BPTT step time & eff. TFLOP/s; speedup vs dense at p=0.5"
+PEAK_HBM_GBS = 8000.0
+PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+KERNELS = ("step", "bwd", "wgrad", "fx", "dx")
+KERNEL_SRC = os.path.join(ROOT, "paper_2106_12089_amd", "csrc", "kernels.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
+
+def kernel_src_hash():
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+# ---------------------------------------------------------------------------
+# Work accounting from the kept counts (counts: [sites][T]; sites = NR of
+# each layer, then RH of each (layer, direction)).
 
 def algorithmic_flops(counts, cfg, lengths=None):
     """Sum over layers, directions and t of 3 * 2 * B_t * 4H * (n_x + n_h):
     the forward product, the input-gradient product and the weight-gradient
     product of every gate GEMM, over kept rows only (B_t = valid rows)."""
     L, D, H, T, B = cfg.num_layers, cfg.num_dirs, cfg.hidden, cfg.seq_len, cfg.batch
-    if lengths is None:
-        bt = np.full(T, B)
-    else:
-        bt = (np.arange(T)[:, None] < np.asarray(lengths)[None, :]).sum(1)
+    bt = np.full(T, B) if lengths is None else \
+        (np.arange(T)[:, None] < np.asarray(lengths)[None, :]).sum(1)
     tot = 0.0
     for l in range(L):
         for d in range(D):
-            nx = counts[l]
-            nh = counts[L + l * D + d]
+            nx, nh = np.asarray(counts[l]), np.asarray(counts[L + l * D + d])
             tot += float(np.sum(3 * 2 * bt * 4 * H * (nx + nh)))
     return tot
 
 
-def dense_flops(cfg, lengths=None):
-    L, D, H, T, B, I = cfg.num_layers, cfg.num_dirs, cfg.hidden, cfg.seq_len, cfg.batch, cfg.input_dim
-    counts = []
-    for l in range(L):
-        counts.append(np.full(T, I if l == 0 else D * H))
-    for _ in range(L * D):
-        counts.append(np.full(T, H))
-    return algorithmic_flops(counts, cfg, lengths)
+def dense_counts(cfg):
+    L, D, H, T, I = cfg.num_layers, cfg.num_dirs, cfg.hidden, cfg.seq_len, cfg.input_dim
+    return [np.full(T, I if l == 0 else D * H) for l in range(L)] + [np.full(T, H)] * (L * D)
 
 
-def time_mode(wl, p_nr, p_rh, compact, steps, warmup, seed0):
+def kernel_work(kind, counts, cfg):
+    """(flops, bytes, launches) of one step for a kernel class; bytes are the
+    algorithmic minimum: every operand read once and every output written
+    once per launch (kept rows only)."""
+    L, D, H, T, B = cfg.num_layers, cfg.num_dirs, cfg.hidden, cfg.seq_len, cfg.batch
+    G = 4 * H
+    e = 2 if cfg.dtype == "bf16" else 4
+    fl = by = 0.0
+    if kind == "step":                      # one launch per (layer, step), directions fused
+        for l in range(L):
+            for d in range(D):
+                nh = np.asarray(counts[L + l * D + d], dtype=np.float64)
+                fl += float(np.sum(2 * B * G * nh))
+                by += float(np.sum(nh * G * e + B * nh * e))           # kept U rows, kept h columns
+                by += T * B * (G * 4 + H * 8 + G * 4 + H * 4 + 2 * H * e + H * 8)
+                by += T * B * H * (4 if l == L - 1 else 4 * e)
+        return fl, by, L * T
+    if kind == "bwd":                       # T pointwise steps + one final pass per layer
+        for l in range(L):
+            for d in range(D):
+                nh = np.asarray(counts[L + l * D + d], dtype=np.float64)
+                fl += float(np.sum(2 * B * G * nh))
+                by += float(np.sum(nh * G * e + B * G * e))            # kept U rows, DA of that step
+                by += T * B * H * (16 + 4 + 4 + 8 + 8 + 4 + 8 * e)
+        return fl, by, L * (T + 1)
+    if kind == "wgrad":                     # dW and dU of every (layer, direction)
+        for l in range(L):
+            kin = cfg.input_dim if l == 0 else D * H
+            for d in range(D):
+                for n, K in ((np.asarray(counts[l], np.float64), kin),
+                             (np.asarray(counts[L + l * D + d], np.float64), H)):
+                    fl += float(np.sum(2 * n * B * G))
+                    by += float(np.sum(n * B * e + G * B * e)) + K * G * 4
+        return fl, by, 2 * L * D
+    if kind == "fx":
+        for l in range(L):
+            kin = cfg.input_dim if l == 0 else D * H
+            n = np.asarray(counts[l], np.float64)
+            for d in range(D):
+                fl += float(np.sum(2 * B * G * n))
+                by += kin * G * e + float(np.sum(B * n * e)) + T * B * G * 4
+        return fl, by, L * D
+    if kind == "dx":
+        for l in range(L):
+            kin = cfg.input_dim if l == 0 else D * H
+            n = np.asarray(counts[l], np.float64)
+            fl += float(np.sum(2 * B * G * n)) * D
+            by += D * (kin * G * e + T * B * G * e) + float(np.sum(B * n * 4))
+        return fl, by, L
+    raise ValueError(kind)
+
+
+# ---------------------------------------------------------------------------
+
+def run_mode(wl, p_nr, p_rh, compact, steps, warmup, timed_kernels=()):
     import torch
+    from paper_2106_12089_amd import binding as B_
     from paper_2106_12089_amd.session import Session
-    s = Session(wl, p_nr, p_rh, compact)
     cfg = wl.cfg
+    s = Session(wl, p_nr, p_rh, compact)
     for i in range(warmup):
         s.step(cfg.mask_seed, 10_000 + i)
     torch.cuda.synchronize()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
-    phase = np.zeros(4)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
     t0 = time.perf_counter()
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start.record()
     for i in range(steps):
-        ev[0].record()
-        s.masks(cfg.mask_seed, seed0 + i)
-        ev[1].record()
+        e = ev[i]
+        e[0].record()
+        s.masks(cfg.mask_seed, i)
+        e[1].record()
         s.forward()
-        ev[2].record()
+        e[2].record()
         s.loss_grad()
-        ev[3].record()
+        e[3].record()
         s.backward()
-        ev[4].record()
-        if i == steps - 1:
-            break
-    end.record()
+        e[4].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    total_ms = start.elapsed_time(end)
-    for k in range(4):
-        phase[k] = ev[k].elapsed_time(ev[k + 1])   # last step's phases
-    # kept counts of every timed step (regenerated; outside the timed region)
-    flops = 0.0
-    lay = None
-    from paper_2106_12089_amd import binding as B_
-    lay = B_.lstm_sd_mask_layout_get(s.dims)
+    total_ms = ev[0][0].elapsed_time(ev[-1][4])
+    phases = np.zeros(4)
+    for e in ev:
+        for k in range(4):
+            phases[k] += e[k].elapsed_time(e[k + 1])
+    phases /= steps
+    # kept counts of every timed step (masks regenerated outside the timed region)
+    counts_all = []
     for i in range(steps):
-        s.masks(cfg.mask_seed, seed0 + i)
-        count = s.mask_views()[3]
-        flops += algorithmic_flops(count, cfg, wl.lengths)
-    return dict(ms=total_ms / steps, wall_ms=wall * 1e3 / steps, flops=flops / steps,
-                phases_last_ms=dict(mask=phase[0], forward=phase[1], loss=phase[2], backward=phase[3]),
-                session=s)
+        s.masks(cfg.mask_seed, i)
+        counts_all.append(s.mask_views()[3].astype(np.float64))
+    counts = np.mean(counts_all, axis=0)
+    # per-kernel timing: a second timed pass per kernel class, events on the launch stream
+    ktime = {}
+    for kname in timed_kernels:
+        B_.lstm_sd_kernel_timer_start(kname)
+        for i in range(steps):
+            s.step(cfg.mask_seed, i)
+        ms, n = B_.lstm_sd_kernel_timer_stop()
+        torch.cuda.synchronize()
+        ktime[kname] = dict(total_ms=ms / steps, launches=n / steps, avg_us=1e3 * ms / max(n, 1))
+    return dict(ms=total_ms / steps, wall_ms=wall * 1e3 / steps, counts=counts,
+                flops=float(np.mean([algorithmic_flops(c, cfg, wl.lengths) for c in counts_all])),
+                phases=dict(mask=phases[0], forward=phases[1], loss=phases[2], backward=phases[3]),
+                ktime=ktime)
+
+
+def roofline(res, cfg):
+    kt = res["ktime"]
+    name = max(kt, key=lambda k: kt[k]["total_ms"])
+    fl, by, nl = kernel_work(name, res["counts"], cfg)
+    launches = kt[name]["launches"]
+    fl_l, by_l = fl / launches, by / launches
+    dur = kt[name]["avg_us"] * 1e-6
+    peak_f = PEAK_TFLOPS["bf16" if cfg.dtype == "bf16" else "f32"]
+    ai = fl_l / by_l
+    ridge = peak_f * 1e12 / (PEAK_HBM_GBS * 1e9)
+    traffic = None
+    try:
+        with open(TRAFFIC_FILE) as f:
+            tr = json.load(f)
+        ent = tr.get(name)
+        if ent and ent.get("src_hash") == kernel_src_hash() and ent.get("workload") == cfg.name:
+            traffic = ent["bytes_per_launch"]
+    except (OSError, ValueError):
+        pass
+    if ai < ridge:
+        out = dict(bound="hbm", achieved=by_l / dur / 1e9, peak=PEAK_HBM_GBS, unit="GB/s")
+    else:
+        out = dict(bound="mfma", achieved=fl_l / dur / 1e12, peak=peak_f, unit="TFLOP/s")
+    out["frac"] = out["achieved"] / out["peak"]
+    out["traffic"] = traffic
+    out.update(kernel=name, launch_avg_us=kt[name]["avg_us"], launches_per_step=launches,
+               algorithmic_bytes_per_launch=by_l, algorithmic_flops_per_launch=fl_l,
+               share_of_step=kt[name]["total_ms"] / res["ms"],
+               kernels_ms_per_step={k: round(v["total_ms"], 4) for k, v in kt.items()})
+    for k in ("achieved", "frac"):
+        out[k] = round(out[k], 5)
+    return out
 
 
 def cpu_baseline(wl, p_nr, p_rh, budget_s=12.0):
-    """The float64 oracle (untuned), timed on the host on whole steps of the
-    same workload until about budget_s seconds of CPU work are done."""
+    """The float64 oracle as it stands, timed on the host on whole training
+    steps of the same workload until about budget_s seconds of CPU work."""
     from oracle import lstm, masks
     cfg = wl.cfg
     try:
@@ -125,10 +228,54 @@ def cpu_baseline(wl, p_nr, p_rh, budget_s=12.0):
                                               for d in range(cfg.num_dirs)]
         flops += algorithmic_flops(counts, cfg, wl.lengths)
         n += 1
-    return dict(value=flops / t_tot / 1e12, unit="TFLOP/s", cores=int(threads), kind="oracle",
-                sample=f"{n} whole training steps of the {cfg.name} workload (float64 NumPy oracle, "
-                       f"{t_tot / n * 1e3:.0f} ms/step)",
-                ms_per_step=t_tot / n * 1e3)
+    return dict(value=round(flops / t_tot / 1e12, 6), unit="TFLOP/s", cores=int(threads), kind="oracle",
+                sample=f"{n} whole training steps of the {cfg.name} workload (NR+ST, masks of steps "
+                       f"0..{n - 1}), float64 NumPy oracle, {t_tot / n * 1e3:.0f} ms/step",
+                ms_per_step=round(t_tot / n * 1e3, 3))
+
+
+KERNEL_SYMBOLS = {"step": "lsd::k_step<", "bwd": "lsd::k_bwd<", "wgrad": "lsd::k_wgrad<",
+                  "fx": "lsd::k_fx<", "dx": "lsd::k_dx<"}
+
+
+def summarize_counters(fetch_csv, write_csv, copy_bytes, workload, command):
+    """Turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE; KiB per
+    dispatch) into HBM bytes per launch of each kernel class.  Each counter is
+    scaled by what it reads for a plain device copy of copy_bytes bytes (the
+    largest copy dispatch in the same run).  Writes profiles/traffic.json."""
+    import csv
+    import collections
+
+    def per_kernel(path):
+        agg = collections.defaultdict(list)
+        copy = 0.0
+        for r in csv.DictReader(open(path)):
+            v = float(r["Counter_Value"])
+            name = r["Kernel_Name"]
+            if "copyBuffer" in name or "copy_kernel" in name:
+                copy = max(copy, v)
+            for k, sym in KERNEL_SYMBOLS.items():
+                if sym in name:
+                    agg[k].append(v)
+        return agg, copy
+
+    fetch, fcopy = per_kernel(fetch_csv)
+    write, wcopy = per_kernel(write_csv)
+    ffac = copy_bytes / (fcopy * 1024.0)
+    wfac = copy_bytes / (wcopy * 1024.0)
+    out = {"_calibration": {"copy_bytes": copy_bytes, "fetch_kib_of_copy": fcopy, "write_kib_of_copy": wcopy,
+                            "fetch_factor": ffac, "write_factor": wfac, "command": command}}
+    for k in KERNEL_SYMBOLS:
+        if k in fetch and k in write:
+            f = float(np.mean(fetch[k])) * 1024.0 * ffac
+            w = float(np.mean(write[k])) * 1024.0 * wfac
+            out[k] = {"workload": workload, "src_hash": kernel_src_hash(), "fetch_kib": float(np.mean(fetch[k])),
+                      "write_kib": float(np.mean(write[k])), "bytes_per_launch": f + w,
+                      "fetch_bytes": f, "write_bytes": w, "dispatches": len(fetch[k])}
+    os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
+    with open(TRAFFIC_FILE, "w") as fo:
+        json.dump(out, fo, indent=1)
+    return out
 
 
 def main(argv=None):
@@ -138,11 +285,21 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=WORKLOAD)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
-    ap.add_argument("--all-modes", action="store_true", help="also time NR+RH+ST and its dense run")
+    ap.add_argument("--no-nrrh", action="store_true", help="skip the NR+RH+ST runs")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="also run a plain device copy of this many MiB (counter calibration)")
+    ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write profiles/traffic.json from two rocprofv3 --pmc runs and exit (no GPU)")
+    ap.add_argument("--counter-command", default="", help="command recorded with --summarize-counters")
     args = ap.parse_args(argv)
+    if args.summarize_counters:
+        out = summarize_counters(*args.summarize_counters, copy_bytes=args.calibrate_copy * (1 << 20),
+                                 workload=args.workload, command=args.counter_command)
+        print(json.dumps(out, indent=1))
+        return 0
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the multi-GPU "
-              "data-parallel path is not part of this build.", file=sys.stderr)
+        print(f"bench.py runs on one GPU (asked for --gpus {args.gpus}): this build has no "
+              "multi-GPU path; the data-parallel design is described but not built.", file=sys.stderr)
         return 2
     import torch
     import workloads
@@ -151,18 +308,13 @@ def main(argv=None):
         return 1
     cfg = workloads.get_config(args.workload)
     wl = workloads.make_workload(cfg)
-    p = cfg.p_values[0] if 0.5 not in cfg.p_values else 0.5
-    res = {}
-    modes = [("nr", p, 0.0)] + ([("nrrh", p, p)] if args.all_modes else [])
-    for name, pn, pr in modes:
-        res[name] = time_mode(wl, pn, pr, 1, args.steps, args.warmup, 0)
-        res[name + "_dense"] = time_mode(wl, pn, pr, 0, args.steps, args.warmup, 0)
-    head = res["nr"]
-    dense = res["nr_dense"]
+    p = 0.5 if 0.5 in cfg.p_values else cfg.p_values[0]
+    head = run_mode(wl, p, 0.0, 1, args.steps, args.warmup, timed_kernels=KERNELS)
+    dense = run_mode(wl, p, 0.0, 0, args.steps, args.warmup)
     out = {
         "metric": METRIC,
         "value": round(head["flops"] / (head["ms"] * 1e-3) / 1e12, 4),
-        "unit": "TFLOP/s (effective, kept-row FLOPs)",
+        "unit": "TFLOP/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(head["ms"], 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
@@ -170,17 +322,31 @@ def main(argv=None):
         "config": {"workload": cfg.name, "layers": cfg.num_layers, "dirs": cfg.num_dirs,
                    "input_dim": cfg.input_dim, "hidden": cfg.hidden, "batch": cfg.batch,
                    "seq_len": cfg.seq_len, "p_nr": p, "p_rh": 0.0, "mode": "NR+ST"},
+        "value_kind": "effective TFLOP/s over kept-row FLOPs",
         "speedup_vs_dense": round(dense["ms"] / head["ms"], 4),
         "dense_ms_per_step": round(dense["ms"], 4),
         "gflop_per_step": round(head["flops"] / 1e9, 4),
-        "dense_equiv_tflops": round(dense_flops(cfg, wl.lengths) / (head["ms"] * 1e-3) / 1e12, 4),
-        "phases_ms": {k: round(v, 4) for k, v in head["phases_last_ms"].items()},
+        "dense_equiv_tflops": round(algorithmic_flops(dense_counts(cfg), cfg, wl.lengths)
+                                    / (head["ms"] * 1e-3) / 1e12, 4),
+        "phases_ms": {k: round(v, 4) for k, v in head["phases"].items()},
+        "phases_ms_dense": {k: round(v, 4) for k, v in dense["phases"].items()},
+        "roofline": roofline(head, cfg),
     }
-    if args.all_modes:
-        r, rd = res["nrrh"], res["nrrh_dense"]
+    if not args.no_nrrh:
+        r = run_mode(wl, p, p, 1, args.steps, args.warmup)
+        rd = run_mode(wl, p, p, 0, args.steps, args.warmup)
         out["nrrh"] = {"ms_per_step": round(r["ms"], 4), "dense_ms_per_step": round(rd["ms"], 4),
                        "speedup_vs_dense": round(rd["ms"] / r["ms"], 4),
-                       "tflops": round(r["flops"] / (r["ms"] * 1e-3) / 1e12, 4)}
+                       "tflops": round(r["flops"] / (r["ms"] * 1e-3) / 1e12, 4),
+                       "phases_ms": {k: round(v, 4) for k, v in r["phases"].items()}}
+    if args.calibrate_copy:
+        n = args.calibrate_copy * (1 << 20) // 4
+        a = torch.ones(n, dtype=torch.float32, device="cuda")
+        b = torch.empty_like(a)
+        torch.cuda.synchronize()
+        b.copy_(a)
+        torch.cuda.synchronize()
+        out["calibration_copy_bytes"] = n * 4
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(wl, p, 0.0)
     print(json.dumps(out), flush=True)

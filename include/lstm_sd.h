@@ -111,13 +111,18 @@ typedef struct {
  *   count int32 [sites][T]        number of listed entries
  *   drop  int32 [sites][T][kmax]  ascending dropped indices (compact = 1);
  *                                 empty when compact = 0
- *   dcount int32 [sites][T]       number of entries of drop */
+ *   dcount int32 [sites][T]       number of entries of drop
+ *   kseg  int32 [sites][T][9]     kseg[x] = number of kept neurons below
+ *                                 floor(x*K(s)/8), x = 0..8: the keep list
+ *                                 split into 8 slices of neuron indices
+ *   dseg  int32 [sites][T][9]     the same for the drop list */
 typedef struct {
     int32_t sites;
     int32_t kmax;
     int32_t seq_len;
     int32_t reserved;
-    size_t mask_off, keep_off, pos_off, count_off, drop_off, dcount_off, total_bytes;
+    size_t mask_off, keep_off, pos_off, count_off, drop_off, dcount_off, kseg_off, dseg_off,
+        total_bytes;
 } lstm_sd_mask_layout;
 
 int         lstm_sd_version(void);
@@ -191,6 +196,18 @@ int lstm_sd_backward(const lstm_sd_dims* dims, const lstm_sd_weights* w,
 int lstm_sd_mse_grad(const lstm_sd_dims* dims, const float* y, const float* target,
                      const int32_t* lengths, float* dy, float* loss,
                      void* workspace, size_t workspace_bytes, void* stream);
+
+/* Instrumentation for measuring one kernel's average duration on the
+ * stream it runs on.  After lstm_sd_kernel_timer_start(name), every launch
+ * of the named kernel made by this library is bracketed by a pair of HIP
+ * events recorded on its launch stream; lstm_sd_kernel_timer_stop()
+ * waits for the last pair, returns the summed elapsed time in milliseconds
+ * and the number of launches, and turns the timer off.  Names:
+ * "mask_build", "transpose", "fx", "step", "bwd", "dx", "wgrad".  Events
+ * are created by the library (no device memory is allocated).  Not
+ * thread-safe; for benchmarks. */
+int lstm_sd_kernel_timer_start(const char* kernel);
+int lstm_sd_kernel_timer_stop(double* total_ms, int64_t* launches);
 
 #ifdef __cplusplus
 }

@@ -43,7 +43,8 @@ class lstm_sd_mask_layout(ctypes.Structure):
                 ("reserved", ctypes.c_int32), ("mask_off", ctypes.c_size_t),
                 ("keep_off", ctypes.c_size_t), ("pos_off", ctypes.c_size_t),
                 ("count_off", ctypes.c_size_t), ("drop_off", ctypes.c_size_t),
-                ("dcount_off", ctypes.c_size_t), ("total_bytes", ctypes.c_size_t)]
+                ("dcount_off", ctypes.c_size_t), ("kseg_off", ctypes.c_size_t),
+                ("dseg_off", ctypes.c_size_t), ("total_bytes", ctypes.c_size_t)]
 
 
 _P = ctypes.c_void_p
@@ -66,6 +67,8 @@ SIGNATURES = {
                                         _P, _SZ, _P, _P, _P, _P, _P, _P, ctypes.POINTER(lstm_sd_grads),
                                         _P, _SZ, _P]),
     "lstm_sd_mse_grad": (ctypes.c_int, [_DIMS, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "lstm_sd_kernel_timer_start": (ctypes.c_int, [ctypes.c_char_p]),
+    "lstm_sd_kernel_timer_stop": (ctypes.c_int, [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]),
 }
 
 _lib = None
@@ -203,3 +206,15 @@ def lstm_sd_backward(dims, W, U, b, x, lengths, h0, c0, mask_buf, reserve, dy, d
 def lstm_sd_mse_grad(dims, y, target, lengths, dy, loss, workspace, stream=None):
     _check(load().lstm_sd_mse_grad(ctypes.byref(dims), _ptr(y), _ptr(target), _ptr(lengths), _ptr(dy),
                                    _ptr(loss), _ptr(workspace), _nbytes(workspace), _stream(stream)))
+
+
+def lstm_sd_kernel_timer_start(kernel: str):
+    _check(load().lstm_sd_kernel_timer_start(kernel.encode()))
+
+
+def lstm_sd_kernel_timer_stop():
+    """Returns (total milliseconds, number of launches)."""
+    ms = ctypes.c_double(0.0)
+    n = ctypes.c_int64(0)
+    _check(load().lstm_sd_kernel_timer_stop(ctypes.byref(ms), ctypes.byref(n)))
+    return ms.value, n.value

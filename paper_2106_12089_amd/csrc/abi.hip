@@ -30,6 +30,8 @@ void launch_db(const float*, float*, int, int, int, hipStream_t);
 void launch_mse(const float*, const float*, const int32_t*, float*, float*, int, float*, int, int, int,
                 hipStream_t);
 int setup_kernel_attributes();
+int kernel_timer_start(const char* name);
+int kernel_timer_stop(double* total_ms, int64_t* launches);
 
 static thread_local std::string g_err;
 
@@ -92,6 +94,8 @@ int make_plan(const lstm_sd_dims* d, Plan* p, const char** why) {
     q.m_count = off;  off = align_up(off + S * T * 4, A);
     q.m_drop = off;   off = align_up(off + S * T * KM * 4, A);
     q.m_dcount = off; off = align_up(off + S * T * 4, A);
+    q.m_kseg = off;   off = align_up(off + S * T * 9 * 4, A);
+    q.m_dseg = off;   off = align_up(off + S * T * 9 * 4, A);
     q.m_total = off;
 
     off = 0;
@@ -141,6 +145,8 @@ static SiteView site_view(const Plan& P, const void* mbuf, int s) {
     v.count = (const int32_t*)(m + P.m_count) + (size_t)s * P.T;
     v.drop = (const int32_t*)(m + P.m_drop) + row;
     v.dcount = (const int32_t*)(m + P.m_dcount) + (size_t)s * P.T;
+    v.kseg = (const int32_t*)(m + P.m_kseg) + (size_t)s * P.T * 9;
+    v.dseg = (const int32_t*)(m + P.m_dseg) + (size_t)s * P.T * 9;
     v.kmax = P.kmax;
     return v;
 }
@@ -173,6 +179,8 @@ static int do_masks(const lstm_sd_dims* dims, uint64_t seed, uint64_t step, void
     a.count = (int32_t*)(m + P.m_count);
     a.drop = (int32_t*)(m + P.m_drop);
     a.dcount = (int32_t*)(m + P.m_dcount);
+    a.kseg = (int32_t*)(m + P.m_kseg);
+    a.dseg = (int32_t*)(m + P.m_dseg);
     a.T = P.T; a.kmax = P.kmax; a.compact = P.compact; a.generate = generate;
     a.seed = seed; a.step = step;
     for (int s = 0; s < P.sites; ++s) {
@@ -260,7 +268,7 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
     const size_t es = P.esize;
     const char* R = (const char*)reserve;
     char* W = (char*)ws;
-    const int nkt = (H + 15) / 16;
+    const int tps_h = ((H + 7) / 8 + 15) / 16;     // 16-unit tiles per XCD slice of the hidden units
     for (int l = L - 1; l >= 0; --l) {
         const int kin = P.kin(l);
         float* dhc = (float*)(W + P.w_dhc);
@@ -276,7 +284,7 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
             memset(&a, 0, sizeof(a));
             a.lengths = lengths; a.B = B; a.H = H; a.BP = BP; a.ldy = D * H;
             a.lddx = l + 1 < L ? P.kin(l + 1) : 0;
-            a.nkt = nkt; a.has_next = s > 0; a.final_pass = final_pass; a.dense = !P.compact; a.s = P.s_rh;
+            a.tps = tps_h; a.has_next = s > 0; a.final_pass = final_pass; a.dense = !P.compact; a.s = P.s_rh;
             for (int d = 0; d < D; ++d) {
                 const int k = l * D + d;
                 const int t = final_pass ? -1 : (d == 0 ? T - 1 - s : s);   // BP order: reverse of FP
@@ -296,6 +304,8 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
                     bd.ncount = rv.count + tn;
                     bd.ndrop = rv.drop + (size_t)tn * P.kmax;
                     bd.ndcount = rv.dcount + tn;
+                    bd.nkseg = rv.kseg + (size_t)tn * 9;
+                    bd.ndseg = rv.dseg + (size_t)tn * 9;
                 }
                 if (final_pass) {
                     bd.dh0 = dh0 + (size_t)k * B * H;
@@ -327,6 +337,7 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
                 a.W[d] = w->W[l * D + d];
             }
             a.site = nv; a.out = dxc_here; a.D = D; a.B = B; a.G = G; a.ldo = kin; a.T = T;
+            a.K = kin; a.tps = ((kin + 7) / 8 + 15) / 16;
             a.dense = !P.compact; a.s = P.s_nr;
             launch_dx<E>(a, kin, st);
             if (l == 0) launch_expand(dxc_here, kin, nv, dx, B, kin, T, st);
@@ -403,6 +414,7 @@ int lstm_sd_mask_layout_get(const lstm_sd_dims* dims, lstm_sd_mask_layout* out) 
     out->sites = P.sites; out->kmax = P.kmax; out->seq_len = P.T; out->reserved = 0;
     out->mask_off = P.m_mask; out->keep_off = P.m_keep; out->pos_off = P.m_pos;
     out->count_off = P.m_count; out->drop_off = P.m_drop; out->dcount_off = P.m_dcount;
+    out->kseg_off = P.m_kseg; out->dseg_off = P.m_dseg;
     out->total_bytes = P.m_total;
     return LSTM_SD_OK;
 }
@@ -476,6 +488,16 @@ int lstm_sd_mse_grad(const lstm_sd_dims* dims, const float* y, const float* targ
     float* partial = (float*)((char*)workspace + P.w_loss);
     launch_mse(y, target, lengths, dy, partial, 1024, loss, P.T, P.B, P.D * P.H, (hipStream_t)stream);
     return hip_check("mse launch");
+}
+
+int lstm_sd_kernel_timer_start(const char* kernel) {
+    if (kernel_timer_start(kernel)) return fail(LSTM_SD_EINVAL, std::string("unknown kernel name: ") + (kernel ? kernel : "(null)"));
+    return LSTM_SD_OK;
+}
+
+int lstm_sd_kernel_timer_stop(double* total_ms, int64_t* launches) {
+    if (kernel_timer_stop(total_ms, launches)) return fail(LSTM_SD_EHIP, "kernel timer: HIP event error");
+    return LSTM_SD_OK;
 }
 
 }  // extern "C"

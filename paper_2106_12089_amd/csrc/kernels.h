@@ -15,6 +15,8 @@ struct MaskArgs {
     int32_t* count;
     int32_t* drop;
     int32_t* dcount;
+    int32_t* kseg;
+    int32_t* dseg;
     int T, kmax, compact, generate;
     uint64_t seed, step;
     int K[MAX_SITES];
@@ -31,6 +33,8 @@ struct SiteView {
     const int32_t* count;
     const int32_t* drop;
     const int32_t* dcount;
+    const int32_t* kseg;                // [T][9]
+    const int32_t* dseg;                // [T][9]
     int kmax;
 };
 
@@ -90,6 +94,8 @@ struct BwdDir {
     const int32_t* ncount;
     const int32_t* ndrop;               // dropped units of that step
     const int32_t* ndcount;
+    const int32_t* nkseg;               // [9] slice offsets of nkeep
+    const int32_t* ndseg;               // [9] slice offsets of ndrop
     const void* U;                      // [H][G]
     // pointwise at t
     const float* gates;                 // [B][G]
@@ -110,7 +116,7 @@ struct BwdDir {
 struct BwdArgs {
     BwdDir d[2];
     const int32_t* lengths;
-    int B, H, BP, ldy, lddx, nkt, has_next, final_pass, dense;
+    int B, H, BP, ldy, lddx, tps, has_next, final_pass, dense;   // tps: tiles per XCD slice
     float s;
 };
 
@@ -121,7 +127,7 @@ struct DxArgs {
     const void* W[2];                   // [K][G]
     SiteView site;
     float* out;                         // [T][B][ldo]
-    int D, B, G, ldo, T, dense;
+    int D, B, G, ldo, T, K, tps, dense;
     float s;
 };
 

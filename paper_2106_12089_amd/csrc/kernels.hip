@@ -11,6 +11,11 @@
 //   transposed activations [K][BP]      weight gradients (contiguous in b)
 //   DA [B][G] and DA^T [G][BP]          backward products / weight gradients
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
+
+#include <string.h>
+
+#include <vector>
 
 #include "device.h"
 #include "kernels.h"
@@ -34,6 +39,20 @@ __device__ __forceinline__ void zero4(T* o) {
     o[0] = o[1] = o[2] = o[3] = zero_val<T>();
 }
 
+// Workgroups are dealt to the 8 XCDs round-robin (linear workgroup id i runs
+// on XCD i % 8).  xcd_tile maps the x index of a grid whose x size is a
+// multiple of 8 to a logical tile so that every XCD owns one contiguous range
+// of tiles (and its L2 keeps the matching slice of the weights); -1 = idle.
+constexpr int NXCD = 8;
+__device__ __forceinline__ int xcd_tile(int bx, int ntiles) {
+    const int per = (ntiles + NXCD - 1) / NXCD;
+    const int x = bx % NXCD, i = bx / NXCD;
+    const int tile = x * per + i;
+    return (i < per && tile < ntiles) ? tile : -1;
+}
+// First neuron of slice x of a K-neuron site (slices of floor(x*K/8)).
+__device__ __forceinline__ int slice_start(int x, int K) { return (x * K) / NXCD; }
+
 // ---------------------------------------------------------------------------
 // Masks (Sec. 3.1, Case-III) and their compaction into keep/drop lists.
 // grid (T, sites), block 256.
@@ -47,6 +66,8 @@ __global__ void __launch_bounds__(256) k_mask_build(MaskArgs a) {
     int32_t* krow = a.keep + row;
     int32_t* prow = a.pos + row;
     int32_t* drow = a.drop + row;
+    int32_t* ksrow = a.kseg + ((size_t)s * a.T + t) * (NXCD + 1);
+    int32_t* dsrow = a.dseg + ((size_t)s * a.T + t) * (NXCD + 1);
     if (a.generate) {
         const uint64_t thr = a.thr[s];
         for (int q = tid; q < (K + 3) / 4; q += blockDim.x) {
@@ -72,6 +93,10 @@ __global__ void __launch_bounds__(256) k_mask_build(MaskArgs a) {
     __syncthreads();
     if (!a.compact) {
         for (int k = tid; k < K; k += blockDim.x) { krow[k] = k; prow[k] = k; }
+        if (tid <= NXCD) {
+            ksrow[tid] = slice_start(tid, K);
+            dsrow[tid] = 0;
+        }
         if (tid == 0) {
             a.count[(size_t)s * a.T + t] = K;
             a.dcount[(size_t)s * a.T + t] = 0;
@@ -97,6 +122,8 @@ __global__ void __launch_bounds__(256) k_mask_build(MaskArgs a) {
         if (k < K) {
             if (f) { krow[off + pre] = k; prow[k] = off + pre; }
             else { drow[doff + dpre] = k; prow[k] = -1; }
+            for (int x = 0; x < NXCD; ++x)
+                if (k == slice_start(x, K)) { ksrow[x] = off + pre; dsrow[x] = doff + dpre; }
         }
         base += tot;
         dbase += dtot;
@@ -105,6 +132,8 @@ __global__ void __launch_bounds__(256) k_mask_build(MaskArgs a) {
     if (tid == 0) {
         a.count[(size_t)s * a.T + t] = base;
         a.dcount[(size_t)s * a.T + t] = dbase;
+        ksrow[NXCD] = base;
+        dsrow[NXCD] = dbase;
     }
 }
 
@@ -137,10 +166,12 @@ __global__ void __launch_bounds__(256) k_transpose(TransArgs a) {
 template <typename T>
 __global__ void __launch_bounds__(256) k_fx(FxArgs a) {
     __shared__ int kidx[LSTM_SD_MAX_K];
+    const int ctile = xcd_tile(blockIdx.x, (a.G + 63) / 64);
+    if (ctile < 0) return;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int t = blockIdx.z;
     const int m0 = blockIdx.y * 64;
-    const int n = blockIdx.x * 64 + w * 16 + (lane & 15);
+    const int n = ctile * 64 + w * 16 + (lane & 15);
     const bool nok = n < a.G;
     const int g8 = 8 * (lane >> 4);
     const T* X = (const T*)a.X + (size_t)t * a.B * a.ldx;
@@ -204,9 +235,11 @@ __global__ void __launch_bounds__(1024) k_step(StepArgs a) {
     __shared__ int kidx[LSTM_SD_MAX_K];
     __shared__ float red[16][MG][16 * NT + 1];
     const StepDir& D = a.d[blockIdx.z];
+    const int utile = xcd_tile(blockIdx.x, (a.H + UPW - 1) / UPW);
+    if (utile < 0) return;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int H = a.H, G = 4 * H, B = a.B;
-    const int u0 = blockIdx.x * UPW;
+    const int u0 = utile * UPW;
     const int m0 = blockIdx.y * MG;
     const int g8 = 8 * (lane >> 4);
     const T* hp = (const T*)D.hprev;
@@ -322,20 +355,27 @@ __global__ void __launch_bounds__(1024) k_bwd(BwdArgs a) {
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int H = a.H, G = 4 * H, B = a.B;
     const int m0 = blockIdx.y * 64;
-    const bool kept_tile = a.has_next && (int)blockIdx.x < a.nkt;
-    int j0, nlist;
+    // Slot -> (XCD slice x, tile i of that slice).  Slice x holds units
+    // [floor(xH/8), floor((x+1)H/8)), so a unit is always handled on the same
+    // XCD and its rows of U stay in that XCD's L2 from step to step.
+    const int nkslots = a.has_next ? NXCD * a.tps : 0;
+    const bool kept_tile = (int)blockIdx.x < nkslots;
+    const int slot = kept_tile ? blockIdx.x : blockIdx.x - nkslots;
+    const int x = slot % NXCD, ti = slot / NXCD;
+    int lo, hi;
     const int32_t* list;
     if (kept_tile) {
-        j0 = blockIdx.x * 16; nlist = *D.ncount; list = D.nkeep;
+        lo = D.nkseg[x]; hi = D.nkseg[x + 1]; list = D.nkeep;
+    } else if (a.has_next) {
+        lo = D.ndseg[x]; hi = D.ndseg[x + 1]; list = D.ndrop;
     } else {
-        j0 = (blockIdx.x - (a.has_next ? a.nkt : 0)) * 16;
-        if (a.has_next) { nlist = *D.ndcount; list = D.ndrop; }
-        else { nlist = H; list = nullptr; }
+        lo = slice_start(x, H); hi = slice_start(x + 1, H); list = nullptr;
     }
-    if (j0 >= nlist) return;
+    const int j0 = lo + 16 * ti;
+    if (ti >= a.tps || j0 >= hi) return;
     if (threadIdx.x < 16) {
         const int j = j0 + threadIdx.x;
-        units[threadIdx.x] = j < nlist ? (list ? list[j] : j) : -1;
+        units[threadIdx.x] = j < hi ? (list ? list[j] : j) : -1;
     }
     __syncthreads();
     if (kept_tile) {
@@ -456,9 +496,13 @@ __global__ void __launch_bounds__(256) k_dx(DxArgs a) {
     __shared__ float red[4][64][17];
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int t = blockIdx.y;
-    const int cnt = a.site.count[t];
-    const int j0 = blockIdx.x * 16;
-    if (j0 >= cnt) return;
+    // slot -> (XCD slice x, tile ti): kept rows of t inside slice x of W
+    const int x = blockIdx.x % NXCD, ti = blockIdx.x / NXCD;
+    const int32_t* ks = a.site.kseg + (size_t)t * (NXCD + 1);
+    const int hi = ks[x + 1];
+    const int j0 = ks[x] + 16 * ti;
+    if (ti >= a.tps || j0 >= hi) return;
+    const int cnt = hi;                     // columns of this tile end at the slice end
     const int m0 = blockIdx.z * 64;
     const int j = j0 + (lane & 15);
     const int g8 = 8 * (lane >> 4);
@@ -522,8 +566,10 @@ __global__ void __launch_bounds__(256) k_dx(DxArgs a) {
 template <typename T>
 __global__ void __launch_bounds__(512) k_wgrad(WgArgs a) {
     extern __shared__ float acc_lds[];   // [K][16]
+    const int ctile = xcd_tile(blockIdx.x, (a.G + 15) / 16);
+    if (ctile < 0) return;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int n0 = blockIdx.x * 16;
+    const int n0 = ctile * 16;
     const int col = lane & 15;
     const int n = n0 + col;
     const bool nok = n < a.G;
@@ -680,6 +726,68 @@ __global__ void __launch_bounds__(256) k_mse_final(const float* partial, int np,
 }
 
 // ---------------------------------------------------------------------------
+// Kernel timer (instrumentation): HIP event pairs around the launches of one
+// kernel class.
+enum KernelId { KID_NONE = -1, KID_MASK, KID_TRANS, KID_FX, KID_STEP, KID_BWD, KID_DX, KID_WGRAD, KID_COUNT };
+static const char* const kKernelNames[KID_COUNT] = {"mask_build", "transpose", "fx", "step", "bwd", "dx", "wgrad"};
+static int g_timer_kid = KID_NONE;
+static std::vector<hipEvent_t> g_ev_pool;
+static size_t g_ev_used = 0;
+
+static hipEvent_t timer_event() {
+    if (g_ev_used == g_ev_pool.size()) {
+        hipEvent_t e;
+        if (hipEventCreate(&e) != hipSuccess) return nullptr;
+        g_ev_pool.push_back(e);
+    }
+    return g_ev_pool[g_ev_used++];
+}
+
+int kernel_timer_start(const char* name) {
+    for (int i = 0; i < KID_COUNT; ++i)
+        if (name && strcmp(name, kKernelNames[i]) == 0) {
+            g_timer_kid = i;
+            g_ev_used = 0;
+            return 0;
+        }
+    return -1;
+}
+int kernel_timer_stop(double* total_ms, int64_t* launches) {
+    g_timer_kid = KID_NONE;
+    double tot = 0.0;
+    int64_t n = 0;
+    if (g_ev_used >= 2) {
+        if (hipEventSynchronize(g_ev_pool[g_ev_used - 1]) != hipSuccess) return -1;
+        for (size_t i = 0; i + 1 < g_ev_used; i += 2) {
+            float ms = 0.f;
+            if (hipEventElapsedTime(&ms, g_ev_pool[i], g_ev_pool[i + 1]) != hipSuccess) return -1;
+            tot += ms;
+            ++n;
+        }
+    }
+    g_ev_used = 0;
+    if (total_ms) *total_ms = tot;
+    if (launches) *launches = n;
+    return 0;
+}
+
+// Launch a kernel; while the timer is on for its class, the launch carries
+// a start/stop event pair (timestamps of the dispatch itself).
+template <typename... KArgs, typename... Args>
+static void launch_k(int kid, void (*kernel)(KArgs...), dim3 grid, dim3 block, size_t shm, hipStream_t st,
+                     Args... args) {
+    if (g_timer_kid == kid) {
+        hipEvent_t e0 = timer_event(), e1 = timer_event();
+        if (e0 && e1) {
+            hipExtLaunchKernelGGL(kernel, grid, block, (uint32_t)shm, st, e0, e1, 0, args...);
+            return;
+        }
+    }
+    kernel<<<grid, block, shm, st>>>(args...);
+}
+static inline int xcd_grid(int ntiles) { return NXCD * ((ntiles + NXCD - 1) / NXCD); }
+
+// ---------------------------------------------------------------------------
 // Launchers (host).
 static inline int nblk(long n, int bs, int cap = 4096) {
     long g = (n + bs - 1) / bs;
@@ -688,59 +796,57 @@ static inline int nblk(long n, int bs, int cap = 4096) {
 }
 
 void launch_mask_build(const MaskArgs& a, int sites, hipStream_t st) {
-    hipLaunchKernelGGL(k_mask_build, dim3(a.T, sites), dim3(256), 0, st, a);
+    launch_k(KID_MASK, k_mask_build, dim3(a.T, sites), dim3(256), 0, st, a);
 }
 template <typename T>
 void launch_transpose(const TransArgs& a, int N, hipStream_t st) {
-    hipLaunchKernelGGL(k_transpose<T>, dim3((a.K + 31) / 32, a.BP / 32, N), dim3(32, 8), 0, st, a);
+    launch_k(KID_TRANS, k_transpose<T>, dim3((a.K + 31) / 32, a.BP / 32, N), dim3(32, 8), 0, st, a);
 }
 template <typename T>
 void launch_fx(const FxArgs& a, hipStream_t st) {
-    hipLaunchKernelGGL(k_fx<T>, dim3((a.G + 63) / 64, (a.B + 63) / 64, a.T), dim3(256), 0, st, a);
+    launch_k(KID_FX, k_fx<T>, dim3(xcd_grid((a.G + 63) / 64), (a.B + 63) / 64, a.T), dim3(256), 0, st, a);
 }
 template <typename T>
 void launch_step(const StepArgs& a, int D, hipStream_t st) {
-    if (a.H > 1024) {
-        hipLaunchKernelGGL((k_step<T, 2>), dim3((a.H + 7) / 8, (a.B + 31) / 32, D), dim3(1024), 0, st, a);
-    } else {
-        hipLaunchKernelGGL((k_step<T, 1>), dim3((a.H + 3) / 4, (a.B + 63) / 64, D), dim3(1024), 0, st, a);
-    }
+    if (a.H > 1024)
+        launch_k(KID_STEP, k_step<T, 2>, dim3(xcd_grid((a.H + 7) / 8), (a.B + 31) / 32, D), dim3(1024), 0, st, a);
+    else
+        launch_k(KID_STEP, k_step<T, 1>, dim3(xcd_grid((a.H + 3) / 4), (a.B + 63) / 64, D), dim3(1024), 0, st, a);
 }
 template <typename T>
 void launch_bwd(const BwdArgs& a, int D, hipStream_t st) {
-    const int ndt = (a.H + 15) / 16;
-    const int nx = (a.has_next ? a.nkt : 0) + ndt;
-    hipLaunchKernelGGL(k_bwd<T>, dim3(nx, (a.B + 63) / 64, D), dim3(1024), 0, st, a);
+    const int nx = (a.has_next ? 2 : 1) * NXCD * a.tps;
+    launch_k(KID_BWD, k_bwd<T>, dim3(nx, (a.B + 63) / 64, D), dim3(1024), 0, st, a);
 }
 template <typename T>
 void launch_dx(const DxArgs& a, int K, hipStream_t st) {
-    hipLaunchKernelGGL(k_dx<T>, dim3((K + 15) / 16, a.T, (a.B + 63) / 64), dim3(256), 0, st, a);
+    launch_k(KID_DX, k_dx<T>, dim3(NXCD * a.tps, a.T, (a.B + 63) / 64), dim3(256), 0, st, a);
 }
 template <typename T>
 void launch_wgrad(const WgArgs& a, int ts, hipStream_t st) {
     const size_t lds = (size_t)a.K * 16 * sizeof(float);
-    hipLaunchKernelGGL(k_wgrad<T>, dim3((a.G + 15) / 16, ts), dim3(512), lds, st, a);
+    launch_k(KID_WGRAD, k_wgrad<T>, dim3(xcd_grid((a.G + 15) / 16), ts), dim3(512), lds, st, a);
 }
 void launch_wreduce(const float* part, float* dW, long n, int ts, hipStream_t st) {
-    hipLaunchKernelGGL(k_wreduce, dim3(nblk(n, 256, 8192)), dim3(256), 0, st, part, dW, n, ts);
+    launch_k(KID_NONE, k_wreduce, dim3(nblk(n, 256, 8192)), dim3(256), 0, st, part, dW, n, ts);
 }
 template <typename T>
 void launch_fwd_init(const void* h0, const float* c0, float* hT, float* cT, long n, hipStream_t st) {
-    hipLaunchKernelGGL(k_fwd_init<T>, dim3(nblk(n, 256)), dim3(256), 0, st, (const T*)h0, c0, hT, cT, n);
+    launch_k(KID_NONE, k_fwd_init<T>, dim3(nblk(n, 256)), dim3(256), 0, st, (const T*)h0, c0, hT, cT, n);
 }
 void launch_bwd_init(const float* dhT, const float* dcT, float* dhc, float* dcs, long n, hipStream_t st) {
-    hipLaunchKernelGGL(k_bwd_init, dim3(nblk(n, 256)), dim3(256), 0, st, dhT, dcT, dhc, dcs, n);
+    launch_k(KID_NONE, k_bwd_init, dim3(nblk(n, 256)), dim3(256), 0, st, dhT, dcT, dhc, dcs, n);
 }
 void launch_expand(const float* dxc, int ldc, const SiteView& s, float* dx, int B, int K, int T, hipStream_t st) {
-    hipLaunchKernelGGL(k_expand, dim3(nblk((long)T * B * K, 256)), dim3(256), 0, st, dxc, ldc, s, dx, B, K, T);
+    launch_k(KID_NONE, k_expand, dim3(nblk((long)T * B * K, 256)), dim3(256), 0, st, dxc, ldc, s, dx, B, K, T);
 }
 void launch_db(const float* dbpart, float* db, int G, int T, int ng, hipStream_t st) {
-    hipLaunchKernelGGL(k_db, dim3((G + 255) / 256), dim3(256), 0, st, dbpart, db, G, T, ng);
+    launch_k(KID_NONE, k_db, dim3((G + 255) / 256), dim3(256), 0, st, dbpart, db, G, T, ng);
 }
 void launch_mse(const float* y, const float* tg, const int32_t* lengths, float* dy, float* partial, int np,
                 float* loss, int T, int B, int F, hipStream_t st) {
-    hipLaunchKernelGGL(k_mse, dim3(np), dim3(256), 0, st, y, tg, lengths, dy, partial, T, B, F);
-    hipLaunchKernelGGL(k_mse_final, dim3(1), dim3(256), 0, st, partial, np, lengths, loss, T, B, F);
+    launch_k(KID_NONE, k_mse, dim3(np), dim3(256), 0, st, y, tg, lengths, dy, partial, T, B, F);
+    launch_k(KID_NONE, k_mse_final, dim3(1), dim3(256), 0, st, (const float*)partial, np, lengths, loss, T, B, F);
 }
 
 static int g_attr_done = 0;

@@ -22,7 +22,7 @@ struct Plan {
     int ts;               // time splits of the weight-gradient kernel
 
     // mask buffer
-    size_t m_mask, m_keep, m_pos, m_count, m_drop, m_dcount, m_total;
+    size_t m_mask, m_keep, m_pos, m_count, m_drop, m_dcount, m_kseg, m_dseg, m_total;
 
     // reserve
     size_t r_gates, r_c, r_hrecT, r_dir_bytes;  // inside one (l, d) block

@@ -31,10 +31,18 @@ def workload(name):
 
 def check_masks(sess, cfg, m_nr, m_rh, compact):
     mask, keep, pos, count, drop, dcount = sess.mask_views()
+    kseg, dseg = sess.last_segments
     for s, ref in enumerate(site_list(cfg, m_nr, m_rh)):
         K = ref.shape[1]
         assert np.array_equal(mask[s, :, :K], ref), f"mask site {s}"
+        starts = [(x * K) // 8 for x in range(9)]
         for t in range(ref.shape[0]):
+            if compact:
+                kept_below = [int(ref[t][:st].sum()) for st in starts]
+                assert list(kseg[s, t]) == kept_below
+                assert list(dseg[s, t]) == [st - kb for st, kb in zip(starts, kept_below)]
+            else:
+                assert list(kseg[s, t]) == starts and not dseg[s, t].any()
             if compact:
                 kl = np.nonzero(ref[t])[0]
                 assert count[s, t] == len(kl)
@@ -129,3 +137,26 @@ def test_fresh_masks_per_step():
     torch.cuda.synchronize()
     m_nr, m_rh = oracle_masks(cfg, 0.5, 0.5, step=5)
     check_masks(s, cfg, m_nr, m_rh, 1)
+
+
+def test_kernel_timer_counts_launches():
+    from paper_2106_12089_amd import binding as B_
+    from paper_2106_12089_amd.session import Session
+    cfg = workloads.get_config("tiny")
+    wl = workload("tiny")
+    say("[gpu] kernel timer")
+    s = Session(wl, 0.5, 0.5, 1)
+    s.masks(cfg.mask_seed, 0)
+    torch.cuda.synchronize()
+    for name, per_step in (("step", cfg.num_layers * cfg.seq_len), ("bwd", cfg.num_layers * (cfg.seq_len + 1)),
+                           ("wgrad", 2 * cfg.num_layers * cfg.num_dirs)):
+        B_.lstm_sd_kernel_timer_start(name)
+        for _ in range(3):
+            s.forward()
+            s.loss_grad()
+            s.backward()
+        ms, n = B_.lstm_sd_kernel_timer_stop()
+        assert n == 3 * per_step, (name, n)
+        assert 0.0 < ms < 1e4
+    with pytest.raises(B_.LstmSdError):
+        B_.lstm_sd_kernel_timer_start("no_such_kernel")
