@@ -33,7 +33,7 @@ WORKLOAD = "lm_medium"
 METRIC = "LSTM fwd+BPTT step time & eff. TFLOP/s; speedup vs dense at p=0.5"
 PEAK_HBM_GBS = 8000.0
 PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
-KERNELS = ("step", "bwd", "wgrad", "fx", "dx")
+KERNELS = ("fwd_persist", "step", "bwd", "wgrad", "fx", "dx")
 KERNEL_SRC = os.path.join(ROOT, "paper_2106_12089_amd", "csrc", "kernels.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
@@ -84,6 +84,15 @@ def kernel_work(kind, counts, cfg):
                 by += T * B * (G * 4 + H * 8 + G * 4 + H * 4 + 2 * H * e + H * 8)
                 by += T * B * H * (4 if l == L - 1 else 4 * e)
         return fl, by, L * T
+    if kind == "fwd_persist":               # one launch per layer runs every step (both directions)
+        for l in range(L):
+            for d in range(D):
+                nh = np.asarray(counts[L + l * D + d], dtype=np.float64)
+                fl += float(np.sum(2 * B * G * nh))
+                by += H * G * e                                        # U slice, read once per launch
+                by += T * B * (G * 4 + G * 4 + H * 4 + 2 * H * e)      # gx, gates, c, h^T + exchange
+                by += T * B * H * (4 if l == L - 1 else 2 * e) + B * H * 16
+        return fl, by, L
     if kind == "bwd":                       # T pointwise steps + one final pass per layer
         for l in range(L):
             for d in range(D):
@@ -234,7 +243,8 @@ def cpu_baseline(wl, p_nr, p_rh, budget_s=12.0):
                 ms_per_step=round(t_tot / n * 1e3, 3))
 
 
-KERNEL_SYMBOLS = {"step": "lsd::k_step<", "bwd": "lsd::k_bwd<", "wgrad": "lsd::k_wgrad<",
+KERNEL_SYMBOLS = {"fwd_persist": "lsd::k_fwd_persist<", "step": "lsd::k_step<", "bwd": "lsd::k_bwd<",
+                  "wgrad": "lsd::k_wgrad<",
                   "fx": "lsd::k_fx<", "dx": "lsd::k_dx<"}
 
 

@@ -203,7 +203,9 @@ int lstm_sd_mse_grad(const lstm_sd_dims* dims, const float* y, const float* targ
  * events recorded on its launch stream; lstm_sd_kernel_timer_stop()
  * waits for the last pair, returns the summed elapsed time in milliseconds
  * and the number of launches, and turns the timer off.  Names:
- * "mask_build", "transpose", "fx", "step", "bwd", "dx", "wgrad".  Events
+ * "mask_build", "transpose", "fx", "step", "bwd", "dx", "wgrad",
+ * "fwd_persist", "bwd_persist" (the persistent recurrent kernels, one launch
+ * per layer; their pair is recorded around the cooperative launch).  Events
  * are created by the library (no device memory is allocated).  Not
  * thread-safe; for benchmarks. */
 int lstm_sd_kernel_timer_start(const char* kernel);

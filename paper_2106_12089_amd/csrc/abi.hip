@@ -4,6 +4,7 @@
 
 #include <math.h>
 #include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <string>
@@ -30,6 +31,10 @@ void launch_db(const float*, float*, int, int, int, hipStream_t);
 void launch_mse(const float*, const float*, const int32_t*, float*, float*, int, float*, int, int, int,
                 hipStream_t);
 int setup_kernel_attributes();
+bool timer_pair(int kid, hipEvent_t* e0, hipEvent_t* e1);
+template <typename T>
+hipError_t launch_fwd_persist(PFwdArgs& a, int D, hipStream_t st, int timer_on, hipEvent_t e0, hipEvent_t e1);
+constexpr int KID_FWDP_ = 7;
 int kernel_timer_start(const char* name);
 int kernel_timer_stop(double* total_ms, int64_t* launches);
 
@@ -71,6 +76,7 @@ int make_plan(const lstm_sd_dims* d, Plan* p, const char** why) {
     q.esize = d->dtype == LSTM_SD_DTYPE_BF16 ? 2 : 4;
     q.G = 4 * q.H;
     q.BP = (q.B + 31) / 32 * 32;
+    q.HP = (q.H + 7) / 8 * 8;
     q.MGc = (q.B + 63) / 64;
     q.sites = q.L + q.L * q.D;
     q.kin_max = q.L > 1 ? (q.I > q.D * q.H ? q.I : q.D * q.H) : q.I;
@@ -113,7 +119,7 @@ int make_plan(const lstm_sd_dims* d, Plan* p, const char** why) {
 
     off = 0;
     q.w_gx = off;   off = align_up(off + D * T * B * G * 4, A);
-    q.w_hrec = off; off = align_up(off + D * 2 * B * H * es, A);
+    q.w_hrec = off; off = align_up(off + D * 2 * B * (size_t)q.HP * es, A);
     const size_t fwd = off;
     off = 0;
     q.w_da = off;     off = align_up(off + D * T * B * G * es, A);
@@ -124,9 +130,29 @@ int make_plan(const lstm_sd_dims* d, Plan* p, const char** why) {
     q.w_dxc = off;    off = align_up(off + 2 * T * B * (size_t)q.kin_max * 4, A);
     q.w_wpart = off;  off = align_up(off + (q.ts > 1 ? (size_t)q.ts * KM * G * 4 : 0), A);
     const size_t bwd = off;
-    q.w_loss = align_up(fwd > bwd ? fwd : bwd, A);
+    q.w_sync = align_up(fwd > bwd ? fwd : bwd, A);
+    q.w_loss = q.w_sync + 8192;           // barrier counters (2), then the error flag at +4096
     q.w_total = q.w_loss + 16384;
     return LSTM_SD_OK;
+}
+
+// Persistent recurrent kernels are used unless LSTM_SD_PERSIST=0 (a debug
+// switch that forces the per-step kernels).
+static bool use_persistent() {
+    const char* v = getenv("LSTM_SD_PERSIST");
+    return !(v && v[0] == '0');
+}
+
+// Wall-clock ticks of the grid-barrier time-out (0.5 s).
+static long long barrier_timeout_ticks() {
+    static long long ticks = 0;
+    if (!ticks) {
+        int dev = 0, khz = 0;
+        hipGetDevice(&dev);
+        if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess || khz <= 0) khz = 100000;
+        ticks = (long long)khz * 500;
+    }
+    return ticks;
 }
 
 static int hip_check(const char* where) {
@@ -221,6 +247,42 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
             f.B = B; f.G = G; f.T = T; f.dense = !P.compact; f.s = P.s_nr;
             launch_fx<E>(f, st);
         }
+        if (use_persistent()) {
+            PFwdArgs pa;
+            memset(&pa, 0, sizeof(pa));
+            pa.lengths = lengths;
+            pa.bar = (unsigned*)(W + P.w_sync);
+            pa.err = (int*)(W + P.w_sync + 4096);
+            pa.timeout = barrier_timeout_ticks();
+            pa.B = B; pa.H = H; pa.HP = P.HP; pa.T = T; pa.BP = BP; pa.ldy = D * H; pa.dense = !P.compact;
+            pa.s = P.s_rh;
+            for (int d = 0; d < D; ++d) {
+                const int k = l * D + d;
+                char* rd = R + P.rdir(l, d);
+                PFwdDir& pd = pa.d[d];
+                pd.h0 = (const char*)h0 + (size_t)k * B * H * es;
+                pd.U = w->U[k];
+                pd.gx = (const float*)(W + P.w_gx) + (size_t)d * T * B * G;
+                pd.c0 = c0 + (size_t)k * B * H;
+                pd.rh = site_view(P, mbuf, P.site_rh(l, d));
+                pd.gates = (float*)(rd + P.r_gates);
+                pd.cres = (float*)(rd + P.r_c);
+                pd.hrecT = rd + P.r_hrecT;
+                pd.hx = W + P.w_hrec + (size_t)d * 2 * B * P.HP * es;
+                pd.hT = hT + (size_t)k * B * H;
+                pd.cT = cT + (size_t)k * B * H;
+                if (l == L - 1) {
+                    pd.y = y + d * H;
+                } else {
+                    pd.ybuf = R + P.rybuf(l) + (size_t)d * H * es;
+                    pd.ybufT = R + P.rybufT(l) + (size_t)d * H * BP * es;
+                }
+            }
+            hipEvent_t e0 = nullptr, e1 = nullptr;
+            const bool timed = timer_pair(KID_FWDP_, &e0, &e1);
+            if (launch_fwd_persist<E>(pa, D, st, timed, e0, e1) == hipSuccess) continue;
+            (void)hipGetLastError();          // does not fit: per-step kernels below
+        }
         for (int s = 0; s < T; ++s) {
             StepArgs a;
             memset(&a, 0, sizeof(a));
@@ -229,12 +291,12 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
                 const int k = l * D + d;
                 const int t = d == 0 ? s : T - 1 - s;
                 char* rd = R + P.rdir(l, d);
-                char* hrec2 = W + P.w_hrec + (size_t)d * 2 * B * H * es;
+                char* hrec2 = W + P.w_hrec + (size_t)d * 2 * B * P.HP * es;
                 StepDir& sd = a.d[d];
                 sd.t = t;
                 sd.hprev = s == 0 ? (const void*)((const char*)h0 + (size_t)k * B * H * es)
-                                  : (const void*)(hrec2 + (size_t)((s - 1) & 1) * B * H * es);
-                sd.hrec = hrec2 + (size_t)(s & 1) * B * H * es;
+                                  : (const void*)(hrec2 + (size_t)((s - 1) & 1) * B * P.HP * es);
+                sd.hrec = hrec2 + (size_t)(s & 1) * B * P.HP * es;
                 sd.hrecT = rd + P.r_hrecT + (size_t)t * H * BP * es;
                 sd.U = w->U[k];
                 sd.gx = (const float*)(W + P.w_gx) + ((size_t)d * T + t) * B * G;

@@ -82,13 +82,12 @@ __device__ __forceinline__ u64x4 philox4x64_10(u64x4 c, uint64_t k0, uint64_t k1
 }
 
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ float sigmoidf_(float z) { return 1.0f / (1.0f + __expf(-z)); }
-__device__ __forceinline__ float tanhf_(float z) {
-    // tanh z = 2 sigmoid(2z) - 1, written to stay accurate for small |z|
-    float a = fabsf(z);
-    float e = __expf(-2.0f * a);
-    float t = (1.0f - e) / (1.0f + e);
-    return copysignf(t, z);
-}
+// Gate activations on the hardware exponential (v_exp_f32 via __expf) and
+// reciprocal (v_rcp_f32).  sigmoid z = 1 / (1 + e^-z);  tanh z = 1 - 2 / (1 + e^{2z}),
+// which saturates to +-1 without overflow (e^{2z} -> inf gives 1, -> 0 gives
+// -1).  Absolute error a few 1e-7; the absolute error of tanh near 0 is that
+// of 1 - (1 - 2z), i.e. about one float ulp of 1.
+__device__ __forceinline__ float sigmoid_fast(float z) { return __builtin_amdgcn_rcpf(1.0f + __expf(-z)); }
+__device__ __forceinline__ float tanh_fast(float z) { return 1.0f - 2.0f * __builtin_amdgcn_rcpf(1.0f + __expf(2.0f * z)); }
 
 }  // namespace lsd

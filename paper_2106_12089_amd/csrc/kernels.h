@@ -146,4 +146,32 @@ struct WgArgs {
     float s;
 };
 
+// Persistent forward recurrence of one layer (both directions): one
+// cooperative launch runs all T steps.
+struct PFwdDir {
+    const void* h0;                     // [B][H] row-major h0 (dtype)
+    const void* U;                      // [H][4H]
+    const float* gx;                    // [T][B][4H] input product incl. bias
+    const float* c0;                    // [B][H]
+    SiteView rh;                        // RH site of (l, d)
+    float* gates;                       // [T][B][4H]
+    float* cres;                        // [T][B][H]
+    void* hrecT;                        // [T][H][BP]
+    void* hx;                           // [2][B][HP] exchange: h_t compacted by the next step's keep list
+    float* hT;                          // [B][H]
+    float* cT;                          // [B][H]
+    float* y;                           // top layer: y + d*H (rows ld ldy, t stride B*ldy), or null
+    void* ybuf;                         // inner layer: ybuf + d*H, or null
+    void* ybufT;                        // inner layer: ybufT + d*H*BP (t stride ldy*BP), or null
+};
+struct PFwdArgs {
+    PFwdDir d[2];
+    const int32_t* lengths;
+    unsigned* bar;                      // [2] barrier counters (zeroed before launch)
+    int* err;                           // barrier time-out flag
+    long long timeout;                  // wall-clock ticks
+    int B, H, HP, T, BP, ldy, dense, ntiles, mgroups;
+    float s;
+};
+
 }  // namespace lsd

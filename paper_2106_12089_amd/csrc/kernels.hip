@@ -309,13 +309,13 @@ __global__ void __launch_bounds__(1024) k_step(StepArgs a) {
                 for (int i = 0; i < 16; ++i) v += red[i][rr][cc];
                 pre[g] = a.s * v + D.gx[(size_t)b * G + g * H + u];
             }
-            const float ig = 1.0f / (1.0f + expf(-pre[0]));
-            const float fg = 1.0f / (1.0f + expf(-pre[1]));
-            const float gg = tanhf(pre[2]);
-            const float og = 1.0f / (1.0f + expf(-pre[3]));
+            const float ig = sigmoid_fast(pre[0]);
+            const float fg = sigmoid_fast(pre[1]);
+            const float gg = tanh_fast(pre[2]);
+            const float og = sigmoid_fast(pre[3]);
             const float cp = D.cT[(size_t)b * H + u];
             const float cn = fg * cp + ig * gg;
-            const float hn = og * tanhf(cn);
+            const float hn = og * tanh_fast(cn);
             const bool valid = (a.lengths == nullptr) || (D.t < a.lengths[b]);
             float* gt = D.gates + (size_t)b * G;
             gt[u] = ig; gt[H + u] = fg; gt[2 * H + u] = gg; gt[3 * H + u] = og;
@@ -448,7 +448,7 @@ __global__ void __launch_bounds__(1024) k_bwd(BwdArgs a) {
                 const float ig = gt[u], fg = gt[H + u], gg = gt[2 * H + u], og = gt[3 * H + u];
                 const float ct = D.cres[(size_t)b * H + u];
                 const float cp = D.cprev[(size_t)b * H + u];
-                const float tc = tanhf(ct);
+                const float tc = tanh_fast(ct);
                 const float dout = dh * tc;                            // Eq. 7
                 const float dc = dh * og * (1.0f - tc * tc) + dcin;    // Eq. 7
                 da4[0] = dc * gg * ig * (1.0f - ig);                   // Eq. 9, sigmoid'
@@ -728,8 +728,10 @@ __global__ void __launch_bounds__(256) k_mse_final(const float* partial, int np,
 // ---------------------------------------------------------------------------
 // Kernel timer (instrumentation): HIP event pairs around the launches of one
 // kernel class.
-enum KernelId { KID_NONE = -1, KID_MASK, KID_TRANS, KID_FX, KID_STEP, KID_BWD, KID_DX, KID_WGRAD, KID_COUNT };
-static const char* const kKernelNames[KID_COUNT] = {"mask_build", "transpose", "fx", "step", "bwd", "dx", "wgrad"};
+enum KernelId { KID_NONE = -1, KID_MASK, KID_TRANS, KID_FX, KID_STEP, KID_BWD, KID_DX, KID_WGRAD, KID_FWDP, KID_BWDP,
+                KID_COUNT };
+static const char* const kKernelNames[KID_COUNT] = {"mask_build", "transpose", "fx", "step", "bwd", "dx", "wgrad",
+                                                    "fwd_persist", "bwd_persist"};
 static int g_timer_kid = KID_NONE;
 static std::vector<hipEvent_t> g_ev_pool;
 static size_t g_ev_used = 0;
@@ -741,6 +743,14 @@ static hipEvent_t timer_event() {
         g_ev_pool.push_back(e);
     }
     return g_ev_pool[g_ev_used++];
+}
+
+// Event pair for a launch of kernel class kid, or false if its timer is off.
+bool timer_pair(int kid, hipEvent_t* e0, hipEvent_t* e1) {
+    if (g_timer_kid != kid) return false;
+    *e0 = timer_event();
+    *e1 = timer_event();
+    return *e0 && *e1;
 }
 
 int kernel_timer_start(const char* name) {

@@ -1,0 +1,377 @@
+// Persistent recurrent kernels (gfx950): one cooperative launch runs every
+// time step of a layer.  Each workgroup keeps its slice of the recurrent
+// weight U in LDS and its part of the cell state in registers for the whole
+// sequence; the workgroups meet at a grid barrier once per step.
+//
+// The producer of h_t knows the next step's keep list (all masks are drawn
+// before the forward pass), so it writes h_t already compacted by that list
+// ("compaction at the producer"): the consumer reads its MFMA A fragments as
+// contiguous 16-byte loads and never touches a dropped column.
+#include <hip/hip_runtime.h>
+
+#include "device.h"
+#include "kernels.h"
+#include "../../include/lstm_sd.h"
+
+namespace lsd {
+
+// ---------------------------------------------------------------------------
+// Cross-workgroup exchange and grid barrier.
+//
+// Values that other workgroups read during the same launch (the compacted
+// h_t, the backward DA_t) are written and read with relaxed agent-scope
+// atomic accesses: on gfx950 these are ordinary loads and stores carrying the
+// device-coherence bit, so no L2 writeback or invalidate of unrelated data is
+// needed.  A workgroup signals the end of a step by waiting for its own
+// stores to complete, synchronising its threads and adding 1 to the
+// direction's counter; a waiting workgroup spins (thread 0) until the counter
+// reaches the target.  The spin is bounded by wall-clock time; on time-out,
+// or when another workgroup has timed out, it reports failure and the kernel
+// ends (outputs are then poisoned with NaN).
+__device__ __forceinline__ void grid_arrive(unsigned* bar) {
+    __builtin_amdgcn_s_waitcnt(0);      // this thread's stores have completed
+    __syncthreads();
+    if (threadIdx.x == 0) __hip_atomic_fetch_add(bar, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Wait until the counter reaches target.  Returns false on time-out or when
+// another workgroup has timed out (err set).
+__device__ __forceinline__ bool grid_wait(unsigned* bar, unsigned target, int* err, long long timeout) {
+    __shared__ int ok;
+    if (threadIdx.x == 0) {
+        int good = 1;
+        const long long t0 = wall_clock64();
+        while (__hip_atomic_load(bar, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+            if (__hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) { good = 0; break; }
+            if (wall_clock64() - t0 > timeout) {
+                __hip_atomic_fetch_or(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                good = 0;
+                break;
+            }
+        }
+        ok = good;
+    }
+    __syncthreads();
+    return ok != 0;
+}
+
+// coherent (agent-scope) element store and 8-element load of exchange data
+__device__ __forceinline__ void xstore(bf16* p, bf16 v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void xstore(float* p, float v) {
+    __hip_atomic_store((uint32_t*)p, __float_as_uint(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void xload8(const bf16* p, bf16* o) {
+    const unsigned long long* q = (const unsigned long long*)p;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const unsigned long long v = __hip_atomic_load(q + h, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[4 * h + e] = (bf16)((v >> (16 * e)) & 0xffffu);
+    }
+}
+__device__ __forceinline__ void xload8(const float* p, float* o) {
+    const unsigned long long* q = (const unsigned long long*)p;
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+        const unsigned long long v = __hip_atomic_load(q + h, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        o[2 * h] = __uint_as_float((uint32_t)v);
+        o[2 * h + 1] = __uint_as_float((uint32_t)(v >> 32));
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Persistent forward recurrence (Eq. 1-6) of one layer, both directions.
+// Workgroup w -> (direction, unit tile, row group).  A unit tile is 4*NT
+// hidden units = NT 16-column MFMA tiles (the four gates of 4 units each);
+// a row group is MG batch rows.  512 threads = 8 waves; the contraction over
+// the kept recurrent neurons is split over the waves (each wave issues all of
+// its exchange loads before its first MFMA) and reduced in LDS.
+// Dynamic LDS: U slice [H][16*NT+2] (dtype), keep list [H+32] (int16),
+// reduction [8][MG][16*NT] (float).
+constexpr int PF_NW = 8;
+
+template <typename T, int NT, int MG>
+__global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
+    constexpr int UPW = 4 * NT, MT = MG / 16, NW = PF_NW, NC = 16 * NT, UP = NC + 2;
+    constexpr int NTH = 64 * NW;
+    constexpr int PPT = (MG * UPW + NTH - 1) / NTH;
+    constexpr int MAXC = MT <= 2 ? 6 : 3;       // chunks per wave per round (registers)
+    extern __shared__ __align__(16) char smem[];
+    const int H = a.H, G = 4 * H, B = a.B, T_ = a.T, HP = a.HP;
+    T* Us = (T*)smem;
+    int16_t* kidx = (int16_t*)(smem + (((size_t)H * UP * sizeof(T) + 15) & ~(size_t)15));
+    float* red = (float*)((char*)kidx + (((size_t)(H + 32) * 2 + 15) & ~(size_t)15));
+
+    const int nslot = a.ntiles * a.mgroups;
+    const int d = blockIdx.x / nslot, rem = blockIdx.x % nslot;
+    const int tile = rem / a.mgroups, mg = rem % a.mgroups;
+    const PFwdDir& D = a.d[d];
+    const int u0 = tile * UPW, m0 = mg * MG;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int g8 = 8 * (lane >> 4);
+    unsigned* bar = a.bar + d;
+
+    // U slice -> LDS: column c = nt*16 + g*4 + cu holds U[k][g*H + u0 + 4nt + cu]
+    {
+        const T* U = (const T*)D.U;
+        for (int i = tid; i < H * NC; i += NTH) {
+            const int k = i / NC, c = i % NC;
+            const int nt = c >> 4, cc = c & 15;
+            const int u = u0 + 4 * nt + (cc & 3);
+            Us[k * UP + c] = u < H ? U[(size_t)k * G + (cc >> 2) * H + u] : zero_val<T>();
+        }
+    }
+    // register state of this thread's (row, unit) pairs
+    float creg[PPT], hreg[PPT];
+    int pb[PPT], pu[PPT];
+#pragma unroll
+    for (int q = 0; q < PPT; ++q) {
+        const int p = tid + NTH * q;
+        const int rr = p / UPW, uu = p % UPW;
+        pb[q] = (p < MG * UPW) ? m0 + rr : B;
+        pu[q] = u0 + uu;
+        const bool ok = pb[q] < B && pu[q] < H;
+        creg[q] = ok ? D.c0[(size_t)pb[q] * H + pu[q]] : 0.f;
+        hreg[q] = ok ? to_f32<T>(((const T*)D.h0)[(size_t)pb[q] * H + pu[q]]) : 0.f;
+    }
+    // per-step inputs that do not depend on the recurrence, loaded one step ahead
+    float gxr[PPT][4];
+    int pn[PPT];
+    bool mn[PPT], valid[PPT];
+    int cnt = 0, cnt_next = 0;
+    constexpr int KPT = (LSTM_SD_MAX_K + NTH - 1) / NTH;   // keep-list entries per thread
+    int kreg[KPT];
+    auto prefetch = [&](int s) {
+        const int t = d == 0 ? s : T_ - 1 - s;
+        const int tn = d == 0 ? t + 1 : t - 1;
+        const bool has_next = s + 1 < T_;
+        cnt_next = D.rh.count[t];
+        const int32_t* krow = D.rh.keep + (size_t)t * D.rh.kmax;
+#pragma unroll
+        for (int i = 0; i < KPT; ++i) {
+            const int j = tid + NTH * i;
+            kreg[i] = j < cnt_next ? krow[j] : 0;
+        }
+#pragma unroll
+        for (int q = 0; q < PPT; ++q) {
+            const bool ok = pb[q] < B && pu[q] < H;
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                gxr[q][g] = ok ? D.gx[((size_t)t * B + pb[q]) * G + g * H + pu[q]] : 0.f;
+            pn[q] = (ok && has_next) ? D.rh.pos[(size_t)tn * D.rh.kmax + pu[q]] : -1;
+            mn[q] = (ok && has_next) ? D.rh.mask[(size_t)tn * D.rh.kmax + pu[q]] != 0 : false;
+            valid[q] = ok && (a.lengths == nullptr || t < a.lengths[pb[q]]);
+        }
+    };
+
+    // the keep list of the coming step, from registers to LDS
+    auto commit_kidx = [&]() {
+        cnt = cnt_next;
+#pragma unroll
+        for (int i = 0; i < KPT; ++i) {
+            const int j = tid + NTH * i;
+            if (j < cnt) kidx[j] = (int16_t)kreg[i];
+        }
+    };
+
+    // prologue: h0 compacted by the keep list of the first step
+    const int tfirst = d == 0 ? 0 : T_ - 1;
+    {
+        const int32_t* pos = D.rh.pos + (size_t)tfirst * D.rh.kmax;
+        const uint8_t* msk = D.rh.mask + (size_t)tfirst * D.rh.kmax;
+        T* hx0 = (T*)D.hx;
+#pragma unroll
+        for (int q = 0; q < PPT; ++q) {
+            if (pb[q] < B && pu[q] < H) {
+                const int pp = pos[pu[q]];
+                if (pp >= 0)
+                    xstore(hx0 + (size_t)pb[q] * HP + pp,
+                           (a.dense && !msk[pu[q]]) ? zero_val<T>() : from_f32<T>(hreg[q]));
+            }
+        }
+    }
+    prefetch(0);
+    grid_arrive(bar);
+
+    for (int s = 0; s < T_; ++s) {
+        const int t = d == 0 ? s : T_ - 1 - s;
+        // ---- wait for h_{t-1} of every workgroup of this direction
+        commit_kidx();
+        if (!grid_wait(bar, (unsigned)(s + 1) * (unsigned)nslot, a.err, a.timeout)) break;
+        const T* hc = (const T*)D.hx + (size_t)(s & 1) * B * HP;
+        f32x4_t acc[MT][NT];
+#pragma unroll
+        for (int i = 0; i < MT; ++i)
+#pragma unroll
+            for (int j = 0; j < NT; ++j) acc[i][j] = f32x4_t{0, 0, 0, 0};
+        const int nch = (cnt + 31) / 32;
+        for (int c0 = 0; c0 < nch; c0 += NW * MAXC) {
+            // issue every exchange load of this round first
+            Frag<T> fa[MAXC][MT];
+#pragma unroll
+            for (int i = 0; i < MAXC; ++i) {
+                const int kc = 32 * (c0 + w + NW * i);
+                const bool jin = kc + g8 < cnt;
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) {
+                    const int row = m0 + mt * 16 + (lane & 15);
+                    if (row < B && jin) xload8(hc + (size_t)row * HP + kc + g8, fa[i][mt].v);
+                    else {
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) fa[i][mt].v[e] = zero_val<T>();
+                    }
+                }
+            }
+#pragma unroll
+            for (int i = 0; i < MAXC; ++i) {
+                const int kc = 32 * (c0 + w + NW * i);
+                if (kc >= cnt) break;
+                Frag<T> fb[NT];
+                const int4 k8 = *(const int4*)(kidx + kc + g8);     // 8 int16 keep indices
+                const int kw[4] = {k8.x, k8.y, k8.z, k8.w};
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const int j = kc + g8 + e;
+                    const int k = j < cnt ? (int)(int16_t)(kw[e >> 1] >> (16 * (e & 1))) : -1;
+#pragma unroll
+                    for (int nt = 0; nt < NT; ++nt)
+                        fb[nt].v[e] = k >= 0 ? Us[k * UP + nt * 16 + (lane & 15)] : zero_val<T>();
+                }
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        if (kc + g8 + e >= cnt) fa[i][mt].v[e] = zero_val<T>();
+#pragma unroll
+                    for (int nt = 0; nt < NT; ++nt) mma_16x16x32(fa[i][mt], fb[nt], acc[mt][nt]);
+                }
+            }
+        }
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    red[(w * MG + mt * 16 + acc_row(lane, r)) * NC + nt * 16 + (lane & 15)] = acc[mt][nt][r];
+        __syncthreads();
+        // ---- pointwise (Eq. 1-6) and outputs; next step's inputs are loaded meanwhile
+        float gxc[PPT][4];
+        int pnc[PPT];
+        bool mnc[PPT], vc[PPT];
+#pragma unroll
+        for (int q = 0; q < PPT; ++q) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g) gxc[q][g] = gxr[q][g];
+            pnc[q] = pn[q]; mnc[q] = mn[q]; vc[q] = valid[q];
+        }
+        if (s + 1 < T_) prefetch(s + 1);
+        T* hxn = (T*)D.hx + (size_t)((s + 1) & 1) * B * HP;
+#pragma unroll
+        for (int q = 0; q < PPT; ++q) {
+            const int b = pb[q], u = pu[q];
+            if (b >= B || u >= H) continue;
+            const int rr = b - m0, uu = u - u0, nt = uu >> 2, cu = uu & 3;
+            float pre[4];
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int cc = nt * 16 + g * 4 + cu;
+                float v = 0.f;
+#pragma unroll
+                for (int i = 0; i < NW; ++i) v += red[(i * MG + rr) * NC + cc];
+                pre[g] = a.s * v + gxc[q][g];
+            }
+            const float ig = sigmoid_fast(pre[0]);
+            const float fg = sigmoid_fast(pre[1]);
+            const float gg = tanh_fast(pre[2]);
+            const float og = sigmoid_fast(pre[3]);
+            const float cp = creg[q];
+            const float cn = fg * cp + ig * gg;
+            const float hn = og * tanh_fast(cn);
+            const T hv = from_f32<T>(vc[q] ? hn : hreg[q]);
+            if (pnc[q] >= 0) xstore(hxn + (size_t)b * HP + pnc[q], (a.dense && !mnc[q]) ? zero_val<T>() : hv);
+            float* gt = D.gates + ((size_t)t * B + b) * G;
+            gt[u] = ig; gt[H + u] = fg; gt[2 * H + u] = gg; gt[3 * H + u] = og;
+            D.cres[((size_t)t * B + b) * H + u] = vc[q] ? cn : cp;
+            if (vc[q]) { creg[q] = cn; hreg[q] = hn; }
+            ((T*)D.hrecT)[((size_t)t * H + u) * a.BP + b] = hv;
+            if (D.y) D.y[((size_t)t * B + b) * a.ldy + u] = vc[q] ? hn : 0.0f;
+            if (D.ybuf) {
+                const T yv = vc[q] ? from_f32<T>(hn) : zero_val<T>();
+                ((T*)D.ybuf)[((size_t)t * B + b) * a.ldy + u] = yv;
+                ((T*)D.ybufT)[((size_t)t * a.ldy + u) * a.BP + b] = yv;
+            }
+        }
+        grid_arrive(bar);
+    }
+    // ---- final state (NaN if the barrier timed out)
+    const bool failed = __hip_atomic_load(a.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0;
+#pragma unroll
+    for (int q = 0; q < PPT; ++q) {
+        if (pb[q] < B && pu[q] < H) {
+            D.hT[(size_t)pb[q] * H + pu[q]] = failed ? __builtin_nanf("") : hreg[q];
+            D.cT[(size_t)pb[q] * H + pu[q]] = failed ? __builtin_nanf("") : creg[q];
+        }
+    }
+}
+
+__global__ void k_zero_sync(unsigned* bar, int n, int* err) {
+    for (int i = threadIdx.x; i < n; i += blockDim.x) bar[i] = 0u;
+    if (threadIdx.x == 0) *err = 0;
+}
+
+// ---------------------------------------------------------------------------
+// Host side.
+size_t fwd_persist_lds(int H, int NT, int MG, int esize) {
+    const size_t us = ((size_t)H * (16 * NT + 2) * esize + 15) & ~(size_t)15;
+    const size_t kx = ((size_t)(H + 32) * 2 + 15) & ~(size_t)15;
+    return us + kx + (size_t)PF_NW * MG * 16 * NT * 4;
+}
+
+template <typename T, int NT, int MG>
+static hipError_t launch_fwd_persist_t(const PFwdArgs& a, int nwg, size_t lds, hipStream_t st) {
+    auto fn = k_fwd_persist<T, NT, MG>;
+    hipError_t e = hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    int per_cu = 0;
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, 64 * PF_NW, lds);
+    if (e != hipSuccess) return e;
+    int dev = 0, ncu = 0;
+    hipGetDevice(&dev);
+    hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
+    if (per_cu < 1 || nwg > per_cu * ncu) return hipErrorCooperativeLaunchTooLarge;
+    PFwdArgs arg = a;
+    void* params[] = {&arg};
+    return hipLaunchCooperativeKernel((const void*)fn, dim3(nwg), dim3(64 * PF_NW), params, (unsigned)lds, st);
+}
+
+// Launches the persistent forward layer if it fits; returns hipSuccess or an
+// error (then nothing was launched and the caller uses the per-step kernels).
+template <typename T>
+hipError_t launch_fwd_persist(PFwdArgs& a, int D, hipStream_t st, int kid_timer_on, hipEvent_t e0, hipEvent_t e1) {
+    int NT, MG;
+    MG = a.B <= 32 ? 32 : 64;
+    NT = a.H >= 512 ? 2 : 1;            // fewer, wider unit tiles: a cheaper barrier
+    const int upw = 4 * NT;
+    a.ntiles = (a.H + upw - 1) / upw;
+    a.mgroups = (a.B + MG - 1) / MG;
+    const int nwg = D * a.ntiles * a.mgroups;
+    const size_t lds = fwd_persist_lds(a.H, NT, MG, (int)sizeof(T));
+    if (lds > 160 * 1024) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_zero_sync, dim3(1), dim3(64), 0, st, a.bar, 2, a.err);
+    if (kid_timer_on) hipEventRecord(e0, st);
+    hipError_t e;
+    if (NT == 1 && MG == 32) e = launch_fwd_persist_t<T, 1, 32>(a, nwg, lds, st);
+    else if (NT == 1) e = launch_fwd_persist_t<T, 1, 64>(a, nwg, lds, st);
+    else if (MG == 32) e = launch_fwd_persist_t<T, 2, 32>(a, nwg, lds, st);
+    else e = launch_fwd_persist_t<T, 2, 64>(a, nwg, lds, st);
+    if (kid_timer_on && e == hipSuccess) hipEventRecord(e1, st);
+    return e;
+}
+
+template hipError_t launch_fwd_persist<float>(PFwdArgs&, int, hipStream_t, int, hipEvent_t, hipEvent_t);
+template hipError_t launch_fwd_persist<bf16>(PFwdArgs&, int, hipStream_t, int, hipEvent_t, hipEvent_t);
+
+}  // namespace lsd

@@ -20,6 +20,7 @@ struct Plan {
     int MGc;              // number of 64-row groups of the batch
     int sites, kmax, kin_max;
     int ts;               // time splits of the weight-gradient kernel
+    int HP;               // H rounded up to 8 (row pitch of the h exchange buffer)
 
     // mask buffer
     size_t m_mask, m_keep, m_pos, m_count, m_drop, m_dcount, m_kseg, m_dseg, m_total;
@@ -34,6 +35,7 @@ struct Plan {
     // workspace
     size_t w_gx, w_hrec;                        // forward
     size_t w_da, w_daT, w_dbpart, w_dc, w_dhc, w_dxc, w_wpart;  // backward
+    size_t w_sync;                              // barrier counters and error flag
     size_t w_loss, w_total;
 
     int kin(int l) const { return l == 0 ? I : D * H; }

@@ -140,3 +140,34 @@ def test_mse_kernel_matches_oracle():
     loss, dy = lstm.loss_mse(y, wl.target, wl.lengths)
     assert abs(s.loss.item() - loss) / loss < 1e-5
     assert np.allclose(s.dy.cpu().numpy(), dy, rtol=1e-5, atol=1e-9)
+
+
+@pytest.mark.parametrize("name,mode", [("lm_medium", "nrrh"), ("tagger", "nr"), ("tiny", "nrrh_dense"),
+                                       ("seq2seq_enc", "nrrh")])
+def test_persistent_and_per_step_paths_agree(name, mode, monkeypatch):
+    """The persistent recurrent kernels and the per-step kernels give the same
+    step (to the bf16 bar), and the persistent kernels really run."""
+    from paper_2106_12089_amd import binding as B_
+    from paper_2106_12089_amd.session import Session
+    from tests._parity import mode_rates
+    cfg = workloads.get_config(name)
+    wl = workloads.make_workload(cfg)
+    p = cfg.p_values[0]
+    p_nr, p_rh, compact = mode_rates(cfg, mode, p)
+    say(f"[gpu] persistent vs per-step {name} {mode}")
+    outs = []
+    for flag in ("1", "0"):
+        monkeypatch.setenv("LSTM_SD_PERSIST", flag)
+        s = Session(wl, p_nr, p_rh, compact)
+        s.masks(cfg.mask_seed, 2)
+        B_.lstm_sd_kernel_timer_start("fwd_persist")
+        s.forward()
+        _, n = B_.lstm_sd_kernel_timer_stop()
+        assert n == (cfg.num_layers if flag == "1" else 0)
+        s.loss_grad()
+        s.backward()
+        torch.cuda.synchronize()
+        outs.append(s.outputs())
+    errs = compare(outs[0], outs[1])
+    assert max(errs.values()) <= TOL[cfg.dtype], errs
+    assert np.isfinite(outs[0]["hT"]).all()
