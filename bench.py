@@ -33,7 +33,7 @@ WORKLOAD = "lm_medium"
 METRIC = "LSTM fwd+BPTT step time & eff. TFLOP/s; speedup vs dense at p=0.5"
 PEAK_HBM_GBS = 8000.0
 PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
-KERNELS = ("fwd_persist", "step", "bwd", "wgrad", "fx", "dx")
+KERNELS = ("fwd_persist", "step", "bwd_persist", "bwd", "wgrad", "fx", "dx")
 KERNEL_SRC = os.path.join(ROOT, "paper_2106_12089_amd", "csrc", "kernels.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
@@ -92,6 +92,16 @@ def kernel_work(kind, counts, cfg):
                 by += H * G * e                                        # U slice, read once per launch
                 by += T * B * (G * 4 + G * 4 + H * 4 + 2 * H * e)      # gx, gates, c, h^T + exchange
                 by += T * B * H * (4 if l == L - 1 else 2 * e) + B * H * 16
+        return fl, by, L
+    if kind == "bwd_persist":               # one launch per layer runs every BPTT step (both directions)
+        for l in range(L):
+            for d in range(D):
+                nh = np.asarray(counts[L + l * D + d], dtype=np.float64)
+                fl += float(np.sum(2 * B * G * nh))
+                by += H * G * e                                        # U rows, read once per launch
+                by += T * B * G * e                                    # DA of each step, read once
+                by += T * B * H * (16 + 4 + 4 + 4 + 8 * e)             # gates, c, c_prev, dy; DA + DA^T
+                by += B * H * 16
         return fl, by, L
     if kind == "bwd":                       # T pointwise steps + one final pass per layer
         for l in range(L):
@@ -243,7 +253,8 @@ def cpu_baseline(wl, p_nr, p_rh, budget_s=12.0):
                 ms_per_step=round(t_tot / n * 1e3, 3))
 
 
-KERNEL_SYMBOLS = {"fwd_persist": "lsd::k_fwd_persist<", "step": "lsd::k_step<", "bwd": "lsd::k_bwd<",
+KERNEL_SYMBOLS = {"fwd_persist": "lsd::k_fwd_persist<", "step": "lsd::k_step<", "bwd_persist": "lsd::k_bwd_persist<",
+                  "bwd": "lsd::k_bwd<",
                   "wgrad": "lsd::k_wgrad<",
                   "fx": "lsd::k_fx<", "dx": "lsd::k_dx<"}
 

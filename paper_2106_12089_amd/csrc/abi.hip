@@ -35,6 +35,9 @@ bool timer_pair(int kid, hipEvent_t* e0, hipEvent_t* e1);
 template <typename T>
 hipError_t launch_fwd_persist(PFwdArgs& a, int D, hipStream_t st, int timer_on, hipEvent_t e0, hipEvent_t e1);
 constexpr int KID_FWDP_ = 7;
+constexpr int KID_BWDP_ = 8;
+template <typename T>
+hipError_t launch_bwd_persist(PBwdArgs& a, int D, hipStream_t st, int timer_on, hipEvent_t e0, hipEvent_t e1);
 int kernel_timer_start(const char* name);
 int kernel_timer_stop(double* total_ms, int64_t* launches);
 
@@ -339,8 +342,47 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
                         dhc, dcs, (long)D * B * H, st);
         float* dxc_above = (float*)(W + P.w_dxc) + (size_t)((l + 1) & 1) * T * B * P.kin_max;
         float* dxc_here = (float*)(W + P.w_dxc) + (size_t)(l & 1) * T * B * P.kin_max;
+        bool persistent_done = false;
+        if (use_persistent()) {
+            PBwdArgs pa;
+            memset(&pa, 0, sizeof(pa));
+            pa.lengths = lengths;
+            pa.bar = (unsigned*)(W + P.w_sync);
+            pa.err = (int*)(W + P.w_sync + 4096);
+            pa.timeout = barrier_timeout_ticks();
+            pa.B = B; pa.H = H; pa.T = T; pa.BP = BP; pa.ldy = D * H;
+            pa.lddx = l + 1 < L ? P.kin(l + 1) : 0;
+            pa.kmax = P.kmax; pa.dense = !P.compact; pa.mgc = P.MGc; pa.s = P.s_rh;
+            for (int d = 0; d < D; ++d) {
+                const int k = l * D + d;
+                const char* rd = R + P.rdir(l, d);
+                PBwdDir& pd = pa.d[d];
+                pd.U = w->U[k];
+                pd.rh = site_view(P, mbuf, P.site_rh(l, d));
+                pd.gates = (const float*)(rd + P.r_gates);
+                pd.cres = (const float*)(rd + P.r_c);
+                pd.c0 = c0 + (size_t)k * B * H;
+                if (l == L - 1) {
+                    pd.dy = dy + d * H;
+                } else {
+                    pd.dxc = dxc_above;
+                    pd.dxpos = site_view(P, mbuf, P.site_nr(l + 1)).pos + d * H;
+                }
+                pd.dhT = dhT ? dhT + (size_t)k * B * H : nullptr;
+                pd.dcT = dcT ? dcT + (size_t)k * B * H : nullptr;
+                pd.da = W + P.w_da + (size_t)d * T * B * G * es;
+                pd.daT = W + P.w_daT + (size_t)d * T * G * BP * es;
+                pd.dbpart = (float*)(W + P.w_dbpart) + (size_t)d * T * P.MGc * G;
+                pd.dh0 = dh0 + (size_t)k * B * H;
+                pd.dc0 = dc0 + (size_t)k * B * H;
+            }
+            hipEvent_t e0 = nullptr, e1 = nullptr;
+            const bool timed = timer_pair(KID_BWDP_, &e0, &e1);
+            if (launch_bwd_persist<E>(pa, D, st, timed, e0, e1) == hipSuccess) persistent_done = true;
+            else (void)hipGetLastError();     // does not fit: per-step kernels below
+        }
         // T pointwise steps plus one final pass (recurrent gradient of h0)
-        for (int s = 0; s <= T; ++s) {
+        for (int s = 0; s <= T && !persistent_done; ++s) {
             const bool final_pass = s == T;
             BwdArgs a;
             memset(&a, 0, sizeof(a));

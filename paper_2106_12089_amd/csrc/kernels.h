@@ -174,4 +174,33 @@ struct PFwdArgs {
     float s;
 };
 
+// Persistent BPTT of one layer (both directions): one cooperative launch
+// runs all T backward steps and the final pass that forms dh0/dc0.
+struct PBwdDir {
+    const void* U;                      // [H][4H]
+    SiteView rh;                        // RH site of (l, d)
+    const float* gates;                 // [T][B][4H]
+    const float* cres;                  // [T][B][H]
+    const float* c0;                    // [B][H]
+    const float* dy;                    // top layer: dy + d*H (rows ld ldy, t stride B*ldy), or null
+    const float* dxc;                   // inner layer: compacted dx of the layer above [T][B][lddx], or null
+    const int32_t* dxpos;               // NR pos of the layer above, + d*H (t stride kmax)
+    const float* dhT;                   // [B][H] or null
+    const float* dcT;                   // [B][H] or null
+    void* da;                           // [T][B][4H] (exchange; also read by later kernels)
+    void* daT;                          // [T][4H][BP]
+    float* dbpart;                      // [T][MGc][4H]
+    float* dh0;                         // [B][H]
+    float* dc0;                         // [B][H]
+};
+struct PBwdArgs {
+    PBwdDir d[2];
+    const int32_t* lengths;
+    unsigned* bar;
+    int* err;
+    long long timeout;
+    int B, H, T, BP, ldy, lddx, kmax, dense, ntiles, mgroups, mgc;
+    float s;
+};
+
 }  // namespace lsd

@@ -81,6 +81,35 @@ __device__ __forceinline__ void xload8(const float* p, float* o) {
     }
 }
 
+// coherent load of 4 consecutive elements (8-byte aligned bf16 / 16-byte f32)
+__device__ __forceinline__ void xload4(const bf16* p, bf16* o) {
+    const unsigned long long v = __hip_atomic_load((const unsigned long long*)p, __ATOMIC_RELAXED,
+                                                   __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] = (bf16)((v >> (16 * e)) & 0xffffu);
+}
+__device__ __forceinline__ void xload4(const float* p, float* o) {
+    const unsigned long long* q = (const unsigned long long*)p;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const unsigned long long v = __hip_atomic_load(q + h, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        o[2 * h] = __uint_as_float((uint32_t)v);
+        o[2 * h + 1] = __uint_as_float((uint32_t)(v >> 32));
+    }
+}
+// 8 consecutive elements from LDS (16-byte aligned)
+__device__ __forceinline__ void lds8(const bf16* p, bf16* o) {
+    const uint4 v = *(const uint4*)p;
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] = (bf16)((w[e >> 1] >> (16 * (e & 1))) & 0xffffu);
+}
+__device__ __forceinline__ void lds8(const float* p, float* o) {
+    const float4 v0 = *(const float4*)p, v1 = *(const float4*)(p + 4);
+    o[0] = v0.x; o[1] = v0.y; o[2] = v0.z; o[3] = v0.w;
+    o[4] = v1.x; o[5] = v1.y; o[6] = v1.z; o[7] = v1.w;
+}
+
 // ---------------------------------------------------------------------------
 // Persistent forward recurrence (Eq. 1-6) of one layer, both directions.
 // Workgroup w -> (direction, unit tile, row group).  A unit tile is 4*NT
@@ -317,6 +346,248 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// Persistent BPTT (Eq. 7-10) of one layer, both directions.
+// Workgroup w -> (direction, unit tile of UB units, row group of MG rows).
+// 1024 threads = 16 waves.  Per step: the recurrent gradient of the tile's
+// units from DA of the step processed before (Eq. 10; contraction over 4H
+// split over the waves; skipped when every unit of the tile was dropped),
+// then the pointwise backward (Eq. 7-9) with the dc and pass-through
+// carries held in registers.  Dynamic LDS: U rows [UB][GP] (dtype),
+// reduction [16][MG][16] (float).
+constexpr int PB_NW = 16;
+
+template <typename T, int UB, int MG>
+__global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
+    constexpr int MT = MG / 16, NW = PB_NW, NTH = 64 * NW;
+    constexpr int PPT = (MG * UB + NTH - 1) / NTH;
+    constexpr int MAXC = (MT <= 2 ? 6 : 2) / (sizeof(T) == 4 ? 2 : 1);   // 128 VGPRs at 1024 threads
+    extern __shared__ __align__(16) char smem[];
+    const int H = a.H, G = 4 * H, B = a.B, T_ = a.T;
+    const int GP = (G + 31) / 32 * 32 + 8;       // row pitch; zero past 4H up to the last chunk
+    T* Ur = (T*)smem;                                            // [UB][GP]
+    float* red = (float*)(smem + (((size_t)UB * GP * sizeof(T) + 15) & ~(size_t)15));
+
+    const int nslot = a.ntiles * a.mgroups;
+    const int d = blockIdx.x / nslot, rem = blockIdx.x % nslot;
+    const int tile = rem / a.mgroups, mg = rem % a.mgroups;
+    const PBwdDir& D = a.d[d];
+    const int u0 = tile * UB, m0 = mg * MG;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int g8 = 8 * (lane >> 4);
+    unsigned* bar = a.bar + d;
+
+    // rows of U for the tile's units -> LDS (zero past 4H and past H)
+    {
+        const T* U = (const T*)D.U;
+        for (int i = tid; i < UB * GP; i += NTH) {
+            const int r = i / GP, n = i % GP;
+            const int u = u0 + r;
+            Ur[i] = (u < H && n < G) ? U[(size_t)u * G + n] : zero_val<T>();
+        }
+    }
+    // this thread's (row, unit) pairs and their carries
+    float dcs[PPT], dhc[PPT];
+    int pb[PPT], pu[PPT];
+#pragma unroll
+    for (int q = 0; q < PPT; ++q) {
+        const int p = tid + NTH * q;
+        pb[q] = (p < MG * UB) ? m0 + p / UB : B;
+        pu[q] = u0 + p % UB;
+        const bool ok = pb[q] < B && pu[q] < H;
+        dhc[q] = (ok && D.dhT) ? D.dhT[(size_t)pb[q] * H + pu[q]] : 0.f;
+        dcs[q] = (ok && D.dcT) ? D.dcT[(size_t)pb[q] * H + pu[q]] : 0.f;
+    }
+    // per-step inputs (independent of the recurrence), loaded one step ahead
+    float gt4[PPT][4], ctv[PPT], cpv[PPT], dyv[PPT];
+    bool vld[PPT];
+    int tile_kept = 0;                  // any unit of the tile kept at the step processed before
+    auto prefetch = [&](int s) {
+        const int t = d == 0 ? T_ - 1 - s : s;
+        const int tp = d == 0 ? t - 1 : t + 1;            // forward predecessor of t
+#pragma unroll
+        for (int q = 0; q < PPT; ++q) {
+            const int b = pb[q], u = pu[q];
+            const bool ok = b < B && u < H;
+            vld[q] = ok && (a.lengths == nullptr || t < a.lengths[b]);
+            const float* gr = D.gates + ((size_t)t * B + b) * G;
+#pragma unroll
+            for (int g = 0; g < 4; ++g) gt4[q][g] = ok ? gr[g * H + u] : 0.f;
+            ctv[q] = ok ? D.cres[((size_t)t * B + b) * H + u] : 0.f;
+            cpv[q] = !ok ? 0.f : (s == T_ - 1 ? D.c0[(size_t)b * H + u] : D.cres[((size_t)tp * B + b) * H + u]);
+            float v = 0.f;
+            if (vld[q]) {
+                if (D.dy) v = D.dy[((size_t)t * B + b) * a.ldy + u];
+                else if (D.dxc) {
+                    const int p = D.dxpos[(size_t)t * a.kmax + u];
+                    if (p >= 0) v = D.dxc[((size_t)t * B + b) * a.lddx + p];
+                }
+            }
+            dyv[q] = v;
+        }
+    };
+    // whether the tile has a unit kept at step tn (the recurrent gradient of
+    // a dropped unit is exactly zero)
+    auto tile_any_kept = [&](int tn) {
+        __shared__ int any;
+        if (tid == 0) any = 0;
+        __syncthreads();
+        if (tid < UB) {
+            const int u = u0 + tid;
+            if (u < H && D.rh.mask[(size_t)tn * a.kmax + u]) any = 1;
+        }
+        __syncthreads();
+        return any;
+    };
+
+    // the recurrent gradient of the tile's units from DA of step tn into red
+    auto recurrent_product = [&](int tn) {
+        const T* DA = (const T*)D.da + (size_t)tn * B * G;
+        f32x4_t acc[MT];
+#pragma unroll
+        for (int i = 0; i < MT; ++i) acc[i] = f32x4_t{0, 0, 0, 0};
+        const int nch = (G + 31) / 32;
+        const int ul = lane & 15;
+        for (int c0 = 0; c0 < nch; c0 += NW * MAXC) {
+            Frag<T> fa[MAXC][MT];
+#pragma unroll
+            for (int i = 0; i < MAXC; ++i) {
+                const int n = 32 * (c0 + w + NW * i) + g8;
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) {
+                    const int row = m0 + mt * 16 + (lane & 15);
+#pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        if (row < B && n + 4 * h < G) {
+                            xload4(DA + (size_t)row * G + n + 4 * h, fa[i][mt].v + 4 * h);
+                        } else {
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) fa[i][mt].v[4 * h + e] = zero_val<T>();
+                        }
+                    }
+                }
+            }
+#pragma unroll
+            for (int i = 0; i < MAXC; ++i) {
+                const int n = 32 * (c0 + w + NW * i);
+                if (n >= G) break;
+                Frag<T> fb;
+                lds8(Ur + (size_t)ul * GP + n + g8, fb.v);                 // zero past 4H
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) mma_16x16x32(fa[i][mt], fb, acc[mt]);
+            }
+        }
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) red[(w * MG + mt * 16 + acc_row(lane, r)) * 16 + (lane & 15)] = acc[mt][r];
+        __syncthreads();
+    };
+    auto reduced = [&](int rr, int i) {
+        float v = 0.f;
+#pragma unroll
+        for (int q = 0; q < NW; ++q) v += red[(q * MG + rr) * 16 + i];
+        return v;
+    };
+
+    prefetch(0);
+    for (int s = 0; s <= T_; ++s) {
+        const bool final_pass = s == T_;
+        const int t = final_pass ? -1 : (d == 0 ? T_ - 1 - s : s);
+        const int tn = d == 0 ? T_ - s : s - 1;            // step processed just before
+        const bool has_next = s > 0;
+        int kept = 0;
+        if (has_next) {
+            kept = tile_any_kept(tn);
+            if (!grid_wait(bar, (unsigned)s * (unsigned)nslot, a.err, a.timeout)) break;
+            if (kept) recurrent_product(tn);
+        }
+        // copies of this step's inputs, then the next step's loads go out
+        float g4c[PPT][4], ctc[PPT], cpc[PPT], dyc[PPT];
+        bool vc[PPT];
+#pragma unroll
+        for (int q = 0; q < PPT; ++q) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g) g4c[q][g] = gt4[q][g];
+            ctc[q] = ctv[q]; cpc[q] = cpv[q]; dyc[q] = dyv[q]; vc[q] = vld[q];
+        }
+        if (s + 1 < T_) prefetch(s + 1);
+        float da4[PPT][4];
+#pragma unroll
+        for (int q = 0; q < PPT; ++q) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g) da4[q][g] = 0.f;
+            const int b = pb[q], u = pu[q];
+            if (b >= B || u >= H) continue;
+            float dh = dhc[q];
+            if (kept) {
+                // units dropped at step tn get no recurrent gradient (output sparsity, Eq. 10)
+                const float sc = D.rh.mask[(size_t)tn * a.kmax + u] ? a.s : 0.0f;
+                dh += sc * reduced(b - m0, u - u0);
+            }
+            if (final_pass) {
+                D.dh0[(size_t)b * H + u] = dh;
+                D.dc0[(size_t)b * H + u] = dcs[q];
+                continue;
+            }
+            if (vc[q]) {
+                dh += dyc[q];
+                const float ig = g4c[q][0], fg = g4c[q][1], gg = g4c[q][2], og = g4c[q][3];
+                const float tc = tanh_fast(ctc[q]);
+                const float dout = dh * tc;                            // Eq. 7
+                const float dc = dh * og * (1.0f - tc * tc) + dcs[q];  // Eq. 7
+                da4[q][0] = dc * gg * ig * (1.0f - ig);                // Eq. 9, sigmoid'
+                da4[q][1] = dc * cpc[q] * fg * (1.0f - fg);            // Eq. 8, sigmoid'
+                da4[q][2] = dc * ig * (1.0f - gg * gg);                // Eq. 9, tanh'
+                da4[q][3] = dout * og * (1.0f - og);                   // Eq. 7, sigmoid'
+                dcs[q] = dc * fg;                                      // Eq. 8
+                dhc[q] = 0.0f;
+            } else {
+                dhc[q] = dh;                                           // frozen row: pass through
+            }
+            T* dar = (T*)D.da + ((size_t)t * B + b) * G;
+            T* dat = (T*)D.daT + (size_t)t * G * a.BP;
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const T v = from_f32<T>(da4[q][g]);
+                xstore(dar + g * H + u, v);
+                dat[(size_t)(g * H + u) * a.BP + b] = v;
+            }
+        }
+        if (final_pass) break;
+        // bias-gradient partial over the tile's rows
+        __syncthreads();
+        float* rb = red;                                   // [MG][UB][4]
+#pragma unroll
+        for (int q = 0; q < PPT; ++q) {
+            const int p = tid + NTH * q;
+            if (p < MG * UB) {
+#pragma unroll
+                for (int g = 0; g < 4; ++g) rb[p * 4 + g] = da4[q][g];
+            }
+        }
+        __syncthreads();
+        if (tid < 4 * UB) {
+            const int i = tid >> 2, g = tid & 3, u = u0 + i;
+            if (u < H) {
+                float sum = 0.f;
+                for (int rr = 0; rr < MG; ++rr) sum += rb[(rr * UB + i) * 4 + g];
+                D.dbpart[((size_t)t * a.mgc + mg) * G + g * H + u] = sum;
+            }
+        }
+        grid_arrive(bar);
+    }
+    // a timed-out barrier poisons the input-state gradients
+    if (__hip_atomic_load(a.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
+#pragma unroll
+        for (int q = 0; q < PPT; ++q)
+            if (pb[q] < B && pu[q] < H) {
+                D.dh0[(size_t)pb[q] * H + pu[q]] = __builtin_nanf("");
+                D.dc0[(size_t)pb[q] * H + pu[q]] = __builtin_nanf("");
+            }
+    }
+}
+
 __global__ void k_zero_sync(unsigned* bar, int n, int* err) {
     for (int i = threadIdx.x; i < n; i += blockDim.x) bar[i] = 0u;
     if (threadIdx.x == 0) *err = 0;
@@ -373,5 +644,53 @@ hipError_t launch_fwd_persist(PFwdArgs& a, int D, hipStream_t st, int kid_timer_
 
 template hipError_t launch_fwd_persist<float>(PFwdArgs&, int, hipStream_t, int, hipEvent_t, hipEvent_t);
 template hipError_t launch_fwd_persist<bf16>(PFwdArgs&, int, hipStream_t, int, hipEvent_t, hipEvent_t);
+
+size_t bwd_persist_lds(int H, int UB, int MG, int esize) {
+    const size_t G = 4 * (size_t)H, GP = (G + 31) / 32 * 32 + 8;
+    return (((size_t)UB * GP * esize + 15) & ~(size_t)15) + (size_t)PB_NW * MG * 16 * 4;
+}
+
+template <typename T, int UB, int MG>
+static hipError_t launch_bwd_persist_t(const PBwdArgs& a, int nwg, size_t lds, hipStream_t st) {
+    auto fn = k_bwd_persist<T, UB, MG>;
+    hipError_t e = hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    int per_cu = 0;
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, 64 * PB_NW, lds);
+    if (e != hipSuccess) return e;
+    int dev = 0, ncu = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return hipErrorInvalidDevice;
+    if (hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return hipErrorInvalidDevice;
+    if (per_cu < 1 || nwg > per_cu * ncu) return hipErrorCooperativeLaunchTooLarge;
+    PBwdArgs arg = a;
+    void* params[] = {&arg};
+    return hipLaunchCooperativeKernel((const void*)fn, dim3(nwg), dim3(64 * PB_NW), params, (unsigned)lds, st);
+}
+
+// Launches the persistent backward layer if it fits (else returns an error
+// and nothing was launched).
+template <typename T>
+hipError_t launch_bwd_persist(PBwdArgs& a, int D, hipStream_t st, int timer_on, hipEvent_t e0, hipEvent_t e1) {
+    const int MG = a.B <= 32 ? 32 : 64;
+    a.mgroups = (a.B + MG - 1) / MG;
+    int UB = 16;
+    if (bwd_persist_lds(a.H, 16, MG, (int)sizeof(T)) > 160 * 1024) UB = 8;
+    const size_t lds = bwd_persist_lds(a.H, UB, MG, (int)sizeof(T));
+    if (lds > 160 * 1024) return hipErrorInvalidValue;
+    a.ntiles = (a.H + UB - 1) / UB;
+    const int nwg = D * a.ntiles * a.mgroups;
+    hipLaunchKernelGGL(k_zero_sync, dim3(1), dim3(64), 0, st, a.bar, 2, a.err);
+    if (timer_on) (void)hipEventRecord(e0, st);
+    hipError_t e;
+    if (UB == 16 && MG == 32) e = launch_bwd_persist_t<T, 16, 32>(a, nwg, lds, st);
+    else if (UB == 16) e = launch_bwd_persist_t<T, 16, 64>(a, nwg, lds, st);
+    else if (MG == 32) e = launch_bwd_persist_t<T, 8, 32>(a, nwg, lds, st);
+    else e = launch_bwd_persist_t<T, 8, 64>(a, nwg, lds, st);
+    if (timer_on && e == hipSuccess) (void)hipEventRecord(e1, st);
+    return e;
+}
+
+template hipError_t launch_bwd_persist<float>(PBwdArgs&, int, hipStream_t, int, hipEvent_t, hipEvent_t);
+template hipError_t launch_bwd_persist<bf16>(PBwdArgs&, int, hipStream_t, int, hipEvent_t, hipEvent_t);
 
 }  // namespace lsd

@@ -165,7 +165,10 @@ def test_persistent_and_per_step_paths_agree(name, mode, monkeypatch):
         _, n = B_.lstm_sd_kernel_timer_stop()
         assert n == (cfg.num_layers if flag == "1" else 0)
         s.loss_grad()
+        B_.lstm_sd_kernel_timer_start("bwd_persist")
         s.backward()
+        _, n = B_.lstm_sd_kernel_timer_stop()
+        assert n == (cfg.num_layers if flag == "1" else 0)
         torch.cuda.synchronize()
         outs.append(s.outputs())
     errs = compare(outs[0], outs[1])

@@ -149,7 +149,7 @@ def test_kernel_timer_counts_launches():
     s.masks(cfg.mask_seed, 0)
     torch.cuda.synchronize()
     for name, per_step in (("fwd_persist", cfg.num_layers), ("step", 0),
-                           ("bwd", cfg.num_layers * (cfg.seq_len + 1)),
+                           ("bwd_persist", cfg.num_layers), ("bwd", 0),
                            ("wgrad", 2 * cfg.num_layers * cfg.num_dirs)):
         B_.lstm_sd_kernel_timer_start(name)
         for _ in range(3):
