@@ -80,6 +80,9 @@ int make_plan(const lstm_sd_dims* d, Plan* p, const char** why) {
     q.G = 4 * q.H;
     q.BP = (q.B + 31) / 32 * 32;
     q.HP = (q.H + 7) / 8 * 8;
+    q.mtiles = (q.B + 15) / 16;
+    q.das = (size_t)q.B * q.G;               // DA block per step: row-major [B][4H]
+    q.hxs = (size_t)((q.H + 31) / 32) * q.mtiles * 512;
     q.MGc = (q.B + 63) / 64;
     q.sites = q.L + q.L * q.D;
     q.kin_max = q.L > 1 ? (q.I > q.D * q.H ? q.I : q.D * q.H) : q.I;
@@ -123,9 +126,10 @@ int make_plan(const lstm_sd_dims* d, Plan* p, const char** why) {
     off = 0;
     q.w_gx = off;   off = align_up(off + D * T * B * G * 4, A);
     q.w_hrec = off; off = align_up(off + D * 2 * B * (size_t)q.HP * es, A);
+    q.w_hx = off;   off = align_up(off + D * 2 * (size_t)q.hxs * es, A);
     const size_t fwd = off;
     off = 0;
-    q.w_da = off;     off = align_up(off + D * T * B * G * es, A);
+    q.w_da = off;     off = align_up(off + D * T * (size_t)q.das * es, A);
     q.w_daT = off;    off = align_up(off + D * T * G * BP * es, A);
     q.w_dbpart = off; off = align_up(off + D * T * (size_t)q.MGc * G * 4, A);
     q.w_dc = off;     off = align_up(off + D * B * H * 4, A);
@@ -258,6 +262,7 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
             pa.err = (int*)(W + P.w_sync + 4096);
             pa.timeout = barrier_timeout_ticks();
             pa.B = B; pa.H = H; pa.HP = P.HP; pa.T = T; pa.BP = BP; pa.ldy = D * H; pa.dense = !P.compact;
+            pa.mtiles = P.mtiles;
             pa.s = P.s_rh;
             for (int d = 0; d < D; ++d) {
                 const int k = l * D + d;
@@ -271,7 +276,7 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
                 pd.gates = (float*)(rd + P.r_gates);
                 pd.cres = (float*)(rd + P.r_c);
                 pd.hrecT = rd + P.r_hrecT;
-                pd.hx = W + P.w_hrec + (size_t)d * 2 * B * P.HP * es;
+                pd.hx = W + P.w_hx + (size_t)d * 2 * P.hxs * es;
                 pd.hT = hT + (size_t)k * B * H;
                 pd.cT = cT + (size_t)k * B * H;
                 if (l == L - 1) {
@@ -352,7 +357,7 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
             pa.timeout = barrier_timeout_ticks();
             pa.B = B; pa.H = H; pa.T = T; pa.BP = BP; pa.ldy = D * H;
             pa.lddx = l + 1 < L ? P.kin(l + 1) : 0;
-            pa.kmax = P.kmax; pa.dense = !P.compact; pa.mgc = P.MGc; pa.s = P.s_rh;
+            pa.kmax = P.kmax; pa.dense = !P.compact; pa.mgc = P.MGc; pa.mtiles = P.mtiles; pa.s = P.s_rh;
             for (int d = 0; d < D; ++d) {
                 const int k = l * D + d;
                 const char* rd = R + P.rdir(l, d);
@@ -370,7 +375,7 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
                 }
                 pd.dhT = dhT ? dhT + (size_t)k * B * H : nullptr;
                 pd.dcT = dcT ? dcT + (size_t)k * B * H : nullptr;
-                pd.da = W + P.w_da + (size_t)d * T * B * G * es;
+                pd.da = W + P.w_da + (size_t)d * T * P.das * es;
                 pd.daT = W + P.w_daT + (size_t)d * T * G * BP * es;
                 pd.dbpart = (float*)(W + P.w_dbpart) + (size_t)d * T * P.MGc * G;
                 pd.dh0 = dh0 + (size_t)k * B * H;
@@ -388,7 +393,7 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
             memset(&a, 0, sizeof(a));
             a.lengths = lengths; a.B = B; a.H = H; a.BP = BP; a.ldy = D * H;
             a.lddx = l + 1 < L ? P.kin(l + 1) : 0;
-            a.tps = tps_h; a.has_next = s > 0; a.final_pass = final_pass; a.dense = !P.compact; a.s = P.s_rh;
+            a.tps = tps_h; a.has_next = s > 0; a.mtiles = P.mtiles; a.final_pass = final_pass; a.dense = !P.compact; a.s = P.s_rh;
             for (int d = 0; d < D; ++d) {
                 const int k = l * D + d;
                 const int t = final_pass ? -1 : (d == 0 ? T - 1 - s : s);   // BP order: reverse of FP
@@ -402,7 +407,7 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
                 bd.dhc = dhc + (size_t)d * B * H;
                 bd.dcs = dcs + (size_t)d * B * H;
                 if (s > 0) {
-                    bd.da_next = W + P.w_da + ((size_t)d * T + tn) * B * G * es;
+                    bd.da_next = W + P.w_da + ((size_t)d * T + tn) * P.das * es;
                     bd.nmask = rv.mask + (size_t)tn * P.kmax;
                     bd.nkeep = rv.keep + (size_t)tn * P.kmax;
                     bd.ncount = rv.count + tn;
@@ -426,7 +431,7 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
                     bd.dxc = dxc_above + (size_t)t * B * a.lddx;
                     bd.dxpos = sv.pos + (size_t)t * P.kmax + d * H;
                 }
-                bd.da = W + P.w_da + ((size_t)d * T + t) * B * G * es;
+                bd.da = W + P.w_da + ((size_t)d * T + t) * P.das * es;
                 bd.daT = W + P.w_daT + ((size_t)d * T + t) * G * BP * es;
                 bd.dbpart = (float*)(W + P.w_dbpart) + ((size_t)d * T + t) * P.MGc * G;
             }
@@ -437,11 +442,11 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
             DxArgs a;
             memset(&a, 0, sizeof(a));
             for (int d = 0; d < D; ++d) {
-                a.da[d] = W + P.w_da + (size_t)d * T * B * G * es;
+                a.da[d] = W + P.w_da + (size_t)d * T * P.das * es;
                 a.W[d] = w->W[l * D + d];
             }
             a.site = nv; a.out = dxc_here; a.D = D; a.B = B; a.G = G; a.ldo = kin; a.T = T;
-            a.K = kin; a.tps = ((kin + 7) / 8 + 15) / 16;
+            a.K = kin; a.tps = ((kin + 7) / 8 + 15) / 16; a.mtiles = P.mtiles;
             a.dense = !P.compact; a.s = P.s_nr;
             launch_dx<E>(a, kin, st);
             if (l == 0) launch_expand(dxc_here, kin, nv, dx, B, kin, T, st);

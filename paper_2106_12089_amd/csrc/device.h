@@ -53,6 +53,21 @@ __device__ __forceinline__ void mma_16x16x32(const Frag<float>& a, const Frag<fl
     for (int e = 0; e < 8; ++e) c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.v[e], b.v[e], c, 0, 0, 0);
 }
 
+// Fragment-major layout of a [rows][cols] matrix whose rows are the M side
+// of an MFMA product: 32-column chunks x 16-row tiles x 64 lanes x 8
+// elements.  Element (row, col) of a matrix with `mtiles` 16-row tiles sits
+// at frag_off(row, col, mtiles); the A fragment of (chunk c, tile mt) is the
+// 16 bytes of lane l at frag_lane_off(c, mt, l, mtiles), and a wave reads it
+// as one contiguous 1 KB block.  A buffer holds ceil(cols/32)*mtiles*512
+// elements.
+__device__ __forceinline__ size_t frag_lane_off(int c, int mt, int lane, int mtiles) {
+    return (((size_t)c * mtiles + mt) * 64 + lane) << 3;
+}
+__device__ __forceinline__ size_t frag_off(int row, int col, int mtiles) {
+    const int k = col & 31;
+    return frag_lane_off(col >> 5, row >> 4, (k >> 3) * 16 + (row & 15), mtiles) + (k & 7);
+}
+
 // Output element r (0..3) of lane l of a 16x16 accumulator sits at
 // row 4*(l/16) + r, column l%16.
 __device__ __forceinline__ int acc_row(int lane, int r) { return 4 * (lane >> 4) + r; }

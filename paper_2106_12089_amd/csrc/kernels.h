@@ -88,7 +88,7 @@ struct StepArgs {
 // the pointwise backward (Eq. 7-9 and activation derivatives) at t.
 struct BwdDir {
     // recurrent gradient from the previously processed step (has_next)
-    const void* da_next;                // [B][G] dtype
+    const void* da_next;                // [B][G] DA of that step (dtype)
     const uint8_t* nmask;               // RH mask row of that step
     const int32_t* nkeep;               // kept units of that step
     const int32_t* ncount;
@@ -106,7 +106,7 @@ struct BwdDir {
     const int32_t* dxpos;               // NR pos row of the layer above at t, + d*H
     float* dhc;                         // [B][H] pass-through carry, in place
     float* dcs;                         // [B][H] cell-gradient carry, in place
-    void* da;                           // [B][G] dtype (row-major)
+    void* da;                           // [B][G] DA_t (dtype)
     void* daT;                          // [G][BP] dtype (transposed)
     float* dbpart;                      // [MG][G] for this t
     float* dh0;                         // final pass: [B][H]
@@ -117,6 +117,7 @@ struct BwdArgs {
     BwdDir d[2];
     const int32_t* lengths;
     int B, H, BP, ldy, lddx, tps, has_next, final_pass, dense;   // tps: tiles per XCD slice
+    int mtiles;                         // 16-row tiles of the batch (fragment-major DA)
     float s;
 };
 
@@ -127,7 +128,7 @@ struct DxArgs {
     const void* W[2];                   // [K][G]
     SiteView site;
     float* out;                         // [T][B][ldo]
-    int D, B, G, ldo, T, K, tps, dense;
+    int D, B, G, ldo, T, K, tps, dense, mtiles;
     float s;
 };
 
@@ -157,7 +158,7 @@ struct PFwdDir {
     float* gates;                       // [T][B][4H]
     float* cres;                        // [T][B][H]
     void* hrecT;                        // [T][H][BP]
-    void* hx;                           // [2][B][HP] exchange: h_t compacted by the next step's keep list
+    void* hx;                           // [2] fragment-major slots: h_t compacted by the next step's keep list
     float* hT;                          // [B][H]
     float* cT;                          // [B][H]
     float* y;                           // top layer: y + d*H (rows ld ldy, t stride B*ldy), or null
@@ -170,7 +171,7 @@ struct PFwdArgs {
     unsigned* bar;                      // [2] barrier counters (zeroed before launch)
     int* err;                           // barrier time-out flag
     long long timeout;                  // wall-clock ticks
-    int B, H, HP, T, BP, ldy, dense, ntiles, mgroups;
+    int B, H, HP, T, BP, ldy, dense, ntiles, mgroups, mtiles;
     float s;
 };
 
@@ -187,7 +188,7 @@ struct PBwdDir {
     const int32_t* dxpos;               // NR pos of the layer above, + d*H (t stride kmax)
     const float* dhT;                   // [B][H] or null
     const float* dcT;                   // [B][H] or null
-    void* da;                           // [T][B][4H] (exchange; also read by later kernels)
+    void* da;                           // [T][B][4H] (exchange; also read by the dX product)
     void* daT;                          // [T][4H][BP]
     float* dbpart;                      // [T][MGc][4H]
     float* dh0;                         // [B][H]
@@ -199,7 +200,7 @@ struct PBwdArgs {
     unsigned* bar;
     int* err;
     long long timeout;
-    int B, H, T, BP, ldy, lddx, kmax, dense, ntiles, mgroups, mgc;
+    int B, H, T, BP, ldy, lddx, kmax, dense, ntiles, mgroups, mgc, mtiles;
     float s;
 };
 

@@ -38,7 +38,6 @@ template <typename T>
 __device__ __forceinline__ void zero4(T* o) {
     o[0] = o[1] = o[2] = o[3] = zero_val<T>();
 }
-
 // Workgroups are dealt to the 8 XCDs round-robin (linear workgroup id i runs
 // on XCD i % 8).  xcd_tile maps the x index of a grid whose x size is a
 // multiple of 8 to a logical tile so that every XCD owns one contiguous range

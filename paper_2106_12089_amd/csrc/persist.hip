@@ -19,10 +19,11 @@ namespace lsd {
 // Cross-workgroup exchange and grid barrier.
 //
 // Values that other workgroups read during the same launch (the compacted
-// h_t, the backward DA_t) are written and read with relaxed agent-scope
-// atomic accesses: on gfx950 these are ordinary loads and stores carrying the
-// device-coherence bit, so no L2 writeback or invalidate of unrelated data is
-// needed.  A workgroup signals the end of a step by waiting for its own
+// h_t, the backward DA_t) are written with relaxed agent-scope atomic stores
+// (ordinary stores carrying the device-coherence bit, written through to the
+// coherent level), so a producer never writes back its L2.  A consumer
+// performs one agent-scope acquire fence after the barrier (an invalidate of
+// its caches) and then reads with plain wide loads at full cache bandwidth.  A workgroup signals the end of a step by waiting for its own
 // stores to complete, synchronising its threads and adding 1 to the
 // direction's counter; a waiting workgroup spins (thread 0) until the counter
 // reaches the target.  The spin is bounded by wall-clock time; on time-out,
@@ -49,6 +50,9 @@ __device__ __forceinline__ bool grid_wait(unsigned* bar, unsigned target, int* e
                 break;
             }
         }
+        // acquire: invalidate this CU's L1 and the XCD's L2 (no writeback), so
+        // the plain loads that follow fetch what other workgroups published
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
         ok = good;
     }
     __syncthreads();
@@ -97,7 +101,17 @@ __device__ __forceinline__ void xload4(const float* p, float* o) {
         o[2 * h + 1] = __uint_as_float((uint32_t)(v >> 32));
     }
 }
-// 8 consecutive elements from LDS (16-byte aligned)
+// 4 consecutive elements, plain load (8-byte aligned bf16 / 16-byte f32)
+__device__ __forceinline__ void ld4g(const bf16* p, bf16* o) {
+    const uint2 v = *(const uint2*)p;
+    o[0] = (bf16)(v.x & 0xffffu); o[1] = (bf16)(v.x >> 16);
+    o[2] = (bf16)(v.y & 0xffffu); o[3] = (bf16)(v.y >> 16);
+}
+__device__ __forceinline__ void ld4g(const float* p, float* o) {
+    const float4 v = *(const float4*)p;
+    o[0] = v.x; o[1] = v.y; o[2] = v.z; o[3] = v.w;
+}
+// 8 consecutive elements (LDS or global, 16-byte aligned)
 __device__ __forceinline__ void lds8(const bf16* p, bf16* o) {
     const uint4 v = *(const uint4*)p;
     const uint32_t w[4] = {v.x, v.y, v.z, v.w};
@@ -128,7 +142,7 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
     constexpr int PPT = (MG * UPW + NTH - 1) / NTH;
     constexpr int MAXC = MT <= 2 ? 6 : 3;       // chunks per wave per round (registers)
     extern __shared__ __align__(16) char smem[];
-    const int H = a.H, G = 4 * H, B = a.B, T_ = a.T, HP = a.HP;
+    const int H = a.H, G = 4 * H, B = a.B, T_ = a.T;
     T* Us = (T*)smem;
     int16_t* kidx = (int16_t*)(smem + (((size_t)H * UP * sizeof(T) + 15) & ~(size_t)15));
     float* red = (float*)((char*)kidx + (((size_t)(H + 32) * 2 + 15) & ~(size_t)15));
@@ -216,7 +230,7 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
             if (pb[q] < B && pu[q] < H) {
                 const int pp = pos[pu[q]];
                 if (pp >= 0)
-                    xstore(hx0 + (size_t)pb[q] * HP + pp,
+                    xstore(hx0 + frag_off(pb[q], pp, a.mtiles),
                            (a.dense && !msk[pu[q]]) ? zero_val<T>() : from_f32<T>(hreg[q]));
             }
         }
@@ -229,7 +243,8 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
         // ---- wait for h_{t-1} of every workgroup of this direction
         commit_kidx();
         if (!grid_wait(bar, (unsigned)(s + 1) * (unsigned)nslot, a.err, a.timeout)) break;
-        const T* hc = (const T*)D.hx + (size_t)(s & 1) * B * HP;
+        const size_t hxs = (size_t)((H + 31) / 32) * a.mtiles * 512;     // elements per slot
+        const T* hc = (const T*)D.hx + (size_t)(s & 1) * hxs;
         f32x4_t acc[MT][NT];
 #pragma unroll
         for (int i = 0; i < MT; ++i)
@@ -241,12 +256,12 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
             Frag<T> fa[MAXC][MT];
 #pragma unroll
             for (int i = 0; i < MAXC; ++i) {
-                const int kc = 32 * (c0 + w + NW * i);
-                const bool jin = kc + g8 < cnt;
+                const int c = c0 + w + NW * i;
+                const bool jin = 32 * c + g8 < cnt;
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) {
                     const int row = m0 + mt * 16 + (lane & 15);
-                    if (row < B && jin) xload8(hc + (size_t)row * HP + kc + g8, fa[i][mt].v);
+                    if (row < B && jin) lds8(hc + frag_lane_off(c, m0 / 16 + mt, lane, a.mtiles), fa[i][mt].v);
                     else {
 #pragma unroll
                         for (int e = 0; e < 8; ++e) fa[i][mt].v[e] = zero_val<T>();
@@ -297,7 +312,7 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
             pnc[q] = pn[q]; mnc[q] = mn[q]; vc[q] = valid[q];
         }
         if (s + 1 < T_) prefetch(s + 1);
-        T* hxn = (T*)D.hx + (size_t)((s + 1) & 1) * B * HP;
+        T* hxn = (T*)D.hx + (size_t)((s + 1) & 1) * hxs;
 #pragma unroll
         for (int q = 0; q < PPT; ++q) {
             const int b = pb[q], u = pu[q];
@@ -320,7 +335,7 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
             const float cn = fg * cp + ig * gg;
             const float hn = og * tanh_fast(cn);
             const T hv = from_f32<T>(vc[q] ? hn : hreg[q]);
-            if (pnc[q] >= 0) xstore(hxn + (size_t)b * HP + pnc[q], (a.dense && !mnc[q]) ? zero_val<T>() : hv);
+            if (pnc[q] >= 0) xstore(hxn + frag_off(b, pnc[q], a.mtiles), (a.dense && !mnc[q]) ? zero_val<T>() : hv);
             float* gt = D.gates + ((size_t)t * B + b) * G;
             gt[u] = ig; gt[H + u] = fg; gt[2 * H + u] = gg; gt[3 * H + u] = og;
             D.cres[((size_t)t * B + b) * H + u] = vc[q] ? cn : cp;
@@ -458,9 +473,8 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
                     const int row = m0 + mt * 16 + (lane & 15);
 #pragma unroll
                     for (int h = 0; h < 2; ++h) {
-                        if (row < B && n + 4 * h < G) {
-                            xload4(DA + (size_t)row * G + n + 4 * h, fa[i][mt].v + 4 * h);
-                        } else {
+                        if (row < B && n + 4 * h < G) ld4g(DA + (size_t)row * G + n + 4 * h, fa[i][mt].v + 4 * h);
+                        else {
 #pragma unroll
                             for (int e = 0; e < 4; ++e) fa[i][mt].v[4 * h + e] = zero_val<T>();
                         }

@@ -20,7 +20,9 @@ struct Plan {
     int MGc;              // number of 64-row groups of the batch
     int sites, kmax, kin_max;
     int ts;               // time splits of the weight-gradient kernel
-    int HP;               // H rounded up to 8 (row pitch of the h exchange buffer)
+    int HP;               // H rounded up to 8 (row pitch of the per-step h buffer)
+    int mtiles;           // 16-row tiles of the batch
+    size_t das, hxs;      // elements of one fragment-major DA block / h exchange slot
 
     // mask buffer
     size_t m_mask, m_keep, m_pos, m_count, m_drop, m_dcount, m_kseg, m_dseg, m_total;
@@ -33,7 +35,7 @@ struct Plan {
     size_t r_total;
 
     // workspace
-    size_t w_gx, w_hrec;                        // forward
+    size_t w_gx, w_hrec, w_hx;                  // forward
     size_t w_da, w_daT, w_dbpart, w_dc, w_dhc, w_dxc, w_wpart;  // backward
     size_t w_sync;                              // barrier counters and error flag
     size_t w_loss, w_total;
