@@ -92,6 +92,7 @@ int make_plan(const lstm_sd_dims* d, Plan* p, const char** why) {
         int ts = (512 + ncol - 1) / ncol;
         if (ts > 8) ts = 8;
         if (ts > q.T) ts = q.T;
+        if (ts < (q.T + 63) / 64) ts = (q.T + 63) / 64;   // at most 64 steps per workgroup
         if (ts < 1) ts = 1;
         const int tper = (q.T + ts - 1) / ts;
         q.ts = (q.T + tper - 1) / tper;
@@ -155,7 +156,7 @@ static long long barrier_timeout_ticks() {
     static long long ticks = 0;
     if (!ticks) {
         int dev = 0, khz = 0;
-        hipGetDevice(&dev);
+        if (hipGetDevice(&dev) != hipSuccess) dev = 0;
         if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess || khz <= 0) khz = 100000;
         ticks = (long long)khz * 500;
     }

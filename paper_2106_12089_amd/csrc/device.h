@@ -68,6 +68,19 @@ __device__ __forceinline__ size_t frag_off(int row, int col, int mtiles) {
     return frag_lane_off(col >> 5, row >> 4, (k >> 3) * 16 + (row & 15), mtiles) + (k & 7);
 }
 
+// 8 consecutive elements (16-byte aligned bf16, 32-byte aligned f32)
+__device__ __forceinline__ void ld8(const bf16* p, bf16* o) {
+    const uint4 v = *(const uint4*)p;
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] = (bf16)((w[e >> 1] >> (16 * (e & 1))) & 0xffffu);
+}
+__device__ __forceinline__ void ld8(const float* p, float* o) {
+    const float4 v0 = *(const float4*)p, v1 = *(const float4*)(p + 4);
+    o[0] = v0.x; o[1] = v0.y; o[2] = v0.z; o[3] = v0.w;
+    o[4] = v1.x; o[5] = v1.y; o[6] = v1.z; o[7] = v1.w;
+}
+
 // Output element r (0..3) of lane l of a 16x16 accumulator sits at
 // row 4*(l/16) + r, column l%16.
 __device__ __forceinline__ int acc_row(int lane, int r) { return 4 * (lane >> 4) + r; }

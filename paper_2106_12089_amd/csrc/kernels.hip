@@ -557,68 +557,228 @@ __global__ void __launch_bounds__(256) k_dx(DxArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Row-sparse weight gradient (Eq. 11; Sec. 3.2 WG).  grid (ceil(G/16), TS),
-// block 512, dynamic LDS K*16 floats.  A workgroup owns 16 columns of the
-// gradient for every row and the time steps [ts*tper, ts*tper + tper); at each
-// t the kept rows are processed in 16-row tiles (distinct rows per tile, so
-// waves never touch the same LDS row), and never-kept rows stay zero.
+// Row-sparse weight gradient (Eq. 11; Sec. 3.2 WG).  grid (ceil(G/16) on
+// the XCD mapping, TS), block 512 (8 waves), dynamic LDS (K+1)*WG_LD floats.
+// A workgroup owns 16 gradient columns for all K rows over the time steps
+// [ts*tper, ts*tper + tper) (tper <= 64).  Wave w owns the rows of slice w,
+// [floor(wK/8), floor((w+1)K/8)): at each t it takes the kept rows of its
+// slice (keep-list entries kseg[t][w] .. kseg[t][w+1]) in 16-row tiles,
+// multiplies them with the 16 DA^T columns and adds each tile into its rows
+// of the LDS accumulator.  No two waves touch the same LDS row, so the waves
+// run without barriers.
+//
+// The kernel is built to issue few vector-ALU instructions per MFMA: the
+// operands are fetched with buffer loads (32-bit offsets, out-of-range reads
+// return 0) into packed registers, only the padded batch entries are zeroed
+// (one AND per register), and the A rows of absent tile rows are not zeroed
+// at all: their products land in the spare LDS row K, which is never read
+// back.  Each wave loads the row indices and the DA^T fragment of t+1 while
+// t is multiplied.  All kept rows of a step are distinct, so the LDS sums
+// read every row of the step first and then write them.  Rows never kept
+// stay zero.
+constexpr int WG_LD = 17;   // LDS row stride (floats): spreads the 4 rows of a tile over the banks
 template <typename T>
+struct WgTiles { static constexpr int N = 6; };   // 16-row tiles in registers at once
+template <>
+struct WgTiles<float> { static constexpr int N = 4; };
+
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+constexpr int BUF_FLAGS = 0x00020000;             // raw 32-bit buffer resource word 3 (gfx9)
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, BUF_FLAGS);
+}
+// 8 consecutive elements of one operand row as packed dwords
+template <typename T> struct Raw8 { static constexpr int NW = 4 * (int)sizeof(T) / 2; uint32_t w[NW]; };
+
+template <typename T>
+__device__ __forceinline__ void raw_load(Raw8<T>& f, __amdgpu_buffer_rsrc_t r, uint32_t off) {
+#pragma unroll
+    for (int q = 0; q < Raw8<T>::NW / 4; ++q) {
+        const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, off + 16 * q, 0, 0);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) f.w[4 * q + e] = v[e];
+    }
+}
+// AND masks that zero the elements at batch index >= B of a fragment whose
+// first element sits at batch index b0
+template <typename T>
+__device__ __forceinline__ void pad_mask(int b0, int B, uint32_t* m) {
+    if (sizeof(T) == 2) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            m[q] = (b0 + 2 * q < B ? 0x0000ffffu : 0u) | (b0 + 2 * q + 1 < B ? 0xffff0000u : 0u);
+    } else {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) m[q] = b0 + q < B ? 0xffffffffu : 0u;
+    }
+}
+template <typename T>
+__device__ __forceinline__ void raw_and(Raw8<T>& f, const uint32_t* m) {
+#pragma unroll
+    for (int q = 0; q < Raw8<T>::NW; ++q) f.w[q] &= m[q];
+}
+__device__ __forceinline__ void raw_mma(const Raw8<bf16>& a, const Raw8<bf16>& b, f32x4_t& c) {
+    const u32x4_t av = {a.w[0], a.w[1], a.w[2], a.w[3]}, bv = {b.w[0], b.w[1], b.w[2], b.w[3]};
+    c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, av), __builtin_bit_cast(bf16x8_t, bv),
+                                                c, 0, 0, 0);
+}
+__device__ __forceinline__ void raw_mma(const Raw8<float>& a, const Raw8<float>& b, f32x4_t& c) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+        c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w[e]), __uint_as_float(b.w[e]), c, 0, 0, 0);
+}
+
+template <typename T, bool DENSE>
 __global__ void __launch_bounds__(512) k_wgrad(WgArgs a) {
-    extern __shared__ float acc_lds[];   // [K][16]
+    constexpr int MAXT = WgTiles<T>::N;
+    constexpr int NW = Raw8<T>::NW;
+    constexpr uint32_t ES = sizeof(T);
+    extern __shared__ float acc_lds[];   // [K + 1][WG_LD]
     const int ctile = xcd_tile(blockIdx.x, (a.G + 15) / 16);
     if (ctile < 0) return;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int n0 = ctile * 16;
-    const int col = lane & 15;
-    const int n = n0 + col;
-    const bool nok = n < a.G;
-    const int g8 = 8 * (lane >> 4);
-    for (int i = threadIdx.x; i < a.K * 16; i += blockDim.x) acc_lds[i] = 0.0f;
-    __syncthreads();
+    const int col = lane & 15, g8 = 8 * (lane >> 4);
+    const int n0 = ctile * 16, n = n0 + col;
+    const int r0 = slice_start(w, a.K), r1 = slice_start(w + 1, a.K);
+    for (int i = r0 * 16 + lane; i < r1 * 16; i += 64) acc_lds[(i >> 4) * WG_LD + (i & 15)] = 0.0f;
     const int t0 = blockIdx.y * a.tper;
     const int t1 = min(a.T, t0 + a.tper);
-    for (int t = t0; t < t1; ++t) {
-        const int cnt = a.site.count[t];
-        const int32_t* krow = a.site.keep + (size_t)t * a.site.kmax;
-        const uint8_t* mrow = a.site.mask + (size_t)t * a.site.kmax;
+    // lane j holds the keep-list range of this wave's slice at t0 + j
+    int segb = 0, sege = 0;
+    if (t0 + lane < t1) {
+        segb = a.site.kseg[(size_t)(t0 + lane) * (NXCD + 1) + w];
+        sege = a.site.kseg[(size_t)(t0 + lane) * (NXCD + 1) + w + 1];
+    }
+    uint32_t pm0[NW], pmb[NW];                 // batch-pad masks of chunk 0 (A side; B side adds n < G)
+    pad_mask<T>(g8, a.B, pm0);
+#pragma unroll
+    for (int q = 0; q < NW; ++q) pmb[q] = n < a.G ? pm0[q] : 0u;
+    const uint32_t boff = (uint32_t)(min(n, a.G - 1) * a.BP + g8) * ES;   // DA^T fragment offset
+    const uint32_t abytes = (uint32_t)a.K * a.BP * ES, bbytes = (uint32_t)a.G * a.BP * ES;
+    const int spare = a.K * WG_LD;
+
+    // keep-list entries (and, dense mode, mask bytes) of the A-fragment rows
+    // of tiles jt0 .. jt0+MAXT-1 at t.  In dense mode the keep list is the
+    // identity, so mask[j] is the mask byte of row keep[j].
+    auto rows_issue = [&](int t, int jt0, int* kv, int* mv) {
+        const int jb = __builtin_amdgcn_readlane(segb, t - t0);
+        const int je = __builtin_amdgcn_readlane(sege, t - t0);
+        const __amdgpu_buffer_rsrc_t kr = buf_rsrc(a.site.keep + (size_t)t * a.site.kmax, (uint32_t)a.site.kmax * 4);
+        const __amdgpu_buffer_rsrc_t mr = buf_rsrc(a.site.mask + (size_t)t * a.site.kmax, (uint32_t)a.site.kmax);
+#pragma unroll
+        for (int i = 0; i < MAXT; ++i) {
+            const int j = jb + (jt0 + i) * 16 + col;
+            const int jc = j < je ? j : 0;
+            kv[i] = (int)__builtin_amdgcn_raw_buffer_load_b32(kr, (uint32_t)jc * 4, 0, 0);
+            if (DENSE) mv[i] = (int)__builtin_amdgcn_raw_buffer_load_b8(mr, (uint32_t)jc, 0, 0);
+        }
+    };
+    // row of each tile's A-fragment lane; absent rows read row 0 and add
+    // into the spare row
+    auto rows_resolve = [&](int t, int jt0, const int* kv, const int* mv, int* kk, int* la) {
+        const int jb = __builtin_amdgcn_readlane(segb, t - t0);
+        const int je = __builtin_amdgcn_readlane(sege, t - t0);
+#pragma unroll
+        for (int i = 0; i < MAXT; ++i) {
+            const int j = jb + (jt0 + i) * 16 + col;
+            const bool ok = j < je && (!DENSE || mv[i]);
+            kk[i] = ok ? kv[i] : 0;
+            la[i] = ok ? kv[i] * WG_LD : spare;
+        }
+    };
+    auto act_rsrc = [&](int t) {
         const T* act = (a.actT_first && t == a.t_first) ? (const T*)a.actT_first
                                                         : (const T*)a.actT + (long)(t + a.shift) * a.tstride;
-        const T* DAT = (const T*)a.daT + (size_t)t * a.G * a.BP;
-        for (int jt = w; jt * 16 < cnt; jt += 8) {
-            const int j = jt * 16 + (lane & 15);
-            int k = -1;
-            if (j < cnt) {
-                k = krow[j];
-                if (a.dense && !mrow[k]) k = -1;
-            }
-            f32x4_t acc = {0, 0, 0, 0};
-            for (int bc = 0; bc < a.B; bc += 32) {
-                Frag<T> fa, fb;
+        return buf_rsrc(act, abytes);
+    };
+    auto dat_rsrc = [&](int t) { return buf_rsrc((const T*)a.daT + (size_t)t * a.G * a.BP, bbytes); };
+    auto a_issue = [&](__amdgpu_buffer_rsrc_t ar, int bc, const int* kk, Raw8<T>* fa) {
 #pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    const int b = bc + g8 + 4 * h;
-                    if (k >= 0) ld4(act + (size_t)k * a.BP + b, fa.v + 4 * h);
-                    else zero4(fa.v + 4 * h);
-                    if (nok) ld4(DAT + (size_t)n * a.BP + b, fb.v + 4 * h);
-                    else zero4(fb.v + 4 * h);
+        for (int i = 0; i < MAXT; ++i) raw_load(fa[i], ar, (uint32_t)(kk[i] * a.BP + bc + g8) * ES);
+    };
+    // multiply the tiles (chunk-0 fragments already loaded), finish the other
+    // batch chunks, and add the tiles into their LDS rows.  Tiles past nt
+    // are multiplied too (their rows are absent): unconditional products
+    // keep the loads out of branches.
+    auto finish = [&](__amdgpu_buffer_rsrc_t ar, __amdgpu_buffer_rsrc_t br, const int* kk, const int* la, int nt,
+                      Raw8<T>* fa, const Raw8<T>& fb0) {
+        f32x4_t acc[MAXT];
 #pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        if (b + e >= a.B) { fa.v[4 * h + e] = zero_val<T>(); fb.v[4 * h + e] = zero_val<T>(); }
-                }
-                mma_16x16x32(fa, fb, acc);
-            }
+        for (int i = 0; i < MAXT; ++i) {
+            raw_and(fa[i], pm0);
+            acc[i] = f32x4_t{0, 0, 0, 0};
+            raw_mma(fa[i], fb0, acc[i]);
+        }
+        for (int bc = 32; bc < a.B; bc += 32) {
+            Raw8<T> fb;
+            raw_load(fb, br, boff + (uint32_t)bc * ES);
+            a_issue(ar, bc, kk, fa);
+            uint32_t pm[NW];
+            pad_mask<T>(bc + g8, a.B, pm);
+            raw_and(fb, pm);
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int jr = jt * 16 + acc_row(lane, r);
-                if (jr < cnt) acc_lds[krow[jr] * 16 + col] += a.s * acc[r];
+            for (int i = 0; i < MAXT; ++i) {
+                raw_and(fa[i], pm);
+                raw_mma(fa[i], fb, acc[i]);
             }
         }
-        __syncthreads();
+        // output r of this lane is row 4*(lane/16)+r of the tile, whose LDS
+        // row address is held by that lane
+        int addr[MAXT][4];
+        float old[MAXT][4];
+#pragma unroll
+        for (int i = 0; i < MAXT; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) addr[i][r] = __shfl(la[i], acc_row(lane, r)) + col;
+#pragma unroll
+        for (int i = 0; i < MAXT; ++i)
+            if (i < nt)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) old[i][r] = acc_lds[addr[i][r]];
+#pragma unroll
+        for (int i = 0; i < MAXT; ++i)
+            if (i < nt)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) acc_lds[addr[i][r]] = old[i][r] + a.s * acc[i][r];
+    };
+
+    int kv[MAXT], mv[MAXT];
+    Raw8<T> fb;
+    if (t0 < t1) {
+        rows_issue(t0, 0, kv, mv);
+        raw_load(fb, dat_rsrc(t0), boff);
+    }
+    for (int t = t0; t < t1; ++t) {
+        const __amdgpu_buffer_rsrc_t ar = act_rsrc(t), br = dat_rsrc(t);
+        const int cnt = __builtin_amdgcn_readlane(sege, t - t0) - __builtin_amdgcn_readlane(segb, t - t0);
+        const int ntile = (cnt + 15) >> 4;
+        int kc[MAXT], la[MAXT];
+        rows_resolve(t, 0, kv, mv, kc, la);
+        Raw8<T> fb0 = fb;
+        Raw8<T> fa[MAXT];
+        a_issue(ar, 0, kc, fa);
+        {   // next step's rows and fragment (the last step reloads its own:
+            // an unconditional issue keeps the wait counts exact)
+            const int tn = min(t + 1, t1 - 1);
+            rows_issue(tn, 0, kv, mv);
+            raw_load(fb, dat_rsrc(tn), boff);
+        }
+        __builtin_amdgcn_sched_barrier(0);     // keep the uses below the prefetch
+        raw_and(fb0, pmb);
+        finish(ar, br, kc, la, min(ntile, MAXT), fa, fb0);
+        for (int jt0 = MAXT; jt0 < ntile; jt0 += MAXT) {
+            int kv2[MAXT], mv2[MAXT];
+            rows_issue(t, jt0, kv2, mv2);
+            rows_resolve(t, jt0, kv2, mv2, kc, la);
+            a_issue(ar, 0, kc, fa);
+            finish(ar, br, kc, la, min(ntile - jt0, MAXT), fa, fb0);
+        }
     }
     float* out = a.out + (size_t)blockIdx.y * a.K * a.G;
-    for (int i = threadIdx.x; i < a.K * 16; i += blockDim.x) {
+    for (int i = r0 * 16 + lane; i < r1 * 16; i += 64) {
         const int kr = i >> 4, cc = i & 15;
-        if (n0 + cc < a.G) out[(size_t)kr * a.G + n0 + cc] = acc_lds[i];
+        if (n0 + cc < a.G) out[(size_t)kr * a.G + n0 + cc] = acc_lds[kr * WG_LD + cc];
     }
 }
 
@@ -833,8 +993,10 @@ void launch_dx(const DxArgs& a, int K, hipStream_t st) {
 }
 template <typename T>
 void launch_wgrad(const WgArgs& a, int ts, hipStream_t st) {
-    const size_t lds = (size_t)a.K * 16 * sizeof(float);
-    launch_k(KID_WGRAD, k_wgrad<T>, dim3(xcd_grid((a.G + 15) / 16), ts), dim3(512), lds, st, a);
+    const size_t lds = (size_t)(a.K + 1) * WG_LD * sizeof(float);
+    const dim3 grid(xcd_grid((a.G + 15) / 16), ts);
+    if (a.dense) launch_k(KID_WGRAD, k_wgrad<T, true>, grid, dim3(512), lds, st, a);
+    else launch_k(KID_WGRAD, k_wgrad<T, false>, grid, dim3(512), lds, st, a);
 }
 void launch_wreduce(const float* part, float* dW, long n, int ts, hipStream_t st) {
     launch_k(KID_NONE, k_wreduce, dim3(nblk(n, 256, 8192)), dim3(256), 0, st, part, dW, n, ts);
@@ -862,9 +1024,10 @@ static int g_attr_done = 0;
 int setup_kernel_attributes() {
     if (g_attr_done) return 0;
     const int lds = 160 * 1024;
-    hipError_t e1 = hipFuncSetAttribute((const void*)k_wgrad<float>, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-    hipError_t e2 = hipFuncSetAttribute((const void*)k_wgrad<bf16>, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-    if (e1 != hipSuccess || e2 != hipSuccess) return LSTM_SD_EHIP;
+    const void* fns[4] = {(const void*)k_wgrad<float, false>, (const void*)k_wgrad<bf16, false>,
+                          (const void*)k_wgrad<float, true>, (const void*)k_wgrad<bf16, true>};
+    for (const void* f : fns)
+        if (hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, lds) != hipSuccess) return LSTM_SD_EHIP;
     g_attr_done = 1;
     return 0;
 }

@@ -9,6 +9,11 @@
 // contiguous 16-byte loads and never touches a dropped column.
 #include <hip/hip_runtime.h>
 
+#include <stdlib.h>
+
+#include <mutex>
+#include <vector>
+
 #include "device.h"
 #include "kernels.h"
 #include "../../include/lstm_sd.h"
@@ -609,6 +614,42 @@ __global__ void k_zero_sync(unsigned* bar, int n, int* err) {
 
 // ---------------------------------------------------------------------------
 // Host side.
+
+// Checks (once per device, kernel and LDS size) that nwg workgroups of the
+// kernel can be resident at once; sets the dynamic LDS limit on first use.
+static hipError_t resident_limit(const void* fn, int threads, size_t lds, int nwg) {
+    struct Entry { int dev; const void* fn; size_t lds; int max_wg; };
+    static std::vector<Entry> cache;
+    static std::mutex mu;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    int max_wg = -1;
+    for (const Entry& c : cache)
+        if (c.dev == dev && c.fn == fn && c.lds == lds) max_wg = c.max_wg;
+    if (max_wg < 0) {
+        hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (e != hipSuccess) return e;
+        int per_cu = 0, ncu = 0;
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, threads, lds);
+        if (e != hipSuccess) return e;
+        if (hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+            return hipErrorInvalidDevice;
+        max_wg = per_cu * ncu;
+        cache.push_back({dev, fn, lds, max_wg});
+    }
+    return (nwg <= max_wg) ? hipSuccess : hipErrorCooperativeLaunchTooLarge;
+}
+
+// The persistent grids fit the device (resident_limit) and the stream runs
+// them after the previous kernel has drained, so every workgroup is placed
+// at once; a barrier wait is bounded in any case (timeout -> error flag).
+// LSTM_SD_COOP=1 launches them through the cooperative-launch API instead,
+// which also guarantees co-residency when other streams keep the device busy.
+static bool cooperative_api() {
+    const char* v = getenv("LSTM_SD_COOP");
+    return v && v[0] == '1';
+}
 size_t fwd_persist_lds(int H, int NT, int MG, int esize) {
     const size_t us = ((size_t)H * (16 * NT + 2) * esize + 15) & ~(size_t)15;
     const size_t kx = ((size_t)(H + 32) * 2 + 15) & ~(size_t)15;
@@ -618,15 +659,12 @@ size_t fwd_persist_lds(int H, int NT, int MG, int esize) {
 template <typename T, int NT, int MG>
 static hipError_t launch_fwd_persist_t(const PFwdArgs& a, int nwg, size_t lds, hipStream_t st) {
     auto fn = k_fwd_persist<T, NT, MG>;
-    hipError_t e = hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    const hipError_t e = resident_limit((const void*)fn, 64 * PF_NW, lds, nwg);
     if (e != hipSuccess) return e;
-    int per_cu = 0;
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, 64 * PF_NW, lds);
-    if (e != hipSuccess) return e;
-    int dev = 0, ncu = 0;
-    hipGetDevice(&dev);
-    hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev);
-    if (per_cu < 1 || nwg > per_cu * ncu) return hipErrorCooperativeLaunchTooLarge;
+    if (!cooperative_api()) {
+        hipLaunchKernelGGL(fn, dim3(nwg), dim3(64 * PF_NW), lds, st, a);
+        return hipGetLastError();
+    }
     PFwdArgs arg = a;
     void* params[] = {&arg};
     return hipLaunchCooperativeKernel((const void*)fn, dim3(nwg), dim3(64 * PF_NW), params, (unsigned)lds, st);
@@ -646,13 +684,13 @@ hipError_t launch_fwd_persist(PFwdArgs& a, int D, hipStream_t st, int kid_timer_
     const size_t lds = fwd_persist_lds(a.H, NT, MG, (int)sizeof(T));
     if (lds > 160 * 1024) return hipErrorInvalidValue;
     hipLaunchKernelGGL(k_zero_sync, dim3(1), dim3(64), 0, st, a.bar, 2, a.err);
-    if (kid_timer_on) hipEventRecord(e0, st);
+    if (kid_timer_on) (void)hipEventRecord(e0, st);
     hipError_t e;
     if (NT == 1 && MG == 32) e = launch_fwd_persist_t<T, 1, 32>(a, nwg, lds, st);
     else if (NT == 1) e = launch_fwd_persist_t<T, 1, 64>(a, nwg, lds, st);
     else if (MG == 32) e = launch_fwd_persist_t<T, 2, 32>(a, nwg, lds, st);
     else e = launch_fwd_persist_t<T, 2, 64>(a, nwg, lds, st);
-    if (kid_timer_on && e == hipSuccess) hipEventRecord(e1, st);
+    if (kid_timer_on && e == hipSuccess) (void)hipEventRecord(e1, st);
     return e;
 }
 
@@ -667,15 +705,12 @@ size_t bwd_persist_lds(int H, int UB, int MG, int esize) {
 template <typename T, int UB, int MG>
 static hipError_t launch_bwd_persist_t(const PBwdArgs& a, int nwg, size_t lds, hipStream_t st) {
     auto fn = k_bwd_persist<T, UB, MG>;
-    hipError_t e = hipFuncSetAttribute((const void*)fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    const hipError_t e = resident_limit((const void*)fn, 64 * PB_NW, lds, nwg);
     if (e != hipSuccess) return e;
-    int per_cu = 0;
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, 64 * PB_NW, lds);
-    if (e != hipSuccess) return e;
-    int dev = 0, ncu = 0;
-    if (hipGetDevice(&dev) != hipSuccess) return hipErrorInvalidDevice;
-    if (hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return hipErrorInvalidDevice;
-    if (per_cu < 1 || nwg > per_cu * ncu) return hipErrorCooperativeLaunchTooLarge;
+    if (!cooperative_api()) {
+        hipLaunchKernelGGL(fn, dim3(nwg), dim3(64 * PB_NW), lds, st, a);
+        return hipGetLastError();
+    }
     PBwdArgs arg = a;
     void* params[] = {&arg};
     return hipLaunchCooperativeKernel((const void*)fn, dim3(nwg), dim3(64 * PB_NW), params, (unsigned)lds, st);
