@@ -252,7 +252,7 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
             f.bias = w->b[l * D + d];
             f.site = site_view(P, mbuf, P.site_nr(l));
             f.Gx = (float*)(W + P.w_gx) + (size_t)d * T * B * G;
-            f.B = B; f.G = G; f.T = T; f.dense = !P.compact; f.s = P.s_nr;
+            f.K = kin; f.B = B; f.G = G; f.T = T; f.dense = !P.compact; f.s = P.s_nr;
             launch_fx<E>(f, st);
         }
         if (use_persistent()) {

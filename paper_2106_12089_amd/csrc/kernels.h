@@ -50,6 +50,7 @@ struct TransArgs {
 struct FxArgs {
     const void* X; int ldx;             // X + (t*B + b)*ldx
     const void* W;                      // [K][G]
+    int K;
     const float* bias;
     SiteView site;
     float* Gx;                          // [T][B][G]

@@ -158,66 +158,159 @@ __global__ void __launch_bounds__(256) k_transpose(TransArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Buffer-resource loads and packed 8-element operand fragments.
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+constexpr int BUF_FLAGS = 0x00020000;             // raw 32-bit buffer resource word 3 (gfx9)
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, BUF_FLAGS);
+}
+// 8 consecutive elements of one operand row as packed dwords
+template <typename T> struct Raw8 { static constexpr int NW = 4 * (int)sizeof(T) / 2; uint32_t w[NW]; };
+
+template <typename T>
+__device__ __forceinline__ void raw_load(Raw8<T>& f, __amdgpu_buffer_rsrc_t r, uint32_t off) {
+#pragma unroll
+    for (int q = 0; q < Raw8<T>::NW / 4; ++q) {
+        const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, off + 16 * q, 0, 0);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) f.w[4 * q + e] = v[e];
+    }
+}
+// AND masks that zero the elements at batch index >= B of a fragment whose
+// first element sits at batch index b0
+template <typename T>
+__device__ __forceinline__ void pad_mask(int b0, int B, uint32_t* m) {
+    if (sizeof(T) == 2) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            m[q] = (b0 + 2 * q < B ? 0x0000ffffu : 0u) | (b0 + 2 * q + 1 < B ? 0xffff0000u : 0u);
+    } else {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) m[q] = b0 + q < B ? 0xffffffffu : 0u;
+    }
+}
+template <typename T>
+__device__ __forceinline__ void raw_and(Raw8<T>& f, const uint32_t* m) {
+#pragma unroll
+    for (int q = 0; q < Raw8<T>::NW; ++q) f.w[q] &= m[q];
+}
+__device__ __forceinline__ void raw_mma(const Raw8<bf16>& a, const Raw8<bf16>& b, f32x4_t& c) {
+    const u32x4_t av = {a.w[0], a.w[1], a.w[2], a.w[3]}, bv = {b.w[0], b.w[1], b.w[2], b.w[3]};
+    c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, av), __builtin_bit_cast(bf16x8_t, bv),
+                                                c, 0, 0, 0);
+}
+__device__ __forceinline__ void raw_mma(const Raw8<float>& a, const Raw8<float>& b, f32x4_t& c) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+        c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w[e]), __uint_as_float(b.w[e]), c, 0, 0, 0);
+}
+
+// ---------------------------------------------------------------------------
 // Forward input product, all t (Eq. 1-4 first term; Sec. 3.2, FP input
 // sparsity: the dropped columns of x and rows of W are skipped).
-// grid (ceil(G/64), ceil(B/64), T), block 256: wave w owns 16 columns and up
-// to 4 row tiles; the keep row of t is staged in LDS.
-template <typename T>
+// grid (ceil(G/128) on the XCD mapping, T, ceil(B/32)), block 256.  A
+// workgroup computes a 32-row x 128-column tile of Gx_t; wave w owns columns
+// 32w .. 32w+31 (two 16-column MFMA tiles) for both 16-row tiles.  The
+// contraction runs over the keep list of t in chunks of 32 kept rows: each
+// chunk of W (32 gathered rows x 128 columns, loaded as whole row segments)
+// and of X (32 rows x the 32 gathered columns) is staged in LDS, double
+// buffered so that chunk i+1 is fetched while chunk i is multiplied.
+// Columns past G read neighbouring (or, at the end, out-of-range = zero) W
+// data and are never stored.
+constexpr int FX_NB = 128, FX_MB = 32, FX_KC = 32, FX_LD = FX_KC + 8;
+constexpr int FX_WLD = FX_NB + 8;
+
+template <typename T, bool DENSE>
 __global__ void __launch_bounds__(256) k_fx(FxArgs a) {
+    constexpr uint32_t ES = sizeof(T);
+    __shared__ __attribute__((aligned(16))) T ws[2][FX_KC][FX_WLD];   // W chunk [k][n]
+    __shared__ __attribute__((aligned(16))) T xs[2][FX_MB][FX_LD];    // X chunk [row][k]
     __shared__ int kidx[LSTM_SD_MAX_K];
-    const int ctile = xcd_tile(blockIdx.x, (a.G + 63) / 64);
+    const int ctile = xcd_tile(blockIdx.x, (a.G + FX_NB - 1) / FX_NB);
     if (ctile < 0) return;
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int t = blockIdx.z;
-    const int m0 = blockIdx.y * 64;
-    const int n = ctile * 64 + w * 16 + (lane & 15);
-    const bool nok = n < a.G;
-    const int g8 = 8 * (lane >> 4);
-    const T* X = (const T*)a.X + (size_t)t * a.B * a.ldx;
-    const T* W = (const T*)a.W;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int t = blockIdx.y, m0 = blockIdx.z * FX_MB, n0 = ctile * FX_NB;
+    const int g8 = 8 * (lane >> 4), cl = lane & 15;
     const int32_t* krow = a.site.keep + (size_t)t * a.site.kmax;
     const uint8_t* mrow = a.site.mask + (size_t)t * a.site.kmax;
     const int cnt = a.site.count[t];
-    for (int j = threadIdx.x; j < cnt; j += blockDim.x) {
+    for (int j = tid; j < cnt; j += blockDim.x) {
         const int k = krow[j];
-        kidx[j] = (a.dense && !mrow[k]) ? -1 : k;
+        kidx[j] = (DENSE && !mrow[j]) ? -1 : k;        // dense mode: the keep list is the identity
     }
     __syncthreads();
-    const int mtiles = min(4, (a.B - m0 + 15) / 16);
-    f32x4_t acc[4];
+    const __amdgpu_buffer_rsrc_t wr = buf_rsrc(a.W, (uint32_t)a.K * a.G * ES);
+    const T* X = (const T*)a.X + (size_t)t * a.B * a.ldx;
+
+    // staging roles: W row r = tid/8, 16 columns at 16*(tid%8); X row tid/8, 4 kept columns at 4*(tid%8)
+    const int sr = tid >> 3, sq = tid & 7;
+    constexpr int WNW = 16 * (int)ES / 16;             // 16-byte loads per W segment (2 bf16, 4 f32)
+    u32x4_t wreg[WNW];
+    T xreg[4];
+    auto fetch = [&](int kc) {
+        const int j = kc + sr;
+        const int k = j < cnt ? kidx[j] : -1;
+        const uint32_t off = ((uint32_t)max(k, 0) * a.G + n0 + 16 * sq) * ES;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) acc[i] = f32x4_t{0, 0, 0, 0};
-    for (int kc = 0; kc < cnt; kc += 32) {
-        int kk[8];
+        for (int q = 0; q < WNW; ++q) wreg[q] = __builtin_amdgcn_raw_buffer_load_b128(wr, off + 16 * q, 0, 0);
+        const int row = m0 + sr;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const int j = kc + g8 + e;
-            kk[e] = j < cnt ? kidx[j] : -1;
+        for (int q = 0; q < 4; ++q) {
+            const int jj = kc + 4 * sq + q;
+            const int kk = jj < cnt ? kidx[jj] : -1;
+            xreg[q] = (kk >= 0 && row < a.B) ? X[(size_t)row * a.ldx + kk] : zero_val<T>();
         }
-        Frag<T> fb;
+    };
+    auto commit = [&](int buf) {
+        uint4* wd = (uint4*)&ws[buf][sr][16 * sq];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) fb.v[e] = (kk[e] >= 0 && nok) ? W[(size_t)kk[e] * a.G + n] : zero_val<T>();
+        for (int q = 0; q < WNW; ++q) wd[q] = make_uint4(wreg[q][0], wreg[q][1], wreg[q][2], wreg[q][3]);
 #pragma unroll
-        for (int mt = 0; mt < 4; ++mt) {
-            if (mt < mtiles) {
-                const int row = m0 + mt * 16 + (lane & 15);
-                const bool rok = row < a.B;
-                Frag<T> fa;
+        for (int q = 0; q < 4; ++q) xs[buf][sr][4 * sq + q] = xreg[q];
+    };
+
+    f32x4_t acc[2][2];
 #pragma unroll
-                for (int e = 0; e < 8; ++e)
-                    fa.v[e] = (kk[e] >= 0 && rok) ? X[(size_t)row * a.ldx + kk[e]] : zero_val<T>();
-                mma_16x16x32(fa, fb, acc[mt]);
-            }
-        }
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int c = 0; c < 2; ++c) acc[i][c] = f32x4_t{0, 0, 0, 0};
+    const int nchunk = (cnt + FX_KC - 1) / FX_KC;
+    if (nchunk > 0) {
+        fetch(0);
+        commit(0);
     }
-    if (nok) {
+    __syncthreads();
+    for (int ch = 0; ch < nchunk; ++ch) {
+        const int buf = ch & 1;
+        if (ch + 1 < nchunk) fetch((ch + 1) * FX_KC);
+        Frag<T> fa[2], fb[2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) fa[i].v[e] = xs[buf][16 * i + cl][g8 + e];
+#pragma unroll
+        for (int c = 0; c < 2; ++c)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) fb[c].v[e] = ws[buf][g8 + e][32 * w + 16 * c + cl];
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int c = 0; c < 2; ++c) mma_16x16x32(fa[i], fb[c], acc[i][c]);
+        if (ch + 1 < nchunk) commit(buf ^ 1);
+        __syncthreads();
+    }
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+        const int n = n0 + 32 * w + 16 * c + cl;
+        if (n >= a.G) continue;
         const float bn = a.bias[n];
 #pragma unroll
-        for (int mt = 0; mt < 4; ++mt)
+        for (int i = 0; i < 2; ++i)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                const int row = m0 + mt * 16 + acc_row(lane, r);
-                if (mt < mtiles && row < a.B) a.Gx[((size_t)t * a.B + row) * a.G + n] = a.s * acc[mt][r] + bn;
+                const int row = m0 + 16 * i + acc_row(lane, r);
+                if (row < a.B) a.Gx[((size_t)t * a.B + row) * a.G + n] = a.s * acc[i][c][r] + bn;
             }
     }
 }
@@ -490,8 +583,10 @@ __global__ void __launch_bounds__(1024) k_bwd(BwdArgs a) {
 // Output-sparse input gradient, all t (Eq. 10), summed over directions.
 // grid (ceil(K/16), T, ceil(B/64)), block 256: 16 kept columns per
 // workgroup, the contraction over 4H split over the 4 waves.
-template <typename T>
+template <typename T, int MT>
 __global__ void __launch_bounds__(256) k_dx(DxArgs a) {
+    constexpr int U = sizeof(T) == 2 ? 4 : 2;           // 32-column chunks per wave loaded together
+    constexpr uint32_t ES = sizeof(T);
     __shared__ float red[4][64][17];
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int t = blockIdx.y;
@@ -503,49 +598,52 @@ __global__ void __launch_bounds__(256) k_dx(DxArgs a) {
     if (ti >= a.tps || j0 >= hi) return;
     const int cnt = hi;                     // columns of this tile end at the slice end
     const int m0 = blockIdx.z * 64;
-    const int j = j0 + (lane & 15);
+    const int cl = lane & 15;
+    const int j = j0 + cl;
     const int g8 = 8 * (lane >> 4);
     const int32_t* krow = a.site.keep + (size_t)t * a.site.kmax;
     const uint8_t* mrow = a.site.mask + (size_t)t * a.site.kmax;
-    const int k = (j < cnt) ? krow[j] : -1;
-    const int mtiles = min(4, (a.B - m0 + 15) / 16);
-    f32x4_t acc[4];
+    // absent columns (j past the slice) read row 0; their outputs are not stored
+    const int kr = (j < cnt) ? krow[j] : 0;
+    f32x4_t acc[MT];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) acc[i] = f32x4_t{0, 0, 0, 0};
+    for (int i = 0; i < MT; ++i) acc[i] = f32x4_t{0, 0, 0, 0};
     for (int d = 0; d < a.D; ++d) {
-        const T* DA = (const T*)a.da[d] + (size_t)t * a.B * a.G;
-        const T* Wk = (const T*)a.W[d];
-        for (int nc = 32 * w; nc < a.G; nc += 128) {
-            Frag<T> fb;
+        // rows past B fall outside the DA_t resource and read as zero
+        const __amdgpu_buffer_rsrc_t dr = buf_rsrc((const T*)a.da[d] + (size_t)t * a.B * a.G, (uint32_t)a.B * a.G * ES);
+        const __amdgpu_buffer_rsrc_t wr = buf_rsrc(a.W[d], (uint32_t)a.K * a.G * ES);
+        const uint32_t woff = ((uint32_t)kr * a.G + g8) * ES;
+        for (int nc0 = 32 * w; nc0 < a.G; nc0 += 128 * U) {
+            Raw8<T> fb[U], fa[U][MT];
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const int n = nc + g8 + 4 * h;
-                if (k >= 0 && n < a.G) ld4(Wk + (size_t)k * a.G + n, fb.v + 4 * h);
-                else zero4(fb.v + 4 * h);
+            for (int u = 0; u < U; ++u) {
+                const uint32_t nc = nc0 + 128 * u;
+                raw_load(fb[u], wr, woff + nc * ES);
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+                    raw_load(fa[u][mt], dr, ((uint32_t)(m0 + 16 * mt + cl) * a.G + nc + g8) * ES);
             }
 #pragma unroll
-            for (int mt = 0; mt < 4; ++mt) {
-                if (mt < mtiles) {
-                    const int row = m0 + mt * 16 + (lane & 15);
-                    Frag<T> fa;
+            for (int u = 0; u < U; ++u) {
+                const int nc = nc0 + 128 * u;
+                if (nc + 32 > a.G) {            // chunk reaches past G: zero the DA side there
+                    uint32_t m[Raw8<T>::NW];
+                    pad_mask<T>(nc + g8, a.G, m);
 #pragma unroll
-                    for (int h = 0; h < 2; ++h) {
-                        const int n = nc + g8 + 4 * h;
-                        if (row < a.B && n < a.G) ld4(DA + (size_t)row * a.G + n, fa.v + 4 * h);
-                        else zero4(fa.v + 4 * h);
-                    }
-                    mma_16x16x32(fa, fb, acc[mt]);
+                    for (int mt = 0; mt < MT; ++mt) raw_and(fa[u][mt], m);
                 }
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) raw_mma(fa[u][mt], fb[u], acc[mt]);
             }
         }
     }
 #pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
+    for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) red[w][mt * 16 + acc_row(lane, r)][lane & 15] = acc[mt][r];
+        for (int r = 0; r < 4; ++r) red[w][mt * 16 + acc_row(lane, r)][cl] = acc[mt][r];
     __syncthreads();
     float* out = a.out + (size_t)t * a.B * a.ldo;
-    for (int q = threadIdx.x; q < 64 * 16; q += 256) {
+    for (int q = threadIdx.x; q < 16 * MT * 16; q += 256) {
         const int rr = q >> 4, c = q & 15;
         const int row = m0 + rr, jj = j0 + c;
         if (row < a.B && jj < cnt) {
@@ -581,53 +679,6 @@ template <typename T>
 struct WgTiles { static constexpr int N = 6; };   // 16-row tiles in registers at once
 template <>
 struct WgTiles<float> { static constexpr int N = 4; };
-
-typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
-constexpr int BUF_FLAGS = 0x00020000;             // raw 32-bit buffer resource word 3 (gfx9)
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* base, uint32_t bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, BUF_FLAGS);
-}
-// 8 consecutive elements of one operand row as packed dwords
-template <typename T> struct Raw8 { static constexpr int NW = 4 * (int)sizeof(T) / 2; uint32_t w[NW]; };
-
-template <typename T>
-__device__ __forceinline__ void raw_load(Raw8<T>& f, __amdgpu_buffer_rsrc_t r, uint32_t off) {
-#pragma unroll
-    for (int q = 0; q < Raw8<T>::NW / 4; ++q) {
-        const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, off + 16 * q, 0, 0);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) f.w[4 * q + e] = v[e];
-    }
-}
-// AND masks that zero the elements at batch index >= B of a fragment whose
-// first element sits at batch index b0
-template <typename T>
-__device__ __forceinline__ void pad_mask(int b0, int B, uint32_t* m) {
-    if (sizeof(T) == 2) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-            m[q] = (b0 + 2 * q < B ? 0x0000ffffu : 0u) | (b0 + 2 * q + 1 < B ? 0xffff0000u : 0u);
-    } else {
-#pragma unroll
-        for (int q = 0; q < 8; ++q) m[q] = b0 + q < B ? 0xffffffffu : 0u;
-    }
-}
-template <typename T>
-__device__ __forceinline__ void raw_and(Raw8<T>& f, const uint32_t* m) {
-#pragma unroll
-    for (int q = 0; q < Raw8<T>::NW; ++q) f.w[q] &= m[q];
-}
-__device__ __forceinline__ void raw_mma(const Raw8<bf16>& a, const Raw8<bf16>& b, f32x4_t& c) {
-    const u32x4_t av = {a.w[0], a.w[1], a.w[2], a.w[3]}, bv = {b.w[0], b.w[1], b.w[2], b.w[3]};
-    c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, av), __builtin_bit_cast(bf16x8_t, bv),
-                                                c, 0, 0, 0);
-}
-__device__ __forceinline__ void raw_mma(const Raw8<float>& a, const Raw8<float>& b, f32x4_t& c) {
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-        c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w[e]), __uint_as_float(b.w[e]), c, 0, 0, 0);
-}
 
 template <typename T, bool DENSE>
 __global__ void __launch_bounds__(512) k_wgrad(WgArgs a) {
@@ -973,7 +1024,9 @@ void launch_transpose(const TransArgs& a, int N, hipStream_t st) {
 }
 template <typename T>
 void launch_fx(const FxArgs& a, hipStream_t st) {
-    launch_k(KID_FX, k_fx<T>, dim3(xcd_grid((a.G + 63) / 64), (a.B + 63) / 64, a.T), dim3(256), 0, st, a);
+    const dim3 grid(xcd_grid((a.G + FX_NB - 1) / FX_NB), a.T, (a.B + FX_MB - 1) / FX_MB);
+    if (a.dense) launch_k(KID_FX, k_fx<T, true>, grid, dim3(256), 0, st, a);
+    else launch_k(KID_FX, k_fx<T, false>, grid, dim3(256), 0, st, a);
 }
 template <typename T>
 void launch_step(const StepArgs& a, int D, hipStream_t st) {
@@ -989,7 +1042,10 @@ void launch_bwd(const BwdArgs& a, int D, hipStream_t st) {
 }
 template <typename T>
 void launch_dx(const DxArgs& a, int K, hipStream_t st) {
-    launch_k(KID_DX, k_dx<T>, dim3(NXCD * a.tps, a.T, (a.B + 63) / 64), dim3(256), 0, st, a);
+    const dim3 grid(NXCD * a.tps, a.T, (a.B + 63) / 64);
+    if (a.B <= 16) launch_k(KID_DX, k_dx<T, 1>, grid, dim3(256), 0, st, a);
+    else if (a.B <= 32) launch_k(KID_DX, k_dx<T, 2>, grid, dim3(256), 0, st, a);
+    else launch_k(KID_DX, k_dx<T, 4>, grid, dim3(256), 0, st, a);
 }
 template <typename T>
 void launch_wgrad(const WgArgs& a, int ts, hipStream_t st) {
