@@ -81,6 +81,75 @@ __device__ __forceinline__ void ld8(const float* p, float* o) {
     o[4] = v1.x; o[5] = v1.y; o[6] = v1.z; o[7] = v1.w;
 }
 
+// ---------------------------------------------------------------------------
+// Buffer-resource loads (32-bit offsets; reads past the resource return 0)
+// and 8-element operand fragments held as packed dwords.
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+constexpr int BUF_FLAGS = 0x00020000;             // raw 32-bit buffer resource word 3 (gfx9)
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, BUF_FLAGS);
+}
+// 8 consecutive elements of one operand row as packed dwords
+template <typename T> struct Raw8 { static constexpr int NW = 4 * (int)sizeof(T) / 2; uint32_t w[NW]; };
+
+template <typename T>
+__device__ __forceinline__ void raw_load(Raw8<T>& f, __amdgpu_buffer_rsrc_t r, uint32_t off) {
+#pragma unroll
+    for (int q = 0; q < Raw8<T>::NW / 4; ++q) {
+        const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, off + 16 * q, 0, 0);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) f.w[4 * q + e] = v[e];
+    }
+}
+// AND masks that zero the elements at index >= B of a fragment whose first
+// element sits at index b0
+template <typename T>
+__device__ __forceinline__ void pad_mask(int b0, int B, uint32_t* m) {
+    if (sizeof(T) == 2) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            m[q] = (b0 + 2 * q < B ? 0x0000ffffu : 0u) | (b0 + 2 * q + 1 < B ? 0xffff0000u : 0u);
+    } else {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) m[q] = b0 + q < B ? 0xffffffffu : 0u;
+    }
+}
+template <typename T>
+__device__ __forceinline__ void raw_and(Raw8<T>& f, const uint32_t* m) {
+#pragma unroll
+    for (int q = 0; q < Raw8<T>::NW; ++q) f.w[q] &= m[q];
+}
+__device__ __forceinline__ void raw_mma(const Raw8<bf16>& a, const Raw8<bf16>& b, f32x4_t& c) {
+    const u32x4_t av = {a.w[0], a.w[1], a.w[2], a.w[3]}, bv = {b.w[0], b.w[1], b.w[2], b.w[3]};
+    c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, av), __builtin_bit_cast(bf16x8_t, bv),
+                                                c, 0, 0, 0);
+}
+__device__ __forceinline__ void raw_mma(const Raw8<float>& a, const Raw8<float>& b, f32x4_t& c) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+        c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w[e]), __uint_as_float(b.w[e]), c, 0, 0, 0);
+}
+
+// 8 elements from LDS (16-byte aligned)
+template <typename T>
+__device__ __forceinline__ void raw_lds(Raw8<T>& f, const T* p) {
+#pragma unroll
+    for (int q = 0; q < Raw8<T>::NW / 4; ++q) {
+        const uint4 v = *(const uint4*)((const char*)p + 16 * q);
+        f.w[4 * q] = v.x; f.w[4 * q + 1] = v.y; f.w[4 * q + 2] = v.z; f.w[4 * q + 3] = v.w;
+    }
+}
+// pack an element-wise fragment
+__device__ __forceinline__ void raw_from(Raw8<bf16>& f, const Frag<bf16>& x) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) f.w[q] = (uint32_t)x.v[2 * q] | ((uint32_t)x.v[2 * q + 1] << 16);
+}
+__device__ __forceinline__ void raw_from(Raw8<float>& f, const Frag<float>& x) {
+#pragma unroll
+    for (int q = 0; q < 8; ++q) f.w[q] = __float_as_uint(x.v[q]);
+}
+
 // Output element r (0..3) of lane l of a 16x16 accumulator sits at
 // row 4*(l/16) + r, column l%16.
 __device__ __forceinline__ int acc_row(int lane, int r) { return 4 * (lane >> 4) + r; }

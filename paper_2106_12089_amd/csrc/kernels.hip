@@ -158,55 +158,6 @@ __global__ void __launch_bounds__(256) k_transpose(TransArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Buffer-resource loads and packed 8-element operand fragments.
-typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
-constexpr int BUF_FLAGS = 0x00020000;             // raw 32-bit buffer resource word 3 (gfx9)
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* base, uint32_t bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, BUF_FLAGS);
-}
-// 8 consecutive elements of one operand row as packed dwords
-template <typename T> struct Raw8 { static constexpr int NW = 4 * (int)sizeof(T) / 2; uint32_t w[NW]; };
-
-template <typename T>
-__device__ __forceinline__ void raw_load(Raw8<T>& f, __amdgpu_buffer_rsrc_t r, uint32_t off) {
-#pragma unroll
-    for (int q = 0; q < Raw8<T>::NW / 4; ++q) {
-        const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, off + 16 * q, 0, 0);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) f.w[4 * q + e] = v[e];
-    }
-}
-// AND masks that zero the elements at batch index >= B of a fragment whose
-// first element sits at batch index b0
-template <typename T>
-__device__ __forceinline__ void pad_mask(int b0, int B, uint32_t* m) {
-    if (sizeof(T) == 2) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-            m[q] = (b0 + 2 * q < B ? 0x0000ffffu : 0u) | (b0 + 2 * q + 1 < B ? 0xffff0000u : 0u);
-    } else {
-#pragma unroll
-        for (int q = 0; q < 8; ++q) m[q] = b0 + q < B ? 0xffffffffu : 0u;
-    }
-}
-template <typename T>
-__device__ __forceinline__ void raw_and(Raw8<T>& f, const uint32_t* m) {
-#pragma unroll
-    for (int q = 0; q < Raw8<T>::NW; ++q) f.w[q] &= m[q];
-}
-__device__ __forceinline__ void raw_mma(const Raw8<bf16>& a, const Raw8<bf16>& b, f32x4_t& c) {
-    const u32x4_t av = {a.w[0], a.w[1], a.w[2], a.w[3]}, bv = {b.w[0], b.w[1], b.w[2], b.w[3]};
-    c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, av), __builtin_bit_cast(bf16x8_t, bv),
-                                                c, 0, 0, 0);
-}
-__device__ __forceinline__ void raw_mma(const Raw8<float>& a, const Raw8<float>& b, f32x4_t& c) {
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-        c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w[e]), __uint_as_float(b.w[e]), c, 0, 0, 0);
-}
-
-// ---------------------------------------------------------------------------
 // Forward input product, all t (Eq. 1-4 first term; Sec. 3.2, FP input
 // sparsity: the dropped columns of x and rows of W are skipped).
 // grid (ceil(G/128) on the XCD mapping, T, ceil(B/32)), block 256.  A

@@ -256,22 +256,18 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
 #pragma unroll
             for (int j = 0; j < NT; ++j) acc[i][j] = f32x4_t{0, 0, 0, 0};
         const int nch = (cnt + 31) / 32;
+        // chunks past the slot read as 0; rows past B hold stale values that
+        // only reach output rows that are never used
+        const __amdgpu_buffer_rsrc_t hr = buf_rsrc(hc, (uint32_t)(hxs * sizeof(T)));
         for (int c0 = 0; c0 < nch; c0 += NW * MAXC) {
             // issue every exchange load of this round first
-            Frag<T> fa[MAXC][MT];
+            Raw8<T> fa[MAXC][MT];
 #pragma unroll
             for (int i = 0; i < MAXC; ++i) {
                 const int c = c0 + w + NW * i;
-                const bool jin = 32 * c + g8 < cnt;
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt) {
-                    const int row = m0 + mt * 16 + (lane & 15);
-                    if (row < B && jin) lds8(hc + frag_lane_off(c, m0 / 16 + mt, lane, a.mtiles), fa[i][mt].v);
-                    else {
-#pragma unroll
-                        for (int e = 0; e < 8; ++e) fa[i][mt].v[e] = zero_val<T>();
-                    }
-                }
+                for (int mt = 0; mt < MT; ++mt)
+                    raw_load(fa[i][mt], hr, (uint32_t)(frag_lane_off(c, m0 / 16 + mt, lane, a.mtiles) * sizeof(T)));
             }
 #pragma unroll
             for (int i = 0; i < MAXC; ++i) {
@@ -288,14 +284,19 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
                     for (int nt = 0; nt < NT; ++nt)
                         fb[nt].v[e] = k >= 0 ? Us[k * UP + nt * 16 + (lane & 15)] : zero_val<T>();
                 }
+                Raw8<T> fbr[NT];
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt) {
+                for (int nt = 0; nt < NT; ++nt) raw_from(fbr[nt], fb[nt]);
+                if (kc + 32 > cnt) {            // last chunk: slots past the keep count hold stale values
+                    uint32_t m[Raw8<T>::NW];
+                    pad_mask<T>(kc + g8, cnt, m);
 #pragma unroll
-                    for (int e = 0; e < 8; ++e)
-                        if (kc + g8 + e >= cnt) fa[i][mt].v[e] = zero_val<T>();
-#pragma unroll
-                    for (int nt = 0; nt < NT; ++nt) mma_16x16x32(fa[i][mt], fb[nt], acc[mt][nt]);
+                    for (int mt = 0; mt < MT; ++mt) raw_and(fa[i][mt], m);
                 }
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                    for (int nt = 0; nt < NT; ++nt) raw_mma(fa[i][mt], fbr[nt], acc[mt][nt]);
             }
         }
 #pragma unroll
@@ -306,18 +307,9 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
                 for (int r = 0; r < 4; ++r)
                     red[(w * MG + mt * 16 + acc_row(lane, r)) * NC + nt * 16 + (lane & 15)] = acc[mt][nt][r];
         __syncthreads();
-        // ---- pointwise (Eq. 1-6) and outputs; next step's inputs are loaded meanwhile
-        float gxc[PPT][4];
-        int pnc[PPT];
-        bool mnc[PPT], vc[PPT];
-#pragma unroll
-        for (int q = 0; q < PPT; ++q) {
-#pragma unroll
-            for (int g = 0; g < 4; ++g) gxc[q][g] = gxr[q][g];
-            pnc[q] = pn[q]; mnc[q] = mn[q]; vc[q] = valid[q];
-        }
-        if (s + 1 < T_) prefetch(s + 1);
+        // ---- pointwise (Eq. 1-6); h_t is published first
         T* hxn = (T*)D.hx + (size_t)((s + 1) & 1) * hxs;
+        float og4[PPT][4], cnv[PPT], hnv[PPT];
 #pragma unroll
         for (int q = 0; q < PPT; ++q) {
             const int b = pb[q], u = pu[q];
@@ -330,30 +322,41 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
                 float v = 0.f;
 #pragma unroll
                 for (int i = 0; i < NW; ++i) v += red[(i * MG + rr) * NC + cc];
-                pre[g] = a.s * v + gxc[q][g];
+                pre[g] = a.s * v + gxr[q][g];
             }
-            const float ig = sigmoid_fast(pre[0]);
-            const float fg = sigmoid_fast(pre[1]);
-            const float gg = tanh_fast(pre[2]);
-            const float og = sigmoid_fast(pre[3]);
+            og4[q][0] = sigmoid_fast(pre[0]);
+            og4[q][1] = sigmoid_fast(pre[1]);
+            og4[q][2] = tanh_fast(pre[2]);
+            og4[q][3] = sigmoid_fast(pre[3]);
             const float cp = creg[q];
-            const float cn = fg * cp + ig * gg;
-            const float hn = og * tanh_fast(cn);
-            const T hv = from_f32<T>(vc[q] ? hn : hreg[q]);
-            if (pnc[q] >= 0) xstore(hxn + frag_off(b, pnc[q], a.mtiles), (a.dense && !mnc[q]) ? zero_val<T>() : hv);
+            cnv[q] = og4[q][1] * cp + og4[q][0] * og4[q][2];
+            hnv[q] = og4[q][3] * tanh_fast(cnv[q]);
+            const T hv = from_f32<T>(valid[q] ? hnv[q] : hreg[q]);
+            if (pn[q] >= 0) xstore(hxn + frag_off(b, pn[q], a.mtiles), (a.dense && !mn[q]) ? zero_val<T>() : hv);
+        }
+        grid_arrive(bar);
+        // outputs only later kernels read, and the next step's inputs, go out
+        // while the other workgroups finish the step
+#pragma unroll
+        for (int q = 0; q < PPT; ++q) {
+            const int b = pb[q], u = pu[q];
+            if (b >= B || u >= H) continue;
+            const bool vq = valid[q];
+            const float cp = creg[q], cn = vq ? cnv[q] : cp, hn = hnv[q];
+            const T hv = from_f32<T>(vq ? hn : hreg[q]);
             float* gt = D.gates + ((size_t)t * B + b) * G;
-            gt[u] = ig; gt[H + u] = fg; gt[2 * H + u] = gg; gt[3 * H + u] = og;
-            D.cres[((size_t)t * B + b) * H + u] = vc[q] ? cn : cp;
-            if (vc[q]) { creg[q] = cn; hreg[q] = hn; }
+            gt[u] = og4[q][0]; gt[H + u] = og4[q][1]; gt[2 * H + u] = og4[q][2]; gt[3 * H + u] = og4[q][3];
+            D.cres[((size_t)t * B + b) * H + u] = cn;
+            if (vq) { creg[q] = cnv[q]; hreg[q] = hn; }
             ((T*)D.hrecT)[((size_t)t * H + u) * a.BP + b] = hv;
-            if (D.y) D.y[((size_t)t * B + b) * a.ldy + u] = vc[q] ? hn : 0.0f;
+            if (D.y) D.y[((size_t)t * B + b) * a.ldy + u] = vq ? hn : 0.0f;
             if (D.ybuf) {
-                const T yv = vc[q] ? from_f32<T>(hn) : zero_val<T>();
+                const T yv = vq ? from_f32<T>(hn) : zero_val<T>();
                 ((T*)D.ybuf)[((size_t)t * B + b) * a.ldy + u] = yv;
                 ((T*)D.ybufT)[((size_t)t * a.ldy + u) * a.BP + b] = yv;
             }
         }
-        grid_arrive(bar);
+        if (s + 1 < T_) prefetch(s + 1);
     }
     // ---- final state (NaN if the barrier timed out)
     const bool failed = __hip_atomic_load(a.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0;
@@ -462,38 +465,31 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
 
     // the recurrent gradient of the tile's units from DA of step tn into red
     auto recurrent_product = [&](int tn) {
-        const T* DA = (const T*)D.da + (size_t)tn * B * G;
+        // rows past B fall outside the DA_t resource (read as 0); columns
+        // past 4H meet the zero padding of the U rows
+        const __amdgpu_buffer_rsrc_t dr = buf_rsrc((const T*)D.da + (size_t)tn * B * G, (uint32_t)B * G * sizeof(T));
         f32x4_t acc[MT];
 #pragma unroll
         for (int i = 0; i < MT; ++i) acc[i] = f32x4_t{0, 0, 0, 0};
         const int nch = (G + 31) / 32;
         const int ul = lane & 15;
         for (int c0 = 0; c0 < nch; c0 += NW * MAXC) {
-            Frag<T> fa[MAXC][MT];
+            Raw8<T> fa[MAXC][MT];
 #pragma unroll
             for (int i = 0; i < MAXC; ++i) {
                 const int n = 32 * (c0 + w + NW * i) + g8;
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt) {
-                    const int row = m0 + mt * 16 + (lane & 15);
-#pragma unroll
-                    for (int h = 0; h < 2; ++h) {
-                        if (row < B && n + 4 * h < G) ld4g(DA + (size_t)row * G + n + 4 * h, fa[i][mt].v + 4 * h);
-                        else {
-#pragma unroll
-                            for (int e = 0; e < 4; ++e) fa[i][mt].v[4 * h + e] = zero_val<T>();
-                        }
-                    }
-                }
+                for (int mt = 0; mt < MT; ++mt)
+                    raw_load(fa[i][mt], dr, ((uint32_t)(m0 + mt * 16 + ul) * G + n) * (uint32_t)sizeof(T));
             }
 #pragma unroll
             for (int i = 0; i < MAXC; ++i) {
                 const int n = 32 * (c0 + w + NW * i);
                 if (n >= G) break;
-                Frag<T> fb;
-                lds8(Ur + (size_t)ul * GP + n + g8, fb.v);                 // zero past 4H
+                Raw8<T> fb;
+                raw_lds(fb, Ur + (size_t)ul * GP + n + g8);
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt) mma_16x16x32(fa[i][mt], fb, acc[mt]);
+                for (int mt = 0; mt < MT; ++mt) raw_mma(fa[i][mt], fb, acc[mt]);
             }
         }
 #pragma unroll
@@ -521,16 +517,6 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
             if (!grid_wait(bar, (unsigned)s * (unsigned)nslot, a.err, a.timeout)) break;
             if (kept) recurrent_product(tn);
         }
-        // copies of this step's inputs, then the next step's loads go out
-        float g4c[PPT][4], ctc[PPT], cpc[PPT], dyc[PPT];
-        bool vc[PPT];
-#pragma unroll
-        for (int q = 0; q < PPT; ++q) {
-#pragma unroll
-            for (int g = 0; g < 4; ++g) g4c[q][g] = gt4[q][g];
-            ctc[q] = ctv[q]; cpc[q] = cpv[q]; dyc[q] = dyv[q]; vc[q] = vld[q];
-        }
-        if (s + 1 < T_) prefetch(s + 1);
         float da4[PPT][4];
 #pragma unroll
         for (int q = 0; q < PPT; ++q) {
@@ -549,14 +535,14 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
                 D.dc0[(size_t)b * H + u] = dcs[q];
                 continue;
             }
-            if (vc[q]) {
-                dh += dyc[q];
-                const float ig = g4c[q][0], fg = g4c[q][1], gg = g4c[q][2], og = g4c[q][3];
-                const float tc = tanh_fast(ctc[q]);
+            if (vld[q]) {
+                dh += dyv[q];
+                const float ig = gt4[q][0], fg = gt4[q][1], gg = gt4[q][2], og = gt4[q][3];
+                const float tc = tanh_fast(ctv[q]);
                 const float dout = dh * tc;                            // Eq. 7
                 const float dc = dh * og * (1.0f - tc * tc) + dcs[q];  // Eq. 7
                 da4[q][0] = dc * gg * ig * (1.0f - ig);                // Eq. 9, sigmoid'
-                da4[q][1] = dc * cpc[q] * fg * (1.0f - fg);            // Eq. 8, sigmoid'
+                da4[q][1] = dc * cpv[q] * fg * (1.0f - fg);            // Eq. 8, sigmoid'
                 da4[q][2] = dc * ig * (1.0f - gg * gg);                // Eq. 9, tanh'
                 da4[q][3] = dout * og * (1.0f - og);                   // Eq. 7, sigmoid'
                 dcs[q] = dc * fg;                                      // Eq. 8
@@ -565,17 +551,23 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
                 dhc[q] = dh;                                           // frozen row: pass through
             }
             T* dar = (T*)D.da + ((size_t)t * B + b) * G;
-            T* dat = (T*)D.daT + (size_t)t * G * a.BP;
 #pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                const T v = from_f32<T>(da4[q][g]);
-                xstore(dar + g * H + u, v);
-                dat[(size_t)(g * H + u) * a.BP + b] = v;
-            }
+            for (int g = 0; g < 4; ++g) xstore(dar + g * H + u, from_f32<T>(da4[q][g]));
         }
         if (final_pass) break;
+        grid_arrive(bar);                                  // DA_t is published
+        // the outputs only later kernels read, and the next step's inputs,
+        // go out while the other workgroups finish the step
+#pragma unroll
+        for (int q = 0; q < PPT; ++q) {
+            const int b = pb[q], u = pu[q];
+            if (b >= B || u >= H) continue;
+            T* dat = (T*)D.daT + (size_t)t * G * a.BP;
+#pragma unroll
+            for (int g = 0; g < 4; ++g) dat[(size_t)(g * H + u) * a.BP + b] = from_f32<T>(da4[q][g]);
+        }
+        if (s + 1 < T_) prefetch(s + 1);
         // bias-gradient partial over the tile's rows
-        __syncthreads();
         float* rb = red;                                   // [MG][UB][4]
 #pragma unroll
         for (int q = 0; q < PPT; ++q) {
@@ -594,7 +586,6 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
                 D.dbpart[((size_t)t * a.mgc + mg) * G + g * H + u] = sum;
             }
         }
-        grid_arrive(bar);
     }
     // a timed-out barrier poisons the input-state gradients
     if (__hip_atomic_load(a.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
