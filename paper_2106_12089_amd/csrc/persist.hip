@@ -136,20 +136,26 @@ __device__ __forceinline__ void lds8(const float* p, float* o) {
 // a row group is MG batch rows.  512 threads = 8 waves; the contraction over
 // the kept recurrent neurons is split over the waves (each wave issues all of
 // its exchange loads before its first MFMA) and reduced in LDS.
-// Dynamic LDS: U slice [H][16*NT+2] (dtype), keep list [H+32] (int16),
-// reduction [8][MG][16*NT] (float).
+// Dynamic LDS: U slice transposed [16*NT][HP] (dtype; HP = H rounded up to
+// 32, plus 8, zero past H), keep list [H+32] (int16), reduction
+// [8][MG][16*NT] (float).  With every recurrent neuron kept (the keep list is
+// the identity) a B fragment is one 16-byte LDS read per column tile;
+// otherwise its 8 rows are gathered through the keep list.
 constexpr int PF_NW = 8;
+
+__host__ __device__ inline int fwd_hp(int H) { return (H + 31) / 32 * 32 + 8; }
 
 template <typename T, int NT, int MG>
 __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
-    constexpr int UPW = 4 * NT, MT = MG / 16, NW = PF_NW, NC = 16 * NT, UP = NC + 2;
+    constexpr int UPW = 4 * NT, MT = MG / 16, NW = PF_NW, NC = 16 * NT;
     constexpr int NTH = 64 * NW;
     constexpr int PPT = (MG * UPW + NTH - 1) / NTH;
-    constexpr int MAXC = MT <= 2 ? 6 : 3;       // chunks per wave per round (registers)
+    constexpr int MAXC = MT <= 2 ? 3 : 2;       // chunks per wave per round (registers)
     extern __shared__ __align__(16) char smem[];
     const int H = a.H, G = 4 * H, B = a.B, T_ = a.T;
-    T* Us = (T*)smem;
-    int16_t* kidx = (int16_t*)(smem + (((size_t)H * UP * sizeof(T) + 15) & ~(size_t)15));
+    const int HP = fwd_hp(H);
+    T* Ut = (T*)smem;
+    int16_t* kidx = (int16_t*)(smem + (((size_t)NC * HP * sizeof(T) + 15) & ~(size_t)15));
     float* red = (float*)((char*)kidx + (((size_t)(H + 32) * 2 + 15) & ~(size_t)15));
 
     const int nslot = a.ntiles * a.mgroups;
@@ -161,14 +167,14 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
     const int g8 = 8 * (lane >> 4);
     unsigned* bar = a.bar + d;
 
-    // U slice -> LDS: column c = nt*16 + g*4 + cu holds U[k][g*H + u0 + 4nt + cu]
+    // U slice -> LDS, transposed: row c = nt*16 + g*4 + cu holds U[k][g*H + u0 + 4nt + cu]
     {
         const T* U = (const T*)D.U;
-        for (int i = tid; i < H * NC; i += NTH) {
+        for (int i = tid; i < HP * NC; i += NTH) {
             const int k = i / NC, c = i % NC;
             const int nt = c >> 4, cc = c & 15;
             const int u = u0 + 4 * nt + (cc & 3);
-            Us[k * UP + c] = u < H ? U[(size_t)k * G + (cc >> 2) * H + u] : zero_val<T>();
+            Ut[c * HP + k] = (u < H && k < H) ? U[(size_t)k * G + (cc >> 2) * H + u] : zero_val<T>();
         }
     }
     // register state of this thread's (row, unit) pairs
@@ -184,35 +190,33 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
         creg[q] = ok ? D.c0[(size_t)pb[q] * H + pu[q]] : 0.f;
         hreg[q] = ok ? to_f32<T>(((const T*)D.h0)[(size_t)pb[q] * H + pu[q]]) : 0.f;
     }
-    // per-step inputs that do not depend on the recurrence, loaded one step ahead
+    // per-step inputs that do not depend on the recurrence, loaded one step
+    // ahead from clamped (valid) addresses without branches; pointwise uses
+    // them only for valid (row, unit) pairs
     float gxr[PPT][4];
-    int pn[PPT];
-    bool mn[PPT], valid[PPT];
+    int pn[PPT], mnr[PPT], lenr[PPT];
     int cnt = 0, cnt_next = 0;
     constexpr int KPT = (LSTM_SD_MAX_K + NTH - 1) / NTH;   // keep-list entries per thread
     int kreg[KPT];
     auto prefetch = [&](int s) {
         const int t = d == 0 ? s : T_ - 1 - s;
-        const int tn = d == 0 ? t + 1 : t - 1;
         const bool has_next = s + 1 < T_;
+        const int tn = has_next ? (d == 0 ? t + 1 : t - 1) : t;
         cnt_next = D.rh.count[t];
         const int32_t* krow = D.rh.keep + (size_t)t * D.rh.kmax;
 #pragma unroll
-        for (int i = 0; i < KPT; ++i) {
-            const int j = tid + NTH * i;
-            kreg[i] = j < cnt_next ? krow[j] : 0;
-        }
+        for (int i = 0; i < KPT; ++i) kreg[i] = krow[min(tid + NTH * i, D.rh.kmax - 1)];
 #pragma unroll
         for (int q = 0; q < PPT; ++q) {
-            const bool ok = pb[q] < B && pu[q] < H;
+            const int bc = min(pb[q], B - 1), uc = min(pu[q], H - 1);
 #pragma unroll
-            for (int g = 0; g < 4; ++g)
-                gxr[q][g] = ok ? D.gx[((size_t)t * B + pb[q]) * G + g * H + pu[q]] : 0.f;
-            pn[q] = (ok && has_next) ? D.rh.pos[(size_t)tn * D.rh.kmax + pu[q]] : -1;
-            mn[q] = (ok && has_next) ? D.rh.mask[(size_t)tn * D.rh.kmax + pu[q]] != 0 : false;
-            valid[q] = ok && (a.lengths == nullptr || t < a.lengths[pb[q]]);
+            for (int g = 0; g < 4; ++g) gxr[q][g] = D.gx[((size_t)t * B + bc) * G + g * H + uc];
+            pn[q] = has_next ? D.rh.pos[(size_t)tn * D.rh.kmax + uc] : -1;
+            mnr[q] = D.rh.mask[(size_t)tn * D.rh.kmax + uc];
+            lenr[q] = a.lengths ? a.lengths[bc] : T_;
         }
     };
+    auto is_valid = [&](int q, int t) { return pb[q] < B && pu[q] < H && t < lenr[q]; };
 
     // the keep list of the coming step, from registers to LDS
     auto commit_kidx = [&]() {
@@ -269,24 +273,35 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
                 for (int mt = 0; mt < MT; ++mt)
                     raw_load(fa[i][mt], hr, (uint32_t)(frag_lane_off(c, m0 / 16 + mt, lane, a.mtiles) * sizeof(T)));
             }
+            // every chunk slot of the round is multiplied (slots past the keep
+            // count have a zeroed A side and read B rows at offset 0): no
+            // branch lets the compiler sink the loads above into the products
 #pragma unroll
             for (int i = 0; i < MAXC; ++i) {
                 const int kc = 32 * (c0 + w + NW * i);
-                if (kc >= cnt) break;
-                Frag<T> fb[NT];
-                const int4 k8 = *(const int4*)(kidx + kc + g8);     // 8 int16 keep indices
-                const int kw[4] = {k8.x, k8.y, k8.z, k8.w};
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const int j = kc + g8 + e;
-                    const int k = j < cnt ? (int)(int16_t)(kw[e >> 1] >> (16 * (e & 1))) : -1;
-#pragma unroll
-                    for (int nt = 0; nt < NT; ++nt)
-                        fb[nt].v[e] = k >= 0 ? Us[k * UP + nt * 16 + (lane & 15)] : zero_val<T>();
-                }
                 Raw8<T> fbr[NT];
+                if (cnt == H) {                 // identity keep list: contiguous rows
+                    const int kb = kc < cnt ? kc : 0;
 #pragma unroll
-                for (int nt = 0; nt < NT; ++nt) raw_from(fbr[nt], fb[nt]);
+                    for (int nt = 0; nt < NT; ++nt) raw_lds(fbr[nt], Ut + (size_t)(nt * 16 + (lane & 15)) * HP + kb + g8);
+                } else {
+                    const int4 k8 = *(const int4*)(kidx + kc + g8);     // 8 int16 keep indices
+                    const int kw[4] = {k8.x, k8.y, k8.z, k8.w};
+                    int kk[8];
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const int j = kc + g8 + e;
+                        kk[e] = j < cnt ? (int)(int16_t)(kw[e >> 1] >> (16 * (e & 1))) : 0;
+                    }
+#pragma unroll
+                    for (int nt = 0; nt < NT; ++nt) {
+                        const T* row = Ut + (size_t)(nt * 16 + (lane & 15)) * HP;
+                        Frag<T> fb;
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) fb.v[e] = row[kk[e]];
+                        raw_from(fbr[nt], fb);
+                    }
+                }
                 if (kc + 32 > cnt) {            // last chunk: slots past the keep count hold stale values
                     uint32_t m[Raw8<T>::NW];
                     pad_mask<T>(kc + g8, cnt, m);
@@ -331,8 +346,8 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
             const float cp = creg[q];
             cnv[q] = og4[q][1] * cp + og4[q][0] * og4[q][2];
             hnv[q] = og4[q][3] * tanh_fast(cnv[q]);
-            const T hv = from_f32<T>(valid[q] ? hnv[q] : hreg[q]);
-            if (pn[q] >= 0) xstore(hxn + frag_off(b, pn[q], a.mtiles), (a.dense && !mn[q]) ? zero_val<T>() : hv);
+            const T hv = from_f32<T>(is_valid(q, t) ? hnv[q] : hreg[q]);
+            if (pn[q] >= 0) xstore(hxn + frag_off(b, pn[q], a.mtiles), (a.dense && !mnr[q]) ? zero_val<T>() : hv);
         }
         grid_arrive(bar);
         // outputs only later kernels read, and the next step's inputs, go out
@@ -341,7 +356,7 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
         for (int q = 0; q < PPT; ++q) {
             const int b = pb[q], u = pu[q];
             if (b >= B || u >= H) continue;
-            const bool vq = valid[q];
+            const bool vq = is_valid(q, t);
             const float cp = creg[q], cn = vq ? cnv[q] : cp, hn = hnv[q];
             const T hv = from_f32<T>(vq ? hn : hreg[q]);
             float* gt = D.gates + ((size_t)t * B + b) * G;
@@ -642,7 +657,7 @@ static bool cooperative_api() {
     return v && v[0] == '1';
 }
 size_t fwd_persist_lds(int H, int NT, int MG, int esize) {
-    const size_t us = ((size_t)H * (16 * NT + 2) * esize + 15) & ~(size_t)15;
+    const size_t us = ((size_t)16 * NT * fwd_hp(H) * esize + 15) & ~(size_t)15;
     const size_t kx = ((size_t)(H + 32) * 2 + 15) & ~(size_t)15;
     return us + kx + (size_t)PF_NW * MG * 16 * NT * 4;
 }
