@@ -24,10 +24,9 @@ template <typename T> void launch_bwd(const BwdArgs& a, int D, hipStream_t st);
 template <typename T> void launch_dx(const DxArgs& a, int K, hipStream_t st);
 template <typename T> void launch_wgrad(const WgArgs& a, int ts, hipStream_t st);
 template <typename T> void launch_fwd_init(const void*, const float*, float*, float*, long, hipStream_t);
-void launch_wreduce(const float* part, float* dW, long n, int ts, hipStream_t st);
+void launch_wreduce(const float* part, float* dW, float* db, long n, long ostride, int G, int ts, hipStream_t st);
 void launch_bwd_init(const float*, const float*, float*, float*, long, hipStream_t);
 void launch_expand(const float*, int, const SiteView&, float*, int, int, int, hipStream_t);
-void launch_db(const float*, float*, int, int, int, hipStream_t);
 void launch_mse(const float*, const float*, const int32_t*, float*, float*, int, float*, int, int, int,
                 hipStream_t);
 int setup_kernel_attributes();
@@ -132,11 +131,10 @@ int make_plan(const lstm_sd_dims* d, Plan* p, const char** why) {
     off = 0;
     q.w_da = off;     off = align_up(off + D * T * (size_t)q.das * es, A);
     q.w_daT = off;    off = align_up(off + D * T * G * BP * es, A);
-    q.w_dbpart = off; off = align_up(off + D * T * (size_t)q.MGc * G * 4, A);
     q.w_dc = off;     off = align_up(off + D * B * H * 4, A);
     q.w_dhc = off;    off = align_up(off + D * B * H * 4, A);
     q.w_dxc = off;    off = align_up(off + 2 * T * B * (size_t)q.kin_max * 4, A);
-    q.w_wpart = off;  off = align_up(off + (q.ts > 1 ? (size_t)q.ts * KM * G * 4 : 0), A);
+    q.w_wpart = off;  off = align_up(off + (q.ts > 1 ? (size_t)q.ts * (KM + 1) * G * 4 : 0), A);
     const size_t bwd = off;
     q.w_sync = align_up(fwd > bwd ? fwd : bwd, A);
     q.w_loss = q.w_sync + 8192;           // barrier counters (2), then the error flag at +4096
@@ -378,7 +376,6 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
                 pd.dcT = dcT ? dcT + (size_t)k * B * H : nullptr;
                 pd.da = W + P.w_da + (size_t)d * T * P.das * es;
                 pd.daT = W + P.w_daT + (size_t)d * T * G * BP * es;
-                pd.dbpart = (float*)(W + P.w_dbpart) + (size_t)d * T * P.MGc * G;
                 pd.dh0 = dh0 + (size_t)k * B * H;
                 pd.dc0 = dc0 + (size_t)k * B * H;
             }
@@ -434,7 +431,6 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
                 }
                 bd.da = W + P.w_da + ((size_t)d * T + t) * P.das * es;
                 bd.daT = W + P.w_daT + ((size_t)d * T + t) * G * BP * es;
-                bd.dbpart = (float*)(W + P.w_dbpart) + ((size_t)d * T + t) * P.MGc * G;
             }
             launch_bwd<E>(a, D, st);
         }
@@ -465,8 +461,10 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
             a.site = nv; a.K = kin; a.B = B; a.BP = BP; a.G = G; a.T = T; a.tper = tper;
             a.dense = !P.compact; a.s = P.s_nr;
             a.out = P.ts > 1 ? wpart : g->dW[k];
+            a.ostride = (long)(kin + 1) * G;
+            a.db = g->db[k];                      // the bias gradient rides on the input-weight pass
             launch_wgrad<E>(a, P.ts, st);
-            if (P.ts > 1) launch_wreduce(wpart, g->dW[k], (long)kin * G, P.ts, st);
+            if (P.ts > 1) launch_wreduce(wpart, g->dW[k], g->db[k], (long)kin * G, a.ostride, G, P.ts, st);
 
             WgArgs u = a;
             u.actT = rd + P.r_hrecT; u.tstride = (long)H * BP;
@@ -476,10 +474,11 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
             u.site = site_view(P, mbuf, P.site_rh(l, d));
             u.K = H; u.s = P.s_rh;
             u.out = P.ts > 1 ? wpart : g->dU[k];
+            u.ostride = (long)H * G;
+            u.db = nullptr;
             launch_wgrad<E>(u, P.ts, st);
-            if (P.ts > 1) launch_wreduce(wpart, g->dU[k], (long)H * G, P.ts, st);
+            if (P.ts > 1) launch_wreduce(wpart, g->dU[k], nullptr, (long)H * G, u.ostride, G, P.ts, st);
 
-            launch_db((const float*)(W + P.w_dbpart) + (size_t)d * T * P.MGc * G, g->db[k], G, T, P.MGc, st);
         }
     }
     return hip_check("backward launch");

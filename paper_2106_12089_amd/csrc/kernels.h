@@ -109,7 +109,6 @@ struct BwdDir {
     float* dcs;                         // [B][H] cell-gradient carry, in place
     void* da;                           // [B][G] DA_t (dtype)
     void* daT;                          // [G][BP] dtype (transposed)
-    float* dbpart;                      // [MG][G] for this t
     float* dh0;                         // final pass: [B][H]
     float* dc0;
     int t;
@@ -143,7 +142,10 @@ struct WgArgs {
     int t_first, shift;
     const void* daT;                    // [T][G][BP]
     SiteView site;
-    float* out;                         // [TS][K][G] partials (or dW when TS == 1)
+    float* out;                         // partial ts at out + ts*ostride: [K][G] (or dW when TS == 1)
+    long ostride;
+    float* db;                          // non-null: also the bias gradient (Eq. 11): row K of each
+                                        // partial when TS > 1, else db itself
     int K, B, BP, G, T, tper, dense;
     float s;
 };
@@ -191,7 +193,6 @@ struct PBwdDir {
     const float* dcT;                   // [B][H] or null
     void* da;                           // [T][B][4H] (exchange; also read by the dX product)
     void* daT;                          // [T][4H][BP]
-    float* dbpart;                      // [T][MGc][4H]
     float* dh0;                         // [B][H]
     float* dc0;                         // [B][H]
 };

@@ -513,21 +513,6 @@ __global__ void __launch_bounds__(1024) k_bwd(BwdArgs a) {
             }
         }
     }
-    if (a.final_pass) return;
-    // bias-gradient partial over this workgroup's rows: reuse red
-    __syncthreads();
-#pragma unroll
-    for (int g = 0; g < 4; ++g) red[g][rr][i] = da4[g];
-    __syncthreads();
-    if (threadIdx.x < 64) {
-        const int g = threadIdx.x >> 4, q = threadIdx.x & 15;
-        const int uq = units[q];
-        if (uq >= 0) {
-            float s = 0.f;
-            for (int r = 0; r < 64; ++r) s += red[g][r][q];
-            D.dbpart[(size_t)blockIdx.y * G + g * H + uq] = s;
-        }
-    }
 }
 
 // ---------------------------------------------------------------------------
@@ -703,8 +688,20 @@ __global__ void __launch_bounds__(512) k_wgrad(WgArgs a) {
     // batch chunks, and add the tiles into their LDS rows.  Tiles past nt
     // are multiplied too (their rows are absent): unconditional products
     // keep the loads out of branches.
+    // bias gradient (wave 0): the column sums of the DA^T fragments
+    const bool do_db = a.db != nullptr && w == 0;
+    float dbacc = 0.f;
+    auto db_add = [&](const Raw8<T>& f) {
+        if (sizeof(T) == 2) {
+#pragma unroll
+            for (int q = 0; q < NW; ++q) dbacc += __uint_as_float(f.w[q] << 16) + __uint_as_float(f.w[q] & 0xffff0000u);
+        } else {
+#pragma unroll
+            for (int q = 0; q < NW; ++q) dbacc += __uint_as_float(f.w[q]);
+        }
+    };
     auto finish = [&](__amdgpu_buffer_rsrc_t ar, __amdgpu_buffer_rsrc_t br, const int* kk, const int* la, int nt,
-                      Raw8<T>* fa, const Raw8<T>& fb0) {
+                      Raw8<T>* fa, const Raw8<T>& fb0, bool first_round) {
         f32x4_t acc[MAXT];
 #pragma unroll
         for (int i = 0; i < MAXT; ++i) {
@@ -719,6 +716,8 @@ __global__ void __launch_bounds__(512) k_wgrad(WgArgs a) {
             uint32_t pm[NW];
             pad_mask<T>(bc + g8, a.B, pm);
             raw_and(fb, pm);
+            if (n >= a.G) raw_and(fb, pmb);             // pmb is all zero past G
+            if (do_db && first_round) db_add(fb);
 #pragma unroll
             for (int i = 0; i < MAXT; ++i) {
                 raw_and(fa[i], pm);
@@ -768,28 +767,40 @@ __global__ void __launch_bounds__(512) k_wgrad(WgArgs a) {
         }
         __builtin_amdgcn_sched_barrier(0);     // keep the uses below the prefetch
         raw_and(fb0, pmb);
-        finish(ar, br, kc, la, min(ntile, MAXT), fa, fb0);
+        if (do_db) db_add(fb0);
+        finish(ar, br, kc, la, min(ntile, MAXT), fa, fb0, true);
         for (int jt0 = MAXT; jt0 < ntile; jt0 += MAXT) {
             int kv2[MAXT], mv2[MAXT];
             rows_issue(t, jt0, kv2, mv2);
             rows_resolve(t, jt0, kv2, mv2, kc, la);
             a_issue(ar, 0, kc, fa);
-            finish(ar, br, kc, la, min(ntile - jt0, MAXT), fa, fb0);
+            finish(ar, br, kc, la, min(ntile - jt0, MAXT), fa, fb0, false);
         }
     }
-    float* out = a.out + (size_t)blockIdx.y * a.K * a.G;
+    if (do_db) {                               // lanes l, l+16, l+32, l+48 hold column l
+        dbacc += __shfl_xor(dbacc, 16);
+        dbacc += __shfl_xor(dbacc, 32);
+        if (lane < 16 && n < a.G) {
+            if (gridDim.y == 1) a.db[n] = dbacc;
+            else a.out[(size_t)blockIdx.y * a.ostride + (size_t)a.K * a.G + n] = dbacc;
+        }
+    }
+    float* out = a.out + (size_t)blockIdx.y * a.ostride;
     for (int i = r0 * 16 + lane; i < r1 * 16; i += 64) {
         const int kr = i >> 4, cc = i & 15;
         if (n0 + cc < a.G) out[(size_t)kr * a.G + n0 + cc] = acc_lds[kr * WG_LD + cc];
     }
 }
 
-// dW = sum over ts of the partials
-__global__ void k_wreduce(const float* part, float* dW, long n, int ts) {
-    for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < n; i += (long)gridDim.x * blockDim.x) {
+// dW = sum over ts of the partials (each ostride floats apart); with db,
+// the row after the K*G gradient entries sums into db
+__global__ void k_wreduce(const float* part, float* dW, float* db, long n, long ostride, int G, int ts) {
+    const long nn = db ? n + G : n;
+    for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < nn; i += (long)gridDim.x * blockDim.x) {
         float s = 0.f;
-        for (int q = 0; q < ts; ++q) s += part[(size_t)q * n + i];
-        dW[i] = s;
+        for (int q = 0; q < ts; ++q) s += part[(size_t)q * ostride + i];
+        if (i < n) dW[i] = s;
+        else db[i - n] = s;
     }
 }
 
@@ -823,16 +834,6 @@ __global__ void k_expand(const float* dxc, int ldc, SiteView site, float* dx, in
         const int p = site.pos[(size_t)t * site.kmax + k];
         dx[i] = p >= 0 ? dxc[tb * ldc + p] : 0.0f;
     }
-}
-
-// db[n] = sum over t and row groups of dbpart[t][g][n]
-__global__ void k_db(const float* dbpart, float* db, int G, int T, int ng) {
-    const int n = blockIdx.x * blockDim.x + threadIdx.x;
-    if (n >= G) return;
-    float s = 0.f;
-    for (int t = 0; t < T; ++t)
-        for (int g = 0; g < ng; ++g) s += dbpart[((size_t)t * ng + g) * G + n];
-    db[n] = s;
 }
 
 // MSE loss gradient (a loss of the synthetic workloads).
@@ -1005,8 +1006,8 @@ void launch_wgrad(const WgArgs& a, int ts, hipStream_t st) {
     if (a.dense) launch_k(KID_WGRAD, k_wgrad<T, true>, grid, dim3(512), lds, st, a);
     else launch_k(KID_WGRAD, k_wgrad<T, false>, grid, dim3(512), lds, st, a);
 }
-void launch_wreduce(const float* part, float* dW, long n, int ts, hipStream_t st) {
-    launch_k(KID_NONE, k_wreduce, dim3(nblk(n, 256, 8192)), dim3(256), 0, st, part, dW, n, ts);
+void launch_wreduce(const float* part, float* dW, float* db, long n, long ostride, int G, int ts, hipStream_t st) {
+    launch_k(KID_NONE, k_wreduce, dim3(nblk(n + G, 256, 8192)), dim3(256), 0, st, part, dW, db, n, ostride, G, ts);
 }
 template <typename T>
 void launch_fwd_init(const void* h0, const float* c0, float* hT, float* cT, long n, hipStream_t st) {
@@ -1017,9 +1018,6 @@ void launch_bwd_init(const float* dhT, const float* dcT, float* dhc, float* dcs,
 }
 void launch_expand(const float* dxc, int ldc, const SiteView& s, float* dx, int B, int K, int T, hipStream_t st) {
     launch_k(KID_NONE, k_expand, dim3(nblk((long)T * B * K, 256)), dim3(256), 0, st, dxc, ldc, s, dx, B, K, T);
-}
-void launch_db(const float* dbpart, float* db, int G, int T, int ng, hipStream_t st) {
-    launch_k(KID_NONE, k_db, dim3((G + 255) / 256), dim3(256), 0, st, dbpart, db, G, T, ng);
 }
 void launch_mse(const float* y, const float* tg, const int32_t* lengths, float* dy, float* partial, int np,
                 float* loss, int T, int B, int F, hipStream_t st) {

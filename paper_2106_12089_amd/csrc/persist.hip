@@ -371,7 +371,7 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
                 ((T*)D.ybufT)[((size_t)t * a.ldy + u) * a.BP + b] = yv;
             }
         }
-        if (s + 1 < T_) prefetch(s + 1);
+        prefetch(s + 1);
     }
     // ---- final state (NaN if the barrier timed out)
     const bool failed = __hip_atomic_load(a.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0;
@@ -437,45 +437,44 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
         dcs[q] = (ok && D.dcT) ? D.dcT[(size_t)pb[q] * H + pu[q]] : 0.f;
     }
     // per-step inputs (independent of the recurrence), loaded one step ahead
-    float gt4[PPT][4], ctv[PPT], cpv[PPT], dyv[PPT];
-    bool vld[PPT];
-    int tile_kept = 0;                  // any unit of the tile kept at the step processed before
+    // from clamped (valid) addresses without branches; the pointwise uses
+    // them only for valid (row, unit) pairs.  For iteration s: the inputs of
+    // step t(s), and the masks of the tile's units at the step processed
+    // before it (whether the tile gets a recurrent gradient, Eq. 10).
+    float gt4[PPT][4], ctv[PPT], cpv[PPT], dyr[PPT], dxv[PPT];
+    int lenr[PPT], dxp[PPT], mkr[PPT];
+    auto step_t = [&](int s) { return d == 0 ? T_ - 1 - s : s; };
     auto prefetch = [&](int s) {
-        const int t = d == 0 ? T_ - 1 - s : s;
+        const int t = step_t(min(s, T_ - 1));
         const int tp = d == 0 ? t - 1 : t + 1;            // forward predecessor of t
+        const int tn = step_t(max(s - 1, 0));
 #pragma unroll
         for (int q = 0; q < PPT; ++q) {
-            const int b = pb[q], u = pu[q];
-            const bool ok = b < B && u < H;
-            vld[q] = ok && (a.lengths == nullptr || t < a.lengths[b]);
-            const float* gr = D.gates + ((size_t)t * B + b) * G;
+            const int bc = min(pb[q], B - 1), uc = min(pu[q], H - 1);
+            lenr[q] = a.lengths ? a.lengths[bc] : T_;
+            const float* gr = D.gates + ((size_t)t * B + bc) * G;
 #pragma unroll
-            for (int g = 0; g < 4; ++g) gt4[q][g] = ok ? gr[g * H + u] : 0.f;
-            ctv[q] = ok ? D.cres[((size_t)t * B + b) * H + u] : 0.f;
-            cpv[q] = !ok ? 0.f : (s == T_ - 1 ? D.c0[(size_t)b * H + u] : D.cres[((size_t)tp * B + b) * H + u]);
-            float v = 0.f;
-            if (vld[q]) {
-                if (D.dy) v = D.dy[((size_t)t * B + b) * a.ldy + u];
-                else if (D.dxc) {
-                    const int p = D.dxpos[(size_t)t * a.kmax + u];
-                    if (p >= 0) v = D.dxc[((size_t)t * B + b) * a.lddx + p];
-                }
-            }
-            dyv[q] = v;
+            for (int g = 0; g < 4; ++g) gt4[q][g] = gr[g * H + uc];
+            ctv[q] = D.cres[((size_t)t * B + bc) * H + uc];
+            cpv[q] = *(s >= T_ - 1 ? D.c0 + (size_t)bc * H + uc : D.cres + ((size_t)tp * B + bc) * H + uc);
+            if (D.dy) dyr[q] = D.dy[((size_t)t * B + bc) * a.ldy + uc];
+            else if (D.dxc) dxp[q] = D.dxpos[(size_t)t * a.kmax + uc];
+            mkr[q] = D.rh.mask[(size_t)tn * a.kmax + uc];
         }
     };
-    // whether the tile has a unit kept at step tn (the recurrent gradient of
-    // a dropped unit is exactly zero)
-    auto tile_any_kept = [&](int tn) {
-        __shared__ int any;
-        if (tid == 0) any = 0;
-        __syncthreads();
-        if (tid < UB) {
-            const int u = u0 + tid;
-            if (u < H && D.rh.mask[(size_t)tn * a.kmax + u]) any = 1;
-        }
-        __syncthreads();
-        return any;
+    // the layer above's input gradient at its compact position (a load that
+    // depends on dxp; issued right after the barrier, beside the DA loads)
+    auto fetch_dx = [&](int t) {
+        if (D.dy || !D.dxc) return;
+#pragma unroll
+        for (int q = 0; q < PPT; ++q)
+            dxv[q] = D.dxc[((size_t)t * B + min(pb[q], B - 1)) * a.lddx + max(dxp[q], 0)];
+    };
+    // whether the tile has a unit kept at the step processed before (the
+    // recurrent gradient of a dropped unit is exactly zero); a wave covers
+    // every unit of the tile
+    auto tile_any_kept = [&]() {
+        return __builtin_amdgcn_ballot_w64(pu[0] < H && mkr[0] != 0) != 0;
     };
 
     // the recurrent gradient of the tile's units from DA of step tn into red
@@ -523,14 +522,17 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
     prefetch(0);
     for (int s = 0; s <= T_; ++s) {
         const bool final_pass = s == T_;
-        const int t = final_pass ? -1 : (d == 0 ? T_ - 1 - s : s);
+        const int t = final_pass ? -1 : step_t(s);
         const int tn = d == 0 ? T_ - s : s - 1;            // step processed just before
         const bool has_next = s > 0;
-        int kept = 0;
+        bool kept = false;
         if (has_next) {
-            kept = tile_any_kept(tn);
+            kept = tile_any_kept();
             if (!grid_wait(bar, (unsigned)s * (unsigned)nslot, a.err, a.timeout)) break;
+            if (!final_pass) fetch_dx(t);
             if (kept) recurrent_product(tn);
+        } else {
+            fetch_dx(t);
         }
         float da4[PPT][4];
 #pragma unroll
@@ -542,7 +544,7 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
             float dh = dhc[q];
             if (kept) {
                 // units dropped at step tn get no recurrent gradient (output sparsity, Eq. 10)
-                const float sc = D.rh.mask[(size_t)tn * a.kmax + u] ? a.s : 0.0f;
+                const float sc = mkr[q] ? a.s : 0.0f;
                 dh += sc * reduced(b - m0, u - u0);
             }
             if (final_pass) {
@@ -550,8 +552,8 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
                 D.dc0[(size_t)b * H + u] = dcs[q];
                 continue;
             }
-            if (vld[q]) {
-                dh += dyv[q];
+            if (t < lenr[q]) {
+                dh += D.dy ? dyr[q] : (D.dxc && dxp[q] >= 0 ? dxv[q] : 0.0f);
                 const float ig = gt4[q][0], fg = gt4[q][1], gg = gt4[q][2], og = gt4[q][3];
                 const float tc = tanh_fast(ctv[q]);
                 const float dout = dh * tc;                            // Eq. 7
@@ -581,26 +583,7 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
 #pragma unroll
             for (int g = 0; g < 4; ++g) dat[(size_t)(g * H + u) * a.BP + b] = from_f32<T>(da4[q][g]);
         }
-        if (s + 1 < T_) prefetch(s + 1);
-        // bias-gradient partial over the tile's rows
-        float* rb = red;                                   // [MG][UB][4]
-#pragma unroll
-        for (int q = 0; q < PPT; ++q) {
-            const int p = tid + NTH * q;
-            if (p < MG * UB) {
-#pragma unroll
-                for (int g = 0; g < 4; ++g) rb[p * 4 + g] = da4[q][g];
-            }
-        }
-        __syncthreads();
-        if (tid < 4 * UB) {
-            const int i = tid >> 2, g = tid & 3, u = u0 + i;
-            if (u < H) {
-                float sum = 0.f;
-                for (int rr = 0; rr < MG; ++rr) sum += rb[(rr * UB + i) * 4 + g];
-                D.dbpart[((size_t)t * a.mgc + mg) * G + g * H + u] = sum;
-            }
-        }
+        prefetch(s + 1);
     }
     // a timed-out barrier poisons the input-state gradients
     if (__hip_atomic_load(a.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
