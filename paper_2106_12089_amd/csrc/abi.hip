@@ -25,7 +25,7 @@ template <typename T> void launch_dx(const DxArgs& a, int K, hipStream_t st);
 template <typename T> void launch_wgrad(const WgArgs& a, int ts, hipStream_t st);
 template <typename T> void launch_fwd_init(const void*, const float*, float*, float*, long, hipStream_t);
 void launch_wreduce(const float* part, float* dW, float* db, long n, long ostride, int G, int ts, hipStream_t st);
-void launch_bwd_init(const float*, const float*, float*, float*, long, hipStream_t);
+void launch_bwd_init(const float*, const float*, float*, float*, long, void*, int, int, int, long, long, hipStream_t);
 void launch_expand(const float*, int, const SiteView&, float*, int, int, int, hipStream_t);
 void launch_mse(const float*, const float*, const int32_t*, float*, float*, int, float*, int, int, int,
                 hipStream_t);
@@ -80,7 +80,7 @@ int make_plan(const lstm_sd_dims* d, Plan* p, const char** why) {
     q.BP = (q.B + 31) / 32 * 32;
     q.HP = (q.H + 7) / 8 * 8;
     q.mtiles = (q.B + 15) / 16;
-    q.das = (size_t)q.B * q.G;               // DA block per step: row-major [B][4H]
+    q.das = (size_t)((q.G + 31) / 32) * q.mtiles * 512;   // DA block per step: fragment-major [B][4H]
     q.hxs = (size_t)((q.H + 31) / 32) * q.mtiles * 512;
     q.MGc = (q.B + 63) / 64;
     q.sites = q.L + q.L * q.D;
@@ -343,7 +343,8 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
         float* dhc = (float*)(W + P.w_dhc);
         float* dcs = (float*)(W + P.w_dc);
         launch_bwd_init(dhT ? dhT + (size_t)l * D * B * H : nullptr, dcT ? dcT + (size_t)l * D * B * H : nullptr,
-                        dhc, dcs, (long)D * B * H, st);
+                        dhc, dcs, (long)D * B * H, l == L - 1 ? (void*)(W + P.w_da) : nullptr, (int)es, G,
+                        P.mtiles, (long)D * T, (long)P.das, st);
         float* dxc_above = (float*)(W + P.w_dxc) + (size_t)((l + 1) & 1) * T * B * P.kin_max;
         float* dxc_here = (float*)(W + P.w_dxc) + (size_t)(l & 1) * T * B * P.kin_max;
         bool persistent_done = false;

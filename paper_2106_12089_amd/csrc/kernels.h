@@ -89,7 +89,7 @@ struct StepArgs {
 // the pointwise backward (Eq. 7-9 and activation derivatives) at t.
 struct BwdDir {
     // recurrent gradient from the previously processed step (has_next)
-    const void* da_next;                // [B][G] DA of that step (dtype)
+    const void* da_next;                // DA of that step, fragment-major [B][G] (dtype)
     const uint8_t* nmask;               // RH mask row of that step
     const int32_t* nkeep;               // kept units of that step
     const int32_t* ncount;
@@ -107,7 +107,7 @@ struct BwdDir {
     const int32_t* dxpos;               // NR pos row of the layer above at t, + d*H
     float* dhc;                         // [B][H] pass-through carry, in place
     float* dcs;                         // [B][H] cell-gradient carry, in place
-    void* da;                           // [B][G] DA_t (dtype)
+    void* da;                           // DA_t, fragment-major [B][G] (dtype)
     void* daT;                          // [G][BP] dtype (transposed)
     float* dh0;                         // final pass: [B][H]
     float* dc0;
@@ -124,7 +124,7 @@ struct BwdArgs {
 // Output-sparse input gradient, all t, summed over directions:
 //   out[t][b][j] = s * m * sum_d sum_n DA_d[t][b][n] W_d[keep_t[j]][n]
 struct DxArgs {
-    const void* da[2];                  // DA_d [T][B][G]
+    const void* da[2];                  // DA_d [T] x fragment-major [B][G]
     const void* W[2];                   // [K][G]
     SiteView site;
     float* out;                         // [T][B][ldo]
@@ -191,7 +191,7 @@ struct PBwdDir {
     const int32_t* dxpos;               // NR pos of the layer above, + d*H (t stride kmax)
     const float* dhT;                   // [B][H] or null
     const float* dcT;                   // [B][H] or null
-    void* da;                           // [T][B][4H] (exchange; also read by the dX product)
+    void* da;                           // [T] x fragment-major [B][4H] (exchange; also read by the dX product)
     void* daT;                          // [T][4H][BP]
     float* dh0;                         // [B][H]
     float* dc0;                         // [B][H]

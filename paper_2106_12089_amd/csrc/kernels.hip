@@ -9,7 +9,8 @@
 // Layouts (B = batch, BP = B rounded up to 32, G = 4H):
 //   row-major activations [B][K]        forward products (gather along K)
 //   transposed activations [K][BP]      weight gradients (contiguous in b)
-//   DA [B][G] and DA^T [G][BP]          backward products / weight gradients
+//   DA [B][G] fragment-major            backward products (one 1 KB block per A fragment)
+//   DA^T [G][BP]                        weight gradients
 #include <hip/hip_runtime.h>
 #include <hip/hip_ext.h>
 
@@ -443,12 +444,12 @@ __global__ void __launch_bounds__(1024) k_bwd(BwdArgs a) {
                 if (mt < mtiles) {
                     const int row = m0 + mt * 16 + (lane & 15);
                     Frag<T> fa;
+                    // fragment-major DA: entries past B or 4H are never written
+                    ld4(DA + frag_lane_off(nc >> 5, (m0 >> 4) + mt, lane, a.mtiles), fa.v);
+                    ld4(DA + frag_lane_off(nc >> 5, (m0 >> 4) + mt, lane, a.mtiles) + 4, fa.v + 4);
 #pragma unroll
-                    for (int h = 0; h < 2; ++h) {
-                        const int n = nc + g8 + 4 * h;
-                        if (row < B && n < G) ld4(DA + (size_t)row * G + n, fa.v + 4 * h);
-                        else zero4(fa.v + 4 * h);
-                    }
+                    for (int e = 0; e < 8; ++e)
+                        if (row >= B || nc + g8 + e >= G) fa.v[e] = zero_val<T>();
                     mma_16x16x32(fa, fb, acc[mt]);
                 }
             }
@@ -503,12 +504,11 @@ __global__ void __launch_bounds__(1024) k_bwd(BwdArgs a) {
             } else {
                 D.dhc[(size_t)b * H + u] = dh;                         // frozen row: pass through
             }
-            T* dar = (T*)D.da + (size_t)b * G;
             T* dat = (T*)D.daT;
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
                 const T v = from_f32<T>(da4[g]);
-                dar[g * H + u] = v;
+                ((T*)D.da)[frag_off(b, g * H + u, a.mtiles)] = v;
                 dat[(size_t)(g * H + u) * a.BP + b] = v;
             }
         }
@@ -545,8 +545,10 @@ __global__ void __launch_bounds__(256) k_dx(DxArgs a) {
 #pragma unroll
     for (int i = 0; i < MT; ++i) acc[i] = f32x4_t{0, 0, 0, 0};
     for (int d = 0; d < a.D; ++d) {
-        // rows past B fall outside the DA_t resource and read as zero
-        const __amdgpu_buffer_rsrc_t dr = buf_rsrc((const T*)a.da[d] + (size_t)t * a.B * a.G, (uint32_t)a.B * a.G * ES);
+        // DA_t is fragment-major; rows past B hold stale values that only
+        // reach output rows that are never stored
+        const size_t das = (size_t)((a.G + 31) / 32) * a.mtiles * 512;
+        const __amdgpu_buffer_rsrc_t dr = buf_rsrc((const T*)a.da[d] + (size_t)t * das, (uint32_t)(das * ES));
         const __amdgpu_buffer_rsrc_t wr = buf_rsrc(a.W[d], (uint32_t)a.K * a.G * ES);
         const uint32_t woff = ((uint32_t)kr * a.G + g8) * ES;
         for (int nc0 = 32 * w; nc0 < a.G; nc0 += 128 * U) {
@@ -557,12 +559,12 @@ __global__ void __launch_bounds__(256) k_dx(DxArgs a) {
                 raw_load(fb[u], wr, woff + nc * ES);
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt)
-                    raw_load(fa[u][mt], dr, ((uint32_t)(m0 + 16 * mt + cl) * a.G + nc + g8) * ES);
+                    raw_load(fa[u][mt], dr, (uint32_t)(frag_lane_off(nc >> 5, (m0 >> 4) + mt, lane, a.mtiles) * ES));
             }
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const int nc = nc0 + 128 * u;
-                if (nc + 32 > a.G) {            // chunk reaches past G: zero the DA side there
+                if (nc + 32 > a.G) {            // chunk reaches past G: zero the DA side there (never written)
                     uint32_t m[Raw8<T>::NW];
                     pad_mask<T>(nc + g8, a.G, m);
 #pragma unroll
@@ -817,10 +819,22 @@ __global__ void k_fwd_init(const T* h0, const float* c0, float* hT, float* cT, l
 }
 
 // carries <- dhT/dcT slices (or zero)
-__global__ void k_bwd_init(const float* dhT, const float* dcT, float* dhc, float* dcs, long n) {
+// and, when da is given, zero the columns 4H .. (last 32-column chunk end)
+// of every fragment-major DA block (nblk blocks of das elements of es
+// bytes): no kernel writes them, and the backward products read them
+__global__ void k_bwd_init(const float* dhT, const float* dcT, float* dhc, float* dcs, long n,
+                           void* da, int es, int G, int mtiles, long nblk, long das) {
     for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < n; i += (long)gridDim.x * blockDim.x) {
         dhc[i] = dhT ? dhT[i] : 0.0f;
         dcs[i] = dcT ? dcT[i] : 0.0f;
+    }
+    const int padc = (G % 32) ? 32 - G % 32 : 0, rows = 16 * mtiles;
+    const long np = da ? nblk * rows * padc : 0;
+    for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < np; i += (long)gridDim.x * blockDim.x) {
+        const long blk = i / (rows * padc), rem = i % (rows * padc);
+        const size_t off = (size_t)blk * das + frag_off((int)(rem / padc), G + (int)(rem % padc), mtiles);
+        if (es == 2) ((uint16_t*)da)[off] = 0;
+        else ((uint32_t*)da)[off] = 0u;
     }
 }
 
@@ -1013,8 +1027,10 @@ template <typename T>
 void launch_fwd_init(const void* h0, const float* c0, float* hT, float* cT, long n, hipStream_t st) {
     launch_k(KID_NONE, k_fwd_init<T>, dim3(nblk(n, 256)), dim3(256), 0, st, (const T*)h0, c0, hT, cT, n);
 }
-void launch_bwd_init(const float* dhT, const float* dcT, float* dhc, float* dcs, long n, hipStream_t st) {
-    launch_k(KID_NONE, k_bwd_init, dim3(nblk(n, 256)), dim3(256), 0, st, dhT, dcT, dhc, dcs, n);
+void launch_bwd_init(const float* dhT, const float* dcT, float* dhc, float* dcs, long n, void* da, int es, int G,
+                     int mtiles, long nblocks, long das, hipStream_t st) {
+    launch_k(KID_NONE, k_bwd_init, dim3(nblk(n, 256)), dim3(256), 0, st, dhT, dcT, dhc, dcs, n, da, es, G, mtiles,
+             nblocks, das);
 }
 void launch_expand(const float* dxc, int ldc, const SiteView& s, float* dx, int B, int K, int T, hipStream_t st) {
     launch_k(KID_NONE, k_expand, dim3(nblk((long)T * B * K, 256)), dim3(256), 0, st, dxc, ldc, s, dx, B, K, T);

@@ -410,6 +410,7 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
     const int d = blockIdx.x / nslot, rem = blockIdx.x % nslot;
     const int tile = rem / a.mgroups, mg = rem % a.mgroups;
     const PBwdDir& D = a.d[d];
+    const size_t das = (size_t)((G + 31) / 32) * a.mtiles * 512;   // fragment-major DA block per step
     const int u0 = tile * UB, m0 = mg * MG;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int g8 = 8 * (lane >> 4);
@@ -479,9 +480,10 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
 
     // the recurrent gradient of the tile's units from DA of step tn into red
     auto recurrent_product = [&](int tn) {
-        // rows past B fall outside the DA_t resource (read as 0); columns
-        // past 4H meet the zero padding of the U rows
-        const __amdgpu_buffer_rsrc_t dr = buf_rsrc((const T*)D.da + (size_t)tn * B * G, (uint32_t)B * G * sizeof(T));
+        // DA_t is fragment-major: rows past B hold stale values that only
+        // reach output rows that are never used; the columns past 4H of the
+        // last chunk are zero (cleared before the backward pass)
+        const __amdgpu_buffer_rsrc_t dr = buf_rsrc((const T*)D.da + (size_t)tn * das, (uint32_t)(das * sizeof(T)));
         f32x4_t acc[MT];
 #pragma unroll
         for (int i = 0; i < MT; ++i) acc[i] = f32x4_t{0, 0, 0, 0};
@@ -494,7 +496,7 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
                 const int n = 32 * (c0 + w + NW * i) + g8;
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt)
-                    raw_load(fa[i][mt], dr, ((uint32_t)(m0 + mt * 16 + ul) * G + n) * (uint32_t)sizeof(T));
+                    raw_load(fa[i][mt], dr, (uint32_t)(frag_lane_off(c0 + w + NW * i, m0 / 16 + mt, lane, a.mtiles) * sizeof(T)));
             }
 #pragma unroll
             for (int i = 0; i < MAXC; ++i) {
@@ -567,9 +569,9 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
             } else {
                 dhc[q] = dh;                                           // frozen row: pass through
             }
-            T* dar = (T*)D.da + ((size_t)t * B + b) * G;
+            T* dar = (T*)D.da + (size_t)t * das;
 #pragma unroll
-            for (int g = 0; g < 4; ++g) xstore(dar + g * H + u, from_f32<T>(da4[q][g]));
+            for (int g = 0; g < 4; ++g) xstore(dar + frag_off(b, g * H + u, a.mtiles), from_f32<T>(da4[q][g]));
         }
         if (final_pass) break;
         grid_arrive(bar);                                  // DA_t is published
