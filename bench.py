@@ -34,13 +34,18 @@ METRIC = "LSTM fwd+BPTT step time & eff. TFLOP/s; speedup vs dense at p=0.5"
 PEAK_HBM_GBS = 8000.0
 PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
 KERNELS = ("fwd_persist", "step", "bwd_persist", "bwd", "wgrad", "fx", "dx")
-KERNEL_SRC = os.path.join(ROOT, "paper_2106_12089_amd", "csrc", "kernels.hip")
+KERNEL_SRC_DIR = os.path.join(ROOT, "paper_2106_12089_amd", "csrc")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
 
 def kernel_src_hash():
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of every HIP source and header the kernels are built from."""
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(KERNEL_SRC_DIR)):
+        if name.endswith((".hip", ".h")):
+            with open(os.path.join(KERNEL_SRC_DIR, name), "rb") as f:
+                h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
 
 
 # ---------------------------------------------------------------------------
@@ -307,6 +312,7 @@ def main(argv=None):
     ap.add_argument("--workload", default=WORKLOAD)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--no-nrrh", action="store_true", help="skip the NR+RH+ST runs")
+    ap.add_argument("--no-dense", action="store_true", help="skip the dense comparison runs (counter passes)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="also run a plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -331,7 +337,7 @@ def main(argv=None):
     wl = workloads.make_workload(cfg)
     p = 0.5 if 0.5 in cfg.p_values else cfg.p_values[0]
     head = run_mode(wl, p, 0.0, 1, args.steps, args.warmup, timed_kernels=KERNELS)
-    dense = run_mode(wl, p, 0.0, 0, args.steps, args.warmup)
+    dense = None if args.no_dense else run_mode(wl, p, 0.0, 0, args.steps, args.warmup)
     out = {
         "metric": METRIC,
         "value": round(head["flops"] / (head["ms"] * 1e-3) / 1e12, 4),
@@ -344,20 +350,20 @@ def main(argv=None):
                    "input_dim": cfg.input_dim, "hidden": cfg.hidden, "batch": cfg.batch,
                    "seq_len": cfg.seq_len, "p_nr": p, "p_rh": 0.0, "mode": "NR+ST"},
         "value_kind": "effective TFLOP/s over kept-row FLOPs",
-        "speedup_vs_dense": round(dense["ms"] / head["ms"], 4),
-        "dense_ms_per_step": round(dense["ms"], 4),
+        "speedup_vs_dense": round(dense["ms"] / head["ms"], 4) if dense else None,
+        "dense_ms_per_step": round(dense["ms"], 4) if dense else None,
         "gflop_per_step": round(head["flops"] / 1e9, 4),
         "dense_equiv_tflops": round(algorithmic_flops(dense_counts(cfg), cfg, wl.lengths)
                                     / (head["ms"] * 1e-3) / 1e12, 4),
         "phases_ms": {k: round(v, 4) for k, v in head["phases"].items()},
-        "phases_ms_dense": {k: round(v, 4) for k, v in dense["phases"].items()},
+        "phases_ms_dense": {k: round(v, 4) for k, v in dense["phases"].items()} if dense else None,
         "roofline": roofline(head, cfg),
     }
     if not args.no_nrrh:
         r = run_mode(wl, p, p, 1, args.steps, args.warmup)
-        rd = run_mode(wl, p, p, 0, args.steps, args.warmup)
-        out["nrrh"] = {"ms_per_step": round(r["ms"], 4), "dense_ms_per_step": round(rd["ms"], 4),
-                       "speedup_vs_dense": round(rd["ms"] / r["ms"], 4),
+        rd = None if args.no_dense else run_mode(wl, p, p, 0, args.steps, args.warmup)
+        out["nrrh"] = {"ms_per_step": round(r["ms"], 4), "dense_ms_per_step": round(rd["ms"], 4) if rd else None,
+                       "speedup_vs_dense": round(rd["ms"] / r["ms"], 4) if rd else None,
                        "tflops": round(r["flops"] / (r["ms"] * 1e-3) / 1e12, 4),
                        "phases_ms": {k: round(v, 4) for k, v in r["phases"].items()}}
     if args.calibrate_copy:
