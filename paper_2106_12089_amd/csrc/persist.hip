@@ -198,9 +198,10 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
     int cnt = 0, cnt_next = 0;
     constexpr int KPT = (LSTM_SD_MAX_K + NTH - 1) / NTH;   // keep-list entries per thread
     int kreg[KPT];
-    auto prefetch = [&](int s) {
-        const int t = d == 0 ? s : T_ - 1 - s;
-        const bool has_next = s + 1 < T_;
+    auto prefetch = [&](int s) {                  // s may be T_ (after the last step): clamped
+        const int sc = min(s, T_ - 1);
+        const int t = d == 0 ? sc : T_ - 1 - sc;
+        const bool has_next = sc + 1 < T_;
         const int tn = has_next ? (d == 0 ? t + 1 : t - 1) : t;
         cnt_next = D.rh.count[t];
         const int32_t* krow = D.rh.keep + (size_t)t * D.rh.kmax;
