@@ -32,7 +32,7 @@ void launch_mse(const float*, const float*, const int32_t*, float*, float*, int,
 int setup_kernel_attributes();
 bool timer_pair(int kid, hipEvent_t* e0, hipEvent_t* e1);
 template <typename T>
-hipError_t launch_fwd_persist(PFwdArgs& a, int D, hipStream_t st, int timer_on, hipEvent_t e0, hipEvent_t e1);
+hipError_t launch_fwd_persist(PFwdArgs& a, hipStream_t st, int timer_on, hipEvent_t e0, hipEvent_t e1);
 constexpr int KID_FWDP_ = 7;
 constexpr int KID_BWDP_ = 8;
 template <typename T>
@@ -82,6 +82,7 @@ int make_plan(const lstm_sd_dims* d, Plan* p, const char** why) {
     q.mtiles = (q.B + 15) / 16;
     q.das = (size_t)((q.G + 31) / 32) * q.mtiles * 512;   // DA block per step: fragment-major [B][4H]
     q.hxs = (size_t)((q.H + 31) / 32) * q.mtiles * 512;
+    q.xxs = (size_t)((q.D * q.H + 31) / 32) * q.mtiles * 512;
     q.MGc = (q.B + 63) / 64;
     q.sites = q.L + q.L * q.D;
     q.kin_max = q.L > 1 ? (q.I > q.D * q.H ? q.I : q.D * q.H) : q.I;
@@ -126,7 +127,8 @@ int make_plan(const lstm_sd_dims* d, Plan* p, const char** why) {
     off = 0;
     q.w_gx = off;   off = align_up(off + D * T * B * G * 4, A);
     q.w_hrec = off; off = align_up(off + D * 2 * B * (size_t)q.HP * es, A);
-    q.w_hx = off;   off = align_up(off + D * 2 * (size_t)q.hxs * es, A);
+    q.w_hx = off;   off = align_up(off + (D > (size_t)q.L ? D : (size_t)q.L) * 2 * (size_t)q.hxs * es, A);
+    q.w_xx = off;   off = align_up(off + (size_t)(q.L - 1) * T * q.xxs * es, A);
     const size_t fwd = off;
     off = 0;
     q.w_da = off;     off = align_up(off + D * T * (size_t)q.das * es, A);
@@ -144,6 +146,12 @@ int make_plan(const lstm_sd_dims* d, Plan* p, const char** why) {
 
 // Persistent recurrent kernels are used unless LSTM_SD_PERSIST=0 (a debug
 // switch that forces the per-step kernels).
+// LSTM_SD_STACK=0 runs a unidirectional stack one layer per launch
+static bool use_stacked() {
+    const char* v = getenv("LSTM_SD_STACK");
+    return !(v && v[0] == '0');
+}
+
 static bool use_persistent() {
     const char* v = getenv("LSTM_SD_PERSIST");
     return !(v && v[0] == '0');
@@ -240,6 +248,85 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
         t.src = h0; t.dst = R + P.r_h0T; t.K = H;
         launch_transpose<E>(t, L * D, st);
     }
+    // Unidirectional stack: every layer's recurrence in one persistent
+    // launch, layer l one step behind layer l-1, each layer above the first
+    // computing its input product from what the layer below published.
+    auto fill_slot = [&](PFwdDir& pd, int l, int d) {
+        const int k = l * D + d;
+        char* rd = R + P.rdir(l, d);
+        pd.h0 = (const char*)h0 + (size_t)k * B * H * es;
+        pd.U = w->U[k];
+        pd.gx = (const float*)(W + P.w_gx) + (size_t)d * T * B * G;
+        pd.c0 = c0 + (size_t)k * B * H;
+        pd.rh = site_view(P, mbuf, P.site_rh(l, d));
+        pd.gates = (float*)(rd + P.r_gates);
+        pd.cres = (float*)(rd + P.r_c);
+        pd.hrecT = rd + P.r_hrecT;
+        pd.hT = hT + (size_t)k * B * H;
+        pd.cT = cT + (size_t)k * B * H;
+        pd.dir = d;
+        pd.below = -1;
+        if (l == L - 1) {
+            pd.y = y + d * H;
+        } else {
+            pd.ybuf = R + P.rybuf(l) + (size_t)d * H * es;
+            pd.ybufT = R + P.rybufT(l) + (size_t)d * H * BP * es;
+        }
+    };
+    auto common_args = [&](PFwdArgs& pa) {
+        memset(&pa, 0, sizeof(pa));
+        pa.lengths = lengths;
+        pa.bar = (unsigned*)(W + P.w_sync);
+        pa.err = (int*)(W + P.w_sync + 4096);
+        pa.timeout = barrier_timeout_ticks();
+        pa.B = B; pa.H = H; pa.HP = P.HP; pa.T = T; pa.BP = BP; pa.ldy = D * H; pa.dense = !P.compact;
+        pa.mtiles = P.mtiles;
+        pa.s = P.s_rh; pa.s_nr = P.s_nr;
+        pa.xxs = P.xxs;
+    };
+    auto launch_fx_layer = [&](int l) {
+        const int kin = P.kin(l);
+        const void* X = l == 0 ? x : (const void*)(R + P.rybuf(l - 1));
+        for (int d = 0; d < D; ++d) {
+            FxArgs f;
+            f.X = X; f.ldx = kin;
+            f.W = w->W[l * D + d];
+            f.bias = w->b[l * D + d];
+            f.site = site_view(P, mbuf, P.site_nr(l));
+            f.Gx = (float*)(W + P.w_gx) + (size_t)d * T * B * G;
+            f.K = kin; f.B = B; f.G = G; f.T = T; f.dense = !P.compact; f.s = P.s_nr;
+            launch_fx<E>(f, st);
+        }
+    };
+    if (use_persistent() && use_stacked() && D == 1 && L > 1 && L <= 4) {
+        launch_fx_layer(0);
+        PFwdArgs pa;
+        common_args(pa);
+        pa.nslots = L;
+        pa.kin_max = P.kin(1);
+        pa.KP = fwd_hp(pa.kin_max);
+        for (int l = 0; l < L; ++l) {
+            PFwdDir& pd = pa.d[l];
+            fill_slot(pd, l, 0);
+            pd.hx = W + P.w_hx + (size_t)l * 2 * P.hxs * es;
+            if (l > 0) {
+                pd.Win = w->W[l];
+                pd.bias = w->b[l];
+                pd.nr = site_view(P, mbuf, P.site_nr(l));
+                pd.xin = W + P.w_xx + (size_t)(l - 1) * T * P.xxs * es;
+                pd.kin = P.kin(l);
+                pd.below = l - 1;
+            }
+            if (l < L - 1) {
+                pd.xout = W + P.w_xx + (size_t)l * T * P.xxs * es;
+                pd.nr_up = site_view(P, mbuf, P.site_nr(l + 1));
+            }
+        }
+        hipEvent_t e0 = nullptr, e1 = nullptr;
+        const bool timed = timer_pair(KID_FWDP_, &e0, &e1);
+        if (launch_fwd_persist<E>(pa, st, timed, e0, e1) == hipSuccess) return hip_check("forward launch");
+        (void)hipGetLastError();              // does not fit: one layer at a time below
+    }
     for (int l = 0; l < L; ++l) {
         const int kin = P.kin(l);
         const void* X = l == 0 ? x : (const void*)(R + P.rybuf(l - 1));
@@ -255,39 +342,15 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
         }
         if (use_persistent()) {
             PFwdArgs pa;
-            memset(&pa, 0, sizeof(pa));
-            pa.lengths = lengths;
-            pa.bar = (unsigned*)(W + P.w_sync);
-            pa.err = (int*)(W + P.w_sync + 4096);
-            pa.timeout = barrier_timeout_ticks();
-            pa.B = B; pa.H = H; pa.HP = P.HP; pa.T = T; pa.BP = BP; pa.ldy = D * H; pa.dense = !P.compact;
-            pa.mtiles = P.mtiles;
-            pa.s = P.s_rh;
+            common_args(pa);
+            pa.nslots = D;
             for (int d = 0; d < D; ++d) {
-                const int k = l * D + d;
-                char* rd = R + P.rdir(l, d);
-                PFwdDir& pd = pa.d[d];
-                pd.h0 = (const char*)h0 + (size_t)k * B * H * es;
-                pd.U = w->U[k];
-                pd.gx = (const float*)(W + P.w_gx) + (size_t)d * T * B * G;
-                pd.c0 = c0 + (size_t)k * B * H;
-                pd.rh = site_view(P, mbuf, P.site_rh(l, d));
-                pd.gates = (float*)(rd + P.r_gates);
-                pd.cres = (float*)(rd + P.r_c);
-                pd.hrecT = rd + P.r_hrecT;
-                pd.hx = W + P.w_hx + (size_t)d * 2 * P.hxs * es;
-                pd.hT = hT + (size_t)k * B * H;
-                pd.cT = cT + (size_t)k * B * H;
-                if (l == L - 1) {
-                    pd.y = y + d * H;
-                } else {
-                    pd.ybuf = R + P.rybuf(l) + (size_t)d * H * es;
-                    pd.ybufT = R + P.rybufT(l) + (size_t)d * H * BP * es;
-                }
+                fill_slot(pa.d[d], l, d);
+                pa.d[d].hx = W + P.w_hx + (size_t)d * 2 * P.hxs * es;
             }
             hipEvent_t e0 = nullptr, e1 = nullptr;
             const bool timed = timer_pair(KID_FWDP_, &e0, &e1);
-            if (launch_fwd_persist<E>(pa, D, st, timed, e0, e1) == hipSuccess) continue;
+            if (launch_fwd_persist<E>(pa, st, timed, e0, e1) == hipSuccess) continue;
             (void)hipGetLastError();          // does not fit: per-step kernels below
         }
         for (int s = 0; s < T; ++s) {

@@ -42,12 +42,15 @@ __device__ __forceinline__ void grid_arrive(unsigned* bar) {
 
 // Wait until the counter reaches target.  Returns false on time-out or when
 // another workgroup has timed out (err set).
-__device__ __forceinline__ bool grid_wait(unsigned* bar, unsigned target, int* err, long long timeout) {
+// With seen (LDS), thread 0 also records the last counter value it read.
+__device__ __forceinline__ bool grid_wait(unsigned* bar, unsigned target, int* err, long long timeout,
+                                          unsigned* seen = nullptr) {
     __shared__ int ok;
     if (threadIdx.x == 0) {
         int good = 1;
         const long long t0 = wall_clock64();
-        while (__hip_atomic_load(bar, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+        unsigned v;
+        while ((v = __hip_atomic_load(bar, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) < target) {
             if (__hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) { good = 0; break; }
             if (wall_clock64() - t0 > timeout) {
                 __hip_atomic_fetch_or(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -59,6 +62,7 @@ __device__ __forceinline__ bool grid_wait(unsigned* bar, unsigned target, int* e
         // the plain loads that follow fetch what other workgroups published
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
         ok = good;
+        if (seen) *seen = v;
     }
     __syncthreads();
     return ok != 0;
@@ -130,20 +134,24 @@ __device__ __forceinline__ void lds8(const float* p, float* o) {
 }
 
 // ---------------------------------------------------------------------------
-// Persistent forward recurrence (Eq. 1-6) of one layer, both directions.
-// Workgroup w -> (direction, unit tile, row group).  A unit tile is 4*NT
-// hidden units = NT 16-column MFMA tiles (the four gates of 4 units each);
-// a row group is MG batch rows.  512 threads = 8 waves; the contraction over
-// the kept recurrent neurons is split over the waves (each wave issues all of
-// its exchange loads before its first MFMA) and reduced in LDS.
+// Persistent forward recurrence (Eq. 1-6).  A launch runs every step of its
+// slots: the two directions of one layer, or every layer of a
+// unidirectional stack (layer l then works on step t while layer l-1 works on
+// step t+1; each layer computes its own input product from the output the
+// layer below published, so no separate input-product pass is needed above
+// the first layer).
+// Workgroup w -> (slot, unit tile, row group).  A unit tile is 4*NT hidden
+// units = NT 16-column MFMA tiles (the four gates of 4 units each); a row
+// group is MG batch rows.  512 threads = 8 waves; each contraction over kept
+// neurons is split over the waves (each wave issues all of its exchange
+// loads before its first MFMA) and reduced in LDS.
 // Dynamic LDS: U slice transposed [16*NT][HP] (dtype; HP = H rounded up to
-// 32, plus 8, zero past H), keep list [H+32] (int16), reduction
-// [8][MG][16*NT] (float).  With every recurrent neuron kept (the keep list is
-// the identity) a B fragment is one 16-byte LDS read per column tile;
-// otherwise its 8 rows are gathered through the keep list.
+// 32, plus 8, zero past H), the W slice likewise [16*NT][KP] when a slot
+// computes its input product, keep lists [H+32] and [kin_max+32] (int16),
+// reduction [8][MG][16*NT] (float).  With every neuron of a contraction kept
+// (its keep list is the identity) a B fragment is one 16-byte LDS read per
+// column tile; otherwise its 8 rows are gathered through the keep list.
 constexpr int PF_NW = 8;
-
-__host__ __device__ inline int fwd_hp(int H) { return (H + 31) / 32 * 32 + 8; }
 
 template <typename T, int NT, int MG>
 __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
@@ -153,10 +161,12 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
     constexpr int MAXC = MT <= 2 ? 3 : 2;       // chunks per wave per round (registers)
     extern __shared__ __align__(16) char smem[];
     const int H = a.H, G = 4 * H, B = a.B, T_ = a.T;
-    const int HP = fwd_hp(H);
+    const int HP = fwd_hp(H), KP = a.KP;
     T* Ut = (T*)smem;
-    int16_t* kidx = (int16_t*)(smem + (((size_t)NC * HP * sizeof(T) + 15) & ~(size_t)15));
-    float* red = (float*)((char*)kidx + (((size_t)(H + 32) * 2 + 15) & ~(size_t)15));
+    T* Wt = (T*)(smem + (((size_t)NC * HP * sizeof(T) + 15) & ~(size_t)15));
+    int16_t* kidx = (int16_t*)((char*)Wt + (((size_t)NC * KP * sizeof(T) + 15) & ~(size_t)15));
+    int16_t* kidx_x = kidx + (((H + 32) + 7) & ~7);
+    float* red = (float*)((char*)kidx_x + (KP ? (((size_t)(a.kin_max + 32) * 2 + 15) & ~(size_t)15) : 0));
 
     const int nslot = a.ntiles * a.mgroups;
     const int d = blockIdx.x / nslot, rem = blockIdx.x % nslot;
@@ -166,8 +176,14 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int g8 = 8 * (lane >> 4);
     unsigned* bar = a.bar + d;
+    unsigned* bar_below = D.below >= 0 ? a.bar + D.below : nullptr;
+    __shared__ unsigned below_seen;               // last value of the layer below's counter read
+    unsigned seen_below = 0;                      // its copy in every thread
+    const bool has_x = D.Win != nullptr;
+    const int kin = D.kin;
 
-    // U slice -> LDS, transposed: row c = nt*16 + g*4 + cu holds U[k][g*H + u0 + 4nt + cu]
+    // U slice (and W slice) -> LDS, transposed: row c = nt*16 + g*4 + cu holds
+    // column g*H + u0 + 4nt + cu of the weight
     {
         const T* U = (const T*)D.U;
         for (int i = tid; i < HP * NC; i += NTH) {
@@ -176,9 +192,18 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
             const int u = u0 + 4 * nt + (cc & 3);
             Ut[c * HP + k] = (u < H && k < H) ? U[(size_t)k * G + (cc >> 2) * H + u] : zero_val<T>();
         }
+        if (has_x) {
+            const T* Wi = (const T*)D.Win;
+            for (int i = tid; i < KP * NC; i += NTH) {
+                const int k = i / NC, c = i % NC;
+                const int nt = c >> 4, cc = c & 15;
+                const int u = u0 + 4 * nt + (cc & 3);
+                Wt[c * KP + k] = (u < H && k < kin) ? Wi[(size_t)k * G + (cc >> 2) * H + u] : zero_val<T>();
+            }
+        }
     }
     // register state of this thread's (row, unit) pairs
-    float creg[PPT], hreg[PPT];
+    float creg[PPT], hreg[PPT], biasr[PPT][4];
     int pb[PPT], pu[PPT];
 #pragma unroll
     for (int q = 0; q < PPT; ++q) {
@@ -189,37 +214,52 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
         const bool ok = pb[q] < B && pu[q] < H;
         creg[q] = ok ? D.c0[(size_t)pb[q] * H + pu[q]] : 0.f;
         hreg[q] = ok ? to_f32<T>(((const T*)D.h0)[(size_t)pb[q] * H + pu[q]]) : 0.f;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) biasr[q][g] = has_x ? D.bias[g * H + min(pu[q], H - 1)] : 0.f;
     }
     // per-step inputs that do not depend on the recurrence, loaded one step
     // ahead from clamped (valid) addresses without branches; pointwise uses
     // them only for valid (row, unit) pairs
     float gxr[PPT][4];
-    int pn[PPT], mnr[PPT], lenr[PPT];
-    int cnt = 0, cnt_next = 0;
+    int pn[PPT], mnr[PPT], lenr[PPT], pup[PPT], mup[PPT];
+    int cnt = 0, cnt_next = 0, cnt_x = 0, cnt_x_next = 0;
     constexpr int KPT = (LSTM_SD_MAX_K + NTH - 1) / NTH;   // keep-list entries per thread
-    int kreg[KPT];
+    int kreg[KPT], kreg_x[KPT];
+    auto step_t = [&](int s) { return D.dir == 0 ? s : T_ - 1 - s; };
     auto prefetch = [&](int s) {                  // s may be T_ (after the last step): clamped
         const int sc = min(s, T_ - 1);
-        const int t = d == 0 ? sc : T_ - 1 - sc;
+        const int t = step_t(sc);
         const bool has_next = sc + 1 < T_;
-        const int tn = has_next ? (d == 0 ? t + 1 : t - 1) : t;
+        const int tn = has_next ? step_t(sc + 1) : t;
         cnt_next = D.rh.count[t];
         const int32_t* krow = D.rh.keep + (size_t)t * D.rh.kmax;
 #pragma unroll
         for (int i = 0; i < KPT; ++i) kreg[i] = krow[min(tid + NTH * i, D.rh.kmax - 1)];
+        if (has_x) {
+            cnt_x_next = D.nr.count[t];
+            const int32_t* kx = D.nr.keep + (size_t)t * D.nr.kmax;
+#pragma unroll
+            for (int i = 0; i < KPT; ++i) kreg_x[i] = kx[min(tid + NTH * i, D.nr.kmax - 1)];
+        }
 #pragma unroll
         for (int q = 0; q < PPT; ++q) {
             const int bc = min(pb[q], B - 1), uc = min(pu[q], H - 1);
+            if (!has_x) {
 #pragma unroll
-            for (int g = 0; g < 4; ++g) gxr[q][g] = D.gx[((size_t)t * B + bc) * G + g * H + uc];
+                for (int g = 0; g < 4; ++g) gxr[q][g] = D.gx[((size_t)t * B + bc) * G + g * H + uc];
+            }
             pn[q] = has_next ? D.rh.pos[(size_t)tn * D.rh.kmax + uc] : -1;
             mnr[q] = D.rh.mask[(size_t)tn * D.rh.kmax + uc];
             lenr[q] = a.lengths ? a.lengths[bc] : T_;
+            if (D.xout) {
+                pup[q] = D.nr_up.pos[(size_t)t * D.nr_up.kmax + uc];
+                mup[q] = D.nr_up.mask[(size_t)t * D.nr_up.kmax + uc];
+            }
         }
     };
     auto is_valid = [&](int q, int t) { return pb[q] < B && pu[q] < H && t < lenr[q]; };
 
-    // the keep list of the coming step, from registers to LDS
+    // the keep lists of the coming step, from registers to LDS
     auto commit_kidx = [&]() {
         cnt = cnt_next;
 #pragma unroll
@@ -227,10 +267,86 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
             const int j = tid + NTH * i;
             if (j < cnt) kidx[j] = (int16_t)kreg[i];
         }
+        if (has_x) {
+            cnt_x = cnt_x_next;
+#pragma unroll
+            for (int i = 0; i < KPT; ++i) {
+                const int j = tid + NTH * i;
+                if (j < cnt_x) kidx_x[j] = (int16_t)kreg_x[i];
+            }
+        }
+    };
+
+    // acc += (compacted A from the exchange) x (weight slice rows of the keep
+    // list), in rounds of NW*MAXC 32-neuron chunks.  src holds one step's
+    // fragment-major slot of slot_elems elements, Bt the transposed weight
+    // slice of pitch bp, kfull the contraction length when nothing is
+    // dropped.  issue() loads the A fragments of round c0 (chunks past the
+    // slot read as 0; rows past B hold stale values that only reach output
+    // rows that are never used); compute() multiplies every chunk slot of the
+    // round (slots past the keep count have a zeroed A side and read B rows at
+    // offset 0: no branch lets the compiler sink the loads into the products).
+    auto issue = [&](const T* src, size_t slot_elems, int c0, Raw8<T> (&fa)[MAXC][MT]) {
+        const __amdgpu_buffer_rsrc_t hr = buf_rsrc(src, (uint32_t)(slot_elems * sizeof(T)));
+#pragma unroll
+        for (int i = 0; i < MAXC; ++i) {
+            const int c = c0 + w + NW * i;
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+                raw_load(fa[i][mt], hr, (uint32_t)(frag_lane_off(c, m0 / 16 + mt, lane, a.mtiles) * sizeof(T)));
+        }
+    };
+    auto compute = [&](Raw8<T> (&fa)[MAXC][MT], int c0, int n, const int16_t* kid, const T* Bt, int bp, int kfull,
+                       f32x4_t (&acc)[MT][NT]) {
+#pragma unroll
+        for (int i = 0; i < MAXC; ++i) {
+            const int kc = 32 * (c0 + w + NW * i);
+            Raw8<T> fbr[NT];
+            if (n == kfull) {                   // identity keep list: contiguous rows
+                const int kb = kc < n ? kc : 0;
+#pragma unroll
+                for (int nt = 0; nt < NT; ++nt) raw_lds(fbr[nt], Bt + (size_t)(nt * 16 + (lane & 15)) * bp + kb + g8);
+            } else {
+                const int4 k8 = *(const int4*)(kid + kc + g8);          // 8 int16 keep indices
+                const int kw[4] = {k8.x, k8.y, k8.z, k8.w};
+                int kk[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const int j = kc + g8 + e;
+                    kk[e] = j < n ? (int)(int16_t)(kw[e >> 1] >> (16 * (e & 1))) : 0;
+                }
+#pragma unroll
+                for (int nt = 0; nt < NT; ++nt) {
+                    const T* row = Bt + (size_t)(nt * 16 + (lane & 15)) * bp;
+                    Frag<T> fb;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) fb.v[e] = row[kk[e]];
+                    raw_from(fbr[nt], fb);
+                }
+            }
+            if (kc + 32 > n) {                  // last chunk: slots past the keep count hold stale values
+                uint32_t m[Raw8<T>::NW];
+                pad_mask<T>(kc + g8, n, m);
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) raw_and(fa[i][mt], m);
+            }
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int nt = 0; nt < NT; ++nt) raw_mma(fa[i][mt], fbr[nt], acc[mt][nt]);
+        }
+    };
+    auto contract = [&](const T* src, size_t slot_elems, int n, const int16_t* kid, const T* Bt, int bp, int kfull,
+                        f32x4_t (&acc)[MT][NT]) {
+        for (int c0 = 0; c0 < (n + 31) / 32; c0 += NW * MAXC) {
+            Raw8<T> fa[MAXC][MT];
+            issue(src, slot_elems, c0, fa);
+            compute(fa, c0, n, kid, Bt, bp, kfull, acc);
+        }
     };
 
     // prologue: h0 compacted by the keep list of the first step
-    const int tfirst = d == 0 ? 0 : T_ - 1;
+    const int tfirst = step_t(0);
     {
         const int32_t* pos = D.rh.pos + (size_t)tfirst * D.rh.kmax;
         const uint8_t* msk = D.rh.mask + (size_t)tfirst * D.rh.kmax;
@@ -248,73 +364,45 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
     prefetch(0);
     grid_arrive(bar);
 
+    const size_t hxs = (size_t)((H + 31) / 32) * a.mtiles * 512;     // elements per h slot
     for (int s = 0; s < T_; ++s) {
-        const int t = d == 0 ? s : T_ - 1 - s;
-        // ---- wait for h_{t-1} of every workgroup of this direction
+        const int t = step_t(s);
+        // ---- wait for h_{t-1} of every workgroup of this slot (and for the
+        // layer below to have published x_t)
         commit_kidx();
+        // x_t of the layer below (which runs ahead: a counter value seen
+        // earlier usually covers this step), then h_{t-1} of this slot
+        // (the skip decision uses a register copy taken after the wait's
+        // barrier: every thread must take the same branch around the waits)
+        if (has_x && seen_below < (unsigned)(s + 2) * (unsigned)nslot) {
+            if (!grid_wait(bar_below, (unsigned)(s + 2) * (unsigned)nslot, a.err, a.timeout, &below_seen)) break;
+            seen_below = below_seen;
+        }
         if (!grid_wait(bar, (unsigned)(s + 1) * (unsigned)nslot, a.err, a.timeout)) break;
-        const size_t hxs = (size_t)((H + 31) / 32) * a.mtiles * 512;     // elements per slot
-        const T* hc = (const T*)D.hx + (size_t)(s & 1) * hxs;
-        f32x4_t acc[MT][NT];
+        f32x4_t acc[MT][NT], accx[MT][NT];
 #pragma unroll
         for (int i = 0; i < MT; ++i)
 #pragma unroll
-            for (int j = 0; j < NT; ++j) acc[i][j] = f32x4_t{0, 0, 0, 0};
-        const int nch = (cnt + 31) / 32;
-        // chunks past the slot read as 0; rows past B hold stale values that
-        // only reach output rows that are never used
-        const __amdgpu_buffer_rsrc_t hr = buf_rsrc(hc, (uint32_t)(hxs * sizeof(T)));
-        for (int c0 = 0; c0 < nch; c0 += NW * MAXC) {
-            // issue every exchange load of this round first
-            Raw8<T> fa[MAXC][MT];
-#pragma unroll
-            for (int i = 0; i < MAXC; ++i) {
-                const int c = c0 + w + NW * i;
-#pragma unroll
-                for (int mt = 0; mt < MT; ++mt)
-                    raw_load(fa[i][mt], hr, (uint32_t)(frag_lane_off(c, m0 / 16 + mt, lane, a.mtiles) * sizeof(T)));
-            }
-            // every chunk slot of the round is multiplied (slots past the keep
-            // count have a zeroed A side and read B rows at offset 0): no
-            // branch lets the compiler sink the loads above into the products
-#pragma unroll
-            for (int i = 0; i < MAXC; ++i) {
-                const int kc = 32 * (c0 + w + NW * i);
-                Raw8<T> fbr[NT];
-                if (cnt == H) {                 // identity keep list: contiguous rows
-                    const int kb = kc < cnt ? kc : 0;
-#pragma unroll
-                    for (int nt = 0; nt < NT; ++nt) raw_lds(fbr[nt], Ut + (size_t)(nt * 16 + (lane & 15)) * HP + kb + g8);
-                } else {
-                    const int4 k8 = *(const int4*)(kidx + kc + g8);     // 8 int16 keep indices
-                    const int kw[4] = {k8.x, k8.y, k8.z, k8.w};
-                    int kk[8];
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        const int j = kc + g8 + e;
-                        kk[e] = j < cnt ? (int)(int16_t)(kw[e >> 1] >> (16 * (e & 1))) : 0;
-                    }
-#pragma unroll
-                    for (int nt = 0; nt < NT; ++nt) {
-                        const T* row = Ut + (size_t)(nt * 16 + (lane & 15)) * HP;
-                        Frag<T> fb;
-#pragma unroll
-                        for (int e = 0; e < 8; ++e) fb.v[e] = row[kk[e]];
-                        raw_from(fbr[nt], fb);
-                    }
-                }
-                if (kc + 32 > cnt) {            // last chunk: slots past the keep count hold stale values
-                    uint32_t m[Raw8<T>::NW];
-                    pad_mask<T>(kc + g8, cnt, m);
-#pragma unroll
-                    for (int mt = 0; mt < MT; ++mt) raw_and(fa[i][mt], m);
-                }
-#pragma unroll
-                for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-                    for (int nt = 0; nt < NT; ++nt) raw_mma(fa[i][mt], fbr[nt], acc[mt][nt]);
-            }
+            for (int j = 0; j < NT; ++j) acc[i][j] = accx[i][j] = f32x4_t{0, 0, 0, 0};
+        const T* hsrc = (const T*)D.hx + (size_t)(s & 1) * hxs;
+        const T* xsrc = has_x ? (const T*)D.xin + (size_t)t * a.xxs : nullptr;
+        if (has_x && cnt <= 32 * NW * MAXC && cnt_x <= 32 * NW * MAXC) {
+            // one round each: both sets of exchange loads go out together
+            Raw8<T> fh[MAXC][MT], fx[MAXC][MT];
+            issue(hsrc, hxs, 0, fh);
+            issue(xsrc, a.xxs, 0, fx);
+            compute(fh, 0, cnt, kidx, Ut, HP, H, acc);
+            compute(fx, 0, cnt_x, kidx_x, Wt, KP, kin, accx);
+        } else {
+            contract(hsrc, hxs, cnt, kidx, Ut, HP, H, acc);
+            if (has_x) contract(xsrc, a.xxs, cnt_x, kidx_x, Wt, KP, kin, accx);
         }
+#pragma unroll
+        for (int i = 0; i < MT; ++i)
+#pragma unroll
+            for (int j = 0; j < NT; ++j)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) acc[i][j][r] = a.s * acc[i][j][r] + a.s_nr * accx[i][j][r];
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -323,7 +411,7 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
                 for (int r = 0; r < 4; ++r)
                     red[(w * MG + mt * 16 + acc_row(lane, r)) * NC + nt * 16 + (lane & 15)] = acc[mt][nt][r];
         __syncthreads();
-        // ---- pointwise (Eq. 1-6); h_t is published first
+        // ---- pointwise (Eq. 1-6); h_t (and the layer above's x_t) is published first
         T* hxn = (T*)D.hx + (size_t)((s + 1) & 1) * hxs;
         float og4[PPT][4], cnv[PPT], hnv[PPT];
 #pragma unroll
@@ -338,7 +426,7 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
                 float v = 0.f;
 #pragma unroll
                 for (int i = 0; i < NW; ++i) v += red[(i * MG + rr) * NC + cc];
-                pre[g] = a.s * v + gxr[q][g];
+                pre[g] = v + (has_x ? biasr[q][g] : gxr[q][g]);
             }
             og4[q][0] = sigmoid_fast(pre[0]);
             og4[q][1] = sigmoid_fast(pre[1]);
@@ -347,8 +435,13 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
             const float cp = creg[q];
             cnv[q] = og4[q][1] * cp + og4[q][0] * og4[q][2];
             hnv[q] = og4[q][3] * tanh_fast(cnv[q]);
-            const T hv = from_f32<T>(is_valid(q, t) ? hnv[q] : hreg[q]);
+            const bool vq = is_valid(q, t);
+            const T hv = from_f32<T>(vq ? hnv[q] : hreg[q]);
             if (pn[q] >= 0) xstore(hxn + frag_off(b, pn[q], a.mtiles), (a.dense && !mnr[q]) ? zero_val<T>() : hv);
+            if (D.xout && pup[q] >= 0) {
+                const T yv = (vq && !(a.dense && !mup[q])) ? from_f32<T>(hnv[q]) : zero_val<T>();
+                xstore((T*)D.xout + (size_t)t * a.xxs + frag_off(b, pup[q], a.mtiles), yv);
+            }
         }
         grid_arrive(bar);
         // outputs only later kernels read, and the next step's inputs, go out
@@ -642,10 +735,12 @@ static bool cooperative_api() {
     const char* v = getenv("LSTM_SD_COOP");
     return v && v[0] == '1';
 }
-size_t fwd_persist_lds(int H, int NT, int MG, int esize) {
+size_t fwd_persist_lds(int H, int NT, int MG, int esize, int KP, int kin_max) {
     const size_t us = ((size_t)16 * NT * fwd_hp(H) * esize + 15) & ~(size_t)15;
-    const size_t kx = ((size_t)(H + 32) * 2 + 15) & ~(size_t)15;
-    return us + kx + (size_t)PF_NW * MG * 16 * NT * 4;
+    const size_t ws = ((size_t)16 * NT * KP * esize + 15) & ~(size_t)15;
+    const size_t kx = (size_t)(((H + 32) + 7) & ~7) * 2;
+    const size_t kxx = KP ? (((size_t)(kin_max + 32) * 2 + 15) & ~(size_t)15) : 0;
+    return us + ws + kx + kxx + (size_t)PF_NW * MG * 16 * NT * 4;
 }
 
 template <typename T, int NT, int MG>
@@ -665,17 +760,17 @@ static hipError_t launch_fwd_persist_t(const PFwdArgs& a, int nwg, size_t lds, h
 // Launches the persistent forward layer if it fits; returns hipSuccess or an
 // error (then nothing was launched and the caller uses the per-step kernels).
 template <typename T>
-hipError_t launch_fwd_persist(PFwdArgs& a, int D, hipStream_t st, int kid_timer_on, hipEvent_t e0, hipEvent_t e1) {
+hipError_t launch_fwd_persist(PFwdArgs& a, hipStream_t st, int kid_timer_on, hipEvent_t e0, hipEvent_t e1) {
     int NT, MG;
     MG = a.B <= 32 ? 32 : 64;
     NT = a.H >= 512 ? 2 : 1;            // fewer, wider unit tiles: a cheaper barrier
     const int upw = 4 * NT;
     a.ntiles = (a.H + upw - 1) / upw;
     a.mgroups = (a.B + MG - 1) / MG;
-    const int nwg = D * a.ntiles * a.mgroups;
-    const size_t lds = fwd_persist_lds(a.H, NT, MG, (int)sizeof(T));
-    if (lds > 160 * 1024) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_zero_sync, dim3(1), dim3(64), 0, st, a.bar, 2, a.err);
+    const int nwg = a.nslots * a.ntiles * a.mgroups;
+    const size_t lds = fwd_persist_lds(a.H, NT, MG, (int)sizeof(T), a.KP, a.kin_max);
+    if (lds > 160 * 1024 || a.nslots > 4) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_zero_sync, dim3(1), dim3(64), 0, st, a.bar, a.nslots, a.err);
     if (kid_timer_on) (void)hipEventRecord(e0, st);
     hipError_t e;
     if (NT == 1 && MG == 32) e = launch_fwd_persist_t<T, 1, 32>(a, nwg, lds, st);
@@ -686,8 +781,8 @@ hipError_t launch_fwd_persist(PFwdArgs& a, int D, hipStream_t st, int kid_timer_
     return e;
 }
 
-template hipError_t launch_fwd_persist<float>(PFwdArgs&, int, hipStream_t, int, hipEvent_t, hipEvent_t);
-template hipError_t launch_fwd_persist<bf16>(PFwdArgs&, int, hipStream_t, int, hipEvent_t, hipEvent_t);
+template hipError_t launch_fwd_persist<float>(PFwdArgs&, hipStream_t, int, hipEvent_t, hipEvent_t);
+template hipError_t launch_fwd_persist<bf16>(PFwdArgs&, hipStream_t, int, hipEvent_t, hipEvent_t);
 
 size_t bwd_persist_lds(int H, int UB, int MG, int esize) {
     const size_t G = 4 * (size_t)H, GP = (G + 31) / 32 * 32 + 8;

@@ -23,6 +23,7 @@ struct Plan {
     int HP;               // H rounded up to 8 (row pitch of the per-step h buffer)
     int mtiles;           // 16-row tiles of the batch
     size_t das, hxs;      // elements of one fragment-major DA block / h exchange slot
+    size_t xxs;           // elements of one layer-input exchange slot (stacked forward)
 
     // mask buffer
     size_t m_mask, m_keep, m_pos, m_count, m_drop, m_dcount, m_kseg, m_dseg, m_total;
@@ -35,7 +36,7 @@ struct Plan {
     size_t r_total;
 
     // workspace
-    size_t w_gx, w_hrec, w_hx;                  // forward
+    size_t w_gx, w_hrec, w_hx, w_xx;            // forward
     size_t w_da, w_daT, w_dc, w_dhc, w_dxc, w_wpart;  // backward
     size_t w_sync;                              // barrier counters and error flag
     size_t w_loss, w_total;

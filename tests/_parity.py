@@ -70,3 +70,11 @@ def compare(gpu, ref, keys=("y", "hT", "cT", "dx", "dh0", "dc0"), rows=None):
 def say(*a):
     print(*a, flush=True)
     sys.stdout.flush()
+
+
+def fwd_persist_launches(cfg, stacked=True):
+    """Persistent forward launches per forward pass: one for a unidirectional
+    stack run in one launch, else one per layer."""
+    if stacked and cfg.num_dirs == 1 and 1 < cfg.num_layers <= 4:
+        return 1
+    return cfg.num_layers

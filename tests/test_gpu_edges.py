@@ -8,7 +8,7 @@ import numpy as np
 import pytest
 
 import workloads
-from tests._parity import TOL, compare, oracle_step, say, site_list
+from tests._parity import TOL, compare, fwd_persist_launches, oracle_step, say, site_list
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -163,7 +163,7 @@ def test_persistent_and_per_step_paths_agree(name, mode, monkeypatch):
         B_.lstm_sd_kernel_timer_start("fwd_persist")
         s.forward()
         _, n = B_.lstm_sd_kernel_timer_stop()
-        assert n == (cfg.num_layers if flag == "1" else 0)
+        assert n == (fwd_persist_launches(cfg) if flag == "1" else 0)
         s.loss_grad()
         B_.lstm_sd_kernel_timer_start("bwd_persist")
         s.backward()
@@ -174,3 +174,36 @@ def test_persistent_and_per_step_paths_agree(name, mode, monkeypatch):
     errs = compare(outs[0], outs[1])
     assert max(errs.values()) <= TOL[cfg.dtype], errs
     assert np.isfinite(outs[0]["hT"]).all()
+
+
+@pytest.mark.parametrize("name,mode", [("lm_medium", "nrrh"), ("lm_medium", "nr_dense"), ("tiny", "nr"),
+                                       ("seq2seq_enc", "nrrh")])
+def test_stacked_and_per_layer_forward_agree(name, mode, monkeypatch):
+    """A unidirectional stack run as one persistent launch (each layer computing
+    its input product from what the layer below published) gives the same step
+    as one launch per layer with the separate input-product pass."""
+    from paper_2106_12089_amd import binding as B_
+    from paper_2106_12089_amd.session import Session
+    from tests._parity import mode_rates
+    cfg = workloads.get_config(name)
+    wl = workloads.make_workload(cfg)
+    p = cfg.p_values[0]
+    p_nr, p_rh, compact = mode_rates(cfg, mode, p)
+    say(f"[gpu] stacked vs per-layer forward {name} {mode}")
+    outs = []
+    for flag in ("1", "0"):
+        monkeypatch.setenv("LSTM_SD_STACK", flag)
+        s = Session(wl, p_nr, p_rh, compact)
+        s.masks(cfg.mask_seed, 4)
+        B_.lstm_sd_kernel_timer_start("fwd_persist")
+        s.forward()
+        _, n = B_.lstm_sd_kernel_timer_stop()
+        assert n == fwd_persist_launches(cfg, stacked=flag == "1")
+        s.loss_grad()
+        s.backward()
+        torch.cuda.synchronize()
+        outs.append(s.outputs())
+    errs = compare(outs[0], outs[1])
+    assert max(errs.values()) <= TOL[cfg.dtype], errs
+    for k in ("y", "hT", "cT"):
+        assert np.isfinite(outs[0][k]).all(), k

@@ -11,7 +11,8 @@ import numpy as np
 import pytest
 
 import workloads
-from tests._parity import (TOL, compare, mode_rates, oracle_masks, oracle_step, say, site_list)
+from tests._parity import (TOL, compare, fwd_persist_launches, mode_rates, oracle_masks, oracle_step, say,
+                           site_list)
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -148,7 +149,7 @@ def test_kernel_timer_counts_launches():
     s = Session(wl, 0.5, 0.5, 1)
     s.masks(cfg.mask_seed, 0)
     torch.cuda.synchronize()
-    for name, per_step in (("fwd_persist", cfg.num_layers), ("step", 0),
+    for name, per_step in (("fwd_persist", fwd_persist_launches(cfg)), ("step", 0),
                            ("bwd_persist", cfg.num_layers), ("bwd", 0),
                            ("wgrad", 2 * cfg.num_layers * cfg.num_dirs)):
         B_.lstm_sd_kernel_timer_start(name)
@@ -161,3 +162,30 @@ def test_kernel_timer_counts_launches():
         assert (0.0 < ms < 1e4) if per_step else ms == 0.0
     with pytest.raises(B_.LstmSdError):
         B_.lstm_sd_kernel_timer_start("no_such_kernel")
+
+
+@pytest.mark.parametrize("compact,p_rh", [(1, 0.5), (0, 0.5), (1, 0.0)])
+def test_repeats_bit_identical(compact, p_rh):
+    """The same step repeated on the same masks is bit-identical: the
+    cross-workgroup exchanges of the persistent kernels leave no room for a
+    read that races its producer."""
+    from paper_2106_12089_amd.session import Session
+    cfg = workloads.get_config("lm_medium")
+    wl = workload("lm_medium")
+    say(f"[gpu] repeats lm_medium compact={compact} p_rh={p_rh}")
+    s = Session(wl, 0.5, p_rh, compact)
+    s.masks(cfg.mask_seed, 1)
+    ref = None
+    for it in range(8):
+        s.forward()
+        s.loss_grad()
+        s.backward()
+        torch.cuda.synchronize()
+        o = s.outputs()
+        cur = {k: np.concatenate([np.ravel(a) for a in v]) if isinstance(v, list) else np.ravel(v)
+               for k, v in o.items() if v is not None and k != "loss"}
+        if ref is None:
+            ref = cur
+            continue
+        diff = [k for k in ref if not np.array_equal(ref[k], cur[k])]
+        assert not diff, (it, diff)
