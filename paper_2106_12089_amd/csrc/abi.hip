@@ -36,7 +36,7 @@ hipError_t launch_fwd_persist(PFwdArgs& a, hipStream_t st, int timer_on, hipEven
 constexpr int KID_FWDP_ = 7;
 constexpr int KID_BWDP_ = 8;
 template <typename T>
-hipError_t launch_bwd_persist(PBwdArgs& a, int D, hipStream_t st, int timer_on, hipEvent_t e0, hipEvent_t e1);
+hipError_t launch_bwd_persist(PBwdArgs& a, hipStream_t st, int timer_on, hipEvent_t e0, hipEvent_t e1);
 int kernel_timer_start(const char* name);
 int kernel_timer_stop(double* total_ms, int64_t* launches);
 
@@ -131,8 +131,10 @@ int make_plan(const lstm_sd_dims* d, Plan* p, const char** why) {
     q.w_xx = off;   off = align_up(off + (size_t)(q.L - 1) * T * q.xxs * es, A);
     const size_t fwd = off;
     off = 0;
-    q.w_da = off;     off = align_up(off + D * T * (size_t)q.das * es, A);
-    q.w_daT = off;    off = align_up(off + D * T * G * BP * es, A);
+    const size_t NR = D > (size_t)q.L ? D : (size_t)q.L;   // DA regions: per direction, or per layer of a stack
+    q.w_da = off;     off = align_up(off + NR * T * (size_t)q.das * es, A);
+    q.w_daT = off;    off = align_up(off + NR * T * G * BP * es, A);
+    q.w_dxw = off;    off = align_up(off + (size_t)(q.L - 1) * T * B * H * 4, A);
     q.w_dc = off;     off = align_up(off + D * B * H * 4, A);
     q.w_dhc = off;    off = align_up(off + D * B * H * 4, A);
     q.w_dxc = off;    off = align_up(off + 2 * T * B * (size_t)q.kin_max * 4, A);
@@ -401,8 +403,129 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
     const char* R = (const char*)reserve;
     char* W = (char*)ws;
     const int tps_h = ((H + 7) / 8 + 15) / 16;     // 16-unit tiles per XCD slice of the hidden units
-    for (int l = L - 1; l >= 0; --l) {
+    // DA and DA^T regions: one per direction, or one per layer when a
+    // unidirectional stack runs in one launch
+    auto da_of = [&](int reg) { return W + P.w_da + (size_t)reg * T * P.das * es; };
+    auto daT_of = [&](int reg) { return W + P.w_daT + (size_t)reg * T * G * BP * es; };
+    auto common_args = [&](PBwdArgs& pa) {
+        memset(&pa, 0, sizeof(pa));
+        pa.lengths = lengths;
+        pa.bar = (unsigned*)(W + P.w_sync);
+        pa.err = (int*)(W + P.w_sync + 4096);
+        pa.timeout = barrier_timeout_ticks();
+        pa.B = B; pa.H = H; pa.T = T; pa.BP = BP; pa.ldy = D * H;
+        pa.kmax = P.kmax; pa.dense = !P.compact; pa.mtiles = P.mtiles; pa.s = P.s_rh; pa.s_nr = P.s_nr;
+    };
+    auto fill_layer = [&](PBwdDir& pd, int l, int d, int reg) {
+        const int k = l * D + d;
+        const char* rd = R + P.rdir(l, d);
+        pd.U = w->U[k];
+        pd.rh = site_view(P, mbuf, P.site_rh(l, d));
+        pd.gates = (const float*)(rd + P.r_gates);
+        pd.cres = (const float*)(rd + P.r_c);
+        pd.c0 = c0 + (size_t)k * B * H;
+        if (l == L - 1) pd.dy = dy + d * H;
+        pd.dhT = dhT ? dhT + (size_t)k * B * H : nullptr;
+        pd.dcT = dcT ? dcT + (size_t)k * B * H : nullptr;
+        pd.da = da_of(reg);
+        pd.daT = daT_of(reg);
+        pd.dh0 = dh0 + (size_t)k * B * H;
+        pd.dc0 = dc0 + (size_t)k * B * H;
+        pd.dir = d;
+        pd.above = -1;
+    };
+    // input gradient of layer l for the layer below (and the caller's dx)
+    auto layer_dx = [&](int l, int reg0, float* dxc_here) {
         const int kin = P.kin(l);
+        const SiteView nv = site_view(P, mbuf, P.site_nr(l));
+        DxArgs a;
+        memset(&a, 0, sizeof(a));
+        for (int d = 0; d < D; ++d) {
+            a.da[d] = da_of(reg0 + d);
+            a.W[d] = w->W[l * D + d];
+        }
+        a.site = nv; a.out = dxc_here; a.D = D; a.B = B; a.G = G; a.ldo = kin; a.T = T;
+        a.K = kin; a.tps = ((kin + 7) / 8 + 15) / 16; a.mtiles = P.mtiles;
+        a.dense = !P.compact; a.s = P.s_nr;
+        launch_dx<E>(a, kin, st);
+        if (l == 0) launch_expand(dxc_here, kin, nv, dx, B, kin, T, st);
+    };
+    // weight and bias gradients of layer l (Eq. 11)
+    auto layer_wgrad = [&](int l, int reg0) {
+        const int kin = P.kin(l);
+        const SiteView nv = site_view(P, mbuf, P.site_nr(l));
+        const void* XT = l == 0 ? (const void*)(R + P.r_xT) : (const void*)(R + P.rybufT(l - 1));
+        const int tper = (T + P.ts - 1) / P.ts;
+        float* wpart = (float*)(W + P.w_wpart);
+        for (int d = 0; d < D; ++d) {
+            const int k = l * D + d;
+            const char* rd = R + P.rdir(l, d);
+            WgArgs a;
+            memset(&a, 0, sizeof(a));
+            a.actT = XT; a.tstride = (long)kin * BP; a.actT_first = nullptr; a.t_first = -1; a.shift = 0;
+            a.daT = daT_of(reg0 + d);
+            a.site = nv; a.K = kin; a.B = B; a.BP = BP; a.G = G; a.T = T; a.tper = tper;
+            a.dense = !P.compact; a.s = P.s_nr;
+            a.out = P.ts > 1 ? wpart : g->dW[k];
+            a.ostride = (long)(kin + 1) * G;
+            a.db = g->db[k];                      // the bias gradient rides on the input-weight pass
+            launch_wgrad<E>(a, P.ts, st);
+            if (P.ts > 1) launch_wreduce(wpart, g->dW[k], g->db[k], (long)kin * G, a.ostride, G, P.ts, st);
+
+            WgArgs u = a;
+            u.actT = rd + P.r_hrecT; u.tstride = (long)H * BP;
+            u.actT_first = R + P.r_h0T + (size_t)k * H * BP * es;
+            u.t_first = d == 0 ? 0 : T - 1;
+            u.shift = d == 0 ? -1 : 1;
+            u.site = site_view(P, mbuf, P.site_rh(l, d));
+            u.K = H; u.s = P.s_rh;
+            u.out = P.ts > 1 ? wpart : g->dU[k];
+            u.ostride = (long)H * G;
+            u.db = nullptr;
+            launch_wgrad<E>(u, P.ts, st);
+            if (P.ts > 1) launch_wreduce(wpart, g->dU[k], nullptr, (long)H * G, u.ostride, G, P.ts, st);
+        }
+    };
+
+    // Unidirectional stack: every layer's BPTT in one persistent launch, with
+    // a worker between layers l+1 and l forming dx of layer l+1 per step.
+    if (use_persistent() && use_stacked() && D == 1 && L > 1 && 2 * L - 1 <= 8) {
+        launch_bwd_init(nullptr, nullptr, nullptr, nullptr, 0, W + P.w_da, (int)es, G, P.mtiles, (long)L * T,
+                        (long)P.das, st);
+        PBwdArgs pa;
+        common_args(pa);
+        pa.nslots = 2 * L - 1;
+        for (int l = L - 1; l >= 0; --l) {
+            const int slot = 2 * (L - 1 - l);             // layer l; its worker (dx of l for l-1) at slot + 1
+            fill_layer(pa.d[slot], l, 0, l);
+            if (l < L - 1) {
+                pa.d[slot].above = slot - 1;
+                pa.d[slot].dxw = (const float*)(W + P.w_dxw) + (size_t)l * T * B * H;
+            }
+            if (l > 0) {
+                PBwdDir& wk = pa.d[slot + 1];
+                wk.role = 1;
+                wk.src = slot;
+                wk.dir = 0;
+                wk.above = -1;
+                wk.Wup = w->W[l];
+                wk.nr_up = site_view(P, mbuf, P.site_nr(l));
+                wk.dxw_out = (float*)(W + P.w_dxw) + (size_t)(l - 1) * T * B * H;
+                wk.dh0 = dh0 + (size_t)l * B * H;         // unused by a worker (poisoning targets only)
+                wk.dc0 = dc0 + (size_t)l * B * H;
+            }
+        }
+        hipEvent_t e0 = nullptr, e1 = nullptr;
+        const bool timed = timer_pair(KID_BWDP_, &e0, &e1);
+        if (launch_bwd_persist<E>(pa, st, timed, e0, e1) == hipSuccess) {
+            if (dx) layer_dx(0, 0, (float*)(W + P.w_dxc));
+            for (int l = L - 1; l >= 0; --l) layer_wgrad(l, l);
+            return hip_check("backward launch");
+        }
+        (void)hipGetLastError();              // does not fit: one layer at a time below
+    }
+
+    for (int l = L - 1; l >= 0; --l) {
         float* dhc = (float*)(W + P.w_dhc);
         float* dcs = (float*)(W + P.w_dc);
         launch_bwd_init(dhT ? dhT + (size_t)l * D * B * H : nullptr, dcT ? dcT + (size_t)l * D * B * H : nullptr,
@@ -413,39 +536,20 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
         bool persistent_done = false;
         if (use_persistent()) {
             PBwdArgs pa;
-            memset(&pa, 0, sizeof(pa));
-            pa.lengths = lengths;
-            pa.bar = (unsigned*)(W + P.w_sync);
-            pa.err = (int*)(W + P.w_sync + 4096);
-            pa.timeout = barrier_timeout_ticks();
-            pa.B = B; pa.H = H; pa.T = T; pa.BP = BP; pa.ldy = D * H;
+            common_args(pa);
+            pa.nslots = D;
             pa.lddx = l + 1 < L ? P.kin(l + 1) : 0;
-            pa.kmax = P.kmax; pa.dense = !P.compact; pa.mgc = P.MGc; pa.mtiles = P.mtiles; pa.s = P.s_rh;
             for (int d = 0; d < D; ++d) {
-                const int k = l * D + d;
-                const char* rd = R + P.rdir(l, d);
                 PBwdDir& pd = pa.d[d];
-                pd.U = w->U[k];
-                pd.rh = site_view(P, mbuf, P.site_rh(l, d));
-                pd.gates = (const float*)(rd + P.r_gates);
-                pd.cres = (const float*)(rd + P.r_c);
-                pd.c0 = c0 + (size_t)k * B * H;
-                if (l == L - 1) {
-                    pd.dy = dy + d * H;
-                } else {
+                fill_layer(pd, l, d, d);
+                if (l < L - 1) {
                     pd.dxc = dxc_above;
                     pd.dxpos = site_view(P, mbuf, P.site_nr(l + 1)).pos + d * H;
                 }
-                pd.dhT = dhT ? dhT + (size_t)k * B * H : nullptr;
-                pd.dcT = dcT ? dcT + (size_t)k * B * H : nullptr;
-                pd.da = W + P.w_da + (size_t)d * T * P.das * es;
-                pd.daT = W + P.w_daT + (size_t)d * T * G * BP * es;
-                pd.dh0 = dh0 + (size_t)k * B * H;
-                pd.dc0 = dc0 + (size_t)k * B * H;
             }
             hipEvent_t e0 = nullptr, e1 = nullptr;
             const bool timed = timer_pair(KID_BWDP_, &e0, &e1);
-            if (launch_bwd_persist<E>(pa, D, st, timed, e0, e1) == hipSuccess) persistent_done = true;
+            if (launch_bwd_persist<E>(pa, st, timed, e0, e1) == hipSuccess) persistent_done = true;
             else (void)hipGetLastError();     // does not fit: per-step kernels below
         }
         // T pointwise steps plus one final pass (recurrent gradient of h0)
@@ -469,7 +573,7 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
                 bd.dhc = dhc + (size_t)d * B * H;
                 bd.dcs = dcs + (size_t)d * B * H;
                 if (s > 0) {
-                    bd.da_next = W + P.w_da + ((size_t)d * T + tn) * P.das * es;
+                    bd.da_next = (char*)da_of(d) + (size_t)tn * P.das * es;
                     bd.nmask = rv.mask + (size_t)tn * P.kmax;
                     bd.nkeep = rv.keep + (size_t)tn * P.kmax;
                     bd.ncount = rv.count + tn;
@@ -493,57 +597,13 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
                     bd.dxc = dxc_above + (size_t)t * B * a.lddx;
                     bd.dxpos = sv.pos + (size_t)t * P.kmax + d * H;
                 }
-                bd.da = W + P.w_da + ((size_t)d * T + t) * P.das * es;
-                bd.daT = W + P.w_daT + ((size_t)d * T + t) * G * BP * es;
+                bd.da = (char*)da_of(d) + (size_t)t * P.das * es;
+                bd.daT = (char*)daT_of(d) + (size_t)t * G * BP * es;
             }
             launch_bwd<E>(a, D, st);
         }
-        const SiteView nv = site_view(P, mbuf, P.site_nr(l));
-        if (l > 0 || dx) {
-            DxArgs a;
-            memset(&a, 0, sizeof(a));
-            for (int d = 0; d < D; ++d) {
-                a.da[d] = W + P.w_da + (size_t)d * T * P.das * es;
-                a.W[d] = w->W[l * D + d];
-            }
-            a.site = nv; a.out = dxc_here; a.D = D; a.B = B; a.G = G; a.ldo = kin; a.T = T;
-            a.K = kin; a.tps = ((kin + 7) / 8 + 15) / 16; a.mtiles = P.mtiles;
-            a.dense = !P.compact; a.s = P.s_nr;
-            launch_dx<E>(a, kin, st);
-            if (l == 0) launch_expand(dxc_here, kin, nv, dx, B, kin, T, st);
-        }
-        const void* XT = l == 0 ? (const void*)(R + P.r_xT) : (const void*)(R + P.rybufT(l - 1));
-        const int tper = (T + P.ts - 1) / P.ts;
-        float* wpart = (float*)(W + P.w_wpart);
-        for (int d = 0; d < D; ++d) {
-            const int k = l * D + d;
-            const char* rd = R + P.rdir(l, d);
-            WgArgs a;
-            memset(&a, 0, sizeof(a));
-            a.actT = XT; a.tstride = (long)kin * BP; a.actT_first = nullptr; a.t_first = -1; a.shift = 0;
-            a.daT = W + P.w_daT + (size_t)d * T * G * BP * es;
-            a.site = nv; a.K = kin; a.B = B; a.BP = BP; a.G = G; a.T = T; a.tper = tper;
-            a.dense = !P.compact; a.s = P.s_nr;
-            a.out = P.ts > 1 ? wpart : g->dW[k];
-            a.ostride = (long)(kin + 1) * G;
-            a.db = g->db[k];                      // the bias gradient rides on the input-weight pass
-            launch_wgrad<E>(a, P.ts, st);
-            if (P.ts > 1) launch_wreduce(wpart, g->dW[k], g->db[k], (long)kin * G, a.ostride, G, P.ts, st);
-
-            WgArgs u = a;
-            u.actT = rd + P.r_hrecT; u.tstride = (long)H * BP;
-            u.actT_first = R + P.r_h0T + (size_t)k * H * BP * es;
-            u.t_first = d == 0 ? 0 : T - 1;
-            u.shift = d == 0 ? -1 : 1;
-            u.site = site_view(P, mbuf, P.site_rh(l, d));
-            u.K = H; u.s = P.s_rh;
-            u.out = P.ts > 1 ? wpart : g->dU[k];
-            u.ostride = (long)H * G;
-            u.db = nullptr;
-            launch_wgrad<E>(u, P.ts, st);
-            if (P.ts > 1) launch_wreduce(wpart, g->dU[k], nullptr, (long)H * G, u.ostride, G, P.ts, st);
-
-        }
+        if (l > 0 || dx) layer_dx(l, 0, dxc_here);
+        layer_wgrad(l, 0);
     }
     return hip_check("backward launch");
 }

@@ -215,15 +215,26 @@ struct PBwdDir {
     void* daT;                          // [T][4H][BP]
     float* dh0;                         // [B][H]
     float* dc0;                         // [B][H]
+    int dir;                            // 0: t = T-1 .. 0 (BP of the forward direction);  1: t = 0 .. T-1
+    // A unidirectional stack in one launch: the input gradient of layer l+1
+    // (Eq. 10, dx = s * da W^T over the kept inputs) is formed per step by a
+    // worker slot from the DA layer l+1 publishes, and read by layer l.
+    int role;                           // 0: the recurrence of one layer (direction); 1: input-gradient worker
+    int src;                            // worker: slot of the layer whose DA it reads
+    int above;                          // layer: worker slot that provides its dh input, or -1
+    const float* dxw;                   // layer: [T][B][H] that input (with above)
+    const void* Wup;                    // worker: input weights [H][4H] of the layer above
+    SiteView nr_up;                     // worker: NR site of the layer above (output sparsity and scale)
+    float* dxw_out;                     // worker: [T][B][H]
 };
 struct PBwdArgs {
-    PBwdDir d[2];
+    PBwdDir d[8];                       // slots: the directions of one layer, or the layers and workers of a stack
     const int32_t* lengths;
     unsigned* bar;
     int* err;
     long long timeout;
-    int B, H, T, BP, ldy, lddx, kmax, dense, ntiles, mgroups, mgc, mtiles;
-    float s;
+    int B, H, T, BP, ldy, lddx, kmax, dense, ntiles, mgroups, mtiles, nslots;
+    float s, s_nr;
 };
 
 }  // namespace lsd

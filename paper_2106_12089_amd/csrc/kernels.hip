@@ -1029,8 +1029,9 @@ void launch_fwd_init(const void* h0, const float* c0, float* hT, float* cT, long
 }
 void launch_bwd_init(const float* dhT, const float* dcT, float* dhc, float* dcs, long n, void* da, int es, int G,
                      int mtiles, long nblocks, long das, hipStream_t st) {
-    launch_k(KID_NONE, k_bwd_init, dim3(nblk(n, 256)), dim3(256), 0, st, dhT, dcT, dhc, dcs, n, da, es, G, mtiles,
-             nblocks, das);
+    const long np = da ? nblocks * 16 * mtiles * 32 : 0;      // upper bound of the DA padding entries
+    launch_k(KID_NONE, k_bwd_init, dim3(nblk(n > np ? n : np, 256)), dim3(256), 0, st, dhT, dcT, dhc, dcs, n, da, es,
+             G, mtiles, nblocks, das);
 }
 void launch_expand(const float* dxc, int ldc, const SiteView& s, float* dx, int B, int K, int T, hipStream_t st) {
     launch_k(KID_NONE, k_expand, dim3(nblk((long)T * B * K, 256)), dim3(256), 0, st, dxc, ldc, s, dx, B, K, T);

@@ -479,8 +479,12 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Persistent BPTT (Eq. 7-10) of one layer, both directions.
-// Workgroup w -> (direction, unit tile of UB units, row group of MG rows).
+// Persistent BPTT (Eq. 7-10).  A launch runs every step of its slots: the
+// two directions of one layer, or the layers of a unidirectional stack
+// together with one input-gradient worker between each pair of layers (the
+// top layer works on step t, the worker below it forms that layer's dx_t from
+// the published DA_t, and the next layer uses it one step later).
+// Workgroup w -> (slot, unit tile of UB units, row group of MG rows).
 // 1024 threads = 16 waves.  Per step: the recurrent gradient of the tile's
 // units from DA of the step processed before (Eq. 10; contraction over 4H
 // split over the waves; skipped when every unit of the tile was dropped),
@@ -509,10 +513,12 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int g8 = 8 * (lane >> 4);
     unsigned* bar = a.bar + d;
+    const bool worker = D.role == 1;
 
-    // rows of U for the tile's units -> LDS (zero past 4H and past H)
+    // rows of U (a worker: of the input weights of the layer above) for the
+    // tile's units -> LDS (zero past 4H and past H)
     {
-        const T* U = (const T*)D.U;
+        const T* U = (const T*)(worker ? D.Wup : D.U);
         for (int i = tid; i < UB * GP; i += NTH) {
             const int r = i / GP, n = i % GP;
             const int u = u0 + r;
@@ -538,10 +544,10 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
     // before it (whether the tile gets a recurrent gradient, Eq. 10).
     float gt4[PPT][4], ctv[PPT], cpv[PPT], dyr[PPT], dxv[PPT];
     int lenr[PPT], dxp[PPT], mkr[PPT];
-    auto step_t = [&](int s) { return d == 0 ? T_ - 1 - s : s; };
+    auto step_t = [&](int s) { return D.dir == 0 ? T_ - 1 - s : s; };
     auto prefetch = [&](int s) {
         const int t = step_t(min(s, T_ - 1));
-        const int tp = d == 0 ? t - 1 : t + 1;            // forward predecessor of t
+        const int tp = D.dir == 0 ? t - 1 : t + 1;        // forward predecessor of t
         const int tn = step_t(max(s - 1, 0));
 #pragma unroll
         for (int q = 0; q < PPT; ++q) {
@@ -557,9 +563,15 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
             mkr[q] = D.rh.mask[(size_t)tn * a.kmax + uc];
         }
     };
-    // the layer above's input gradient at its compact position (a load that
-    // depends on dxp; issued right after the barrier, beside the DA loads)
+    // the layer above's input gradient: at its compact position (a load that
+    // depends on dxp), or from the worker of a stack; issued right after the
+    // barrier, beside the DA loads
     auto fetch_dx = [&](int t) {
+        if (D.dxw) {
+#pragma unroll
+            for (int q = 0; q < PPT; ++q) dxv[q] = D.dxw[((size_t)t * B + min(pb[q], B - 1)) * H + min(pu[q], H - 1)];
+            return;
+        }
         if (D.dy || !D.dxc) return;
 #pragma unroll
         for (int q = 0; q < PPT; ++q)
@@ -572,12 +584,13 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
         return __builtin_amdgcn_ballot_w64(pu[0] < H && mkr[0] != 0) != 0;
     };
 
-    // the recurrent gradient of the tile's units from DA of step tn into red
-    auto recurrent_product = [&](int tn) {
+    // the gradient of the tile's units (Eq. 10) from DA of step tn (of this
+    // slot, or of src for a worker) into red
+    auto recurrent_product = [&](int tn, const void* da_base) {
         // DA_t is fragment-major: rows past B hold stale values that only
         // reach output rows that are never used; the columns past 4H of the
         // last chunk are zero (cleared before the backward pass)
-        const __amdgpu_buffer_rsrc_t dr = buf_rsrc((const T*)D.da + (size_t)tn * das, (uint32_t)(das * sizeof(T)));
+        const __amdgpu_buffer_rsrc_t dr = buf_rsrc((const T*)da_base + (size_t)tn * das, (uint32_t)(das * sizeof(T)));
         f32x4_t acc[MT];
 #pragma unroll
         for (int i = 0; i < MT; ++i) acc[i] = f32x4_t{0, 0, 0, 0};
@@ -615,21 +628,59 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
         return v;
     };
 
+    if (worker) {
+        // dx_t of the layer above restricted to this tile's inputs, for every
+        // t in that layer's order, as soon as its DA_t is published
+        const PBwdDir& S = a.d[D.src];
+        unsigned* bar_src = a.bar + D.src;
+        for (int s = 0; s < T_; ++s) {
+            const int t = step_t(s);
+            int mk[PPT];
+#pragma unroll
+            for (int q = 0; q < PPT; ++q) mk[q] = D.nr_up.mask[(size_t)t * D.nr_up.kmax + min(pu[q], H - 1)];
+            if (!grid_wait(bar_src, (unsigned)(s + 1) * (unsigned)nslot, a.err, a.timeout)) break;
+            recurrent_product(t, S.da);
+#pragma unroll
+            for (int q = 0; q < PPT; ++q) {
+                const int b = pb[q], u = pu[q];
+                if (b >= B || u >= H) continue;
+                // dropped inputs get no gradient (output sparsity, Eq. 10)
+                const float v = mk[q] ? a.s_nr * reduced(b - m0, u - u0) : 0.0f;
+                xstore(D.dxw_out + ((size_t)t * B + b) * H + u, v);
+            }
+            grid_arrive(bar);
+        }
+        return;
+    }
+
+    unsigned* bar_above = D.above >= 0 ? a.bar + D.above : nullptr;
+    __shared__ unsigned above_seen;               // last value of the worker's counter read
+    unsigned seen_above = 0;                      // its copy in every thread (uniform waits)
+    // wait until the worker has formed dx of step s (usually already seen)
+    auto wait_above = [&](int s) {
+        if (bar_above && seen_above < (unsigned)(s + 1) * (unsigned)nslot) {
+            if (!grid_wait(bar_above, (unsigned)(s + 1) * (unsigned)nslot, a.err, a.timeout, &above_seen))
+                return false;
+            seen_above = above_seen;
+        }
+        return true;
+    };
     prefetch(0);
     for (int s = 0; s <= T_; ++s) {
         const bool final_pass = s == T_;
         const int t = final_pass ? -1 : step_t(s);
-        const int tn = d == 0 ? T_ - s : s - 1;            // step processed just before
+        const int tn = D.dir == 0 ? T_ - s : s - 1;        // step processed just before
         const bool has_next = s > 0;
         bool kept = false;
         if (has_next) {
             kept = tile_any_kept();
             if (!grid_wait(bar, (unsigned)s * (unsigned)nslot, a.err, a.timeout)) break;
-            if (!final_pass) fetch_dx(t);
-            if (kept) recurrent_product(tn);
-        } else {
+        }
+        if (!final_pass) {
+            if (!wait_above(s)) break;
             fetch_dx(t);
         }
+        if (kept) recurrent_product(tn, D.da);
         float da4[PPT][4];
 #pragma unroll
         for (int q = 0; q < PPT; ++q) {
@@ -649,7 +700,7 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
                 continue;
             }
             if (t < lenr[q]) {
-                dh += D.dy ? dyr[q] : (D.dxc && dxp[q] >= 0 ? dxv[q] : 0.0f);
+                dh += D.dy ? dyr[q] : D.dxw ? dxv[q] : (D.dxc && dxp[q] >= 0 ? dxv[q] : 0.0f);
                 const float ig = gt4[q][0], fg = gt4[q][1], gg = gt4[q][2], og = gt4[q][3];
                 const float tc = tanh_fast(ctv[q]);
                 const float dout = dh * tc;                            // Eq. 7
@@ -806,7 +857,7 @@ static hipError_t launch_bwd_persist_t(const PBwdArgs& a, int nwg, size_t lds, h
 // Launches the persistent backward layer if it fits (else returns an error
 // and nothing was launched).
 template <typename T>
-hipError_t launch_bwd_persist(PBwdArgs& a, int D, hipStream_t st, int timer_on, hipEvent_t e0, hipEvent_t e1) {
+hipError_t launch_bwd_persist(PBwdArgs& a, hipStream_t st, int timer_on, hipEvent_t e0, hipEvent_t e1) {
     const int MG = a.B <= 32 ? 32 : 64;
     a.mgroups = (a.B + MG - 1) / MG;
     int UB = 16;
@@ -814,8 +865,9 @@ hipError_t launch_bwd_persist(PBwdArgs& a, int D, hipStream_t st, int timer_on, 
     const size_t lds = bwd_persist_lds(a.H, UB, MG, (int)sizeof(T));
     if (lds > 160 * 1024) return hipErrorInvalidValue;
     a.ntiles = (a.H + UB - 1) / UB;
-    const int nwg = D * a.ntiles * a.mgroups;
-    hipLaunchKernelGGL(k_zero_sync, dim3(1), dim3(64), 0, st, a.bar, 2, a.err);
+    const int nwg = a.nslots * a.ntiles * a.mgroups;
+    if (a.nslots > 8) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_zero_sync, dim3(1), dim3(64), 0, st, a.bar, a.nslots, a.err);
     if (timer_on) (void)hipEventRecord(e0, st);
     hipError_t e;
     if (UB == 16 && MG == 32) e = launch_bwd_persist_t<T, 16, 32>(a, nwg, lds, st);
@@ -826,7 +878,7 @@ hipError_t launch_bwd_persist(PBwdArgs& a, int D, hipStream_t st, int timer_on, 
     return e;
 }
 
-template hipError_t launch_bwd_persist<float>(PBwdArgs&, int, hipStream_t, int, hipEvent_t, hipEvent_t);
-template hipError_t launch_bwd_persist<bf16>(PBwdArgs&, int, hipStream_t, int, hipEvent_t, hipEvent_t);
+template hipError_t launch_bwd_persist<float>(PBwdArgs&, hipStream_t, int, hipEvent_t, hipEvent_t);
+template hipError_t launch_bwd_persist<bf16>(PBwdArgs&, hipStream_t, int, hipEvent_t, hipEvent_t);
 
 }  // namespace lsd

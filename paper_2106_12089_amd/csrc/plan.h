@@ -37,7 +37,7 @@ struct Plan {
 
     // workspace
     size_t w_gx, w_hrec, w_hx, w_xx;            // forward
-    size_t w_da, w_daT, w_dc, w_dhc, w_dxc, w_wpart;  // backward
+    size_t w_da, w_daT, w_dxw, w_dc, w_dhc, w_dxc, w_wpart;  // backward
     size_t w_sync;                              // barrier counters and error flag
     size_t w_loss, w_total;
 

@@ -73,8 +73,8 @@ def say(*a):
 
 
 def fwd_persist_launches(cfg, stacked=True):
-    """Persistent forward launches per forward pass: one for a unidirectional
-    stack run in one launch, else one per layer."""
+    """Persistent launches per forward (or backward) pass: one for a
+    unidirectional stack run in one launch, else one per layer."""
     if stacked and cfg.num_dirs == 1 and 1 < cfg.num_layers <= 4:
         return 1
     return cfg.num_layers

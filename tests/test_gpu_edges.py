@@ -168,7 +168,7 @@ def test_persistent_and_per_step_paths_agree(name, mode, monkeypatch):
         B_.lstm_sd_kernel_timer_start("bwd_persist")
         s.backward()
         _, n = B_.lstm_sd_kernel_timer_stop()
-        assert n == (cfg.num_layers if flag == "1" else 0)
+        assert n == (fwd_persist_launches(cfg) if flag == "1" else 0)
         torch.cuda.synchronize()
         outs.append(s.outputs())
     errs = compare(outs[0], outs[1])
@@ -178,10 +178,12 @@ def test_persistent_and_per_step_paths_agree(name, mode, monkeypatch):
 
 @pytest.mark.parametrize("name,mode", [("lm_medium", "nrrh"), ("lm_medium", "nr_dense"), ("tiny", "nr"),
                                        ("seq2seq_enc", "nrrh")])
-def test_stacked_and_per_layer_forward_agree(name, mode, monkeypatch):
-    """A unidirectional stack run as one persistent launch (each layer computing
-    its input product from what the layer below published) gives the same step
-    as one launch per layer with the separate input-product pass."""
+def test_stacked_and_per_layer_agree(name, mode, monkeypatch):
+    """A unidirectional stack run as one persistent launch per pass (forward:
+    each layer forms its input product from what the layer below published;
+    backward: a worker forms each layer's input gradient from the DA the layer
+    publishes) gives the same step as one launch per layer with the separate
+    input-product and input-gradient passes."""
     from paper_2106_12089_amd import binding as B_
     from paper_2106_12089_amd.session import Session
     from tests._parity import mode_rates
@@ -189,7 +191,7 @@ def test_stacked_and_per_layer_forward_agree(name, mode, monkeypatch):
     wl = workloads.make_workload(cfg)
     p = cfg.p_values[0]
     p_nr, p_rh, compact = mode_rates(cfg, mode, p)
-    say(f"[gpu] stacked vs per-layer forward {name} {mode}")
+    say(f"[gpu] stacked vs per-layer {name} {mode}")
     outs = []
     for flag in ("1", "0"):
         monkeypatch.setenv("LSTM_SD_STACK", flag)
@@ -200,10 +202,13 @@ def test_stacked_and_per_layer_forward_agree(name, mode, monkeypatch):
         _, n = B_.lstm_sd_kernel_timer_stop()
         assert n == fwd_persist_launches(cfg, stacked=flag == "1")
         s.loss_grad()
+        B_.lstm_sd_kernel_timer_start("bwd_persist")
         s.backward()
+        _, n = B_.lstm_sd_kernel_timer_stop()
+        assert n == fwd_persist_launches(cfg, stacked=flag == "1")
         torch.cuda.synchronize()
         outs.append(s.outputs())
     errs = compare(outs[0], outs[1])
     assert max(errs.values()) <= TOL[cfg.dtype], errs
-    for k in ("y", "hT", "cT"):
+    for k in ("y", "hT", "cT", "dx", "dh0", "dc0"):
         assert np.isfinite(outs[0][k]).all(), k

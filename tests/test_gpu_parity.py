@@ -150,7 +150,7 @@ def test_kernel_timer_counts_launches():
     s.masks(cfg.mask_seed, 0)
     torch.cuda.synchronize()
     for name, per_step in (("fwd_persist", fwd_persist_launches(cfg)), ("step", 0),
-                           ("bwd_persist", cfg.num_layers), ("bwd", 0),
+                           ("bwd_persist", fwd_persist_launches(cfg)), ("bwd", 0),
                            ("wgrad", 2 * cfg.num_layers * cfg.num_dirs)):
         B_.lstm_sd_kernel_timer_start(name)
         for _ in range(3):
