@@ -102,6 +102,10 @@ __device__ __forceinline__ void raw_load(Raw8<T>& f, __amdgpu_buffer_rsrc_t r, u
         for (int e = 0; e < 4; ++e) f.w[4 * q + e] = v[e];
     }
 }
+// A buffer offset past every resource: the load returns 0 and moves no data.
+// Used for A-fragment lanes whose row lies past the batch.
+constexpr uint32_t OOB_OFF = 0x80000000u;
+
 // AND masks that zero the elements at index >= B of a fragment whose first
 // element sits at index b0
 template <typename T>

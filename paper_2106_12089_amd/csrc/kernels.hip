@@ -545,8 +545,8 @@ __global__ void __launch_bounds__(256) k_dx(DxArgs a) {
 #pragma unroll
     for (int i = 0; i < MT; ++i) acc[i] = f32x4_t{0, 0, 0, 0};
     for (int d = 0; d < a.D; ++d) {
-        // DA_t is fragment-major; rows past B hold stale values that only
-        // reach output rows that are never stored
+        // DA_t is fragment-major; lanes of rows past B read 0 without moving
+        // data
         const size_t das = (size_t)((a.G + 31) / 32) * a.mtiles * 512;
         const __amdgpu_buffer_rsrc_t dr = buf_rsrc((const T*)a.da[d] + (size_t)t * das, (uint32_t)(das * ES));
         const __amdgpu_buffer_rsrc_t wr = buf_rsrc(a.W[d], (uint32_t)a.K * a.G * ES);
@@ -559,7 +559,7 @@ __global__ void __launch_bounds__(256) k_dx(DxArgs a) {
                 raw_load(fb[u], wr, woff + nc * ES);
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt)
-                    raw_load(fa[u][mt], dr, (uint32_t)(frag_lane_off(nc >> 5, (m0 >> 4) + mt, lane, a.mtiles) * ES));
+                    raw_load(fa[u][mt], dr, m0 + 16 * mt + cl < a.B ? (uint32_t)(frag_lane_off(nc >> 5, (m0 >> 4) + mt, lane, a.mtiles) * ES) : OOB_OFF);
             }
 #pragma unroll
             for (int u = 0; u < U; ++u) {

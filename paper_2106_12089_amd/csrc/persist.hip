@@ -282,8 +282,8 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
     // fragment-major slot of slot_elems elements, Bt the transposed weight
     // slice of pitch bp, kfull the contraction length when nothing is
     // dropped.  issue() loads the A fragments of round c0 (chunks past the
-    // slot read as 0; rows past B hold stale values that only reach output
-    // rows that are never used); compute() multiplies every chunk slot of the
+    // slot, and lanes of rows past B, read as 0 without moving data);
+    // compute() multiplies every chunk slot of the
     // round (slots past the keep count have a zeroed A side and read B rows at
     // offset 0: no branch lets the compiler sink the loads into the products).
     auto issue = [&](const T* src, size_t slot_elems, int c0, Raw8<T> (&fa)[MAXC][MT]) {
@@ -293,7 +293,7 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
             const int c = c0 + w + NW * i;
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt)
-                raw_load(fa[i][mt], hr, (uint32_t)(frag_lane_off(c, m0 / 16 + mt, lane, a.mtiles) * sizeof(T)));
+                raw_load(fa[i][mt], hr, m0 + 16 * mt + (lane & 15) < B ? (uint32_t)(frag_lane_off(c, m0 / 16 + mt, lane, a.mtiles) * sizeof(T)) : OOB_OFF);
         }
     };
     auto compute = [&](Raw8<T> (&fa)[MAXC][MT], int c0, int n, const int16_t* kid, const T* Bt, int bp, int kfull,
@@ -588,8 +588,9 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
     // slot, or of src for a worker) into red
     auto recurrent_product = [&](int tn, const void* da_base) {
         // DA_t is fragment-major: rows past B hold stale values that only
-        // reach output rows that are never used; the columns past 4H of the
-        // last chunk are zero (cleared before the backward pass)
+        // reach output rows that are never used (reading them is cheaper here
+        // than a per-lane offset select); the columns past 4H of the last
+        // chunk are zero (cleared before the backward pass)
         const __amdgpu_buffer_rsrc_t dr = buf_rsrc((const T*)da_base + (size_t)tn * das, (uint32_t)(das * sizeof(T)));
         f32x4_t acc[MT];
 #pragma unroll
