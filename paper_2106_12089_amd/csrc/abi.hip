@@ -469,6 +469,7 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
             a.out = P.ts > 1 ? wpart : g->dW[k];
             a.ostride = (long)(kin + 1) * G;
             a.db = g->db[k];                      // the bias gradient rides on the input-weight pass
+            a.full = P.p_nr == 0.0 || !P.compact;
             launch_wgrad<E>(a, P.ts, st);
             if (P.ts > 1) launch_wreduce(wpart, g->dW[k], g->db[k], (long)kin * G, a.ostride, G, P.ts, st);
 
@@ -482,6 +483,7 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
             u.out = P.ts > 1 ? wpart : g->dU[k];
             u.ostride = (long)H * G;
             u.db = nullptr;
+            u.full = P.p_rh == 0.0 || !P.compact;
             launch_wgrad<E>(u, P.ts, st);
             if (P.ts > 1) launch_wreduce(wpart, g->dU[k], nullptr, (long)H * G, u.ostride, G, P.ts, st);
         }

@@ -147,6 +147,7 @@ struct WgArgs {
     float* db;                          // non-null: also the bias gradient (Eq. 11): row K of each
                                         // partial when TS > 1, else db itself
     int K, B, BP, G, T, tper, dense;
+    int full;                           // every keep list of the site is the identity (p = 0, or dense mode)
     float s;
 };
 

@@ -592,52 +592,72 @@ __global__ void __launch_bounds__(256) k_dx(DxArgs a) {
     }
 }
 
+// column sums of a packed fragment (bias gradient)
+template <typename T>
+__device__ __forceinline__ void db_add_raw(const Raw8<T>& f, float& acc) {
+    if (sizeof(T) == 2) {
+#pragma unroll
+        for (int q = 0; q < Raw8<T>::NW; ++q) acc += __uint_as_float(f.w[q] << 16) + __uint_as_float(f.w[q] & 0xffff0000u);
+    } else {
+#pragma unroll
+        for (int q = 0; q < Raw8<T>::NW; ++q) acc += __uint_as_float(f.w[q]);
+    }
+}
+
 // ---------------------------------------------------------------------------
-// Row-sparse weight gradient (Eq. 11; Sec. 3.2 WG).  grid (ceil(G/16) on
-// the XCD mapping, TS), block 512 (8 waves), dynamic LDS (K+1)*WG_LD floats.
-// A workgroup owns 16 gradient columns for all K rows over the time steps
-// [ts*tper, ts*tper + tper) (tper <= 64).  Wave w owns the rows of slice w,
-// [floor(wK/8), floor((w+1)K/8)): at each t it takes the kept rows of its
-// slice (keep-list entries kseg[t][w] .. kseg[t][w+1]) in 16-row tiles,
-// multiplies them with the 16 DA^T columns and adds each tile into its rows
-// of the LDS accumulator.  No two waves touch the same LDS row, so the waves
-// run without barriers.
+// Row-sparse weight gradient (Eq. 11; Sec. 3.2 WG).  grid (8 * ceil(G/128),
+// TS), block 512 (8 waves), dynamic LDS (rows of a slice + 1) * WG_LDC floats.
+// Workgroup i owns neuron slice x = i % 8, the rows [floor(xK/8),
+// floor((x+1)K/8)) (workgroup i runs on XCD i % 8, so a slice's activation
+// rows stay in one XCD's L2), and the 128 gradient columns of block i / 8,
+// over the time steps [ts*tper, ts*tper + tper) (tper <= 64).  At each t the
+// kept rows of the slice (keep-list entries kseg[t][x] .. kseg[t][x+1]) are
+// taken in 16-row tiles; wave w multiplies them with its 16 DA^T columns and
+// adds each tile into its columns of the LDS accumulator.  Waves own disjoint
+// columns, so they run without barriers until the final write; the gathered
+// rows are shared through the cache.
 //
 // The kernel is built to issue few vector-ALU instructions per MFMA: the
 // operands are fetched with buffer loads (32-bit offsets, out-of-range reads
 // return 0) into packed registers, only the padded batch entries are zeroed
 // (one AND per register), and the A rows of absent tile rows are not zeroed
-// at all: their products land in the spare LDS row K, which is never read
-// back.  Each wave loads the row indices and the DA^T fragment of t+1 while
-// t is multiplied.  All kept rows of a step are distinct, so the LDS sums
-// read every row of the step first and then write them.  Rows never kept
-// stay zero.
-constexpr int WG_LD = 17;   // LDS row stride (floats): spreads the 4 rows of a tile over the banks
+// at all: their products land in a spare LDS row, which is never read back.
+// Each wave loads the row indices and the DA^T fragment of t+1 while t is
+// multiplied.  All kept rows of a step are distinct, so the LDS sums read
+// every row of the step first and then write them.  Rows never kept stay
+// zero.  Every wave also sums its DA^T fragments: the bias gradient.
+constexpr int WG_NB = 128;                 // gradient columns per workgroup
+constexpr int WG_LDC = WG_NB + 4;          // LDS accumulator row pitch (floats)
 template <typename T>
 struct WgTiles { static constexpr int N = 6; };   // 16-row tiles in registers at once
 template <>
 struct WgTiles<float> { static constexpr int N = 4; };
+
+// LDS bytes of the row-sparse weight gradient for a K-row weight
+inline size_t wgrad_lds_bytes(int K) { return (size_t)((K + NXCD - 1) / NXCD + 1) * WG_LDC * sizeof(float); }
 
 template <typename T, bool DENSE>
 __global__ void __launch_bounds__(512) k_wgrad(WgArgs a) {
     constexpr int MAXT = WgTiles<T>::N;
     constexpr int NW = Raw8<T>::NW;
     constexpr uint32_t ES = sizeof(T);
-    extern __shared__ float acc_lds[];   // [K + 1][WG_LD]
-    const int ctile = xcd_tile(blockIdx.x, (a.G + 15) / 16);
-    if (ctile < 0) return;
+    extern __shared__ float acc_lds[];   // [rows of the slice + 1][WG_LDC]
+    const int x = blockIdx.x % NXCD, cb = blockIdx.x / NXCD;
+    if (cb * WG_NB >= a.G) return;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int col = lane & 15, g8 = 8 * (lane >> 4);
-    const int n0 = ctile * 16, n = n0 + col;
-    const int r0 = slice_start(w, a.K), r1 = slice_start(w + 1, a.K);
-    for (int i = r0 * 16 + lane; i < r1 * 16; i += 64) acc_lds[(i >> 4) * WG_LD + (i & 15)] = 0.0f;
+    const int c0 = 16 * w;                       // this wave's columns within the block
+    const int n0 = cb * WG_NB, n = n0 + c0 + col;
+    const int r0 = slice_start(x, a.K), r1 = slice_start(x + 1, a.K);
+    const int nrow = r1 - r0;
+    for (int i = lane; i < (nrow + 1) * 16; i += 64) acc_lds[(i >> 4) * WG_LDC + c0 + (i & 15)] = 0.0f;
     const int t0 = blockIdx.y * a.tper;
     const int t1 = min(a.T, t0 + a.tper);
-    // lane j holds the keep-list range of this wave's slice at t0 + j
+    // lane j holds the keep-list range of slice x at t0 + j
     int segb = 0, sege = 0;
     if (t0 + lane < t1) {
-        segb = a.site.kseg[(size_t)(t0 + lane) * (NXCD + 1) + w];
-        sege = a.site.kseg[(size_t)(t0 + lane) * (NXCD + 1) + w + 1];
+        segb = a.site.kseg[(size_t)(t0 + lane) * (NXCD + 1) + x];
+        sege = a.site.kseg[(size_t)(t0 + lane) * (NXCD + 1) + x + 1];
     }
     uint32_t pm0[NW], pmb[NW];                 // batch-pad masks of chunk 0 (A side; B side adds n < G)
     pad_mask<T>(g8, a.B, pm0);
@@ -645,7 +665,7 @@ __global__ void __launch_bounds__(512) k_wgrad(WgArgs a) {
     for (int q = 0; q < NW; ++q) pmb[q] = n < a.G ? pm0[q] : 0u;
     const uint32_t boff = (uint32_t)(min(n, a.G - 1) * a.BP + g8) * ES;   // DA^T fragment offset
     const uint32_t abytes = (uint32_t)a.K * a.BP * ES, bbytes = (uint32_t)a.G * a.BP * ES;
-    const int spare = a.K * WG_LD;
+    const int spare = nrow * WG_LDC;
 
     // keep-list entries (and, dense mode, mask bytes) of the A-fragment rows
     // of tiles jt0 .. jt0+MAXT-1 at t.  In dense mode the keep list is the
@@ -673,7 +693,7 @@ __global__ void __launch_bounds__(512) k_wgrad(WgArgs a) {
             const int j = jb + (jt0 + i) * 16 + col;
             const bool ok = j < je && (!DENSE || mv[i]);
             kk[i] = ok ? kv[i] : 0;
-            la[i] = ok ? kv[i] * WG_LD : spare;
+            la[i] = ok ? (kv[i] - r0) * WG_LDC : spare;
         }
     };
     auto act_rsrc = [&](int t) {
@@ -686,22 +706,11 @@ __global__ void __launch_bounds__(512) k_wgrad(WgArgs a) {
 #pragma unroll
         for (int i = 0; i < MAXT; ++i) raw_load(fa[i], ar, (uint32_t)(kk[i] * a.BP + bc + g8) * ES);
     };
+    float dbacc = 0.f;
     // multiply the tiles (chunk-0 fragments already loaded), finish the other
     // batch chunks, and add the tiles into their LDS rows.  Tiles past nt
     // are multiplied too (their rows are absent): unconditional products
     // keep the loads out of branches.
-    // bias gradient (wave 0): the column sums of the DA^T fragments
-    const bool do_db = a.db != nullptr && w == 0;
-    float dbacc = 0.f;
-    auto db_add = [&](const Raw8<T>& f) {
-        if (sizeof(T) == 2) {
-#pragma unroll
-            for (int q = 0; q < NW; ++q) dbacc += __uint_as_float(f.w[q] << 16) + __uint_as_float(f.w[q] & 0xffff0000u);
-        } else {
-#pragma unroll
-            for (int q = 0; q < NW; ++q) dbacc += __uint_as_float(f.w[q]);
-        }
-    };
     auto finish = [&](__amdgpu_buffer_rsrc_t ar, __amdgpu_buffer_rsrc_t br, const int* kk, const int* la, int nt,
                       Raw8<T>* fa, const Raw8<T>& fb0, bool first_round) {
         f32x4_t acc[MAXT];
@@ -719,7 +728,7 @@ __global__ void __launch_bounds__(512) k_wgrad(WgArgs a) {
             pad_mask<T>(bc + g8, a.B, pm);
             raw_and(fb, pm);
             if (n >= a.G) raw_and(fb, pmb);             // pmb is all zero past G
-            if (do_db && first_round) db_add(fb);
+            if (first_round) db_add_raw(fb, dbacc);
 #pragma unroll
             for (int i = 0; i < MAXT; ++i) {
                 raw_and(fa[i], pm);
@@ -733,7 +742,7 @@ __global__ void __launch_bounds__(512) k_wgrad(WgArgs a) {
 #pragma unroll
         for (int i = 0; i < MAXT; ++i)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) addr[i][r] = __shfl(la[i], acc_row(lane, r)) + col;
+            for (int r = 0; r < 4; ++r) addr[i][r] = __shfl(la[i], acc_row(lane, r)) + c0 + col;
 #pragma unroll
         for (int i = 0; i < MAXT; ++i)
             if (i < nt)
@@ -769,7 +778,7 @@ __global__ void __launch_bounds__(512) k_wgrad(WgArgs a) {
         }
         __builtin_amdgcn_sched_barrier(0);     // keep the uses below the prefetch
         raw_and(fb0, pmb);
-        if (do_db) db_add(fb0);
+        db_add_raw(fb0, dbacc);
         finish(ar, br, kc, la, min(ntile, MAXT), fa, fb0, true);
         for (int jt0 = MAXT; jt0 < ntile; jt0 += MAXT) {
             int kv2[MAXT], mv2[MAXT];
@@ -779,7 +788,7 @@ __global__ void __launch_bounds__(512) k_wgrad(WgArgs a) {
             finish(ar, br, kc, la, min(ntile - jt0, MAXT), fa, fb0, false);
         }
     }
-    if (do_db) {                               // lanes l, l+16, l+32, l+48 hold column l
+    if (a.db && x == 0) {                      // lanes l, l+16, l+32, l+48 hold column l
         dbacc += __shfl_xor(dbacc, 16);
         dbacc += __shfl_xor(dbacc, 32);
         if (lane < 16 && n < a.G) {
@@ -787,10 +796,126 @@ __global__ void __launch_bounds__(512) k_wgrad(WgArgs a) {
             else a.out[(size_t)blockIdx.y * a.ostride + (size_t)a.K * a.G + n] = dbacc;
         }
     }
+    __syncthreads();
     float* out = a.out + (size_t)blockIdx.y * a.ostride;
-    for (int i = r0 * 16 + lane; i < r1 * 16; i += 64) {
-        const int kr = i >> 4, cc = i & 15;
-        if (n0 + cc < a.G) out[(size_t)kr * a.G + n0 + cc] = acc_lds[kr * WG_LD + cc];
+    for (int i = threadIdx.x; i < nrow * WG_NB; i += blockDim.x) {
+        const int rr = i / WG_NB, cc = i % WG_NB;
+        if (n0 + cc < a.G) out[(size_t)(r0 + rr) * a.G + n0 + cc] = acc_lds[rr * WG_LDC + cc];
+    }
+}
+
+// Weight gradient of a site whose keep lists are all the identity (p = 0,
+// or the dense comparison mode, where the mask zeroes the dropped rows):
+// every row takes part at every t, so the accumulators stay in registers
+// over the whole t-range; no gather, no scatter.  Same grid as the
+// row-sparse kernel: workgroup i owns slice x = i % 8 and 128 columns; wave w
+// owns 16 columns and every row of the slice, in passes of NTL 16-row tiles.
+// The operands of t+1 are loaded while t is multiplied.  The bias gradient
+// comes from the workgroups of the last slice (never empty: it ends at K).
+template <typename T, bool MASKED, int NTL>
+__global__ void __launch_bounds__(512) k_wgrad_full(WgArgs a) {
+    constexpr int NW = Raw8<T>::NW;
+    constexpr uint32_t ES = sizeof(T);
+    const int x = blockIdx.x % NXCD, cb = blockIdx.x / NXCD;
+    if (cb * WG_NB >= a.G) return;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int col = lane & 15, g8 = 8 * (lane >> 4);
+    const int n = cb * WG_NB + 16 * w + col;
+    const int r0 = slice_start(x, a.K), r1 = slice_start(x + 1, a.K);
+    const int t0 = blockIdx.y * a.tper;
+    const int t1 = min(a.T, t0 + a.tper);
+    uint32_t pm0[NW], pmb[NW];                 // batch-pad masks (B side also zero past G)
+    pad_mask<T>(g8, a.B, pm0);
+#pragma unroll
+    for (int q = 0; q < NW; ++q) pmb[q] = n < a.G ? pm0[q] : 0u;
+    const uint32_t boff = (uint32_t)(min(n, a.G - 1) * a.BP + g8) * ES;
+    const uint32_t abytes = (uint32_t)a.K * a.BP * ES, bbytes = (uint32_t)a.G * a.BP * ES;
+    float dbacc = 0.f;
+    auto act_rsrc = [&](int t) {
+        const T* act = (a.actT_first && t == a.t_first) ? (const T*)a.actT_first
+                                                        : (const T*)a.actT + (long)(t + a.shift) * a.tstride;
+        return buf_rsrc(act, abytes);
+    };
+    auto dat_rsrc = [&](int t) { return buf_rsrc((const T*)a.daT + (size_t)t * a.G * a.BP, bbytes); };
+
+    for (int rb = r0; rb < r1; rb += 16 * NTL) {           // passes over the slice's row tiles
+        const bool first = rb == r0;
+        int rowa[NTL];                         // A-fragment row of this lane in tile i (clamped into K)
+#pragma unroll
+        for (int i = 0; i < NTL; ++i) rowa[i] = min(rb + 16 * i + col, a.K - 1);
+        f32x4_t acc[NTL];
+#pragma unroll
+        for (int i = 0; i < NTL; ++i) acc[i] = f32x4_t{0, 0, 0, 0};
+        Raw8<T> fa[NTL], fb;
+        int mk[NTL];
+        auto issue = [&](int t) {
+            const __amdgpu_buffer_rsrc_t ar = act_rsrc(t);
+#pragma unroll
+            for (int i = 0; i < NTL; ++i) raw_load(fa[i], ar, (uint32_t)(rowa[i] * a.BP + g8) * ES);
+            raw_load(fb, dat_rsrc(t), boff);
+            if (MASKED) {
+                const uint8_t* mrow = a.site.mask + (size_t)t * a.site.kmax;
+#pragma unroll
+                for (int i = 0; i < NTL; ++i) mk[i] = mrow[rowa[i]];
+            }
+        };
+        if (t0 < t1) issue(t0);
+        for (int t = t0; t < t1; ++t) {
+            Raw8<T> ca[NTL], cb = fb;
+            int cm[NTL];
+#pragma unroll
+            for (int i = 0; i < NTL; ++i) { ca[i] = fa[i]; cm[i] = MASKED ? mk[i] : 1; }
+            issue(min(t + 1, t1 - 1));             // the last step reloads its own operands
+            __builtin_amdgcn_sched_barrier(0);     // keep the uses below the prefetch
+            raw_and(cb, pmb);
+            if (first) db_add_raw(cb, dbacc);
+#pragma unroll
+            for (int i = 0; i < NTL; ++i) {
+                raw_and(ca[i], pm0);
+                if (MASKED) {
+#pragma unroll
+                    for (int q = 0; q < NW; ++q) ca[i].w[q] = cm[i] ? ca[i].w[q] : 0u;
+                }
+                raw_mma(ca[i], cb, acc[i]);
+            }
+            for (int bc = 32; bc < a.B; bc += 32) {    // further batch chunks (B > 32)
+                const __amdgpu_buffer_rsrc_t ar = act_rsrc(t);
+                raw_load(cb, dat_rsrc(t), boff + (uint32_t)bc * ES);
+#pragma unroll
+                for (int i = 0; i < NTL; ++i) raw_load(ca[i], ar, (uint32_t)(rowa[i] * a.BP + bc + g8) * ES);
+                uint32_t pm[NW];
+                pad_mask<T>(bc + g8, a.B, pm);
+                raw_and(cb, pm);
+                if (n >= a.G) raw_and(cb, pmb);     // pmb is all zero past G
+                if (first) db_add_raw(cb, dbacc);
+#pragma unroll
+                for (int i = 0; i < NTL; ++i) {
+                    raw_and(ca[i], pm);
+                    if (MASKED) {
+#pragma unroll
+                        for (int q = 0; q < NW; ++q) ca[i].w[q] = cm[i] ? ca[i].w[q] : 0u;
+                    }
+                    raw_mma(ca[i], cb, acc[i]);
+                }
+            }
+        }
+        // output r of this lane is row 4*(lane/16)+r of the tile
+        float* out = a.out + (size_t)blockIdx.y * a.ostride;
+#pragma unroll
+        for (int i = 0; i < NTL; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int row = rb + 16 * i + acc_row(lane, r);
+                if (row < r1 && n < a.G) out[(size_t)row * a.G + n] = a.s * acc[i][r];
+            }
+    }
+    if (a.db && x == NXCD - 1) {               // (the last slice is never empty) lanes l, l+16, l+32, l+48 hold column l
+        dbacc += __shfl_xor(dbacc, 16);
+        dbacc += __shfl_xor(dbacc, 32);
+        if (lane < 16 && n < a.G) {
+            if (gridDim.y == 1) a.db[n] = dbacc;
+            else a.out[(size_t)blockIdx.y * a.ostride + (size_t)a.K * a.G + n] = dbacc;
+        }
     }
 }
 
@@ -1015,10 +1140,17 @@ void launch_dx(const DxArgs& a, int K, hipStream_t st) {
 }
 template <typename T>
 void launch_wgrad(const WgArgs& a, int ts, hipStream_t st) {
-    const size_t lds = (size_t)(a.K + 1) * WG_LD * sizeof(float);
-    const dim3 grid(xcd_grid((a.G + 15) / 16), ts);
-    if (a.dense) launch_k(KID_WGRAD, k_wgrad<T, true>, grid, dim3(512), lds, st, a);
-    else launch_k(KID_WGRAD, k_wgrad<T, false>, grid, dim3(512), lds, st, a);
+    const size_t lds = wgrad_lds_bytes(a.K);
+    const dim3 grid(NXCD * ((a.G + WG_NB - 1) / WG_NB), ts);
+    if (a.full) {
+        constexpr int NTL = sizeof(T) == 2 ? 6 : 4;
+        if (a.dense) launch_k(KID_WGRAD, k_wgrad_full<T, true, NTL>, grid, dim3(512), 0, st, a);
+        else launch_k(KID_WGRAD, k_wgrad_full<T, false, NTL>, grid, dim3(512), 0, st, a);
+    } else if (a.dense) {
+        launch_k(KID_WGRAD, k_wgrad<T, true>, grid, dim3(512), lds, st, a);
+    } else {
+        launch_k(KID_WGRAD, k_wgrad<T, false>, grid, dim3(512), lds, st, a);
+    }
 }
 void launch_wreduce(const float* part, float* dW, float* db, long n, long ostride, int G, int ts, hipStream_t st) {
     launch_k(KID_NONE, k_wreduce, dim3(nblk(n + G, 256, 8192)), dim3(256), 0, st, part, dW, db, n, ostride, G, ts);
