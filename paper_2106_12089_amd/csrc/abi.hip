@@ -22,15 +22,15 @@ template <typename T> void launch_fx(const FxArgs& a, hipStream_t st);
 template <typename T> void launch_step(const StepArgs& a, int D, hipStream_t st);
 template <typename T> void launch_bwd(const BwdArgs& a, int D, hipStream_t st);
 template <typename T> void launch_dx(const DxArgs& a, int K, hipStream_t st);
-template <typename T> void launch_wgrad(const WgArgs& a, int ts, hipStream_t st);
+template <typename T> void launch_wgrad(const WgBatch& b, hipStream_t st);
 template <typename T> void launch_fwd_init(const void*, const float*, float*, float*, long, hipStream_t);
-void launch_wreduce(const float* part, float* dW, float* db, long n, long ostride, int G, int ts, hipStream_t st);
 void launch_bwd_init(const float*, const float*, float*, float*, long, void*, int, int, int, long, long, hipStream_t);
 void launch_expand(const float*, int, const SiteView&, float*, int, int, int, hipStream_t);
 void launch_mse(const float*, const float*, const int32_t*, float*, float*, int, float*, int, int, int,
                 hipStream_t);
 int setup_kernel_attributes();
 bool timer_pair(int kid, hipEvent_t* e0, hipEvent_t* e1);
+void timer_unpair();
 template <typename T>
 hipError_t launch_fwd_persist(PFwdArgs& a, hipStream_t st, int timer_on, hipEvent_t e0, hipEvent_t e1);
 constexpr int KID_FWDP_ = 7;
@@ -87,16 +87,6 @@ int make_plan(const lstm_sd_dims* d, Plan* p, const char** why) {
     q.sites = q.L + q.L * q.D;
     q.kin_max = q.L > 1 ? (q.I > q.D * q.H ? q.I : q.D * q.H) : q.I;
     q.kmax = q.kin_max > q.H ? q.kin_max : q.H;
-    {
-        const int ncol = (q.G + 15) / 16;
-        int ts = (512 + ncol - 1) / ncol;
-        if (ts > 8) ts = 8;
-        if (ts > q.T) ts = q.T;
-        if (ts < (q.T + 63) / 64) ts = (q.T + 63) / 64;   // at most 64 steps per workgroup
-        if (ts < 1) ts = 1;
-        const int tper = (q.T + ts - 1) / ts;
-        q.ts = (q.T + tper - 1) / tper;
-    }
 
     const size_t A = 256, T = q.T, B = q.B, H = q.H, G = q.G, D = q.D, BP = q.BP, es = q.esize;
     const size_t S = q.sites, KM = q.kmax;
@@ -138,7 +128,6 @@ int make_plan(const lstm_sd_dims* d, Plan* p, const char** why) {
     q.w_dc = off;     off = align_up(off + D * B * H * 4, A);
     q.w_dhc = off;    off = align_up(off + D * B * H * 4, A);
     q.w_dxc = off;    off = align_up(off + 2 * T * B * (size_t)q.kin_max * 4, A);
-    q.w_wpart = off;  off = align_up(off + (q.ts > 1 ? (size_t)q.ts * (KM + 1) * G * 4 : 0), A);
     const size_t bwd = off;
     q.w_sync = align_up(fwd > bwd ? fwd : bwd, A);
     q.w_loss = q.w_sync + 8192;           // barrier counters (2), then the error flag at +4096
@@ -328,6 +317,7 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
         const bool timed = timer_pair(KID_FWDP_, &e0, &e1);
         if (launch_fwd_persist<E>(pa, st, timed, e0, e1) == hipSuccess) return hip_check("forward launch");
         (void)hipGetLastError();              // does not fit: one layer at a time below
+        if (timed) timer_unpair();
     }
     for (int l = 0; l < L; ++l) {
         const int kin = P.kin(l);
@@ -354,6 +344,7 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
             const bool timed = timer_pair(KID_FWDP_, &e0, &e1);
             if (launch_fwd_persist<E>(pa, st, timed, e0, e1) == hipSuccess) continue;
             (void)hipGetLastError();          // does not fit: per-step kernels below
+            if (timed) timer_unpair();
         }
         for (int s = 0; s < T; ++s) {
             StepArgs a;
@@ -450,13 +441,22 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
         launch_dx<E>(a, kin, st);
         if (l == 0) launch_expand(dxc_here, kin, nv, dx, B, kin, T, st);
     };
-    // weight and bias gradients of layer l (Eq. 11)
+    // weight and bias gradients (Eq. 11) of layer l: its problems join the
+    // row-sparse or the full batch, one launch each
+    WgBatch wgb[2];                            // [0] row-sparse, [1] full
+    wgb[0].np = wgb[1].np = 0;
+    auto add_wgrad = [&](const WgArgs& a) {
+        WgBatch& b = wgb[a.full ? 1 : 0];
+        if (b.np == WG_MAXP) {                 // full: launch it (its DA is complete)
+            launch_wgrad<E>(b, st);
+            b.np = 0;
+        }
+        b.p[b.np++] = a;
+    };
     auto layer_wgrad = [&](int l, int reg0) {
         const int kin = P.kin(l);
         const SiteView nv = site_view(P, mbuf, P.site_nr(l));
         const void* XT = l == 0 ? (const void*)(R + P.r_xT) : (const void*)(R + P.rybufT(l - 1));
-        const int tper = (T + P.ts - 1) / P.ts;
-        float* wpart = (float*)(W + P.w_wpart);
         for (int d = 0; d < D; ++d) {
             const int k = l * D + d;
             const char* rd = R + P.rdir(l, d);
@@ -464,14 +464,12 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
             memset(&a, 0, sizeof(a));
             a.actT = XT; a.tstride = (long)kin * BP; a.actT_first = nullptr; a.t_first = -1; a.shift = 0;
             a.daT = daT_of(reg0 + d);
-            a.site = nv; a.K = kin; a.B = B; a.BP = BP; a.G = G; a.T = T; a.tper = tper;
+            a.site = nv; a.K = kin; a.B = B; a.BP = BP; a.G = G; a.T = T;
             a.dense = !P.compact; a.s = P.s_nr;
-            a.out = P.ts > 1 ? wpart : g->dW[k];
-            a.ostride = (long)(kin + 1) * G;
+            a.out = g->dW[k];
             a.db = g->db[k];                      // the bias gradient rides on the input-weight pass
             a.full = P.p_nr == 0.0 || !P.compact;
-            launch_wgrad<E>(a, P.ts, st);
-            if (P.ts > 1) launch_wreduce(wpart, g->dW[k], g->db[k], (long)kin * G, a.ostride, G, P.ts, st);
+            add_wgrad(a);
 
             WgArgs u = a;
             u.actT = rd + P.r_hrecT; u.tstride = (long)H * BP;
@@ -480,12 +478,16 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
             u.shift = d == 0 ? -1 : 1;
             u.site = site_view(P, mbuf, P.site_rh(l, d));
             u.K = H; u.s = P.s_rh;
-            u.out = P.ts > 1 ? wpart : g->dU[k];
-            u.ostride = (long)H * G;
+            u.out = g->dU[k];
             u.db = nullptr;
             u.full = P.p_rh == 0.0 || !P.compact;
-            launch_wgrad<E>(u, P.ts, st);
-            if (P.ts > 1) launch_wreduce(wpart, g->dU[k], nullptr, (long)H * G, u.ostride, G, P.ts, st);
+            add_wgrad(u);
+        }
+    };
+    auto flush_wgrad = [&]() {
+        for (WgBatch& b : wgb) {
+            launch_wgrad<E>(b, st);
+            b.np = 0;
         }
     };
 
@@ -522,9 +524,11 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
         if (launch_bwd_persist<E>(pa, st, timed, e0, e1) == hipSuccess) {
             if (dx) layer_dx(0, 0, (float*)(W + P.w_dxc));
             for (int l = L - 1; l >= 0; --l) layer_wgrad(l, l);
+            flush_wgrad();
             return hip_check("backward launch");
         }
         (void)hipGetLastError();              // does not fit: one layer at a time below
+        if (timed) timer_unpair();
     }
 
     for (int l = L - 1; l >= 0; --l) {
@@ -551,8 +555,12 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
             }
             hipEvent_t e0 = nullptr, e1 = nullptr;
             const bool timed = timer_pair(KID_BWDP_, &e0, &e1);
-            if (launch_bwd_persist<E>(pa, st, timed, e0, e1) == hipSuccess) persistent_done = true;
-            else (void)hipGetLastError();     // does not fit: per-step kernels below
+            if (launch_bwd_persist<E>(pa, st, timed, e0, e1) == hipSuccess) {
+                persistent_done = true;
+            } else {
+                (void)hipGetLastError();      // does not fit: per-step kernels below
+                if (timed) timer_unpair();
+            }
         }
         // T pointwise steps plus one final pass (recurrent gradient of h0)
         for (int s = 0; s <= T && !persistent_done; ++s) {
@@ -606,6 +614,7 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
         }
         if (l > 0 || dx) layer_dx(l, 0, dxc_here);
         layer_wgrad(l, 0);
+        flush_wgrad();                        // before the next layer reuses the DA regions
     }
     return hip_check("backward launch");
 }

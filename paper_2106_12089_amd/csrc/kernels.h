@@ -132,9 +132,10 @@ struct DxArgs {
     float s;
 };
 
-// Row-scatter weight gradient of one layer/direction, t in [t0, t1) per
-// workgroup row of the grid:
-//   dW[keep_t[j]][n] += s * sum_b actT_t[keep_t[j]][b] DAT_t[n][b]
+// Weight gradient of one (layer, direction, site), summed over every step:
+//   dW[k][n] = s * sum_t sum_b actT_t[k][b] DAT_t[n][b]
+// over the rows k kept at t (row-sparse), or every row (times the mask byte
+// in dense mode); rows never kept are 0.  dW (and db) are overwritten.
 struct WgArgs {
     const void* actT;                   // actT + (t + shift)*tstride: [K][BP]
     long tstride;
@@ -142,13 +143,17 @@ struct WgArgs {
     int t_first, shift;
     const void* daT;                    // [T][G][BP]
     SiteView site;
-    float* out;                         // partial ts at out + ts*ostride: [K][G] (or dW when TS == 1)
-    long ostride;
-    float* db;                          // non-null: also the bias gradient (Eq. 11): row K of each
-                                        // partial when TS > 1, else db itself
-    int K, B, BP, G, T, tper, dense;
+    float* out;                         // dW [K][G]
+    float* db;                          // non-null: also the bias gradient (Eq. 11), the sum of DA^T
+    int K, B, BP, G, T, dense;
     int full;                           // every keep list of the site is the identity (p = 0, or dense mode)
     float s;
+};
+// Weight gradients of one kind (all row-sparse, or all full) in one launch
+constexpr int WG_MAXP = 8;
+struct WgBatch {
+    WgArgs p[WG_MAXP];
+    int np;
 };
 
 // Persistent forward recurrence of one layer (both directions): one

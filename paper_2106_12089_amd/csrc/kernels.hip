@@ -606,16 +606,16 @@ __device__ __forceinline__ void db_add_raw(const Raw8<T>& f, float& acc) {
 
 // ---------------------------------------------------------------------------
 // Row-sparse weight gradient (Eq. 11; Sec. 3.2 WG).  grid (8 * ceil(G/128),
-// TS), block 512 (8 waves), dynamic LDS (rows of a slice + 1) * WG_LDC floats.
-// Workgroup i owns neuron slice x = i % 8, the rows [floor(xK/8),
-// floor((x+1)K/8)) (workgroup i runs on XCD i % 8, so a slice's activation
-// rows stay in one XCD's L2), and the 128 gradient columns of block i / 8,
-// over the time steps [ts*tper, ts*tper + tper) (tper <= 64).  At each t the
-// kept rows of the slice (keep-list entries kseg[t][x] .. kseg[t][x+1]) are
-// taken in 16-row tiles; wave w multiplies them with its 16 DA^T columns and
-// adds each tile into its columns of the LDS accumulator.  Waves own disjoint
-// columns, so they run without barriers until the final write; the gathered
-// rows are shared through the cache.
+// 1, problems), block 512 (8 waves), dynamic LDS (rows of a slice + 1) *
+// WG_LDC floats.  Workgroup (i, z) owns, for problem z, neuron slice
+// x = i % 8, the rows [floor(xK/8), floor((x+1)K/8)) (workgroup i runs on
+// XCD i % 8, so a slice's activation rows stay in one XCD's L2), and the 128
+// gradient columns of block i / 8, over every time step (no partial sums).
+// At each t the kept rows of the slice (keep-list entries kseg[t][x] ..
+// kseg[t][x+1]) are taken in 16-row tiles; wave w multiplies them with its
+// 16 DA^T columns and adds each tile into its columns of the LDS
+// accumulator.  Waves own disjoint columns, so they run without barriers
+// until the final write; the gathered rows are shared through the cache.
 //
 // The kernel is built to issue few vector-ALU instructions per MFMA: the
 // operands are fetched with buffer loads (32-bit offsets, out-of-range reads
@@ -623,7 +623,8 @@ __device__ __forceinline__ void db_add_raw(const Raw8<T>& f, float& acc) {
 // (one AND per register), and the A rows of absent tile rows are not zeroed
 // at all: their products land in a spare LDS row, which is never read back.
 // Each wave loads the row indices and the DA^T fragment of t+1 while t is
-// multiplied.  All kept rows of a step are distinct, so the LDS sums read
+// multiplied.  The steps run in windows of 64, whose keep-list ranges sit in
+// LDS.  All kept rows of a step are distinct, so the LDS sums read
 // every row of the step first and then write them.  Rows never kept stay
 // zero.  Every wave also sums its DA^T fragments: the bias gradient.
 constexpr int WG_NB = 128;                 // gradient columns per workgroup
@@ -636,8 +637,9 @@ struct WgTiles<float> { static constexpr int N = 4; };
 // LDS bytes of the row-sparse weight gradient for a K-row weight
 inline size_t wgrad_lds_bytes(int K) { return (size_t)((K + NXCD - 1) / NXCD + 1) * WG_LDC * sizeof(float); }
 
-template <typename T, bool DENSE>
-__global__ void __launch_bounds__(512) k_wgrad(WgArgs a) {
+template <typename T, bool DENSE, bool MULTI>
+__global__ void __launch_bounds__(512) k_wgrad(WgBatch bt) {
+    const WgArgs& a = bt.p[blockIdx.z];
     constexpr int MAXT = WgTiles<T>::N;
     constexpr int NW = Raw8<T>::NW;
     constexpr uint32_t ES = sizeof(T);
@@ -651,14 +653,13 @@ __global__ void __launch_bounds__(512) k_wgrad(WgArgs a) {
     const int r0 = slice_start(x, a.K), r1 = slice_start(x + 1, a.K);
     const int nrow = r1 - r0;
     for (int i = lane; i < (nrow + 1) * 16; i += 64) acc_lds[(i >> 4) * WG_LDC + c0 + (i & 15)] = 0.0f;
-    const int t0 = blockIdx.y * a.tper;
-    const int t1 = min(a.T, t0 + a.tper);
-    // lane j holds the keep-list range of slice x at t0 + j
-    int segb = 0, sege = 0;
-    if (t0 + lane < t1) {
-        segb = a.site.kseg[(size_t)(t0 + lane) * (NXCD + 1) + x];
-        sege = a.site.kseg[(size_t)(t0 + lane) * (NXCD + 1) + x + 1];
-    }
+    // keep-list ranges of slice x at the steps t0 .. t1-1 of a window, in LDS
+    // (a table in registers would make the compiler wait for all loads
+    // wherever it is read)
+    __shared__ int segtab[2][64];
+    int t0 = 0, t1 = 0;
+    auto seg_b = [&](int t) { return __builtin_amdgcn_readfirstlane(segtab[0][t - t0]); };
+    auto seg_e = [&](int t) { return __builtin_amdgcn_readfirstlane(segtab[1][t - t0]); };
     uint32_t pm0[NW], pmb[NW];                 // batch-pad masks of chunk 0 (A side; B side adds n < G)
     pad_mask<T>(g8, a.B, pm0);
 #pragma unroll
@@ -671,8 +672,7 @@ __global__ void __launch_bounds__(512) k_wgrad(WgArgs a) {
     // of tiles jt0 .. jt0+MAXT-1 at t.  In dense mode the keep list is the
     // identity, so mask[j] is the mask byte of row keep[j].
     auto rows_issue = [&](int t, int jt0, int* kv, int* mv) {
-        const int jb = __builtin_amdgcn_readlane(segb, t - t0);
-        const int je = __builtin_amdgcn_readlane(sege, t - t0);
+        const int jb = seg_b(t), je = seg_e(t);
         const __amdgpu_buffer_rsrc_t kr = buf_rsrc(a.site.keep + (size_t)t * a.site.kmax, (uint32_t)a.site.kmax * 4);
         const __amdgpu_buffer_rsrc_t mr = buf_rsrc(a.site.mask + (size_t)t * a.site.kmax, (uint32_t)a.site.kmax);
 #pragma unroll
@@ -686,14 +686,15 @@ __global__ void __launch_bounds__(512) k_wgrad(WgArgs a) {
     // row of each tile's A-fragment lane; absent rows read row 0 and add
     // into the spare row
     auto rows_resolve = [&](int t, int jt0, const int* kv, const int* mv, int* kk, int* la) {
-        const int jb = __builtin_amdgcn_readlane(segb, t - t0);
-        const int je = __builtin_amdgcn_readlane(sege, t - t0);
+        const int jb = seg_b(t), je = seg_e(t);
 #pragma unroll
         for (int i = 0; i < MAXT; ++i) {
+            // bitwise selects: a branch here would let the compiler sink the
+            // loads of kv into it
             const int j = jb + (jt0 + i) * 16 + col;
-            const bool ok = j < je && (!DENSE || mv[i]);
-            kk[i] = ok ? kv[i] : 0;
-            la[i] = ok ? (kv[i] - r0) * WG_LDC : spare;
+            const int okm = -(int)(j < je && (!DENSE || mv[i]));
+            kk[i] = kv[i] & okm;
+            la[i] = (((kv[i] - r0) * WG_LDC) & okm) | (spare & ~okm);
         }
     };
     auto act_rsrc = [&](int t) {
@@ -720,7 +721,7 @@ __global__ void __launch_bounds__(512) k_wgrad(WgArgs a) {
             acc[i] = f32x4_t{0, 0, 0, 0};
             raw_mma(fa[i], fb0, acc[i]);
         }
-        for (int bc = 32; bc < a.B; bc += 32) {
+        for (int bc = 32; MULTI && bc < a.B; bc += 32) {
             Raw8<T> fb;
             raw_load(fb, br, boff + (uint32_t)bc * ES);
             a_issue(ar, bc, kk, fa);
@@ -755,49 +756,52 @@ __global__ void __launch_bounds__(512) k_wgrad(WgArgs a) {
                 for (int r = 0; r < 4; ++r) acc_lds[addr[i][r]] = old[i][r] + a.s * acc[i][r];
     };
 
-    int kv[MAXT], mv[MAXT];
-    Raw8<T> fb;
-    if (t0 < t1) {
+    for (t0 = 0; t0 < a.T; t0 += 64) {
+        t1 = min(a.T, t0 + 64);
+        __syncthreads();                       // the previous window's table is no longer read
+        if (threadIdx.x < t1 - t0) {
+            segtab[0][threadIdx.x] = a.site.kseg[(size_t)(t0 + threadIdx.x) * (NXCD + 1) + x];
+            segtab[1][threadIdx.x] = a.site.kseg[(size_t)(t0 + threadIdx.x) * (NXCD + 1) + x + 1];
+        }
+        __syncthreads();
+        int kv[MAXT], mv[MAXT];
+        Raw8<T> fb;
         rows_issue(t0, 0, kv, mv);
         raw_load(fb, dat_rsrc(t0), boff);
-    }
-    for (int t = t0; t < t1; ++t) {
-        const __amdgpu_buffer_rsrc_t ar = act_rsrc(t), br = dat_rsrc(t);
-        const int cnt = __builtin_amdgcn_readlane(sege, t - t0) - __builtin_amdgcn_readlane(segb, t - t0);
-        const int ntile = (cnt + 15) >> 4;
-        int kc[MAXT], la[MAXT];
-        rows_resolve(t, 0, kv, mv, kc, la);
-        Raw8<T> fb0 = fb;
-        Raw8<T> fa[MAXT];
-        a_issue(ar, 0, kc, fa);
-        {   // next step's rows and fragment (the last step reloads its own:
-            // an unconditional issue keeps the wait counts exact)
-            const int tn = min(t + 1, t1 - 1);
-            rows_issue(tn, 0, kv, mv);
-            raw_load(fb, dat_rsrc(tn), boff);
-        }
-        __builtin_amdgcn_sched_barrier(0);     // keep the uses below the prefetch
-        raw_and(fb0, pmb);
-        db_add_raw(fb0, dbacc);
-        finish(ar, br, kc, la, min(ntile, MAXT), fa, fb0, true);
-        for (int jt0 = MAXT; jt0 < ntile; jt0 += MAXT) {
-            int kv2[MAXT], mv2[MAXT];
-            rows_issue(t, jt0, kv2, mv2);
-            rows_resolve(t, jt0, kv2, mv2, kc, la);
+        for (int t = t0; t < t1; ++t) {
+            const __amdgpu_buffer_rsrc_t ar = act_rsrc(t), br = dat_rsrc(t);
+            const int ntile = (seg_e(t) - seg_b(t) + 15) >> 4;
+            int kc[MAXT], la[MAXT];
+            rows_resolve(t, 0, kv, mv, kc, la);
+            Raw8<T> fb0 = fb;
+            Raw8<T> fa[MAXT];
             a_issue(ar, 0, kc, fa);
-            finish(ar, br, kc, la, min(ntile - jt0, MAXT), fa, fb0, false);
+            {   // next step's rows and fragment (the last step reloads its own:
+                // an unconditional issue keeps the wait counts exact)
+                const int tn = min(t + 1, t1 - 1);
+                rows_issue(tn, 0, kv, mv);
+                raw_load(fb, dat_rsrc(tn), boff);
+            }
+            __builtin_amdgcn_sched_barrier(0);     // keep the uses below the prefetch
+            raw_and(fb0, pmb);
+            db_add_raw(fb0, dbacc);
+            finish(ar, br, kc, la, min(ntile, MAXT), fa, fb0, true);
+            for (int jt0 = MAXT; MULTI && jt0 < ntile; jt0 += MAXT) {   // more kept rows than one round
+                int kv2[MAXT], mv2[MAXT];
+                rows_issue(t, jt0, kv2, mv2);
+                rows_resolve(t, jt0, kv2, mv2, kc, la);
+                a_issue(ar, 0, kc, fa);
+                finish(ar, br, kc, la, min(ntile - jt0, MAXT), fa, fb0, false);
+            }
         }
     }
     if (a.db && x == 0) {                      // lanes l, l+16, l+32, l+48 hold column l
         dbacc += __shfl_xor(dbacc, 16);
         dbacc += __shfl_xor(dbacc, 32);
-        if (lane < 16 && n < a.G) {
-            if (gridDim.y == 1) a.db[n] = dbacc;
-            else a.out[(size_t)blockIdx.y * a.ostride + (size_t)a.K * a.G + n] = dbacc;
-        }
+        if (lane < 16 && n < a.G) a.db[n] = dbacc;
     }
     __syncthreads();
-    float* out = a.out + (size_t)blockIdx.y * a.ostride;
+    float* out = a.out;
     for (int i = threadIdx.x; i < nrow * WG_NB; i += blockDim.x) {
         const int rr = i / WG_NB, cc = i % WG_NB;
         if (n0 + cc < a.G) out[(size_t)(r0 + rr) * a.G + n0 + cc] = acc_lds[rr * WG_LDC + cc];
@@ -810,10 +814,11 @@ __global__ void __launch_bounds__(512) k_wgrad(WgArgs a) {
 // over the whole t-range; no gather, no scatter.  Same grid as the
 // row-sparse kernel: workgroup i owns slice x = i % 8 and 128 columns; wave w
 // owns 16 columns and every row of the slice, in passes of NTL 16-row tiles.
-// The operands of t+1 are loaded while t is multiplied.  The bias gradient
+// The operands of two steps are in flight while a step is multiplied.  The bias gradient
 // comes from the workgroups of the last slice (never empty: it ends at K).
-template <typename T, bool MASKED, int NTL>
-__global__ void __launch_bounds__(512) k_wgrad_full(WgArgs a) {
+template <typename T, bool MASKED, int NTL, bool MULTI>
+__global__ void __launch_bounds__(512) k_wgrad_full(WgBatch bt) {
+    const WgArgs& a = bt.p[blockIdx.z];
     constexpr int NW = Raw8<T>::NW;
     constexpr uint32_t ES = sizeof(T);
     const int x = blockIdx.x % NXCD, cb = blockIdx.x / NXCD;
@@ -822,8 +827,7 @@ __global__ void __launch_bounds__(512) k_wgrad_full(WgArgs a) {
     const int col = lane & 15, g8 = 8 * (lane >> 4);
     const int n = cb * WG_NB + 16 * w + col;
     const int r0 = slice_start(x, a.K), r1 = slice_start(x + 1, a.K);
-    const int t0 = blockIdx.y * a.tper;
-    const int t1 = min(a.T, t0 + a.tper);
+    const int t0 = 0, t1 = a.T;
     uint32_t pm0[NW], pmb[NW];                 // batch-pad masks (B side also zero past G)
     pad_mask<T>(g8, a.B, pm0);
 #pragma unroll
@@ -846,27 +850,26 @@ __global__ void __launch_bounds__(512) k_wgrad_full(WgArgs a) {
         f32x4_t acc[NTL];
 #pragma unroll
         for (int i = 0; i < NTL; ++i) acc[i] = f32x4_t{0, 0, 0, 0};
-        Raw8<T> fa[NTL], fb;
-        int mk[NTL];
-        auto issue = [&](int t) {
+        // operands of two steps in flight: slot = step % 2
+        Raw8<T> fa[2][NTL], fb[2];
+        int mk[2][NTL];
+        auto issue = [&](int t, int sl) {
             const __amdgpu_buffer_rsrc_t ar = act_rsrc(t);
 #pragma unroll
-            for (int i = 0; i < NTL; ++i) raw_load(fa[i], ar, (uint32_t)(rowa[i] * a.BP + g8) * ES);
-            raw_load(fb, dat_rsrc(t), boff);
+            for (int i = 0; i < NTL; ++i) raw_load(fa[sl][i], ar, (uint32_t)(rowa[i] * a.BP + g8) * ES);
+            raw_load(fb[sl], dat_rsrc(t), boff);
             if (MASKED) {
-                const uint8_t* mrow = a.site.mask + (size_t)t * a.site.kmax;
+                const __amdgpu_buffer_rsrc_t mr = buf_rsrc(a.site.mask + (size_t)t * a.site.kmax, (uint32_t)a.site.kmax);
 #pragma unroll
-                for (int i = 0; i < NTL; ++i) mk[i] = mrow[rowa[i]];
+                for (int i = 0; i < NTL; ++i) mk[sl][i] = (int)__builtin_amdgcn_raw_buffer_load_b8(mr, (uint32_t)rowa[i], 0, 0);
             }
         };
-        if (t0 < t1) issue(t0);
-        for (int t = t0; t < t1; ++t) {
-            Raw8<T> ca[NTL], cb = fb;
-            int cm[NTL];
-#pragma unroll
-            for (int i = 0; i < NTL; ++i) { ca[i] = fa[i]; cm[i] = MASKED ? mk[i] : 1; }
-            issue(min(t + 1, t1 - 1));             // the last step reloads its own operands
-            __builtin_amdgcn_sched_barrier(0);     // keep the uses below the prefetch
+        // the step in slot sl (none past the range); then that slot takes the
+        // operands of step tn (loads that always go out keep the wait counts exact)
+        auto step = [&](int t, int sl, int tn) {
+          if (t < t1) {
+            Raw8<T>(&ca)[NTL] = fa[sl];
+            Raw8<T>& cb = fb[sl];
             raw_and(cb, pmb);
             if (first) db_add_raw(cb, dbacc);
 #pragma unroll
@@ -874,33 +877,44 @@ __global__ void __launch_bounds__(512) k_wgrad_full(WgArgs a) {
                 raw_and(ca[i], pm0);
                 if (MASKED) {
 #pragma unroll
-                    for (int q = 0; q < NW; ++q) ca[i].w[q] = cm[i] ? ca[i].w[q] : 0u;
+                    for (int q = 0; q < NW; ++q) ca[i].w[q] = mk[sl][i] ? ca[i].w[q] : 0u;
                 }
                 raw_mma(ca[i], cb, acc[i]);
             }
-            for (int bc = 32; bc < a.B; bc += 32) {    // further batch chunks (B > 32)
+            for (int bc = 32; MULTI && bc < a.B; bc += 32) {    // further batch chunks (B > 32)
                 const __amdgpu_buffer_rsrc_t ar = act_rsrc(t);
-                raw_load(cb, dat_rsrc(t), boff + (uint32_t)bc * ES);
+                Raw8<T> xb, xa[NTL];
+                raw_load(xb, dat_rsrc(t), boff + (uint32_t)bc * ES);
 #pragma unroll
-                for (int i = 0; i < NTL; ++i) raw_load(ca[i], ar, (uint32_t)(rowa[i] * a.BP + bc + g8) * ES);
+                for (int i = 0; i < NTL; ++i) raw_load(xa[i], ar, (uint32_t)(rowa[i] * a.BP + bc + g8) * ES);
                 uint32_t pm[NW];
                 pad_mask<T>(bc + g8, a.B, pm);
-                raw_and(cb, pm);
-                if (n >= a.G) raw_and(cb, pmb);     // pmb is all zero past G
-                if (first) db_add_raw(cb, dbacc);
+                raw_and(xb, pm);
+                if (n >= a.G) raw_and(xb, pmb);     // pmb is all zero past G
+                if (first) db_add_raw(xb, dbacc);
 #pragma unroll
                 for (int i = 0; i < NTL; ++i) {
-                    raw_and(ca[i], pm);
+                    raw_and(xa[i], pm);
                     if (MASKED) {
 #pragma unroll
-                        for (int q = 0; q < NW; ++q) ca[i].w[q] = cm[i] ? ca[i].w[q] : 0u;
+                        for (int q = 0; q < NW; ++q) xa[i].w[q] = mk[sl][i] ? xa[i].w[q] : 0u;
                     }
-                    raw_mma(ca[i], cb, acc[i]);
+                    raw_mma(xa[i], xb, acc[i]);
                 }
             }
+          }
+            issue(tn, sl);
+        };
+        if (t0 < t1) {
+            issue(t0, 0);
+            issue(min(t0 + 1, t1 - 1), 1);
+        }
+        for (int t = t0; t < t1; t += 2) {
+            step(t, 0, min(t + 2, t1 - 1));
+            step(t + 1, 1, min(t + 3, t1 - 1));
         }
         // output r of this lane is row 4*(lane/16)+r of the tile
-        float* out = a.out + (size_t)blockIdx.y * a.ostride;
+        float* out = a.out;
 #pragma unroll
         for (int i = 0; i < NTL; ++i)
 #pragma unroll
@@ -912,22 +926,7 @@ __global__ void __launch_bounds__(512) k_wgrad_full(WgArgs a) {
     if (a.db && x == NXCD - 1) {               // (the last slice is never empty) lanes l, l+16, l+32, l+48 hold column l
         dbacc += __shfl_xor(dbacc, 16);
         dbacc += __shfl_xor(dbacc, 32);
-        if (lane < 16 && n < a.G) {
-            if (gridDim.y == 1) a.db[n] = dbacc;
-            else a.out[(size_t)blockIdx.y * a.ostride + (size_t)a.K * a.G + n] = dbacc;
-        }
-    }
-}
-
-// dW = sum over ts of the partials (each ostride floats apart); with db,
-// the row after the K*G gradient entries sums into db
-__global__ void k_wreduce(const float* part, float* dW, float* db, long n, long ostride, int G, int ts) {
-    const long nn = db ? n + G : n;
-    for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < nn; i += (long)gridDim.x * blockDim.x) {
-        float s = 0.f;
-        for (int q = 0; q < ts; ++q) s += part[(size_t)q * ostride + i];
-        if (i < n) dW[i] = s;
-        else db[i - n] = s;
+        if (lane < 16 && n < a.G) a.db[n] = dbacc;
     }
 }
 
@@ -1054,6 +1053,11 @@ bool timer_pair(int kid, hipEvent_t* e0, hipEvent_t* e1) {
     return *e0 && *e1;
 }
 
+// Returns the last pair handed out (its launch did not happen).
+void timer_unpair() {
+    if (g_ev_used >= 2) g_ev_used -= 2;
+}
+
 int kernel_timer_start(const char* name) {
     for (int i = 0; i < KID_COUNT; ++i)
         if (name && strcmp(name, kKernelNames[i]) == 0) {
@@ -1139,21 +1143,32 @@ void launch_dx(const DxArgs& a, int K, hipStream_t st) {
     else launch_k(KID_DX, k_dx<T, 4>, grid, dim3(256), 0, st, a);
 }
 template <typename T>
-void launch_wgrad(const WgArgs& a, int ts, hipStream_t st) {
-    const size_t lds = wgrad_lds_bytes(a.K);
-    const dim3 grid(NXCD * ((a.G + WG_NB - 1) / WG_NB), ts);
+void launch_wgrad(const WgBatch& b, hipStream_t st) {
+    if (b.np == 0) return;
+    const WgArgs& a = b.p[0];                  // the problems share G, B and the kind
+    const dim3 grid(NXCD * ((a.G + WG_NB - 1) / WG_NB), 1, b.np);
+    size_t lds = 0;
+    bool multi = a.B > 32;                     // builds with the extra loops (batch chunks, tile rounds)
+    for (int i = 0; i < b.np; ++i) {
+        lds = std::max(lds, wgrad_lds_bytes(b.p[i].K));
+        multi = multi || (b.p[i].K + NXCD - 1) / NXCD > 16 * WgTiles<T>::N;
+    }
     if (a.full) {
         constexpr int NTL = sizeof(T) == 2 ? 6 : 4;
-        if (a.dense) launch_k(KID_WGRAD, k_wgrad_full<T, true, NTL>, grid, dim3(512), 0, st, a);
-        else launch_k(KID_WGRAD, k_wgrad_full<T, false, NTL>, grid, dim3(512), 0, st, a);
+        if (a.B > 32) {
+            if (a.dense) launch_k(KID_WGRAD, k_wgrad_full<T, true, NTL, true>, grid, dim3(512), 0, st, b);
+            else launch_k(KID_WGRAD, k_wgrad_full<T, false, NTL, true>, grid, dim3(512), 0, st, b);
+        } else {
+            if (a.dense) launch_k(KID_WGRAD, k_wgrad_full<T, true, NTL, false>, grid, dim3(512), 0, st, b);
+            else launch_k(KID_WGRAD, k_wgrad_full<T, false, NTL, false>, grid, dim3(512), 0, st, b);
+        }
     } else if (a.dense) {
-        launch_k(KID_WGRAD, k_wgrad<T, true>, grid, dim3(512), lds, st, a);
+        if (multi) launch_k(KID_WGRAD, k_wgrad<T, true, true>, grid, dim3(512), lds, st, b);
+        else launch_k(KID_WGRAD, k_wgrad<T, true, false>, grid, dim3(512), lds, st, b);
     } else {
-        launch_k(KID_WGRAD, k_wgrad<T, false>, grid, dim3(512), lds, st, a);
+        if (multi) launch_k(KID_WGRAD, k_wgrad<T, false, true>, grid, dim3(512), lds, st, b);
+        else launch_k(KID_WGRAD, k_wgrad<T, false, false>, grid, dim3(512), lds, st, b);
     }
-}
-void launch_wreduce(const float* part, float* dW, float* db, long n, long ostride, int G, int ts, hipStream_t st) {
-    launch_k(KID_NONE, k_wreduce, dim3(nblk(n + G, 256, 8192)), dim3(256), 0, st, part, dW, db, n, ostride, G, ts);
 }
 template <typename T>
 void launch_fwd_init(const void* h0, const float* c0, float* hT, float* cT, long n, hipStream_t st) {
@@ -1177,9 +1192,11 @@ void launch_mse(const float* y, const float* tg, const int32_t* lengths, float* 
 static int g_attr_done = 0;
 int setup_kernel_attributes() {
     if (g_attr_done) return 0;
-    const int lds = 160 * 1024;
-    const void* fns[4] = {(const void*)k_wgrad<float, false>, (const void*)k_wgrad<bf16, false>,
-                          (const void*)k_wgrad<float, true>, (const void*)k_wgrad<bf16, true>};
+    const int lds = 160 * 1024 - 1024;     // (the kernels also hold up to 1 KB of static LDS)
+    const void* fns[8] = {(const void*)k_wgrad<float, false, false>, (const void*)k_wgrad<bf16, false, false>,
+                          (const void*)k_wgrad<float, true, false>, (const void*)k_wgrad<bf16, true, false>,
+                          (const void*)k_wgrad<float, false, true>, (const void*)k_wgrad<bf16, false, true>,
+                          (const void*)k_wgrad<float, true, true>, (const void*)k_wgrad<bf16, true, true>};
     for (const void* f : fns)
         if (hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, lds) != hipSuccess) return LSTM_SD_EHIP;
     g_attr_done = 1;
@@ -1192,7 +1209,7 @@ int setup_kernel_attributes() {
     template void launch_step<T>(const StepArgs&, int, hipStream_t);                        \
     template void launch_bwd<T>(const BwdArgs&, int, hipStream_t);                          \
     template void launch_dx<T>(const DxArgs&, int, hipStream_t);                            \
-    template void launch_wgrad<T>(const WgArgs&, int, hipStream_t);                         \
+    template void launch_wgrad<T>(const WgBatch&, hipStream_t);                             \
     template void launch_fwd_init<T>(const void*, const float*, float*, float*, long, hipStream_t);
 LSD_INST(float)
 LSD_INST(bf16)

@@ -19,7 +19,6 @@ struct Plan {
     int BP;               // batch rounded up to 32 (transposed copies)
     int MGc;              // number of 64-row groups of the batch
     int sites, kmax, kin_max;
-    int ts;               // time splits of the weight-gradient kernel
     int HP;               // H rounded up to 8 (row pitch of the per-step h buffer)
     int mtiles;           // 16-row tiles of the batch
     size_t das, hxs;      // elements of one fragment-major DA block / h exchange slot
@@ -37,7 +36,7 @@ struct Plan {
 
     // workspace
     size_t w_gx, w_hrec, w_hx, w_xx;            // forward
-    size_t w_da, w_daT, w_dxw, w_dc, w_dhc, w_dxc, w_wpart;  // backward
+    size_t w_da, w_daT, w_dxw, w_dc, w_dhc, w_dxc;  // backward
     size_t w_sync;                              // barrier counters and error flag
     size_t w_loss, w_total;
 

@@ -151,7 +151,7 @@ def test_kernel_timer_counts_launches():
     torch.cuda.synchronize()
     for name, per_step in (("fwd_persist", fwd_persist_launches(cfg)), ("step", 0),
                            ("bwd_persist", fwd_persist_launches(cfg)), ("bwd", 0),
-                           ("wgrad", 2 * cfg.num_layers * cfg.num_dirs)):
+                           ("wgrad", fwd_persist_launches(cfg))):   # one batch (all sites row-sparse) per pass
         B_.lstm_sd_kernel_timer_start(name)
         for _ in range(3):
             s.forward()
