@@ -628,6 +628,7 @@ __device__ __forceinline__ void db_add_raw(const Raw8<T>& f, float& acc) {
 // every row of the step first and then write them.  Rows never kept stay
 // zero.  Every wave also sums its DA^T fragments: the bias gradient.
 constexpr int WG_NB = 128;                 // gradient columns per workgroup
+constexpr int WG_NWV = 4;                  // waves per workgroup: 32 columns (two 16-column tiles) each
 constexpr int WG_LDC = WG_NB + 4;          // LDS accumulator row pitch (floats)
 template <typename T>
 struct WgTiles { static constexpr int N = 6; };   // 16-row tiles in registers at once
@@ -638,7 +639,7 @@ struct WgTiles<float> { static constexpr int N = 4; };
 inline size_t wgrad_lds_bytes(int K) { return (size_t)((K + NXCD - 1) / NXCD + 1) * WG_LDC * sizeof(float); }
 
 template <typename T, bool DENSE, bool MULTI>
-__global__ void __launch_bounds__(512) k_wgrad(WgBatch bt) {
+__global__ void __launch_bounds__(64 * WG_NWV) k_wgrad(WgBatch bt) {
     const WgArgs& a = bt.p[blockIdx.z];
     constexpr int MAXT = WgTiles<T>::N;
     constexpr int NW = Raw8<T>::NW;
@@ -648,11 +649,11 @@ __global__ void __launch_bounds__(512) k_wgrad(WgBatch bt) {
     if (cb * WG_NB >= a.G) return;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int col = lane & 15, g8 = 8 * (lane >> 4);
-    const int c0 = 16 * w;                       // this wave's columns within the block
-    const int n0 = cb * WG_NB, n = n0 + c0 + col;
+    const int c0 = 32 * w;                       // this wave's columns within the block: two tiles
+    const int n0 = cb * WG_NB, n = n0 + c0 + col;   // (columns n and n + 16)
     const int r0 = slice_start(x, a.K), r1 = slice_start(x + 1, a.K);
     const int nrow = r1 - r0;
-    for (int i = lane; i < (nrow + 1) * 16; i += 64) acc_lds[(i >> 4) * WG_LDC + c0 + (i & 15)] = 0.0f;
+    for (int i = lane; i < (nrow + 1) * 32; i += 64) acc_lds[(i >> 5) * WG_LDC + c0 + (i & 31)] = 0.0f;
     // keep-list ranges of slice x at the steps t0 .. t1-1 of a window, in LDS
     // (a table in registers would make the compiler wait for all loads
     // wherever it is read)
@@ -660,11 +661,15 @@ __global__ void __launch_bounds__(512) k_wgrad(WgBatch bt) {
     int t0 = 0, t1 = 0;
     auto seg_b = [&](int t) { return __builtin_amdgcn_readfirstlane(segtab[0][t - t0]); };
     auto seg_e = [&](int t) { return __builtin_amdgcn_readfirstlane(segtab[1][t - t0]); };
-    uint32_t pm0[NW], pmb[NW];                 // batch-pad masks of chunk 0 (A side; B side adds n < G)
+    uint32_t pm0[NW], pmb[2][NW];              // batch-pad masks of chunk 0 (A side; B side adds n < G)
     pad_mask<T>(g8, a.B, pm0);
+    uint32_t boff[2];                          // DA^T fragment offsets of the two column tiles
 #pragma unroll
-    for (int q = 0; q < NW; ++q) pmb[q] = n < a.G ? pm0[q] : 0u;
-    const uint32_t boff = (uint32_t)(min(n, a.G - 1) * a.BP + g8) * ES;   // DA^T fragment offset
+    for (int h = 0; h < 2; ++h) {
+#pragma unroll
+        for (int q = 0; q < NW; ++q) pmb[h][q] = n + 16 * h < a.G ? pm0[q] : 0u;
+        boff[h] = (uint32_t)(min(n + 16 * h, a.G - 1) * a.BP + g8) * ES;
+    }
     const uint32_t abytes = (uint32_t)a.K * a.BP * ES, bbytes = (uint32_t)a.G * a.BP * ES;
     const int spare = nrow * WG_LDC;
 
@@ -707,39 +712,47 @@ __global__ void __launch_bounds__(512) k_wgrad(WgBatch bt) {
 #pragma unroll
         for (int i = 0; i < MAXT; ++i) raw_load(fa[i], ar, (uint32_t)(kk[i] * a.BP + bc + g8) * ES);
     };
-    float dbacc = 0.f;
-    // multiply the tiles (chunk-0 fragments already loaded), finish the other
-    // batch chunks, and add the tiles into their LDS rows.  Tiles past nt
-    // are multiplied too (their rows are absent): unconditional products
-    // keep the loads out of branches.
+    float dbacc[2] = {0.f, 0.f};
+    // multiply the tiles (chunk-0 fragments already loaded) with both column
+    // tiles, finish the other batch chunks, and add the tiles into their LDS
+    // rows.  Tiles past nt are multiplied too (their rows are absent):
+    // unconditional products keep the loads out of branches.
     auto finish = [&](__amdgpu_buffer_rsrc_t ar, __amdgpu_buffer_rsrc_t br, const int* kk, const int* la, int nt,
-                      Raw8<T>* fa, const Raw8<T>& fb0, bool first_round) {
-        f32x4_t acc[MAXT];
+                      Raw8<T>* fa, const Raw8<T>* fb0, bool first_round) {
+        f32x4_t acc[MAXT][2];
 #pragma unroll
         for (int i = 0; i < MAXT; ++i) {
             raw_and(fa[i], pm0);
-            acc[i] = f32x4_t{0, 0, 0, 0};
-            raw_mma(fa[i], fb0, acc[i]);
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                acc[i][h] = f32x4_t{0, 0, 0, 0};
+                raw_mma(fa[i], fb0[h], acc[i][h]);
+            }
         }
         for (int bc = 32; MULTI && bc < a.B; bc += 32) {
-            Raw8<T> fb;
-            raw_load(fb, br, boff + (uint32_t)bc * ES);
+            Raw8<T> fb[2];
+            raw_load(fb[0], br, boff[0] + (uint32_t)bc * ES);
+            raw_load(fb[1], br, boff[1] + (uint32_t)bc * ES);
             a_issue(ar, bc, kk, fa);
             uint32_t pm[NW];
             pad_mask<T>(bc + g8, a.B, pm);
-            raw_and(fb, pm);
-            if (n >= a.G) raw_and(fb, pmb);             // pmb is all zero past G
-            if (first_round) db_add_raw(fb, dbacc);
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                raw_and(fb[h], pm);
+                if (n + 16 * h >= a.G) raw_and(fb[h], pmb[h]);   // pmb is all zero past G
+                if (first_round) db_add_raw(fb[h], dbacc[h]);
+            }
 #pragma unroll
             for (int i = 0; i < MAXT; ++i) {
                 raw_and(fa[i], pm);
-                raw_mma(fa[i], fb, acc[i]);
+                raw_mma(fa[i], fb[0], acc[i][0]);
+                raw_mma(fa[i], fb[1], acc[i][1]);
             }
         }
         // output r of this lane is row 4*(lane/16)+r of the tile, whose LDS
         // row address is held by that lane
         int addr[MAXT][4];
-        float old[MAXT][4];
+        float old[MAXT][4][2];
 #pragma unroll
         for (int i = 0; i < MAXT; ++i)
 #pragma unroll
@@ -748,12 +761,18 @@ __global__ void __launch_bounds__(512) k_wgrad(WgBatch bt) {
         for (int i = 0; i < MAXT; ++i)
             if (i < nt)
 #pragma unroll
-                for (int r = 0; r < 4; ++r) old[i][r] = acc_lds[addr[i][r]];
+                for (int r = 0; r < 4; ++r) {
+                    old[i][r][0] = acc_lds[addr[i][r]];
+                    old[i][r][1] = acc_lds[addr[i][r] + 16];
+                }
 #pragma unroll
         for (int i = 0; i < MAXT; ++i)
             if (i < nt)
 #pragma unroll
-                for (int r = 0; r < 4; ++r) acc_lds[addr[i][r]] = old[i][r] + a.s * acc[i][r];
+                for (int r = 0; r < 4; ++r) {
+                    acc_lds[addr[i][r]] = old[i][r][0] + a.s * acc[i][0][r];
+                    acc_lds[addr[i][r] + 16] = old[i][r][1] + a.s * acc[i][1][r];
+                }
     };
 
     for (t0 = 0; t0 < a.T; t0 += 64) {
@@ -765,26 +784,31 @@ __global__ void __launch_bounds__(512) k_wgrad(WgBatch bt) {
         }
         __syncthreads();
         int kv[MAXT], mv[MAXT];
-        Raw8<T> fb;
+        Raw8<T> fb[2];
         rows_issue(t0, 0, kv, mv);
-        raw_load(fb, dat_rsrc(t0), boff);
+        raw_load(fb[0], dat_rsrc(t0), boff[0]);
+        raw_load(fb[1], dat_rsrc(t0), boff[1]);
         for (int t = t0; t < t1; ++t) {
             const __amdgpu_buffer_rsrc_t ar = act_rsrc(t), br = dat_rsrc(t);
             const int ntile = (seg_e(t) - seg_b(t) + 15) >> 4;
             int kc[MAXT], la[MAXT];
             rows_resolve(t, 0, kv, mv, kc, la);
-            Raw8<T> fb0 = fb;
+            Raw8<T> fb0[2] = {fb[0], fb[1]};
             Raw8<T> fa[MAXT];
             a_issue(ar, 0, kc, fa);
-            {   // next step's rows and fragment (the last step reloads its own:
+            {   // next step's rows and fragments (the last step reloads its own:
                 // an unconditional issue keeps the wait counts exact)
                 const int tn = min(t + 1, t1 - 1);
                 rows_issue(tn, 0, kv, mv);
-                raw_load(fb, dat_rsrc(tn), boff);
+                raw_load(fb[0], dat_rsrc(tn), boff[0]);
+                raw_load(fb[1], dat_rsrc(tn), boff[1]);
             }
             __builtin_amdgcn_sched_barrier(0);     // keep the uses below the prefetch
-            raw_and(fb0, pmb);
-            db_add_raw(fb0, dbacc);
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                raw_and(fb0[h], pmb[h]);
+                db_add_raw(fb0[h], dbacc[h]);
+            }
             finish(ar, br, kc, la, min(ntile, MAXT), fa, fb0, true);
             for (int jt0 = MAXT; MULTI && jt0 < ntile; jt0 += MAXT) {   // more kept rows than one round
                 int kv2[MAXT], mv2[MAXT];
@@ -795,10 +819,14 @@ __global__ void __launch_bounds__(512) k_wgrad(WgBatch bt) {
             }
         }
     }
-    if (a.db && x == 0) {                      // lanes l, l+16, l+32, l+48 hold column l
-        dbacc += __shfl_xor(dbacc, 16);
-        dbacc += __shfl_xor(dbacc, 32);
-        if (lane < 16 && n < a.G) a.db[n] = dbacc;
+    if (a.db && x == 0) {                      // lanes l, l+16, l+32, l+48 hold column l (+16)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            float v = dbacc[h];
+            v += __shfl_xor(v, 16);
+            v += __shfl_xor(v, 32);
+            if (lane < 16 && n + 16 * h < a.G) a.db[n + 16 * h] = v;
+        }
     }
     __syncthreads();
     float* out = a.out;
@@ -813,11 +841,12 @@ __global__ void __launch_bounds__(512) k_wgrad(WgBatch bt) {
 // every row takes part at every t, so the accumulators stay in registers
 // over the whole t-range; no gather, no scatter.  Same grid as the
 // row-sparse kernel: workgroup i owns slice x = i % 8 and 128 columns; wave w
-// owns 16 columns and every row of the slice, in passes of NTL 16-row tiles.
-// The operands of two steps are in flight while a step is multiplied.  The bias gradient
-// comes from the workgroups of the last slice (never empty: it ends at K).
+// owns 32 columns (two tiles: each A fragment feeds two products) and every
+// row of the slice, in passes of NTL 16-row tiles.  The operands of two
+// steps are in flight while a step is multiplied.  The bias gradient comes
+// from the workgroups of the last slice (never empty: it ends at K).
 template <typename T, bool MASKED, int NTL, bool MULTI>
-__global__ void __launch_bounds__(512) k_wgrad_full(WgBatch bt) {
+__global__ void __launch_bounds__(64 * WG_NWV) k_wgrad_full(WgBatch bt) {
     const WgArgs& a = bt.p[blockIdx.z];
     constexpr int NW = Raw8<T>::NW;
     constexpr uint32_t ES = sizeof(T);
@@ -825,16 +854,20 @@ __global__ void __launch_bounds__(512) k_wgrad_full(WgBatch bt) {
     if (cb * WG_NB >= a.G) return;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int col = lane & 15, g8 = 8 * (lane >> 4);
-    const int n = cb * WG_NB + 16 * w + col;
+    const int n = cb * WG_NB + 32 * w + col;   // columns n and n + 16
     const int r0 = slice_start(x, a.K), r1 = slice_start(x + 1, a.K);
     const int t0 = 0, t1 = a.T;
-    uint32_t pm0[NW], pmb[NW];                 // batch-pad masks (B side also zero past G)
+    uint32_t pm0[NW], pmb[2][NW];              // batch-pad masks (B side also zero past G)
     pad_mask<T>(g8, a.B, pm0);
+    uint32_t boff[2];
 #pragma unroll
-    for (int q = 0; q < NW; ++q) pmb[q] = n < a.G ? pm0[q] : 0u;
-    const uint32_t boff = (uint32_t)(min(n, a.G - 1) * a.BP + g8) * ES;
+    for (int h = 0; h < 2; ++h) {
+#pragma unroll
+        for (int q = 0; q < NW; ++q) pmb[h][q] = n + 16 * h < a.G ? pm0[q] : 0u;
+        boff[h] = (uint32_t)(min(n + 16 * h, a.G - 1) * a.BP + g8) * ES;
+    }
     const uint32_t abytes = (uint32_t)a.K * a.BP * ES, bbytes = (uint32_t)a.G * a.BP * ES;
-    float dbacc = 0.f;
+    float dbacc[2] = {0.f, 0.f};
     auto act_rsrc = [&](int t) {
         const T* act = (a.actT_first && t == a.t_first) ? (const T*)a.actT_first
                                                         : (const T*)a.actT + (long)(t + a.shift) * a.tstride;
@@ -847,17 +880,18 @@ __global__ void __launch_bounds__(512) k_wgrad_full(WgBatch bt) {
         int rowa[NTL];                         // A-fragment row of this lane in tile i (clamped into K)
 #pragma unroll
         for (int i = 0; i < NTL; ++i) rowa[i] = min(rb + 16 * i + col, a.K - 1);
-        f32x4_t acc[NTL];
+        f32x4_t acc[NTL][2];
 #pragma unroll
-        for (int i = 0; i < NTL; ++i) acc[i] = f32x4_t{0, 0, 0, 0};
+        for (int i = 0; i < NTL; ++i) acc[i][0] = acc[i][1] = f32x4_t{0, 0, 0, 0};
         // operands of two steps in flight: slot = step % 2
-        Raw8<T> fa[2][NTL], fb[2];
+        Raw8<T> fa[2][NTL], fb[2][2];
         int mk[2][NTL];
         auto issue = [&](int t, int sl) {
-            const __amdgpu_buffer_rsrc_t ar = act_rsrc(t);
+            const __amdgpu_buffer_rsrc_t ar = act_rsrc(t), br = dat_rsrc(t);
 #pragma unroll
             for (int i = 0; i < NTL; ++i) raw_load(fa[sl][i], ar, (uint32_t)(rowa[i] * a.BP + g8) * ES);
-            raw_load(fb[sl], dat_rsrc(t), boff);
+            raw_load(fb[sl][0], br, boff[0]);
+            raw_load(fb[sl][1], br, boff[1]);
             if (MASKED) {
                 const __amdgpu_buffer_rsrc_t mr = buf_rsrc(a.site.mask + (size_t)t * a.site.kmax, (uint32_t)a.site.kmax);
 #pragma unroll
@@ -869,9 +903,11 @@ __global__ void __launch_bounds__(512) k_wgrad_full(WgBatch bt) {
         auto step = [&](int t, int sl, int tn) {
           if (t < t1) {
             Raw8<T>(&ca)[NTL] = fa[sl];
-            Raw8<T>& cb = fb[sl];
-            raw_and(cb, pmb);
-            if (first) db_add_raw(cb, dbacc);
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                raw_and(fb[sl][h], pmb[h]);
+                if (first) db_add_raw(fb[sl][h], dbacc[h]);
+            }
 #pragma unroll
             for (int i = 0; i < NTL; ++i) {
                 raw_and(ca[i], pm0);
@@ -879,19 +915,24 @@ __global__ void __launch_bounds__(512) k_wgrad_full(WgBatch bt) {
 #pragma unroll
                     for (int q = 0; q < NW; ++q) ca[i].w[q] = mk[sl][i] ? ca[i].w[q] : 0u;
                 }
-                raw_mma(ca[i], cb, acc[i]);
+                raw_mma(ca[i], fb[sl][0], acc[i][0]);
+                raw_mma(ca[i], fb[sl][1], acc[i][1]);
             }
             for (int bc = 32; MULTI && bc < a.B; bc += 32) {    // further batch chunks (B > 32)
-                const __amdgpu_buffer_rsrc_t ar = act_rsrc(t);
-                Raw8<T> xb, xa[NTL];
-                raw_load(xb, dat_rsrc(t), boff + (uint32_t)bc * ES);
+                const __amdgpu_buffer_rsrc_t ar = act_rsrc(t), br = dat_rsrc(t);
+                Raw8<T> xb[2], xa[NTL];
+                raw_load(xb[0], br, boff[0] + (uint32_t)bc * ES);
+                raw_load(xb[1], br, boff[1] + (uint32_t)bc * ES);
 #pragma unroll
                 for (int i = 0; i < NTL; ++i) raw_load(xa[i], ar, (uint32_t)(rowa[i] * a.BP + bc + g8) * ES);
                 uint32_t pm[NW];
                 pad_mask<T>(bc + g8, a.B, pm);
-                raw_and(xb, pm);
-                if (n >= a.G) raw_and(xb, pmb);     // pmb is all zero past G
-                if (first) db_add_raw(xb, dbacc);
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    raw_and(xb[h], pm);
+                    if (n + 16 * h >= a.G) raw_and(xb[h], pmb[h]);   // pmb is all zero past G
+                    if (first) db_add_raw(xb[h], dbacc[h]);
+                }
 #pragma unroll
                 for (int i = 0; i < NTL; ++i) {
                     raw_and(xa[i], pm);
@@ -899,7 +940,8 @@ __global__ void __launch_bounds__(512) k_wgrad_full(WgBatch bt) {
 #pragma unroll
                         for (int q = 0; q < NW; ++q) xa[i].w[q] = mk[sl][i] ? xa[i].w[q] : 0u;
                     }
-                    raw_mma(xa[i], xb, acc[i]);
+                    raw_mma(xa[i], xb[0], acc[i][0]);
+                    raw_mma(xa[i], xb[1], acc[i][1]);
                 }
             }
           }
@@ -920,13 +962,19 @@ __global__ void __launch_bounds__(512) k_wgrad_full(WgBatch bt) {
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int row = rb + 16 * i + acc_row(lane, r);
-                if (row < r1 && n < a.G) out[(size_t)row * a.G + n] = a.s * acc[i][r];
+#pragma unroll
+                for (int h = 0; h < 2; ++h)
+                    if (row < r1 && n + 16 * h < a.G) out[(size_t)row * a.G + n + 16 * h] = a.s * acc[i][h][r];
             }
     }
     if (a.db && x == NXCD - 1) {               // (the last slice is never empty) lanes l, l+16, l+32, l+48 hold column l
-        dbacc += __shfl_xor(dbacc, 16);
-        dbacc += __shfl_xor(dbacc, 32);
-        if (lane < 16 && n < a.G) a.db[n] = dbacc;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            float v = dbacc[h];
+            v += __shfl_xor(v, 16);
+            v += __shfl_xor(v, 32);
+            if (lane < 16 && n + 16 * h < a.G) a.db[n + 16 * h] = v;
+        }
     }
 }
 
@@ -1156,18 +1204,18 @@ void launch_wgrad(const WgBatch& b, hipStream_t st) {
     if (a.full) {
         constexpr int NTL = sizeof(T) == 2 ? 6 : 4;
         if (a.B > 32) {
-            if (a.dense) launch_k(KID_WGRAD, k_wgrad_full<T, true, NTL, true>, grid, dim3(512), 0, st, b);
-            else launch_k(KID_WGRAD, k_wgrad_full<T, false, NTL, true>, grid, dim3(512), 0, st, b);
+            if (a.dense) launch_k(KID_WGRAD, k_wgrad_full<T, true, NTL, true>, grid, dim3(64 * WG_NWV), 0, st, b);
+            else launch_k(KID_WGRAD, k_wgrad_full<T, false, NTL, true>, grid, dim3(64 * WG_NWV), 0, st, b);
         } else {
-            if (a.dense) launch_k(KID_WGRAD, k_wgrad_full<T, true, NTL, false>, grid, dim3(512), 0, st, b);
-            else launch_k(KID_WGRAD, k_wgrad_full<T, false, NTL, false>, grid, dim3(512), 0, st, b);
+            if (a.dense) launch_k(KID_WGRAD, k_wgrad_full<T, true, NTL, false>, grid, dim3(64 * WG_NWV), 0, st, b);
+            else launch_k(KID_WGRAD, k_wgrad_full<T, false, NTL, false>, grid, dim3(64 * WG_NWV), 0, st, b);
         }
     } else if (a.dense) {
-        if (multi) launch_k(KID_WGRAD, k_wgrad<T, true, true>, grid, dim3(512), lds, st, b);
-        else launch_k(KID_WGRAD, k_wgrad<T, true, false>, grid, dim3(512), lds, st, b);
+        if (multi) launch_k(KID_WGRAD, k_wgrad<T, true, true>, grid, dim3(64 * WG_NWV), lds, st, b);
+        else launch_k(KID_WGRAD, k_wgrad<T, true, false>, grid, dim3(64 * WG_NWV), lds, st, b);
     } else {
-        if (multi) launch_k(KID_WGRAD, k_wgrad<T, false, true>, grid, dim3(512), lds, st, b);
-        else launch_k(KID_WGRAD, k_wgrad<T, false, false>, grid, dim3(512), lds, st, b);
+        if (multi) launch_k(KID_WGRAD, k_wgrad<T, false, true>, grid, dim3(64 * WG_NWV), lds, st, b);
+        else launch_k(KID_WGRAD, k_wgrad<T, false, false>, grid, dim3(64 * WG_NWV), lds, st, b);
     }
 }
 template <typename T>
