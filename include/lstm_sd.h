@@ -112,10 +112,10 @@ typedef struct {
  *   drop  int32 [sites][T][kmax]  ascending dropped indices (compact = 1);
  *                                 empty when compact = 0
  *   dcount int32 [sites][T]       number of entries of drop
- *   kseg  int32 [sites][T][9]     kseg[x] = number of kept neurons below
- *                                 floor(x*K(s)/8), x = 0..8: the keep list
- *                                 split into 8 slices of neuron indices
- *   dseg  int32 [sites][T][9]     the same for the drop list */
+ *   kseg  int32 [sites][T][17]    kseg[x] = number of kept neurons below
+ *                                 floor(x*K(s)/16), x = 0..16: the keep list
+ *                                 split into 16 segments of neuron indices
+ *   dseg  int32 [sites][T][17]    the same for the drop list */
 typedef struct {
     int32_t sites;
     int32_t kmax;

@@ -97,8 +97,8 @@ int make_plan(const lstm_sd_dims* d, Plan* p, const char** why) {
     q.m_count = off;  off = align_up(off + S * T * 4, A);
     q.m_drop = off;   off = align_up(off + S * T * KM * 4, A);
     q.m_dcount = off; off = align_up(off + S * T * 4, A);
-    q.m_kseg = off;   off = align_up(off + S * T * 9 * 4, A);
-    q.m_dseg = off;   off = align_up(off + S * T * 9 * 4, A);
+    q.m_kseg = off;   off = align_up(off + S * T * 17 * 4, A);
+    q.m_dseg = off;   off = align_up(off + S * T * 17 * 4, A);
     q.m_total = off;
 
     off = 0;
@@ -176,8 +176,8 @@ static SiteView site_view(const Plan& P, const void* mbuf, int s) {
     v.count = (const int32_t*)(m + P.m_count) + (size_t)s * P.T;
     v.drop = (const int32_t*)(m + P.m_drop) + row;
     v.dcount = (const int32_t*)(m + P.m_dcount) + (size_t)s * P.T;
-    v.kseg = (const int32_t*)(m + P.m_kseg) + (size_t)s * P.T * 9;
-    v.dseg = (const int32_t*)(m + P.m_dseg) + (size_t)s * P.T * 9;
+    v.kseg = (const int32_t*)(m + P.m_kseg) + (size_t)s * P.T * 17;
+    v.dseg = (const int32_t*)(m + P.m_dseg) + (size_t)s * P.T * 17;
     v.kmax = P.kmax;
     return v;
 }
@@ -589,8 +589,8 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
                     bd.ncount = rv.count + tn;
                     bd.ndrop = rv.drop + (size_t)tn * P.kmax;
                     bd.ndcount = rv.dcount + tn;
-                    bd.nkseg = rv.kseg + (size_t)tn * 9;
-                    bd.ndseg = rv.dseg + (size_t)tn * 9;
+                    bd.nkseg = rv.kseg + (size_t)tn * 17;
+                    bd.ndseg = rv.dseg + (size_t)tn * 17;
                 }
                 if (final_pass) {
                     bd.dh0 = dh0 + (size_t)k * B * H;

@@ -33,8 +33,8 @@ struct SiteView {
     const int32_t* count;
     const int32_t* drop;
     const int32_t* dcount;
-    const int32_t* kseg;                // [T][9]
-    const int32_t* dseg;                // [T][9]
+    const int32_t* kseg;                // [T][17]: keep-list offsets of 16 neuron segments
+    const int32_t* dseg;                // [T][17]
     int kmax;
 };
 
@@ -95,8 +95,8 @@ struct BwdDir {
     const int32_t* ncount;
     const int32_t* ndrop;               // dropped units of that step
     const int32_t* ndcount;
-    const int32_t* nkseg;               // [9] slice offsets of nkeep
-    const int32_t* ndseg;               // [9] slice offsets of ndrop
+    const int32_t* nkseg;               // [17] segment offsets of nkeep (slice x: 2x .. 2x+2)
+    const int32_t* ndseg;               // [17] segment offsets of ndrop
     const void* U;                      // [H][G]
     // pointwise at t
     const float* gates;                 // [B][G]

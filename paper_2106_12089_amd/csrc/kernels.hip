@@ -44,6 +44,7 @@ __device__ __forceinline__ void zero4(T* o) {
 // multiple of 8 to a logical tile so that every XCD owns one contiguous range
 // of tiles (and its L2 keeps the matching slice of the weights); -1 = idle.
 constexpr int NXCD = 8;
+constexpr int NSEG = 16;                   // keep-list segments: slice x of 8 is segments 2x, 2x+1
 __device__ __forceinline__ int xcd_tile(int bx, int ntiles) {
     const int per = (ntiles + NXCD - 1) / NXCD;
     const int x = bx % NXCD, i = bx / NXCD;
@@ -52,6 +53,7 @@ __device__ __forceinline__ int xcd_tile(int bx, int ntiles) {
 }
 // First neuron of slice x of a K-neuron site (slices of floor(x*K/8)).
 __device__ __forceinline__ int slice_start(int x, int K) { return (x * K) / NXCD; }
+__device__ __forceinline__ int seg_start(int x, int K) { return (x * K) / NSEG; }   // seg_start(2x) = slice_start(x)
 
 // ---------------------------------------------------------------------------
 // Masks (Sec. 3.1, Case-III) and their compaction into keep/drop lists.
@@ -66,8 +68,8 @@ __global__ void __launch_bounds__(256) k_mask_build(MaskArgs a) {
     int32_t* krow = a.keep + row;
     int32_t* prow = a.pos + row;
     int32_t* drow = a.drop + row;
-    int32_t* ksrow = a.kseg + ((size_t)s * a.T + t) * (NXCD + 1);
-    int32_t* dsrow = a.dseg + ((size_t)s * a.T + t) * (NXCD + 1);
+    int32_t* ksrow = a.kseg + ((size_t)s * a.T + t) * (NSEG + 1);
+    int32_t* dsrow = a.dseg + ((size_t)s * a.T + t) * (NSEG + 1);
     if (a.generate) {
         const uint64_t thr = a.thr[s];
         for (int q = tid; q < (K + 3) / 4; q += blockDim.x) {
@@ -93,8 +95,8 @@ __global__ void __launch_bounds__(256) k_mask_build(MaskArgs a) {
     __syncthreads();
     if (!a.compact) {
         for (int k = tid; k < K; k += blockDim.x) { krow[k] = k; prow[k] = k; }
-        if (tid <= NXCD) {
-            ksrow[tid] = slice_start(tid, K);
+        if (tid <= NSEG) {
+            ksrow[tid] = seg_start(tid, K);
             dsrow[tid] = 0;
         }
         if (tid == 0) {
@@ -122,8 +124,8 @@ __global__ void __launch_bounds__(256) k_mask_build(MaskArgs a) {
         if (k < K) {
             if (f) { krow[off + pre] = k; prow[k] = off + pre; }
             else { drow[doff + dpre] = k; prow[k] = -1; }
-            for (int x = 0; x < NXCD; ++x)
-                if (k == slice_start(x, K)) { ksrow[x] = off + pre; dsrow[x] = doff + dpre; }
+            for (int x = 0; x < NSEG; ++x)
+                if (k == seg_start(x, K)) { ksrow[x] = off + pre; dsrow[x] = doff + dpre; }
         }
         base += tot;
         dbase += dtot;
@@ -132,8 +134,8 @@ __global__ void __launch_bounds__(256) k_mask_build(MaskArgs a) {
     if (tid == 0) {
         a.count[(size_t)s * a.T + t] = base;
         a.dcount[(size_t)s * a.T + t] = dbase;
-        ksrow[NXCD] = base;
-        dsrow[NXCD] = dbase;
+        ksrow[NSEG] = base;
+        dsrow[NSEG] = dbase;
     }
 }
 
@@ -409,9 +411,9 @@ __global__ void __launch_bounds__(1024) k_bwd(BwdArgs a) {
     int lo, hi;
     const int32_t* list;
     if (kept_tile) {
-        lo = D.nkseg[x]; hi = D.nkseg[x + 1]; list = D.nkeep;
+        lo = D.nkseg[2 * x]; hi = D.nkseg[2 * x + 2]; list = D.nkeep;
     } else if (a.has_next) {
-        lo = D.ndseg[x]; hi = D.ndseg[x + 1]; list = D.ndrop;
+        lo = D.ndseg[2 * x]; hi = D.ndseg[2 * x + 2]; list = D.ndrop;
     } else {
         lo = slice_start(x, H); hi = slice_start(x + 1, H); list = nullptr;
     }
@@ -528,9 +530,9 @@ __global__ void __launch_bounds__(256) k_dx(DxArgs a) {
     const int t = blockIdx.y;
     // slot -> (XCD slice x, tile ti): kept rows of t inside slice x of W
     const int x = blockIdx.x % NXCD, ti = blockIdx.x / NXCD;
-    const int32_t* ks = a.site.kseg + (size_t)t * (NXCD + 1);
-    const int hi = ks[x + 1];
-    const int j0 = ks[x] + 16 * ti;
+    const int32_t* ks = a.site.kseg + (size_t)t * (NSEG + 1);
+    const int hi = ks[2 * x + 2];
+    const int j0 = ks[2 * x] + 16 * ti;
     if (ti >= a.tps || j0 >= hi) return;
     const int cnt = hi;                     // columns of this tile end at the slice end
     const int m0 = blockIdx.z * 64;
@@ -639,9 +641,9 @@ struct WgTiles<float> { static constexpr int N = 4; };
 inline size_t wgrad_lds_bytes(int K) { return (size_t)((K + NXCD - 1) / NXCD + 1) * WG_LDC * sizeof(float); }
 
 template <typename T, bool DENSE, bool MULTI>
-__global__ void __launch_bounds__(64 * WG_NWV) k_wgrad(WgBatch bt) {
+__global__ void __launch_bounds__(128 * WG_NWV) k_wgrad(WgBatch bt) {
     const WgArgs& a = bt.p[blockIdx.z];
-    constexpr int MAXT = WgTiles<T>::N;
+    constexpr int MAXT = WgTiles<T>::N / 2;     // 16-row tiles of a round (a wave takes half a slice)
     constexpr int NW = Raw8<T>::NW;
     constexpr uint32_t ES = sizeof(T);
     extern __shared__ float acc_lds[];   // [rows of the slice + 1][WG_LDC]
@@ -649,18 +651,19 @@ __global__ void __launch_bounds__(64 * WG_NWV) k_wgrad(WgBatch bt) {
     if (cb * WG_NB >= a.G) return;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int col = lane & 15, g8 = 8 * (lane >> 4);
-    const int c0 = 32 * w;                       // this wave's columns within the block: two tiles
+    const int rh = w / WG_NWV;                   // the half of the slice whose kept rows this wave takes
+    const int c0 = 32 * (w % WG_NWV);            // this wave's columns within the block: two tiles
     const int n0 = cb * WG_NB, n = n0 + c0 + col;   // (columns n and n + 16)
     const int r0 = slice_start(x, a.K), r1 = slice_start(x + 1, a.K);
     const int nrow = r1 - r0;
-    for (int i = lane; i < (nrow + 1) * 32; i += 64) acc_lds[(i >> 5) * WG_LDC + c0 + (i & 31)] = 0.0f;
+    for (int i = lane + 64 * rh; i < (nrow + 1) * 32; i += 128) acc_lds[(i >> 5) * WG_LDC + c0 + (i & 31)] = 0.0f;
     // keep-list ranges of slice x at the steps t0 .. t1-1 of a window, in LDS
     // (a table in registers would make the compiler wait for all loads
     // wherever it is read)
-    __shared__ int segtab[2][64];
+    __shared__ int segtab[3][64];                // segments 2x, 2x+1 and their end
     int t0 = 0, t1 = 0;
-    auto seg_b = [&](int t) { return __builtin_amdgcn_readfirstlane(segtab[0][t - t0]); };
-    auto seg_e = [&](int t) { return __builtin_amdgcn_readfirstlane(segtab[1][t - t0]); };
+    auto seg_b = [&](int t) { return __builtin_amdgcn_readfirstlane(segtab[rh][t - t0]); };
+    auto seg_e = [&](int t) { return __builtin_amdgcn_readfirstlane(segtab[rh + 1][t - t0]); };
     uint32_t pm0[NW], pmb[2][NW];              // batch-pad masks of chunk 0 (A side; B side adds n < G)
     pad_mask<T>(g8, a.B, pm0);
     uint32_t boff[2];                          // DA^T fragment offsets of the two column tiles
@@ -779,8 +782,10 @@ __global__ void __launch_bounds__(64 * WG_NWV) k_wgrad(WgBatch bt) {
         t1 = min(a.T, t0 + 64);
         __syncthreads();                       // the previous window's table is no longer read
         if (threadIdx.x < t1 - t0) {
-            segtab[0][threadIdx.x] = a.site.kseg[(size_t)(t0 + threadIdx.x) * (NXCD + 1) + x];
-            segtab[1][threadIdx.x] = a.site.kseg[(size_t)(t0 + threadIdx.x) * (NXCD + 1) + x + 1];
+            const int32_t* ks = a.site.kseg + (size_t)(t0 + threadIdx.x) * (NSEG + 1) + 2 * x;
+            segtab[0][threadIdx.x] = ks[0];
+            segtab[1][threadIdx.x] = ks[1];
+            segtab[2][threadIdx.x] = ks[2];
         }
         __syncthreads();
         int kv[MAXT], mv[MAXT];
@@ -819,7 +824,7 @@ __global__ void __launch_bounds__(64 * WG_NWV) k_wgrad(WgBatch bt) {
             }
         }
     }
-    if (a.db && x == 0) {                      // lanes l, l+16, l+32, l+48 hold column l (+16)
+    if (a.db && x == 0 && rh == 0) {           // lanes l, l+16, l+32, l+48 hold column l (+16)
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
             float v = dbacc[h];
@@ -1199,7 +1204,7 @@ void launch_wgrad(const WgBatch& b, hipStream_t st) {
     bool multi = a.B > 32;                     // builds with the extra loops (batch chunks, tile rounds)
     for (int i = 0; i < b.np; ++i) {
         lds = std::max(lds, wgrad_lds_bytes(b.p[i].K));
-        multi = multi || (b.p[i].K + NXCD - 1) / NXCD > 16 * WgTiles<T>::N;
+        multi = multi || (b.p[i].K + NSEG - 1) / NSEG > 16 * (WgTiles<T>::N / 2);
     }
     if (a.full) {
         constexpr int NTL = sizeof(T) == 2 ? 6 : 4;
@@ -1211,11 +1216,11 @@ void launch_wgrad(const WgBatch& b, hipStream_t st) {
             else launch_k(KID_WGRAD, k_wgrad_full<T, false, NTL, false>, grid, dim3(64 * WG_NWV), 0, st, b);
         }
     } else if (a.dense) {
-        if (multi) launch_k(KID_WGRAD, k_wgrad<T, true, true>, grid, dim3(64 * WG_NWV), lds, st, b);
-        else launch_k(KID_WGRAD, k_wgrad<T, true, false>, grid, dim3(64 * WG_NWV), lds, st, b);
+        if (multi) launch_k(KID_WGRAD, k_wgrad<T, true, true>, grid, dim3(128 * WG_NWV), lds, st, b);
+        else launch_k(KID_WGRAD, k_wgrad<T, true, false>, grid, dim3(128 * WG_NWV), lds, st, b);
     } else {
-        if (multi) launch_k(KID_WGRAD, k_wgrad<T, false, true>, grid, dim3(64 * WG_NWV), lds, st, b);
-        else launch_k(KID_WGRAD, k_wgrad<T, false, false>, grid, dim3(64 * WG_NWV), lds, st, b);
+        if (multi) launch_k(KID_WGRAD, k_wgrad<T, false, true>, grid, dim3(128 * WG_NWV), lds, st, b);
+        else launch_k(KID_WGRAD, k_wgrad<T, false, false>, grid, dim3(128 * WG_NWV), lds, st, b);
     }
 }
 template <typename T>

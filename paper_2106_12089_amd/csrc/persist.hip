@@ -296,6 +296,53 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
                 raw_load(fa[i][mt], hr, m0 + 16 * mt + (lane & 15) < B ? (uint32_t)(frag_lane_off(c, m0 / 16 + mt, lane, a.mtiles) * sizeof(T)) : OOB_OFF);
         }
     };
+    // B fragments (weight-slice rows of the keep list) of round c0, from LDS
+    auto gather_b = [&](int c0, int n, const int16_t* kid, const T* Bt, int bp, int kfull, Raw8<T> (&fbr)[MAXC][NT]) {
+#pragma unroll
+        for (int i = 0; i < MAXC; ++i) {
+            const int kc = 32 * (c0 + w + NW * i);
+            if (n == kfull) {                   // identity keep list: contiguous rows
+                const int kb = kc < n ? kc : 0;
+#pragma unroll
+                for (int nt = 0; nt < NT; ++nt) raw_lds(fbr[i][nt], Bt + (size_t)(nt * 16 + (lane & 15)) * bp + kb + g8);
+            } else {
+                const int4 k8 = *(const int4*)(kid + kc + g8);          // 8 int16 keep indices
+                const int kw[4] = {k8.x, k8.y, k8.z, k8.w};
+                int kk[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const int j = kc + g8 + e;
+                    kk[e] = j < n ? (int)(int16_t)(kw[e >> 1] >> (16 * (e & 1))) : 0;
+                }
+#pragma unroll
+                for (int nt = 0; nt < NT; ++nt) {
+                    const T* row = Bt + (size_t)(nt * 16 + (lane & 15)) * bp;
+                    Frag<T> fb;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) fb.v[e] = row[kk[e]];
+                    raw_from(fbr[i][nt], fb);
+                }
+            }
+        }
+    };
+    // acc += A fragments of round c0 times the B fragments gathered for it
+    auto compute_b = [&](Raw8<T> (&fa)[MAXC][MT], const Raw8<T> (&fbr)[MAXC][NT], int c0, int n,
+                         f32x4_t (&acc)[MT][NT]) {
+#pragma unroll
+        for (int i = 0; i < MAXC; ++i) {
+            const int kc = 32 * (c0 + w + NW * i);
+            if (kc + 32 > n) {                  // last chunk: slots past the keep count hold stale values
+                uint32_t m[Raw8<T>::NW];
+                pad_mask<T>(kc + g8, n, m);
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) raw_and(fa[i][mt], m);
+            }
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int nt = 0; nt < NT; ++nt) raw_mma(fa[i][mt], fbr[i][nt], acc[mt][nt]);
+        }
+    };
     auto compute = [&](Raw8<T> (&fa)[MAXC][MT], int c0, int n, const int16_t* kid, const T* Bt, int bp, int kfull,
                        f32x4_t (&acc)[MT][NT]) {
 #pragma unroll
@@ -370,6 +417,15 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
         // ---- wait for h_{t-1} of every workgroup of this slot (and for the
         // layer below to have published x_t)
         commit_kidx();
+        // when each contraction takes one round, the B fragments of the
+        // recurrent product (U rows through this step's keep list) are read
+        // from LDS before the waits
+        const bool one_round = cnt <= 32 * NW * MAXC && (!has_x || cnt_x <= 32 * NW * MAXC);
+        Raw8<T> bh[MAXC][NT];
+        if (one_round) {
+            __syncthreads();                    // the keep lists just committed
+            gather_b(0, cnt, kidx, Ut, HP, H, bh);
+        }
         // x_t of the layer below (which runs ahead: a counter value seen
         // earlier usually covers this step), then h_{t-1} of this slot
         // (the skip decision uses a register copy taken after the wait's
@@ -386,13 +442,13 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
             for (int j = 0; j < NT; ++j) acc[i][j] = accx[i][j] = f32x4_t{0, 0, 0, 0};
         const T* hsrc = (const T*)D.hx + (size_t)(s & 1) * hxs;
         const T* xsrc = has_x ? (const T*)D.xin + (size_t)t * a.xxs : nullptr;
-        if (has_x && cnt <= 32 * NW * MAXC && cnt_x <= 32 * NW * MAXC) {
+        if (one_round) {
             // one round each: both sets of exchange loads go out together
             Raw8<T> fh[MAXC][MT], fx[MAXC][MT];
             issue(hsrc, hxs, 0, fh);
-            issue(xsrc, a.xxs, 0, fx);
-            compute(fh, 0, cnt, kidx, Ut, HP, H, acc);
-            compute(fx, 0, cnt_x, kidx_x, Wt, KP, kin, accx);
+            if (has_x) issue(xsrc, a.xxs, 0, fx);
+            compute_b(fh, bh, 0, cnt, acc);
+            if (has_x) compute(fx, 0, cnt_x, kidx_x, Wt, KP, kin, accx);
         } else {
             contract(hsrc, hxs, cnt, kidx, Ut, HP, H, acc);
             if (has_x) contract(xsrc, a.xxs, cnt_x, kidx_x, Wt, KP, kin, accx);

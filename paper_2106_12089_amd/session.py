@@ -104,8 +104,8 @@ class Session:
         count = i32(lay.count_off, S * T).reshape(S, T)
         drop = i32(lay.drop_off, S * T * K).reshape(S, T, K)
         dcount = i32(lay.dcount_off, S * T).reshape(S, T)
-        self.last_segments = (i32(lay.kseg_off, S * T * 9).reshape(S, T, 9),
-                              i32(lay.dseg_off, S * T * 9).reshape(S, T, 9))
+        self.last_segments = (i32(lay.kseg_off, S * T * 17).reshape(S, T, 17),
+                              i32(lay.dseg_off, S * T * 17).reshape(S, T, 17))
         return mask, keep, pos, count, drop, dcount
 
     def write_masks(self, mask_u8: np.ndarray):

@@ -36,7 +36,7 @@ def check_masks(sess, cfg, m_nr, m_rh, compact):
     for s, ref in enumerate(site_list(cfg, m_nr, m_rh)):
         K = ref.shape[1]
         assert np.array_equal(mask[s, :, :K], ref), f"mask site {s}"
-        starts = [(x * K) // 8 for x in range(9)]
+        starts = [(x * K) // 16 for x in range(17)]
         for t in range(ref.shape[0]):
             if compact:
                 kept_below = [int(ref[t][:st].sum()) for st in starts]
