@@ -119,6 +119,7 @@ int make_plan(const lstm_sd_dims* d, Plan* p, const char** why) {
     q.w_hrec = off; off = align_up(off + D * 2 * B * (size_t)q.HP * es, A);
     q.w_hx = off;   off = align_up(off + (D > (size_t)q.L ? D : (size_t)q.L) * 2 * (size_t)q.hxs * es, A);
     q.w_xx = off;   off = align_up(off + (size_t)(q.L - 1) * T * q.xxs * es, A);
+    q.w_gxs = off;  off = align_up(off + (q.D == 1 ? (size_t)(q.L - 1) * T * B * G * 4 : 0), A);
     const size_t fwd = off;
     off = 0;
     const size_t NR = D > (size_t)q.L ? D : (size_t)q.L;   // DA regions: per direction, or per layer of a stack
@@ -130,7 +131,7 @@ int make_plan(const lstm_sd_dims* d, Plan* p, const char** why) {
     q.w_dxc = off;    off = align_up(off + 2 * T * B * (size_t)q.kin_max * 4, A);
     const size_t bwd = off;
     q.w_sync = align_up(fwd > bwd ? fwd : bwd, A);
-    q.w_loss = q.w_sync + 8192;           // barrier counters (2), then the error flag at +4096
+    q.w_loss = q.w_sync + 8192;           // barrier counters (one 256-byte line per slot), error flag at +4096
     q.w_total = q.w_loss + 16384;
     return LSTM_SD_OK;
 }
@@ -140,6 +141,12 @@ int make_plan(const lstm_sd_dims* d, Plan* p, const char** why) {
 // LSTM_SD_STACK=0 runs a unidirectional stack one layer per launch
 static bool use_stacked() {
     const char* v = getenv("LSTM_SD_STACK");
+    return !(v && v[0] == '0');
+}
+
+// LSTM_SD_FWD_WORKERS=0: a stacked forward without input-product workers
+static bool use_fwd_workers() {
+    const char* v = getenv("LSTM_SD_FWD_WORKERS");
     return !(v && v[0] == '0');
 }
 
@@ -256,7 +263,8 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
         pd.hT = hT + (size_t)k * B * H;
         pd.cT = cT + (size_t)k * B * H;
         pd.dir = d;
-        pd.below = -1;
+        pd.role = 0;
+        pd.dep = -1;
         if (l == L - 1) {
             pd.y = y + d * H;
         } else {
@@ -289,24 +297,36 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
             launch_fx<E>(f, st);
         }
     };
-    if (use_persistent() && use_stacked() && D == 1 && L > 1 && L <= 4) {
-        launch_fx_layer(0);
+    // A unidirectional stack in one launch: with an input-product worker
+    // slot per layer above the first (slots: layer 0, then worker l at 2l-1
+    // and layer l at 2l), or, when that grid does not fit, with each layer
+    // forming its own input product (slot l).
+    auto stacked = [&](bool workers) -> bool {
         PFwdArgs pa;
         common_args(pa);
-        pa.nslots = L;
+        pa.nslots = workers ? 2 * L - 1 : L;
         pa.kin_max = P.kin(1);
         pa.KP = fwd_hp(pa.kin_max);
         for (int l = 0; l < L; ++l) {
-            PFwdDir& pd = pa.d[l];
+            const int sl = workers && l > 0 ? 2 * l : l;
+            PFwdDir& pd = pa.d[sl];
             fill_slot(pd, l, 0);
             pd.hx = W + P.w_hx + (size_t)l * 2 * P.hxs * es;
             if (l > 0) {
-                pd.Win = w->W[l];
-                pd.bias = w->b[l];
-                pd.nr = site_view(P, mbuf, P.site_nr(l));
-                pd.xin = W + P.w_xx + (size_t)(l - 1) * T * P.xxs * es;
-                pd.kin = P.kin(l);
-                pd.below = l - 1;
+                PFwdDir& xs = workers ? pa.d[sl - 1] : pd;      // the slot forming the input product
+                if (workers) {
+                    fill_slot(xs, l, 0);
+                    xs.role = 1;
+                    xs.gxo = (float*)(W + P.w_gxs) + (size_t)(l - 1) * T * B * G;
+                    pd.gx = xs.gxo;
+                    pd.dep = sl - 1;
+                }
+                xs.dep = workers ? sl - 2 : l - 1;              // the layer below
+                xs.Win = w->W[l];
+                xs.bias = w->b[l];
+                xs.nr = site_view(P, mbuf, P.site_nr(l));
+                xs.xin = W + P.w_xx + (size_t)(l - 1) * T * P.xxs * es;
+                xs.kin = P.kin(l);
             }
             if (l < L - 1) {
                 pd.xout = W + P.w_xx + (size_t)l * T * P.xxs * es;
@@ -315,9 +335,15 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
         }
         hipEvent_t e0 = nullptr, e1 = nullptr;
         const bool timed = timer_pair(KID_FWDP_, &e0, &e1);
-        if (launch_fwd_persist<E>(pa, st, timed, e0, e1) == hipSuccess) return hip_check("forward launch");
-        (void)hipGetLastError();              // does not fit: one layer at a time below
+        if (launch_fwd_persist<E>(pa, st, timed, e0, e1) == hipSuccess) return true;
+        (void)hipGetLastError();              // does not fit
         if (timed) timer_unpair();
+        return false;
+    };
+    if (use_persistent() && use_stacked() && D == 1 && L > 1 && L <= 4) {
+        launch_fx_layer(0);
+        if ((use_fwd_workers() && stacked(true)) || stacked(false)) return hip_check("forward launch");
+        // neither fits: one layer at a time below (layer 0's input product is done)
     }
     for (int l = 0; l < L; ++l) {
         const int kin = P.kin(l);

@@ -174,18 +174,21 @@ struct PFwdDir {
     void* ybuf;                         // inner layer: ybuf + d*H, or null
     void* ybufT;                        // inner layer: ybufT + d*H*BP (t stride ldy*BP), or null
     int dir;                            // 0: t = 0 .. T-1;  1: t = T-1 .. 0
-    // Input product inside the launch (a layer above the first of a
-    // unidirectional stack whose layers run in one launch): the gates get
-    // s_nr * x~_t W over the kept inputs plus the bias, where x_t is the
-    // output of the layer below, published by that layer's slot at step t.
-    const void* Win;                    // [kin][4H], or null (then gx holds input product and bias)
-    const float* bias;                  // [4H] (with Win)
-    SiteView nr;                        // NR site of this layer (keep lists of its input)
-    const void* xin;                    // [T] slots, fragment-major, compacted by nr (with Win)
-    int kin;                            // input width (with Win)
-    int below;                          // slot whose step t must be complete before this slot's step t, or -1
-    void* xout;                         // [T] slots of this layer's output for the layer above, or null
-    SiteView nr_up;                     // NR site of the layer above (compaction of xout)
+    // A unidirectional stack whose layers run in one launch: each layer above
+    // the first has an input-product worker slot, which forms
+    // gx_t = s_nr * x~_t W + b (Eq. 1-4, input part) from x_t, the output of
+    // the layer below that its slot publishes at step t; the layer reads gx
+    // from the worker's output once the worker's counter covers step t.
+    int role;                           // 0: a layer; 1: an input-product worker
+    int dep;                            // worker: slot of the layer below; layer: slot of its worker; or -1
+    const void* Win;                    // worker: [kin][4H]
+    const float* bias;                  // worker: [4H]
+    SiteView nr;                        // worker: NR site of the layer (keep lists of its input)
+    const void* xin;                    // worker: [T] slots, fragment-major, compacted by nr
+    int kin;                            // worker: input width
+    float* gxo;                         // worker: [T][B][4H] output (the layer's gx)
+    void* xout;                         // layer: [T] slots of its output for the layer above, or null
+    SiteView nr_up;                     // layer: NR site of the layer above (compaction of xout)
 };
 // LDS row pitch of a transposed weight slice over K neurons: K rounded up to
 // 32 (whole contraction chunks), plus 8 elements (16-byte rows that start on
@@ -193,13 +196,14 @@ struct PFwdDir {
 __host__ __device__ inline int fwd_hp(int K) { return (K + 31) / 32 * 32 + 8; }
 
 struct PFwdArgs {
-    PFwdDir d[4];                       // slots: the directions of one layer, or the layers of a stack
+    PFwdDir d[8];                       // slots: the directions of one layer, or the layers of a stack and their workers
     const int32_t* lengths;
-    unsigned* bar;                      // [nslots] barrier counters (zeroed before launch)
+    unsigned* bar;                      // barrier counters, slot i at bar + 64 i (zeroed before launch)
     int* err;                           // barrier time-out flag
     long long timeout;                  // wall-clock ticks
     int B, H, HP, T, BP, ldy, dense, ntiles, mgroups, mtiles;
     int nslots, KP, kin_max;            // KP: LDS pitch of the W slices (0: no slot has Win)
+    size_t wofs, kofs;                  // LDS offsets of the W slice and the keep lists (set by the launcher)
     size_t xxs;                         // elements per xin/xout slot
     float s, s_nr;
 };

@@ -34,6 +34,11 @@ namespace lsd {
 // reaches the target.  The spin is bounded by wall-clock time; on time-out,
 // or when another workgroup has timed out, it reports failure and the kernel
 // ends (outputs are then poisoned with NaN).
+// The barrier counter of slot i sits at bar + BAR_PITCH * i: each counter
+// has a cache line of its own (workgroups of one slot poll the counter of
+// another while its own workgroups add to theirs).
+constexpr int BAR_PITCH = 64;
+
 __device__ __forceinline__ void grid_arrive(unsigned* bar) {
     __builtin_amdgcn_s_waitcnt(0);      // this thread's stores have completed
     __syncthreads();
@@ -136,21 +141,22 @@ __device__ __forceinline__ void lds8(const float* p, float* o) {
 // ---------------------------------------------------------------------------
 // Persistent forward recurrence (Eq. 1-6).  A launch runs every step of its
 // slots: the two directions of one layer, or every layer of a
-// unidirectional stack (layer l then works on step t while layer l-1 works on
-// step t+1; each layer computes its own input product from the output the
-// layer below published, so no separate input-product pass is needed above
-// the first layer).
+// unidirectional stack together with one input-product worker per layer
+// above the first.  The worker of layer l forms gx_t = s_nr * x~_t W + b
+// (Eq. 1-4, input part) as soon as layer l-1 has published x_t, and layer l
+// reads it like the first layer reads the input product of the separate
+// pass; so the recurrence of every layer only waits for its own barrier.
 // Workgroup w -> (slot, unit tile, row group).  A unit tile is 4*NT hidden
 // units = NT 16-column MFMA tiles (the four gates of 4 units each); a row
 // group is MG batch rows.  512 threads = 8 waves; each contraction over kept
 // neurons is split over the waves (each wave issues all of its exchange
 // loads before its first MFMA) and reduced in LDS.
-// Dynamic LDS: U slice transposed [16*NT][HP] (dtype; HP = H rounded up to
-// 32, plus 8, zero past H), the W slice likewise [16*NT][KP] when a slot
-// computes its input product, keep lists [H+32] and [kin_max+32] (int16),
-// reduction [8][MG][16*NT] (float).  With every neuron of a contraction kept
-// (its keep list is the identity) a B fragment is one 16-byte LDS read per
-// column tile; otherwise its 8 rows are gathered through the keep list.
+// Dynamic LDS: the weight slice transposed, U [16*NT][HP] for a layer, W
+// [16*NT][KP] for a worker (dtype; pitch = rows rounded up to 32, plus 8,
+// zero past the end), keep lists [H+32] and [kin_max+32] (int16), reduction
+// [8][MG][16*NT] (float).  With every neuron of a contraction kept (its keep
+// list is the identity) a B fragment is one 16-byte LDS read per column
+// tile; otherwise its 8 rows are gathered through the keep list.
 constexpr int PF_NW = 8;
 
 template <typename T, int NT, int MG>
@@ -162,9 +168,9 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
     extern __shared__ __align__(16) char smem[];
     const int H = a.H, G = 4 * H, B = a.B, T_ = a.T;
     const int HP = fwd_hp(H), KP = a.KP;
-    T* Ut = (T*)smem;
-    T* Wt = (T*)(smem + (((size_t)NC * HP * sizeof(T) + 15) & ~(size_t)15));
-    int16_t* kidx = (int16_t*)((char*)Wt + (((size_t)NC * KP * sizeof(T) + 15) & ~(size_t)15));
+    T* Ut = (T*)smem;                             // a layer's U slice
+    T* Wt = (T*)(smem + a.wofs);                  // the W slice (a worker's: in place of U)
+    int16_t* kidx = (int16_t*)(smem + a.kofs);
     int16_t* kidx_x = kidx + (((H + 32) + 7) & ~7);
     float* red = (float*)((char*)kidx_x + (KP ? (((size_t)(a.kin_max + 32) * 2 + 15) & ~(size_t)15) : 0));
 
@@ -175,18 +181,24 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
     const int u0 = tile * UPW, m0 = mg * MG;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int g8 = 8 * (lane >> 4);
-    unsigned* bar = a.bar + d;
-    unsigned* bar_below = D.below >= 0 ? a.bar + D.below : nullptr;
-    __shared__ unsigned below_seen;               // last value of the layer below's counter read
-    unsigned seen_below = 0;                      // its copy in every thread
-    const bool has_x = D.Win != nullptr;
+    unsigned* bar = a.bar + BAR_PITCH * d;
+    // the slot this one depends on: a slot forming an input product, the
+    // layer below (step s needs its counter at (s+2)*nslot: it also arrives
+    // once before its first step); a layer fed by a worker, that worker
+    // ((s+1)*nslot)
+    unsigned* bar_dep = D.dep >= 0 ? a.bar + BAR_PITCH * D.dep : nullptr;
+    __shared__ unsigned dep_seen;                 // last value of that counter read
+    unsigned seen_dep = 0;                        // its copy in every thread
+    const bool worker = D.role == 1;
+    const bool has_x = D.Win != nullptr;          // forms an input product (a worker, or a layer itself)
+    const bool fed = !has_x && D.dep >= 0;        // a layer reading its worker's input product
     const int kin = D.kin;
 
-    // U slice (and W slice) -> LDS, transposed: row c = nt*16 + g*4 + cu holds
+    // U slice (or W slice) -> LDS, transposed: row c = nt*16 + g*4 + cu holds
     // column g*H + u0 + 4nt + cu of the weight
     {
         const T* U = (const T*)D.U;
-        for (int i = tid; i < HP * NC; i += NTH) {
+        for (int i = tid; i < HP * NC && !worker; i += NTH) {
             const int k = i / NC, c = i % NC;
             const int nt = c >> 4, cc = c & 15;
             const int u = u0 + 4 * nt + (cc & 3);
@@ -211,7 +223,7 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
         const int rr = p / UPW, uu = p % UPW;
         pb[q] = (p < MG * UPW) ? m0 + rr : B;
         pu[q] = u0 + uu;
-        const bool ok = pb[q] < B && pu[q] < H;
+        const bool ok = pb[q] < B && pu[q] < H && !worker;
         creg[q] = ok ? D.c0[(size_t)pb[q] * H + pu[q]] : 0.f;
         hreg[q] = ok ? to_f32<T>(((const T*)D.h0)[(size_t)pb[q] * H + pu[q]]) : 0.f;
 #pragma unroll
@@ -226,6 +238,14 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
     constexpr int KPT = (LSTM_SD_MAX_K + NTH - 1) / NTH;   // keep-list entries per thread
     int kreg[KPT], kreg_x[KPT];
     auto step_t = [&](int s) { return D.dir == 0 ? s : T_ - 1 - s; };
+    auto load_gx = [&](int t) {                   // input product and bias of step t
+#pragma unroll
+        for (int q = 0; q < PPT; ++q) {
+            const int bc = min(pb[q], B - 1), uc = min(pu[q], H - 1);
+#pragma unroll
+            for (int g = 0; g < 4; ++g) gxr[q][g] = D.gx[((size_t)t * B + bc) * G + g * H + uc];
+        }
+    };
     auto prefetch = [&](int s) {                  // s may be T_ (after the last step): clamped
         const int sc = min(s, T_ - 1);
         const int t = step_t(sc);
@@ -241,13 +261,10 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
 #pragma unroll
             for (int i = 0; i < KPT; ++i) kreg_x[i] = kx[min(tid + NTH * i, D.nr.kmax - 1)];
         }
+        if (!has_x && !fed) load_gx(t);           // (a fed layer loads it once its worker has published it)
 #pragma unroll
         for (int q = 0; q < PPT; ++q) {
             const int bc = min(pb[q], B - 1), uc = min(pu[q], H - 1);
-            if (!has_x) {
-#pragma unroll
-                for (int g = 0; g < 4; ++g) gxr[q][g] = D.gx[((size_t)t * B + bc) * G + g * H + uc];
-            }
             pn[q] = has_next ? D.rh.pos[(size_t)tn * D.rh.kmax + uc] : -1;
             mnr[q] = D.rh.mask[(size_t)tn * D.rh.kmax + uc];
             lenr[q] = a.lengths ? a.lengths[bc] : T_;
@@ -267,13 +284,13 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
             const int j = tid + NTH * i;
             if (j < cnt) kidx[j] = (int16_t)kreg[i];
         }
-        if (has_x) {
-            cnt_x = cnt_x_next;
+    };
+    auto commit_kidx_x = [&]() {
+        cnt_x = cnt_x_next;
 #pragma unroll
-            for (int i = 0; i < KPT; ++i) {
-                const int j = tid + NTH * i;
-                if (j < cnt_x) kidx_x[j] = (int16_t)kreg_x[i];
-            }
+        for (int i = 0; i < KPT; ++i) {
+            const int j = tid + NTH * i;
+            if (j < cnt_x) kidx_x[j] = (int16_t)kreg_x[i];
         }
     };
 
@@ -392,6 +409,74 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
         }
     };
 
+    // Input product of step s (a worker, or a layer that forms its own at
+    // the end of the step before, off its recurrence's path): x_t, which the
+    // layer below published, times the W-slice rows of the step's keep list,
+    // into accx.  The wait skip uses a register copy of the counter taken
+    // after the wait's barrier: every thread takes the same branch.  Returns
+    // false when a barrier wait failed.
+    f32x4_t accx[MT][NT];
+    auto x_product = [&](int s) -> bool {
+        commit_kidx_x();
+        if (seen_dep < (unsigned)(s + 2) * (unsigned)nslot) {
+            if (!grid_wait(bar_dep, (unsigned)(s + 2) * (unsigned)nslot, a.err, a.timeout, &dep_seen)) return false;
+            seen_dep = dep_seen;
+        } else {
+            __syncthreads();                    // the keep list just committed
+        }
+#pragma unroll
+        for (int i = 0; i < MT; ++i)
+#pragma unroll
+            for (int j = 0; j < NT; ++j) accx[i][j] = f32x4_t{0, 0, 0, 0};
+        contract((const T*)D.xin + (size_t)step_t(s) * a.xxs, a.xxs, cnt_x, kidx_x, Wt, KP, kin, accx);
+        return true;
+    };
+    // this thread's sums over the waves' partial products (in red) of the
+    // four gates of pair q
+    auto red_sum = [&](int q, float* pre) {
+        const int rr = pb[q] - m0, uu = pu[q] - u0, nt = uu >> 2, cu = uu & 3;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const int cc = nt * 16 + g * 4 + cu;
+            float v = 0.f;
+#pragma unroll
+            for (int i = 0; i < NW; ++i) v += red[(i * MG + rr) * NC + cc];
+            pre[g] = v;
+        }
+    };
+    auto red_store = [&](f32x4_t (&acc)[MT][NT]) {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    red[(w * MG + mt * 16 + acc_row(lane, r)) * NC + nt * 16 + (lane & 15)] = acc[mt][nt][r];
+        __syncthreads();
+    };
+
+    if (worker) {
+        // gx_t = s_nr * x~_t W + b for every step, published as soon as x_t is
+        prefetch(0);
+        for (int s = 0; s < T_; ++s) {
+            const int t = step_t(s);
+            if (!x_product(s)) break;
+            red_store(accx);
+#pragma unroll
+            for (int q = 0; q < PPT; ++q) {
+                const int b = pb[q], u = pu[q];
+                if (b >= B || u >= H) continue;
+                float pre[4];
+                red_sum(q, pre);
+#pragma unroll
+                for (int g = 0; g < 4; ++g) xstore(D.gxo + ((size_t)t * B + b) * G + g * H + u, a.s_nr * pre[g] + biasr[q][g]);
+            }
+            prefetch(s + 1);
+            grid_arrive(bar);                   // (also: every wave is past its reads of red)
+        }
+        return;
+    }
+
     // prologue: h0 compacted by the keep list of the first step
     const int tfirst = step_t(0);
     {
@@ -412,61 +497,50 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
     grid_arrive(bar);
 
     const size_t hxs = (size_t)((H + 31) / 32) * a.mtiles * 512;     // elements per h slot
-    for (int s = 0; s < T_; ++s) {
+    const bool x_ok = !has_x || x_product(0);
+    for (int s = 0; s < T_ && x_ok; ++s) {
         const int t = step_t(s);
-        // ---- wait for h_{t-1} of every workgroup of this slot (and for the
-        // layer below to have published x_t)
+        // ---- the input product of t (a layer with a worker: once published;
+        // the loads overlap the wait below), then h_{t-1} of every workgroup
+        // of this slot
+        if (fed) {
+            if (seen_dep < (unsigned)(s + 1) * (unsigned)nslot) {
+                if (!grid_wait(bar_dep, (unsigned)(s + 1) * (unsigned)nslot, a.err, a.timeout, &dep_seen)) break;
+                seen_dep = dep_seen;
+            }
+            load_gx(t);
+        }
         commit_kidx();
-        // when each contraction takes one round, the B fragments of the
-        // recurrent product (U rows through this step's keep list) are read
-        // from LDS before the waits
-        const bool one_round = cnt <= 32 * NW * MAXC && (!has_x || cnt_x <= 32 * NW * MAXC);
+        // when the contraction takes one round, its B fragments (U rows
+        // through this step's keep list) are read from LDS before the wait
+        const bool one_round = cnt <= 32 * NW * MAXC;
         Raw8<T> bh[MAXC][NT];
         if (one_round) {
-            __syncthreads();                    // the keep lists just committed
+            __syncthreads();                    // the keep list just committed
             gather_b(0, cnt, kidx, Ut, HP, H, bh);
         }
-        // x_t of the layer below (which runs ahead: a counter value seen
-        // earlier usually covers this step), then h_{t-1} of this slot
-        // (the skip decision uses a register copy taken after the wait's
-        // barrier: every thread must take the same branch around the waits)
-        if (has_x && seen_below < (unsigned)(s + 2) * (unsigned)nslot) {
-            if (!grid_wait(bar_below, (unsigned)(s + 2) * (unsigned)nslot, a.err, a.timeout, &below_seen)) break;
-            seen_below = below_seen;
-        }
         if (!grid_wait(bar, (unsigned)(s + 1) * (unsigned)nslot, a.err, a.timeout)) break;
-        f32x4_t acc[MT][NT], accx[MT][NT];
+        f32x4_t acc[MT][NT];
 #pragma unroll
         for (int i = 0; i < MT; ++i)
 #pragma unroll
-            for (int j = 0; j < NT; ++j) acc[i][j] = accx[i][j] = f32x4_t{0, 0, 0, 0};
+            for (int j = 0; j < NT; ++j) acc[i][j] = f32x4_t{0, 0, 0, 0};
         const T* hsrc = (const T*)D.hx + (size_t)(s & 1) * hxs;
-        const T* xsrc = has_x ? (const T*)D.xin + (size_t)t * a.xxs : nullptr;
         if (one_round) {
-            // one round each: both sets of exchange loads go out together
-            Raw8<T> fh[MAXC][MT], fx[MAXC][MT];
+            Raw8<T> fh[MAXC][MT];
             issue(hsrc, hxs, 0, fh);
-            if (has_x) issue(xsrc, a.xxs, 0, fx);
             compute_b(fh, bh, 0, cnt, acc);
-            if (has_x) compute(fx, 0, cnt_x, kidx_x, Wt, KP, kin, accx);
         } else {
             contract(hsrc, hxs, cnt, kidx, Ut, HP, H, acc);
-            if (has_x) contract(xsrc, a.xxs, cnt_x, kidx_x, Wt, KP, kin, accx);
         }
 #pragma unroll
         for (int i = 0; i < MT; ++i)
 #pragma unroll
             for (int j = 0; j < NT; ++j)
 #pragma unroll
-                for (int r = 0; r < 4; ++r) acc[i][j][r] = a.s * acc[i][j][r] + a.s_nr * accx[i][j][r];
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
                 for (int r = 0; r < 4; ++r)
-                    red[(w * MG + mt * 16 + acc_row(lane, r)) * NC + nt * 16 + (lane & 15)] = acc[mt][nt][r];
-        __syncthreads();
+                    acc[i][j][r] = has_x ? a.s * acc[i][j][r] + a.s_nr * accx[i][j][r] : a.s * acc[i][j][r];
+        red_store(acc);
         // ---- pointwise (Eq. 1-6); h_t (and the layer above's x_t) is published first
         T* hxn = (T*)D.hx + (size_t)((s + 1) & 1) * hxs;
         float og4[PPT][4], cnv[PPT], hnv[PPT];
@@ -474,16 +548,10 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
         for (int q = 0; q < PPT; ++q) {
             const int b = pb[q], u = pu[q];
             if (b >= B || u >= H) continue;
-            const int rr = b - m0, uu = u - u0, nt = uu >> 2, cu = uu & 3;
             float pre[4];
+            red_sum(q, pre);
 #pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                const int cc = nt * 16 + g * 4 + cu;
-                float v = 0.f;
-#pragma unroll
-                for (int i = 0; i < NW; ++i) v += red[(i * MG + rr) * NC + cc];
-                pre[g] = v + (has_x ? biasr[q][g] : gxr[q][g]);
-            }
+            for (int g = 0; g < 4; ++g) pre[g] += has_x ? biasr[q][g] : gxr[q][g];
             og4[q][0] = sigmoid_fast(pre[0]);
             og4[q][1] = sigmoid_fast(pre[1]);
             og4[q][2] = tanh_fast(pre[2]);
@@ -522,6 +590,7 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
             }
         }
         prefetch(s + 1);
+        if (has_x && s + 1 < T_ && !x_product(s + 1)) break;
     }
     // ---- final state (NaN if the barrier timed out)
     const bool failed = __hip_atomic_load(a.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0;
@@ -568,7 +637,7 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
     const int u0 = tile * UB, m0 = mg * MG;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int g8 = 8 * (lane >> 4);
-    unsigned* bar = a.bar + d;
+    unsigned* bar = a.bar + BAR_PITCH * d;
     const bool worker = D.role == 1;
 
     // rows of U (a worker: of the input weights of the layer above) for the
@@ -689,7 +758,7 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
         // dx_t of the layer above restricted to this tile's inputs, for every
         // t in that layer's order, as soon as its DA_t is published
         const PBwdDir& S = a.d[D.src];
-        unsigned* bar_src = a.bar + D.src;
+        unsigned* bar_src = a.bar + BAR_PITCH * D.src;
         for (int s = 0; s < T_; ++s) {
             const int t = step_t(s);
             int mk[PPT];
@@ -710,7 +779,7 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
         return;
     }
 
-    unsigned* bar_above = D.above >= 0 ? a.bar + D.above : nullptr;
+    unsigned* bar_above = D.above >= 0 ? a.bar + BAR_PITCH * D.above : nullptr;
     __shared__ unsigned above_seen;               // last value of the worker's counter read
     unsigned seen_above = 0;                      // its copy in every thread (uniform waits)
     // wait until the worker has formed dx of step s (usually already seen)
@@ -778,14 +847,29 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
         if (final_pass) break;
         grid_arrive(bar);                                  // DA_t is published
         // the outputs only later kernels read, and the next step's inputs,
-        // go out while the other workgroups finish the step
+        // go out while the other workgroups finish the step.  DA^T (for the
+        // weight gradients) is staged in LDS as the tile's [4*UB][MG] block
+        // (the reduction area is free until the next step's product; rows
+        // past B hold zeros) and written as whole 16-byte pieces of its rows.
+        {
+            T* st = (T*)red;
 #pragma unroll
-        for (int q = 0; q < PPT; ++q) {
-            const int b = pb[q], u = pu[q];
-            if (b >= B || u >= H) continue;
+            for (int q = 0; q < PPT; ++q) {
+                const int p = tid + NTH * q;
+                if (p >= MG * UB) continue;
+                const bool ok = pb[q] < B && pu[q] < H;
+#pragma unroll
+                for (int g = 0; g < 4; ++g) st[(g * UB + p % UB) * MG + p / UB] = from_f32<T>(ok ? da4[q][g] : 0.f);
+            }
+            __syncthreads();
+            constexpr int PPR = MG * (int)sizeof(T) / 16;  // 16-byte pieces of a staged row
             T* dat = (T*)D.daT + (size_t)t * G * a.BP;
-#pragma unroll
-            for (int g = 0; g < 4; ++g) dat[(size_t)(g * H + u) * a.BP + b] = from_f32<T>(da4[q][g]);
+            for (int i = tid; i < 4 * UB * PPR; i += NTH) {
+                const int r = i / PPR, pc = i % PPR;
+                const int u = u0 + r % UB, col = m0 + pc * (16 / (int)sizeof(T));
+                if (u < H && col < a.BP)
+                    *(uint4*)(dat + (size_t)((r / UB) * H + u) * a.BP + col) = *(const uint4*)(st + r * MG + pc * (16 / (int)sizeof(T)));
+            }
         }
         prefetch(s + 1);
     }
@@ -801,7 +885,7 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
 }
 
 __global__ void k_zero_sync(unsigned* bar, int n, int* err) {
-    for (int i = threadIdx.x; i < n; i += blockDim.x) bar[i] = 0u;
+    for (int i = threadIdx.x; i < n; i += blockDim.x) bar[BAR_PITCH * i] = 0u;
     if (threadIdx.x == 0) *err = 0;
 }
 
@@ -843,48 +927,48 @@ static bool cooperative_api() {
     const char* v = getenv("LSTM_SD_COOP");
     return v && v[0] == '1';
 }
-size_t fwd_persist_lds(int H, int NT, int MG, int esize, int KP, int kin_max) {
+// LDS layout: U slice at 0; the W slice at wofs (in place of U when only
+// workers hold W slices, after U when layers form their own input
+// products); keep lists at kofs; then the reduction area.  Returns the size.
+size_t fwd_persist_lds(int H, int NT, int MG, int esize, int KP, int kin_max, bool w_beside_u, size_t* wofs,
+                       size_t* kofs) {
     const size_t us = ((size_t)16 * NT * fwd_hp(H) * esize + 15) & ~(size_t)15;
     const size_t ws = ((size_t)16 * NT * KP * esize + 15) & ~(size_t)15;
+    *wofs = w_beside_u ? us : 0;
+    *kofs = w_beside_u ? us + ws : (us > ws ? us : ws);
     const size_t kx = (size_t)(((H + 32) + 7) & ~7) * 2;
     const size_t kxx = KP ? (((size_t)(kin_max + 32) * 2 + 15) & ~(size_t)15) : 0;
-    return us + ws + kx + kxx + (size_t)PF_NW * MG * 16 * NT * 4;
+    return *kofs + kx + kxx + (size_t)PF_NW * MG * 16 * NT * 4;
 }
 
-template <typename T, int NT, int MG>
-static hipError_t launch_fwd_persist_t(const PFwdArgs& a, int nwg, size_t lds, hipStream_t st) {
-    auto fn = k_fwd_persist<T, NT, MG>;
-    const hipError_t e = resident_limit((const void*)fn, 64 * PF_NW, lds, nwg);
-    if (e != hipSuccess) return e;
-    if (!cooperative_api()) {
-        hipLaunchKernelGGL(fn, dim3(nwg), dim3(64 * PF_NW), lds, st, a);
-        return hipGetLastError();
-    }
-    PFwdArgs arg = a;
-    void* params[] = {&arg};
-    return hipLaunchCooperativeKernel((const void*)fn, dim3(nwg), dim3(64 * PF_NW), params, (unsigned)lds, st);
-}
-
-// Launches the persistent forward layer if it fits; returns hipSuccess or an
-// error (then nothing was launched and the caller uses the per-step kernels).
+// Launches the persistent forward if its grid fits the device at once;
+// returns hipSuccess, or an error before anything was enqueued (the caller
+// then takes another layout or the per-step kernels).
 template <typename T>
 hipError_t launch_fwd_persist(PFwdArgs& a, hipStream_t st, int kid_timer_on, hipEvent_t e0, hipEvent_t e1) {
-    int NT, MG;
-    MG = a.B <= 32 ? 32 : 64;
-    NT = a.H >= 512 ? 2 : 1;            // fewer, wider unit tiles: a cheaper barrier
-    const int upw = 4 * NT;
-    a.ntiles = (a.H + upw - 1) / upw;
+    const int MG = a.B <= 32 ? 32 : 64;
+    const int NT = a.H >= 512 ? 2 : 1;  // fewer, wider unit tiles: a cheaper barrier
+    a.ntiles = (a.H + 4 * NT - 1) / (4 * NT);
     a.mgroups = (a.B + MG - 1) / MG;
     const int nwg = a.nslots * a.ntiles * a.mgroups;
-    const size_t lds = fwd_persist_lds(a.H, NT, MG, (int)sizeof(T), a.KP, a.kin_max);
-    if (lds > 160 * 1024 || a.nslots > 4) return hipErrorInvalidValue;
+    bool w_beside_u = false;            // a layer slot forming its own input product holds U and W
+    for (int i = 0; i < a.nslots; ++i) w_beside_u = w_beside_u || (a.d[i].role == 0 && a.d[i].Win);
+    const size_t lds = fwd_persist_lds(a.H, NT, MG, (int)sizeof(T), a.KP, a.kin_max, w_beside_u, &a.wofs, &a.kofs);
+    if (lds > 160 * 1024 || a.nslots > 8) return hipErrorInvalidValue;
+    void (*fn)(PFwdArgs) = NT == 1 ? (MG == 32 ? k_fwd_persist<T, 1, 32> : k_fwd_persist<T, 1, 64>)
+                                   : (MG == 32 ? k_fwd_persist<T, 2, 32> : k_fwd_persist<T, 2, 64>);
+    hipError_t e = resident_limit((const void*)fn, 64 * PF_NW, lds, nwg);
+    if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_zero_sync, dim3(1), dim3(64), 0, st, a.bar, a.nslots, a.err);
     if (kid_timer_on) (void)hipEventRecord(e0, st);
-    hipError_t e;
-    if (NT == 1 && MG == 32) e = launch_fwd_persist_t<T, 1, 32>(a, nwg, lds, st);
-    else if (NT == 1) e = launch_fwd_persist_t<T, 1, 64>(a, nwg, lds, st);
-    else if (MG == 32) e = launch_fwd_persist_t<T, 2, 32>(a, nwg, lds, st);
-    else e = launch_fwd_persist_t<T, 2, 64>(a, nwg, lds, st);
+    if (!cooperative_api()) {
+        hipLaunchKernelGGL(fn, dim3(nwg), dim3(64 * PF_NW), lds, st, a);
+        e = hipGetLastError();
+    } else {
+        PFwdArgs arg = a;
+        void* params[] = {&arg};
+        e = hipLaunchCooperativeKernel((const void*)fn, dim3(nwg), dim3(64 * PF_NW), params, (unsigned)lds, st);
+    }
     if (kid_timer_on && e == hipSuccess) (void)hipEventRecord(e1, st);
     return e;
 }

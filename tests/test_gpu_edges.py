@@ -180,10 +180,11 @@ def test_persistent_and_per_step_paths_agree(name, mode, monkeypatch):
                                        ("seq2seq_enc", "nrrh")])
 def test_stacked_and_per_layer_agree(name, mode, monkeypatch):
     """A unidirectional stack run as one persistent launch per pass (forward:
-    each layer forms its input product from what the layer below published;
-    backward: a worker forms each layer's input gradient from the DA the layer
-    publishes) gives the same step as one launch per layer with the separate
-    input-product and input-gradient passes."""
+    an input-product worker per layer above the first forms its input product
+    from what the layer below published, or, without workers, each layer
+    forms its own; backward: a worker forms each layer's input gradient from
+    the DA the layer publishes) gives the same step as one launch per layer
+    with the separate input-product and input-gradient passes."""
     from paper_2106_12089_amd import binding as B_
     from paper_2106_12089_amd.session import Session
     from tests._parity import mode_rates
@@ -193,8 +194,9 @@ def test_stacked_and_per_layer_agree(name, mode, monkeypatch):
     p_nr, p_rh, compact = mode_rates(cfg, mode, p)
     say(f"[gpu] stacked vs per-layer {name} {mode}")
     outs = []
-    for flag in ("1", "0"):
+    for flag, workers in (("1", "1"), ("1", "0"), ("0", "1")):
         monkeypatch.setenv("LSTM_SD_STACK", flag)
+        monkeypatch.setenv("LSTM_SD_FWD_WORKERS", workers)
         s = Session(wl, p_nr, p_rh, compact)
         s.masks(cfg.mask_seed, 4)
         B_.lstm_sd_kernel_timer_start("fwd_persist")
@@ -208,7 +210,8 @@ def test_stacked_and_per_layer_agree(name, mode, monkeypatch):
         assert n == fwd_persist_launches(cfg, stacked=flag == "1")
         torch.cuda.synchronize()
         outs.append(s.outputs())
-    errs = compare(outs[0], outs[1])
-    assert max(errs.values()) <= TOL[cfg.dtype], errs
-    for k in ("y", "hT", "cT", "dx", "dh0", "dc0"):
-        assert np.isfinite(outs[0][k]).all(), k
+    for o in outs[:2]:
+        errs = compare(o, outs[2])
+        assert max(errs.values()) <= TOL[cfg.dtype], errs
+        for k in ("y", "hT", "cT", "dx", "dh0", "dc0"):
+            assert np.isfinite(o[k]).all(), k
