@@ -260,7 +260,7 @@ def cpu_baseline(wl, p_nr, p_rh, budget_s=12.0):
 
 KERNEL_SYMBOLS = {"fwd_persist": "lsd::k_fwd_persist<", "step": "lsd::k_step<", "bwd_persist": "lsd::k_bwd_persist<",
                   "bwd": "lsd::k_bwd<",
-                  "wgrad": "lsd::k_wgrad<",
+                  "wgrad": "lsd::k_wgrad",            # the row-sparse and the full kernel
                   "fx": "lsd::k_fx<", "dx": "lsd::k_dx<"}
 
 
