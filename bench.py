@@ -72,14 +72,19 @@ def dense_counts(cfg):
     return [np.full(T, I if l == 0 else D * H) for l in range(L)] + [np.full(T, H)] * (L * D)
 
 
-def kernel_work(kind, counts, cfg):
+def kernel_work(kind, counts, cfg, stacked=False):
     """(flops, bytes, launches) of one step for a kernel class; bytes are the
     algorithmic minimum: every operand read once and every output written
-    once per launch (kept rows only)."""
+    once per launch (kept rows only).  stacked: the unidirectional stack ran
+    as one persistent launch per pass, whose slots also form the input
+    product of every layer above the first (forward) and the input gradient
+    of every layer below the top (backward); the separate passes then cover
+    layer 0 only."""
     L, D, H, T, B = cfg.num_layers, cfg.num_dirs, cfg.hidden, cfg.seq_len, cfg.batch
     G = 4 * H
     e = 2 if cfg.dtype == "bf16" else 4
     fl = by = 0.0
+    upper = range(1, L) if stacked else range(0)     # layers whose input product / gradient moved
     if kind == "step":                      # one launch per (layer, step), directions fused
         for l in range(L):
             for d in range(D):
@@ -97,7 +102,11 @@ def kernel_work(kind, counts, cfg):
                 by += H * G * e                                        # U slice, read once per launch
                 by += T * B * (G * 4 + G * 4 + H * 4 + 2 * H * e)      # gx, gates, c, h^T + exchange
                 by += T * B * H * (4 if l == L - 1 else 2 * e) + B * H * 16
-        return fl, by, L
+        for l in upper:                     # input product: W slice, x~ exchange, gx written and read
+            n = np.asarray(counts[l], dtype=np.float64)
+            fl += float(np.sum(2 * B * G * n))
+            by += cfg.k_in(l) * G * e + float(np.sum(B * n * e)) + T * B * G * 8
+        return fl, by, 1 if stacked else L
     if kind == "bwd_persist":               # one launch per layer runs every BPTT step (both directions)
         for l in range(L):
             for d in range(D):
@@ -107,7 +116,11 @@ def kernel_work(kind, counts, cfg):
                 by += T * B * G * e                                    # DA of each step, read once
                 by += T * B * H * (16 + 4 + 4 + 4 + 8 * e)             # gates, c, c_prev, dy; DA + DA^T
                 by += B * H * 16
-        return fl, by, L
+        for l in upper:                     # input gradient of layer l: W rows, kept columns written and read
+            n = np.asarray(counts[l], dtype=np.float64)
+            fl += float(np.sum(2 * B * G * n))
+            by += cfg.k_in(l) * G * e + float(np.sum(B * n * 8))
+        return fl, by, 1 if stacked else L
     if kind == "bwd":                       # T pointwise steps + one final pass per layer
         for l in range(L):
             for d in range(D):
@@ -126,20 +139,20 @@ def kernel_work(kind, counts, cfg):
                     by += float(np.sum(n * B * e + G * B * e)) + K * G * 4
         return fl, by, 2 * L * D
     if kind == "fx":
-        for l in range(L):
+        for l in range(1 if stacked else L):
             kin = cfg.input_dim if l == 0 else D * H
             n = np.asarray(counts[l], np.float64)
             for d in range(D):
                 fl += float(np.sum(2 * B * G * n))
                 by += kin * G * e + float(np.sum(B * n * e)) + T * B * G * 4
-        return fl, by, L * D
+        return fl, by, (1 if stacked else L) * D
     if kind == "dx":
-        for l in range(L):
+        for l in range(1 if stacked else L):
             kin = cfg.input_dim if l == 0 else D * H
             n = np.asarray(counts[l], np.float64)
             fl += float(np.sum(2 * B * G * n)) * D
             by += D * (kin * G * e + T * B * G * e) + float(np.sum(B * n * 4))
-        return fl, by, L
+        return fl, by, 1 if stacked else L
     raise ValueError(kind)
 
 
@@ -199,7 +212,9 @@ def run_mode(wl, p_nr, p_rh, compact, steps, warmup, timed_kernels=()):
 def roofline(res, cfg):
     kt = res["ktime"]
     name = max(kt, key=lambda k: kt[k]["total_ms"])
-    fl, by, nl = kernel_work(name, res["counts"], cfg)
+    # one persistent launch per pass: the stacked layout ran
+    stacked = cfg.num_layers > 1 and all(kt.get(k, {}).get("launches", 0) == 1 for k in ("fwd_persist", "bwd_persist"))
+    fl, by, nl = kernel_work(name, res["counts"], cfg, stacked)
     launches = kt[name]["launches"]
     fl_l, by_l = fl / launches, by / launches
     dur = kt[name]["avg_us"] * 1e-6
