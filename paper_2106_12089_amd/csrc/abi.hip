@@ -467,12 +467,11 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
         launch_dx<E>(a, kin, st);
         if (l == 0) launch_expand(dxc_here, kin, nv, dx, B, kin, T, st);
     };
-    // weight and bias gradients (Eq. 11) of layer l: its problems join the
-    // row-sparse or the full batch, one launch each
-    WgBatch wgb[2];                            // [0] row-sparse, [1] full
-    wgb[0].np = wgb[1].np = 0;
+    // weight and bias gradients (Eq. 11) of layer l: its problems join one
+    // batch (row-sparse and full problems alike), one launch per batch
+    WgBatch b;
+    b.np = 0;
     auto add_wgrad = [&](const WgArgs& a) {
-        WgBatch& b = wgb[a.full ? 1 : 0];
         if (b.np == WG_MAXP) {                 // full: launch it (its DA is complete)
             launch_wgrad<E>(b, st);
             b.np = 0;
@@ -511,10 +510,8 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
         }
     };
     auto flush_wgrad = [&]() {
-        for (WgBatch& b : wgb) {
-            launch_wgrad<E>(b, st);
-            b.np = 0;
-        }
+        launch_wgrad<E>(b, st);
+        b.np = 0;
     };
 
     // Unidirectional stack: every layer's BPTT in one persistent launch, with

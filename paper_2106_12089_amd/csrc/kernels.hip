@@ -641,12 +641,11 @@ struct WgTiles<float> { static constexpr int N = 4; };
 inline size_t wgrad_lds_bytes(int K) { return (size_t)((K + NXCD - 1) / NXCD + 1) * WG_LDC * sizeof(float); }
 
 template <typename T, bool DENSE, bool MULTI>
-__global__ void __launch_bounds__(128 * WG_NWV) k_wgrad(WgBatch bt) {
-    const WgArgs& a = bt.p[blockIdx.z];
+__device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
     constexpr int MAXT = WgTiles<T>::N / 2;     // 16-row tiles of a round (a wave takes half a slice)
     constexpr int NW = Raw8<T>::NW;
     constexpr uint32_t ES = sizeof(T);
-    extern __shared__ float acc_lds[];   // [rows of the slice + 1][WG_LDC]
+    // acc_lds: [rows of the slice + 1][WG_LDC]
     const int x = blockIdx.x % NXCD, cb = blockIdx.x / NXCD;
     if (cb * WG_NB >= a.G) return;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -851,15 +850,15 @@ __global__ void __launch_bounds__(128 * WG_NWV) k_wgrad(WgBatch bt) {
 // steps are in flight while a step is multiplied.  The bias gradient comes
 // from the workgroups of the last slice (never empty: it ends at K).
 template <typename T, bool MASKED, int NTL, bool MULTI>
-__global__ void __launch_bounds__(64 * WG_NWV) k_wgrad_full(WgBatch bt) {
-    const WgArgs& a = bt.p[blockIdx.z];
+__device__ __forceinline__ void wgrad_full(const WgArgs& a) {
     constexpr int NW = Raw8<T>::NW;
     constexpr uint32_t ES = sizeof(T);
     const int x = blockIdx.x % NXCD, cb = blockIdx.x / NXCD;
     if (cb * WG_NB >= a.G) return;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int col = lane & 15, g8 = 8 * (lane >> 4);
-    const int n = cb * WG_NB + 32 * w + col;   // columns n and n + 16
+    const int rh = w / WG_NWV;                 // which NTL tiles of a pass of 2*NTL this wave takes
+    const int n = cb * WG_NB + 32 * (w % WG_NWV) + col;   // columns n and n + 16
     const int r0 = slice_start(x, a.K), r1 = slice_start(x + 1, a.K);
     const int t0 = 0, t1 = a.T;
     uint32_t pm0[NW], pmb[2][NW];              // batch-pad masks (B side also zero past G)
@@ -880,8 +879,9 @@ __global__ void __launch_bounds__(64 * WG_NWV) k_wgrad_full(WgBatch bt) {
     };
     auto dat_rsrc = [&](int t) { return buf_rsrc((const T*)a.daT + (size_t)t * a.G * a.BP, bbytes); };
 
-    for (int rb = r0; rb < r1; rb += 16 * NTL) {           // passes over the slice's row tiles
-        const bool first = rb == r0;
+    for (int rp = r0; rp < r1; rp += 32 * NTL) {           // passes over the slice's row tiles
+        const bool first = rp == r0;
+        const int rb = rp + 16 * NTL * rh;     // this wave's first row of the pass
         int rowa[NTL];                         // A-fragment row of this lane in tile i (clamped into K)
 #pragma unroll
         for (int i = 0; i < NTL; ++i) rowa[i] = min(rb + 16 * i + col, a.K - 1);
@@ -972,7 +972,7 @@ __global__ void __launch_bounds__(64 * WG_NWV) k_wgrad_full(WgBatch bt) {
                     if (row < r1 && n + 16 * h < a.G) out[(size_t)row * a.G + n + 16 * h] = a.s * acc[i][h][r];
             }
     }
-    if (a.db && x == NXCD - 1) {               // (the last slice is never empty) lanes l, l+16, l+32, l+48 hold column l
+    if (a.db && x == NXCD - 1 && rh == 0) {    // (the last slice is never empty) lanes l, l+16, l+32, l+48 hold column l
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
             float v = dbacc[h];
@@ -981,6 +981,18 @@ __global__ void __launch_bounds__(64 * WG_NWV) k_wgrad_full(WgBatch bt) {
             if (lane < 16 && n + 16 * h < a.G) a.db[n + 16 * h] = v;
         }
     }
+}
+
+// One launch for every weight gradient of a pass (grid z = problem): a
+// problem whose keep lists are all the identity takes the full kernel, the
+// others the row-sparse one; either way every workgroup runs every step, so
+// the two kinds overlap instead of taking a launch each.
+template <typename T, bool MASKED, bool MULTI>
+__global__ void __launch_bounds__(128 * WG_NWV) k_wgrad(WgBatch bt) {
+    extern __shared__ float acc_lds[];
+    const WgArgs& a = bt.p[blockIdx.z];
+    if (a.full) wgrad_full<T, MASKED, WgTiles<T>::N / 2, MULTI>(a);
+    else wgrad_gather<T, false, MULTI>(a, acc_lds);
 }
 
 // ---------------------------------------------------------------------------
@@ -1198,29 +1210,22 @@ void launch_dx(const DxArgs& a, int K, hipStream_t st) {
 template <typename T>
 void launch_wgrad(const WgBatch& b, hipStream_t st) {
     if (b.np == 0) return;
-    const WgArgs& a = b.p[0];                  // the problems share G, B and the kind
+    const WgArgs& a = b.p[0];                  // the problems share G, B and the mode
     const dim3 grid(NXCD * ((a.G + WG_NB - 1) / WG_NB), 1, b.np);
     size_t lds = 0;
     bool multi = a.B > 32;                     // builds with the extra loops (batch chunks, tile rounds)
     for (int i = 0; i < b.np; ++i) {
+        if (b.p[i].full) continue;
         lds = std::max(lds, wgrad_lds_bytes(b.p[i].K));
         multi = multi || (b.p[i].K + NSEG - 1) / NSEG > 16 * (WgTiles<T>::N / 2);
     }
-    if (a.full) {
-        constexpr int NTL = sizeof(T) == 2 ? 6 : 4;
-        if (a.B > 32) {
-            if (a.dense) launch_k(KID_WGRAD, k_wgrad_full<T, true, NTL, true>, grid, dim3(64 * WG_NWV), 0, st, b);
-            else launch_k(KID_WGRAD, k_wgrad_full<T, false, NTL, true>, grid, dim3(64 * WG_NWV), 0, st, b);
-        } else {
-            if (a.dense) launch_k(KID_WGRAD, k_wgrad_full<T, true, NTL, false>, grid, dim3(64 * WG_NWV), 0, st, b);
-            else launch_k(KID_WGRAD, k_wgrad_full<T, false, NTL, false>, grid, dim3(64 * WG_NWV), 0, st, b);
-        }
-    } else if (a.dense) {
-        if (multi) launch_k(KID_WGRAD, k_wgrad<T, true, true>, grid, dim3(128 * WG_NWV), lds, st, b);
-        else launch_k(KID_WGRAD, k_wgrad<T, true, false>, grid, dim3(128 * WG_NWV), lds, st, b);
+    const dim3 blk(128 * WG_NWV);
+    if (a.dense) {
+        if (multi) launch_k(KID_WGRAD, k_wgrad<T, true, true>, grid, blk, lds, st, b);
+        else launch_k(KID_WGRAD, k_wgrad<T, true, false>, grid, blk, lds, st, b);
     } else {
-        if (multi) launch_k(KID_WGRAD, k_wgrad<T, false, true>, grid, dim3(128 * WG_NWV), lds, st, b);
-        else launch_k(KID_WGRAD, k_wgrad<T, false, false>, grid, dim3(128 * WG_NWV), lds, st, b);
+        if (multi) launch_k(KID_WGRAD, k_wgrad<T, false, true>, grid, blk, lds, st, b);
+        else launch_k(KID_WGRAD, k_wgrad<T, false, false>, grid, blk, lds, st, b);
     }
 }
 template <typename T>
