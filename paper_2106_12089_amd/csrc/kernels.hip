@@ -624,8 +624,10 @@ __device__ __forceinline__ void db_add_raw(const Raw8<T>& f, float& acc) {
 // return 0) into packed registers, only the padded batch entries are zeroed
 // (one AND per register), and the A rows of absent tile rows are not zeroed
 // at all: their products land in a spare LDS row, which is never read back.
-// Each wave loads the row indices and the DA^T fragment of t+1 while t is
-// multiplied.  The steps run in windows of 64, whose keep-list ranges sit in
+// The gather is a chain of two loads (keep-list entries, then the rows they
+// name), so each wave runs it ahead: while t is multiplied, the A rows and
+// DA^T fragments of t+1 are in flight, those of t+2 go out, and so do the
+// keep-list entries of t+4.  The steps run in windows of 64, whose keep-list ranges sit in
 // LDS.  All kept rows of a step are distinct, so the LDS sums read
 // every row of the step first and then write them.  Rows never kept stay
 // zero.  Every wave also sums its DA^T fragments: the bias gradient.
@@ -640,7 +642,7 @@ struct WgTiles<float> { static constexpr int N = 4; };
 // LDS bytes of the row-sparse weight gradient for a K-row weight
 inline size_t wgrad_lds_bytes(int K) { return (size_t)((K + NXCD - 1) / NXCD + 1) * WG_LDC * sizeof(float); }
 
-template <typename T, bool DENSE, bool MULTI>
+template <typename T, bool MULTI>
 __device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
     constexpr int MAXT = WgTiles<T>::N / 2;     // 16-row tiles of a round (a wave takes half a slice)
     constexpr int NW = Raw8<T>::NW;
@@ -648,7 +650,7 @@ __device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
     // acc_lds: [rows of the slice + 1][WG_LDC]
     const int x = blockIdx.x % NXCD, cb = blockIdx.x / NXCD;
     if (cb * WG_NB >= a.G) return;
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // (wave-uniform)
     const int col = lane & 15, g8 = 8 * (lane >> 4);
     const int rh = w / WG_NWV;                   // the half of the slice whose kept rows this wave takes
     const int c0 = 32 * (w % WG_NWV);            // this wave's columns within the block: two tiles
@@ -674,34 +676,31 @@ __device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
     }
     const uint32_t abytes = (uint32_t)a.K * a.BP * ES, bbytes = (uint32_t)a.G * a.BP * ES;
     const int spare = nrow * WG_LDC;
+    const bool dbw = a.db && x == 0 && rh == 0;  // this wave writes the bias gradient
 
-    // keep-list entries (and, dense mode, mask bytes) of the A-fragment rows
-    // of tiles jt0 .. jt0+MAXT-1 at t.  In dense mode the keep list is the
-    // identity, so mask[j] is the mask byte of row keep[j].
-    auto rows_issue = [&](int t, int jt0, int* kv, int* mv) {
+    // keep-list entries of the A-fragment rows of tiles jt0 .. jt0+MAXT-1 at t
+    auto rows_issue = [&](int t, int jt0, int* kv) {
         const int jb = seg_b(t), je = seg_e(t);
         const __amdgpu_buffer_rsrc_t kr = buf_rsrc(a.site.keep + (size_t)t * a.site.kmax, (uint32_t)a.site.kmax * 4);
-        const __amdgpu_buffer_rsrc_t mr = buf_rsrc(a.site.mask + (size_t)t * a.site.kmax, (uint32_t)a.site.kmax);
 #pragma unroll
         for (int i = 0; i < MAXT; ++i) {
             const int j = jb + (jt0 + i) * 16 + col;
             const int jc = j < je ? j : 0;
             kv[i] = (int)__builtin_amdgcn_raw_buffer_load_b32(kr, (uint32_t)jc * 4, 0, 0);
-            if (DENSE) mv[i] = (int)__builtin_amdgcn_raw_buffer_load_b8(mr, (uint32_t)jc, 0, 0);
         }
     };
     // row of each tile's A-fragment lane; absent rows read row 0 and add
     // into the spare row
-    auto rows_resolve = [&](int t, int jt0, const int* kv, const int* mv, int* kk, int* la) {
+    auto rows_resolve = [&](int t, int jt0, const int* kv, int* kk, int* la) {
         const int jb = seg_b(t), je = seg_e(t);
 #pragma unroll
         for (int i = 0; i < MAXT; ++i) {
             // bitwise selects: a branch here would let the compiler sink the
             // loads of kv into it
             const int j = jb + (jt0 + i) * 16 + col;
-            const int okm = -(int)(j < je && (!DENSE || mv[i]));
+            const int okm = -(int)(j < je);
             kk[i] = kv[i] & okm;
-            la[i] = (((kv[i] - r0) * WG_LDC) & okm) | (spare & ~okm);
+            la[i] = (__mul24(kv[i] - r0, WG_LDC) & okm) | (spare & ~okm);
         }
     };
     auto act_rsrc = [&](int t) {
@@ -712,13 +711,17 @@ __device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
     auto dat_rsrc = [&](int t) { return buf_rsrc((const T*)a.daT + (size_t)t * a.G * a.BP, bbytes); };
     auto a_issue = [&](__amdgpu_buffer_rsrc_t ar, int bc, const int* kk, Raw8<T>* fa) {
 #pragma unroll
-        for (int i = 0; i < MAXT; ++i) raw_load(fa[i], ar, (uint32_t)(kk[i] * a.BP + bc + g8) * ES);
+        for (int i = 0; i < MAXT; ++i) raw_load(fa[i], ar, (__umul24((uint32_t)kk[i], (uint32_t)a.BP) + bc + g8) * ES);
     };
     float dbacc[2] = {0.f, 0.f};
     // multiply the tiles (chunk-0 fragments already loaded) with both column
     // tiles, finish the other batch chunks, and add the tiles into their LDS
     // rows.  Tiles past nt are multiplied too (their rows are absent):
-    // unconditional products keep the loads out of branches.
+    // unconditional products keep the loads out of branches.  The products
+    // are taken transposed (DA^T fragment as the left operand): the output
+    // column of a lane is then its own A-fragment row, and its four values
+    // are four adjacent gradient columns, so each lane adds one 16-byte piece
+    // of its own row.
     auto finish = [&](__amdgpu_buffer_rsrc_t ar, __amdgpu_buffer_rsrc_t br, const int* kk, const int* la, int nt,
                       Raw8<T>* fa, const Raw8<T>* fb0, bool first_round) {
         f32x4_t acc[MAXT][2];
@@ -728,7 +731,7 @@ __device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
                 acc[i][h] = f32x4_t{0, 0, 0, 0};
-                raw_mma(fa[i], fb0[h], acc[i][h]);
+                raw_mma(fb0[h], fa[i], acc[i][h]);
             }
         }
         for (int bc = 32; MULTI && bc < a.B; bc += 32) {
@@ -747,33 +750,30 @@ __device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
 #pragma unroll
             for (int i = 0; i < MAXT; ++i) {
                 raw_and(fa[i], pm);
-                raw_mma(fa[i], fb[0], acc[i][0]);
-                raw_mma(fa[i], fb[1], acc[i][1]);
+                raw_mma(fb[0], fa[i], acc[i][0]);
+                raw_mma(fb[1], fa[i], acc[i][1]);
             }
         }
-        // output r of this lane is row 4*(lane/16)+r of the tile, whose LDS
-        // row address is held by that lane
-        int addr[MAXT][4];
-        float old[MAXT][4][2];
-#pragma unroll
-        for (int i = 0; i < MAXT; ++i)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) addr[i][r] = __shfl(la[i], acc_row(lane, r)) + c0 + col;
+        // output r of this lane is gradient column 4*(lane/16)+r of the
+        // column tile, in the lane's own row
+        const int cq = c0 + 4 * (lane >> 4);
+        float4 old[MAXT][2];
 #pragma unroll
         for (int i = 0; i < MAXT; ++i)
             if (i < nt)
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    old[i][r][0] = acc_lds[addr[i][r]];
-                    old[i][r][1] = acc_lds[addr[i][r] + 16];
-                }
+                for (int h = 0; h < 2; ++h) old[i][h] = *(const float4*)(acc_lds + la[i] + cq + 16 * h);
 #pragma unroll
         for (int i = 0; i < MAXT; ++i)
             if (i < nt)
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    acc_lds[addr[i][r]] = old[i][r][0] + a.s * acc[i][0][r];
-                    acc_lds[addr[i][r] + 16] = old[i][r][1] + a.s * acc[i][1][r];
+                for (int h = 0; h < 2; ++h) {
+                    float4 v = old[i][h];
+                    v.x += a.s * acc[i][h][0];
+                    v.y += a.s * acc[i][h][1];
+                    v.z += a.s * acc[i][h][2];
+                    v.w += a.s * acc[i][h][3];
+                    *(float4*)(acc_lds + la[i] + cq + 16 * h) = v;
                 }
     };
 
@@ -787,43 +787,57 @@ __device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
             segtab[2][threadIdx.x] = ks[2];
         }
         __syncthreads();
-        int kv[MAXT], mv[MAXT];
-        Raw8<T> fb[2];
-        rows_issue(t0, 0, kv, mv);
-        raw_load(fb[0], dat_rsrc(t0), boff[0]);
-        raw_load(fb[1], dat_rsrc(t0), boff[1]);
-        for (int t = t0; t < t1; ++t) {
-            const __amdgpu_buffer_rsrc_t ar = act_rsrc(t), br = dat_rsrc(t);
-            const int ntile = (seg_e(t) - seg_b(t) + 15) >> 4;
-            int kc[MAXT], la[MAXT];
-            rows_resolve(t, 0, kv, mv, kc, la);
-            Raw8<T> fb0[2] = {fb[0], fb[1]};
-            Raw8<T> fa[MAXT];
-            a_issue(ar, 0, kc, fa);
-            {   // next step's rows and fragments (the last step reloads its own:
-                // an unconditional issue keeps the wait counts exact)
-                const int tn = min(t + 1, t1 - 1);
-                rows_issue(tn, 0, kv, mv);
-                raw_load(fb[0], dat_rsrc(tn), boff[0]);
-                raw_load(fb[1], dat_rsrc(tn), boff[1]);
-            }
-            __builtin_amdgcn_sched_barrier(0);     // keep the uses below the prefetch
+        // ring slots by step parity: the A rows, DA^T fragments and LDS row
+        // addresses of steps t and t+1, the keep-list entries of t+2 and t+3
+        int kv[2][MAXT], kk[2][MAXT], la[2][MAXT];
+        Raw8<T> fa[2][MAXT], fb[2][2];
+        // the operands of step t into slot sl, from its keep-list entries
+        auto prime = [&](int t, int sl) {
+            rows_resolve(t, 0, kv[sl], kk[sl], la[sl]);
+            const __amdgpu_buffer_rsrc_t br = dat_rsrc(t);
+            a_issue(act_rsrc(t), 0, kk[sl], fa[sl]);
+            raw_load(fb[sl][0], br, boff[0]);
+            raw_load(fb[sl][1], br, boff[1]);
+        };
+        // step t from slot sl (none past the window); then the slot takes
+        // the operands of t+2 and the keep-list entries of t+4.  Loads that
+        // always go out (steps clamped into the window) and the same issue
+        // order in the prologue keep the wait counts exact.
+        auto step = [&](int t, int sl) {
+            if (t < t1) {
+                const __amdgpu_buffer_rsrc_t ar = act_rsrc(t), br = dat_rsrc(t);
+                const int ntile = (seg_e(t) - seg_b(t) + 15) >> 4;
+                Raw8<T> fb0[2] = {fb[sl][0], fb[sl][1]};
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                raw_and(fb0[h], pmb[h]);
-                db_add_raw(fb0[h], dbacc[h]);
+                for (int h = 0; h < 2; ++h) {
+                    raw_and(fb0[h], pmb[h]);
+                    if (dbw) db_add_raw(fb0[h], dbacc[h]);
+                }
+                finish(ar, br, kk[sl], la[sl], min(ntile, MAXT), fa[sl], fb0, dbw);
+                for (int jt0 = MAXT; MULTI && jt0 < ntile; jt0 += MAXT) {   // more kept rows than one round
+                    int kv2[MAXT], kc[MAXT], lc[MAXT];
+                    Raw8<T> fa2[MAXT];
+                    rows_issue(t, jt0, kv2);
+                    rows_resolve(t, jt0, kv2, kc, lc);
+                    a_issue(ar, 0, kc, fa2);
+                    finish(ar, br, kc, lc, min(ntile - jt0, MAXT), fa2, fb0, false);
+                }
             }
-            finish(ar, br, kc, la, min(ntile, MAXT), fa, fb0, true);
-            for (int jt0 = MAXT; MULTI && jt0 < ntile; jt0 += MAXT) {   // more kept rows than one round
-                int kv2[MAXT], mv2[MAXT];
-                rows_issue(t, jt0, kv2, mv2);
-                rows_resolve(t, jt0, kv2, mv2, kc, la);
-                a_issue(ar, 0, kc, fa);
-                finish(ar, br, kc, la, min(ntile - jt0, MAXT), fa, fb0, false);
-            }
+            prime(min(t + 2, t1 - 1), sl);
+            rows_issue(min(t + 4, t1 - 1), 0, kv[sl]);
+        };
+        rows_issue(t0, 0, kv[0]);
+        rows_issue(min(t0 + 1, t1 - 1), 0, kv[1]);
+        prime(t0, 0);
+        rows_issue(min(t0 + 2, t1 - 1), 0, kv[0]);
+        prime(min(t0 + 1, t1 - 1), 1);
+        rows_issue(min(t0 + 3, t1 - 1), 0, kv[1]);
+        for (int t = t0; t < t1; t += 2) {
+            step(t, 0);
+            step(t + 1, 1);
         }
     }
-    if (a.db && x == 0 && rh == 0) {           // lanes l, l+16, l+32, l+48 hold column l (+16)
+    if (dbw) {                                 // lanes l, l+16, l+32, l+48 hold column l (+16)
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
             float v = dbacc[h];
@@ -844,23 +858,28 @@ __device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
 // or the dense comparison mode, where the mask zeroes the dropped rows):
 // every row takes part at every t, so the accumulators stay in registers
 // over the whole t-range; no gather, no scatter.  Same grid as the
-// row-sparse kernel: workgroup i owns slice x = i % 8 and 128 columns; wave w
-// owns 32 columns (two tiles: each A fragment feeds two products) and every
-// row of the slice, in passes of NTL 16-row tiles.  The operands of two
-// steps are in flight while a step is multiplied.  The bias gradient comes
-// from the workgroups of the last slice (never empty: it ends at K).
-template <typename T, bool MASKED, int NTL, bool MULTI>
-__device__ __forceinline__ void wgrad_full(const WgArgs& a) {
+// row-sparse kernel: workgroup i owns slice x = i % 8 and 128 columns; wave
+// w owns 32 columns (two tiles: each A fragment feeds two products) and
+// the rows of the slice in passes of 16-row tiles.  The two halves of the
+// workgroup (w / 4) split each pass's tiles, NTW each; a slice that one
+// half's NTW tiles cover instead has the halves split the t-range (even and
+// odd steps), each carrying half the serial chain, and add their sums
+// through LDS at the end.  The operands of two of a wave's steps are in
+// flight while one is multiplied.  The bias gradient comes from the workgroups of the
+// last slice (never empty: it ends at K).
+template <typename T, bool MASKED, int NTW, bool MULTI, int RING = 2>
+__device__ __forceinline__ void wgrad_full(const WgArgs& a, float* red) {
     constexpr int NW = Raw8<T>::NW;
     constexpr uint32_t ES = sizeof(T);
     const int x = blockIdx.x % NXCD, cb = blockIdx.x / NXCD;
     if (cb * WG_NB >= a.G) return;
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // (wave-uniform)
     const int col = lane & 15, g8 = 8 * (lane >> 4);
-    const int rh = w / WG_NWV;                 // which NTL tiles of a pass of 2*NTL this wave takes
+    const int rh = w / WG_NWV;                 // this wave's half of the workgroup
     const int n = cb * WG_NB + 32 * (w % WG_NWV) + col;   // columns n and n + 16
     const int r0 = slice_start(x, a.K), r1 = slice_start(x + 1, a.K);
-    const int t0 = 0, t1 = a.T;
+    const bool tsplit = r1 - r0 <= 16 * NTW;   // the halves split the steps (else the tiles)
+    const int t1 = a.T, tb = tsplit ? rh : 0, ts = tsplit ? 2 : 1;
     uint32_t pm0[NW], pmb[2][NW];              // batch-pad masks (B side also zero past G)
     pad_mask<T>(g8, a.B, pm0);
     uint32_t boff[2];
@@ -872,64 +891,67 @@ __device__ __forceinline__ void wgrad_full(const WgArgs& a) {
     }
     const uint32_t abytes = (uint32_t)a.K * a.BP * ES, bbytes = (uint32_t)a.G * a.BP * ES;
     float dbacc[2] = {0.f, 0.f};
+    const bool dbw = a.db && x == NXCD - 1;    // this workgroup sums the bias gradient
     auto act_rsrc = [&](int t) {
         const T* act = (a.actT_first && t == a.t_first) ? (const T*)a.actT_first
                                                         : (const T*)a.actT + (long)(t + a.shift) * a.tstride;
         return buf_rsrc(act, abytes);
     };
     auto dat_rsrc = [&](int t) { return buf_rsrc((const T*)a.daT + (size_t)t * a.G * a.BP, bbytes); };
+    // this wave's slot of the pass reduction: [tile][half][reg][lane]
+    float* mine = red + (w % WG_NWV) * (NTW * 8 * 64) + lane;
 
-    for (int rp = r0; rp < r1; rp += 32 * NTL) {           // passes over the slice's row tiles
-        const bool first = rp == r0;
-        const int rb = rp + 16 * NTL * rh;     // this wave's first row of the pass
-        int rowa[NTL];                         // A-fragment row of this lane in tile i (clamped into K)
+    for (int rp = r0; rp < r1; rp += 32 * NTW) {           // passes over the slice's row tiles
+        const bool first = rp == r0 && dbw;    // (the bias gradient is summed on the first pass)
+        const int rb = tsplit ? rp : rp + 16 * NTW * rh;   // this wave's first row of the pass
+        int rowa[NTW];                         // A-fragment row of this lane in tile i (clamped into K)
 #pragma unroll
-        for (int i = 0; i < NTL; ++i) rowa[i] = min(rb + 16 * i + col, a.K - 1);
-        f32x4_t acc[NTL][2];
+        for (int i = 0; i < NTW; ++i) rowa[i] = min(rb + 16 * i + col, a.K - 1);
+        f32x4_t acc[NTW][2];
 #pragma unroll
-        for (int i = 0; i < NTL; ++i) acc[i][0] = acc[i][1] = f32x4_t{0, 0, 0, 0};
-        // operands of two steps in flight: slot = step % 2
-        Raw8<T> fa[2][NTL], fb[2][2];
-        int mk[2][NTL];
+        for (int i = 0; i < NTW; ++i) acc[i][0] = acc[i][1] = f32x4_t{0, 0, 0, 0};
+        // operands of two of the wave's steps in flight, slots alternating
+        Raw8<T> fa[RING][NTW], fb[RING][2];
+        int mk[RING][NTW];
         auto issue = [&](int t, int sl) {
             const __amdgpu_buffer_rsrc_t ar = act_rsrc(t), br = dat_rsrc(t);
 #pragma unroll
-            for (int i = 0; i < NTL; ++i) raw_load(fa[sl][i], ar, (uint32_t)(rowa[i] * a.BP + g8) * ES);
+            for (int i = 0; i < NTW; ++i) raw_load(fa[sl][i], ar, (uint32_t)(rowa[i] * a.BP + g8) * ES);
             raw_load(fb[sl][0], br, boff[0]);
             raw_load(fb[sl][1], br, boff[1]);
             if (MASKED) {
                 const __amdgpu_buffer_rsrc_t mr = buf_rsrc(a.site.mask + (size_t)t * a.site.kmax, (uint32_t)a.site.kmax);
 #pragma unroll
-                for (int i = 0; i < NTL; ++i) mk[sl][i] = (int)__builtin_amdgcn_raw_buffer_load_b8(mr, (uint32_t)rowa[i], 0, 0);
+                for (int i = 0; i < NTW; ++i) mk[sl][i] = (int)__builtin_amdgcn_raw_buffer_load_b8(mr, (uint32_t)rowa[i], 0, 0);
             }
         };
         // the step in slot sl (none past the range); then that slot takes the
         // operands of step tn (loads that always go out keep the wait counts exact)
         auto step = [&](int t, int sl, int tn) {
           if (t < t1) {
-            Raw8<T>(&ca)[NTL] = fa[sl];
+            Raw8<T>(&ca)[NTW] = fa[sl];
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
                 raw_and(fb[sl][h], pmb[h]);
                 if (first) db_add_raw(fb[sl][h], dbacc[h]);
             }
 #pragma unroll
-            for (int i = 0; i < NTL; ++i) {
+            for (int i = 0; i < NTW; ++i) {
                 raw_and(ca[i], pm0);
                 if (MASKED) {
 #pragma unroll
                     for (int q = 0; q < NW; ++q) ca[i].w[q] = mk[sl][i] ? ca[i].w[q] : 0u;
                 }
-                raw_mma(ca[i], fb[sl][0], acc[i][0]);
-                raw_mma(ca[i], fb[sl][1], acc[i][1]);
+                raw_mma(fb[sl][0], ca[i], acc[i][0]);
+                raw_mma(fb[sl][1], ca[i], acc[i][1]);
             }
             for (int bc = 32; MULTI && bc < a.B; bc += 32) {    // further batch chunks (B > 32)
                 const __amdgpu_buffer_rsrc_t ar = act_rsrc(t), br = dat_rsrc(t);
-                Raw8<T> xb[2], xa[NTL];
+                Raw8<T> xb[2], xa[NTW];
                 raw_load(xb[0], br, boff[0] + (uint32_t)bc * ES);
                 raw_load(xb[1], br, boff[1] + (uint32_t)bc * ES);
 #pragma unroll
-                for (int i = 0; i < NTL; ++i) raw_load(xa[i], ar, (uint32_t)(rowa[i] * a.BP + bc + g8) * ES);
+                for (int i = 0; i < NTW; ++i) raw_load(xa[i], ar, (uint32_t)(rowa[i] * a.BP + bc + g8) * ES);
                 uint32_t pm[NW];
                 pad_mask<T>(bc + g8, a.B, pm);
 #pragma unroll
@@ -939,60 +961,90 @@ __device__ __forceinline__ void wgrad_full(const WgArgs& a) {
                     if (first) db_add_raw(xb[h], dbacc[h]);
                 }
 #pragma unroll
-                for (int i = 0; i < NTL; ++i) {
+                for (int i = 0; i < NTW; ++i) {
                     raw_and(xa[i], pm);
                     if (MASKED) {
 #pragma unroll
                         for (int q = 0; q < NW; ++q) xa[i].w[q] = mk[sl][i] ? xa[i].w[q] : 0u;
                     }
-                    raw_mma(xa[i], xb[0], acc[i][0]);
-                    raw_mma(xa[i], xb[1], acc[i][1]);
+                    raw_mma(xb[0], xa[i], acc[i][0]);
+                    raw_mma(xb[1], xa[i], acc[i][1]);
                 }
             }
           }
             issue(tn, sl);
         };
-        if (t0 < t1) {
-            issue(t0, 0);
-            issue(min(t0 + 1, t1 - 1), 1);
-        }
-        for (int t = t0; t < t1; t += 2) {
-            step(t, 0, min(t + 2, t1 - 1));
-            step(t + 1, 1, min(t + 3, t1 - 1));
-        }
-        // output r of this lane is row 4*(lane/16)+r of the tile
-        float* out = a.out;
+        if (tb < t1) {
 #pragma unroll
-        for (int i = 0; i < NTL; ++i)
+            for (int j = 0; j < RING; ++j) issue(min(tb + j * ts, t1 - 1), j);
+        }
+        for (int t = tb; t < t1; t += RING * ts) {
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int row = rb + 16 * i + acc_row(lane, r);
+            for (int j = 0; j < RING; ++j) step(t + j * ts, j, min(t + (j + RING) * ts, t1 - 1));
+        }
+        // the odd half hands its sums to the even half
+        if (tsplit && rh) {
+#pragma unroll
+            for (int i = 0; i < NTW; ++i)
 #pragma unroll
                 for (int h = 0; h < 2; ++h)
-                    if (row < r1 && n + 16 * h < a.G) out[(size_t)row * a.G + n + 16 * h] = a.s * acc[i][h][r];
-            }
-    }
-    if (a.db && x == NXCD - 1 && rh == 0) {    // (the last slice is never empty) lanes l, l+16, l+32, l+48 hold column l
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            float v = dbacc[h];
-            v += __shfl_xor(v, 16);
-            v += __shfl_xor(v, 32);
-            if (lane < 16 && n + 16 * h < a.G) a.db[n + 16 * h] = v;
+                    for (int r = 0; r < 4; ++r) mine[((i * 2 + h) * 4 + r) * 64] = acc[i][h][r];
+        }
+        if (tsplit) __syncthreads();
+        if (!tsplit || !rh) {
+            // (transposed products) output r of this lane is gradient column
+            // 4*(lane/16)+r of the column tile, in the lane's own row; G is a
+            // multiple of 4, so the four columns are all in range or none
+            const int nq = n - col + 4 * (lane >> 4);
+#pragma unroll
+            for (int i = 0; i < NTW; ++i) {
+                const int row = rb + 16 * i + col;
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    float4 v;
+                    v.x = a.s * (tsplit ? acc[i][h][0] + mine[((i * 2 + h) * 4 + 0) * 64] : acc[i][h][0]);
+                    v.y = a.s * (tsplit ? acc[i][h][1] + mine[((i * 2 + h) * 4 + 1) * 64] : acc[i][h][1]);
+                    v.z = a.s * (tsplit ? acc[i][h][2] + mine[((i * 2 + h) * 4 + 2) * 64] : acc[i][h][2]);
+                    v.w = a.s * (tsplit ? acc[i][h][3] + mine[((i * 2 + h) * 4 + 3) * 64] : acc[i][h][3]);
+                    if (row < r1 && nq + 16 * h < a.G) *(float4*)(a.out + (size_t)row * a.G + nq + 16 * h) = v;
+                }
+            }
+        }
+        if (tsplit) __syncthreads();           // (the next pass reuses the slots)
+    }
+    if (dbw) {                                 // (the last slice is never empty) lanes l, l+16, l+32, l+48 hold column l
+        if (tsplit && rh) {
+            mine[0] = dbacc[0];
+            mine[64] = dbacc[1];
+        }
+        if (tsplit) __syncthreads();
+        if (!rh) {
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                float v = tsplit ? dbacc[h] + mine[64 * h] : dbacc[h];
+                v += __shfl_xor(v, 16);
+                v += __shfl_xor(v, 32);
+                if (lane < 16 && n + 16 * h < a.G) a.db[n + 16 * h] = v;
+            }
         }
     }
 }
+
+// LDS of the full kernel's pass reduction
+template <typename T>
+constexpr size_t wgrad_full_lds_bytes() { return (size_t)WG_NWV * (WgTiles<T>::N / 2) * 8 * 64 * 4; }
 
 // One launch for every weight gradient of a pass (grid z = problem): a
 // problem whose keep lists are all the identity takes the full kernel, the
 // others the row-sparse one; either way every workgroup runs every step, so
 // the two kinds overlap instead of taking a launch each.
 template <typename T, bool MASKED, bool MULTI>
-__global__ void __launch_bounds__(128 * WG_NWV) k_wgrad(WgBatch bt) {
+__global__ void __launch_bounds__(128 * WG_NWV) __attribute__((amdgpu_waves_per_eu(sizeof(T) == 2 && !MULTI ? 4 : 1))) k_wgrad(WgBatch bt) {
     extern __shared__ float acc_lds[];
     const WgArgs& a = bt.p[blockIdx.z];
-    if (a.full) wgrad_full<T, MASKED, WgTiles<T>::N / 2, MULTI>(a);
-    else wgrad_gather<T, false, MULTI>(a, acc_lds);
+    if (a.full) wgrad_full<T, MASKED, WgTiles<T>::N / 2, MULTI>(a, acc_lds);
+    else wgrad_gather<T, MULTI>(a, acc_lds);
 }
 
 // ---------------------------------------------------------------------------
@@ -1215,7 +1267,10 @@ void launch_wgrad(const WgBatch& b, hipStream_t st) {
     size_t lds = 0;
     bool multi = a.B > 32;                     // builds with the extra loops (batch chunks, tile rounds)
     for (int i = 0; i < b.np; ++i) {
-        if (b.p[i].full) continue;
+        if (b.p[i].full) {
+            lds = std::max(lds, wgrad_full_lds_bytes<T>());
+            continue;
+        }
         lds = std::max(lds, wgrad_lds_bytes(b.p[i].K));
         multi = multi || (b.p[i].K + NSEG - 1) / NSEG > 16 * (WgTiles<T>::N / 2);
     }
