@@ -639,32 +639,47 @@ struct WgTiles { static constexpr int N = 6; };   // 16-row tiles in registers a
 template <>
 struct WgTiles<float> { static constexpr int N = 4; };
 
+// Whether the two halves of a row-sparse weight-gradient workgroup split the
+// t-range (each then takes every kept row of the slice, into an accumulator
+// of its own): when one round of tiles holds the whole slice
+template <typename T>
+__host__ __device__ inline bool wgrad_tsplit(int K) { return (K + NXCD - 1) / NXCD <= 16 * (WgTiles<T>::N / 2); }
 // LDS bytes of the row-sparse weight gradient for a K-row weight
-inline size_t wgrad_lds_bytes(int K) { return (size_t)((K + NXCD - 1) / NXCD + 1) * WG_LDC * sizeof(float); }
+template <typename T>
+inline size_t wgrad_lds_bytes(int K) {
+    return (size_t)(wgrad_tsplit<T>(K) ? 2 : 1) * ((K + NXCD - 1) / NXCD + 1) * WG_LDC * sizeof(float);
+}
 
 template <typename T, bool MULTI>
 __device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
-    constexpr int MAXT = WgTiles<T>::N / 2;     // 16-row tiles of a round (a wave takes half a slice)
+    constexpr int MAXT = WgTiles<T>::N / 2;     // 16-row tiles of a round
     constexpr int NW = Raw8<T>::NW;
     constexpr uint32_t ES = sizeof(T);
-    // acc_lds: [rows of the slice + 1][WG_LDC]
+    // acc_lds: [rows of the slice + 1][WG_LDC], one per half when the halves split the t-range
     const int x = blockIdx.x % NXCD, cb = blockIdx.x / NXCD;
     if (cb * WG_NB >= a.G) return;
     const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // (wave-uniform)
     const int col = lane & 15, g8 = 8 * (lane >> 4);
-    const int rh = w / WG_NWV;                   // the half of the slice whose kept rows this wave takes
+    const int rh = w / WG_NWV;                   // this wave's half of the workgroup
     const int c0 = 32 * (w % WG_NWV);            // this wave's columns within the block: two tiles
     const int n0 = cb * WG_NB, n = n0 + c0 + col;   // (columns n and n + 16)
     const int r0 = slice_start(x, a.K), r1 = slice_start(x + 1, a.K);
     const int nrow = r1 - r0;
-    for (int i = lane + 64 * rh; i < (nrow + 1) * 32; i += 128) acc_lds[(i >> 5) * WG_LDC + c0 + (i & 31)] = 0.0f;
+    // the halves take the even and odd steps (each every kept row of the
+    // slice), or the kept rows of the slice's two segments (each every step)
+    const bool tsplit = wgrad_tsplit<T>(a.K);
+    const int ts = tsplit ? 2 : 1;               // the stride of this wave's steps
+    for (int i = lane + 64 * rh; i < (tsplit ? 2 : 1) * (nrow + 1) * 32; i += 128)
+        acc_lds[(i >> 5) * WG_LDC + c0 + (i & 31)] = 0.0f;
+    float* accr = acc_lds + (tsplit ? rh * (nrow + 1) * WG_LDC : 0);   // this half's accumulator
     // keep-list ranges of slice x at the steps t0 .. t1-1 of a window, in LDS
     // (a table in registers would make the compiler wait for all loads
     // wherever it is read)
     __shared__ int segtab[3][64];                // segments 2x, 2x+1 and their end
     int t0 = 0, t1 = 0;
-    auto seg_b = [&](int t) { return __builtin_amdgcn_readfirstlane(segtab[rh][t - t0]); };
-    auto seg_e = [&](int t) { return __builtin_amdgcn_readfirstlane(segtab[rh + 1][t - t0]); };
+    const int sb = tsplit ? 0 : rh, se = tsplit ? 2 : rh + 1;
+    auto seg_b = [&](int t) { return __builtin_amdgcn_readfirstlane(segtab[sb][t - t0]); };
+    auto seg_e = [&](int t) { return __builtin_amdgcn_readfirstlane(segtab[se][t - t0]); };
     uint32_t pm0[NW], pmb[2][NW];              // batch-pad masks of chunk 0 (A side; B side adds n < G)
     pad_mask<T>(g8, a.B, pm0);
     uint32_t boff[2];                          // DA^T fragment offsets of the two column tiles
@@ -676,7 +691,7 @@ __device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
     }
     const uint32_t abytes = (uint32_t)a.K * a.BP * ES, bbytes = (uint32_t)a.G * a.BP * ES;
     const int spare = nrow * WG_LDC;
-    const bool dbw = a.db && x == 0 && rh == 0;  // this wave writes the bias gradient
+    const bool dbw = a.db && x == 0 && (tsplit || rh == 0);   // this wave sums bias-gradient terms
 
     // keep-list entries of the A-fragment rows of tiles jt0 .. jt0+MAXT-1 at t
     auto rows_issue = [&](int t, int jt0, int* kv) {
@@ -762,7 +777,7 @@ __device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
         for (int i = 0; i < MAXT; ++i)
             if (i < nt)
 #pragma unroll
-                for (int h = 0; h < 2; ++h) old[i][h] = *(const float4*)(acc_lds + la[i] + cq + 16 * h);
+                for (int h = 0; h < 2; ++h) old[i][h] = *(const float4*)(accr + la[i] + cq + 16 * h);
 #pragma unroll
         for (int i = 0; i < MAXT; ++i)
             if (i < nt)
@@ -773,7 +788,7 @@ __device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
                     v.y += a.s * acc[i][h][1];
                     v.z += a.s * acc[i][h][2];
                     v.w += a.s * acc[i][h][3];
-                    *(float4*)(acc_lds + la[i] + cq + 16 * h) = v;
+                    *(float4*)(accr + la[i] + cq + 16 * h) = v;
                 }
     };
 
@@ -787,8 +802,9 @@ __device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
             segtab[2][threadIdx.x] = ks[2];
         }
         __syncthreads();
-        // ring slots by step parity: the A rows, DA^T fragments and LDS row
-        // addresses of steps t and t+1, the keep-list entries of t+2 and t+3
+        // ring slots alternating over the wave's steps (stride ts): the A
+        // rows, DA^T fragments and LDS row addresses of its next two steps,
+        // the keep-list entries of the two after
         int kv[2][MAXT], kk[2][MAXT], la[2][MAXT];
         Raw8<T> fa[2][MAXT], fb[2][2];
         // the operands of step t into slot sl, from its keep-list entries
@@ -800,7 +816,7 @@ __device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
             raw_load(fb[sl][1], br, boff[1]);
         };
         // step t from slot sl (none past the window); then the slot takes
-        // the operands of t+2 and the keep-list entries of t+4.  Loads that
+        // the operands of t+2ts and the keep-list entries of t+4ts.  Loads that
         // always go out (steps clamped into the window) and the same issue
         // order in the prologue keep the wait counts exact.
         auto step = [&](int t, int sl) {
@@ -823,34 +839,48 @@ __device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
                     finish(ar, br, kc, lc, min(ntile - jt0, MAXT), fa2, fb0, false);
                 }
             }
-            prime(min(t + 2, t1 - 1), sl);
-            rows_issue(min(t + 4, t1 - 1), 0, kv[sl]);
+            prime(min(t + 2 * ts, t1 - 1), sl);
+            rows_issue(min(t + 4 * ts, t1 - 1), 0, kv[sl]);
         };
-        rows_issue(t0, 0, kv[0]);
-        rows_issue(min(t0 + 1, t1 - 1), 0, kv[1]);
-        prime(t0, 0);
-        rows_issue(min(t0 + 2, t1 - 1), 0, kv[0]);
-        prime(min(t0 + 1, t1 - 1), 1);
-        rows_issue(min(t0 + 3, t1 - 1), 0, kv[1]);
-        for (int t = t0; t < t1; t += 2) {
+        const int tb = t0 + (tsplit ? rh : 0);
+        rows_issue(min(tb, t1 - 1), 0, kv[0]);
+        rows_issue(min(tb + ts, t1 - 1), 0, kv[1]);
+        prime(min(tb, t1 - 1), 0);
+        rows_issue(min(tb + 2 * ts, t1 - 1), 0, kv[0]);
+        prime(min(tb + ts, t1 - 1), 1);
+        rows_issue(min(tb + 3 * ts, t1 - 1), 0, kv[1]);
+        for (int t = tb; t < t1; t += 2 * ts) {
             step(t, 0);
-            step(t + 1, 1);
-        }
-    }
-    if (dbw) {                                 // lanes l, l+16, l+32, l+48 hold column l (+16)
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            float v = dbacc[h];
-            v += __shfl_xor(v, 16);
-            v += __shfl_xor(v, 32);
-            if (lane < 16 && n + 16 * h < a.G) a.db[n + 16 * h] = v;
+            step(t + ts, 1);
         }
     }
     __syncthreads();
+    if (a.db && x == 0) {                      // lanes l, l+16, l+32, l+48 hold column l (+16)
+        float v[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            v[h] = dbacc[h];
+            v[h] += __shfl_xor(v[h], 16);
+            v[h] += __shfl_xor(v[h], 32);
+        }
+        // the odd half's sums pass through the (no longer used) spare row
+        float* sp = acc_lds + nrow * WG_LDC + c0;
+        if (tsplit && rh && lane < 16) {
+            sp[lane] = v[0];
+            sp[16 + lane] = v[1];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+            if (!rh && lane < 16 && n + 16 * h < a.G) a.db[n + 16 * h] = tsplit ? v[h] + sp[16 * h + lane] : v[h];
+    }
     float* out = a.out;
+    const float* acc2 = acc_lds + (nrow + 1) * WG_LDC;   // the odd half's accumulator
     for (int i = threadIdx.x; i < nrow * WG_NB; i += blockDim.x) {
         const int rr = i / WG_NB, cc = i % WG_NB;
-        if (n0 + cc < a.G) out[(size_t)(r0 + rr) * a.G + n0 + cc] = acc_lds[rr * WG_LDC + cc];
+        if (n0 + cc < a.G)
+            out[(size_t)(r0 + rr) * a.G + n0 + cc] =
+                tsplit ? acc_lds[rr * WG_LDC + cc] + acc2[rr * WG_LDC + cc] : acc_lds[rr * WG_LDC + cc];
     }
 }
 
@@ -1271,7 +1301,7 @@ void launch_wgrad(const WgBatch& b, hipStream_t st) {
             lds = std::max(lds, wgrad_full_lds_bytes<T>());
             continue;
         }
-        lds = std::max(lds, wgrad_lds_bytes(b.p[i].K));
+        lds = std::max(lds, wgrad_lds_bytes<T>(b.p[i].K));
         multi = multi || (b.p[i].K + NSEG - 1) / NSEG > 16 * (WgTiles<T>::N / 2);
     }
     const dim3 blk(128 * WG_NWV);
