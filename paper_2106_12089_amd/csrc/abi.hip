@@ -23,8 +23,9 @@ template <typename T> void launch_step(const StepArgs& a, int D, hipStream_t st)
 template <typename T> void launch_bwd(const BwdArgs& a, int D, hipStream_t st);
 template <typename T> void launch_dx(const DxArgs& a, int K, hipStream_t st);
 template <typename T> void launch_wgrad(const WgBatch& b, hipStream_t st);
-template <typename T> void launch_fwd_init(const void*, const float*, float*, float*, long, hipStream_t);
-void launch_bwd_init(const float*, const float*, float*, float*, long, void*, int, int, int, long, long, hipStream_t);
+template <typename T> void launch_fwd_init(const void*, const float*, float*, float*, long, unsigned*, int*, hipStream_t);
+void launch_bwd_init(const float*, const float*, float*, float*, long, void*, int, int, int, long, long, unsigned*, int*,
+                     hipStream_t);
 void launch_expand(const float*, int, const SiteView&, float*, int, int, int, hipStream_t);
 void launch_mse(const float*, const float*, const int32_t*, float*, float*, int, float*, int, int, int,
                 hipStream_t);
@@ -238,13 +239,12 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
     const size_t es = P.esize;
     char* R = (char*)reserve;
     char* W = (char*)ws;
-    launch_fwd_init<E>(h0, c0, hT, cT, (long)L * D * B * H, st);
-    {
+    launch_fwd_init<E>(h0, c0, hT, cT, (long)L * D * B * H, (unsigned*)(W + P.w_sync), (int*)(W + P.w_sync + 4096), st);
+    {   // x (T matrices) and h0 (L*D matrices), transposed in one launch
         TransArgs t;
-        t.src = x; t.dst = R + P.r_xT; t.B = B; t.K = P.I; t.BP = BP;
-        launch_transpose<E>(t, T, st);
-        t.src = h0; t.dst = R + P.r_h0T; t.K = H;
-        launch_transpose<E>(t, L * D, st);
+        t.src = x; t.dst = R + P.r_xT; t.B = B; t.K = P.I; t.BP = BP; t.n1 = T;
+        t.src2 = h0; t.dst2 = R + P.r_h0T; t.K2 = H;
+        launch_transpose<E>(t, T + L * D, st);
     }
     // Unidirectional stack: every layer's recurrence in one persistent
     // launch, layer l one step behind layer l-1, each layer above the first
@@ -419,6 +419,8 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
     const size_t es = P.esize;
     const char* R = (const char*)reserve;
     char* W = (char*)ws;
+    unsigned* sync_bar = (unsigned*)(W + P.w_sync);
+    int* sync_err = (int*)(W + P.w_sync + 4096);
     const int tps_h = ((H + 7) / 8 + 15) / 16;     // 16-unit tiles per XCD slice of the hidden units
     // DA and DA^T regions: one per direction, or one per layer when a
     // unidirectional stack runs in one launch
@@ -518,7 +520,7 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
     // a worker between layers l+1 and l forming dx of layer l+1 per step.
     if (use_persistent() && use_stacked() && D == 1 && L > 1 && 2 * L - 1 <= 8) {
         launch_bwd_init(nullptr, nullptr, nullptr, nullptr, 0, W + P.w_da, (int)es, G, P.mtiles, (long)L * T,
-                        (long)P.das, st);
+                        (long)P.das, sync_bar, sync_err, st);
         PBwdArgs pa;
         common_args(pa);
         pa.nslots = 2 * L - 1;
@@ -559,7 +561,7 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
         float* dcs = (float*)(W + P.w_dc);
         launch_bwd_init(dhT ? dhT + (size_t)l * D * B * H : nullptr, dcT ? dcT + (size_t)l * D * B * H : nullptr,
                         dhc, dcs, (long)D * B * H, l == L - 1 ? (void*)(W + P.w_da) : nullptr, (int)es, G,
-                        P.mtiles, (long)D * T, (long)P.das, st);
+                        P.mtiles, (long)D * T, (long)P.das, sync_bar, sync_err, st);
         float* dxc_above = (float*)(W + P.w_dxc) + (size_t)((l + 1) & 1) * T * B * P.kin_max;
         float* dxc_here = (float*)(W + P.w_dxc) + (size_t)(l & 1) * T * B * P.kin_max;
         bool persistent_done = false;

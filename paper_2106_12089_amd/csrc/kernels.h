@@ -43,6 +43,10 @@ struct TransArgs {
     const void* src;
     void* dst;
     int B, K, BP;
+    int n1;                             // matrices of the first job; the rest come from the second
+    const void* src2;                   // second job (K2 columns), or unused when every matrix is the first job's
+    void* dst2;
+    int K2;
 };
 
 // Forward input product of one layer/direction, all t in one launch:
@@ -149,7 +153,7 @@ struct WgArgs {
     int full;                           // every keep list of the site is the identity (p = 0, or dense mode)
     float s;
 };
-// Weight gradients of one kind (all row-sparse, or all full) in one launch
+// Weight gradients of a pass (row-sparse and full problems) in one launch
 constexpr int WG_MAXP = 8;
 struct WgBatch {
     WgArgs p[WG_MAXP];
@@ -195,10 +199,17 @@ struct PFwdDir {
 // different banks)
 __host__ __device__ inline int fwd_hp(int K) { return (K + 31) / 32 * 32 + 8; }
 
+// Barrier counters of the persistent kernels: slot i at bar + BAR_PITCH * i
+// (a cache line each), the exit counter at slot BAR_EXIT; the error flag
+// sits apart.  The init kernel of a pass clears them, and each persistent
+// launch leaves them clear for the next.
+constexpr int BAR_PITCH = 64;
+constexpr int BAR_EXIT = 8;
+
 struct PFwdArgs {
     PFwdDir d[8];                       // slots: the directions of one layer, or the layers of a stack and their workers
     const int32_t* lengths;
-    unsigned* bar;                      // barrier counters, slot i at bar + 64 i (zeroed before launch)
+    unsigned* bar;                      // barrier counters, slot i at bar + BAR_PITCH * i (clear at launch)
     int* err;                           // barrier time-out flag
     long long timeout;                  // wall-clock ticks
     int B, H, HP, T, BP, ldy, dense, ntiles, mgroups, mtiles;

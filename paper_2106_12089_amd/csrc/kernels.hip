@@ -140,23 +140,26 @@ __global__ void __launch_bounds__(256) k_mask_build(MaskArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// src [N][B][K] -> dst [N][K][BP], zero rows b in [B, BP).
-// grid (ceil(K/32), BP/32, N), block (32, 8).
+// src [N][B][K] -> dst [N][K][BP], zero rows b in [B, BP); two such jobs
+// (matrices z < n1 from the first, the others from the second) in one launch.
+// grid (ceil(max K/32), BP/32, N), block (32, 8).
 template <typename T>
 __global__ void __launch_bounds__(256) k_transpose(TransArgs a) {
     __shared__ T tile[32][33];
-    const int n = blockIdx.z;
+    const bool second = (int)blockIdx.z >= a.n1;
+    const int n = second ? blockIdx.z - a.n1 : blockIdx.z, K = second ? a.K2 : a.K;
     const int k0 = blockIdx.x * 32, b0 = blockIdx.y * 32;
-    const T* src = (const T*)a.src + (size_t)n * a.B * a.K;
-    T* dst = (T*)a.dst + (size_t)n * a.K * a.BP;
+    if (k0 >= K) return;                       // (the whole workgroup)
+    const T* src = (const T*)(second ? a.src2 : a.src) + (size_t)n * a.B * K;
+    T* dst = (T*)(second ? a.dst2 : a.dst) + (size_t)n * K * a.BP;
     for (int i = threadIdx.y; i < 32; i += 8) {
         const int b = b0 + i, k = k0 + threadIdx.x;
-        tile[i][threadIdx.x] = (b < a.B && k < a.K) ? src[(size_t)b * a.K + k] : zero_val<T>();
+        tile[i][threadIdx.x] = (b < a.B && k < K) ? src[(size_t)b * K + k] : zero_val<T>();
     }
     __syncthreads();
     for (int i = threadIdx.y; i < 32; i += 8) {
         const int k = k0 + i, b = b0 + threadIdx.x;
-        if (k < a.K) dst[(size_t)k * a.BP + b] = tile[threadIdx.x][i];
+        if (k < K) dst[(size_t)k * a.BP + b] = tile[threadIdx.x][i];
     }
 }
 
@@ -1080,9 +1083,18 @@ __global__ void __launch_bounds__(128 * WG_NWV) __attribute__((amdgpu_waves_per_
 // ---------------------------------------------------------------------------
 // Small elementwise kernels.
 
-// hT <- h0 (as float), cT <- c0
+// the persistent kernels' barrier counters and error flag <- 0
+__device__ __forceinline__ void clear_sync(unsigned* bar, int* err) {
+    if (blockIdx.x == 0 && threadIdx.x <= BAR_EXIT) {
+        bar[BAR_PITCH * threadIdx.x] = 0u;
+        if (threadIdx.x == 0) *err = 0;
+    }
+}
+
+// hT <- h0 (as float), cT <- c0; the barrier counters <- 0
 template <typename T>
-__global__ void k_fwd_init(const T* h0, const float* c0, float* hT, float* cT, long n) {
+__global__ void k_fwd_init(const T* h0, const float* c0, float* hT, float* cT, long n, unsigned* bar, int* err) {
+    clear_sync(bar, err);
     for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < n; i += (long)gridDim.x * blockDim.x) {
         hT[i] = to_f32<T>(h0[i]);
         cT[i] = c0[i];
@@ -1094,7 +1106,8 @@ __global__ void k_fwd_init(const T* h0, const float* c0, float* hT, float* cT, l
 // of every fragment-major DA block (nblk blocks of das elements of es
 // bytes): no kernel writes them, and the backward products read them
 __global__ void k_bwd_init(const float* dhT, const float* dcT, float* dhc, float* dcs, long n,
-                           void* da, int es, int G, int mtiles, long nblk, long das) {
+                           void* da, int es, int G, int mtiles, long nblk, long das, unsigned* bar, int* err) {
+    clear_sync(bar, err);
     for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < n; i += (long)gridDim.x * blockDim.x) {
         dhc[i] = dhT ? dhT[i] : 0.0f;
         dcs[i] = dcT ? dcT[i] : 0.0f;
@@ -1262,7 +1275,8 @@ void launch_mask_build(const MaskArgs& a, int sites, hipStream_t st) {
 }
 template <typename T>
 void launch_transpose(const TransArgs& a, int N, hipStream_t st) {
-    launch_k(KID_TRANS, k_transpose<T>, dim3((a.K + 31) / 32, a.BP / 32, N), dim3(32, 8), 0, st, a);
+    const int K = N > a.n1 && a.K2 > a.K ? a.K2 : a.K;
+    launch_k(KID_TRANS, k_transpose<T>, dim3((K + 31) / 32, a.BP / 32, N), dim3(32, 8), 0, st, a);
 }
 template <typename T>
 void launch_fx(const FxArgs& a, hipStream_t st) {
@@ -1314,14 +1328,15 @@ void launch_wgrad(const WgBatch& b, hipStream_t st) {
     }
 }
 template <typename T>
-void launch_fwd_init(const void* h0, const float* c0, float* hT, float* cT, long n, hipStream_t st) {
-    launch_k(KID_NONE, k_fwd_init<T>, dim3(nblk(n, 256)), dim3(256), 0, st, (const T*)h0, c0, hT, cT, n);
+void launch_fwd_init(const void* h0, const float* c0, float* hT, float* cT, long n, unsigned* bar, int* err,
+                     hipStream_t st) {
+    launch_k(KID_NONE, k_fwd_init<T>, dim3(nblk(n, 256)), dim3(256), 0, st, (const T*)h0, c0, hT, cT, n, bar, err);
 }
 void launch_bwd_init(const float* dhT, const float* dcT, float* dhc, float* dcs, long n, void* da, int es, int G,
-                     int mtiles, long nblocks, long das, hipStream_t st) {
+                     int mtiles, long nblocks, long das, unsigned* bar, int* err, hipStream_t st) {
     const long np = da ? nblocks * 16 * mtiles * 32 : 0;      // upper bound of the DA padding entries
     launch_k(KID_NONE, k_bwd_init, dim3(nblk(n > np ? n : np, 256)), dim3(256), 0, st, dhT, dcT, dhc, dcs, n, da, es,
-             G, mtiles, nblocks, das);
+             G, mtiles, nblocks, das, bar, err);
 }
 void launch_expand(const float* dxc, int ldc, const SiteView& s, float* dx, int B, int K, int T, hipStream_t st) {
     launch_k(KID_NONE, k_expand, dim3(nblk((long)T * B * K, 256)), dim3(256), 0, st, dxc, ldc, s, dx, B, K, T);
@@ -1353,7 +1368,7 @@ int setup_kernel_attributes() {
     template void launch_bwd<T>(const BwdArgs&, int, hipStream_t);                          \
     template void launch_dx<T>(const DxArgs&, int, hipStream_t);                            \
     template void launch_wgrad<T>(const WgBatch&, hipStream_t);                             \
-    template void launch_fwd_init<T>(const void*, const float*, float*, float*, long, hipStream_t);
+    template void launch_fwd_init<T>(const void*, const float*, float*, float*, long, unsigned*, int*, hipStream_t);
 LSD_INST(float)
 LSD_INST(bf16)
 

@@ -37,7 +37,6 @@ namespace lsd {
 // The barrier counter of slot i sits at bar + BAR_PITCH * i: each counter
 // has a cache line of its own (workgroups of one slot poll the counter of
 // another while its own workgroups add to theirs).
-constexpr int BAR_PITCH = 64;
 
 __device__ __forceinline__ void grid_arrive(unsigned* bar) {
     __builtin_amdgcn_s_waitcnt(0);      // this thread's stores have completed
@@ -71,6 +70,24 @@ __device__ __forceinline__ bool grid_wait(unsigned* bar, unsigned target, int* e
     }
     __syncthreads();
     return ok != 0;
+}
+
+// Every workgroup ends here, past its last barrier wait; the last one to
+// arrive returns the step counters, the error flag and the exit counter to
+// zero, so the next launch starts clear without a clearing kernel.  (The
+// outputs' time-out check comes before: the flag is read by then.)
+__device__ __forceinline__ void grid_exit(unsigned* bar, int nslots, int* err) {
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        unsigned* ex = bar + BAR_PITCH * BAR_EXIT;
+        const unsigned tk = __hip_atomic_fetch_add(ex, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+        if (tk == gridDim.x - 1) {
+            for (int i = 0; i < nslots; ++i)
+                __hip_atomic_store(bar + BAR_PITCH * i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(err, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(ex, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
 }
 
 // coherent (agent-scope) element store and 8-element load of exchange data
@@ -474,6 +491,7 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
             prefetch(s + 1);
             grid_arrive(bar);                   // (also: every wave is past its reads of red)
         }
+        grid_exit(a.bar, a.nslots, a.err);
         return;
     }
 
@@ -601,6 +619,7 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
             D.cT[(size_t)pb[q] * H + pu[q]] = failed ? __builtin_nanf("") : creg[q];
         }
     }
+    grid_exit(a.bar, a.nslots, a.err);
 }
 
 // ---------------------------------------------------------------------------
@@ -776,6 +795,7 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
             }
             grid_arrive(bar);
         }
+        grid_exit(a.bar, a.nslots, a.err);
         return;
     }
 
@@ -882,11 +902,7 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
                 D.dc0[(size_t)pb[q] * H + pu[q]] = __builtin_nanf("");
             }
     }
-}
-
-__global__ void k_zero_sync(unsigned* bar, int n, int* err) {
-    for (int i = threadIdx.x; i < n; i += blockDim.x) bar[BAR_PITCH * i] = 0u;
-    if (threadIdx.x == 0) *err = 0;
+    grid_exit(a.bar, a.nslots, a.err);
 }
 
 // ---------------------------------------------------------------------------
@@ -959,7 +975,6 @@ hipError_t launch_fwd_persist(PFwdArgs& a, hipStream_t st, int kid_timer_on, hip
                                    : (MG == 32 ? k_fwd_persist<T, 2, 32> : k_fwd_persist<T, 2, 64>);
     hipError_t e = resident_limit((const void*)fn, 64 * PF_NW, lds, nwg);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_zero_sync, dim3(1), dim3(64), 0, st, a.bar, a.nslots, a.err);
     if (kid_timer_on) (void)hipEventRecord(e0, st);
     if (!cooperative_api()) {
         hipLaunchKernelGGL(fn, dim3(nwg), dim3(64 * PF_NW), lds, st, a);
@@ -1008,7 +1023,6 @@ hipError_t launch_bwd_persist(PBwdArgs& a, hipStream_t st, int timer_on, hipEven
     a.ntiles = (a.H + UB - 1) / UB;
     const int nwg = a.nslots * a.ntiles * a.mgroups;
     if (a.nslots > 8) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_zero_sync, dim3(1), dim3(64), 0, st, a.bar, a.nslots, a.err);
     if (timer_on) (void)hipEventRecord(e0, st);
     hipError_t e;
     if (UB == 16 && MG == 32) e = launch_bwd_persist_t<T, 16, 32>(a, nwg, lds, st);
