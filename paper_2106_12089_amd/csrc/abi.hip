@@ -26,7 +26,6 @@ template <typename T> void launch_wgrad(const WgBatch& b, hipStream_t st);
 template <typename T> void launch_fwd_init(const void*, const float*, float*, float*, long, unsigned*, int*, hipStream_t);
 void launch_bwd_init(const float*, const float*, float*, float*, long, void*, int, int, int, long, long, unsigned*, int*,
                      hipStream_t);
-void launch_expand(const float*, int, const SiteView&, float*, int, int, int, hipStream_t);
 void launch_mse(const float*, const float*, const int32_t*, float*, float*, int, float*, int, int, int,
                 hipStream_t);
 int setup_kernel_attributes();
@@ -463,11 +462,11 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
             a.da[d] = da_of(reg0 + d);
             a.W[d] = w->W[l * D + d];
         }
-        a.site = nv; a.out = dxc_here; a.D = D; a.B = B; a.G = G; a.ldo = kin; a.T = T;
-        a.K = kin; a.tps = ((kin + 7) / 8 + 15) / 16; a.mtiles = P.mtiles;
+        // layer 0 writes the caller's full-width dx directly
+        a.site = nv; a.out = l == 0 ? dx : dxc_here; a.scatter = l == 0; a.D = D; a.B = B; a.G = G; a.ldo = kin;
+        a.T = T; a.K = kin; a.tps = ((kin + 7) / 8 + 15) / 16; a.mtiles = P.mtiles;
         a.dense = !P.compact; a.s = P.s_nr;
         launch_dx<E>(a, kin, st);
-        if (l == 0) launch_expand(dxc_here, kin, nv, dx, B, kin, T, st);
     };
     // weight and bias gradients (Eq. 11) of layer l: its problems join one
     // batch (row-sparse and full problems alike), one launch per batch

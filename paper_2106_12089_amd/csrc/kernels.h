@@ -131,7 +131,8 @@ struct DxArgs {
     const void* da[2];                  // DA_d [T] x fragment-major [B][G]
     const void* W[2];                   // [K][G]
     SiteView site;
-    float* out;                         // [T][B][ldo]
+    float* out;                         // [T][B][ldo]: kept columns at their compact positions, or
+    int scatter;                        //   (scatter) every column at its own, the dropped ones as zeros
     int D, B, G, ldo, T, K, tps, dense, mtiles;
     float s;
 };

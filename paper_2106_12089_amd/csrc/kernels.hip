@@ -523,7 +523,10 @@ __global__ void __launch_bounds__(1024) k_bwd(BwdArgs a) {
 // ---------------------------------------------------------------------------
 // Output-sparse input gradient, all t (Eq. 10), summed over directions.
 // grid (ceil(K/16), T, ceil(B/64)), block 256: 16 kept columns per
-// workgroup, the contraction over 4H split over the 4 waves.
+// workgroup, the contraction over 4H split over the 4 waves.  With scatter,
+// the output is the full-width gradient: kept columns go to their own
+// positions, and the workgroup of (slice, tile) also writes the zeros of
+// the same tile of the slice's dropped columns.
 template <typename T, int MT>
 __global__ void __launch_bounds__(256) k_dx(DxArgs a) {
     constexpr int U = sizeof(T) == 2 ? 4 : 2;           // 32-column chunks per wave loaded together
@@ -536,9 +539,18 @@ __global__ void __launch_bounds__(256) k_dx(DxArgs a) {
     const int32_t* ks = a.site.kseg + (size_t)t * (NSEG + 1);
     const int hi = ks[2 * x + 2];
     const int j0 = ks[2 * x] + 16 * ti;
+    const int m0 = blockIdx.z * 64;
+    if (a.scatter && ti < a.tps) {
+        const int32_t* ds = a.site.dseg + (size_t)t * (NSEG + 1);
+        const int dj = ds[2 * x] + 16 * ti + (threadIdx.x & 15);
+        if (dj < ds[2 * x + 2]) {
+            const int kd = a.site.drop[(size_t)t * a.site.kmax + dj];
+            for (int r = threadIdx.x >> 4; r < 16 * MT; r += 16)
+                if (m0 + r < a.B) a.out[((size_t)t * a.B + m0 + r) * a.ldo + kd] = 0.0f;
+        }
+    }
     if (ti >= a.tps || j0 >= hi) return;
     const int cnt = hi;                     // columns of this tile end at the slice end
-    const int m0 = blockIdx.z * 64;
     const int cl = lane & 15;
     const int j = j0 + cl;
     const int g8 = 8 * (lane >> 4);
@@ -592,7 +604,8 @@ __global__ void __launch_bounds__(256) k_dx(DxArgs a) {
         if (row < a.B && jj < cnt) {
             const int kk = krow[jj];
             const float sc = (a.dense && !mrow[kk]) ? 0.0f : a.s;
-            out[(size_t)row * a.ldo + jj] = sc * (red[0][rr][c] + red[1][rr][c] + red[2][rr][c] + red[3][rr][c]);
+            out[(size_t)row * a.ldo + (a.scatter ? kk : jj)] =
+                sc * (red[0][rr][c] + red[1][rr][c] + red[2][rr][c] + red[3][rr][c]);
         }
     }
 }
@@ -1122,18 +1135,6 @@ __global__ void k_bwd_init(const float* dhT, const float* dcT, float* dhc, float
     }
 }
 
-// dx[t][b][k] = dxc[t][b][pos_t[k]] (0 where the neuron is not listed)
-__global__ void k_expand(const float* dxc, int ldc, SiteView site, float* dx, int B, int K, int T) {
-    const long n = (long)T * B * K;
-    for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < n; i += (long)gridDim.x * blockDim.x) {
-        const int k = (int)(i % K);
-        const long tb = i / K;
-        const int t = (int)(tb / B);
-        const int p = site.pos[(size_t)t * site.kmax + k];
-        dx[i] = p >= 0 ? dxc[tb * ldc + p] : 0.0f;
-    }
-}
-
 // MSE loss gradient (a loss of the synthetic workloads).
 __device__ __forceinline__ float nvalid_rows(const int32_t* lengths, int B, int T) {
     if (!lengths) return (float)B * T;
@@ -1337,9 +1338,6 @@ void launch_bwd_init(const float* dhT, const float* dcT, float* dhc, float* dcs,
     const long np = da ? nblocks * 16 * mtiles * 32 : 0;      // upper bound of the DA padding entries
     launch_k(KID_NONE, k_bwd_init, dim3(nblk(n > np ? n : np, 256)), dim3(256), 0, st, dhT, dcT, dhc, dcs, n, da, es,
              G, mtiles, nblocks, das, bar, err);
-}
-void launch_expand(const float* dxc, int ldc, const SiteView& s, float* dx, int B, int K, int T, hipStream_t st) {
-    launch_k(KID_NONE, k_expand, dim3(nblk((long)T * B * K, 256)), dim3(256), 0, st, dxc, ldc, s, dx, B, K, T);
 }
 void launch_mse(const float* y, const float* tg, const int32_t* lengths, float* dy, float* partial, int np,
                 float* loss, int T, int B, int F, hipStream_t st) {
