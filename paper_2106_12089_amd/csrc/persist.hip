@@ -731,24 +731,28 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
     // the gradient of the tile's units (Eq. 10) from DA of step tn (of this
     // slot, or of src for a worker) into red
     auto recurrent_product = [&](int tn, const void* da_base) {
-        // DA_t is fragment-major: rows past B hold stale values that only
-        // reach output rows that are never used (reading them is cheaper here
-        // than a per-lane offset select); the columns past 4H of the last
-        // chunk are zero (cleared before the backward pass)
+        // DA_t is fragment-major: lanes of rows past B read zeros (the cache
+        // lines that hold only such rows are not fetched); the columns past
+        // 4H of the last chunk are zero (cleared before the backward pass)
         const __amdgpu_buffer_rsrc_t dr = buf_rsrc((const T*)da_base + (size_t)tn * das, (uint32_t)(das * sizeof(T)));
         f32x4_t acc[MT];
 #pragma unroll
         for (int i = 0; i < MT; ++i) acc[i] = f32x4_t{0, 0, 0, 0};
         const int nch = (G + 31) / 32;
         const int ul = lane & 15;
+        // byte offset of this lane's fragment of tile mt in chunk 0 (out of
+        // range for rows past B); chunk c adds c * cbytes
+        const uint32_t cbytes = (uint32_t)(a.mtiles * 512 * sizeof(T));
+        uint32_t lofs[MT];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+            lofs[mt] = m0 + 16 * mt + ul < B ? (uint32_t)(frag_lane_off(0, m0 / 16 + mt, lane, a.mtiles) * sizeof(T)) : OOB_OFF;
         for (int c0 = 0; c0 < nch; c0 += NW * MAXC) {
             Raw8<T> fa[MAXC][MT];
 #pragma unroll
             for (int i = 0; i < MAXC; ++i) {
-                const int n = 32 * (c0 + w + NW * i) + g8;
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt)
-                    raw_load(fa[i][mt], dr, (uint32_t)(frag_lane_off(c0 + w + NW * i, m0 / 16 + mt, lane, a.mtiles) * sizeof(T)));
+                for (int mt = 0; mt < MT; ++mt) raw_load(fa[i][mt], dr, lofs[mt] + (uint32_t)(c0 + w + NW * i) * cbytes);
             }
 #pragma unroll
             for (int i = 0; i < MAXC; ++i) {
