@@ -131,7 +131,7 @@ int make_plan(const lstm_sd_dims* d, Plan* p, const char** why) {
     q.w_dxc = off;    off = align_up(off + 2 * T * B * (size_t)q.kin_max * 4, A);
     const size_t bwd = off;
     q.w_sync = align_up(fwd > bwd ? fwd : bwd, A);
-    q.w_loss = q.w_sync + 8192;           // barrier counters (one 256-byte line per slot), error flag at +4096
+    q.w_loss = q.w_sync + align_up(SYNC_BYTES, A);   // barrier counters and error flag
     q.w_total = q.w_loss + 16384;
     return LSTM_SD_OK;
 }
@@ -238,7 +238,8 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
     const size_t es = P.esize;
     char* R = (char*)reserve;
     char* W = (char*)ws;
-    launch_fwd_init<E>(h0, c0, hT, cT, (long)L * D * B * H, (unsigned*)(W + P.w_sync), (int*)(W + P.w_sync + 4096), st);
+    launch_fwd_init<E>(h0, c0, hT, cT, (long)L * D * B * H, (unsigned*)(W + P.w_sync), (int*)(W + P.w_sync + SYNC_ERR_OFS),
+                       st);
     {   // x (T matrices) and h0 (L*D matrices), transposed in one launch
         TransArgs t;
         t.src = x; t.dst = R + P.r_xT; t.B = B; t.K = P.I; t.BP = BP; t.n1 = T;
@@ -275,7 +276,7 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
         memset(&pa, 0, sizeof(pa));
         pa.lengths = lengths;
         pa.bar = (unsigned*)(W + P.w_sync);
-        pa.err = (int*)(W + P.w_sync + 4096);
+        pa.err = (int*)(W + P.w_sync + SYNC_ERR_OFS);
         pa.timeout = barrier_timeout_ticks();
         pa.B = B; pa.H = H; pa.HP = P.HP; pa.T = T; pa.BP = BP; pa.ldy = D * H; pa.dense = !P.compact;
         pa.mtiles = P.mtiles;
@@ -419,7 +420,7 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
     const char* R = (const char*)reserve;
     char* W = (char*)ws;
     unsigned* sync_bar = (unsigned*)(W + P.w_sync);
-    int* sync_err = (int*)(W + P.w_sync + 4096);
+    int* sync_err = (int*)(W + P.w_sync + SYNC_ERR_OFS);
     const int tps_h = ((H + 7) / 8 + 15) / 16;     // 16-unit tiles per XCD slice of the hidden units
     // DA and DA^T regions: one per direction, or one per layer when a
     // unidirectional stack runs in one launch
@@ -429,7 +430,7 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
         memset(&pa, 0, sizeof(pa));
         pa.lengths = lengths;
         pa.bar = (unsigned*)(W + P.w_sync);
-        pa.err = (int*)(W + P.w_sync + 4096);
+        pa.err = (int*)(W + P.w_sync + SYNC_ERR_OFS);
         pa.timeout = barrier_timeout_ticks();
         pa.B = B; pa.H = H; pa.T = T; pa.BP = BP; pa.ldy = D * H;
         pa.kmax = P.kmax; pa.dense = !P.compact; pa.mtiles = P.mtiles; pa.s = P.s_rh; pa.s_nr = P.s_nr;

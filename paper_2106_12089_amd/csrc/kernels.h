@@ -200,17 +200,22 @@ struct PFwdDir {
 // different banks)
 __host__ __device__ inline int fwd_hp(int K) { return (K + 31) / 32 * 32 + 8; }
 
-// Barrier counters of the persistent kernels: slot i at bar + BAR_PITCH * i
-// (a cache line each), the exit counter at slot BAR_EXIT; the error flag
-// sits apart.  The init kernel of a pass clears them, and each persistent
-// launch leaves them clear for the next.
+// Barrier counters of the persistent kernels: slot i has BAR_LINES counters
+// (workgroup j adds to line j % BAR_LINES), line k at bar + BAR_PITCH *
+// (BAR_LINES * i + k), a cache line each; the exit counter is line 0 of
+// slot BAR_EXIT; the error flag sits at SYNC_ERR_OFS bytes.  The init kernel
+// of a pass clears them, and each persistent launch leaves them clear for
+// the next.
 constexpr int BAR_PITCH = 64;
+constexpr int BAR_LINES = 16;
 constexpr int BAR_EXIT = 8;
+constexpr int SYNC_ERR_OFS = BAR_PITCH * 4 * (BAR_LINES * BAR_EXIT + 1);   // bytes
+constexpr int SYNC_BYTES = SYNC_ERR_OFS + 256;
 
 struct PFwdArgs {
     PFwdDir d[8];                       // slots: the directions of one layer, or the layers of a stack and their workers
     const int32_t* lengths;
-    unsigned* bar;                      // barrier counters, slot i at bar + BAR_PITCH * i (clear at launch)
+    unsigned* bar;                      // barrier counters (BAR_LINES lines per slot; clear at launch)
     int* err;                           // barrier time-out flag
     long long timeout;                  // wall-clock ticks
     int B, H, HP, T, BP, ldy, dense, ntiles, mgroups, mtiles;

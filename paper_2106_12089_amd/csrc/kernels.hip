@@ -1098,8 +1098,8 @@ __global__ void __launch_bounds__(128 * WG_NWV) __attribute__((amdgpu_waves_per_
 
 // the persistent kernels' barrier counters and error flag <- 0
 __device__ __forceinline__ void clear_sync(unsigned* bar, int* err) {
-    if (blockIdx.x == 0 && threadIdx.x <= BAR_EXIT) {
-        bar[BAR_PITCH * threadIdx.x] = 0u;
+    if (blockIdx.x == 0) {
+        for (int i = threadIdx.x; i <= BAR_LINES * BAR_EXIT; i += blockDim.x) bar[BAR_PITCH * i] = 0u;
         if (threadIdx.x == 0) *err = 0;
     }
 }

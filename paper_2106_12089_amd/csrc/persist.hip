@@ -34,39 +34,65 @@ namespace lsd {
 // reaches the target.  The spin is bounded by wall-clock time; on time-out,
 // or when another workgroup has timed out, it reports failure and the kernel
 // ends (outputs are then poisoned with NaN).
-// The barrier counter of slot i sits at bar + BAR_PITCH * i: each counter
-// has a cache line of its own (workgroups of one slot poll the counter of
-// another while its own workgroups add to theirs).
+// A slot's counter is split over BAR_LINES cache lines (workgroup j adds to
+// line j % BAR_LINES, lanes of the waiting wave poll one line each): the
+// atomic adds of one line are serialised, and with one line per slot a step
+// of 82 workgroups spent about 0.5 us more in the barrier.  Waits are on
+// step counts: line k of slot d reaches s * (the number of the slot's
+// workgroups on line k) once step s is complete.
 
-__device__ __forceinline__ void grid_arrive(unsigned* bar) {
+// workgroups of slot `slot` (blocks [slot*nslot, (slot+1)*nslot)) that add
+// to line i
+__device__ __forceinline__ unsigned bar_count(int nslot, int slot, int i) {
+    auto upto = [&](int n) { return n > i ? (n - i + BAR_LINES - 1) / BAR_LINES : 0; };
+    return (unsigned)(upto((slot + 1) * nslot) - upto(slot * nslot));
+}
+__device__ __forceinline__ unsigned* slot_bar(unsigned* bar, int slot) { return bar + BAR_PITCH * BAR_LINES * slot; }
+
+__device__ __forceinline__ void grid_arrive(unsigned* sbar) {
     __builtin_amdgcn_s_waitcnt(0);      // this thread's stores have completed
     __syncthreads();
-    if (threadIdx.x == 0) __hip_atomic_fetch_add(bar, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (threadIdx.x == 0)
+        __hip_atomic_fetch_add(sbar + BAR_PITCH * (blockIdx.x % BAR_LINES), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Wait until the counter reaches target.  Returns false on time-out or when
-// another workgroup has timed out (err set).
-// With seen (LDS), thread 0 also records the last counter value it read.
-__device__ __forceinline__ bool grid_wait(unsigned* bar, unsigned target, int* err, long long timeout,
-                                          unsigned* seen = nullptr) {
+// Wait until slot `slot` (counter lines at sbar) has completed `steps`
+// steps.  Returns false on time-out or when another workgroup has timed out
+// (err set).  With seen (LDS), also records the number of steps the lines
+// read last show as complete.
+__device__ __forceinline__ bool grid_wait(unsigned* sbar, int slot, int nslot, unsigned steps, int* err,
+                                          long long timeout, unsigned* seen = nullptr) {
     __shared__ int ok;
-    if (threadIdx.x == 0) {
+    if (threadIdx.x < 64) {
+        const int i = threadIdx.x;
+        const unsigned n = i < BAR_LINES ? bar_count(nslot, slot, i) : 0u;
+        const unsigned* line = sbar + BAR_PITCH * (i < BAR_LINES ? i : 0);
         int good = 1;
         const long long t0 = wall_clock64();
-        unsigned v;
-        while ((v = __hip_atomic_load(bar, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) < target) {
-            if (__hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) { good = 0; break; }
+        unsigned v = 0;
+        for (;;) {
+            v = n ? __hip_atomic_load(line, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
+            const int e = i == 0 ? __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0;
+            if (__builtin_amdgcn_ballot_w64(n != 0 && v < steps * n) == 0) break;
+            if (__builtin_amdgcn_ballot_w64(e != 0) != 0) { good = 0; break; }
             if (wall_clock64() - t0 > timeout) {
-                __hip_atomic_fetch_or(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if (i == 0) __hip_atomic_fetch_or(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 good = 0;
                 break;
             }
         }
-        // acquire: invalidate this CU's L1 and the XCD's L2 (no writeback), so
-        // the plain loads that follow fetch what other workgroups published
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-        ok = good;
-        if (seen) *seen = v;
+        if (seen) {
+            unsigned c = n ? v / n : 0xffffffffu;
+#pragma unroll
+            for (int o = 32; o; o >>= 1) c = min(c, (unsigned)__shfl_xor((int)c, o));
+            if (i == 0) *seen = c;
+        }
+        if (i == 0) {
+            // acquire: invalidate this CU's L1 and the XCD's L2 (no writeback),
+            // so the plain loads that follow fetch what other workgroups published
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+            ok = good;
+        }
     }
     __syncthreads();
     return ok != 0;
@@ -79,10 +105,10 @@ __device__ __forceinline__ bool grid_wait(unsigned* bar, unsigned target, int* e
 __device__ __forceinline__ void grid_exit(unsigned* bar, int nslots, int* err) {
     __syncthreads();
     if (threadIdx.x == 0) {
-        unsigned* ex = bar + BAR_PITCH * BAR_EXIT;
+        unsigned* ex = slot_bar(bar, BAR_EXIT);
         const unsigned tk = __hip_atomic_fetch_add(ex, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
         if (tk == gridDim.x - 1) {
-            for (int i = 0; i < nslots; ++i)
+            for (int i = 0; i < nslots * BAR_LINES; ++i)
                 __hip_atomic_store(bar + BAR_PITCH * i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             __hip_atomic_store(err, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             __hip_atomic_store(ex, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -198,13 +224,13 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
     const int u0 = tile * UPW, m0 = mg * MG;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int g8 = 8 * (lane >> 4);
-    unsigned* bar = a.bar + BAR_PITCH * d;
+    unsigned* bar = slot_bar(a.bar, d);
     // the slot this one depends on: a slot forming an input product, the
     // layer below (step s needs its counter at (s+2)*nslot: it also arrives
     // once before its first step); a layer fed by a worker, that worker
     // ((s+1)*nslot)
-    unsigned* bar_dep = D.dep >= 0 ? a.bar + BAR_PITCH * D.dep : nullptr;
-    __shared__ unsigned dep_seen;                 // last value of that counter read
+    unsigned* bar_dep = D.dep >= 0 ? slot_bar(a.bar, D.dep) : nullptr;
+    __shared__ unsigned dep_seen;                 // steps of that slot last seen complete
     unsigned seen_dep = 0;                        // its copy in every thread
     const bool worker = D.role == 1;
     const bool has_x = D.Win != nullptr;          // forms an input product (a worker, or a layer itself)
@@ -435,8 +461,8 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
     f32x4_t accx[MT][NT];
     auto x_product = [&](int s) -> bool {
         commit_kidx_x();
-        if (seen_dep < (unsigned)(s + 2) * (unsigned)nslot) {
-            if (!grid_wait(bar_dep, (unsigned)(s + 2) * (unsigned)nslot, a.err, a.timeout, &dep_seen)) return false;
+        if (seen_dep < (unsigned)(s + 2)) {
+            if (!grid_wait(bar_dep, D.dep, nslot, (unsigned)(s + 2), a.err, a.timeout, &dep_seen)) return false;
             seen_dep = dep_seen;
         } else {
             __syncthreads();                    // the keep list just committed
@@ -522,8 +548,8 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
         // the loads overlap the wait below), then h_{t-1} of every workgroup
         // of this slot
         if (fed) {
-            if (seen_dep < (unsigned)(s + 1) * (unsigned)nslot) {
-                if (!grid_wait(bar_dep, (unsigned)(s + 1) * (unsigned)nslot, a.err, a.timeout, &dep_seen)) break;
+            if (seen_dep < (unsigned)(s + 1)) {
+                if (!grid_wait(bar_dep, D.dep, nslot, (unsigned)(s + 1), a.err, a.timeout, &dep_seen)) break;
                 seen_dep = dep_seen;
             }
             load_gx(t);
@@ -537,7 +563,7 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
             __syncthreads();                    // the keep list just committed
             gather_b(0, cnt, kidx, Ut, HP, H, bh);
         }
-        if (!grid_wait(bar, (unsigned)(s + 1) * (unsigned)nslot, a.err, a.timeout)) break;
+        if (!grid_wait(bar, d, nslot, (unsigned)(s + 1), a.err, a.timeout)) break;
         f32x4_t acc[MT][NT];
 #pragma unroll
         for (int i = 0; i < MT; ++i)
@@ -656,7 +682,7 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
     const int u0 = tile * UB, m0 = mg * MG;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int g8 = 8 * (lane >> 4);
-    unsigned* bar = a.bar + BAR_PITCH * d;
+    unsigned* bar = slot_bar(a.bar, d);
     const bool worker = D.role == 1;
 
     // rows of U (a worker: of the input weights of the layer above) for the
@@ -781,13 +807,13 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
         // dx_t of the layer above restricted to this tile's inputs, for every
         // t in that layer's order, as soon as its DA_t is published
         const PBwdDir& S = a.d[D.src];
-        unsigned* bar_src = a.bar + BAR_PITCH * D.src;
+        unsigned* bar_src = slot_bar(a.bar, D.src);
         for (int s = 0; s < T_; ++s) {
             const int t = step_t(s);
             int mk[PPT];
 #pragma unroll
             for (int q = 0; q < PPT; ++q) mk[q] = D.nr_up.mask[(size_t)t * D.nr_up.kmax + min(pu[q], H - 1)];
-            if (!grid_wait(bar_src, (unsigned)(s + 1) * (unsigned)nslot, a.err, a.timeout)) break;
+            if (!grid_wait(bar_src, D.src, nslot, (unsigned)(s + 1), a.err, a.timeout)) break;
             recurrent_product(t, S.da);
 #pragma unroll
             for (int q = 0; q < PPT; ++q) {
@@ -803,13 +829,13 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
         return;
     }
 
-    unsigned* bar_above = D.above >= 0 ? a.bar + BAR_PITCH * D.above : nullptr;
-    __shared__ unsigned above_seen;               // last value of the worker's counter read
+    unsigned* bar_above = D.above >= 0 ? slot_bar(a.bar, D.above) : nullptr;
+    __shared__ unsigned above_seen;               // steps of the worker last seen complete
     unsigned seen_above = 0;                      // its copy in every thread (uniform waits)
     // wait until the worker has formed dx of step s (usually already seen)
     auto wait_above = [&](int s) {
-        if (bar_above && seen_above < (unsigned)(s + 1) * (unsigned)nslot) {
-            if (!grid_wait(bar_above, (unsigned)(s + 1) * (unsigned)nslot, a.err, a.timeout, &above_seen))
+        if (bar_above && seen_above < (unsigned)(s + 1)) {
+            if (!grid_wait(bar_above, D.above, nslot, (unsigned)(s + 1), a.err, a.timeout, &above_seen))
                 return false;
             seen_above = above_seen;
         }
@@ -824,7 +850,7 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
         bool kept = false;
         if (has_next) {
             kept = tile_any_kept();
-            if (!grid_wait(bar, (unsigned)s * (unsigned)nslot, a.err, a.timeout)) break;
+            if (!grid_wait(bar, d, nslot, (unsigned)s, a.err, a.timeout)) break;
         }
         if (!final_pass) {
             if (!wait_above(s)) break;
