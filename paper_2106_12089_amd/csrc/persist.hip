@@ -70,15 +70,20 @@ __device__ __forceinline__ bool grid_wait(unsigned* sbar, int slot, int nslot, u
         int good = 1;
         const long long t0 = wall_clock64();
         unsigned v = 0;
+        // (the error flag is read only once a wait has taken a while: a load
+        // of it in every poll made the barrier 0.2 us slower)
         for (;;) {
             v = n ? __hip_atomic_load(line, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
-            const int e = i == 0 ? __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0;
             if (__builtin_amdgcn_ballot_w64(n != 0 && v < steps * n) == 0) break;
-            if (__builtin_amdgcn_ballot_w64(e != 0) != 0) { good = 0; break; }
-            if (wall_clock64() - t0 > timeout) {
+            const long long el = wall_clock64() - t0;
+            if (el > timeout) {
                 if (i == 0) __hip_atomic_fetch_or(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 good = 0;
                 break;
+            }
+            if (el > (timeout >> 12)) {
+                const int e = i == 0 ? __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0;
+                if (__builtin_amdgcn_ballot_w64(e != 0) != 0) { good = 0; break; }
             }
         }
         if (seen) {
