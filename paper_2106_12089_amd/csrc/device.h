@@ -93,11 +93,16 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* base, uin
 // 8 consecutive elements of one operand row as packed dwords
 template <typename T> struct Raw8 { static constexpr int NW = 4 * (int)sizeof(T) / 2; uint32_t w[NW]; };
 
-template <typename T>
+// cache-policy bits of a buffer load: SC1 makes it device-coherent (it reads
+// at the device's coherence point, past the per-XCD L2, whatever the caches
+// hold), the form of an agent-scope atomic load
+constexpr int CPOL_SC1 = 16;
+
+template <typename T, int CPOL = 0>
 __device__ __forceinline__ void raw_load(Raw8<T>& f, __amdgpu_buffer_rsrc_t r, uint32_t off) {
 #pragma unroll
     for (int q = 0; q < Raw8<T>::NW / 4; ++q) {
-        const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, off + 16 * q, 0, 0);
+        const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, off + 16 * q, 0, CPOL);
 #pragma unroll
         for (int e = 0; e < 4; ++e) f.w[4 * q + e] = v[e];
     }

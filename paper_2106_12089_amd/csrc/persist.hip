@@ -24,16 +24,17 @@ namespace lsd {
 // Cross-workgroup exchange and grid barrier.
 //
 // Values that other workgroups read during the same launch (the compacted
-// h_t, the backward DA_t) are written with relaxed agent-scope atomic stores
-// (ordinary stores carrying the device-coherence bit, written through to the
-// coherent level), so a producer never writes back its L2.  A consumer
-// performs one agent-scope acquire fence after the barrier (an invalidate of
-// its caches) and then reads with plain wide loads at full cache bandwidth.  A workgroup signals the end of a step by waiting for its own
-// stores to complete, synchronising its threads and adding 1 to the
-// direction's counter; a waiting workgroup spins (thread 0) until the counter
-// reaches the target.  The spin is bounded by wall-clock time; on time-out,
-// or when another workgroup has timed out, it reports failure and the kernel
-// ends (outputs are then poisoned with NaN).
+// h_t, x_t and gx_t of the forward stack, the backward DA_t and dx_t) are
+// written with relaxed agent-scope atomic stores (ordinary stores carrying
+// the device-coherence bit, written through to the coherent level), so a
+// producer never writes back its L2, and read with device-coherent loads
+// (16-byte buffer loads with the SC1 bit, the form of an agent-scope atomic
+// load), so a consumer needs no cache invalidation.  A workgroup signals the
+// end of a step by waiting for its own stores to complete, synchronising its
+// threads and adding 1 to its slot's counter; a waiting workgroup spins (one
+// wave) until the counter shows the step complete.  The spin is bounded by
+// wall-clock time; on time-out, or when another workgroup has timed out, it
+// reports failure and the kernel ends (outputs are then poisoned with NaN).
 // A slot's counter is split over BAR_LINES cache lines (workgroup j adds to
 // line j % BAR_LINES, lanes of the waiting wave poll one line each): the
 // atomic adds of one line are serialised, and with one line per slot a step
@@ -92,13 +93,12 @@ __device__ __forceinline__ bool grid_wait(unsigned* sbar, int slot, int nslot, u
             for (int o = 32; o; o >>= 1) c = min(c, (unsigned)__shfl_xor((int)c, o));
             if (i == 0) *seen = c;
         }
-        if (i == 0) {
-            // acquire: invalidate this CU's L1 and the XCD's L2 (no writeback),
-            // so the plain loads that follow fetch what other workgroups published
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-            ok = good;
-        }
+        if (i == 0) ok = good;
     }
+    // every read of what other workgroups of this launch published is a
+    // device-coherent load (SC1), issued after this point: no cache needs
+    // invalidating (an agent-scope acquire would invalidate the XCD's L2 from
+    // every workgroup, which cost up to 0.9 us per barrier at 123 workgroups)
     __syncthreads();
     return ok != 0;
 }
@@ -145,6 +145,11 @@ __device__ __forceinline__ void xload8(const float* p, float* o) {
         o[2 * h] = __uint_as_float((uint32_t)v);
         o[2 * h + 1] = __uint_as_float((uint32_t)(v >> 32));
     }
+}
+
+// coherent load of one float
+__device__ __forceinline__ float xload1(const float* p) {
+    return __uint_as_float(__hip_atomic_load((const uint32_t*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
 }
 
 // coherent load of 4 consecutive elements (8-byte aligned bf16 / 16-byte f32)
@@ -290,8 +295,10 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
 #pragma unroll
         for (int q = 0; q < PPT; ++q) {
             const int bc = min(pb[q], B - 1), uc = min(pu[q], H - 1);
+            const float* p = D.gx + ((size_t)t * B + bc) * G + uc;
 #pragma unroll
-            for (int g = 0; g < 4; ++g) gxr[q][g] = D.gx[((size_t)t * B + bc) * G + g * H + uc];
+            for (int g = 0; g < 4; ++g)         // (a fed layer's come from its worker in this launch)
+                gxr[q][g] = fed ? xload1(p + g * H) : p[g * H];
         }
     };
     auto prefetch = [&](int s) {                  // s may be T_ (after the last step): clamped
@@ -358,7 +365,7 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
             const int c = c0 + w + NW * i;
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt)
-                raw_load(fa[i][mt], hr, m0 + 16 * mt + (lane & 15) < B ? (uint32_t)(frag_lane_off(c, m0 / 16 + mt, lane, a.mtiles) * sizeof(T)) : OOB_OFF);
+                raw_load<T, CPOL_SC1>(fa[i][mt], hr, m0 + 16 * mt + (lane & 15) < B ? (uint32_t)(frag_lane_off(c, m0 / 16 + mt, lane, a.mtiles) * sizeof(T)) : OOB_OFF);
         }
     };
     // B fragments (weight-slice rows of the keep list) of round c0, from LDS
@@ -744,7 +751,7 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
     auto fetch_dx = [&](int t) {
         if (D.dxw) {
 #pragma unroll
-            for (int q = 0; q < PPT; ++q) dxv[q] = D.dxw[((size_t)t * B + min(pb[q], B - 1)) * H + min(pu[q], H - 1)];
+            for (int q = 0; q < PPT; ++q) dxv[q] = xload1(D.dxw + ((size_t)t * B + min(pb[q], B - 1)) * H + min(pu[q], H - 1));
             return;
         }
         if (D.dy || !D.dxc) return;
@@ -783,7 +790,7 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
 #pragma unroll
             for (int i = 0; i < MAXC; ++i) {
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt) raw_load(fa[i][mt], dr, lofs[mt] + (uint32_t)(c0 + w + NW * i) * cbytes);
+                for (int mt = 0; mt < MT; ++mt) raw_load<T, CPOL_SC1>(fa[i][mt], dr, lofs[mt] + (uint32_t)(c0 + w + NW * i) * cbytes);
             }
 #pragma unroll
             for (int i = 0; i < MAXC; ++i) {
