@@ -208,6 +208,7 @@ __host__ __device__ inline int fwd_hp(int K) { return (K + 31) / 32 * 32 + 8; }
 // the next.
 constexpr int BAR_PITCH = 64;
 constexpr int BAR_LINES = 16;
+static_assert((BAR_LINES & (BAR_LINES - 1)) == 0 && BAR_LINES <= 32, "counter lines: a power of 2, two slots per wave");
 constexpr int BAR_EXIT = 8;
 constexpr int SYNC_ERR_OFS = BAR_PITCH * 4 * (BAR_LINES * BAR_EXIT + 1);   // bytes
 constexpr int SYNC_BYTES = SYNC_ERR_OFS + 256;

@@ -58,16 +58,23 @@ __device__ __forceinline__ void grid_arrive(unsigned* sbar) {
 }
 
 // Wait until slot `slot` (counter lines at sbar) has completed `steps`
-// steps.  Returns false on time-out or when another workgroup has timed out
-// (err set).  With seen (LDS), also records the number of steps the lines
-// read last show as complete.
+// steps, and, with sbar2, slot `slot2` has completed `steps2` (lanes 0-15
+// poll the first slot's lines, lanes 16-31 the second's, in the same loop:
+// no extra round trip).  Returns false on time-out or when another workgroup
+// has timed out (err set).  With seen / seen2 (LDS), also records the number
+// of steps the lines read last show as complete.
 __device__ __forceinline__ bool grid_wait(unsigned* sbar, int slot, int nslot, unsigned steps, int* err,
-                                          long long timeout, unsigned* seen = nullptr) {
+                                          long long timeout, unsigned* seen = nullptr, unsigned* sbar2 = nullptr,
+                                          int slot2 = 0, unsigned steps2 = 0, unsigned* seen2 = nullptr) {
     __shared__ int ok;
     if (threadIdx.x < 64) {
         const int i = threadIdx.x;
-        const unsigned n = i < BAR_LINES ? bar_count(nslot, slot, i) : 0u;
-        const unsigned* line = sbar + BAR_PITCH * (i < BAR_LINES ? i : 0);
+        const bool second = i >= BAR_LINES;
+        const int li = i & (BAR_LINES - 1);
+        const unsigned n = i < BAR_LINES ? bar_count(nslot, slot, li)
+                         : (i < 2 * BAR_LINES && sbar2) ? bar_count(nslot, slot2, li) : 0u;
+        const unsigned* line = (second && sbar2 ? sbar2 : sbar) + BAR_PITCH * li;
+        const unsigned want = (second ? steps2 : steps) * n;
         int good = 1;
         const long long t0 = wall_clock64();
         unsigned v = 0;
@@ -75,7 +82,7 @@ __device__ __forceinline__ bool grid_wait(unsigned* sbar, int slot, int nslot, u
         // of it in every poll made the barrier 0.2 us slower)
         for (;;) {
             v = n ? __hip_atomic_load(line, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
-            if (__builtin_amdgcn_ballot_w64(n != 0 && v < steps * n) == 0) break;
+            if (__builtin_amdgcn_ballot_w64(n != 0 && v < want) == 0) break;
             const long long el = wall_clock64() - t0;
             if (el > timeout) {
                 if (i == 0) __hip_atomic_fetch_or(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -87,11 +94,13 @@ __device__ __forceinline__ bool grid_wait(unsigned* sbar, int slot, int nslot, u
                 if (__builtin_amdgcn_ballot_w64(e != 0) != 0) { good = 0; break; }
             }
         }
-        if (seen) {
+        if (seen || seen2) {
+            // steps complete per lane; the minimum over each half of the wave
             unsigned c = n ? v / n : 0xffffffffu;
 #pragma unroll
-            for (int o = 32; o; o >>= 1) c = min(c, (unsigned)__shfl_xor((int)c, o));
-            if (i == 0) *seen = c;
+            for (int o = 8; o; o >>= 1) c = min(c, (unsigned)__shfl_xor((int)c, o));
+            if (seen && i == 0) *seen = c;
+            if (seen2 && i == BAR_LINES) *seen2 = c;
         }
         if (i == 0) ok = good;
     }
@@ -556,16 +565,7 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
     const bool x_ok = !has_x || x_product(0);
     for (int s = 0; s < T_ && x_ok; ++s) {
         const int t = step_t(s);
-        // ---- the input product of t (a layer with a worker: once published;
-        // the loads overlap the wait below), then h_{t-1} of every workgroup
-        // of this slot
-        if (fed) {
-            if (seen_dep < (unsigned)(s + 1)) {
-                if (!grid_wait(bar_dep, D.dep, nslot, (unsigned)(s + 1), a.err, a.timeout, &dep_seen)) break;
-                seen_dep = dep_seen;
-            }
-            load_gx(t);
-        }
+        // ---- this step's keep list
         commit_kidx();
         // when the contraction takes one round, its B fragments (U rows
         // through this step's keep list) are read from LDS before the wait
@@ -575,7 +575,14 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
             __syncthreads();                    // the keep list just committed
             gather_b(0, cnt, kidx, Ut, HP, H, bh);
         }
-        if (!grid_wait(bar, d, nslot, (unsigned)(s + 1), a.err, a.timeout)) break;
+        // h_{t-1} of every workgroup of this slot, and (a fed layer) the input
+        // product of t, whose loads then overlap the product below
+        const bool need_dep = fed && seen_dep < (unsigned)(s + 1);
+        if (!grid_wait(bar, d, nslot, (unsigned)(s + 1), a.err, a.timeout, nullptr, need_dep ? bar_dep : nullptr,
+                       D.dep, (unsigned)(s + 1), &dep_seen))
+            break;
+        if (need_dep) seen_dep = dep_seen;
+        if (fed) load_gx(t);
         f32x4_t acc[MT][NT];
 #pragma unroll
         for (int i = 0; i < MT; ++i)
@@ -844,30 +851,24 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
     unsigned* bar_above = D.above >= 0 ? slot_bar(a.bar, D.above) : nullptr;
     __shared__ unsigned above_seen;               // steps of the worker last seen complete
     unsigned seen_above = 0;                      // its copy in every thread (uniform waits)
-    // wait until the worker has formed dx of step s (usually already seen)
-    auto wait_above = [&](int s) {
-        if (bar_above && seen_above < (unsigned)(s + 1)) {
-            if (!grid_wait(bar_above, D.above, nslot, (unsigned)(s + 1), a.err, a.timeout, &above_seen))
-                return false;
-            seen_above = above_seen;
-        }
-        return true;
-    };
     prefetch(0);
     for (int s = 0; s <= T_; ++s) {
         const bool final_pass = s == T_;
         const int t = final_pass ? -1 : step_t(s);
         const int tn = D.dir == 0 ? T_ - s : s - 1;        // step processed just before
         const bool has_next = s > 0;
-        bool kept = false;
-        if (has_next) {
-            kept = tile_any_kept();
-            if (!grid_wait(bar, d, nslot, (unsigned)s, a.err, a.timeout)) break;
+        // DA of the step before from every workgroup of this slot, and the
+        // worker's dx of step s (unless a count read earlier covers it), in
+        // one wait
+        const bool kept = has_next && tile_any_kept();
+        const bool need_above = !final_pass && bar_above && seen_above < (unsigned)(s + 1);
+        if (has_next || need_above) {
+            if (!grid_wait(bar, d, nslot, has_next ? (unsigned)s : 0u, a.err, a.timeout, nullptr,
+                           need_above ? bar_above : nullptr, D.above, (unsigned)(s + 1), &above_seen))
+                break;
+            if (need_above) seen_above = above_seen;
         }
-        if (!final_pass) {
-            if (!wait_above(s)) break;
-            fetch_dx(t);
-        }
+        if (!final_pass) fetch_dx(t);
         if (kept) recurrent_product(tn, D.da);
         float da4[PPT][4];
 #pragma unroll
