@@ -257,24 +257,35 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
     const int kin = D.kin;
 
     // U slice (or W slice) -> LDS, transposed: row c = nt*16 + g*4 + cu holds
-    // column g*H + u0 + 4nt + cu of the weight
+    // column g*H + u0 + 4nt + cu of the weight.  Each thread issues its loads
+    // in batches of LB from clamped (valid) addresses before storing any: a
+    // loop of load-then-store waits a full memory latency per element.
     {
-        const T* U = (const T*)D.U;
-        for (int i = tid; i < HP * NC && !worker; i += NTH) {
-            const int k = i / NC, c = i % NC;
-            const int nt = c >> 4, cc = c & 15;
-            const int u = u0 + 4 * nt + (cc & 3);
-            Ut[c * HP + k] = (u < H && k < H) ? U[(size_t)k * G + (cc >> 2) * H + u] : zero_val<T>();
-        }
-        if (has_x) {
-            const T* Wi = (const T*)D.Win;
-            for (int i = tid; i < KP * NC; i += NTH) {
-                const int k = i / NC, c = i % NC;
-                const int nt = c >> 4, cc = c & 15;
-                const int u = u0 + 4 * nt + (cc & 3);
-                Wt[c * KP + k] = (u < H && k < kin) ? Wi[(size_t)k * G + (cc >> 2) * H + u] : zero_val<T>();
+        constexpr int LB = 16;
+        auto load_slice = [&](const T* Wm, int rows, int krows, T* dst, int pitch) {
+            const int total = pitch * NC;
+            for (int i0 = tid; i0 < total; i0 += NTH * LB) {
+                T v[LB];
+#pragma unroll
+                for (int j = 0; j < LB; ++j) {
+                    const int i = min(i0 + NTH * j, total - 1);
+                    const int k = i / NC, c = i % NC;
+                    const int u = u0 + 4 * (c >> 4) + (c & 3);
+                    v[j] = Wm[(size_t)min(k, krows - 1) * G + ((c & 15) >> 2) * H + min(u, H - 1)];
+                }
+#pragma unroll
+                for (int j = 0; j < LB; ++j) {
+                    const int i = i0 + NTH * j;
+                    if (i < total) {
+                        const int k = i / NC, c = i % NC;
+                        const int u = u0 + 4 * (c >> 4) + (c & 3);
+                        dst[c * pitch + k] = (u < H && k < rows) ? v[j] : zero_val<T>();
+                    }
+                }
             }
-        }
+        };
+        if (!worker) load_slice((const T*)D.U, H, H, Ut, HP);
+        if (has_x) load_slice((const T*)D.Win, kin, kin, Wt, KP);
     }
     // register state of this thread's (row, unit) pairs
     float creg[PPT], hreg[PPT], biasr[PPT][4];
@@ -706,12 +717,28 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
 
     // rows of U (a worker: of the input weights of the layer above) for the
     // tile's units -> LDS (zero past 4H and past H)
+    // (each thread issues its loads in batches before storing any: a loop
+    // of load-then-store waits a full memory latency per element)
     {
+        constexpr int LB = 16;
         const T* U = (const T*)(worker ? D.Wup : D.U);
-        for (int i = tid; i < UB * GP; i += NTH) {
-            const int r = i / GP, n = i % GP;
-            const int u = u0 + r;
-            Ur[i] = (u < H && n < G) ? U[(size_t)u * G + n] : zero_val<T>();
+        const int total = UB * GP;
+        for (int i0 = tid; i0 < total; i0 += NTH * LB) {
+            T v[LB];
+#pragma unroll
+            for (int j = 0; j < LB; ++j) {
+                const int i = min(i0 + NTH * j, total - 1);
+                const int r = i / GP, n = i % GP;
+                v[j] = U[(size_t)min(u0 + r, H - 1) * G + min(n, G - 1)];
+            }
+#pragma unroll
+            for (int j = 0; j < LB; ++j) {
+                const int i = i0 + NTH * j;
+                if (i < total) {
+                    const int r = i / GP, n = i % GP;
+                    Ur[i] = (u0 + r < H && n < G) ? v[j] : zero_val<T>();
+                }
+            }
         }
     }
     // this thread's (row, unit) pairs and their carries
