@@ -23,7 +23,6 @@ template <typename T> void launch_step(const StepArgs& a, int D, hipStream_t st)
 template <typename T> void launch_bwd(const BwdArgs& a, int D, hipStream_t st);
 template <typename T> void launch_dx(const DxArgs& a, int K, hipStream_t st);
 template <typename T> void launch_wgrad(const WgBatch& b, hipStream_t st);
-template <typename T> void launch_fwd_init(const void*, const float*, float*, float*, long, unsigned*, int*, hipStream_t);
 void launch_bwd_init(const float*, const float*, float*, float*, long, void*, int, int, int, long, long, unsigned*, int*,
                      hipStream_t);
 void launch_mse(const float*, const float*, const int32_t*, float*, float*, int, float*, int, int, int,
@@ -238,12 +237,14 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
     const size_t es = P.esize;
     char* R = (char*)reserve;
     char* W = (char*)ws;
-    launch_fwd_init<E>(h0, c0, hT, cT, (long)L * D * B * H, (unsigned*)(W + P.w_sync), (int*)(W + P.w_sync + SYNC_ERR_OFS),
-                       st);
-    {   // x (T matrices) and h0 (L*D matrices), transposed in one launch
+    {   // x (T matrices) and h0 (L*D matrices) transposed, and the pass
+        // initialised (hT, cT, barrier counters), in one launch
         TransArgs t;
+        memset(&t, 0, sizeof(t));
         t.src = x; t.dst = R + P.r_xT; t.B = B; t.K = P.I; t.BP = BP; t.n1 = T;
         t.src2 = h0; t.dst2 = R + P.r_h0T; t.K2 = H;
+        t.h0 = h0; t.c0 = c0; t.hT = hT; t.cT = cT; t.n_init = (long)L * D * B * H;
+        t.bar = (unsigned*)(W + P.w_sync); t.err = (int*)(W + P.w_sync + SYNC_ERR_OFS);
         launch_transpose<E>(t, T + L * D, st);
     }
     // Unidirectional stack: every layer's recurrence in one persistent

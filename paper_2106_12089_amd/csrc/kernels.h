@@ -47,6 +47,14 @@ struct TransArgs {
     const void* src2;                   // second job (K2 columns), or unused when every matrix is the first job's
     void* dst2;
     int K2;
+    // with n_init > 0, one more grid slice initialises the forward pass:
+    // hT <- h0 (as float), cT <- c0 (n_init elements), barrier counters <- 0
+    const void* h0;
+    const float* c0;
+    float *hT, *cT;
+    long n_init;
+    unsigned* bar;
+    int* err;
 };
 
 // Forward input product of one layer/direction, all t in one launch:

@@ -141,11 +141,25 @@ __global__ void __launch_bounds__(256) k_mask_build(MaskArgs a) {
 
 // ---------------------------------------------------------------------------
 // src [N][B][K] -> dst [N][K][BP], zero rows b in [B, BP); two such jobs
-// (matrices z < n1 from the first, the others from the second) in one launch.
-// grid (ceil(max K/32), BP/32, N), block (32, 8).
+// (matrices z < n1 from the first, the others from the second) in one launch,
+// and, with n_init > 0, the forward pass's initialisation in slice z = N.
+// grid (ceil(max K/32), BP/32, N (+1)), block (32, 8).
 template <typename T>
-__global__ void __launch_bounds__(256) k_transpose(TransArgs a) {
+__global__ void __launch_bounds__(256) k_transpose(TransArgs a, int N) {
     __shared__ T tile[32][33];
+    if ((int)blockIdx.z == N) {
+        const int tid = threadIdx.y * 32 + threadIdx.x;
+        const long nb = (long)gridDim.x * gridDim.y, bi = (long)blockIdx.y * gridDim.x + blockIdx.x;
+        if (bi == 0) {
+            for (int i = tid; i <= BAR_LINES * BAR_EXIT; i += 256) a.bar[BAR_PITCH * i] = 0u;
+            if (tid == 0) *a.err = 0;
+        }
+        for (long i = bi * 256 + tid; i < a.n_init; i += nb * 256) {
+            a.hT[i] = to_f32<T>(((const T*)a.h0)[i]);
+            a.cT[i] = a.c0[i];
+        }
+        return;
+    }
     const bool second = (int)blockIdx.z >= a.n1;
     const int n = second ? blockIdx.z - a.n1 : blockIdx.z, K = second ? a.K2 : a.K;
     const int k0 = blockIdx.x * 32, b0 = blockIdx.y * 32;
@@ -1104,15 +1118,6 @@ __device__ __forceinline__ void clear_sync(unsigned* bar, int* err) {
     }
 }
 
-// hT <- h0 (as float), cT <- c0; the barrier counters <- 0
-template <typename T>
-__global__ void k_fwd_init(const T* h0, const float* c0, float* hT, float* cT, long n, unsigned* bar, int* err) {
-    clear_sync(bar, err);
-    for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < n; i += (long)gridDim.x * blockDim.x) {
-        hT[i] = to_f32<T>(h0[i]);
-        cT[i] = c0[i];
-    }
-}
 
 // carries <- dhT/dcT slices (or zero)
 // and, when da is given, zero the columns 4H .. (last 32-column chunk end)
@@ -1277,7 +1282,8 @@ void launch_mask_build(const MaskArgs& a, int sites, hipStream_t st) {
 template <typename T>
 void launch_transpose(const TransArgs& a, int N, hipStream_t st) {
     const int K = N > a.n1 && a.K2 > a.K ? a.K2 : a.K;
-    launch_k(KID_TRANS, k_transpose<T>, dim3((K + 31) / 32, a.BP / 32, N), dim3(32, 8), 0, st, a);
+    launch_k(KID_TRANS, k_transpose<T>, dim3((K + 31) / 32, a.BP / 32, N + (a.n_init > 0 ? 1 : 0)), dim3(32, 8), 0, st,
+             a, N);
 }
 template <typename T>
 void launch_fx(const FxArgs& a, hipStream_t st) {
@@ -1328,11 +1334,6 @@ void launch_wgrad(const WgBatch& b, hipStream_t st) {
         else launch_k(KID_WGRAD, k_wgrad<T, false, false>, grid, blk, lds, st, b);
     }
 }
-template <typename T>
-void launch_fwd_init(const void* h0, const float* c0, float* hT, float* cT, long n, unsigned* bar, int* err,
-                     hipStream_t st) {
-    launch_k(KID_NONE, k_fwd_init<T>, dim3(nblk(n, 256)), dim3(256), 0, st, (const T*)h0, c0, hT, cT, n, bar, err);
-}
 void launch_bwd_init(const float* dhT, const float* dcT, float* dhc, float* dcs, long n, void* da, int es, int G,
                      int mtiles, long nblocks, long das, unsigned* bar, int* err, hipStream_t st) {
     const long np = da ? nblocks * 16 * mtiles * 32 : 0;      // upper bound of the DA padding entries
@@ -1366,7 +1367,7 @@ int setup_kernel_attributes() {
     template void launch_bwd<T>(const BwdArgs&, int, hipStream_t);                          \
     template void launch_dx<T>(const DxArgs&, int, hipStream_t);                            \
     template void launch_wgrad<T>(const WgBatch&, hipStream_t);                             \
-    template void launch_fwd_init<T>(const void*, const float*, float*, float*, long, unsigned*, int*, hipStream_t);
+
 LSD_INST(float)
 LSD_INST(bf16)
 
