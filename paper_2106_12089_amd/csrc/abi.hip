@@ -17,7 +17,6 @@
 namespace lsd {
 
 void launch_mask_build(const MaskArgs& a, int sites, hipStream_t st);
-template <typename T> void launch_transpose(const TransArgs& a, int N, hipStream_t st);
 template <typename T> void launch_fx(const FxArgs& a, hipStream_t st);
 template <typename T> void launch_step(const StepArgs& a, int D, hipStream_t st);
 template <typename T> void launch_bwd(const BwdArgs& a, int D, hipStream_t st);
@@ -237,16 +236,25 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
     const size_t es = P.esize;
     char* R = (char*)reserve;
     char* W = (char*)ws;
-    {   // x (T matrices) and h0 (L*D matrices) transposed, and the pass
-        // initialised (hT, cT, barrier counters), in one launch
-        TransArgs t;
-        memset(&t, 0, sizeof(t));
-        t.src = x; t.dst = R + P.r_xT; t.B = B; t.K = P.I; t.BP = BP; t.n1 = T;
-        t.src2 = h0; t.dst2 = R + P.r_h0T; t.K2 = H;
-        t.h0 = h0; t.c0 = c0; t.hT = hT; t.cT = cT; t.n_init = (long)L * D * B * H;
-        t.bar = (unsigned*)(W + P.w_sync); t.err = (int*)(W + P.w_sync + SYNC_ERR_OFS);
-        launch_transpose<E>(t, T + L * D, st);
-    }
+    // x (T matrices) and h0 (L*D matrices) transposed, and the pass
+    // initialised (hT, cT, barrier counters): these ride on the first input
+    // product launch (independent work, one launch less)
+    TransArgs tr;
+    memset(&tr, 0, sizeof(tr));
+    tr.src = x; tr.dst = R + P.r_xT; tr.B = B; tr.K = P.I; tr.BP = BP; tr.n1 = T;
+    tr.src2 = h0; tr.dst2 = R + P.r_h0T; tr.K2 = H;
+    tr.h0 = h0; tr.c0 = c0; tr.hT = hT; tr.cT = cT; tr.n_init = (long)L * D * B * H;
+    tr.bar = (unsigned*)(W + P.w_sync); tr.err = (int*)(W + P.w_sync + SYNC_ERR_OFS);
+    bool tr_pending = true;
+    auto attach_tr = [&](FxArgs& f) {
+        if (!tr_pending) return;
+        f.tr = tr;
+        f.trN = T + L * D;
+        f.tr_gx = ((P.I > H ? P.I : H) + 31) / 32;
+        f.tr_gy = BP / 32;
+        f.tr_gz = T + L * D + 1;
+        tr_pending = false;
+    };
     // Unidirectional stack: every layer's recurrence in one persistent
     // launch, layer l one step behind layer l-1, each layer above the first
     // computing its input product from what the layer below published.
@@ -289,12 +297,14 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
         const void* X = l == 0 ? x : (const void*)(R + P.rybuf(l - 1));
         for (int d = 0; d < D; ++d) {
             FxArgs f;
+            memset(&f, 0, sizeof(f));
             f.X = X; f.ldx = kin;
             f.W = w->W[l * D + d];
             f.bias = w->b[l * D + d];
             f.site = site_view(P, mbuf, P.site_nr(l));
             f.Gx = (float*)(W + P.w_gx) + (size_t)d * T * B * G;
             f.K = kin; f.B = B; f.G = G; f.T = T; f.dense = !P.compact; f.s = P.s_nr;
+            attach_tr(f);
             launch_fx<E>(f, st);
         }
     };
@@ -351,12 +361,14 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
         const void* X = l == 0 ? x : (const void*)(R + P.rybuf(l - 1));
         for (int d = 0; d < D; ++d) {
             FxArgs f;
+            memset(&f, 0, sizeof(f));
             f.X = X; f.ldx = kin;
             f.W = w->W[l * D + d];
             f.bias = w->b[l * D + d];
             f.site = site_view(P, mbuf, P.site_nr(l));
             f.Gx = (float*)(W + P.w_gx) + (size_t)d * T * B * G;
             f.K = kin; f.B = B; f.G = G; f.T = T; f.dense = !P.compact; f.s = P.s_nr;
+            attach_tr(f);
             launch_fx<E>(f, st);
         }
         if (use_persistent()) {

@@ -68,6 +68,11 @@ struct FxArgs {
     float* Gx;                          // [T][B][G]
     int B, G, T, dense;
     float s;
+    // with tr_gz > 0, the launch also runs the transposes (and the pass
+    // initialisation) of tr, as a virtual (tr_gx, tr_gy, tr_gz) grid of
+    // workgroups past y = T; trN = its matrix count
+    TransArgs tr;
+    int trN, tr_gx, tr_gy, tr_gz;
 };
 
 // One recurrent forward step, per direction (grid.z = direction).

@@ -141,15 +141,16 @@ __global__ void __launch_bounds__(256) k_mask_build(MaskArgs a) {
 
 // ---------------------------------------------------------------------------
 // src [N][B][K] -> dst [N][K][BP], zero rows b in [B, BP); two such jobs
-// (matrices z < n1 from the first, the others from the second) in one launch,
+// (matrices z < n1 from the first, the others from the second) in one grid,
 // and, with n_init > 0, the forward pass's initialisation in slice z = N.
-// grid (ceil(max K/32), BP/32, N (+1)), block (32, 8).
+// One workgroup (256 threads) of a grid (gx = ceil(max K/32), gy = BP/32,
+// N (+1)): block (bx, by, bz).
 template <typename T>
-__global__ void __launch_bounds__(256) k_transpose(TransArgs a, int N) {
-    __shared__ T tile[32][33];
-    if ((int)blockIdx.z == N) {
-        const int tid = threadIdx.y * 32 + threadIdx.x;
-        const long nb = (long)gridDim.x * gridDim.y, bi = (long)blockIdx.y * gridDim.x + blockIdx.x;
+__device__ __forceinline__ void transpose_block(const TransArgs& a, int N, int bx, int by, int bz, int gx, int gy,
+                                                T (*tile)[33]) {
+    const int tid = threadIdx.x, tx = tid & 31, ty = tid >> 5;
+    if (bz == N) {
+        const long nb = (long)gx * gy, bi = (long)by * gx + bx;
         if (bi == 0) {
             for (int i = tid; i <= BAR_LINES * BAR_EXIT; i += 256) a.bar[BAR_PITCH * i] = 0u;
             if (tid == 0) *a.err = 0;
@@ -160,20 +161,20 @@ __global__ void __launch_bounds__(256) k_transpose(TransArgs a, int N) {
         }
         return;
     }
-    const bool second = (int)blockIdx.z >= a.n1;
-    const int n = second ? blockIdx.z - a.n1 : blockIdx.z, K = second ? a.K2 : a.K;
-    const int k0 = blockIdx.x * 32, b0 = blockIdx.y * 32;
+    const bool second = bz >= a.n1;
+    const int n = second ? bz - a.n1 : bz, K = second ? a.K2 : a.K;
+    const int k0 = bx * 32, b0 = by * 32;
     if (k0 >= K) return;                       // (the whole workgroup)
     const T* src = (const T*)(second ? a.src2 : a.src) + (size_t)n * a.B * K;
     T* dst = (T*)(second ? a.dst2 : a.dst) + (size_t)n * K * a.BP;
-    for (int i = threadIdx.y; i < 32; i += 8) {
-        const int b = b0 + i, k = k0 + threadIdx.x;
-        tile[i][threadIdx.x] = (b < a.B && k < K) ? src[(size_t)b * K + k] : zero_val<T>();
+    for (int i = ty; i < 32; i += 8) {
+        const int b = b0 + i, k = k0 + tx;
+        tile[i][tx] = (b < a.B && k < K) ? src[(size_t)b * K + k] : zero_val<T>();
     }
     __syncthreads();
-    for (int i = threadIdx.y; i < 32; i += 8) {
-        const int k = k0 + i, b = b0 + threadIdx.x;
-        if (k < K) dst[(size_t)k * a.BP + b] = tile[threadIdx.x][i];
+    for (int i = ty; i < 32; i += 8) {
+        const int k = k0 + i, b = b0 + tx;
+        if (k < K) dst[(size_t)k * a.BP + b] = tile[tx][i];
     }
 }
 
@@ -198,6 +199,14 @@ __global__ void __launch_bounds__(256) k_fx(FxArgs a) {
     __shared__ __attribute__((aligned(16))) T ws[2][FX_KC][FX_WLD];   // W chunk [k][n]
     __shared__ __attribute__((aligned(16))) T xs[2][FX_MB][FX_LD];    // X chunk [row][k]
     __shared__ int kidx[LSTM_SD_MAX_K];
+    if ((int)blockIdx.y >= a.T) {              // the transposes riding on this launch
+        const long lin = ((long)(blockIdx.y - a.T) * gridDim.z + blockIdx.z) * gridDim.x + blockIdx.x;
+        if (lin < (long)a.tr_gx * a.tr_gy * a.tr_gz) {
+            const int bx = (int)(lin % a.tr_gx), by = (int)(lin / a.tr_gx % a.tr_gy), bz = (int)(lin / ((long)a.tr_gx * a.tr_gy));
+            transpose_block<T>(a.tr, a.trN, bx, by, bz, a.tr_gx, a.tr_gy, (T(*)[33])&xs[0][0][0]);
+        }
+        return;
+    }
     const int ctile = xcd_tile(blockIdx.x, (a.G + FX_NB - 1) / FX_NB);
     if (ctile < 0) return;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -1280,14 +1289,12 @@ void launch_mask_build(const MaskArgs& a, int sites, hipStream_t st) {
     launch_k(KID_MASK, k_mask_build, dim3(a.T, sites), dim3(256), 0, st, a);
 }
 template <typename T>
-void launch_transpose(const TransArgs& a, int N, hipStream_t st) {
-    const int K = N > a.n1 && a.K2 > a.K ? a.K2 : a.K;
-    launch_k(KID_TRANS, k_transpose<T>, dim3((K + 31) / 32, a.BP / 32, N + (a.n_init > 0 ? 1 : 0)), dim3(32, 8), 0, st,
-             a, N);
-}
-template <typename T>
 void launch_fx(const FxArgs& a, hipStream_t st) {
-    const dim3 grid(xcd_grid((a.G + FX_NB - 1) / FX_NB), a.T, (a.B + FX_MB - 1) / FX_MB);
+    dim3 grid(xcd_grid((a.G + FX_NB - 1) / FX_NB), a.T, (a.B + FX_MB - 1) / FX_MB);
+    if (a.tr_gz > 0) {                         // room for the transposes past y = T
+        const long ntr = (long)a.tr_gx * a.tr_gy * a.tr_gz, per_y = (long)grid.x * grid.z;
+        grid.y += (unsigned)((ntr + per_y - 1) / per_y);
+    }
     if (a.dense) launch_k(KID_FX, k_fx<T, true>, grid, dim3(256), 0, st, a);
     else launch_k(KID_FX, k_fx<T, false>, grid, dim3(256), 0, st, a);
 }
@@ -1361,7 +1368,6 @@ int setup_kernel_attributes() {
 }
 
 #define LSD_INST(T)                                                                         \
-    template void launch_transpose<T>(const TransArgs&, int, hipStream_t);                  \
     template void launch_fx<T>(const FxArgs&, hipStream_t);                                 \
     template void launch_step<T>(const StepArgs&, int, hipStream_t);                        \
     template void launch_bwd<T>(const BwdArgs&, int, hipStream_t);                          \
