@@ -671,7 +671,8 @@ __device__ __forceinline__ void db_add_raw(const Raw8<T>& f, float& acc) {
 // every row of the step first and then write them.  Rows never kept stay
 // zero.  Every wave also sums its DA^T fragments: the bias gradient.
 constexpr int WG_NB = 128;                 // gradient columns per workgroup
-constexpr int WG_NWV = 4;                  // waves per workgroup: 32 columns (two 16-column tiles) each
+constexpr int WG_CT = 2;                   // 16-column tiles per wave (each A fragment feeds WG_CT products)
+constexpr int WG_NWV = WG_NB / (16 * WG_CT); // waves per half workgroup
 constexpr int WG_LDC = WG_NB + 4;          // LDS accumulator row pitch (floats)
 template <typename T>
 struct WgTiles { static constexpr int N = 6; };   // 16-row tiles in registers at once
@@ -700,16 +701,16 @@ __device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
     const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // (wave-uniform)
     const int col = lane & 15, g8 = 8 * (lane >> 4);
     const int rh = w / WG_NWV;                   // this wave's half of the workgroup
-    const int c0 = 32 * (w % WG_NWV);            // this wave's columns within the block: two tiles
-    const int n0 = cb * WG_NB, n = n0 + c0 + col;   // (columns n and n + 16)
+    const int c0 = 16 * WG_CT * (w % WG_NWV);    // this wave's columns within the block: WG_CT tiles
+    const int n0 = cb * WG_NB, n = n0 + c0 + col;   // (columns n + 16h)
     const int r0 = slice_start(x, a.K), r1 = slice_start(x + 1, a.K);
     const int nrow = r1 - r0;
     // the halves take the even and odd steps (each every kept row of the
     // slice), or the kept rows of the slice's two segments (each every step)
     const bool tsplit = wgrad_tsplit<T>(a.K);
     const int ts = tsplit ? 2 : 1;               // the stride of this wave's steps
-    for (int i = lane + 64 * rh; i < (tsplit ? 2 : 1) * (nrow + 1) * 32; i += 128)
-        acc_lds[(i >> 5) * WG_LDC + c0 + (i & 31)] = 0.0f;
+    for (int i = lane + 64 * rh; i < (tsplit ? 2 : 1) * (nrow + 1) * 16 * WG_CT; i += 128)
+        acc_lds[(i / (16 * WG_CT)) * WG_LDC + c0 + i % (16 * WG_CT)] = 0.0f;
     float* accr = acc_lds + (tsplit ? rh * (nrow + 1) * WG_LDC : 0);   // this half's accumulator
     // keep-list ranges of slice x at the steps t0 .. t1-1 of a window, in LDS
     // (a table in registers would make the compiler wait for all loads
@@ -719,11 +720,11 @@ __device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
     const int sb = tsplit ? 0 : rh, se = tsplit ? 2 : rh + 1;
     auto seg_b = [&](int t) { return __builtin_amdgcn_readfirstlane(segtab[sb][t - t0]); };
     auto seg_e = [&](int t) { return __builtin_amdgcn_readfirstlane(segtab[se][t - t0]); };
-    uint32_t pm0[NW], pmb[2][NW];              // batch-pad masks of chunk 0 (A side; B side adds n < G)
+    uint32_t pm0[NW], pmb[WG_CT][NW];          // batch-pad masks of chunk 0 (A side; B side adds n < G)
     pad_mask<T>(g8, a.B, pm0);
-    uint32_t boff[2];                          // DA^T fragment offsets of the two column tiles
+    uint32_t boff[WG_CT];                      // DA^T fragment offsets of the column tiles
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
+    for (int h = 0; h < WG_CT; ++h) {
 #pragma unroll
         for (int q = 0; q < NW; ++q) pmb[h][q] = n + 16 * h < a.G ? pm0[q] : 0u;
         boff[h] = (uint32_t)(min(n + 16 * h, a.G - 1) * a.BP + g8) * ES;
@@ -767,7 +768,7 @@ __device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
 #pragma unroll
         for (int i = 0; i < MAXT; ++i) raw_load(fa[i], ar, (__umul24((uint32_t)kk[i], (uint32_t)a.BP) + bc + g8) * ES);
     };
-    float dbacc[2] = {0.f, 0.f};
+    float dbacc[WG_CT] = {};
     // multiply the tiles (chunk-0 fragments already loaded) with both column
     // tiles, finish the other batch chunks, and add the tiles into their LDS
     // rows.  Tiles past nt are multiplied too (their rows are absent):
@@ -778,25 +779,25 @@ __device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
     // of its own row.
     auto finish = [&](__amdgpu_buffer_rsrc_t ar, __amdgpu_buffer_rsrc_t br, const int* kk, const int* la, int nt,
                       Raw8<T>* fa, const Raw8<T>* fb0, bool first_round) {
-        f32x4_t acc[MAXT][2];
+        f32x4_t acc[MAXT][WG_CT];
 #pragma unroll
         for (int i = 0; i < MAXT; ++i) {
             raw_and(fa[i], pm0);
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
+            for (int h = 0; h < WG_CT; ++h) {
                 acc[i][h] = f32x4_t{0, 0, 0, 0};
                 raw_mma(fb0[h], fa[i], acc[i][h]);
             }
         }
         for (int bc = 32; MULTI && bc < a.B; bc += 32) {
-            Raw8<T> fb[2];
-            raw_load(fb[0], br, boff[0] + (uint32_t)bc * ES);
-            raw_load(fb[1], br, boff[1] + (uint32_t)bc * ES);
+            Raw8<T> fb[WG_CT];
+#pragma unroll
+            for (int h = 0; h < WG_CT; ++h) raw_load(fb[h], br, boff[h] + (uint32_t)bc * ES);
             a_issue(ar, bc, kk, fa);
             uint32_t pm[NW];
             pad_mask<T>(bc + g8, a.B, pm);
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
+            for (int h = 0; h < WG_CT; ++h) {
                 raw_and(fb[h], pm);
                 if (n + 16 * h >= a.G) raw_and(fb[h], pmb[h]);   // pmb is all zero past G
                 if (first_round) db_add_raw(fb[h], dbacc[h]);
@@ -804,24 +805,24 @@ __device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
 #pragma unroll
             for (int i = 0; i < MAXT; ++i) {
                 raw_and(fa[i], pm);
-                raw_mma(fb[0], fa[i], acc[i][0]);
-                raw_mma(fb[1], fa[i], acc[i][1]);
+#pragma unroll
+                for (int h = 0; h < WG_CT; ++h) raw_mma(fb[h], fa[i], acc[i][h]);
             }
         }
         // output r of this lane is gradient column 4*(lane/16)+r of the
         // column tile, in the lane's own row
         const int cq = c0 + 4 * (lane >> 4);
-        float4 old[MAXT][2];
+        float4 old[MAXT][WG_CT];
 #pragma unroll
         for (int i = 0; i < MAXT; ++i)
             if (i < nt)
 #pragma unroll
-                for (int h = 0; h < 2; ++h) old[i][h] = *(const float4*)(accr + la[i] + cq + 16 * h);
+                for (int h = 0; h < WG_CT; ++h) old[i][h] = *(const float4*)(accr + la[i] + cq + 16 * h);
 #pragma unroll
         for (int i = 0; i < MAXT; ++i)
             if (i < nt)
 #pragma unroll
-                for (int h = 0; h < 2; ++h) {
+                for (int h = 0; h < WG_CT; ++h) {
                     float4 v = old[i][h];
                     v.x += a.s * acc[i][h][0];
                     v.y += a.s * acc[i][h][1];
@@ -845,14 +846,14 @@ __device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
         // rows, DA^T fragments and LDS row addresses of its next two steps,
         // the keep-list entries of the two after
         int kv[2][MAXT], kk[2][MAXT], la[2][MAXT];
-        Raw8<T> fa[2][MAXT], fb[2][2];
+        Raw8<T> fa[2][MAXT], fb[2][WG_CT];
         // the operands of step t into slot sl, from its keep-list entries
         auto prime = [&](int t, int sl) {
             rows_resolve(t, 0, kv[sl], kk[sl], la[sl]);
             const __amdgpu_buffer_rsrc_t br = dat_rsrc(t);
             a_issue(act_rsrc(t), 0, kk[sl], fa[sl]);
-            raw_load(fb[sl][0], br, boff[0]);
-            raw_load(fb[sl][1], br, boff[1]);
+#pragma unroll
+            for (int h = 0; h < WG_CT; ++h) raw_load(fb[sl][h], br, boff[h]);
         };
         // step t from slot sl (none past the window); then the slot takes
         // the operands of t+2ts and the keep-list entries of t+4ts.  Loads that
@@ -862,9 +863,10 @@ __device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
             if (t < t1) {
                 const __amdgpu_buffer_rsrc_t ar = act_rsrc(t), br = dat_rsrc(t);
                 const int ntile = (seg_e(t) - seg_b(t) + 15) >> 4;
-                Raw8<T> fb0[2] = {fb[sl][0], fb[sl][1]};
+                Raw8<T> fb0[WG_CT];
 #pragma unroll
-                for (int h = 0; h < 2; ++h) {
+                for (int h = 0; h < WG_CT; ++h) {
+                    fb0[h] = fb[sl][h];
                     raw_and(fb0[h], pmb[h]);
                     if (dbw) db_add_raw(fb0[h], dbacc[h]);
                 }
@@ -895,9 +897,9 @@ __device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
     }
     __syncthreads();
     if (a.db && x == 0) {                      // lanes l, l+16, l+32, l+48 hold column l (+16)
-        float v[2];
+        float v[WG_CT];
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
+        for (int h = 0; h < WG_CT; ++h) {
             v[h] = dbacc[h];
             v[h] += __shfl_xor(v[h], 16);
             v[h] += __shfl_xor(v[h], 32);
@@ -905,12 +907,12 @@ __device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
         // the odd half's sums pass through the (no longer used) spare row
         float* sp = acc_lds + nrow * WG_LDC + c0;
         if (tsplit && rh && lane < 16) {
-            sp[lane] = v[0];
-            sp[16 + lane] = v[1];
+#pragma unroll
+            for (int h = 0; h < WG_CT; ++h) sp[16 * h + lane] = v[h];
         }
         __syncthreads();
 #pragma unroll
-        for (int h = 0; h < 2; ++h)
+        for (int h = 0; h < WG_CT; ++h)
             if (!rh && lane < 16 && n + 16 * h < a.G) a.db[n + 16 * h] = tsplit ? v[h] + sp[16 * h + lane] : v[h];
     }
     float* out = a.out;
@@ -945,21 +947,21 @@ __device__ __forceinline__ void wgrad_full(const WgArgs& a, float* red) {
     const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // (wave-uniform)
     const int col = lane & 15, g8 = 8 * (lane >> 4);
     const int rh = w / WG_NWV;                 // this wave's half of the workgroup
-    const int n = cb * WG_NB + 32 * (w % WG_NWV) + col;   // columns n and n + 16
+    const int n = cb * WG_NB + 16 * WG_CT * (w % WG_NWV) + col;   // columns n + 16h
     const int r0 = slice_start(x, a.K), r1 = slice_start(x + 1, a.K);
     const bool tsplit = r1 - r0 <= 16 * NTW;   // the halves split the steps (else the tiles)
     const int t1 = a.T, tb = tsplit ? rh : 0, ts = tsplit ? 2 : 1;
-    uint32_t pm0[NW], pmb[2][NW];              // batch-pad masks (B side also zero past G)
+    uint32_t pm0[NW], pmb[WG_CT][NW];          // batch-pad masks (B side also zero past G)
     pad_mask<T>(g8, a.B, pm0);
-    uint32_t boff[2];
+    uint32_t boff[WG_CT];
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
+    for (int h = 0; h < WG_CT; ++h) {
 #pragma unroll
         for (int q = 0; q < NW; ++q) pmb[h][q] = n + 16 * h < a.G ? pm0[q] : 0u;
         boff[h] = (uint32_t)(min(n + 16 * h, a.G - 1) * a.BP + g8) * ES;
     }
     const uint32_t abytes = (uint32_t)a.K * a.BP * ES, bbytes = (uint32_t)a.G * a.BP * ES;
-    float dbacc[2] = {0.f, 0.f};
+    float dbacc[WG_CT] = {};
     const bool dbw = a.db && x == NXCD - 1;    // this workgroup sums the bias gradient
     auto act_rsrc = [&](int t) {
         const T* act = (a.actT_first && t == a.t_first) ? (const T*)a.actT_first
@@ -968,7 +970,7 @@ __device__ __forceinline__ void wgrad_full(const WgArgs& a, float* red) {
     };
     auto dat_rsrc = [&](int t) { return buf_rsrc((const T*)a.daT + (size_t)t * a.G * a.BP, bbytes); };
     // this wave's slot of the pass reduction: [tile][half][reg][lane]
-    float* mine = red + (w % WG_NWV) * (NTW * 8 * 64) + lane;
+    float* mine = red + (w % WG_NWV) * (NTW * WG_CT * 4 * 64) + lane;
 
     for (int rp = r0; rp < r1; rp += 32 * NTW) {           // passes over the slice's row tiles
         const bool first = rp == r0 && dbw;    // (the bias gradient is summed on the first pass)
@@ -976,18 +978,20 @@ __device__ __forceinline__ void wgrad_full(const WgArgs& a, float* red) {
         int rowa[NTW];                         // A-fragment row of this lane in tile i (clamped into K)
 #pragma unroll
         for (int i = 0; i < NTW; ++i) rowa[i] = min(rb + 16 * i + col, a.K - 1);
-        f32x4_t acc[NTW][2];
+        f32x4_t acc[NTW][WG_CT];
 #pragma unroll
-        for (int i = 0; i < NTW; ++i) acc[i][0] = acc[i][1] = f32x4_t{0, 0, 0, 0};
+        for (int i = 0; i < NTW; ++i)
+#pragma unroll
+            for (int h = 0; h < WG_CT; ++h) acc[i][h] = f32x4_t{0, 0, 0, 0};
         // operands of two of the wave's steps in flight, slots alternating
-        Raw8<T> fa[RING][NTW], fb[RING][2];
+        Raw8<T> fa[RING][NTW], fb[RING][WG_CT];
         int mk[RING][NTW];
         auto issue = [&](int t, int sl) {
             const __amdgpu_buffer_rsrc_t ar = act_rsrc(t), br = dat_rsrc(t);
 #pragma unroll
             for (int i = 0; i < NTW; ++i) raw_load(fa[sl][i], ar, (uint32_t)(rowa[i] * a.BP + g8) * ES);
-            raw_load(fb[sl][0], br, boff[0]);
-            raw_load(fb[sl][1], br, boff[1]);
+#pragma unroll
+            for (int h = 0; h < WG_CT; ++h) raw_load(fb[sl][h], br, boff[h]);
             if (MASKED) {
                 const __amdgpu_buffer_rsrc_t mr = buf_rsrc(a.site.mask + (size_t)t * a.site.kmax, (uint32_t)a.site.kmax);
 #pragma unroll
@@ -1000,7 +1004,7 @@ __device__ __forceinline__ void wgrad_full(const WgArgs& a, float* red) {
           if (t < t1) {
             Raw8<T>(&ca)[NTW] = fa[sl];
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
+            for (int h = 0; h < WG_CT; ++h) {
                 raw_and(fb[sl][h], pmb[h]);
                 if (first) db_add_raw(fb[sl][h], dbacc[h]);
             }
@@ -1011,20 +1015,20 @@ __device__ __forceinline__ void wgrad_full(const WgArgs& a, float* red) {
 #pragma unroll
                     for (int q = 0; q < NW; ++q) ca[i].w[q] = mk[sl][i] ? ca[i].w[q] : 0u;
                 }
-                raw_mma(fb[sl][0], ca[i], acc[i][0]);
-                raw_mma(fb[sl][1], ca[i], acc[i][1]);
+#pragma unroll
+                for (int h = 0; h < WG_CT; ++h) raw_mma(fb[sl][h], ca[i], acc[i][h]);
             }
             for (int bc = 32; MULTI && bc < a.B; bc += 32) {    // further batch chunks (B > 32)
                 const __amdgpu_buffer_rsrc_t ar = act_rsrc(t), br = dat_rsrc(t);
-                Raw8<T> xb[2], xa[NTW];
-                raw_load(xb[0], br, boff[0] + (uint32_t)bc * ES);
-                raw_load(xb[1], br, boff[1] + (uint32_t)bc * ES);
+                Raw8<T> xb[WG_CT], xa[NTW];
+#pragma unroll
+                for (int h = 0; h < WG_CT; ++h) raw_load(xb[h], br, boff[h] + (uint32_t)bc * ES);
 #pragma unroll
                 for (int i = 0; i < NTW; ++i) raw_load(xa[i], ar, (uint32_t)(rowa[i] * a.BP + bc + g8) * ES);
                 uint32_t pm[NW];
                 pad_mask<T>(bc + g8, a.B, pm);
 #pragma unroll
-                for (int h = 0; h < 2; ++h) {
+                for (int h = 0; h < WG_CT; ++h) {
                     raw_and(xb[h], pm);
                     if (n + 16 * h >= a.G) raw_and(xb[h], pmb[h]);   // pmb is all zero past G
                     if (first) db_add_raw(xb[h], dbacc[h]);
@@ -1036,8 +1040,8 @@ __device__ __forceinline__ void wgrad_full(const WgArgs& a, float* red) {
 #pragma unroll
                         for (int q = 0; q < NW; ++q) xa[i].w[q] = mk[sl][i] ? xa[i].w[q] : 0u;
                     }
-                    raw_mma(xb[0], xa[i], acc[i][0]);
-                    raw_mma(xb[1], xa[i], acc[i][1]);
+#pragma unroll
+                    for (int h = 0; h < WG_CT; ++h) raw_mma(xb[h], xa[i], acc[i][h]);
                 }
             }
           }
@@ -1056,9 +1060,9 @@ __device__ __forceinline__ void wgrad_full(const WgArgs& a, float* red) {
 #pragma unroll
             for (int i = 0; i < NTW; ++i)
 #pragma unroll
-                for (int h = 0; h < 2; ++h)
+                for (int h = 0; h < WG_CT; ++h)
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) mine[((i * 2 + h) * 4 + r) * 64] = acc[i][h][r];
+                    for (int r = 0; r < 4; ++r) mine[((i * WG_CT + h) * 4 + r) * 64] = acc[i][h][r];
         }
         if (tsplit) __syncthreads();
         if (!tsplit || !rh) {
@@ -1070,12 +1074,12 @@ __device__ __forceinline__ void wgrad_full(const WgArgs& a, float* red) {
             for (int i = 0; i < NTW; ++i) {
                 const int row = rb + 16 * i + col;
 #pragma unroll
-                for (int h = 0; h < 2; ++h) {
+                for (int h = 0; h < WG_CT; ++h) {
                     float4 v;
-                    v.x = a.s * (tsplit ? acc[i][h][0] + mine[((i * 2 + h) * 4 + 0) * 64] : acc[i][h][0]);
-                    v.y = a.s * (tsplit ? acc[i][h][1] + mine[((i * 2 + h) * 4 + 1) * 64] : acc[i][h][1]);
-                    v.z = a.s * (tsplit ? acc[i][h][2] + mine[((i * 2 + h) * 4 + 2) * 64] : acc[i][h][2]);
-                    v.w = a.s * (tsplit ? acc[i][h][3] + mine[((i * 2 + h) * 4 + 3) * 64] : acc[i][h][3]);
+                    v.x = a.s * (tsplit ? acc[i][h][0] + mine[((i * WG_CT + h) * 4 + 0) * 64] : acc[i][h][0]);
+                    v.y = a.s * (tsplit ? acc[i][h][1] + mine[((i * WG_CT + h) * 4 + 1) * 64] : acc[i][h][1]);
+                    v.z = a.s * (tsplit ? acc[i][h][2] + mine[((i * WG_CT + h) * 4 + 2) * 64] : acc[i][h][2]);
+                    v.w = a.s * (tsplit ? acc[i][h][3] + mine[((i * WG_CT + h) * 4 + 3) * 64] : acc[i][h][3]);
                     if (row < r1 && nq + 16 * h < a.G) *(float4*)(a.out + (size_t)row * a.G + nq + 16 * h) = v;
                 }
             }
@@ -1084,13 +1088,13 @@ __device__ __forceinline__ void wgrad_full(const WgArgs& a, float* red) {
     }
     if (dbw) {                                 // (the last slice is never empty) lanes l, l+16, l+32, l+48 hold column l
         if (tsplit && rh) {
-            mine[0] = dbacc[0];
-            mine[64] = dbacc[1];
+#pragma unroll
+            for (int h = 0; h < WG_CT; ++h) mine[64 * h] = dbacc[h];
         }
         if (tsplit) __syncthreads();
         if (!rh) {
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
+            for (int h = 0; h < WG_CT; ++h) {
                 float v = tsplit ? dbacc[h] + mine[64 * h] : dbacc[h];
                 v += __shfl_xor(v, 16);
                 v += __shfl_xor(v, 32);
@@ -1102,7 +1106,7 @@ __device__ __forceinline__ void wgrad_full(const WgArgs& a, float* red) {
 
 // LDS of the full kernel's pass reduction
 template <typename T>
-constexpr size_t wgrad_full_lds_bytes() { return (size_t)WG_NWV * (WgTiles<T>::N / 2) * 8 * 64 * 4; }
+constexpr size_t wgrad_full_lds_bytes() { return (size_t)WG_NWV * (WgTiles<T>::N / 2) * WG_CT * 4 * 64 * 4; }
 
 // One launch for every weight gradient of a pass (grid z = problem): a
 // problem whose keep lists are all the identity takes the full kernel, the
