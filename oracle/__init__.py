@@ -12,5 +12,7 @@ Contents
   lstm    -- dense float64 LSTM forward (Eq. 1-6) with the masks applied as
              elementwise multipliers, and back-propagation through time
              (Eq. 7-11) written out by hand.
+  embedding -- the embedding-table gradient of a language model's input:
+             the layer-0 input gradient rows summed by token id.
 """
-from . import philox, masks, lstm  # noqa: F401
+from . import philox, masks, lstm, embedding  # noqa: F401

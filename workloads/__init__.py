@@ -110,6 +110,7 @@ class Workload:
     c0: np.ndarray           # [L*D][B][H] float32
     target: np.ndarray       # [T][B][D*H] float32 (MSE target)
     lengths: Optional[np.ndarray]  # [B] int32 or None
+    tokens: Optional[np.ndarray] = None   # [T][B] int32 token ids of an embedding input, or None
 
     @property
     def batch(self):
@@ -135,6 +136,7 @@ def make_workload(cfg: Config, batch: Optional[int] = None) -> Workload:
     q = round_to_bf16 if bf else (lambda a: np.asarray(a, dtype=np.float32))
 
     # layer input
+    ids = None
     if cfg.input_kind == "embedding":
         table = rng.normal(0.0, cfg.input_std, size=(cfg.vocab, I)).astype(np.float32)
         ids = _zipf_ids(rng, cfg.vocab, (T, B))
@@ -169,7 +171,8 @@ def make_workload(cfg: Config, batch: Optional[int] = None) -> Workload:
         valid = np.arange(T)[:, None] < lengths[None, :]
         x = np.where(valid[:, :, None], x, 0.0).astype(np.float32)
     x = q(x)
-    return Workload(cfg, np.ascontiguousarray(x), W, U, bias, h0, c0, target, lengths)
+    tokens = None if ids is None else np.ascontiguousarray(ids.astype(np.int32))
+    return Workload(cfg, np.ascontiguousarray(x), W, U, bias, h0, c0, target, lengths, tokens)
 
 
 def slice_rows(wl: Workload, rows) -> Workload:
@@ -179,4 +182,5 @@ def slice_rows(wl: Workload, rows) -> Workload:
     return Workload(wl.cfg, np.ascontiguousarray(wl.x[:, rows]), wl.W, wl.U, wl.b,
                     np.ascontiguousarray(wl.h0[:, rows]), np.ascontiguousarray(wl.c0[:, rows]),
                     np.ascontiguousarray(wl.target[:, rows]),
-                    None if wl.lengths is None else np.ascontiguousarray(wl.lengths[rows]))
+                    None if wl.lengths is None else np.ascontiguousarray(wl.lengths[rows]),
+                    None if wl.tokens is None else np.ascontiguousarray(wl.tokens[:, rows]))
