@@ -209,6 +209,38 @@ def run_mode(wl, p_nr, p_rh, compact, steps, warmup, timed_kernels=()):
                 ktime=ktime)
 
 
+def run_embedding(wl, p_nr, steps, warmup):
+    """Embedding-table gradient after the step (lstm_sd_embedding_backward) on
+    a language-model workload: its kernel's average duration (HIP events on
+    its launch stream) and algorithmic bytes per launch (token ids, the kept
+    columns of dx, one read and one write of each touched row of d_emb)."""
+    import torch
+    from paper_2106_12089_amd import binding as B_
+    from paper_2106_12089_amd.session import Session
+    cfg = wl.cfg
+    s = Session(wl, p_nr, 0.0, 1)
+    tok = torch.from_numpy(wl.tokens.astype(np.int32)).cuda()
+    d_emb = torch.zeros(cfg.vocab, s.I, dtype=torch.float32, device="cuda")
+    for i in range(warmup):
+        s.step(cfg.mask_seed, 10_000 + i)
+        s.embedding_backward(tok, cfg.vocab, d_emb)
+    torch.cuda.synchronize()
+    B_.lstm_sd_kernel_timer_start("emb_grad")
+    nbytes = []
+    rows = len(np.unique(wl.tokens))
+    for i in range(steps):
+        s.step(cfg.mask_seed, i)
+        s.embedding_backward(tok, cfg.vocab, d_emb)
+        kept = s.mask_views()[3][0].astype(np.int64)      # layer-0 NR kept count per step t
+        nbytes.append(wl.tokens.size * 4 + int(kept.sum()) * s.B * 4 + rows * s.I * 8)
+    ms, n = B_.lstm_sd_kernel_timer_stop()
+    torch.cuda.synchronize()
+    us = 1e3 * ms / max(n, 1)
+    b = float(np.mean(nbytes))
+    return {"avg_us": round(us, 3), "launches_per_step": n / steps, "bytes_per_launch": int(b),
+            "achieved_gbs": round(b / (us * 1e-6) / 1e9, 1), "vocab": cfg.vocab, "rows_touched": rows}
+
+
 def roofline(res, cfg):
     kt = res["ktime"]
     name = max(kt, key=lambda k: kt[k]["total_ms"])
@@ -381,6 +413,8 @@ def main(argv=None):
                        "speedup_vs_dense": round(rd["ms"] / r["ms"], 4) if rd else None,
                        "tflops": round(r["flops"] / (r["ms"] * 1e-3) / 1e12, 4),
                        "phases_ms": {k: round(v, 4) for k, v in r["phases"].items()}}
+    if wl.tokens is not None:
+        out["embedding_backward"] = run_embedding(wl, p, args.steps, args.warmup)
     if args.calibrate_copy:
         n = args.calibrate_copy * (1 << 20) // 4
         a = torch.ones(n, dtype=torch.float32, device="cuda")

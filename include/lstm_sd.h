@@ -197,6 +197,25 @@ int lstm_sd_mse_grad(const lstm_sd_dims* dims, const float* y, const float* targ
                      const int32_t* lengths, float* dy, float* loss,
                      void* workspace, size_t workspace_bytes, void* stream);
 
+/* Embedding-table gradient of a language model whose layer-0 input is an
+ * embedding lookup, x_t[b] = E[tokens[t][b]]: the step just below the path.
+ * Row v of d_emb receives the sum of the layer-0 input gradient rows dx_t[b]
+ * over every (t, b) with tokens[t][b] = v, over the columns kept at t (layer
+ * 0's NR mask; dx is zero in the dropped columns, Eq. 10, and they are not
+ * accumulated).  Each row's sum is formed in a fixed order (ascending (t, b)
+ * within chunks of 2048 positions) and added once per chunk: deterministic,
+ * no atomics on d_emb.
+ *   tokens   device [T][B] int32; ids outside [0, vocab) are skipped
+ *   vocab    rows of the table (> 0)
+ *   dx       device [T][B][I] float: lstm_sd_backward's dx
+ *   mask_buf device, the masks of the step (as for lstm_sd_backward)
+ *   d_emb    device [vocab][I] float, accumulated into (+=): rows of tokens
+ *            that occur change, the others are not touched
+ * Errors: LSTM_SD_EINVAL (null pointer, vocab <= 0, bad dims),
+ * LSTM_SD_EWORKSPACE (mask_bytes too small), LSTM_SD_EHIP. */
+int lstm_sd_embedding_backward(const lstm_sd_dims* dims, const int32_t* tokens, int vocab, const float* dx,
+                               const void* mask_buf, size_t mask_bytes, float* d_emb, void* stream);
+
 /* Instrumentation for measuring one kernel's average duration on the
  * stream it runs on.  After lstm_sd_kernel_timer_start(name), every launch
  * of the named kernel made by this library is bracketed by a pair of HIP
@@ -205,7 +224,8 @@ int lstm_sd_mse_grad(const lstm_sd_dims* dims, const float* y, const float* targ
  * and the number of launches, and turns the timer off.  Names:
  * "mask_build", "transpose", "fx", "step", "bwd", "dx", "wgrad",
  * "fwd_persist", "bwd_persist" (the persistent recurrent kernels, one launch
- * per layer; their pair is recorded around the cooperative launch).  Events
+ * per layer; their pair is recorded around the cooperative launch),
+ * "emb_grad" (lstm_sd_embedding_backward's one kernel).  Events
  * are created by the library (no device memory is allocated).  Not
  * thread-safe; for benchmarks. */
 int lstm_sd_kernel_timer_start(const char* kernel);

@@ -67,6 +67,7 @@ SIGNATURES = {
                                         _P, _SZ, _P, _P, _P, _P, _P, _P, ctypes.POINTER(lstm_sd_grads),
                                         _P, _SZ, _P]),
     "lstm_sd_mse_grad": (ctypes.c_int, [_DIMS, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "lstm_sd_embedding_backward": (ctypes.c_int, [_DIMS, _P, ctypes.c_int, _P, _P, _SZ, _P, _P]),
     "lstm_sd_kernel_timer_start": (ctypes.c_int, [ctypes.c_char_p]),
     "lstm_sd_kernel_timer_stop": (ctypes.c_int, [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]),
 }
@@ -206,6 +207,11 @@ def lstm_sd_backward(dims, W, U, b, x, lengths, h0, c0, mask_buf, reserve, dy, d
 def lstm_sd_mse_grad(dims, y, target, lengths, dy, loss, workspace, stream=None):
     _check(load().lstm_sd_mse_grad(ctypes.byref(dims), _ptr(y), _ptr(target), _ptr(lengths), _ptr(dy),
                                    _ptr(loss), _ptr(workspace), _nbytes(workspace), _stream(stream)))
+
+
+def lstm_sd_embedding_backward(dims, tokens, vocab, dx, mask_buf, d_emb, stream=None):
+    _check(load().lstm_sd_embedding_backward(ctypes.byref(dims), _ptr(tokens), int(vocab), _ptr(dx), _ptr(mask_buf),
+                                             _nbytes(mask_buf), _ptr(d_emb), _stream(stream)))
 
 
 def lstm_sd_kernel_timer_start(kernel: str):

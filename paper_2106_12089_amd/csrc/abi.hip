@@ -24,6 +24,7 @@ template <typename T> void launch_dx(const DxArgs& a, int K, hipStream_t st);
 template <typename T> void launch_wgrad(const WgBatch& b, hipStream_t st);
 void launch_bwd_init(const float*, const float*, float*, float*, long, void*, int, int, int, long, long, unsigned*, int*,
                      hipStream_t);
+void launch_emb_grad(const int32_t*, int, int, int, const float*, const SiteView&, int, float*, hipStream_t);
 void launch_mse(const float*, const float*, const int32_t*, float*, float*, int, float*, int, int, int,
                 hipStream_t);
 int setup_kernel_attributes();
@@ -770,6 +771,19 @@ int lstm_sd_mse_grad(const lstm_sd_dims* dims, const float* y, const float* targ
     float* partial = (float*)((char*)workspace + P.w_loss);
     launch_mse(y, target, lengths, dy, partial, 1024, loss, P.T, P.B, P.D * P.H, (hipStream_t)stream);
     return hip_check("mse launch");
+}
+
+int lstm_sd_embedding_backward(const lstm_sd_dims* dims, const int32_t* tokens, int vocab, const float* dx,
+                               const void* mask_buf, size_t mask_bytes, float* d_emb, void* stream) {
+    Plan P; const char* why = nullptr;
+    int rc = make_plan(dims, &P, &why);
+    if (rc) return fail(rc, why);
+    if (!tokens || !dx || !mask_buf || !d_emb) return fail(LSTM_SD_EINVAL, "a required pointer is NULL");
+    if (vocab <= 0) return fail(LSTM_SD_EINVAL, "vocab must be positive");
+    if (mask_bytes < P.m_total) return fail(LSTM_SD_EWORKSPACE, "mask_bytes smaller than lstm_sd_mask_bytes()");
+    const SiteView nr0 = site_view(P, mask_buf, P.site_nr(0));
+    launch_emb_grad(tokens, P.T * P.B, P.B, vocab, dx, nr0, P.I, d_emb, (hipStream_t)stream);
+    return hip_check("embedding gradient launch");
 }
 
 int lstm_sd_kernel_timer_start(const char* kernel) {

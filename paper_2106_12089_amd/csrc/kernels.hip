@@ -1153,6 +1153,95 @@ __global__ void k_bwd_init(const float* dhT, const float* dcT, float* dhc, float
     }
 }
 
+// Embedding-table gradient of a language model's input: the layer-0 input
+// gradient dx_t[b] is added into row tokens[t][b] of d_emb, over the columns
+// kept at t (the dropped columns of dx are zero, Eq. 10).  grid
+// (ceil(V/EM_VB), ceil(I/EM_CW)): a workgroup owns EM_VB token ids and EM_CW
+// columns (lane = column); block 256 (4 waves).  Wave w scans the position
+// groups w, w+4, ... (64 positions each, ascending), picks the positions
+// whose token it owns with a ballot, loads their dx rows EM_BATCH at a time
+// (independent loads in flight) and adds them into its own partial sums in
+// LDS with LDS float adds: one wave's LDS operations complete in issue
+// order, so each partial is summed in ascending position order.  Then the
+// wave that owns token j (j mod 4) adds the four partials in wave order and
+// writes row j once (all its loads before its stores): a fixed summation
+// order, no global atomics, the same result on every run.  A Zipf-distributed
+// text puts most positions in the first workgroup's range; its waves still
+// share them evenly.
+constexpr int EM_VB = 64, EM_CW = 64, EM_BATCH = 16;
+
+__global__ void __launch_bounds__(256) k_emb_grad(const int32_t* tokens, int N, int B, int V, const float* dx,
+                                                  SiteView nr0, int I, float* d_emb) {
+    __shared__ float part[4][EM_VB][EM_CW];
+    __shared__ int touched[EM_VB];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int v0 = blockIdx.x * EM_VB;
+    const int vn = min(EM_VB, V - v0);                 // token ids v0 .. v0+vn-1
+    const int col = blockIdx.y * EM_CW + lane;
+    const bool colok = col < I;
+    const int colc = colok ? col : I - 1;              // lanes past I read a valid column, never written
+    float4* pz = reinterpret_cast<float4*>(&part[w][0][0]);
+    for (int i = lane; i < EM_VB * EM_CW / 4; i += 64) pz[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (tid < EM_VB) touched[tid] = 0;
+    __syncthreads();
+    for (int g = w * 64; g < N; g += 256) {
+        const int pos = g + lane;
+        const int tk = pos < N ? tokens[pos] : -1;
+        const bool act = tk >= v0 && tk - v0 < vn;     // (tk >= v0 >= 0: no wrap-around)
+        const int j = act ? tk - v0 : 0;
+        const int moff = (pos < N ? pos / B : 0) * nr0.kmax;
+        uint64_t left = __builtin_amdgcn_ballot_w64(act);
+        while (left) {
+            int sp[EM_BATCH], sj[EM_BATCH], sm[EM_BATCH];
+            int nb = 0;
+#pragma unroll
+            for (int k = 0; k < EM_BATCH; ++k) {
+                if (left) {
+                    const int idx = __builtin_ctzll(left);
+                    left &= left - 1;
+                    sp[k] = __builtin_amdgcn_readlane(pos, idx);
+                    sj[k] = __builtin_amdgcn_readlane(j, idx);
+                    sm[k] = __builtin_amdgcn_readlane(moff, idx);
+                    nb = k + 1;
+                } else {                               // (a valid position; its value is not added)
+                    sp[k] = sp[0];
+                    sj[k] = sj[0];
+                    sm[k] = sm[0];
+                }
+            }
+            float d[EM_BATCH];
+            bool m[EM_BATCH];
+#pragma unroll
+            for (int k = 0; k < EM_BATCH; ++k) {
+                d[k] = dx[(size_t)sp[k] * I + colc];
+                m[k] = nr0.mask[(size_t)sm[k] + colc] != 0;
+            }
+#pragma unroll
+            for (int k = 0; k < EM_BATCH; ++k)
+                if (k < nb)
+                    __hip_atomic_fetch_add(&part[w][sj[k]][lane], m[k] ? d[k] : 0.0f, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_WORKGROUP);
+            if (lane == 0)
+                for (int k = 0; k < nb; ++k) touched[sj[k]] = 1;
+        }
+    }
+    __syncthreads();
+    constexpr int NQ = EM_VB / 4;
+    float tot[NQ], old[NQ];
+    bool own[NQ];
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+        const int jj = w + 4 * q;
+        own[q] = jj < vn && touched[jj] && colok;
+        tot[q] = ((part[0][jj][lane] + part[1][jj][lane]) + part[2][jj][lane]) + part[3][jj][lane];
+        old[q] = own[q] ? d_emb[(size_t)(v0 + jj) * I + col] : 0.0f;
+    }
+#pragma unroll
+    for (int q = 0; q < NQ; ++q)
+        if (own[q]) d_emb[(size_t)(v0 + w + 4 * q) * I + col] = old[q] + tot[q];
+}
+
 // MSE loss gradient (a loss of the synthetic workloads).
 __device__ __forceinline__ float nvalid_rows(const int32_t* lengths, int B, int T) {
     if (!lengths) return (float)B * T;
@@ -1208,9 +1297,9 @@ __global__ void __launch_bounds__(256) k_mse_final(const float* partial, int np,
 // Kernel timer (instrumentation): HIP event pairs around the launches of one
 // kernel class.
 enum KernelId { KID_NONE = -1, KID_MASK, KID_TRANS, KID_FX, KID_STEP, KID_BWD, KID_DX, KID_WGRAD, KID_FWDP, KID_BWDP,
-                KID_COUNT };
+                KID_EMB, KID_COUNT };
 static const char* const kKernelNames[KID_COUNT] = {"mask_build", "transpose", "fx", "step", "bwd", "dx", "wgrad",
-                                                    "fwd_persist", "bwd_persist"};
+                                                    "fwd_persist", "bwd_persist", "emb_grad"};
 static int g_timer_kid = KID_NONE;
 static std::vector<hipEvent_t> g_ev_pool;
 static size_t g_ev_used = 0;
@@ -1350,6 +1439,11 @@ void launch_bwd_init(const float* dhT, const float* dcT, float* dhc, float* dcs,
     const long np = da ? nblocks * 16 * mtiles * 32 : 0;      // upper bound of the DA padding entries
     launch_k(KID_NONE, k_bwd_init, dim3(nblk(n > np ? n : np, 256)), dim3(256), 0, st, dhT, dcT, dhc, dcs, n, da, es,
              G, mtiles, nblocks, das, bar, err);
+}
+void launch_emb_grad(const int32_t* tokens, int N, int B, int V, const float* dx, const SiteView& nr0, int I,
+                     float* d_emb, hipStream_t st) {
+    launch_k(KID_EMB, k_emb_grad, dim3((V + EM_VB - 1) / EM_VB, (I + EM_CW - 1) / EM_CW), dim3(256), 0, st, tokens, N,
+             B, V, dx, nr0, I, d_emb);
 }
 void launch_mse(const float* y, const float* tg, const int32_t* lengths, float* dy, float* partial, int np,
                 float* loss, int T, int B, int F, hipStream_t st) {

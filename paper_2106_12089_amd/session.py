@@ -84,6 +84,14 @@ class Session:
                             self.dx if want_dx else None, self.dh0, self.dc0, self.dW, self.dU, self.db,
                             self.workspace)
 
+    def embedding_backward(self, tokens, vocab: int, d_emb=None):
+        """Embedding-table gradient from this step's dx (lstm_sd_embedding_backward):
+        accumulated into d_emb [vocab][I] (a new zero tensor when None), returned."""
+        if d_emb is None:
+            d_emb = torch.zeros(vocab, self.I, dtype=torch.float32, device=self.dx.device)
+        B_.lstm_sd_embedding_backward(self.dims, tokens, vocab, self.dx, self.mask_buf, d_emb)
+        return d_emb
+
     def step(self, seed: int, step: int):
         self.masks(seed, step)
         self.forward()
