@@ -14,5 +14,8 @@ Contents
              (Eq. 7-11) written out by hand.
   embedding -- the embedding-table gradient of a language model's input:
              the layer-0 input gradient rows summed by token id.
+  head    -- the output head: pre-FC structured output dropout, the FC
+             (vocabulary projection) layer and the softmax cross-entropy
+             loss, forward and backward.
 """
-from . import philox, masks, lstm, embedding  # noqa: F401
+from . import philox, masks, lstm, embedding, head  # noqa: F401

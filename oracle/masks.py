@@ -11,7 +11,9 @@ HIP library, implemented independently):
   * neuron k is dropped at t iff word < floor(p * 2**64), computed exactly
     with Python integers, so the drop decision is integer and bit-exact;
   * stream ids: the non-recurrent (NR) input of layer l uses 4*l; the
-    recurrent (RH) input of layer l, direction d uses 4*l + 2 + d.
+    recurrent (RH) input of layer l, direction d uses 4*l + 2 + d; the
+    output (pre-FC) site of an L-layer stack uses 4*L, the NR stream a
+    layer L would have (the FC layer is the next consumer of the output).
 
 A keep list is the ascending list of kept neuron indices at one t; its
 length is the keep count.  The paper calls packing the kept rows "matrix
@@ -39,6 +41,10 @@ def nr_stream(layer: int) -> int:
 
 def rh_stream(layer: int, direction: int) -> int:
     return 4 * layer + 2 + direction
+
+
+def out_stream(num_layers: int) -> int:
+    return 4 * num_layers
 
 
 def uniform_words(seed: int, step: int, stream: int, T: int, K: int) -> np.ndarray:

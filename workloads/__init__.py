@@ -111,6 +111,11 @@ class Workload:
     target: np.ndarray       # [T][B][D*H] float32 (MSE target)
     lengths: Optional[np.ndarray]  # [B] int32 or None
     tokens: Optional[np.ndarray] = None   # [T][B] int32 token ids of an embedding input, or None
+    # output head of a language model (embedding inputs only): the next token
+    # as target, an FC layer [D*H][V] (input-major) and its bias [V]
+    targets: Optional[np.ndarray] = None  # [T][B] int32
+    W_fc: Optional[np.ndarray] = None     # [D*H][V] float32 (bf16-representable for bf16 configs)
+    b_fc: Optional[np.ndarray] = None     # [V] float32
 
     @property
     def batch(self):
@@ -172,7 +177,17 @@ def make_workload(cfg: Config, batch: Optional[int] = None) -> Workload:
         x = np.where(valid[:, :, None], x, 0.0).astype(np.float32)
     x = q(x)
     tokens = None if ids is None else np.ascontiguousarray(ids.astype(np.int32))
-    return Workload(cfg, np.ascontiguousarray(x), W, U, bias, h0, c0, target, lengths, tokens)
+    targets = W_fc = b_fc = None
+    if ids is not None:
+        # drawn from a generator of their own, so the draws above do not move
+        hr = np.random.Generator(np.random.PCG64([cfg.seed, 1]))
+        nxt = _zipf_ids(hr, cfg.vocab, (1, B))
+        targets = np.ascontiguousarray(np.concatenate([ids[1:], nxt]).astype(np.int32))
+        a = cfg.weight_scale
+        W_fc = q(hr.uniform(-a, a, size=(D * H, cfg.vocab)).astype(np.float32))
+        b_fc = hr.uniform(-a, a, size=(cfg.vocab,)).astype(np.float32)
+    return Workload(cfg, np.ascontiguousarray(x), W, U, bias, h0, c0, target, lengths, tokens, targets,
+                    W_fc, b_fc)
 
 
 def slice_rows(wl: Workload, rows) -> Workload:
@@ -183,4 +198,6 @@ def slice_rows(wl: Workload, rows) -> Workload:
                     np.ascontiguousarray(wl.h0[:, rows]), np.ascontiguousarray(wl.c0[:, rows]),
                     np.ascontiguousarray(wl.target[:, rows]),
                     None if wl.lengths is None else np.ascontiguousarray(wl.lengths[rows]),
-                    None if wl.tokens is None else np.ascontiguousarray(wl.tokens[:, rows]))
+                    None if wl.tokens is None else np.ascontiguousarray(wl.tokens[:, rows]),
+                    None if wl.targets is None else np.ascontiguousarray(wl.targets[:, rows]),
+                    wl.W_fc, wl.b_fc)
