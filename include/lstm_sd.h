@@ -216,6 +216,71 @@ int lstm_sd_mse_grad(const lstm_sd_dims* dims, const float* y, const float* targ
 int lstm_sd_embedding_backward(const lstm_sd_dims* dims, const int32_t* tokens, int vocab, const float* dx,
                                const void* mask_buf, size_t mask_bytes, float* d_emb, void* stream);
 
+/* ---------------------------------------------------------------------------
+ * Output head of a language model: structured dropout on the top LSTM
+ * output before the FC (vocabulary projection) layer, the FC layer, and the
+ * softmax cross-entropy loss.  The paper's timings include the FC layers'
+ * products after compaction (Sec. 4, experimental setup); its language
+ * models drop the LSTM output before the FC layer (Sec. 4.1) and its
+ * translation models the final encoder/decoder outputs, the projection being
+ * sized by the vocabulary (Sec. 4.2).  A Case-III mask on the FC input
+ * (Sec. 3.1) propagates as in Sec. 3.2 for one product: the forward product
+ * reads only the kept input columns, the input gradient is written only in
+ * the kept columns, and the weight gradient only in the rows kept at each t.
+ *   z[t][b] = (s * m[t] * y[t][b]) W + c,   s = 1/(1-p_out)
+ *   loss    = mean over rows that count of logsumexp(z) - z[target]
+ * A row (t, b) counts when t < lengths[b] and its target is in [0, vocab)
+ * (other targets act as an ignore index). */
+typedef struct {
+    int32_t features;     /* F = D*H of the LSTM below, 1 .. LSTM_SD_MAX_K */
+    int32_t vocab;        /* V >= 4, a multiple of 4; F*V*sizeof(dtype) < 2^31 */
+    int32_t batch;        /* B, as the LSTM */
+    int32_t seq_len;      /* T, as the LSTM */
+    int32_t dtype;        /* LSTM_SD_DTYPE_F32 or LSTM_SD_DTYPE_BF16 */
+    int32_t compact;      /* 1 = skip dropped rows (method), 0 = dense baseline */
+    int32_t stream_id;    /* mask stream of the output site: 4*L for an L-layer stack */
+    int32_t reserved;
+    double p_out;         /* output dropout rate, [0, 1) */
+} lstm_sd_head_dims;
+
+/* Sizes (0 and the error set for invalid dims).  The head's mask buffer has
+ * the layout of lstm_sd_mask_layout with one site of K = features. */
+size_t lstm_sd_head_mask_bytes(const lstm_sd_head_dims* hd);
+size_t lstm_sd_head_workspace_bytes(const lstm_sd_head_dims* hd);
+int    lstm_sd_head_mask_layout_get(const lstm_sd_head_dims* hd, lstm_sd_mask_layout* out);
+
+/* Draw the output site's mask for one training step with the generator of
+ * lstm_sd_mask_generate (stream id hd->stream_id, rate p_out). */
+int lstm_sd_head_mask_generate(const lstm_sd_head_dims* hd, uint64_t seed, uint64_t step,
+                               void* mask_buf, size_t mask_bytes, void* stream);
+
+/* Forward: logits of every (t, b).
+ *   W_fc     device [F][V], dtype (input-major, as the LSTM weights)
+ *   b_fc     device [V] float
+ *   y        device [T][B][F] float: the top LSTM output (lstm_sd_forward's y)
+ *   logits   device [T][B][V] float (written)
+ *   workspace device, lstm_sd_head_workspace_bytes(hd); it carries the
+ *            forward's prepared input to lstm_sd_head_backward, so the same
+ *            buffer must reach the backward unchanged. */
+int lstm_sd_head_forward(const lstm_sd_head_dims* hd, const void* W_fc, const float* b_fc, const float* y,
+                         const void* mask_buf, size_t mask_bytes, float* logits, void* workspace,
+                         size_t workspace_bytes, void* stream);
+
+/* Loss and backward of the head.
+ *   targets  device [T][B] int32;  lengths device [B] int32 or NULL
+ *   logits   device [T][B][V] float from lstm_sd_head_forward
+ *   loss     device float[1] (written): the mean cross-entropy (0 if no row counts)
+ *   dy       device [T][B][F] float (written): the gradient for the top LSTM
+ *            output, zero in the columns dropped at t (feed it to
+ *            lstm_sd_backward as dy)
+ *   dW_fc    device [F][V] float (overwritten): zero in rows never kept
+ *   db_fc    device [V] float (overwritten)
+ * Errors: LSTM_SD_EINVAL, LSTM_SD_EUNSUPPORTED, LSTM_SD_EWORKSPACE, LSTM_SD_EHIP. */
+int lstm_sd_head_backward(const lstm_sd_head_dims* hd, const void* W_fc, const int32_t* targets,
+                          const int32_t* lengths, const void* mask_buf, size_t mask_bytes, const float* logits,
+                          float* loss, float* dy, float* dW_fc, float* db_fc, void* workspace,
+                          size_t workspace_bytes, void* stream);
+
 /* Instrumentation for measuring one kernel's average duration on the
  * stream it runs on.  After lstm_sd_kernel_timer_start(name), every launch
  * of the named kernel made by this library is bracketed by a pair of HIP
@@ -225,7 +290,9 @@ int lstm_sd_embedding_backward(const lstm_sd_dims* dims, const int32_t* tokens, 
  * "mask_build", "transpose", "fx", "step", "bwd", "dx", "wgrad",
  * "fwd_persist", "bwd_persist" (the persistent recurrent kernels, one launch
  * per layer; their pair is recorded around the cooperative launch),
- * "emb_grad" (lstm_sd_embedding_backward's one kernel).  Events
+ * "emb_grad" (lstm_sd_embedding_backward's one kernel), "ce" (the head's
+ * softmax cross-entropy kernels; the head's FC products count as "fx", "dx"
+ * and "wgrad").  Events
  * are created by the library (no device memory is allocated).  Not
  * thread-safe; for benchmarks. */
 int lstm_sd_kernel_timer_start(const char* kernel);

@@ -47,9 +47,16 @@ class lstm_sd_mask_layout(ctypes.Structure):
                 ("dseg_off", ctypes.c_size_t), ("total_bytes", ctypes.c_size_t)]
 
 
+class lstm_sd_head_dims(ctypes.Structure):
+    _fields_ = [("features", ctypes.c_int32), ("vocab", ctypes.c_int32), ("batch", ctypes.c_int32),
+                ("seq_len", ctypes.c_int32), ("dtype", ctypes.c_int32), ("compact", ctypes.c_int32),
+                ("stream_id", ctypes.c_int32), ("reserved", ctypes.c_int32), ("p_out", ctypes.c_double)]
+
+
 _P = ctypes.c_void_p
 _SZ = ctypes.c_size_t
 _DIMS = ctypes.POINTER(lstm_sd_dims)
+_HD = ctypes.POINTER(lstm_sd_head_dims)
 
 # name -> (restype, argtypes); the header's declarations
 SIGNATURES = {
@@ -68,6 +75,12 @@ SIGNATURES = {
                                         _P, _SZ, _P]),
     "lstm_sd_mse_grad": (ctypes.c_int, [_DIMS, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "lstm_sd_embedding_backward": (ctypes.c_int, [_DIMS, _P, ctypes.c_int, _P, _P, _SZ, _P, _P]),
+    "lstm_sd_head_mask_bytes": (_SZ, [_HD]),
+    "lstm_sd_head_workspace_bytes": (_SZ, [_HD]),
+    "lstm_sd_head_mask_layout_get": (ctypes.c_int, [_HD, ctypes.POINTER(lstm_sd_mask_layout)]),
+    "lstm_sd_head_mask_generate": (ctypes.c_int, [_HD, ctypes.c_uint64, ctypes.c_uint64, _P, _SZ, _P]),
+    "lstm_sd_head_forward": (ctypes.c_int, [_HD, _P, _P, _P, _P, _SZ, _P, _P, _SZ, _P]),
+    "lstm_sd_head_backward": (ctypes.c_int, [_HD, _P, _P, _P, _P, _SZ, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "lstm_sd_kernel_timer_start": (ctypes.c_int, [ctypes.c_char_p]),
     "lstm_sd_kernel_timer_stop": (ctypes.c_int, [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]),
 }
@@ -212,6 +225,51 @@ def lstm_sd_mse_grad(dims, y, target, lengths, dy, loss, workspace, stream=None)
 def lstm_sd_embedding_backward(dims, tokens, vocab, dx, mask_buf, d_emb, stream=None):
     _check(load().lstm_sd_embedding_backward(ctypes.byref(dims), _ptr(tokens), int(vocab), _ptr(dx), _ptr(mask_buf),
                                              _nbytes(mask_buf), _ptr(d_emb), _stream(stream)))
+
+
+def make_head_dims(features, vocab, batch, seq_len, dtype=DTYPE_BF16, compact=1, stream_id=0,
+                   p_out=0.0) -> lstm_sd_head_dims:
+    return lstm_sd_head_dims(features, vocab, batch, seq_len, dtype, compact, stream_id, 0, float(p_out))
+
+
+def lstm_sd_head_mask_bytes(hd) -> int:
+    n = load().lstm_sd_head_mask_bytes(ctypes.byref(hd))
+    if n == 0:
+        raise LstmSdError(EINVAL, lstm_sd_last_error())
+    return n
+
+
+def lstm_sd_head_workspace_bytes(hd) -> int:
+    n = load().lstm_sd_head_workspace_bytes(ctypes.byref(hd))
+    if n == 0:
+        raise LstmSdError(EINVAL, lstm_sd_last_error())
+    return n
+
+
+def lstm_sd_head_mask_layout_get(hd) -> lstm_sd_mask_layout:
+    out = lstm_sd_mask_layout()
+    _check(load().lstm_sd_head_mask_layout_get(ctypes.byref(hd), ctypes.byref(out)))
+    return out
+
+
+def lstm_sd_head_mask_generate(hd, seed, step, mask_buf, stream=None):
+    _check(load().lstm_sd_head_mask_generate(ctypes.byref(hd), ctypes.c_uint64(seed & (2**64 - 1)),
+                                             ctypes.c_uint64(step), _ptr(mask_buf), _nbytes(mask_buf),
+                                             _stream(stream)))
+
+
+def lstm_sd_head_forward(hd, W_fc, b_fc, y, mask_buf, logits, workspace, stream=None):
+    _check(load().lstm_sd_head_forward(ctypes.byref(hd), _ptr(W_fc), _ptr(b_fc), _ptr(y), _ptr(mask_buf),
+                                       _nbytes(mask_buf), _ptr(logits), _ptr(workspace), _nbytes(workspace),
+                                       _stream(stream)))
+
+
+def lstm_sd_head_backward(hd, W_fc, targets, lengths, mask_buf, logits, loss, dy, dW_fc, db_fc, workspace,
+                          stream=None):
+    _check(load().lstm_sd_head_backward(ctypes.byref(hd), _ptr(W_fc), _ptr(targets), _ptr(lengths),
+                                        _ptr(mask_buf), _nbytes(mask_buf), _ptr(logits), _ptr(loss), _ptr(dy),
+                                        _ptr(dW_fc), _ptr(db_fc), _ptr(workspace), _nbytes(workspace),
+                                        _stream(stream)))
 
 
 def lstm_sd_kernel_timer_start(kernel: str):

@@ -25,6 +25,12 @@ template <typename T> void launch_wgrad(const WgBatch& b, hipStream_t st);
 void launch_bwd_init(const float*, const float*, float*, float*, long, void*, int, int, int, long, long, unsigned*, int*,
                      hipStream_t);
 void launch_emb_grad(const int32_t*, int, int, int, const float*, const SiteView&, int, float*, hipStream_t);
+template <typename T> void launch_head_prep(const float*, void*, void*, int, int, int, int, hipStream_t);
+void launch_ce_loss(const float*, const int32_t*, const int32_t*, int, int, int, float*, float*, float*, float*, float*,
+                    hipStream_t);
+template <typename T>
+void launch_ce_grad(const float*, const int32_t*, const int32_t*, const float*, const float*, int, int, int, int, int,
+                    void*, void*, hipStream_t);
 void launch_mse(const float*, const float*, const int32_t*, float*, float*, int, float*, int, int, int,
                 hipStream_t);
 int setup_kernel_attributes();
@@ -662,6 +668,115 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
 
 using namespace lsd;
 
+// ---------------------------------------------------------------------------
+// Output head (pre-FC output dropout, FC layer, softmax cross-entropy).
+struct HeadPlan {
+    int F, V, B, T, dtype, compact, sid, BP, mtiles;
+    double p;
+    float s;
+    size_t esize, das;
+    // mask buffer: one site, kmax = F
+    size_t m_mask, m_keep, m_pos, m_count, m_drop, m_dcount, m_kseg, m_dseg, m_total;
+    // workspace
+    size_t w_yb, w_ybT, w_da, w_daT, w_lse, w_rowloss, w_rowok, w_ninv, w_total;
+};
+
+static int make_head_plan(const lstm_sd_head_dims* d, HeadPlan* p, const char** why) {
+    if (!d) { *why = "head dims is NULL"; return LSTM_SD_EINVAL; }
+    if (d->features < 1 || d->batch < 1 || d->seq_len < 1 || d->vocab < 1) {
+        *why = "dimensions must be >= 1"; return LSTM_SD_EINVAL;
+    }
+    if (!(d->p_out >= 0.0 && d->p_out < 1.0)) { *why = "p_out must be in [0, 1)"; return LSTM_SD_EINVAL; }
+    if (d->compact != 0 && d->compact != 1) { *why = "compact must be 0 or 1"; return LSTM_SD_EINVAL; }
+    if (d->stream_id < 0) { *why = "stream_id must be >= 0"; return LSTM_SD_EINVAL; }
+    if (d->dtype != LSTM_SD_DTYPE_F32 && d->dtype != LSTM_SD_DTYPE_BF16) {
+        *why = "dtype must be 0 (f32) or 1 (bf16)"; return LSTM_SD_EUNSUPPORTED;
+    }
+    const size_t es = d->dtype == LSTM_SD_DTYPE_BF16 ? 2 : 4;
+    if (d->features > LSTM_SD_MAX_K) { *why = "features must be <= LSTM_SD_MAX_K"; return LSTM_SD_EUNSUPPORTED; }
+    if (d->vocab < 4 || d->vocab % 4) { *why = "vocab must be a multiple of 4"; return LSTM_SD_EUNSUPPORTED; }
+    if ((size_t)d->features * d->vocab * es >= (1ull << 31)) {
+        *why = "features*vocab*sizeof(dtype) must be < 2^31"; return LSTM_SD_EUNSUPPORTED;
+    }
+    if ((long)d->batch * d->seq_len > (1L << 24) || d->batch > 65536 || d->seq_len > 65535) {
+        *why = "batch*seq_len too large"; return LSTM_SD_EUNSUPPORTED;
+    }
+    HeadPlan& q = *p;
+    q.F = d->features; q.V = d->vocab; q.B = d->batch; q.T = d->seq_len; q.dtype = d->dtype;
+    q.compact = d->compact; q.sid = d->stream_id; q.p = d->p_out; q.s = inv_keep(d->p_out);
+    q.esize = es;
+    q.BP = (q.B + 31) / 32 * 32;
+    q.mtiles = (q.B + 15) / 16;
+    q.das = (size_t)((q.V + 31) / 32) * q.mtiles * 512;
+    const size_t A = 256, T = q.T, B = q.B, F = q.F, V = q.V, BP = q.BP;
+    size_t off = 0;
+    q.m_mask = off;   off = align_up(off + T * F, A);
+    q.m_keep = off;   off = align_up(off + T * F * 4, A);
+    q.m_pos = off;    off = align_up(off + T * F * 4, A);
+    q.m_count = off;  off = align_up(off + T * 4, A);
+    q.m_drop = off;   off = align_up(off + T * F * 4, A);
+    q.m_dcount = off; off = align_up(off + T * 4, A);
+    q.m_kseg = off;   off = align_up(off + T * 17 * 4, A);
+    q.m_dseg = off;   off = align_up(off + T * 17 * 4, A);
+    q.m_total = off;
+    off = 0;
+    q.w_yb = off;      off = align_up(off + T * B * F * es, A);
+    q.w_ybT = off;     off = align_up(off + T * F * BP * es, A);
+    q.w_da = off;      off = align_up(off + T * q.das * es, A);
+    q.w_daT = off;     off = align_up(off + T * V * BP * es, A);
+    q.w_lse = off;     off = align_up(off + T * B * 4, A);
+    q.w_rowloss = off; off = align_up(off + T * B * 4, A);
+    q.w_rowok = off;   off = align_up(off + T * B * 4, A);
+    q.w_ninv = off;    off = align_up(off + 4, A);
+    q.w_total = off;
+    return LSTM_SD_OK;
+}
+
+static SiteView head_site(const HeadPlan& P, const void* mbuf) {
+    const char* m = (const char*)mbuf;
+    SiteView v;
+    v.mask = (const uint8_t*)(m + P.m_mask);
+    v.keep = (const int32_t*)(m + P.m_keep);
+    v.pos = (const int32_t*)(m + P.m_pos);
+    v.count = (const int32_t*)(m + P.m_count);
+    v.drop = (const int32_t*)(m + P.m_drop);
+    v.dcount = (const int32_t*)(m + P.m_dcount);
+    v.kseg = (const int32_t*)(m + P.m_kseg);
+    v.dseg = (const int32_t*)(m + P.m_dseg);
+    v.kmax = P.F;
+    return v;
+}
+
+template <typename E>
+static void head_backward_impl(const HeadPlan& P, const void* W_fc, const int32_t* tgt, const int32_t* lengths,
+                               const void* mbuf, const float* logits, float* loss, float* dy, float* dW, float* db,
+                               char* W, hipStream_t st) {
+    float* lse = (float*)(W + P.w_lse);
+    float* ninv = (float*)(W + P.w_ninv);
+    launch_ce_loss(logits, tgt, lengths, P.T, P.B, P.V, lse, (float*)(W + P.w_rowloss), (float*)(W + P.w_rowok), loss,
+                   ninv, st);
+    launch_ce_grad<E>(logits, tgt, lengths, lse, ninv, P.T, P.B, P.V, P.BP, P.mtiles, W + P.w_da, W + P.w_daT, st);
+    const SiteView site = head_site(P, mbuf);
+    DxArgs a;
+    memset(&a, 0, sizeof(a));
+    a.da[0] = W + P.w_da; a.W[0] = W_fc;
+    a.site = site; a.out = dy; a.scatter = 1; a.D = 1; a.B = P.B; a.G = P.V; a.ldo = P.F;
+    a.T = P.T; a.K = P.F; a.tps = ((P.F + 7) / 8 + 15) / 16; a.mtiles = P.mtiles;
+    a.dense = !P.compact; a.s = P.s;
+    launch_dx<E>(a, P.F, st);
+    WgBatch b;
+    memset(&b, 0, sizeof(b));
+    b.np = 1;
+    WgArgs& g = b.p[0];
+    g.actT = W + P.w_ybT; g.tstride = (long)P.F * P.BP; g.actT_first = nullptr; g.t_first = -1; g.shift = 0;
+    g.daT = W + P.w_daT;
+    g.site = site; g.K = P.F; g.B = P.B; g.BP = P.BP; g.G = P.V; g.T = P.T;
+    g.dense = !P.compact; g.s = P.s;
+    g.out = dW; g.db = db;
+    g.full = P.p == 0.0 || !P.compact;
+    launch_wgrad<E>(b, st);
+}
+
 extern "C" {
 
 int lstm_sd_version(void) { return 1; }
@@ -784,6 +899,104 @@ int lstm_sd_embedding_backward(const lstm_sd_dims* dims, const int32_t* tokens, 
     const SiteView nr0 = site_view(P, mask_buf, P.site_nr(0));
     launch_emb_grad(tokens, P.T * P.B, P.B, vocab, dx, nr0, P.I, d_emb, (hipStream_t)stream);
     return hip_check("embedding gradient launch");
+}
+
+size_t lstm_sd_head_mask_bytes(const lstm_sd_head_dims* hd) {
+    HeadPlan P; const char* why = nullptr;
+    if (int rc = make_head_plan(hd, &P, &why)) { fail(rc, why); return 0; }
+    return P.m_total;
+}
+
+size_t lstm_sd_head_workspace_bytes(const lstm_sd_head_dims* hd) {
+    HeadPlan P; const char* why = nullptr;
+    if (int rc = make_head_plan(hd, &P, &why)) { fail(rc, why); return 0; }
+    return P.w_total;
+}
+
+int lstm_sd_head_mask_layout_get(const lstm_sd_head_dims* hd, lstm_sd_mask_layout* out) {
+    HeadPlan P; const char* why = nullptr;
+    if (int rc = make_head_plan(hd, &P, &why)) return fail(rc, why);
+    if (!out) return fail(LSTM_SD_EINVAL, "out is NULL");
+    out->sites = 1; out->kmax = P.F; out->seq_len = P.T; out->reserved = 0;
+    out->mask_off = P.m_mask; out->keep_off = P.m_keep; out->pos_off = P.m_pos;
+    out->count_off = P.m_count; out->drop_off = P.m_drop; out->dcount_off = P.m_dcount;
+    out->kseg_off = P.m_kseg; out->dseg_off = P.m_dseg;
+    out->total_bytes = P.m_total;
+    return LSTM_SD_OK;
+}
+
+int lstm_sd_head_mask_generate(const lstm_sd_head_dims* hd, uint64_t seed, uint64_t step, void* mask_buf,
+                               size_t mask_bytes, void* stream) {
+    HeadPlan P; const char* why = nullptr;
+    if (int rc = make_head_plan(hd, &P, &why)) return fail(rc, why);
+    if (!mask_buf) return fail(LSTM_SD_EINVAL, "mask_buf is NULL");
+    if (mask_bytes < P.m_total) return fail(LSTM_SD_EWORKSPACE, "mask_bytes smaller than lstm_sd_head_mask_bytes()");
+    MaskArgs a;
+    memset(&a, 0, sizeof(a));
+    char* m = (char*)mask_buf;
+    a.mask = (uint8_t*)(m + P.m_mask);
+    a.keep = (int32_t*)(m + P.m_keep);
+    a.pos = (int32_t*)(m + P.m_pos);
+    a.count = (int32_t*)(m + P.m_count);
+    a.drop = (int32_t*)(m + P.m_drop);
+    a.dcount = (int32_t*)(m + P.m_dcount);
+    a.kseg = (int32_t*)(m + P.m_kseg);
+    a.dseg = (int32_t*)(m + P.m_dseg);
+    a.T = P.T; a.kmax = P.F; a.compact = P.compact; a.generate = 1;
+    a.seed = seed; a.step = step;
+    a.K[0] = P.F;
+    a.sid[0] = P.sid;
+    a.thr[0] = threshold64(P.p);
+    launch_mask_build(a, 1, (hipStream_t)stream);
+    return hip_check("head mask kernel launch");
+}
+
+int lstm_sd_head_forward(const lstm_sd_head_dims* hd, const void* W_fc, const float* b_fc, const float* y,
+                         const void* mask_buf, size_t mask_bytes, float* logits, void* workspace,
+                         size_t workspace_bytes, void* stream) {
+    HeadPlan P; const char* why = nullptr;
+    if (int rc = make_head_plan(hd, &P, &why)) return fail(rc, why);
+    if (!W_fc || !b_fc || !y || !mask_buf || !logits || !workspace)
+        return fail(LSTM_SD_EINVAL, "a required pointer is NULL");
+    if (mask_bytes < P.m_total) return fail(LSTM_SD_EWORKSPACE, "mask_bytes smaller than lstm_sd_head_mask_bytes()");
+    if (workspace_bytes < P.w_total)
+        return fail(LSTM_SD_EWORKSPACE, "workspace_bytes smaller than lstm_sd_head_workspace_bytes()");
+    hipStream_t st = (hipStream_t)stream;
+    char* W = (char*)workspace;
+    FxArgs f;
+    memset(&f, 0, sizeof(f));
+    f.X = W + P.w_yb; f.ldx = P.F; f.W = W_fc; f.K = P.F; f.bias = b_fc; f.site = head_site(P, mask_buf);
+    f.Gx = logits; f.B = P.B; f.G = P.V; f.T = P.T; f.dense = !P.compact; f.s = P.s;
+    if (P.dtype == LSTM_SD_DTYPE_BF16) {
+        launch_head_prep<bf16>(y, W + P.w_yb, W + P.w_ybT, P.T, P.B, P.F, P.BP, st);
+        launch_fx<bf16>(f, st);
+    } else {
+        launch_head_prep<float>(y, W + P.w_yb, W + P.w_ybT, P.T, P.B, P.F, P.BP, st);
+        launch_fx<float>(f, st);
+    }
+    return hip_check("head forward launch");
+}
+
+int lstm_sd_head_backward(const lstm_sd_head_dims* hd, const void* W_fc, const int32_t* targets,
+                          const int32_t* lengths, const void* mask_buf, size_t mask_bytes, const float* logits,
+                          float* loss, float* dy, float* dW_fc, float* db_fc, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+    HeadPlan P; const char* why = nullptr;
+    if (int rc = make_head_plan(hd, &P, &why)) return fail(rc, why);
+    if (!W_fc || !targets || !mask_buf || !logits || !loss || !dy || !dW_fc || !db_fc || !workspace)
+        return fail(LSTM_SD_EINVAL, "a required pointer is NULL");
+    if (mask_bytes < P.m_total) return fail(LSTM_SD_EWORKSPACE, "mask_bytes smaller than lstm_sd_head_mask_bytes()");
+    if (workspace_bytes < P.w_total)
+        return fail(LSTM_SD_EWORKSPACE, "workspace_bytes smaller than lstm_sd_head_workspace_bytes()");
+    if (setup_kernel_attributes()) return fail(LSTM_SD_EHIP, "hipFuncSetAttribute failed");
+    hipStream_t st = (hipStream_t)stream;
+    if (P.dtype == LSTM_SD_DTYPE_BF16)
+        head_backward_impl<bf16>(P, W_fc, targets, lengths, mask_buf, logits, loss, dy, dW_fc, db_fc,
+                                 (char*)workspace, st);
+    else
+        head_backward_impl<float>(P, W_fc, targets, lengths, mask_buf, logits, loss, dy, dW_fc, db_fc,
+                                  (char*)workspace, st);
+    return hip_check("head backward launch");
 }
 
 int lstm_sd_kernel_timer_start(const char* kernel) {

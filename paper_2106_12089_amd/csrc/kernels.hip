@@ -1242,6 +1242,165 @@ __global__ void __launch_bounds__(256) k_emb_grad(const int32_t* tokens, int N, 
         if (own[q]) d_emb[(size_t)(v0 + w + 4 * q) * I + col] = old[q] + tot[q];
 }
 
+// ---------------------------------------------------------------------------
+// Output head of a language model (pre-FC output dropout, FC layer, softmax
+// cross-entropy).  The FC products run on the input-product, dX and weight-
+// gradient kernels above (K = the LSTM output width, G = the vocabulary);
+// these kernels prepare their operands.
+
+// y [T][B][F] f32 -> yb [T][B][F] and ybT [T][F][BP] in the compute type
+// (rows b >= B of ybT are zero).  grid (ceil(F/32), BP/32, T), block 256.
+template <typename T>
+__global__ void __launch_bounds__(256) k_head_prep(const float* y, T* yb, T* ybT, int B, int F, int BP) {
+    __shared__ float tile[32][33];
+    const int f0 = blockIdx.x * 32, b0 = blockIdx.y * 32, t = blockIdx.z;
+    const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+    for (int r = ty; r < 32; r += 8) {
+        const int b = b0 + r, f = f0 + tx;
+        float v = 0.0f;
+        if (b < B && f < F) {
+            v = y[((size_t)t * B + b) * F + f];
+            yb[((size_t)t * B + b) * F + f] = from_f32<T>(v);
+        }
+        tile[r][tx] = v;
+    }
+    __syncthreads();
+    for (int r = ty; r < 32; r += 8) {
+        const int f = f0 + r, b = b0 + tx;
+        if (f < F) ybT[((size_t)t * F + f) * BP + b] = from_f32<T>(tile[tx][r]);
+    }
+}
+
+__device__ __forceinline__ bool ce_row_valid(const int32_t* tgt, const int32_t* lengths, int t, int b, int B, int V) {
+    const int g = tgt[(size_t)t * B + b];
+    return g >= 0 && g < V && (!lengths || t < lengths[b]);
+}
+
+// Per row (t, b) of the logits: lse = log sum_v exp z_v (one pass, a running
+// maximum per thread, merged in a fixed tree), the row's loss
+// lse - z[target] and whether it counts.  grid T*B, block 256.
+__global__ void __launch_bounds__(256) k_ce_rows(const float* z, const int32_t* tgt, const int32_t* lengths, int B,
+                                                 int V, float* lse, float* rowloss, float* rowok) {
+    __shared__ float sm[256], ss[256];
+    const long row = blockIdx.x;
+    const int t = (int)(row / B), b = (int)(row % B);
+    const float* zr = z + row * V;
+    float m = -INFINITY, sum = 0.0f;
+    for (int v = threadIdx.x; v < V; v += 256) {
+        const float x = zr[v];
+        if (x > m) {
+            sum = sum * expf(m - x) + 1.0f;
+            m = x;
+        } else {
+            sum += expf(x - m);
+        }
+    }
+    sm[threadIdx.x] = m;
+    ss[threadIdx.x] = sum;
+    __syncthreads();
+    for (int h = 128; h > 0; h >>= 1) {
+        if (threadIdx.x < h) {
+            const float m1 = sm[threadIdx.x], m2 = sm[threadIdx.x + h];
+            const float mm = fmaxf(m1, m2);
+            const float s1 = m1 == -INFINITY ? 0.0f : ss[threadIdx.x] * expf(m1 - mm);
+            const float s2 = m2 == -INFINITY ? 0.0f : ss[threadIdx.x + h] * expf(m2 - mm);
+            sm[threadIdx.x] = mm;
+            ss[threadIdx.x] = s1 + s2;
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        const float l = sm[0] + logf(ss[0]);
+        const bool ok = ce_row_valid(tgt, lengths, t, b, B, V);
+        lse[row] = l;
+        rowloss[row] = ok ? l - zr[tgt[row]] : 0.0f;
+        rowok[row] = ok ? 1.0f : 0.0f;
+    }
+}
+
+// loss = sum of the row losses / N, ninv = 1/N (0 when N = 0), N = rows that
+// count; a fixed summation order.  One workgroup of 256.
+__global__ void __launch_bounds__(256) k_ce_final(const float* rowloss, const float* rowok, long n, float* loss,
+                                                  float* ninv) {
+    __shared__ float sl[256], sn[256];
+    float a = 0.0f, c = 0.0f;
+    for (long i = threadIdx.x; i < n; i += 256) {
+        a += rowloss[i];
+        c += rowok[i];
+    }
+    sl[threadIdx.x] = a;
+    sn[threadIdx.x] = c;
+    __syncthreads();
+    for (int h = 128; h > 0; h >>= 1) {
+        if (threadIdx.x < h) {
+            sl[threadIdx.x] += sl[threadIdx.x + h];
+            sn[threadIdx.x] += sn[threadIdx.x + h];
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        const float N = sn[0];
+        loss[0] = N > 0.0f ? sl[0] / N : 0.0f;
+        ninv[0] = N > 0.0f ? 1.0f / N : 0.0f;
+    }
+}
+
+// dz = (softmax(z) - onehot(target)) / N on rows that count, 0 elsewhere,
+// written in the compute type twice: fragment-major per t (the A operand of
+// the dX product) and transposed [T][V][BP] (the weight-gradient operand).
+// grid (ceil(V/64), T), block 256: a workgroup owns 64 columns of one t and
+// walks the rows 32 at a time through an LDS tile.
+template <typename T>
+__global__ void __launch_bounds__(256) k_ce_grad(const float* z, const int32_t* tgt, const int32_t* lengths,
+                                                 const float* lse, const float* ninv, int B, int V, int BP,
+                                                 int mtiles, T* da, T* daT) {
+    __shared__ float tile[32][65];
+    const int v0 = blockIdx.x * 64, t = blockIdx.y;
+    const int tid = threadIdx.x;
+    const float sc = ninv[0];
+    const int nchunk = (V + 31) / 32;
+    const size_t das = (size_t)nchunk * mtiles * 512;
+    T* dat = da + (size_t)t * das;
+    for (int b0 = 0; b0 < BP; b0 += 32) {
+        for (int r = tid >> 6; r < 32; r += 4) {
+            const int b = b0 + r, v = v0 + (tid & 63);
+            float d = 0.0f;
+            if (b < B && v < V && ce_row_valid(tgt, lengths, t, b, B, V)) {
+                const size_t row = (size_t)t * B + b;
+                d = (expf(z[row * V + v] - lse[row]) - (v == tgt[row] ? 1.0f : 0.0f)) * sc;
+            }
+            tile[r][tid & 63] = d;
+        }
+        __syncthreads();
+        {   // transposed: thread -> column v0 + tid/4, rows 8*(tid%4) .. +7
+            const int v = v0 + (tid >> 2), r0 = 8 * (tid & 3);
+            if (v < V) {
+                T o[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) o[e] = from_f32<T>(tile[r0 + e][tid >> 2]);
+                T* dst = daT + ((size_t)t * V + v) * BP + b0 + r0;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) dst[e] = o[e];
+            }
+        }
+        {   // fragment-major: 2 chunks x 2 row tiles, one 16x32 fragment per wave
+            const int f = tid >> 6, lane = tid & 63;
+            const int cc = f & 1, mm = f >> 1;
+            const int c = (v0 >> 5) + cc, mt = (b0 >> 4) + mm;
+            if (c < nchunk && mt < mtiles) {
+                const int r = 16 * mm + (lane & 15), k0 = 32 * cc + 8 * (lane >> 4);
+                T o[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) o[e] = from_f32<T>(tile[r][k0 + e]);
+                T* dst = dat + frag_lane_off(c, mt, lane, mtiles);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) dst[e] = o[e];
+            }
+        }
+        __syncthreads();
+    }
+}
+
 // MSE loss gradient (a loss of the synthetic workloads).
 __device__ __forceinline__ float nvalid_rows(const int32_t* lengths, int B, int T) {
     if (!lengths) return (float)B * T;
@@ -1297,9 +1456,10 @@ __global__ void __launch_bounds__(256) k_mse_final(const float* partial, int np,
 // Kernel timer (instrumentation): HIP event pairs around the launches of one
 // kernel class.
 enum KernelId { KID_NONE = -1, KID_MASK, KID_TRANS, KID_FX, KID_STEP, KID_BWD, KID_DX, KID_WGRAD, KID_FWDP, KID_BWDP,
-                KID_EMB, KID_COUNT };
+                KID_EMB, KID_CE, KID_COUNT };
 static const char* const kKernelNames[KID_COUNT] = {"mask_build", "transpose", "fx", "step", "bwd", "dx", "wgrad",
-                                                    "fwd_persist", "bwd_persist", "emb_grad"};
+                                                    "fwd_persist", "bwd_persist", "emb_grad",
+                                                    "ce"};
 static int g_timer_kid = KID_NONE;
 static std::vector<hipEvent_t> g_ev_pool;
 static size_t g_ev_used = 0;
@@ -1445,6 +1605,30 @@ void launch_emb_grad(const int32_t* tokens, int N, int B, int V, const float* dx
     launch_k(KID_EMB, k_emb_grad, dim3((V + EM_VB - 1) / EM_VB, (I + EM_CW - 1) / EM_CW), dim3(256), 0, st, tokens, N,
              B, V, dx, nr0, I, d_emb);
 }
+template <typename T>
+void launch_head_prep(const float* y, void* yb, void* ybT, int T_, int B, int F, int BP, hipStream_t st) {
+    launch_k(KID_NONE, k_head_prep<T>, dim3((F + 31) / 32, BP / 32, T_), dim3(256), 0, st, y, (T*)yb, (T*)ybT, B, F,
+             BP);
+}
+template void launch_head_prep<float>(const float*, void*, void*, int, int, int, int, hipStream_t);
+template void launch_head_prep<bf16>(const float*, void*, void*, int, int, int, int, hipStream_t);
+void launch_ce_loss(const float* z, const int32_t* tgt, const int32_t* lengths, int T_, int B, int V, float* lse,
+                    float* rowloss, float* rowok, float* loss, float* ninv, hipStream_t st) {
+    launch_k(KID_CE, k_ce_rows, dim3((unsigned)((long)T_ * B)), dim3(256), 0, st, z, tgt, lengths, B, V, lse, rowloss,
+             rowok);
+    launch_k(KID_CE, k_ce_final, dim3(1), dim3(256), 0, st, (const float*)rowloss, (const float*)rowok, (long)T_ * B,
+             loss, ninv);
+}
+template <typename T>
+void launch_ce_grad(const float* z, const int32_t* tgt, const int32_t* lengths, const float* lse, const float* ninv,
+                    int T_, int B, int V, int BP, int mtiles, void* da, void* daT, hipStream_t st) {
+    launch_k(KID_CE, k_ce_grad<T>, dim3((V + 63) / 64, T_), dim3(256), 0, st, z, tgt, lengths, lse, ninv, B, V, BP,
+             mtiles, (T*)da, (T*)daT);
+}
+template void launch_ce_grad<float>(const float*, const int32_t*, const int32_t*, const float*, const float*, int,
+                                    int, int, int, int, void*, void*, hipStream_t);
+template void launch_ce_grad<bf16>(const float*, const int32_t*, const int32_t*, const float*, const float*, int,
+                                   int, int, int, int, void*, void*, hipStream_t);
 void launch_mse(const float* y, const float* tg, const int32_t* lengths, float* dy, float* partial, int np,
                 float* loss, int T, int B, int F, hipStream_t st) {
     launch_k(KID_NONE, k_mse, dim3(np), dim3(256), 0, st, y, tg, lengths, dy, partial, T, B, F);

@@ -131,3 +131,59 @@ class Session:
         return dict(y=g(self.y), hT=g(self.hT), cT=g(self.cT), dx=g(self.dx), dh0=g(self.dh0),
                     dc0=g(self.dc0), dW=[g(t) for t in self.dW], dU=[g(t) for t in self.dU],
                     db=[g(t) for t in self.db], loss=float(self.loss.item()), dy=g(self.dy))
+
+
+class HeadSession:
+    """Buffers and calls of a language model's output head (pre-FC structured
+    output dropout, FC layer, softmax cross-entropy) on the top output of an
+    L-layer stack.
+
+    wl:      a workload with W_fc [F][V], b_fc [V] and targets [T][B]
+    p_out:   output dropout rate; compact: 1 = method, 0 = dense
+    """
+
+    def __init__(self, wl, p_out: float, compact: int, device: str = "cuda:0"):
+        cfg = wl.cfg
+        self.cfg, self.wl = cfg, wl
+        dev = torch.device(device)
+        self.T, self.B = wl.x.shape[0], wl.x.shape[1]
+        self.F, self.V = wl.W_fc.shape
+        bf16 = cfg.dtype == "bf16"
+        dt = torch.bfloat16 if bf16 else torch.float32
+        self.hd = B_.make_head_dims(self.F, self.V, self.B, self.T, B_.DTYPE_BF16 if bf16 else B_.DTYPE_F32,
+                                    compact, 4 * cfg.num_layers, p_out)
+        f = lambda a, t=torch.float32: torch.from_numpy(np.ascontiguousarray(a)).to(dev).to(t)
+        self.W_fc = f(wl.W_fc, dt)
+        self.b_fc = f(wl.b_fc)
+        self.targets = f(wl.targets, torch.int32)
+        self.lengths = None if wl.lengths is None else f(wl.lengths, torch.int32)
+        u8 = torch.uint8
+        self.mask_buf = torch.zeros(B_.lstm_sd_head_mask_bytes(self.hd), dtype=u8, device=dev)
+        self.workspace = torch.zeros(B_.lstm_sd_head_workspace_bytes(self.hd), dtype=u8, device=dev)
+        z = lambda *s: torch.zeros(*s, dtype=torch.float32, device=dev)
+        self.logits = z(self.T, self.B, self.V)
+        self.loss = z(1)
+        self.dy = z(self.T, self.B, self.F)
+        self.dW = z(self.F, self.V)
+        self.db = z(self.V)
+
+    def masks(self, seed: int, step: int):
+        B_.lstm_sd_head_mask_generate(self.hd, seed, step, self.mask_buf)
+
+    def forward(self, y):
+        B_.lstm_sd_head_forward(self.hd, self.W_fc, self.b_fc, y, self.mask_buf, self.logits, self.workspace)
+
+    def backward(self):
+        B_.lstm_sd_head_backward(self.hd, self.W_fc, self.targets, self.lengths, self.mask_buf, self.logits,
+                                 self.loss, self.dy, self.dW, self.db, self.workspace)
+
+    def mask_view(self):
+        """The output mask bytes [T][F] (1 = kept)."""
+        lay = B_.lstm_sd_head_mask_layout_get(self.hd)
+        raw = self.mask_buf.cpu().numpy()
+        return raw[lay.mask_off:lay.mask_off + self.T * self.F].reshape(self.T, self.F)
+
+    def outputs(self):
+        g = lambda t: t.detach().float().cpu().numpy().astype(np.float64)
+        return dict(z=g(self.logits), loss=float(self.loss.item()), dy=g(self.dy), dW=g(self.dW),
+                    dc=g(self.db))

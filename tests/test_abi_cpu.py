@@ -103,3 +103,55 @@ def test_forward_rejects_small_reserve_before_device_work():
     rc = lib.lstm_sd_forward(ctypes.byref(d), ctypes.byref(w), fake, None, fake, fake, fake, mb, fake, fake,
                              fake, fake, 1, fake, 10**9, None)
     assert rc == B.EWORKSPACE and "reserve" in B.lstm_sd_last_error()
+
+
+def head_dims(**kw):
+    base = dict(features=650, vocab=10000, batch=20, seq_len=35, dtype=B.DTYPE_BF16, compact=1, stream_id=8,
+                p_out=0.5)
+    base.update(kw)
+    return B.make_head_dims(**base)
+
+
+def test_head_sizes_and_layout():
+    hd = head_dims()
+    mb = B.lstm_sd_head_mask_bytes(hd)
+    lay = B.lstm_sd_head_mask_layout_get(hd)
+    assert lay.sites == 1 and lay.kmax == 650 and lay.seq_len == 35 and lay.total_bytes == mb
+    assert lay.mask_off == 0 and lay.keep_off >= 35 * 650
+    ws = B.lstm_sd_head_workspace_bytes(hd)
+    # at least: the prepared input twice and the loss gradient twice (compute type)
+    assert ws >= 2 * (35 * 20 * 650 * 2) and ws >= 35 * 10000 * 32 * 2
+    assert B.lstm_sd_head_workspace_bytes(head_dims(batch=40)) > ws
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(features=0), B.EINVAL), (dict(vocab=0), B.EINVAL), (dict(p_out=1.0), B.EINVAL),
+    (dict(compact=3), B.EINVAL), (dict(stream_id=-1), B.EINVAL), (dict(dtype=5), B.EUNSUPPORTED),
+    (dict(features=4096), B.EUNSUPPORTED), (dict(vocab=10002), B.EUNSUPPORTED),
+    (dict(features=2048, vocab=600000), B.EUNSUPPORTED),
+])
+def test_head_invalid_dims_rejected(kw, code):
+    lib = B.load()
+    hd = head_dims(**kw)
+    assert lib.lstm_sd_head_mask_bytes(ctypes.byref(hd)) == 0
+    assert lib.lstm_sd_head_workspace_bytes(ctypes.byref(hd)) == 0
+    assert lib.lstm_sd_head_mask_generate(ctypes.byref(hd), 1, 0, None, 0, None) == code
+    assert lib.lstm_sd_head_forward(ctypes.byref(hd), *([None] * 4), 0, None, None, 0, None) == code
+    assert lib.lstm_sd_head_backward(ctypes.byref(hd), *([None] * 4), 0, *([None] * 6), 0, None) == code
+
+
+def test_head_null_pointers_and_small_buffers_rejected():
+    lib = B.load()
+    hd = head_dims(features=16, vocab=64, batch=2, seq_len=3)
+    fake = 4096  # never dereferenced: the checks fail first
+    mb = B.lstm_sd_head_mask_bytes(hd)
+    ws = B.lstm_sd_head_workspace_bytes(hd)
+    assert lib.lstm_sd_head_mask_generate(ctypes.byref(hd), 1, 0, fake, mb - 1, None) == B.EWORKSPACE
+    assert lib.lstm_sd_head_forward(ctypes.byref(hd), fake, None, fake, fake, mb, fake, fake, ws, None) == B.EINVAL
+    assert lib.lstm_sd_head_forward(ctypes.byref(hd), fake, fake, fake, fake, mb, fake, fake, ws - 1,
+                                    None) == B.EWORKSPACE
+    assert lib.lstm_sd_head_backward(ctypes.byref(hd), fake, fake, None, fake, mb, fake, fake, fake, fake, None,
+                                     fake, ws, None) == B.EINVAL
+    assert lib.lstm_sd_head_backward(ctypes.byref(hd), fake, fake, None, fake, mb - 1, fake, fake, fake, fake,
+                                     fake, fake, ws, None) == B.EWORKSPACE
+    assert lib.lstm_sd_head_mask_layout_get(ctypes.byref(hd), None) == B.EINVAL
