@@ -237,8 +237,122 @@ def run_embedding(wl, p_nr, steps, warmup):
     torch.cuda.synchronize()
     us = 1e3 * ms / max(n, 1)
     b = float(np.mean(nbytes))
-    return {"avg_us": round(us, 3), "launches_per_step": n / steps, "bytes_per_launch": int(b),
-            "achieved_gbs": round(b / (us * 1e-6) / 1e9, 1), "vocab": cfg.vocab, "rows_touched": rows}
+    a = b / (us * 1e-6) / 1e9
+    return {"avg_us": round(us, 3), "launches_per_step": n / steps, "vocab": cfg.vocab, "rows_touched": rows,
+            "roofline": {"bound": "hbm", "achieved": round(a, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                         "frac": round(a / PEAK_HBM_GBS, 5), "kernel": "emb_grad",
+                         "algorithmic_bytes_per_launch": int(b), "traffic": None}}
+
+
+def run_head(wl, p, steps, warmup, compact):
+    """The output head (pre-FC structured dropout, FC layer, softmax
+    cross-entropy) alone, and the whole LM step with it (LSTM forward, head,
+    LSTM backward fed by the head's dy), timed with events on the stream;
+    FC FLOPs counted over the kept input columns (forward, dX and dW
+    products: 3 * 2 * B * V per kept (t, column))."""
+    import torch
+    from paper_2106_12089_amd import binding as B_
+    from paper_2106_12089_amd.session import HeadSession, Session
+    cfg = wl.cfg
+    h = HeadSession(wl, p, compact)
+    s = Session(wl, p, 0.0, compact)
+    s.masks(cfg.mask_seed, 0)
+    s.forward()
+    torch.cuda.synchronize()
+
+    def head_step(i):
+        h.masks(cfg.mask_seed, i)
+        h.forward(s.y)
+        h.backward()
+
+    def lm_step(i):
+        s.masks(cfg.mask_seed, i)
+        h.masks(cfg.mask_seed, i)
+        s.forward()
+        h.forward(s.y)
+        h.backward()
+        s.backward(dy=h.dy)
+
+    out = {}
+    for name, fn in (("head", head_step), ("lm_step", lm_step)):
+        for i in range(warmup):
+            fn(10_000 + i)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for i in range(steps):
+            fn(i)
+        e1.record()
+        torch.cuda.synchronize()
+        out[name] = e0.elapsed_time(e1) / steps
+    kept = []
+    for i in range(steps):
+        h.masks(cfg.mask_seed, i)
+        kept.append(int(h.mask_view().sum()) if compact else h.T * h.F)
+    out["flops"] = 6.0 * h.B * h.V * float(np.mean(kept))
+    ktime = {}
+    for kname in ("fx", "dx", "wgrad", "ce"):
+        B_.lstm_sd_kernel_timer_start(kname)
+        for i in range(steps):
+            head_step(i)
+        ms, n = B_.lstm_sd_kernel_timer_stop()
+        torch.cuda.synchronize()
+        ktime[kname] = round(1e3 * ms / steps, 2)
+    out["kernels_us_per_step"] = ktime
+    # algorithmic work per launch (each operand once, each result once)
+    es = 2 if cfg.dtype == "bf16" else 4
+    T, B, F, V = h.T, h.B, h.F, h.V
+    kf = out["flops"] / 3.0                    # one FC product over the kept columns
+    out["work"] = {
+        "fx": dict(bytes=T * B * F * es + F * V * es + V * 4 + T * B * V * 4, flops=kf),
+        "dx": dict(bytes=T * B * V * es + F * V * es + T * B * F * 4, flops=kf),
+        "wgrad": dict(bytes=T * F * B * es + T * V * B * es + F * V * 4 + V * 4, flops=kf),
+        "ce": dict(bytes=T * B * V * 4 + 2 * T * B * V * es + T * B * 4, flops=0.0),
+    }
+    return out
+
+
+def head_roofline(hc, cfg):
+    """Roofline of the head's dominant kernel (by time): HBM-bound when its
+    arithmetic intensity is below the ridge point, else MFMA-bound."""
+    k = max(hc["kernels_us_per_step"], key=hc["kernels_us_per_step"].get)
+    us = hc["kernels_us_per_step"][k]
+    w = hc["work"][k]
+    peak_f = PEAK_TFLOPS["bf16" if cfg.dtype == "bf16" else "f32"]
+    ridge = peak_f * 1e12 / (PEAK_HBM_GBS * 1e9)
+    if w["flops"] / w["bytes"] >= ridge:
+        a = w["flops"] / (us * 1e-6) / 1e12
+        r = dict(bound="mfma", achieved=round(a, 3), peak=peak_f, unit="TFLOP/s", frac=round(a / peak_f, 5))
+    else:
+        a = w["bytes"] / (us * 1e-6) / 1e9
+        r = dict(bound="hbm", achieved=round(a, 1), peak=PEAK_HBM_GBS, unit="GB/s", frac=round(a / PEAK_HBM_GBS, 5))
+    r.update(kernel=k, launch_us=us, algorithmic_bytes_per_launch=int(w["bytes"]),
+             algorithmic_flops_per_launch=w["flops"], traffic=None)
+    return r
+
+
+def head_cpu_baseline(wl, p):
+    """The head's float64 oracle (forward, loss, backward) timed once on the
+    host on the same workload."""
+    from oracle import head, masks
+    cfg = wl.cfg
+    y = np.random.default_rng(0).normal(0.0, 0.5, size=(cfg.seq_len, cfg.batch, wl.W_fc.shape[0]))
+    m = masks.keep_mask(cfg.mask_seed, 0, masks.out_stream(cfg.num_layers), cfg.seq_len, wl.W_fc.shape[0], p)
+    t0 = time.perf_counter()
+    head.head_step(y, wl.W_fc, wl.b_fc, m, p, wl.targets, wl.lengths)
+    return dict(ms_per_step=round((time.perf_counter() - t0) * 1e3, 1), kind="oracle",
+                sample="one head step (forward, loss, backward) of the same workload, float64 NumPy")
+
+
+def embedding_cpu_baseline(wl, p):
+    from oracle import embedding, masks
+    cfg = wl.cfg
+    dx = np.random.default_rng(0).normal(size=(cfg.seq_len, cfg.batch, cfg.input_dim))
+    m = masks.keep_mask(cfg.mask_seed, 0, masks.nr_stream(0), cfg.seq_len, cfg.input_dim, p)
+    t0 = time.perf_counter()
+    embedding.embedding_grad(wl.tokens, dx, m, np.zeros((cfg.vocab, cfg.input_dim)))
+    return dict(ms_per_step=round((time.perf_counter() - t0) * 1e3, 2), kind="oracle",
+                sample="one embedding-gradient call of the same workload, float64 NumPy loop")
 
 
 def roofline(res, cfg):
@@ -360,6 +474,7 @@ def main(argv=None):
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--no-nrrh", action="store_true", help="skip the NR+RH+ST runs")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense comparison runs (counter passes)")
+    ap.add_argument("--no-head", action="store_true", help="skip the language-model output head runs")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="also run a plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -415,6 +530,24 @@ def main(argv=None):
                        "phases_ms": {k: round(v, 4) for k, v in r["phases"].items()}}
     if wl.tokens is not None:
         out["embedding_backward"] = run_embedding(wl, p, args.steps, args.warmup)
+        if not args.no_cpu:
+            out["embedding_backward"]["cpu_baseline"] = embedding_cpu_baseline(wl, p)
+    if wl.W_fc is not None and not args.no_head:
+        hc = run_head(wl, p, args.steps, args.warmup, 1)
+        hd = None if args.no_dense else run_head(wl, p, args.steps, args.warmup, 0)
+        out["head"] = {"vocab": int(wl.W_fc.shape[1]), "p_out": p, "ms_per_step": round(hc["head"], 4),
+                       "dense_ms_per_step": round(hd["head"], 4) if hd else None,
+                       "speedup_vs_dense": round(hd["head"] / hc["head"], 4) if hd else None,
+                       "tflops": round(hc["flops"] / (hc["head"] * 1e-3) / 1e12, 2),
+                       "gflop_per_step": round(hc["flops"] / 1e9, 3),
+                       "kernels_us_per_step": hc["kernels_us_per_step"],
+                       "kernels_us_per_step_dense": hd["kernels_us_per_step"] if hd else None,
+                       "roofline": head_roofline(hc, cfg)}
+        if not args.no_cpu:
+            out["head"]["cpu_baseline"] = head_cpu_baseline(wl, p)
+        out["lm_step_with_head"] = {"ms_per_step": round(hc["lm_step"], 4),
+                                    "dense_ms_per_step": round(hd["lm_step"], 4) if hd else None,
+                                    "speedup_vs_dense": round(hd["lm_step"] / hc["lm_step"], 4) if hd else None}
     if args.calibrate_copy:
         n = args.calibrate_copy * (1 << 20) // 4
         a = torch.ones(n, dtype=torch.float32, device="cuda")

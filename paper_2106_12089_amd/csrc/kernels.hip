@@ -1276,44 +1276,65 @@ __device__ __forceinline__ bool ce_row_valid(const int32_t* tgt, const int32_t* 
     return g >= 0 && g < V && (!lengths || t < lengths[b]);
 }
 
-// Per row (t, b) of the logits: lse = log sum_v exp z_v (one pass, a running
-// maximum per thread, merged in a fixed tree), the row's loss
-// lse - z[target] and whether it counts.  grid T*B, block 256.
+// fixed-order sum / maximum over a 256-thread block (wave shuffles, then the
+// four wave results in order); every thread gets the result
+__device__ __forceinline__ float block_max256(float v, float* red) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+    __syncthreads();
+    return fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+}
+__device__ __forceinline__ float block_sum256(float v, float* red) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+    __syncthreads();
+    return ((red[0] + red[1]) + red[2]) + red[3];
+}
+
+// Per row (t, b) of the logits: lse = log sum_v exp z_v (a pass for the
+// maximum, a pass for the sum; 16-byte loads, four in flight per thread),
+// the row's loss lse - z[target] and whether it counts.  grid T*B, block 256.
 __global__ void __launch_bounds__(256) k_ce_rows(const float* z, const int32_t* tgt, const int32_t* lengths, int B,
                                                  int V, float* lse, float* rowloss, float* rowok) {
-    __shared__ float sm[256], ss[256];
+    __shared__ float red[4];
     const long row = blockIdx.x;
     const int t = (int)(row / B), b = (int)(row % B);
-    const float* zr = z + row * V;
-    float m = -INFINITY, sum = 0.0f;
-    for (int v = threadIdx.x; v < V; v += 256) {
-        const float x = zr[v];
-        if (x > m) {
-            sum = sum * expf(m - x) + 1.0f;
-            m = x;
-        } else {
-            sum += expf(x - m);
+    const float4* z4 = (const float4*)(z + row * V);   // V is a multiple of 4
+    const int n4 = V >> 2, tid = threadIdx.x;
+    float m = -INFINITY;
+    for (int i0 = tid; i0 < n4; i0 += 1024) {
+        float4 q[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int i = i0 + 256 * u;
+            q[u] = i < n4 ? z4[i] : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
         }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) m = fmaxf(m, fmaxf(fmaxf(q[u].x, q[u].y), fmaxf(q[u].z, q[u].w)));
     }
-    sm[threadIdx.x] = m;
-    ss[threadIdx.x] = sum;
-    __syncthreads();
-    for (int h = 128; h > 0; h >>= 1) {
-        if (threadIdx.x < h) {
-            const float m1 = sm[threadIdx.x], m2 = sm[threadIdx.x + h];
-            const float mm = fmaxf(m1, m2);
-            const float s1 = m1 == -INFINITY ? 0.0f : ss[threadIdx.x] * expf(m1 - mm);
-            const float s2 = m2 == -INFINITY ? 0.0f : ss[threadIdx.x + h] * expf(m2 - mm);
-            sm[threadIdx.x] = mm;
-            ss[threadIdx.x] = s1 + s2;
+    const float M = block_max256(m, red);
+    float sum = 0.0f;
+    for (int i0 = tid; i0 < n4; i0 += 1024) {
+        float4 q[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int i = i0 + 256 * u;
+            q[u] = i < n4 ? z4[i] : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
         }
-        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            sum += ((expf(q[u].x - M) + expf(q[u].y - M)) + expf(q[u].z - M)) + expf(q[u].w - M);
     }
-    if (threadIdx.x == 0) {
-        const float l = sm[0] + logf(ss[0]);
+    const float S = block_sum256(sum, red);
+    if (tid == 0) {
+        const float l = M + logf(S);
         const bool ok = ce_row_valid(tgt, lengths, t, b, B, V);
         lse[row] = l;
-        rowloss[row] = ok ? l - zr[tgt[row]] : 0.0f;
+        rowloss[row] = ok ? l - z[row * V + tgt[row]] : 0.0f;
         rowok[row] = ok ? 1.0f : 0.0f;
     }
 }
@@ -1345,6 +1366,19 @@ __global__ void __launch_bounds__(256) k_ce_final(const float* rowloss, const fl
     }
 }
 
+// 8 consecutive values to 16-byte-aligned memory in the compute type, as
+// whole 16-byte stores
+__device__ __forceinline__ void st8(bf16* dst, const float* v) {
+    uint32_t w[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) w[q] = (uint32_t)f2bf(v[2 * q]) | ((uint32_t)f2bf(v[2 * q + 1]) << 16);
+    *(uint4*)dst = make_uint4(w[0], w[1], w[2], w[3]);
+}
+__device__ __forceinline__ void st8(float* dst, const float* v) {
+    ((float4*)dst)[0] = make_float4(v[0], v[1], v[2], v[3]);
+    ((float4*)dst)[1] = make_float4(v[4], v[5], v[6], v[7]);
+}
+
 // dz = (softmax(z) - onehot(target)) / N on rows that count, 0 elsewhere,
 // written in the compute type twice: fragment-major per t (the A operand of
 // the dX product) and transposed [T][V][BP] (the weight-gradient operand).
@@ -1361,26 +1395,37 @@ __global__ void __launch_bounds__(256) k_ce_grad(const float* z, const int32_t* 
     const int nchunk = (V + 31) / 32;
     const size_t das = (size_t)nchunk * mtiles * 512;
     T* dat = da + (size_t)t * das;
+    __shared__ int rtgt[32];                   // target of each row of the block, -1 if the row does not count
+    __shared__ float rlse[32];
     for (int b0 = 0; b0 < BP; b0 += 32) {
-        for (int r = tid >> 6; r < 32; r += 4) {
-            const int b = b0 + r, v = v0 + (tid & 63);
-            float d = 0.0f;
-            if (b < B && v < V && ce_row_valid(tgt, lengths, t, b, B, V)) {
-                const size_t row = (size_t)t * B + b;
-                d = (expf(z[row * V + v] - lse[row]) - (v == tgt[row] ? 1.0f : 0.0f)) * sc;
-            }
-            tile[r][tid & 63] = d;
+        if (tid < 32) {
+            const int b = b0 + tid;
+            const bool ok = b < B && ce_row_valid(tgt, lengths, t, b, B, V);
+            rtgt[tid] = ok ? tgt[(size_t)t * B + b] : -1;
+            rlse[tid] = ok ? lse[(size_t)t * B + b] : 0.0f;
+        }
+        __syncthreads();
+        const int v = v0 + (tid & 63);
+        float zv[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {              // independent loads, all in flight
+            const int r = (tid >> 6) + 4 * i;
+            zv[i] = (rtgt[r] >= 0 && v < V) ? z[((size_t)t * B + b0 + r) * V + v] : 0.0f;
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int r = (tid >> 6) + 4 * i;
+            tile[r][tid & 63] = (rtgt[r] >= 0 && v < V) ? (expf(zv[i] - rlse[r]) - (v == rtgt[r] ? 1.0f : 0.0f)) * sc
+                                                        : 0.0f;
         }
         __syncthreads();
         {   // transposed: thread -> column v0 + tid/4, rows 8*(tid%4) .. +7
             const int v = v0 + (tid >> 2), r0 = 8 * (tid & 3);
             if (v < V) {
-                T o[8];
+                float o[8];
 #pragma unroll
-                for (int e = 0; e < 8; ++e) o[e] = from_f32<T>(tile[r0 + e][tid >> 2]);
-                T* dst = daT + ((size_t)t * V + v) * BP + b0 + r0;
-#pragma unroll
-                for (int e = 0; e < 8; ++e) dst[e] = o[e];
+                for (int e = 0; e < 8; ++e) o[e] = tile[r0 + e][tid >> 2];
+                st8(daT + ((size_t)t * V + v) * BP + b0 + r0, o);
             }
         }
         {   // fragment-major: 2 chunks x 2 row tiles, one 16x32 fragment per wave
@@ -1389,12 +1434,10 @@ __global__ void __launch_bounds__(256) k_ce_grad(const float* z, const int32_t* 
             const int c = (v0 >> 5) + cc, mt = (b0 >> 4) + mm;
             if (c < nchunk && mt < mtiles) {
                 const int r = 16 * mm + (lane & 15), k0 = 32 * cc + 8 * (lane >> 4);
-                T o[8];
+                float o[8];
 #pragma unroll
-                for (int e = 0; e < 8; ++e) o[e] = from_f32<T>(tile[r][k0 + e]);
-                T* dst = dat + frag_lane_off(c, mt, lane, mtiles);
-#pragma unroll
-                for (int e = 0; e < 8; ++e) dst[e] = o[e];
+                for (int e = 0; e < 8; ++e) o[e] = tile[r][k0 + e];
+                st8(dat + frag_lane_off(c, mt, lane, mtiles), o);
             }
         }
         __syncthreads();
