@@ -1157,22 +1157,25 @@ __global__ void k_bwd_init(const float* dhT, const float* dcT, float* dhc, float
 // gradient dx_t[b] is added into row tokens[t][b] of d_emb, over the columns
 // kept at t (the dropped columns of dx are zero, Eq. 10).  grid
 // (ceil(V/EM_VB), ceil(I/EM_CW)): a workgroup owns EM_VB token ids and EM_CW
-// columns (lane = column); block 256 (4 waves).  Wave w scans the position
-// groups w, w+4, ... (64 positions each, ascending), picks the positions
-// whose token it owns with a ballot, loads their dx rows EM_BATCH at a time
-// (independent loads in flight) and adds them into its own partial sums in
-// LDS with LDS float adds: one wave's LDS operations complete in issue
-// order, so each partial is summed in ascending position order.  Then the
-// wave that owns token j (j mod 4) adds the four partials in wave order and
-// writes row j once (all its loads before its stores): a fixed summation
-// order, no global atomics, the same result on every run.  A Zipf-distributed
-// text puts most positions in the first workgroup's range; its waves still
-// share them evenly.
-constexpr int EM_VB = 64, EM_CW = 64, EM_BATCH = 16;
+// columns (lane = column); block 256 (4 waves).  Wave w takes the position
+// groups w, w+4, ... (64 positions each, ascending), loading the token ids of
+// EM_TG groups at once, and lists the positions whose token it owns, in
+// order, in LDS (a ballot and a prefix count per group).  It then walks its
+// list EM_BATCH positions at a time (their dx values and mask bytes all in
+// flight) and adds them into its own partial sums in LDS, in list order (a
+// plain read-modify-write: LDS float atomics, back to back on the rows of a
+// frequent token, were twice as slow), so each partial is summed in
+// ascending position order.  Finally the wave that owns token j
+// (j mod 4) adds the four partials in wave order and writes row j once (all
+// its loads before its stores): a fixed summation order, no global atomics,
+// the same result on every run.  A Zipf-distributed text puts most positions
+// in the first workgroup's range; its four waves still share them.
+constexpr int EM_VB = 64, EM_CW = 64, EM_BATCH = 16, EM_TG = 4, EM_LIST = 256;
 
 __global__ void __launch_bounds__(256) k_emb_grad(const int32_t* tokens, int N, int B, int V, const float* dx,
                                                   SiteView nr0, int I, float* d_emb) {
     __shared__ float part[4][EM_VB][EM_CW];
+    __shared__ int lpos[4][EM_LIST], lj[4][EM_LIST], lm[4][EM_LIST];   // position, token - v0, mask row offset
     __shared__ int touched[EM_VB];
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -1185,30 +1188,16 @@ __global__ void __launch_bounds__(256) k_emb_grad(const int32_t* tokens, int N, 
     for (int i = lane; i < EM_VB * EM_CW / 4; i += 64) pz[i] = make_float4(0.f, 0.f, 0.f, 0.f);
     if (tid < EM_VB) touched[tid] = 0;
     __syncthreads();
-    for (int g = w * 64; g < N; g += 256) {
-        const int pos = g + lane;
-        const int tk = pos < N ? tokens[pos] : -1;
-        const bool act = tk >= v0 && tk - v0 < vn;     // (tk >= v0 >= 0: no wrap-around)
-        const int j = act ? tk - v0 : 0;
-        const int moff = (pos < N ? pos / B : 0) * nr0.kmax;
-        uint64_t left = __builtin_amdgcn_ballot_w64(act);
-        while (left) {
+    // add the listed positions [0, nl) into this wave's partial sums
+    auto drain = [&](int nl) {
+        for (int k0 = 0; k0 < nl; k0 += EM_BATCH) {
             int sp[EM_BATCH], sj[EM_BATCH], sm[EM_BATCH];
-            int nb = 0;
 #pragma unroll
             for (int k = 0; k < EM_BATCH; ++k) {
-                if (left) {
-                    const int idx = __builtin_ctzll(left);
-                    left &= left - 1;
-                    sp[k] = __builtin_amdgcn_readlane(pos, idx);
-                    sj[k] = __builtin_amdgcn_readlane(j, idx);
-                    sm[k] = __builtin_amdgcn_readlane(moff, idx);
-                    nb = k + 1;
-                } else {                               // (a valid position; its value is not added)
-                    sp[k] = sp[0];
-                    sj[k] = sj[0];
-                    sm[k] = sm[0];
-                }
+                const int e = min(k0 + k, nl - 1);     // (past the end: a listed position, not added)
+                sp[k] = lpos[w][e];
+                sj[k] = lj[w][e];
+                sm[k] = lm[w][e];
             }
             float d[EM_BATCH];
             bool m[EM_BATCH];
@@ -1219,13 +1208,38 @@ __global__ void __launch_bounds__(256) k_emb_grad(const int32_t* tokens, int N, 
             }
 #pragma unroll
             for (int k = 0; k < EM_BATCH; ++k)
-                if (k < nb)
-                    __hip_atomic_fetch_add(&part[w][sj[k]][lane], m[k] ? d[k] : 0.0f, __ATOMIC_RELAXED,
-                                           __HIP_MEMORY_SCOPE_WORKGROUP);
+                if (k0 + k < nl) part[w][sj[k]][lane] += m[k] ? d[k] : 0.0f;
             if (lane == 0)
-                for (int k = 0; k < nb; ++k) touched[sj[k]] = 1;
+                for (int k = 0; k < EM_BATCH && k0 + k < nl; ++k) touched[sj[k]] = 1;
+        }
+    };
+    int nl = 0;                                        // (wave-uniform) listed positions
+    for (int g0 = 64 * w; g0 < N; g0 += 256 * EM_TG) {
+        int tk[EM_TG];
+#pragma unroll
+        for (int u = 0; u < EM_TG; ++u) {              // the token ids of EM_TG groups, loaded together
+            const int pos = g0 + 256 * u + lane;
+            tk[u] = pos < N ? tokens[pos] : -1;
+        }
+#pragma unroll
+        for (int u = 0; u < EM_TG; ++u) {
+            const int pos = g0 + 256 * u + lane;
+            const bool act = tk[u] >= v0 && tk[u] - v0 < vn;   // (tk >= v0 >= 0: no wrap-around)
+            const uint64_t bal = __builtin_amdgcn_ballot_w64(act);
+            if (nl + 64 > EM_LIST) {                   // the list could overflow: drain it first
+                drain(nl);
+                nl = 0;
+            }
+            if (act) {
+                const int r = __builtin_popcountll(bal & ((1ull << lane) - 1ull));
+                lpos[w][nl + r] = pos;
+                lj[w][nl + r] = tk[u] - v0;
+                lm[w][nl + r] = (pos / B) * nr0.kmax;
+            }
+            nl += __builtin_popcountll(bal);
         }
     }
+    drain(nl);
     __syncthreads();
     constexpr int NQ = EM_VB / 4;
     float tot[NQ], old[NQ];
