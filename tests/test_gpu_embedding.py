@@ -28,20 +28,23 @@ def _session(cfg, wl, p_nr, p_rh, compact=1):
     return s
 
 
-@pytest.mark.parametrize("p_rh,compact", [(0.0, 1), (0.5, 1), (0.5, 0)])
-def test_lm_medium_step(p_rh, compact):
-    cfg = workloads.get_config("lm_medium")
+@pytest.mark.parametrize("name,p_rh,compact", [("lm_medium", 0.0, 1), ("lm_medium", 0.5, 1), ("lm_medium", 0.5, 0),
+                                               ("lm_large", 0.0, 1), ("seq2seq_enc", 0.0, 1)])
+def test_step(name, p_rh, compact):
+    cfg = workloads.get_config(name)
     wl = workloads.make_workload(cfg)
-    say(f"[gpu] embedding lm_medium p_rh={p_rh} compact={compact}")
-    s = _session(cfg, wl, 0.5, p_rh, compact)
+    p = cfg.p_values[0]
+    p_rh = p if p_rh else 0.0
+    say(f"[gpu] embedding {name} p={p} p_rh={p_rh} compact={compact}")
+    s = _session(cfg, wl, p, p_rh, compact)
     s.forward()
     s.loss_grad()
     s.backward()
     tok = torch.from_numpy(wl.tokens).cuda()
     d = s.embedding_backward(tok, cfg.vocab)
     torch.cuda.synchronize()
-    m_nr, m_rh = oracle_masks(cfg, 0.5, p_rh)
-    ref = oracle_step(wl, 0.5, p_rh, m_nr, m_rh)
+    m_nr, m_rh = oracle_masks(cfg, p, p_rh)
+    ref = oracle_step(wl, p, p_rh, m_nr, m_rh)
     want = embedding.embedding_grad(wl.tokens, ref["dx"], m_nr[0], np.zeros((cfg.vocab, cfg.input_dim)))
     err = rel(d.cpu().numpy(), want)
     say("   rel err", err)

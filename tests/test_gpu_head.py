@@ -62,14 +62,17 @@ def _run_head(cfg, wl, y, p, compact):
     return h.outputs(), ref, m
 
 
-@pytest.mark.parametrize("compact", [1, 0])
-def test_lm_medium_head_alone(compact):
-    cfg = workloads.get_config("lm_medium")
+@pytest.mark.parametrize("name,compact", [("lm_medium", 1), ("lm_medium", 0), ("lm_large", 1),
+                                          ("seq2seq_enc", 1)])
+def test_head_alone(name, compact):
+    cfg = workloads.get_config(name)
     wl = workloads.make_workload(cfg)
-    say(f"[gpu] head lm_medium alone compact={compact}")
+    p = cfg.p_values[0]
+    say(f"[gpu] head {name} alone compact={compact} p={p}")
+    F = cfg.num_dirs * cfg.hidden
     y = workloads.round_to_bf16(np.random.default_rng(5).normal(0, 0.5, size=(cfg.seq_len, cfg.batch,
-                                                                             cfg.hidden)).astype(np.float32))
-    got, ref, m = _run_head(cfg, wl, y, 0.5, compact)
+                                                                             F)).astype(np.float32))
+    got, ref, m = _run_head(cfg, wl, y, p, compact)
     _check(got, ref, TOL["bf16"])
     never = m.sum(axis=0) == 0
     assert not got["dW"][never].any()
