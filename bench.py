@@ -158,7 +158,7 @@ def kernel_work(kind, counts, cfg, stacked=False):
 
 # ---------------------------------------------------------------------------
 
-def run_mode(wl, p_nr, p_rh, compact, steps, warmup, timed_kernels=()):
+def run_mode(wl, p_nr, p_rh, compact, steps, warmup, timed_kernels=(), fixed=False):
     import torch
     from paper_2106_12089_amd import binding as B_
     from paper_2106_12089_amd.session import Session
@@ -168,6 +168,8 @@ def run_mode(wl, p_nr, p_rh, compact, steps, warmup, timed_kernels=()):
         s.step(cfg.mask_seed, 10_000 + i)
     torch.cuda.synchronize()
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
+    if fixed:                                  # Case-IV: one mask draw for the whole sequence
+        s.masks = lambda seed, step, _m=s.masks: _m(seed, step, fixed=True)
     t0 = time.perf_counter()
     for i in range(steps):
         e = ev[i]
@@ -475,6 +477,7 @@ def main(argv=None):
     ap.add_argument("--no-nrrh", action="store_true", help="skip the NR+RH+ST runs")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense comparison runs (counter passes)")
     ap.add_argument("--no-head", action="store_true", help="skip the language-model output head runs")
+    ap.add_argument("--no-case4", action="store_true", help="skip the Case-IV (fixed-in-time mask) runs")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="also run a plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -528,6 +531,11 @@ def main(argv=None):
                        "speedup_vs_dense": round(rd["ms"] / r["ms"], 4) if rd else None,
                        "tflops": round(r["flops"] / (r["ms"] * 1e-3) / 1e12, 4),
                        "phases_ms": {k: round(v, 4) for k, v in r["phases"].items()}}
+    if not args.no_case4:
+        c4 = run_mode(wl, p, 0.0, 1, args.steps, args.warmup, fixed=True)
+        c4r = run_mode(wl, p, p, 1, args.steps, args.warmup, fixed=True)
+        out["case4"] = {"what": "Case-IV masks (one draw per site for the whole sequence), same kernels",
+                        "ms_per_step": round(c4["ms"], 4), "nrrh_ms_per_step": round(c4r["ms"], 4)}
     if wl.tokens is not None:
         out["embedding_backward"] = run_embedding(wl, p, args.steps, args.warmup)
         if not args.no_cpu:

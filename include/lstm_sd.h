@@ -144,6 +144,15 @@ int    lstm_sd_mask_layout_get(const lstm_sd_dims* dims, lstm_sd_mask_layout* ou
 int lstm_sd_mask_generate(const lstm_sd_dims* dims, uint64_t seed, uint64_t step,
                           void* mask_buf, size_t mask_bytes, void* stream);
 
+/* Case-IV masks (Sec. 3, the most restrictive case: structured in the batch
+ * and the same at every time step; the paper keeps Case-III because this one
+ * varies too little): one draw per site for the whole sequence, the draw of
+ * t = 0 of lstm_sd_mask_generate, repeated at every t, with its keep lists.
+ * Every other entry point takes the result unchanged.  For comparing the
+ * cost of per-t randomness. */
+int lstm_sd_mask_generate_fixed(const lstm_sd_dims* dims, uint64_t seed, uint64_t step,
+                                void* mask_buf, size_t mask_bytes, void* stream);
+
 /* Rebuild keep, pos and count from the mask bytes already in mask_buf
  * (written by the caller, e.g. to force a pattern). */
 int lstm_sd_mask_compact(const lstm_sd_dims* dims, void* mask_buf, size_t mask_bytes,

@@ -70,6 +70,12 @@ def keep_mask(seed: int, step: int, stream: int, T: int, K: int, p: float) -> np
     return (~drop).astype(np.uint8)
 
 
+def keep_mask_fixed(seed: int, step: int, stream: int, T: int, K: int, p: float) -> np.ndarray:
+    """Case-IV (Sec. 3: structured in the batch and the same at every time
+    step): the draw of t = 0 repeated at every t."""
+    return np.repeat(keep_mask(seed, step, stream, 1, K, p), T, axis=0)
+
+
 def keep_lists(mask: np.ndarray):
     """Ascending kept indices per t and their counts."""
     lists = [np.nonzero(mask[t])[0].astype(np.int32) for t in range(mask.shape[0])]
@@ -78,12 +84,13 @@ def keep_lists(mask: np.ndarray):
 
 
 def all_masks(seed: int, step: int, num_layers: int, num_dirs: int, T: int,
-              k_in, hidden: int, p_nr: float, p_rh: float):
+              k_in, hidden: int, p_nr: float, p_rh: float, fixed: bool = False):
     """Masks for every site of a stacked (bi)LSTM.
 
     Returns (nr, rh): nr[l] is [T][k_in(l)], rh[l][d] is [T][hidden].
     """
-    nr = [keep_mask(seed, step, nr_stream(l), T, k_in(l), p_nr) for l in range(num_layers)]
-    rh = [[keep_mask(seed, step, rh_stream(l, d), T, hidden, p_rh) for d in range(num_dirs)]
+    draw = keep_mask_fixed if fixed else keep_mask
+    nr = [draw(seed, step, nr_stream(l), T, k_in(l), p_nr) for l in range(num_layers)]
+    rh = [[draw(seed, step, rh_stream(l, d), T, hidden, p_rh) for d in range(num_dirs)]
           for l in range(num_layers)]
     return nr, rh

@@ -68,6 +68,7 @@ SIGNATURES = {
     "lstm_sd_mask_layout_get": (ctypes.c_int, [_DIMS, ctypes.POINTER(lstm_sd_mask_layout)]),
     "lstm_sd_mask_generate": (ctypes.c_int, [_DIMS, ctypes.c_uint64, ctypes.c_uint64, _P, _SZ, _P]),
     "lstm_sd_mask_compact": (ctypes.c_int, [_DIMS, _P, _SZ, _P]),
+    "lstm_sd_mask_generate_fixed": (ctypes.c_int, [_DIMS, ctypes.c_uint64, ctypes.c_uint64, _P, _SZ, _P]),
     "lstm_sd_forward": (ctypes.c_int, [_DIMS, ctypes.POINTER(lstm_sd_weights), _P, _P, _P, _P, _P, _SZ,
                                        _P, _P, _P, _P, _SZ, _P, _SZ, _P]),
     "lstm_sd_backward": (ctypes.c_int, [_DIMS, ctypes.POINTER(lstm_sd_weights), _P, _P, _P, _P, _P, _SZ,
@@ -184,6 +185,12 @@ def lstm_sd_mask_generate(dims, seed, step, mask_buf, stream=None):
     _check(load().lstm_sd_mask_generate(ctypes.byref(dims), ctypes.c_uint64(seed & (2**64 - 1)),
                                         ctypes.c_uint64(step), _ptr(mask_buf),
                                         mask_buf.numel() * mask_buf.element_size(), _stream(stream)))
+
+
+def lstm_sd_mask_generate_fixed(dims, seed, step, mask_buf, stream=None):
+    _check(load().lstm_sd_mask_generate_fixed(ctypes.byref(dims), ctypes.c_uint64(seed & (2**64 - 1)),
+                                              ctypes.c_uint64(step), _ptr(mask_buf), _nbytes(mask_buf),
+                                              _stream(stream)))
 
 
 def lstm_sd_mask_compact(dims, mask_buf, stream=None):

@@ -206,7 +206,7 @@ static uint64_t threshold64(double p) {
 }
 
 static int do_masks(const lstm_sd_dims* dims, uint64_t seed, uint64_t step, void* mbuf, size_t mbytes,
-                    void* stream, int generate) {
+                    void* stream, int generate, int fixed = 0) {
     Plan P;
     const char* why = nullptr;
     int rc = make_plan(dims, &P, &why);
@@ -224,7 +224,7 @@ static int do_masks(const lstm_sd_dims* dims, uint64_t seed, uint64_t step, void
     a.dcount = (int32_t*)(m + P.m_dcount);
     a.kseg = (int32_t*)(m + P.m_kseg);
     a.dseg = (int32_t*)(m + P.m_dseg);
-    a.T = P.T; a.kmax = P.kmax; a.compact = P.compact; a.generate = generate;
+    a.T = P.T; a.kmax = P.kmax; a.compact = P.compact; a.generate = generate; a.fixed = fixed;
     a.seed = seed; a.step = step;
     for (int s = 0; s < P.sites; ++s) {
         a.K[s] = P.site_k(s);
@@ -820,6 +820,11 @@ int lstm_sd_mask_layout_get(const lstm_sd_dims* dims, lstm_sd_mask_layout* out) 
 int lstm_sd_mask_generate(const lstm_sd_dims* dims, uint64_t seed, uint64_t step, void* mask_buf,
                           size_t mask_bytes, void* stream) {
     return do_masks(dims, seed, step, mask_buf, mask_bytes, stream, 1);
+}
+
+int lstm_sd_mask_generate_fixed(const lstm_sd_dims* dims, uint64_t seed, uint64_t step, void* mask_buf,
+                                size_t mask_bytes, void* stream) {
+    return do_masks(dims, seed, step, mask_buf, mask_bytes, stream, 1, 1);
 }
 
 int lstm_sd_mask_compact(const lstm_sd_dims* dims, void* mask_buf, size_t mask_bytes, void* stream) {

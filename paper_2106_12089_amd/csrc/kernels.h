@@ -18,6 +18,7 @@ struct MaskArgs {
     int32_t* kseg;
     int32_t* dseg;
     int T, kmax, compact, generate;
+    int fixed;                          // 1: every t takes the draw of t = 0 (one mask for the whole sequence)
     uint64_t seed, step;
     int K[MAX_SITES];
     int sid[MAX_SITES];

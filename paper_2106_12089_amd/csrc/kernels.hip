@@ -75,7 +75,7 @@ __global__ void __launch_bounds__(256) k_mask_build(MaskArgs a) {
         for (int q = tid; q < (K + 3) / 4; q += blockDim.x) {
             u64x4 c;
             c.x[0] = (uint64_t)q;
-            c.x[1] = (uint64_t)t;
+            c.x[1] = a.fixed ? 0ull : (uint64_t)t;
             c.x[2] = (uint64_t)a.sid[s];
             c.x[3] = a.step;
             const u64x4 r = philox4x64_10(c, a.seed, 0ull);

@@ -63,8 +63,13 @@ class Session:
             self.dy.fill_(1.0)      # d(sum y)/dy, constant
 
     # -- calls ---------------------------------------------------------------
-    def masks(self, seed: int, step: int):
-        B_.lstm_sd_mask_generate(self.dims, seed, step, self.mask_buf)
+    def masks(self, seed: int, step: int, fixed: bool = False):
+        """Case-III masks (fresh at every t), or with fixed the Case-IV ones
+        (one draw for the whole sequence)."""
+        if fixed:
+            B_.lstm_sd_mask_generate_fixed(self.dims, seed, step, self.mask_buf)
+        else:
+            B_.lstm_sd_mask_generate(self.dims, seed, step, self.mask_buf)
 
     def masks_compact(self):
         B_.lstm_sd_mask_compact(self.dims, self.mask_buf)

@@ -91,3 +91,18 @@ def test_stream_ids_distinct():
         for d in range(2):
             ids.add(masks.rh_stream(l, d))
     assert len(ids) == 12
+
+
+def test_case4_fixed_masks():
+    """Case-IV (one mask for the whole sequence): every row is the t = 0 row of
+    the Case-III draw, and the drop fraction over many neurons is near p."""
+    from oracle import masks as M
+    T, K, p = 7, 4000, 0.3
+    f = M.keep_mask_fixed(5, 2, M.nr_stream(1), T, K, p)
+    c3 = M.keep_mask(5, 2, M.nr_stream(1), T, K, p)
+    assert f.shape == (T, K)
+    assert all(np.array_equal(f[t], c3[0]) for t in range(T))
+    assert not all(np.array_equal(c3[t], c3[0]) for t in range(T))   # Case-III does vary in t
+    assert abs(1.0 - f[0].mean() - p) < 5 * np.sqrt(p * (1 - p) / K)
+    nr, rh = M.all_masks(5, 2, 2, 2, T, lambda l: 16 if l == 0 else 24, 12, p, p, fixed=True)
+    assert all(np.array_equal(m, np.repeat(m[:1], T, axis=0)) for m in nr + [r for x in rh for r in x])
