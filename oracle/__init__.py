@@ -17,5 +17,7 @@ Contents
   head    -- the output head: pre-FC structured output dropout, the FC
              (vocabulary projection) layer and the softmax cross-entropy
              loss, forward and backward.
+  case1   -- the Case-I ("NR+Random") comparator: per-element input
+             dropout on every layer, run dense.
 """
-from . import philox, masks, lstm, embedding, head  # noqa: F401
+from . import philox, masks, lstm, embedding, head, case1  # noqa: F401
