@@ -211,6 +211,25 @@ def run_mode(wl, p_nr, p_rh, compact, steps, warmup, timed_kernels=(), fixed=Fal
                 ktime=ktime)
 
 
+def run_case1(wl, p, steps, warmup):
+    """The Case-I ("NR+Random") comparator's whole step (per-element input
+    dropout on every layer, each layer dense), timed with events."""
+    import torch
+    from paper_2106_12089_amd.session import Case1Session
+    cfg = wl.cfg
+    c = Case1Session(wl, p)
+    for i in range(warmup):
+        c.step(cfg.mask_seed, 10_000 + i)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(steps):
+        c.step(cfg.mask_seed, i)
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
 def run_embedding(wl, p_nr, steps, warmup):
     """Embedding-table gradient after the step (lstm_sd_embedding_backward) on
     a language-model workload: its kernel's average duration (HIP events on
@@ -478,6 +497,7 @@ def main(argv=None):
     ap.add_argument("--no-dense", action="store_true", help="skip the dense comparison runs (counter passes)")
     ap.add_argument("--no-head", action="store_true", help="skip the language-model output head runs")
     ap.add_argument("--no-case4", action="store_true", help="skip the Case-IV (fixed-in-time mask) runs")
+    ap.add_argument("--no-case1", action="store_true", help="skip the Case-I (NR+Random) comparator run")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="also run a plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -531,6 +551,10 @@ def main(argv=None):
                        "speedup_vs_dense": round(rd["ms"] / r["ms"], 4) if rd else None,
                        "tflops": round(r["flops"] / (r["ms"] * 1e-3) / 1e12, 4),
                        "phases_ms": {k: round(v, 4) for k, v in r["phases"].items()}}
+    if not args.no_case1:
+        c1 = run_case1(wl, p, args.steps, args.warmup)
+        out["case1"] = {"what": "Case-I (NR+Random) comparator: per-element input dropout, every layer dense",
+                        "ms_per_step": round(c1, 4), "speedup_of_nr_st": round(c1 / head["ms"], 4)}
     if not args.no_case4:
         c4 = run_mode(wl, p, 0.0, 1, args.steps, args.warmup, fixed=True)
         c4r = run_mode(wl, p, p, 1, args.steps, args.warmup, fixed=True)

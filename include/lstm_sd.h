@@ -290,6 +290,27 @@ int lstm_sd_head_backward(const lstm_sd_head_dims* hd, const void* W_fc, const i
                           float* loss, float* dy, float* dW_fc, float* db_fc, void* workspace,
                           size_t workspace_bytes, void* stream);
 
+/* ---------------------------------------------------------------------------
+ * Case-I dropout, the comparator of the paper's "NR+Random" baselines (Sec. 3,
+ * Sec. 4): an unstructured mask, one keep bit per element (t, b, k) of a layer
+ * input, so no row of a product can be skipped; the step then runs dense.
+ * Element (t, b, k) is dropped iff word k%4 of Philox4x64-10(key = (seed, 0),
+ * counter = (k/4, t, stream_id + 2^32 (b+1), step)) is below floor(p * 2^64)
+ * (the Case-III generator with the batch row in the stream's high word).
+ *   src   device [T][B][K], src_dtype;  dst device [T][B][K], dst_dtype:
+ *         dst = src * kept / (1-p)
+ *   mask  device [T][B][K] uint8 (written): 1 = kept
+ * A stack of L layers takes one call per layer input (stream 4l for layer l,
+ * as the Case-III NR site) and a single-layer dense step per layer. */
+int lstm_sd_case1_dropout(int32_t seq_len, int32_t batch, int32_t features, int32_t src_dtype, const void* src,
+                          int32_t dst_dtype, void* dst, uint8_t* mask, uint64_t seed, uint64_t step,
+                          int32_t stream_id, double p, void* stream);
+
+/* The gradient through lstm_sd_case1_dropout: dsrc = dx * mask / (1-p).
+ *   dx, dsrc  device [T][B][K] float (may alias);  mask as written by the forward */
+int lstm_sd_case1_dropout_backward(int32_t seq_len, int32_t batch, int32_t features, const float* dx,
+                                   const uint8_t* mask, double p, float* dsrc, void* stream);
+
 /* Instrumentation for measuring one kernel's average duration on the
  * stream it runs on.  After lstm_sd_kernel_timer_start(name), every launch
  * of the named kernel made by this library is bracketed by a pair of HIP

@@ -76,6 +76,11 @@ SIGNATURES = {
                                         _P, _SZ, _P]),
     "lstm_sd_mse_grad": (ctypes.c_int, [_DIMS, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "lstm_sd_embedding_backward": (ctypes.c_int, [_DIMS, _P, ctypes.c_int, _P, _P, _SZ, _P, _P]),
+    "lstm_sd_case1_dropout": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _P,
+                                             ctypes.c_int32, _P, _P, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_int32,
+                                             ctypes.c_double, _P]),
+    "lstm_sd_case1_dropout_backward": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _P, _P,
+                                                      ctypes.c_double, _P, _P]),
     "lstm_sd_head_mask_bytes": (_SZ, [_HD]),
     "lstm_sd_head_workspace_bytes": (_SZ, [_HD]),
     "lstm_sd_head_mask_layout_get": (ctypes.c_int, [_HD, ctypes.POINTER(lstm_sd_mask_layout)]),
@@ -232,6 +237,17 @@ def lstm_sd_mse_grad(dims, y, target, lengths, dy, loss, workspace, stream=None)
 def lstm_sd_embedding_backward(dims, tokens, vocab, dx, mask_buf, d_emb, stream=None):
     _check(load().lstm_sd_embedding_backward(ctypes.byref(dims), _ptr(tokens), int(vocab), _ptr(dx), _ptr(mask_buf),
                                              _nbytes(mask_buf), _ptr(d_emb), _stream(stream)))
+
+
+def lstm_sd_case1_dropout(T, B, K, src_dtype, src, dst_dtype, dst, mask, seed, step, stream_id, p, stream=None):
+    _check(load().lstm_sd_case1_dropout(T, B, K, src_dtype, _ptr(src), dst_dtype, _ptr(dst), _ptr(mask),
+                                        ctypes.c_uint64(seed & (2**64 - 1)), ctypes.c_uint64(step), stream_id,
+                                        float(p), _stream(stream)))
+
+
+def lstm_sd_case1_dropout_backward(T, B, K, dx, mask, p, dsrc, stream=None):
+    _check(load().lstm_sd_case1_dropout_backward(T, B, K, _ptr(dx), _ptr(mask), float(p), _ptr(dsrc),
+                                                 _stream(stream)))
 
 
 def make_head_dims(features, vocab, batch, seq_len, dtype=DTYPE_BF16, compact=1, stream_id=0,

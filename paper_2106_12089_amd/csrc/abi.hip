@@ -25,6 +25,9 @@ template <typename T> void launch_wgrad(const WgBatch& b, hipStream_t st);
 void launch_bwd_init(const float*, const float*, float*, float*, long, void*, int, int, int, long, long, unsigned*, int*,
                      hipStream_t);
 void launch_emb_grad(const int32_t*, int, int, int, const float*, const SiteView&, int, float*, hipStream_t);
+void launch_case1_drop(int, int, const void*, void*, uint8_t*, int, int, int, uint64_t, uint64_t, uint64_t, uint64_t,
+                       float, hipStream_t);
+void launch_case1_undrop(const float*, const uint8_t*, float*, long, float, hipStream_t);
 template <typename T> void launch_head_prep(const float*, void*, void*, int, int, int, int, hipStream_t);
 void launch_ce_loss(const float*, const int32_t*, const int32_t*, int, int, int, float*, float*, float*, float*, float*,
                     hipStream_t);
@@ -1002,6 +1005,35 @@ int lstm_sd_head_backward(const lstm_sd_head_dims* hd, const void* W_fc, const i
         head_backward_impl<float>(P, W_fc, targets, lengths, mask_buf, logits, loss, dy, dW_fc, db_fc,
                                   (char*)workspace, st);
     return hip_check("head backward launch");
+}
+
+static const char* case1_check(int T, int B, int K, double p) {
+    if (T < 1 || B < 1 || K < 1) return "dimensions must be >= 1";
+    if (!(p >= 0.0 && p < 1.0)) return "p must be in [0, 1)";
+    if ((long)T * B > (1L << 24) || B > 65536 || T > 65535) return "seq_len*batch too large";
+    return nullptr;
+}
+
+int lstm_sd_case1_dropout(int32_t seq_len, int32_t batch, int32_t features, int32_t src_dtype, const void* src,
+                          int32_t dst_dtype, void* dst, uint8_t* mask, uint64_t seed, uint64_t step, int32_t stream_id,
+                          double p, void* stream) {
+    if (const char* why = case1_check(seq_len, batch, features, p)) return fail(LSTM_SD_EINVAL, why);
+    if (stream_id < 0) return fail(LSTM_SD_EINVAL, "stream_id must be >= 0");
+    if ((src_dtype != LSTM_SD_DTYPE_F32 && src_dtype != LSTM_SD_DTYPE_BF16) ||
+        (dst_dtype != LSTM_SD_DTYPE_F32 && dst_dtype != LSTM_SD_DTYPE_BF16))
+        return fail(LSTM_SD_EUNSUPPORTED, "dtypes must be 0 (f32) or 1 (bf16)");
+    if (!src || !dst || !mask) return fail(LSTM_SD_EINVAL, "a required pointer is NULL");
+    launch_case1_drop(src_dtype == LSTM_SD_DTYPE_F32, dst_dtype == LSTM_SD_DTYPE_BF16, src, dst, mask, seq_len, batch,
+                      features, seed, step, (uint64_t)stream_id, threshold64(p), inv_keep(p), (hipStream_t)stream);
+    return hip_check("case-I dropout launch");
+}
+
+int lstm_sd_case1_dropout_backward(int32_t seq_len, int32_t batch, int32_t features, const float* dx,
+                                   const uint8_t* mask, double p, float* dsrc, void* stream) {
+    if (const char* why = case1_check(seq_len, batch, features, p)) return fail(LSTM_SD_EINVAL, why);
+    if (!dx || !mask || !dsrc) return fail(LSTM_SD_EINVAL, "a required pointer is NULL");
+    launch_case1_undrop(dx, mask, dsrc, (long)seq_len * batch * features, inv_keep(p), (hipStream_t)stream);
+    return hip_check("case-I dropout backward launch");
 }
 
 int lstm_sd_kernel_timer_start(const char* kernel) {

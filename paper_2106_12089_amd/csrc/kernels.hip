@@ -1257,6 +1257,43 @@ __global__ void __launch_bounds__(256) k_emb_grad(const int32_t* tokens, int N, 
 }
 
 // ---------------------------------------------------------------------------
+// Case-I dropout (the comparator of the paper's "NR+Random" baselines): one
+// keep bit per element (t, b, k) of a layer input, drawn with the generator
+// of the masks above with the batch row in the high word of the stream
+// counter: counter (k/4, t, sid + 2^32 (b + 1), step), word k%4.
+// dst = src * kept * s in the compute type; mask [T][B][K] bytes.
+// grid (ceil(K/4 / 64), B, T), block 64: a thread draws 4 elements.
+template <typename S, typename T>
+__global__ void __launch_bounds__(64) k_case1_drop(const S* src, T* dst, uint8_t* mask, int B, int K, uint64_t seed,
+                                                   uint64_t step, uint64_t sid, uint64_t thr, float s) {
+    const int q = blockIdx.x * 64 + threadIdx.x, b = blockIdx.y, t = blockIdx.z;
+    if (4 * q >= K) return;
+    u64x4 c;
+    c.x[0] = (uint64_t)q;
+    c.x[1] = (uint64_t)t;
+    c.x[2] = sid + ((uint64_t)(b + 1) << 32);
+    c.x[3] = step;
+    const u64x4 r = philox4x64_10(c, seed, 0ull);
+    const size_t row = ((size_t)t * B + b) * K;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const int k = 4 * q + e;
+        if (k < K) {
+            const uint8_t kept = (thr == 0 || r.x[e] >= thr) ? 1 : 0;
+            mask[row + k] = kept;
+            dst[row + k] = from_f32<T>(kept ? s * to_f32<S>(src[row + k]) : 0.0f);
+        }
+    }
+}
+
+// dsrc = dx * mask * s (the input gradient through the Case-I dropout)
+__global__ void __launch_bounds__(256) k_case1_undrop(const float* dx, const uint8_t* mask, float* dsrc, long n,
+                                                      float s) {
+    for (long i = blockIdx.x * 256L + threadIdx.x; i < n; i += (long)gridDim.x * 256)
+        dsrc[i] = mask[i] ? s * dx[i] : 0.0f;
+}
+
+// ---------------------------------------------------------------------------
 // Output head of a language model (pre-FC output dropout, FC layer, softmax
 // cross-entropy).  The FC products run on the input-product, dX and weight-
 // gradient kernels above (K = the LSTM output width, G = the vocabulary);
@@ -1686,6 +1723,25 @@ template void launch_ce_grad<float>(const float*, const int32_t*, const int32_t*
                                     int, int, int, int, void*, void*, hipStream_t);
 template void launch_ce_grad<bf16>(const float*, const int32_t*, const int32_t*, const float*, const float*, int,
                                    int, int, int, int, void*, void*, hipStream_t);
+void launch_case1_drop(int src_f32, int dst_bf16, const void* src, void* dst, uint8_t* mask, int T_, int B, int K,
+                       uint64_t seed, uint64_t step, uint64_t sid, uint64_t thr, float s, hipStream_t st) {
+    const dim3 grid(((K + 3) / 4 + 63) / 64, B, T_);
+    if (src_f32 && dst_bf16)
+        launch_k(KID_NONE, k_case1_drop<float, bf16>, grid, dim3(64), 0, st, (const float*)src, (bf16*)dst, mask, B, K,
+                 seed, step, sid, thr, s);
+    else if (src_f32)
+        launch_k(KID_NONE, k_case1_drop<float, float>, grid, dim3(64), 0, st, (const float*)src, (float*)dst, mask, B,
+                 K, seed, step, sid, thr, s);
+    else if (dst_bf16)
+        launch_k(KID_NONE, k_case1_drop<bf16, bf16>, grid, dim3(64), 0, st, (const bf16*)src, (bf16*)dst, mask, B, K,
+                 seed, step, sid, thr, s);
+    else
+        launch_k(KID_NONE, k_case1_drop<float, float>, grid, dim3(64), 0, st, (const float*)src, (float*)dst, mask, B,
+                 K, seed, step, sid, thr, s);
+}
+void launch_case1_undrop(const float* dx, const uint8_t* mask, float* dsrc, long n, float s, hipStream_t st) {
+    launch_k(KID_NONE, k_case1_undrop, dim3(nblk(n, 256)), dim3(256), 0, st, dx, mask, dsrc, n, s);
+}
 void launch_mse(const float* y, const float* tg, const int32_t* lengths, float* dy, float* partial, int np,
                 float* loss, int T, int B, int F, hipStream_t st) {
     launch_k(KID_NONE, k_mse, dim3(np), dim3(256), 0, st, y, tg, lengths, dy, partial, T, B, F);

@@ -192,3 +192,59 @@ class HeadSession:
         g = lambda t: t.detach().float().cpu().numpy().astype(np.float64)
         return dict(z=g(self.logits), loss=float(self.loss.item()), dy=g(self.dy), dW=g(self.dW),
                     dc=g(self.db))
+
+
+class Case1Session:
+    """The Case-I ("NR+Random") comparator: per-element dropout on every
+    layer's input (lstm_sd_case1_dropout), each layer a single-layer step
+    without dropout (identity keep lists, every row multiplied), the input
+    gradients taken back through the same masks.
+
+    wl: a workload; p: the input dropout rate of every layer."""
+
+    def __init__(self, wl, p: float, device: str = "cuda:0"):
+        import dataclasses
+        import types
+        cfg = wl.cfg
+        self.cfg, self.wl, self.p = cfg, wl, p
+        self.L, self.D, self.H = cfg.num_layers, cfg.num_dirs, cfg.hidden
+        self.T, self.B = wl.x.shape[0], wl.x.shape[1]
+        self.bf16 = cfg.dtype == "bf16"
+        self.layers = []
+        for l in range(self.L):
+            kin = cfg.k_in(l)
+            lcfg = dataclasses.replace(cfg, num_layers=1, input_dim=kin)
+            sl = slice(l * self.D, (l + 1) * self.D)
+            lwl = types.SimpleNamespace(cfg=lcfg, x=wl.x if l == 0 else np.zeros((self.T, self.B, kin), np.float32),
+                                        W=wl.W[sl], U=wl.U[sl], b=wl.b[sl], h0=wl.h0[sl], c0=wl.c0[sl],
+                                        target=wl.target, lengths=wl.lengths)
+            s = Session(lwl, 0.0, 0.0, 1, device)
+            s.masks(0, 0)                      # p = 0: identity keep lists, the same at every step
+            self.layers.append(s)
+        self.x0 = self.layers[0].x.clone()
+        dev = self.layers[0].x.device
+        self.drop_masks = [torch.zeros(self.T, self.B, cfg.k_in(l), dtype=torch.uint8, device=dev)
+                           for l in range(self.L)]
+        self.dx = torch.zeros(self.T, self.B, cfg.input_dim, dtype=torch.float32, device=dev)
+        self.y = self.layers[-1].y
+
+    def step(self, seed: int, step: int):
+        dt = B_.DTYPE_BF16 if self.bf16 else B_.DTYPE_F32
+        for l, s in enumerate(self.layers):
+            src, sdt = (self.x0, dt) if l == 0 else (self.layers[l - 1].y, B_.DTYPE_F32)
+            B_.lstm_sd_case1_dropout(self.T, self.B, s.I, sdt, src, dt, s.x, self.drop_masks[l], seed, step, 4 * l,
+                                     self.p)
+            s.forward()
+        self.layers[-1].loss_grad()
+        for l in reversed(range(self.L)):
+            s = self.layers[l]
+            s.backward(dy=None if l == self.L - 1 else self.layers[l].dy)
+            out = self.dx if l == 0 else self.layers[l - 1].dy
+            B_.lstm_sd_case1_dropout_backward(self.T, self.B, s.I, s.dx, self.drop_masks[l], self.p, out)
+
+    def outputs(self):
+        g = lambda t: t.detach().float().cpu().numpy().astype(np.float64)
+        top = self.layers[-1]
+        return dict(y=g(top.y), loss=float(top.loss.item()), dx=g(self.dx),
+                    dW=[g(t) for s in self.layers for t in s.dW], dU=[g(t) for s in self.layers for t in s.dU],
+                    db=[g(t) for s in self.layers for t in s.db])

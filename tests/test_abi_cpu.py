@@ -18,7 +18,7 @@ pytestmark = pytest.mark.skipif(not os.path.exists(B.LIB_PATH), reason="library 
 def declared_functions():
     src = open(HEADER).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(lstm_sd_[a-z_]+)\s*\(", src)))
+    return sorted(set(re.findall(r"\b(lstm_sd_[a-z0-9_]+)\s*\(", src)))
 
 
 def test_every_declared_symbol_is_exported():
