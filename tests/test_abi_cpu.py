@@ -155,3 +155,17 @@ def test_head_null_pointers_and_small_buffers_rejected():
     assert lib.lstm_sd_head_backward(ctypes.byref(hd), fake, fake, None, fake, mb - 1, fake, fake, fake, fake,
                                      fake, fake, ws, None) == B.EWORKSPACE
     assert lib.lstm_sd_head_mask_layout_get(ctypes.byref(hd), None) == B.EINVAL
+
+
+def test_case1_entry_points_validate_before_device_work():
+    lib = B.load()
+    fake = 4096  # never dereferenced: the checks fail first
+    D = ctypes.c_double
+    assert lib.lstm_sd_case1_dropout(0, 2, 3, 0, fake, 0, fake, fake, 1, 0, 0, D(0.5), None) == B.EINVAL
+    assert lib.lstm_sd_case1_dropout(4, 2, 3, 0, fake, 0, fake, fake, 1, 0, 0, D(1.0), None) == B.EINVAL
+    assert lib.lstm_sd_case1_dropout(4, 2, 3, 0, fake, 0, fake, fake, 1, 0, -1, D(0.5), None) == B.EINVAL
+    assert lib.lstm_sd_case1_dropout(4, 2, 3, 3, fake, 0, fake, fake, 1, 0, 0, D(0.5), None) == B.EUNSUPPORTED
+    assert lib.lstm_sd_case1_dropout(4, 2, 3, 0, None, 0, fake, fake, 1, 0, 0, D(0.5), None) == B.EINVAL
+    assert lib.lstm_sd_case1_dropout_backward(4, 2, 3, fake, None, D(0.5), fake, None) == B.EINVAL
+    assert lib.lstm_sd_case1_dropout_backward(4, 2, 0, fake, fake, D(0.5), fake, None) == B.EINVAL
+    assert "dimensions" in B.lstm_sd_last_error()
