@@ -215,3 +215,25 @@ def test_stacked_and_per_layer_agree(name, mode, monkeypatch):
         assert max(errs.values()) <= TOL[cfg.dtype], errs
         for k in ("y", "hT", "cT", "dx", "dh0", "dc0"):
             assert np.isfinite(o[k]).all(), k
+
+
+def test_mse_loss_repeated_calls():
+    """Repeated loss calls on the same outputs give the same bits (a fixed
+    summation order), and the loss matches the oracle's."""
+    from paper_2106_12089_amd.session import Session
+    cfg, wl = make("mse", loss="mse", dtype="f32", batch=19, seq_len=5)
+    say("[gpu] mse repeated calls")
+    s = Session(wl, 0.5, 0.0, 1)
+    s.masks(cfg.mask_seed, 0)
+    s.forward()
+    vals = []
+    for _ in range(3):
+        s.loss_grad()
+        torch.cuda.synchronize()
+        vals.append(s.loss.item())
+    assert vals[0] == vals[1] == vals[2]
+    from oracle import masks as om
+    m_nr, m_rh = om.all_masks(cfg.mask_seed, 0, cfg.num_layers, cfg.num_dirs, cfg.seq_len, cfg.k_in, cfg.hidden,
+                              0.5, 0.0)
+    ref = oracle_step(wl, 0.5, 0.0, m_nr, m_rh)
+    assert abs(vals[0] - ref["loss"]) <= TOL["f32"] * abs(ref["loss"])
