@@ -199,6 +199,7 @@ def run_mode(wl, p_nr, p_rh, compact, steps, warmup, timed_kernels=(), fixed=Fal
         for k in range(4):
             phases[k] += e[k].elapsed_time(e[k + 1])
     phases /= steps
+    per_step = np.array([e[0].elapsed_time(e[4]) for e in ev])   # the instrumented pass, per step
     # kept counts of every timed step (masks regenerated outside the timed region)
     counts_all = []
     for i in range(steps):
@@ -217,7 +218,7 @@ def run_mode(wl, p_nr, p_rh, compact, steps, warmup, timed_kernels=(), fixed=Fal
     return dict(ms=total_ms / steps, wall_ms=wall * 1e3 / steps, counts=counts,
                 flops=float(np.mean([algorithmic_flops(c, cfg, wl.lengths) for c in counts_all])),
                 phases=dict(mask=phases[0], forward=phases[1], loss=phases[2], backward=phases[3]),
-                ktime=ktime)
+                ktime=ktime, pct=[float(np.percentile(per_step, q)) for q in (10, 50, 90)])
 
 
 def run_case1(wl, p, steps, warmup):
@@ -443,7 +444,16 @@ def cpu_baseline(wl, p_nr, p_rh, budget_s=12.0):
                                               for d in range(cfg.num_dirs)]
         flops += algorithmic_flops(counts, cfg, wl.lengths)
         n += 1
+    model = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
     return dict(value=round(flops / t_tot / 1e12, 6), unit="TFLOP/s", cores=int(threads), kind="oracle",
+                cpu_count=os.cpu_count(), cpu_model=model,
                 sample=f"{n} whole training steps of the {cfg.name} workload (NR+ST, masks of steps "
                        f"0..{n - 1}), float64 NumPy oracle, {t_tot / n * 1e3:.0f} ms/step",
                 ms_per_step=round(t_tot / n * 1e3, 3))
@@ -531,7 +541,7 @@ def main(argv=None):
     wl = workloads.make_workload(cfg)
     p = 0.5 if 0.5 in cfg.p_values else cfg.p_values[0]
     head = run_mode(wl, p, 0.0, 1, args.steps, args.warmup, timed_kernels=KERNELS)
-    dense = None if args.no_dense else run_mode(wl, p, 0.0, 0, args.steps, args.warmup)
+    dense = None if args.no_dense else run_mode(wl, p, 0.0, 0, args.steps, args.warmup, timed_kernels=KERNELS)
     out = {
         "metric": METRIC,
         "value": round(head["flops"] / (head["ms"] * 1e-3) / 1e12, 4),
@@ -551,6 +561,11 @@ def main(argv=None):
                                     / (head["ms"] * 1e-3) / 1e12, 4),
         "phases_ms": {k: round(v, 4) for k, v in head["phases"].items()},
         "phases_ms_dense": {k: round(v, 4) for k, v in dense["phases"].items()} if dense else None,
+        "step_ms_p10_p50_p90": [round(v, 4) for v in head["pct"]],
+        "step_ms_p10_p50_p90_note": "per-step times of the pass with phase events (about 19 us above the clean pass)",
+        "speedup_per_kernel": {k: round(dense["ktime"][k]["total_ms"] / head["ktime"][k]["total_ms"], 4)
+                               for k in head["ktime"] if dense and head["ktime"][k]["total_ms"] > 0
+                               and dense["ktime"][k]["total_ms"] > 0} if dense else None,
         "roofline": roofline(head, cfg),
     }
     if not args.no_nrrh:
