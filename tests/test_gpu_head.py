@@ -167,3 +167,42 @@ def test_repeat_is_deterministic():
     for k in ("z", "dy", "dW", "dc"):
         assert np.array_equal(outs[0][k], outs[1][k]), k
     assert outs[0]["loss"] == outs[1]["loss"]
+
+
+def test_bidirectional_stack_with_head():
+    """The head on a bidirectional stack's output (F = 2H, the tagger's shape
+    with a synthetic FC layer and targets), chained through the LSTM
+    backward, against the oracle chain (NR+RH+ST at the stack, p_out = 0.5)."""
+    from paper_2106_12089_amd.session import HeadSession, Session
+    cfg = workloads.get_config("tagger")
+    wl = workloads.make_workload(cfg)
+    F, V, p = cfg.num_dirs * cfg.hidden, 96, 0.5
+    rng = np.random.default_rng(8)
+    wl.W_fc = workloads.round_to_bf16(rng.uniform(-0.1, 0.1, size=(F, V)).astype(np.float32))
+    wl.b_fc = rng.uniform(-0.1, 0.1, size=(V,)).astype(np.float32)
+    wl.targets = rng.integers(0, V, size=(cfg.seq_len, cfg.batch)).astype(np.int32)
+    say("[gpu] head on the bidirectional tagger stack")
+    s = Session(wl, p, p, 1)
+    s.masks(cfg.mask_seed, 0)
+    s.forward()
+    h = HeadSession(wl, p, 1)
+    h.masks(cfg.mask_seed, 0)
+    h.forward(s.y)
+    h.backward()
+    s.backward(dy=h.dy)
+    torch.cuda.synchronize()
+    m_nr, m_rh = oracle_masks(cfg, p, p)
+    P = lstm.params_from(wl.W, wl.U, wl.b, cfg.num_layers, cfg.num_dirs)
+    y, _, _, cache = lstm.forward(P, wl.x, wl.h0, wl.c0, m_nr, m_rh, p, p, wl.lengths)
+    m = _out_mask(cfg, F, p)
+    assert np.array_equal(h.mask_view(), m)
+    hs = head.head_step(y, wl.W_fc, wl.b_fc, m, p, wl.targets, wl.lengths)
+    g = lstm.backward(cache, hs["dy"])
+    _check(h.outputs(), hs, TOL["bf16"])
+    gpu = s.outputs()
+    errs = {"dx": rel(gpu["dx"], g["dx"])}
+    for k in ("dW", "dU", "db"):
+        for i, (a, r) in enumerate(zip(gpu[k], g[k])):
+            errs[f"{k}{i}"] = rel(a, r)
+    say("   lstm errs", {k: f"{v:.2e}" for k, v in errs.items()})
+    assert max(errs.values()) <= TOL["bf16"], errs
