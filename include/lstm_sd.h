@@ -211,9 +211,9 @@ int lstm_sd_mse_grad(const lstm_sd_dims* dims, const float* y, const float* targ
  * Row v of d_emb receives the sum of the layer-0 input gradient rows dx_t[b]
  * over every (t, b) with tokens[t][b] = v, over the columns kept at t (layer
  * 0's NR mask; dx is zero in the dropped columns, Eq. 10, and they are not
- * accumulated).  Each row's sum is formed in a fixed order (ascending (t, b)
- * within chunks of 2048 positions) and added once per chunk: deterministic,
- * no atomics on d_emb.
+ * accumulated).  Each row's sum is formed in a fixed order (four partial
+ * sums over interleaved groups of 64 positions, each ascending, then added in
+ * group order) and added to d_emb once: deterministic, no atomics on d_emb.
  *   tokens   device [T][B] int32; ids outside [0, vocab) are skipped
  *   vocab    rows of the table (> 0)
  *   dx       device [T][B][I] float: lstm_sd_backward's dx
