@@ -82,6 +82,12 @@ typedef struct {
     int32_t compact;      /* 1 = skip dropped rows (method), 0 = dense baseline */
     double p_nr;          /* non-recurrent dropout rate, [0, 1) */
     double p_rh;          /* recurrent dropout rate, [0, 1) */
+    /* Per-layer rates (a dropout vector with one rate per site, as AWD-LSTM
+     * uses, Sec. 4.1): NULL, or a host array of L rates in [0, 1) that
+     * replaces p_nr (the NR rate of layer l's input) or p_rh (the RH rate of
+     * both directions of layer l).  Read during each call only. */
+    const double* p_nr_layer;
+    const double* p_rh_layer;
 } lstm_sd_dims;
 
 /* Host arrays of L*D device pointers, index l*D + d. */
@@ -153,8 +159,11 @@ int lstm_sd_mask_generate(const lstm_sd_dims* dims, uint64_t seed, uint64_t step
 int lstm_sd_mask_generate_fixed(const lstm_sd_dims* dims, uint64_t seed, uint64_t step,
                                 void* mask_buf, size_t mask_bytes, void* stream);
 
-/* Rebuild keep, pos and count from the mask bytes already in mask_buf
- * (written by the caller, e.g. to force a pattern). */
+/* The compaction step alone ("matrix compaction", Sec. 4) on masks the
+ * caller wrote: rebuild keep, pos, count, drop, dcount, kseg and dseg from
+ * the mask bytes already in mask_buf (one Case-III row per site and t,
+ * Sec. 3.1), e.g. to force a pattern such as a step with every neuron
+ * dropped.  mask_buf: device, lstm_sd_mask_bytes(dims) bytes. */
 int lstm_sd_mask_compact(const lstm_sd_dims* dims, void* mask_buf, size_t mask_bytes,
                          void* stream);
 
@@ -311,6 +320,27 @@ int lstm_sd_case1_dropout(int32_t seq_len, int32_t batch, int32_t features, int3
 int lstm_sd_case1_dropout_backward(int32_t seq_len, int32_t batch, int32_t features, const float* dx,
                                    const uint8_t* mask, double p, float* dsrc, void* stream);
 
+/* Failure of a step's persistent kernels.  The recurrences run as persistent
+ * launches whose workgroups meet at a grid barrier once per time step (one
+ * step of Eq. 1-6 forward, of Eq. 7-10 backward, needs the whole h_{t-1} or
+ * DA of the step before).  Every barrier wait is bounded by wall-clock time
+ * (0.5 s by default); a wait that times out stops its launch, and then:
+ *   - the forward writes NaN into hT, cT and every step of y;
+ *   - the backward writes NaN into dh0, dc0, dx and every weight and bias
+ *     gradient (also when it was the forward of the same step that failed);
+ *   - the pass bit (1 = forward, 2 = backward) is ORed into a status word in
+ *     the workspace, which lstm_sd_forward's first kernel clears.
+ * lstm_sd_status waits for `stream` (a host synchronisation: not for graph
+ * capture) and returns LSTM_SD_EHIP with a message naming the failed pass
+ * when the status word of `workspace` is set since the last lstm_sd_forward
+ * on it, else LSTM_SD_OK.  A time-out cannot happen while the grid runs
+ * alone on the device; it guards against a device shared with other work.
+ * lstm_sd_set_barrier_timeout sets the bound for the whole process: seconds
+ * < 0 restores the default; 0 makes every wait fail at once (every kernel
+ * still ends normally), to exercise this path from the host. */
+int lstm_sd_status(const lstm_sd_dims* dims, const void* workspace, size_t workspace_bytes, void* stream);
+int lstm_sd_set_barrier_timeout(double seconds);
+
 /* Instrumentation for measuring one kernel's average duration on the
  * stream it runs on.  After lstm_sd_kernel_timer_start(name), every launch
  * of the named kernel made by this library is bracketed by a pair of HIP
@@ -318,8 +348,8 @@ int lstm_sd_case1_dropout_backward(int32_t seq_len, int32_t batch, int32_t featu
  * waits for the last pair, returns the summed elapsed time in milliseconds
  * and the number of launches, and turns the timer off.  Names:
  * "mask_build", "transpose", "fx", "step", "bwd", "dx", "wgrad",
- * "fwd_persist", "bwd_persist" (the persistent recurrent kernels, one launch
- * per layer; their pair is recorded around the cooperative launch),
+ * "fwd_persist", "bwd_persist" (the persistent recurrent kernels: one launch
+ * per layer, or one for a whole unidirectional stack),
  * "emb_grad" (lstm_sd_embedding_backward's one kernel), "ce" (the head's
  * softmax cross-entropy kernels; the head's FC products count as "fx", "dx"
  * and "wgrad").  Events

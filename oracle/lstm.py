@@ -14,6 +14,9 @@ column blocks i | f | g | o of a [K][4H] weight, K-major):
     h_t      = o * tanh(c_t)                     (Eq. 6)
   where s = 1/(1-p) (inverted dropout; the paper does not state the scale)
   and the masks are broadcast over the batch rows (Case-III, Sec. 3.1).
+  Each rate is one number for every layer, or one per layer (a dropout
+  vector with a rate per site, as the AWD-LSTM workload of Sec. 4.1 uses):
+  layer l then takes p_nr[l] on its input and p_rh[l] on its recurrence.
   The recurrent mask touches only the copy of h_prev that enters U; the
   carried h and the cell state are never dropped (Sec. 3.2, FP paragraph).
   The reverse direction runs t = T-1 .. 0 with h_prev = h_{t+1}.  Layer
@@ -46,6 +49,11 @@ def _sigmoid(z):
 
 def _scale(p: float) -> float:
     return 1.0 / (1.0 - p) if p > 0.0 else 1.0
+
+
+def layer_rate(p, l: int) -> float:
+    """The rate of layer l: p itself, or p[l] for a per-layer sequence."""
+    return float(p[l]) if isinstance(p, (list, tuple, np.ndarray)) else float(p)
 
 
 @dataclasses.dataclass
@@ -87,13 +95,13 @@ def forward(params: Params, x, h0, c0, m_nr, m_rh, p_nr: float, p_rh: float,
     L, D, H = params.num_layers, params.num_dirs, params.hidden
     x = np.asarray(x, dtype=np.float64)
     T, B, _ = x.shape
-    s_nr, s_rh = _scale(p_nr), _scale(p_rh)
     valid = _valid(lengths, T, B)
     hT = np.zeros((L * D, B, H))
     cT = np.zeros((L * D, B, H))
     inp = x
     layer_in, steps = [], []
     for l in range(L):
+        s_nr, s_rh = _scale(layer_rate(p_nr, l)), _scale(layer_rate(p_rh, l))
         xt = inp * (np.asarray(m_nr[l], dtype=np.float64)[:, None, :] * s_nr)
         layer_in.append(xt)
         outs = []
@@ -140,7 +148,6 @@ def backward(cache: Cache, dy, dhT=None, dcT=None):
     L, D, H = P.num_layers, P.num_dirs, P.hidden
     dy = np.asarray(dy, dtype=np.float64)
     T, B, _ = dy.shape
-    s_nr, s_rh = _scale(cache.p_nr), _scale(cache.p_rh)
     valid = _valid(cache.lengths, T, B)
     dW = [None] * (L * D)
     dU = [None] * (L * D)
@@ -149,6 +156,7 @@ def backward(cache: Cache, dy, dhT=None, dcT=None):
     dc0 = np.zeros((L * D, B, H))
     dout = dy                      # gradient w.r.t. the current layer's output
     for l in range(L - 1, -1, -1):
+        s_nr, s_rh = _scale(layer_rate(cache.p_nr, l)), _scale(layer_rate(cache.p_rh, l))
         xt = cache.layer_in[l]
         dxt = np.zeros_like(xt)    # gradient w.r.t. x~ (masked input)
         for d in range(D):

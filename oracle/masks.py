@@ -84,13 +84,16 @@ def keep_lists(mask: np.ndarray):
 
 
 def all_masks(seed: int, step: int, num_layers: int, num_dirs: int, T: int,
-              k_in, hidden: int, p_nr: float, p_rh: float, fixed: bool = False):
-    """Masks for every site of a stacked (bi)LSTM.
+              k_in, hidden: int, p_nr, p_rh, fixed: bool = False):
+    """Masks for every site of a stacked (bi)LSTM.  p_nr and p_rh are one
+    rate for every layer or a sequence of one rate per layer (each site then
+    draws with its own layer's rate).
 
     Returns (nr, rh): nr[l] is [T][k_in(l)], rh[l][d] is [T][hidden].
     """
     draw = keep_mask_fixed if fixed else keep_mask
-    nr = [draw(seed, step, nr_stream(l), T, k_in(l), p_nr) for l in range(num_layers)]
-    rh = [[draw(seed, step, rh_stream(l, d), T, hidden, p_rh) for d in range(num_dirs)]
+    rate = lambda p, l: float(p[l]) if isinstance(p, (list, tuple, np.ndarray)) else float(p)
+    nr = [draw(seed, step, nr_stream(l), T, k_in(l), rate(p_nr, l)) for l in range(num_layers)]
+    rh = [[draw(seed, step, rh_stream(l, d), T, hidden, rate(p_rh, l)) for d in range(num_dirs)]
           for l in range(num_layers)]
     return nr, rh

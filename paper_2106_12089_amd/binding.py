@@ -25,7 +25,9 @@ class lstm_sd_dims(ctypes.Structure):
                 ("hidden", ctypes.c_int32), ("batch", ctypes.c_int32),
                 ("seq_len", ctypes.c_int32), ("num_dirs", ctypes.c_int32),
                 ("dtype", ctypes.c_int32), ("compact", ctypes.c_int32),
-                ("p_nr", ctypes.c_double), ("p_rh", ctypes.c_double)]
+                ("p_nr", ctypes.c_double), ("p_rh", ctypes.c_double),
+                ("p_nr_layer", ctypes.POINTER(ctypes.c_double)),
+                ("p_rh_layer", ctypes.POINTER(ctypes.c_double))]
 
 
 class lstm_sd_weights(ctypes.Structure):
@@ -87,6 +89,8 @@ SIGNATURES = {
     "lstm_sd_head_mask_generate": (ctypes.c_int, [_HD, ctypes.c_uint64, ctypes.c_uint64, _P, _SZ, _P]),
     "lstm_sd_head_forward": (ctypes.c_int, [_HD, _P, _P, _P, _P, _SZ, _P, _P, _SZ, _P]),
     "lstm_sd_head_backward": (ctypes.c_int, [_HD, _P, _P, _P, _P, _SZ, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "lstm_sd_status": (ctypes.c_int, [_DIMS, _P, _SZ, _P]),
+    "lstm_sd_set_barrier_timeout": (ctypes.c_int, [ctypes.c_double]),
     "lstm_sd_kernel_timer_start": (ctypes.c_int, [ctypes.c_char_p]),
     "lstm_sd_kernel_timer_stop": (ctypes.c_int, [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]),
 }
@@ -123,10 +127,29 @@ def _check(rc):
     return rc
 
 
+def _rates(p, num_layers):
+    """A scalar rate, or a per-layer sequence as a ctypes double array (the
+    structure's pointer field keeps it alive)."""
+    if isinstance(p, (list, tuple)):
+        if len(p) != num_layers:
+            raise ValueError(f"{len(p)} per-layer rates for {num_layers} layers")
+        return float(p[0]), (ctypes.c_double * num_layers)(*[float(v) for v in p])
+    return float(p), None
+
+
 def make_dims(num_layers, input_dim, hidden, batch, seq_len, num_dirs=1, dtype=DTYPE_BF16,
               compact=1, p_nr=0.0, p_rh=0.0) -> lstm_sd_dims:
-    return lstm_sd_dims(num_layers, input_dim, hidden, batch, seq_len, num_dirs, dtype, compact,
-                        float(p_nr), float(p_rh))
+    """p_nr / p_rh: one rate for every layer, or a list of L rates."""
+    nr, nr_arr = _rates(p_nr, num_layers)
+    rh, rh_arr = _rates(p_rh, num_layers)
+    d = lstm_sd_dims(num_layers, input_dim, hidden, batch, seq_len, num_dirs, dtype, compact, nr, rh)
+    if nr_arr is not None:
+        d.p_nr_layer = ctypes.cast(nr_arr, ctypes.POINTER(ctypes.c_double))
+        d._keep_nr = nr_arr
+    if rh_arr is not None:
+        d.p_rh_layer = ctypes.cast(rh_arr, ctypes.POINTER(ctypes.c_double))
+        d._keep_rh = rh_arr
+    return d
 
 
 def _ptr(t):
@@ -293,6 +316,18 @@ def lstm_sd_head_backward(hd, W_fc, targets, lengths, mask_buf, logits, loss, dy
                                         _ptr(mask_buf), _nbytes(mask_buf), _ptr(logits), _ptr(loss), _ptr(dy),
                                         _ptr(dW_fc), _ptr(db_fc), _ptr(workspace), _nbytes(workspace),
                                         _stream(stream)))
+
+
+def lstm_sd_status(dims, workspace, stream=None):
+    """Waits for the stream; raises LstmSdError (EHIP) if a grid barrier of
+    the step last run on this workspace timed out."""
+    _check(load().lstm_sd_status(ctypes.byref(dims), _ptr(workspace), _nbytes(workspace), _stream(stream)))
+
+
+def lstm_sd_set_barrier_timeout(seconds: float):
+    """Process-wide bound of a grid-barrier wait; < 0 restores the default,
+    0 makes every wait fail at once (tests of the failure path)."""
+    _check(load().lstm_sd_set_barrier_timeout(float(seconds)))
 
 
 def lstm_sd_kernel_timer_start(kernel: str):

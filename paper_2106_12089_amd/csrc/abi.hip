@@ -7,6 +7,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <atomic>
 #include <string>
 
 #include "../../include/lstm_sd.h"
@@ -66,6 +67,12 @@ int make_plan(const lstm_sd_dims* d, Plan* p, const char** why) {
     if (!(d->p_nr >= 0.0 && d->p_nr < 1.0) || !(d->p_rh >= 0.0 && d->p_rh < 1.0)) {
         *why = "dropout rates must be in [0, 1)"; return LSTM_SD_EINVAL;
     }
+    for (int l = 0; l < d->num_layers && l < 16; ++l) {
+        const double a = d->p_nr_layer ? d->p_nr_layer[l] : 0.0, b = d->p_rh_layer ? d->p_rh_layer[l] : 0.0;
+        if (!(a >= 0.0 && a < 1.0) || !(b >= 0.0 && b < 1.0)) {
+            *why = "per-layer dropout rates must be in [0, 1)"; return LSTM_SD_EINVAL;
+        }
+    }
     if (d->compact != 0 && d->compact != 1) { *why = "compact must be 0 or 1"; return LSTM_SD_EINVAL; }
     if (d->dtype != LSTM_SD_DTYPE_F32 && d->dtype != LSTM_SD_DTYPE_BF16) {
         *why = "dtype must be 0 (f32) or 1 (bf16)"; return LSTM_SD_EUNSUPPORTED;
@@ -81,8 +88,13 @@ int make_plan(const lstm_sd_dims* d, Plan* p, const char** why) {
     Plan& q = *p;
     q.L = d->num_layers; q.I = d->input_dim; q.H = d->hidden; q.B = d->batch; q.T = d->seq_len;
     q.D = d->num_dirs; q.dtype = d->dtype; q.compact = d->compact;
-    q.p_nr = d->p_nr; q.p_rh = d->p_rh;
-    q.s_nr = inv_keep(d->p_nr); q.s_rh = inv_keep(d->p_rh);
+    for (int l = 0; l < 16; ++l) {
+        const bool in = l < q.L;
+        q.p_nr[l] = in && d->p_nr_layer ? d->p_nr_layer[l] : d->p_nr;
+        q.p_rh[l] = in && d->p_rh_layer ? d->p_rh_layer[l] : d->p_rh;
+        q.s_nr[l] = inv_keep(q.p_nr[l]);
+        q.s_rh[l] = inv_keep(q.p_rh[l]);
+    }
     q.esize = d->dtype == LSTM_SD_DTYPE_BF16 ? 2 : 4;
     q.G = 4 * q.H;
     q.BP = (q.B + 31) / 32 * 32;
@@ -163,16 +175,20 @@ static bool use_persistent() {
     return !(v && v[0] == '0');
 }
 
-// Wall-clock ticks of the grid-barrier time-out (0.5 s).
+// Grid-barrier time-out of the persistent kernels: 0.5 s by default, or
+// what lstm_sd_set_barrier_timeout set (process-wide), in wall-clock ticks.
+static std::atomic<double> g_timeout_s{-1.0};
 static long long barrier_timeout_ticks() {
-    static long long ticks = 0;
-    if (!ticks) {
-        int dev = 0, khz = 0;
+    static int khz = 0;
+    if (!khz) {
+        int dev = 0, k = 0;
         if (hipGetDevice(&dev) != hipSuccess) dev = 0;
-        if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess || khz <= 0) khz = 100000;
-        ticks = (long long)khz * 500;
+        if (hipDeviceGetAttribute(&k, hipDeviceAttributeWallClockRate, dev) != hipSuccess || k <= 0) k = 100000;
+        khz = k;
     }
-    return ticks;
+    const double sec = g_timeout_s.load();
+    if (sec < 0.0) return (long long)khz * 500;
+    return (long long)(sec * 1000.0 * khz);
 }
 
 static int hip_check(const char* where) {
@@ -232,7 +248,7 @@ static int do_masks(const lstm_sd_dims* dims, uint64_t seed, uint64_t step, void
     for (int s = 0; s < P.sites; ++s) {
         a.K[s] = P.site_k(s);
         a.sid[s] = P.stream_id(s);
-        a.thr[s] = threshold64(s < P.L ? P.p_nr : P.p_rh);
+        a.thr[s] = threshold64(P.site_p(s));
     }
     launch_mask_build(a, P.sites, (hipStream_t)stream);
     return hip_check("mask kernel launch");
@@ -282,6 +298,8 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
         pd.hT = hT + (size_t)k * B * H;
         pd.cT = cT + (size_t)k * B * H;
         pd.dir = d;
+        pd.s_rh = P.s_rh[l];
+        pd.s_nr = P.s_nr[l];
         pd.role = 0;
         pd.dep = -1;
         if (l == L - 1) {
@@ -299,7 +317,6 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
         pa.timeout = barrier_timeout_ticks();
         pa.B = B; pa.H = H; pa.HP = P.HP; pa.T = T; pa.BP = BP; pa.ldy = D * H; pa.dense = !P.compact;
         pa.mtiles = P.mtiles;
-        pa.s = P.s_rh; pa.s_nr = P.s_nr;
         pa.xxs = P.xxs;
     };
     auto launch_fx_layer = [&](int l) {
@@ -313,7 +330,7 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
             f.bias = w->b[l * D + d];
             f.site = site_view(P, mbuf, P.site_nr(l));
             f.Gx = (float*)(W + P.w_gx) + (size_t)d * T * B * G;
-            f.K = kin; f.B = B; f.G = G; f.T = T; f.dense = !P.compact; f.s = P.s_nr;
+            f.K = kin; f.B = B; f.G = G; f.T = T; f.dense = !P.compact; f.s = P.s_nr[l];
             attach_tr(f);
             launch_fx<E>(f, st);
         }
@@ -377,7 +394,7 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
             f.bias = w->b[l * D + d];
             f.site = site_view(P, mbuf, P.site_nr(l));
             f.Gx = (float*)(W + P.w_gx) + (size_t)d * T * B * G;
-            f.K = kin; f.B = B; f.G = G; f.T = T; f.dense = !P.compact; f.s = P.s_nr;
+            f.K = kin; f.B = B; f.G = G; f.T = T; f.dense = !P.compact; f.s = P.s_nr[l];
             attach_tr(f);
             launch_fx<E>(f, st);
         }
@@ -398,7 +415,7 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
         for (int s = 0; s < T; ++s) {
             StepArgs a;
             memset(&a, 0, sizeof(a));
-            a.lengths = lengths; a.B = B; a.H = H; a.ldy = D * H; a.BP = BP; a.dense = !P.compact; a.s = P.s_rh;
+            a.lengths = lengths; a.B = B; a.H = H; a.ldy = D * H; a.BP = BP; a.dense = !P.compact; a.s = P.s_rh[l];
             for (int d = 0; d < D; ++d) {
                 const int k = l * D + d;
                 const int t = d == 0 ? s : T - 1 - s;
@@ -444,6 +461,7 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
     char* W = (char*)ws;
     unsigned* sync_bar = (unsigned*)(W + P.w_sync);
     int* sync_err = (int*)(W + P.w_sync + SYNC_ERR_OFS);
+    const int* sync_status = (const int*)(W + P.w_sync + SYNC_STATUS_OFS);
     const int tps_h = ((H + 7) / 8 + 15) / 16;     // 16-unit tiles per XCD slice of the hidden units
     // DA and DA^T regions: one per direction, or one per layer when a
     // unidirectional stack runs in one launch
@@ -456,7 +474,7 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
         pa.err = (int*)(W + P.w_sync + SYNC_ERR_OFS);
         pa.timeout = barrier_timeout_ticks();
         pa.B = B; pa.H = H; pa.T = T; pa.BP = BP; pa.ldy = D * H;
-        pa.kmax = P.kmax; pa.dense = !P.compact; pa.mtiles = P.mtiles; pa.s = P.s_rh; pa.s_nr = P.s_nr;
+        pa.kmax = P.kmax; pa.dense = !P.compact; pa.mtiles = P.mtiles;
     };
     auto fill_layer = [&](PBwdDir& pd, int l, int d, int reg) {
         const int k = l * D + d;
@@ -474,6 +492,7 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
         pd.dh0 = dh0 + (size_t)k * B * H;
         pd.dc0 = dc0 + (size_t)k * B * H;
         pd.dir = d;
+        pd.s_rh = P.s_rh[l];
         pd.above = -1;
     };
     // input gradient of layer l for the layer below (and the caller's dx)
@@ -489,13 +508,15 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
         // layer 0 writes the caller's full-width dx directly
         a.site = nv; a.out = l == 0 ? dx : dxc_here; a.scatter = l == 0; a.D = D; a.B = B; a.G = G; a.ldo = kin;
         a.T = T; a.K = kin; a.tps = ((kin + 7) / 8 + 15) / 16; a.mtiles = P.mtiles;
-        a.dense = !P.compact; a.s = P.s_nr;
+        a.dense = !P.compact; a.s = P.s_nr[l];
+        a.status = sync_status;
         launch_dx<E>(a, kin, st);
     };
     // weight and bias gradients (Eq. 11) of layer l: its problems join one
     // batch (row-sparse and full problems alike), one launch per batch
     WgBatch b;
     b.np = 0;
+    b.status = sync_status;
     auto add_wgrad = [&](const WgArgs& a) {
         if (b.np == WG_MAXP) {                 // full: launch it (its DA is complete)
             launch_wgrad<E>(b, st);
@@ -515,10 +536,10 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
             a.actT = XT; a.tstride = (long)kin * BP; a.actT_first = nullptr; a.t_first = -1; a.shift = 0;
             a.daT = daT_of(reg0 + d);
             a.site = nv; a.K = kin; a.B = B; a.BP = BP; a.G = G; a.T = T;
-            a.dense = !P.compact; a.s = P.s_nr;
+            a.dense = !P.compact; a.s = P.s_nr[l];
             a.out = g->dW[k];
             a.db = g->db[k];                      // the bias gradient rides on the input-weight pass
-            a.full = P.p_nr == 0.0 || !P.compact;
+            a.full = P.p_nr[l] == 0.0 || !P.compact;
             add_wgrad(a);
 
             WgArgs u = a;
@@ -527,10 +548,10 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
             u.t_first = d == 0 ? 0 : T - 1;
             u.shift = d == 0 ? -1 : 1;
             u.site = site_view(P, mbuf, P.site_rh(l, d));
-            u.K = H; u.s = P.s_rh;
+            u.K = H; u.s = P.s_rh[l];
             u.out = g->dU[k];
             u.db = nullptr;
-            u.full = P.p_rh == 0.0 || !P.compact;
+            u.full = P.p_rh[l] == 0.0 || !P.compact;
             add_wgrad(u);
         }
     };
@@ -561,6 +582,7 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
                 wk.dir = 0;
                 wk.above = -1;
                 wk.Wup = w->W[l];
+                wk.s_nr = P.s_nr[l];
                 wk.nr_up = site_view(P, mbuf, P.site_nr(l));
                 wk.dxw_out = (float*)(W + P.w_dxw) + (size_t)(l - 1) * T * B * H;
                 wk.dh0 = dh0 + (size_t)l * B * H;         // unused by a worker (poisoning targets only)
@@ -617,7 +639,7 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
             memset(&a, 0, sizeof(a));
             a.lengths = lengths; a.B = B; a.H = H; a.BP = BP; a.ldy = D * H;
             a.lddx = l + 1 < L ? P.kin(l + 1) : 0;
-            a.tps = tps_h; a.has_next = s > 0; a.mtiles = P.mtiles; a.final_pass = final_pass; a.dense = !P.compact; a.s = P.s_rh;
+            a.tps = tps_h; a.has_next = s > 0; a.mtiles = P.mtiles; a.final_pass = final_pass; a.dense = !P.compact; a.s = P.s_rh[l];
             for (int d = 0; d < D; ++d) {
                 const int k = l * D + d;
                 const int t = final_pass ? -1 : (d == 0 ? T - 1 - s : s);   // BP order: reverse of FP
@@ -1034,6 +1056,31 @@ int lstm_sd_case1_dropout_backward(int32_t seq_len, int32_t batch, int32_t featu
     if (!dx || !mask || !dsrc) return fail(LSTM_SD_EINVAL, "a required pointer is NULL");
     launch_case1_undrop(dx, mask, dsrc, (long)seq_len * batch * features, inv_keep(p), (hipStream_t)stream);
     return hip_check("case-I dropout backward launch");
+}
+
+int lstm_sd_status(const lstm_sd_dims* dims, const void* workspace, size_t workspace_bytes, void* stream) {
+    Plan P; const char* why = nullptr;
+    int rc = make_plan(dims, &P, &why);
+    if (rc) return fail(rc, why);
+    if (!workspace) return fail(LSTM_SD_EINVAL, "workspace is NULL");
+    if (workspace_bytes < P.w_total) return fail(LSTM_SD_EWORKSPACE, "workspace_bytes smaller than lstm_sd_workspace_bytes()");
+    int v = 0;
+    hipError_t e = hipStreamSynchronize((hipStream_t)stream);
+    if (e == hipSuccess) e = hipMemcpy(&v, (const char*)workspace + P.w_sync + SYNC_STATUS_OFS, sizeof(v), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return fail(LSTM_SD_EHIP, std::string("status read: ") + hipGetErrorString(e));
+    if (v == 0) return LSTM_SD_OK;
+    std::string m = "grid barrier time-out in the";
+    if (v & STATUS_FWD) m += " forward";
+    if ((v & STATUS_FWD) && (v & STATUS_BWD)) m += " and the";
+    if (v & STATUS_BWD) m += " backward";
+    m += " pass of the last step: its outputs were written as NaN";
+    return fail(LSTM_SD_EHIP, m);
+}
+
+int lstm_sd_set_barrier_timeout(double seconds) {
+    if (!(seconds == seconds)) return fail(LSTM_SD_EINVAL, "time-out is NaN");
+    g_timeout_s.store(seconds < 0.0 ? -1.0 : seconds);
+    return LSTM_SD_OK;
 }
 
 int lstm_sd_kernel_timer_start(const char* kernel) {

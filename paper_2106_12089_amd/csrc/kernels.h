@@ -55,7 +55,7 @@ struct TransArgs {
     float *hT, *cT;
     long n_init;
     unsigned* bar;
-    int* err;
+    int* err;                           // (the status word follows at SYNC_STATUS_OFS - SYNC_ERR_OFS bytes)
 };
 
 // Forward input product of one layer/direction, all t in one launch:
@@ -149,6 +149,7 @@ struct DxArgs {
     int scatter;                        //   (scatter) every column at its own, the dropped ones as zeros
     int D, B, G, ldo, T, K, tps, dense, mtiles;
     float s;
+    const int* status;                  // sticky barrier status of the step, or null: when set, NaN is written
 };
 
 // Weight gradient of one (layer, direction, site), summed over every step:
@@ -173,10 +174,11 @@ constexpr int WG_MAXP = 8;
 struct WgBatch {
     WgArgs p[WG_MAXP];
     int np;
+    const int* status;                  // sticky barrier status of the step, or null: when set, NaN is written
 };
 
 // Persistent forward recurrence of one layer (both directions): one
-// cooperative launch runs all T steps.
+// launch runs all T steps.
 struct PFwdDir {
     const void* h0;                     // [B][H] row-major h0 (dtype)
     const void* U;                      // [H][4H]
@@ -193,6 +195,7 @@ struct PFwdDir {
     void* ybuf;                         // inner layer: ybuf + d*H, or null
     void* ybufT;                        // inner layer: ybufT + d*H*BP (t stride ldy*BP), or null
     int dir;                            // 0: t = 0 .. T-1;  1: t = T-1 .. 0
+    float s_rh, s_nr;                   // dropout scales of the slot's layer (RH; NR of its input)
     // A unidirectional stack whose layers run in one launch: each layer above
     // the first has an input-product worker slot, which forms
     // gx_t = s_nr * x~_t W + b (Eq. 1-4, input part) from x_t, the output of
@@ -225,6 +228,13 @@ constexpr int BAR_LINES = 16;
 static_assert((BAR_LINES & (BAR_LINES - 1)) == 0 && BAR_LINES <= 32, "counter lines: a power of 2, two slots per wave");
 constexpr int BAR_EXIT = 8;
 constexpr int SYNC_ERR_OFS = BAR_PITCH * 4 * (BAR_LINES * BAR_EXIT + 1);   // bytes
+// Sticky status word (a cache line of its own): a persistent launch whose
+// barrier wait timed out ORs its pass bit into it.  The forward pass's init
+// clears it, nothing else does, so after a backward it tells whether the
+// forward or the backward of that step failed; the weight- and
+// input-gradient kernels read it and write NaN instead of values when set.
+constexpr int SYNC_STATUS_OFS = SYNC_ERR_OFS + 128;
+constexpr int STATUS_FWD = 1, STATUS_BWD = 2;
 constexpr int SYNC_BYTES = SYNC_ERR_OFS + 256;
 
 struct PFwdArgs {
@@ -232,15 +242,14 @@ struct PFwdArgs {
     const int32_t* lengths;
     unsigned* bar;                      // barrier counters (BAR_LINES lines per slot; clear at launch)
     int* err;                           // barrier time-out flag
-    long long timeout;                  // wall-clock ticks
+    long long timeout;                  // wall-clock ticks (<= 0: every wait fails at once)
     int B, H, HP, T, BP, ldy, dense, ntiles, mgroups, mtiles;
     int nslots, KP, kin_max;            // KP: LDS pitch of the W slices (0: no slot has Win)
     size_t wofs, kofs;                  // LDS offsets of the W slice and the keep lists (set by the launcher)
     size_t xxs;                         // elements per xin/xout slot
-    float s, s_nr;
 };
 
-// Persistent BPTT of one layer (both directions): one cooperative launch
+// Persistent BPTT of one layer (both directions): one launch
 // runs all T backward steps and the final pass that forms dh0/dc0.
 struct PBwdDir {
     const void* U;                      // [H][4H]
@@ -258,6 +267,7 @@ struct PBwdDir {
     float* dh0;                         // [B][H]
     float* dc0;                         // [B][H]
     int dir;                            // 0: t = T-1 .. 0 (BP of the forward direction);  1: t = 0 .. T-1
+    float s_rh, s_nr;                   // layer: its RH scale; worker: the NR scale of the layer above
     // A unidirectional stack in one launch: the input gradient of layer l+1
     // (Eq. 10, dx = s * da W^T over the kept inputs) is formed per step by a
     // worker slot from the DA layer l+1 publishes, and read by layer l.
@@ -274,9 +284,8 @@ struct PBwdArgs {
     const int32_t* lengths;
     unsigned* bar;
     int* err;
-    long long timeout;
+    long long timeout;                  // wall-clock ticks (<= 0: every wait fails at once)
     int B, H, T, BP, ldy, lddx, kmax, dense, ntiles, mgroups, mtiles, nslots;
-    float s, s_nr;
 };
 
 }  // namespace lsd

@@ -153,7 +153,10 @@ __device__ __forceinline__ void transpose_block(const TransArgs& a, int N, int b
         const long nb = (long)gx * gy, bi = (long)by * gx + bx;
         if (bi == 0) {
             for (int i = tid; i <= BAR_LINES * BAR_EXIT; i += 256) a.bar[BAR_PITCH * i] = 0u;
-            if (tid == 0) *a.err = 0;
+            if (tid == 0) {
+                *a.err = 0;
+                *(int*)((char*)a.err + (SYNC_STATUS_OFS - SYNC_ERR_OFS)) = 0;   // a new step's status
+            }
         }
         for (long i = bi * 256 + tid; i < a.n_init; i += nb * 256) {
             a.hT[i] = to_f32<T>(((const T*)a.h0)[i]);
@@ -563,13 +566,15 @@ __global__ void __launch_bounds__(256) k_dx(DxArgs a) {
     const int hi = ks[2 * x + 2];
     const int j0 = ks[2 * x] + 16 * ti;
     const int m0 = blockIdx.z * 64;
+    // a step whose recurrence timed out gets NaN in every output
+    const bool failed = a.status && *a.status != 0;
     if (a.scatter && ti < a.tps) {
         const int32_t* ds = a.site.dseg + (size_t)t * (NSEG + 1);
         const int dj = ds[2 * x] + 16 * ti + (threadIdx.x & 15);
         if (dj < ds[2 * x + 2]) {
             const int kd = a.site.drop[(size_t)t * a.site.kmax + dj];
             for (int r = threadIdx.x >> 4; r < 16 * MT; r += 16)
-                if (m0 + r < a.B) a.out[((size_t)t * a.B + m0 + r) * a.ldo + kd] = 0.0f;
+                if (m0 + r < a.B) a.out[((size_t)t * a.B + m0 + r) * a.ldo + kd] = failed ? __builtin_nanf("") : 0.0f;
         }
     }
     if (ti >= a.tps || j0 >= hi) return;
@@ -628,7 +633,7 @@ __global__ void __launch_bounds__(256) k_dx(DxArgs a) {
             const int kk = krow[jj];
             const float sc = (a.dense && !mrow[kk]) ? 0.0f : a.s;
             out[(size_t)row * a.ldo + (a.scatter ? kk : jj)] =
-                sc * (red[0][rr][c] + red[1][rr][c] + red[2][rr][c] + red[3][rr][c]);
+                failed ? __builtin_nanf("") : sc * (red[0][rr][c] + red[1][rr][c] + red[2][rr][c] + red[3][rr][c]);
         }
     }
 }
@@ -1104,6 +1109,21 @@ __device__ __forceinline__ void wgrad_full(const WgArgs& a, float* red) {
     }
 }
 
+// NaN into the part of a problem's outputs this workgroup owns (slice x =
+// i % 8 of the rows, 128 columns of block i / 8; slice 0 also the bias)
+__device__ __forceinline__ void wgrad_poison(const WgArgs& a) {
+    const int x = blockIdx.x % NXCD, n0 = (blockIdx.x / NXCD) * WG_NB;
+    const int r0 = slice_start(x, a.K), r1 = slice_start(x + 1, a.K);
+    const float nan = __builtin_nanf("");
+    for (int i = threadIdx.x; i < (r1 - r0) * WG_NB; i += blockDim.x) {
+        const int rr = i / WG_NB, cc = i % WG_NB;
+        if (n0 + cc < a.G) a.out[(size_t)(r0 + rr) * a.G + n0 + cc] = nan;
+    }
+    if (a.db && x == 0)
+        for (int c = threadIdx.x; c < WG_NB; c += blockDim.x)
+            if (n0 + c < a.G) a.db[n0 + c] = nan;
+}
+
 // LDS of the full kernel's pass reduction
 template <typename T>
 constexpr size_t wgrad_full_lds_bytes() { return (size_t)WG_NWV * (WgTiles<T>::N / 2) * WG_CT * 4 * 64 * 4; }
@@ -1116,6 +1136,10 @@ template <typename T, bool MASKED, bool MULTI>
 __global__ void __launch_bounds__(128 * WG_NWV) __attribute__((amdgpu_waves_per_eu(sizeof(T) == 2 && !MULTI ? 4 : 1))) k_wgrad(WgBatch bt) {
     extern __shared__ float acc_lds[];
     const WgArgs& a = bt.p[blockIdx.z];
+    if (bt.status && *bt.status != 0) {        // the step's recurrence timed out: NaN in every output
+        wgrad_poison(a);
+        return;
+    }
     if (a.full) wgrad_full<T, MASKED, WgTiles<T>::N / 2, MULTI>(a, acc_lds);
     else wgrad_gather<T, MULTI>(a, acc_lds);
 }

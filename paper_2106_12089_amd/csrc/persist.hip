@@ -1,4 +1,4 @@
-// Persistent recurrent kernels (gfx950): one cooperative launch runs every
+// Persistent recurrent kernels (gfx950): one launch runs every
 // time step of a layer.  Each workgroup keeps its slice of the recurrent
 // weight U in LDS and its part of the cell state in registers for the whole
 // sequence; the workgroups meet at a grid barrier once per step.
@@ -49,6 +49,8 @@ __device__ __forceinline__ unsigned bar_count(int nslot, int slot, int i) {
     return (unsigned)(upto((slot + 1) * nslot) - upto(slot * nslot));
 }
 __device__ __forceinline__ unsigned* slot_bar(unsigned* bar, int slot) { return bar + BAR_PITCH * BAR_LINES * slot; }
+// the sticky status word of the step, beside the error flag
+__device__ __forceinline__ int* sync_status(int* err) { return (int*)((char*)err + (SYNC_STATUS_OFS - SYNC_ERR_OFS)); }
 
 __device__ __forceinline__ void grid_arrive(unsigned* sbar) {
     __builtin_amdgcn_s_waitcnt(0);      // this thread's stores have completed
@@ -64,9 +66,23 @@ __device__ __forceinline__ void grid_arrive(unsigned* sbar) {
 // has timed out (err set).  With seen / seen2 (LDS), also records the number
 // of steps the lines read last show as complete.
 __device__ __forceinline__ bool grid_wait(unsigned* sbar, int slot, int nslot, unsigned steps, int* err,
-                                          long long timeout, unsigned* seen = nullptr, unsigned* sbar2 = nullptr,
-                                          int slot2 = 0, unsigned steps2 = 0, unsigned* seen2 = nullptr) {
+                                          long long timeout, int fail_bit, unsigned* seen = nullptr,
+                                          unsigned* sbar2 = nullptr, int slot2 = 0, unsigned steps2 = 0,
+                                          unsigned* seen2 = nullptr) {
     __shared__ int ok;
+    if (timeout <= 0) {
+        // a zero time-out (set from the host, for tests of the failure
+        // path): every wait fails at once, so every workgroup leaves through
+        // the time-out path without spinning.  The flags are set before the
+        // workgroup barrier, so every thread reads them set afterwards.
+        if (threadIdx.x == 0) {
+            __hip_atomic_fetch_or(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_fetch_or(sync_status(err), fail_bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __builtin_amdgcn_s_waitcnt(0);      // both have completed
+        }
+        __syncthreads();
+        return false;
+    }
     if (threadIdx.x < 64) {
         const int i = threadIdx.x;
         const bool second = i >= BAR_LINES;
@@ -85,7 +101,11 @@ __device__ __forceinline__ bool grid_wait(unsigned* sbar, int slot, int nslot, u
             if (__builtin_amdgcn_ballot_w64(n != 0 && v < want) == 0) break;
             const long long el = wall_clock64() - t0;
             if (el > timeout) {
-                if (i == 0) __hip_atomic_fetch_or(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if (i == 0) {
+                    __hip_atomic_fetch_or(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    __hip_atomic_fetch_or(sync_status(err), fail_bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    __builtin_amdgcn_s_waitcnt(0);
+                }
                 good = 0;
                 break;
             }
@@ -115,7 +135,9 @@ __device__ __forceinline__ bool grid_wait(unsigned* sbar, int slot, int nslot, u
 // Every workgroup ends here, past its last barrier wait; the last one to
 // arrive returns the step counters, the error flag and the exit counter to
 // zero, so the next launch starts clear without a clearing kernel.  (The
-// outputs' time-out check comes before: the flag is read by then.)
+// outputs' time-out check comes before: the flag is read by then.  A
+// time-out stays recorded in the sticky status word, which this does not
+// clear.)
 __device__ __forceinline__ void grid_exit(unsigned* bar, int nslots, int* err) {
     __syncthreads();
     if (threadIdx.x == 0) {
@@ -494,7 +516,7 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
     auto x_product = [&](int s) -> bool {
         commit_kidx_x();
         if (seen_dep < (unsigned)(s + 2)) {
-            if (!grid_wait(bar_dep, D.dep, nslot, (unsigned)(s + 2), a.err, a.timeout, &dep_seen)) return false;
+            if (!grid_wait(bar_dep, D.dep, nslot, (unsigned)(s + 2), a.err, a.timeout, STATUS_FWD, &dep_seen)) return false;
             seen_dep = dep_seen;
         } else {
             __syncthreads();                    // the keep list just committed
@@ -544,7 +566,7 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
                 float pre[4];
                 red_sum(q, pre);
 #pragma unroll
-                for (int g = 0; g < 4; ++g) xstore(D.gxo + ((size_t)t * B + b) * G + g * H + u, a.s_nr * pre[g] + biasr[q][g]);
+                for (int g = 0; g < 4; ++g) xstore(D.gxo + ((size_t)t * B + b) * G + g * H + u, D.s_nr * pre[g] + biasr[q][g]);
             }
             prefetch(s + 1);
             grid_arrive(bar);                   // (also: every wave is past its reads of red)
@@ -589,7 +611,7 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
         // h_{t-1} of every workgroup of this slot, and (a fed layer) the input
         // product of t, whose loads then overlap the product below
         const bool need_dep = fed && seen_dep < (unsigned)(s + 1);
-        if (!grid_wait(bar, d, nslot, (unsigned)(s + 1), a.err, a.timeout, nullptr, need_dep ? bar_dep : nullptr,
+        if (!grid_wait(bar, d, nslot, (unsigned)(s + 1), a.err, a.timeout, STATUS_FWD, nullptr, need_dep ? bar_dep : nullptr,
                        D.dep, (unsigned)(s + 1), &dep_seen))
             break;
         if (need_dep) seen_dep = dep_seen;
@@ -613,7 +635,7 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
             for (int j = 0; j < NT; ++j)
 #pragma unroll
                 for (int r = 0; r < 4; ++r)
-                    acc[i][j][r] = has_x ? a.s * acc[i][j][r] + a.s_nr * accx[i][j][r] : a.s * acc[i][j][r];
+                    acc[i][j][r] = has_x ? D.s_rh * acc[i][j][r] + D.s_nr * accx[i][j][r] : D.s_rh * acc[i][j][r];
         red_store(acc);
         // ---- pointwise (Eq. 1-6); h_t (and the layer above's x_t) is published first
         T* hxn = (T*)D.hx + (size_t)((s + 1) & 1) * hxs;
@@ -666,13 +688,16 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
         prefetch(s + 1);
         if (has_x && s + 1 < T_ && !x_product(s + 1)) break;
     }
-    // ---- final state (NaN if the barrier timed out)
+    // ---- final state (NaN if the barrier timed out, and then also every
+    // step of the top layer's output)
     const bool failed = __hip_atomic_load(a.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0;
 #pragma unroll
     for (int q = 0; q < PPT; ++q) {
         if (pb[q] < B && pu[q] < H) {
             D.hT[(size_t)pb[q] * H + pu[q]] = failed ? __builtin_nanf("") : hreg[q];
             D.cT[(size_t)pb[q] * H + pu[q]] = failed ? __builtin_nanf("") : creg[q];
+            if (failed && D.y)
+                for (int t = 0; t < T_; ++t) D.y[((size_t)t * B + pb[q]) * a.ldy + pu[q]] = __builtin_nanf("");
         }
     }
     grid_exit(a.bar, a.nslots, a.err);
@@ -859,14 +884,14 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
             int mk[PPT];
 #pragma unroll
             for (int q = 0; q < PPT; ++q) mk[q] = D.nr_up.mask[(size_t)t * D.nr_up.kmax + min(pu[q], H - 1)];
-            if (!grid_wait(bar_src, D.src, nslot, (unsigned)(s + 1), a.err, a.timeout)) break;
+            if (!grid_wait(bar_src, D.src, nslot, (unsigned)(s + 1), a.err, a.timeout, STATUS_BWD)) break;
             recurrent_product(t, S.da);
 #pragma unroll
             for (int q = 0; q < PPT; ++q) {
                 const int b = pb[q], u = pu[q];
                 if (b >= B || u >= H) continue;
                 // dropped inputs get no gradient (output sparsity, Eq. 10)
-                const float v = mk[q] ? a.s_nr * reduced(b - m0, u - u0) : 0.0f;
+                const float v = mk[q] ? D.s_nr * reduced(b - m0, u - u0) : 0.0f;
                 xstore(D.dxw_out + ((size_t)t * B + b) * H + u, v);
             }
             grid_arrive(bar);
@@ -890,7 +915,7 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
         const bool kept = has_next && tile_any_kept();
         const bool need_above = !final_pass && bar_above && seen_above < (unsigned)(s + 1);
         if (has_next || need_above) {
-            if (!grid_wait(bar, d, nslot, has_next ? (unsigned)s : 0u, a.err, a.timeout, nullptr,
+            if (!grid_wait(bar, d, nslot, has_next ? (unsigned)s : 0u, a.err, a.timeout, STATUS_BWD, nullptr,
                            need_above ? bar_above : nullptr, D.above, (unsigned)(s + 1), &above_seen))
                 break;
             if (need_above) seen_above = above_seen;
@@ -907,7 +932,7 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
             float dh = dhc[q];
             if (kept) {
                 // units dropped at step tn get no recurrent gradient (output sparsity, Eq. 10)
-                const float sc = mkr[q] ? a.s : 0.0f;
+                const float sc = mkr[q] ? D.s_rh : 0.0f;
                 dh += sc * reduced(b - m0, u - u0);
             }
             if (final_pass) {
@@ -963,8 +988,10 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
         }
         prefetch(s + 1);
     }
-    // a timed-out barrier poisons the input-state gradients
-    if (__hip_atomic_load(a.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
+    // a timed-out barrier, here or in the forward pass of the step, poisons
+    // the input-state gradients
+    if (__hip_atomic_load(a.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0 ||
+        __hip_atomic_load(sync_status(a.err), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
 #pragma unroll
         for (int q = 0; q < PPT; ++q)
             if (pb[q] < B && pu[q] < H) {
@@ -1006,13 +1033,8 @@ static hipError_t resident_limit(const void* fn, int threads, size_t lds, int nw
 
 // The persistent grids fit the device (resident_limit) and the stream runs
 // them after the previous kernel has drained, so every workgroup is placed
-// at once; a barrier wait is bounded in any case (timeout -> error flag).
-// LSTM_SD_COOP=1 launches them through the cooperative-launch API instead,
-// which also guarantees co-residency when other streams keep the device busy.
-static bool cooperative_api() {
-    const char* v = getenv("LSTM_SD_COOP");
-    return v && v[0] == '1';
-}
+// at once; a barrier wait is bounded in any case (time-out -> error flag and
+// the sticky status word that lstm_sd_status reads).
 // LDS layout: U slice at 0; the W slice at wofs (in place of U when only
 // workers hold W slices, after U when layers form their own input
 // products); keep lists at kofs; then the reduction area.  Returns the size.
@@ -1046,14 +1068,8 @@ hipError_t launch_fwd_persist(PFwdArgs& a, hipStream_t st, int kid_timer_on, hip
     hipError_t e = resident_limit((const void*)fn, 64 * PF_NW, lds, nwg);
     if (e != hipSuccess) return e;
     if (kid_timer_on) (void)hipEventRecord(e0, st);
-    if (!cooperative_api()) {
-        hipLaunchKernelGGL(fn, dim3(nwg), dim3(64 * PF_NW), lds, st, a);
-        e = hipGetLastError();
-    } else {
-        PFwdArgs arg = a;
-        void* params[] = {&arg};
-        e = hipLaunchCooperativeKernel((const void*)fn, dim3(nwg), dim3(64 * PF_NW), params, (unsigned)lds, st);
-    }
+    hipLaunchKernelGGL(fn, dim3(nwg), dim3(64 * PF_NW), lds, st, a);
+    e = hipGetLastError();
     if (kid_timer_on && e == hipSuccess) (void)hipEventRecord(e1, st);
     return e;
 }
@@ -1071,13 +1087,8 @@ static hipError_t launch_bwd_persist_t(const PBwdArgs& a, int nwg, size_t lds, h
     auto fn = k_bwd_persist<T, UB, MG>;
     const hipError_t e = resident_limit((const void*)fn, 64 * PB_NW, lds, nwg);
     if (e != hipSuccess) return e;
-    if (!cooperative_api()) {
-        hipLaunchKernelGGL(fn, dim3(nwg), dim3(64 * PB_NW), lds, st, a);
-        return hipGetLastError();
-    }
-    PBwdArgs arg = a;
-    void* params[] = {&arg};
-    return hipLaunchCooperativeKernel((const void*)fn, dim3(nwg), dim3(64 * PB_NW), params, (unsigned)lds, st);
+    hipLaunchKernelGGL(fn, dim3(nwg), dim3(64 * PB_NW), lds, st, a);
+    return hipGetLastError();
 }
 
 // Launches the persistent backward layer if it fits (else returns an error

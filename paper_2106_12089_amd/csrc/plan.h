@@ -12,8 +12,8 @@ inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 struct Plan {
     int L, I, H, B, T, D, dtype, compact;
-    double p_nr, p_rh;
-    float s_nr, s_rh;     // 1/(1-p) computed in double, rounded to float
+    double p_nr[16], p_rh[16];   // per layer
+    float s_nr[16], s_rh[16];    // 1/(1-p) computed in double, rounded to float
     int esize;            // bytes per element of x/W/U/h copies
     int G;                // 4H
     int BP;               // batch rounded up to 32 (transposed copies)
@@ -44,6 +44,7 @@ struct Plan {
     int site_nr(int l) const { return l; }
     int site_rh(int l, int d) const { return L + l * D + d; }
     int site_k(int s) const { return s < L ? kin(s) : H; }
+    double site_p(int s) const { return s < L ? p_nr[s] : p_rh[(s - L) / D]; }
     int stream_id(int s) const {
         if (s < L) return 4 * s;
         int r = s - L, l = r / D, d = r % D;

@@ -169,3 +169,27 @@ def test_case1_entry_points_validate_before_device_work():
     assert lib.lstm_sd_case1_dropout_backward(4, 2, 3, fake, None, D(0.5), fake, None) == B.EINVAL
     assert lib.lstm_sd_case1_dropout_backward(4, 2, 0, fake, fake, D(0.5), fake, None) == B.EINVAL
     assert "dimensions" in B.lstm_sd_last_error()
+
+
+def test_per_layer_rates_validated():
+    lib = B.load()
+    good = dims(num_layers=3, p_nr=[0.4, 0.25, 0.25], p_rh=[0.5, 0.5, 0.5])
+    assert B.lstm_sd_mask_bytes(good) == B.lstm_sd_mask_bytes(dims(num_layers=3))
+    for bad in (dict(p_nr=[0.4, 1.0, 0.25]), dict(p_rh=[0.5, -0.1, 0.5]), dict(p_nr=[0.4, float("nan"), 0.2])):
+        d = dims(num_layers=3, **bad)
+        assert lib.lstm_sd_mask_bytes(ctypes.byref(d)) == 0
+        assert "per-layer" in B.lstm_sd_last_error()
+        assert lib.lstm_sd_mask_generate(ctypes.byref(d), 1, 0, None, 0, None) == B.EINVAL
+    with pytest.raises(ValueError):
+        dims(num_layers=3, p_nr=[0.4, 0.25])
+
+
+def test_status_and_timeout_validate_before_device_work():
+    lib = B.load()
+    d = dims()
+    fake = 4096  # never dereferenced: the checks fail first
+    assert lib.lstm_sd_status(ctypes.byref(d), None, 10**9, None) == B.EINVAL
+    assert lib.lstm_sd_status(ctypes.byref(d), fake, 16, None) == B.EWORKSPACE
+    assert lib.lstm_sd_status(ctypes.byref(dims(hidden=0)), fake, 10**9, None) == B.EINVAL
+    assert lib.lstm_sd_set_barrier_timeout(ctypes.c_double(float("nan"))) == B.EINVAL
+    assert lib.lstm_sd_set_barrier_timeout(ctypes.c_double(-1.0)) == B.OK

@@ -2,17 +2,24 @@
 seeded workloads, at the workloads' full sizes, in every dropout mode.
 
 Bar: masks, keep lists and counts bit-exact; every output and gradient
-within a normwise relative error of 1e-4 (fp32 path) or 2e-2 (bf16 MFMA
-path); structurally zero entries exactly zero.  The stress shape is checked
-on a sample of batch rows: the GPU runs the full batch, the gradient of a
-loss that only sees the sampled rows is fed to both sides, and the oracle
-runs on those rows alone (rows are independent under batch-shared masks)."""
+within 1e-4 (fp32 path) or 2e-2 (bf16 MFMA path) by three measures each:
+the normwise relative error, max|gpu - ref| / max|ref|, and the normwise
+error of every 16x16 block (the MFMA tile) against the block's own norm;
+structurally zero entries exactly zero.  The stress shape is checked on 32
+batch rows, two in every 16-row tile: the GPU runs the full batch, the
+gradient of a loss that only sees the sampled rows is fed to both sides, and
+the oracle runs on those rows alone (rows are independent under
+batch-shared masks); one stress case also runs the oracle on the full
+batch, so that the weight gradients see every row.  LM-medium and the tagger
+also run at full size in fp32."""
+import dataclasses
+
 import numpy as np
 import pytest
 
 import workloads
 from tests._parity import (TOL, compare, fwd_persist_launches, mode_rates, oracle_masks, oracle_step, say,
-                           site_list)
+                           site_list, summary)
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -22,6 +29,11 @@ CASES = [(c, p) for c in ("tiny", "lm_medium", "lm_large", "seq2seq_enc", "tagge
          for p in workloads.get_config(c).p_values]
 
 _WL = {}
+
+# two rows in every 16-row MFMA tile of the stress batch (256 rows), at
+# lane positions that vary from tile to tile
+STRESS_ROWS = np.array(sorted({16 * i + o for i in range(16) for o in ((7 * i + 3) % 16, (7 * i + 11) % 16)}))
+assert len(STRESS_ROWS) == 32 and len(set(STRESS_ROWS // 16)) == 16
 
 
 def workload(name):
@@ -76,7 +88,7 @@ def test_step_parity(name, p, mode):
     tol = TOL[cfg.dtype]
     sess.forward()
     if name == "stress":
-        rows = np.array([0, 37, 101, 255])
+        rows = STRESS_ROWS
         sub = workloads.slice_rows(wl, rows)
         ref = oracle_step(sub, p_nr, p_rh, m_nr, m_rh)     # dy = MSE gradient over the sampled rows
         dy_full = np.zeros((cfg.seq_len, cfg.batch, cfg.num_dirs * cfg.hidden), dtype=np.float32)
@@ -100,7 +112,7 @@ def test_step_parity(name, p, mode):
         errs = compare(gpu, ref)
         if ref["loss"] is not None and cfg.loss == "mse":
             errs["loss"] = abs(gpu["loss"] - ref["loss"]) / abs(ref["loss"])
-    say("   errs max", max(errs.values()), {k: f"{v:.2e}" for k, v in errs.items()})
+    say("   errs", summary(errs), {k: f"{v:.2e}" for k, v in errs.items() if "." not in k})
     bad = {k: v for k, v in errs.items() if not v <= tol}
     assert not bad, bad
     # output sparsity (Eq. 10): dropped input columns get exactly zero gradient
@@ -189,3 +201,54 @@ def test_repeats_bit_identical(compact, p_rh):
             continue
         diff = [k for k in ref if not np.array_equal(ref[k], cur[k])]
         assert not diff, (it, diff)
+
+
+def test_stress_full_batch():
+    """Stress (B = 256, H = 1024, T = 64) at p = 0.5 in the paper's headline
+    mode, against the oracle on every batch row: every row tile of every
+    product, and weight gradients summed over the whole batch."""
+    from paper_2106_12089_amd.session import Session
+    cfg = workloads.get_config("stress")
+    wl = workload("stress")
+    p_nr, p_rh, compact = mode_rates(cfg, "nrrh", 0.5)
+    say("[gpu] stress full batch nrrh p=0.5")
+    sess = Session(wl, p_nr, p_rh, compact)
+    sess.masks(cfg.mask_seed, 0)
+    sess.forward()
+    sess.loss_grad()
+    sess.backward()
+    torch.cuda.synchronize()
+    gpu = sess.outputs()
+    m_nr, m_rh = oracle_masks(cfg, p_nr, p_rh)
+    ref = oracle_step(wl, p_nr, p_rh, m_nr, m_rh)
+    errs = compare(gpu, ref)
+    errs["loss"] = abs(gpu["loss"] - ref["loss"]) / abs(ref["loss"])
+    say("   errs", summary(errs))
+    bad = {k: v for k, v in errs.items() if not v <= TOL[cfg.dtype]}
+    assert not bad, bad
+
+
+@pytest.mark.parametrize("mode", ["nr", "nrrh", "nrrh_dense"])
+@pytest.mark.parametrize("name", ["lm_medium", "tagger"])
+def test_full_size_f32(name, mode):
+    """The fp32 path at full workload sizes (wide K, every tile layout and
+    XCD slicing of the bf16 runs) held to the fp32 bound of 1e-4."""
+    from paper_2106_12089_amd.session import Session
+    cfg = dataclasses.replace(workloads.get_config(name), dtype="f32")
+    wl = workloads.make_workload(cfg)
+    p_nr, p_rh, compact = mode_rates(cfg, mode, 0.5)
+    say(f"[gpu] f32 full size {name} {mode}")
+    sess = Session(wl, p_nr, p_rh, compact)
+    sess.masks(cfg.mask_seed, 0)
+    sess.forward()
+    sess.loss_grad()
+    sess.backward()
+    torch.cuda.synchronize()
+    gpu = sess.outputs()
+    m_nr, m_rh = oracle_masks(cfg, p_nr, p_rh)
+    ref = oracle_step(wl, p_nr, p_rh, m_nr, m_rh)
+    errs = compare(gpu, ref)
+    errs["loss"] = abs(gpu["loss"] - ref["loss"]) / abs(ref["loss"])
+    say("   errs", summary(errs))
+    bad = {k: v for k, v in errs.items() if not v <= TOL["f32"]}
+    assert not bad, bad

@@ -106,3 +106,22 @@ def test_case4_fixed_masks():
     assert abs(1.0 - f[0].mean() - p) < 5 * np.sqrt(p * (1 - p) / K)
     nr, rh = M.all_masks(5, 2, 2, 2, T, lambda l: 16 if l == 0 else 24, 12, p, p, fixed=True)
     assert all(np.array_equal(m, np.repeat(m[:1], T, axis=0)) for m in nr + [r for x in rh for r in x])
+
+
+def test_per_layer_rates():
+    """A rate per layer (the AWD-LSTM dropout vector): each site draws from
+    its own stream with its own layer's threshold; the brute-force drop
+    decision word < floor(p * 2^64) holds site by site, and each site's drop
+    fraction sits within 5 sigma of its own rate."""
+    T, H, I, L = 300, 400, 300, 3
+    p_nr, p_rh = [0.4, 0.25, 0.1], [0.5, 0.0, 0.7]
+    k_in = lambda l: I if l == 0 else H
+    nr, rh = masks.all_masks(99, 4, L, 1, T, k_in, H, p_nr, p_rh)
+    for l in range(L):
+        for m, stream, p in ((nr[l], masks.nr_stream(l), p_nr[l]), (rh[l][0], masks.rh_stream(l, 0), p_rh[l])):
+            u = masks.uniform_words(99, 4, stream, T, m.shape[1])
+            thr = (int(p * 2 ** 53) << 11) if p in (0.5, 0.25) else masks.drop_threshold(p)
+            assert np.array_equal(m == 0, u < np.uint64(thr)) if thr else m.all()
+            n = m.size
+            drop = n - int(m.sum())
+            assert abs(drop - n * p) <= 5 * np.sqrt(n * p * (1 - p)) + 1e-9

@@ -81,8 +81,9 @@ def _masked_cells(P, x, h0, c0, m_nr, m_rh, p_nr, p_rh, lengths):
     output and everything that needs a gradient."""
     L, D, H = P.num_layers, P.num_dirs, P.hidden
     T, B, I = x.shape
-    s_nr = 1.0 / (1.0 - p_nr) if p_nr > 0 else 1.0
-    s_rh = 1.0 / (1.0 - p_rh) if p_rh > 0 else 1.0
+    per_layer = lambda p: list(p) if isinstance(p, (list, tuple)) else [p] * L
+    s_nr = [1.0 / (1.0 - p) if p > 0 else 1.0 for p in per_layer(p_nr)]
+    s_rh = [1.0 / (1.0 - p) if p > 0 else 1.0 for p in per_layer(p_rh)]
     xt = torch.tensor(x, requires_grad=True)
     h0t = torch.tensor(h0, requires_grad=True)
     c0t = torch.tensor(c0, requires_grad=True)
@@ -93,7 +94,7 @@ def _masked_cells(P, x, h0, c0, m_nr, m_rh, p_nr, p_rh, lengths):
     hT, cT = [], []
     for l in range(L):
         mn = torch.tensor(m_nr[l], dtype=torch.float64)
-        xin = inp * mn[:, None, :] * s_nr
+        xin = inp * mn[:, None, :] * s_nr[l]
         outs = []
         for d in range(D):
             k = l * D + d
@@ -109,7 +110,7 @@ def _masked_cells(P, x, h0, c0, m_nr, m_rh, p_nr, p_rh, lengths):
             ys = [None] * T
             order = range(T) if d == 0 else range(T - 1, -1, -1)
             for t in order:
-                hn, cn = cell(xin[t], (h * mr[t][None, :] * s_rh, c))
+                hn, cn = cell(xin[t], (h * mr[t][None, :] * s_rh[l], c))
                 v = valid[t][:, None]
                 ys[t] = torch.where(v, hn, torch.zeros_like(hn))
                 h = torch.where(v, hn, h)
@@ -122,7 +123,10 @@ def _masked_cells(P, x, h0, c0, m_nr, m_rh, p_nr, p_rh, lengths):
 
 
 @pytest.mark.parametrize("L,D,p_nr,p_rh", [(2, 1, 0.5, 0.0), (2, 1, 0.5, 0.5), (1, 2, 0.3, 0.7),
-                                           (2, 2, 0.65, 0.65), (3, 1, 0.7, 0.3)])
+                                           (2, 2, 0.65, 0.65), (3, 1, 0.7, 0.3),
+                                           # a rate per layer (the AWD-LSTM dropout vector of Sec. 4.1)
+                                           (3, 1, [0.4, 0.25, 0.25], [0.5, 0.5, 0.5]),
+                                           (2, 2, [0.3, 0.6], [0.0, 0.45])])
 @pytest.mark.parametrize("with_lengths", [False, True])
 def test_masked_equals_torch_cells(L, D, p_nr, p_rh, with_lengths):
     T, B, I, H = 6, 4, 7, 5

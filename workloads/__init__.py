@@ -44,6 +44,12 @@ class Config:
     weight_init: str = "normal"   # "normal" (N(0, weight_scale)) or "uniform" (U(+-weight_scale))
     weight_scale: float = 0.1
     min_len: Optional[int] = None  # if set, lengths ~ U{min_len..seq_len}
+    input_init: str = "normal"     # embedding table: "normal" N(0, input_std) or "uniform" U(+-input_std)
+    # a rate per layer (the dropout vector of a model with one rate per
+    # site): NR of layer l's input, RH of layer l; None = p for every layer
+    p_nr_layers: Optional[tuple] = None
+    p_rh_layers: Optional[tuple] = None
+    p_out: Optional[float] = None  # rate of the output (pre-FC) site, if the model fixes one
 
     @property
     def mask_seed(self) -> int:
@@ -67,6 +73,15 @@ def _cfgs():
                "normal", 1.0, 0, "uniform", 1.0 / np.sqrt(256)),
         Config("stress", 2, 1, 1024, 1024, 256, 64, (0.3, 0.5, 0.7), "bf16", "mse", 6,
                "normal", 1.0, 0, "uniform", 1.0 / np.sqrt(1024)),
+        # AWD-LSTM shape (Sec. 4.1): 3 layers, embedding 400, every hidden
+        # layer 1150, LSTM weights U(+-1/sqrt(H)), embeddings U(+-0.1); input
+        # dropout 0.4 on layer 0, 0.25 between layers, 0.4 before the FC
+        # layer, and 0.5 on the recurrent weights, which structured becomes
+        # RH dropout on h_{t-1}.  Batch 20 and 70 steps per sequence are the
+        # usual PTB settings of that model (the paper does not restate them).
+        Config("awd_lstm", 3, 1, 400, 1150, 20, 70, (0.4,), "bf16", "mse", 7,
+               "embedding", 0.1, 10000, "uniform", 1.0 / np.sqrt(1150), input_init="uniform",
+               p_nr_layers=(0.4, 0.25, 0.25), p_rh_layers=(0.5, 0.5, 0.5), p_out=0.4),
     ]
     return {c.name: c for c in cs}
 
@@ -143,7 +158,10 @@ def make_workload(cfg: Config, batch: Optional[int] = None) -> Workload:
     # layer input
     ids = None
     if cfg.input_kind == "embedding":
-        table = rng.normal(0.0, cfg.input_std, size=(cfg.vocab, I)).astype(np.float32)
+        if cfg.input_init == "uniform":
+            table = rng.uniform(-cfg.input_std, cfg.input_std, size=(cfg.vocab, I)).astype(np.float32)
+        else:
+            table = rng.normal(0.0, cfg.input_std, size=(cfg.vocab, I)).astype(np.float32)
         ids = _zipf_ids(rng, cfg.vocab, (T, B))
         x = table[ids]
     else:
