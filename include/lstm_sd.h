@@ -201,6 +201,28 @@ int lstm_sd_backward(const lstm_sd_dims* dims, const lstm_sd_weights* w,
                      float* dx, float* dh0, float* dc0, const lstm_sd_grads* g,
                      void* workspace, size_t workspace_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * forward pass of lstm_sd_forward with the same arguments except the
+ * workspace, which the library holds itself in a file-scope device array of
+ * LSTM_SD_STATIC_WORKSPACE_MAX bytes (each GPU the library runs on holds one
+ * until the process ends).  The call allocates nothing; the caller still
+ * owns the mask, reserve and output buffers, and `reserve` feeds
+ * lstm_sd_backward (with a workspace of the caller's) as after
+ * lstm_sd_forward.  Dims whose lstm_sd_workspace_bytes exceeds the maximum
+ * are rejected with LSTM_SD_EUNSUPPORTED before any device work.  Every call
+ * on one GPU uses the same array, and the pass clears what it needs cleared
+ * in its first kernel: calls that overlap on one GPU (other streams, other
+ * threads) race, so order them on one stream.  A barrier time-out is visible
+ * as NaN in hT, cT and y (there is no workspace to pass to lstm_sd_status). */
+#define LSTM_SD_STATIC_WORKSPACE_MAX ((size_t)64 << 20)
+int lstm_sd_forward_static(const lstm_sd_dims* dims, const lstm_sd_weights* w,
+                           const void* x, const int32_t* lengths,
+                           const void* h0, const float* c0,
+                           const void* mask_buf, size_t mask_bytes,
+                           float* y, float* hT, float* cT,
+                           void* reserve, size_t reserve_bytes, void* stream);
+
 /* Mean-squared-error loss of y against target over valid (t, b) and all
  * D*H features, and its gradient: loss = sum (y-target)^2 / N,
  * dy = 2 (y - target) / N at valid positions and 0 elsewhere, with N =

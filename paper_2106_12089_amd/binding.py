@@ -89,6 +89,8 @@ SIGNATURES = {
     "lstm_sd_head_mask_generate": (ctypes.c_int, [_HD, ctypes.c_uint64, ctypes.c_uint64, _P, _SZ, _P]),
     "lstm_sd_head_forward": (ctypes.c_int, [_HD, _P, _P, _P, _P, _SZ, _P, _P, _SZ, _P]),
     "lstm_sd_head_backward": (ctypes.c_int, [_HD, _P, _P, _P, _P, _SZ, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "lstm_sd_forward_static": (ctypes.c_int, [_DIMS, ctypes.POINTER(lstm_sd_weights), _P, _P, _P, _P, _P, _SZ,
+                                              _P, _P, _P, _P, _SZ, _P]),
     "lstm_sd_status": (ctypes.c_int, [_DIMS, _P, _SZ, _P]),
     "lstm_sd_set_barrier_timeout": (ctypes.c_int, [ctypes.c_double]),
     "lstm_sd_kernel_timer_start": (ctypes.c_int, [ctypes.c_char_p]),
@@ -316,6 +318,18 @@ def lstm_sd_head_backward(hd, W_fc, targets, lengths, mask_buf, logits, loss, dy
                                         _ptr(mask_buf), _nbytes(mask_buf), _ptr(logits), _ptr(loss), _ptr(dy),
                                         _ptr(dW_fc), _ptr(db_fc), _ptr(workspace), _nbytes(workspace),
                                         _stream(stream)))
+
+
+STATIC_WORKSPACE_MAX = 64 << 20
+
+
+def lstm_sd_forward_static(dims, W, U, b, x, lengths, h0, c0, mask_buf, y, hT, cT, reserve, stream=None):
+    """lstm_sd_forward with the library's own workspace (allocates nothing)."""
+    keep = (_ptr_array(W), _ptr_array(U), _ptr_array(b))
+    w = lstm_sd_weights(keep[0], keep[1], keep[2])
+    _check(load().lstm_sd_forward_static(ctypes.byref(dims), ctypes.byref(w), _ptr(x), _ptr(lengths), _ptr(h0),
+                                         _ptr(c0), _ptr(mask_buf), _nbytes(mask_buf), _ptr(y), _ptr(hT), _ptr(cT),
+                                         _ptr(reserve), _nbytes(reserve), _stream(stream)))
 
 
 def lstm_sd_status(dims, workspace, stream=None):

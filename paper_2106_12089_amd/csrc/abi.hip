@@ -8,6 +8,7 @@
 #include <string.h>
 
 #include <atomic>
+#include <mutex>
 #include <string>
 
 #include "../../include/lstm_sd.h"
@@ -1056,6 +1057,59 @@ int lstm_sd_case1_dropout_backward(int32_t seq_len, int32_t batch, int32_t featu
     if (!dx || !mask || !dsrc) return fail(LSTM_SD_EINVAL, "a required pointer is NULL");
     launch_case1_undrop(dx, mask, dsrc, (long)seq_len * batch * features, inv_keep(p), (hipStream_t)stream);
     return hip_check("case-I dropout backward launch");
+}
+
+// ---------------------------------------------------------------------------
+// The forward pass with the library's own workspace, for callers that cannot
+// allocate.  `scratch` is a file-scope device array: each GPU the library
+// runs on holds its own copy until the process ends.  In host code its name
+// is not a device address; the address of the current device's copy comes
+// from hipGetSymbolAddress, taken once per device on the first call there,
+// and only that pointer reaches kernels.
+static __device__ __align__(256) char scratch[LSTM_SD_STATIC_WORKSPACE_MAX];
+
+static int scratch_ptr(void** out) {
+    constexpr int MAXDEV = 64;
+    static std::mutex mu;
+    static void* ptr[MAXDEV] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(LSTM_SD_EHIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+    if (dev < 0 || dev >= MAXDEV) return fail(LSTM_SD_EUNSUPPORTED, "device index beyond the static workspace table");
+    std::lock_guard<std::mutex> lock(mu);
+    if (!ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return fail(LSTM_SD_EHIP, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+        ptr[dev] = p;
+    }
+    *out = ptr[dev];
+    return LSTM_SD_OK;
+}
+
+int lstm_sd_forward_static(const lstm_sd_dims* dims, const lstm_sd_weights* w, const void* x, const int32_t* lengths,
+                           const void* h0, const float* c0, const void* mask_buf, size_t mask_bytes, float* y,
+                           float* hT, float* cT, void* reserve, size_t reserve_bytes, void* stream) {
+    Plan P; const char* why = nullptr;
+    int rc = make_plan(dims, &P, &why);
+    if (rc) return fail(rc, why);
+    if (P.w_total > LSTM_SD_STATIC_WORKSPACE_MAX)
+        return fail(LSTM_SD_EUNSUPPORTED, "lstm_sd_workspace_bytes(dims) exceeds LSTM_SD_STATIC_WORKSPACE_MAX");
+    if (!w || !w->W || !w->U || !w->b) return fail(LSTM_SD_EINVAL, "weights is NULL");
+    for (int k = 0; k < P.L * P.D; ++k)
+        if (!w->W[k] || !w->U[k] || !w->b[k]) return fail(LSTM_SD_EINVAL, "a weight pointer is NULL");
+    if (!x || !h0 || !c0 || !mask_buf || !y || !hT || !cT || !reserve)
+        return fail(LSTM_SD_EINVAL, "a required pointer is NULL");
+    if (mask_bytes < P.m_total) return fail(LSTM_SD_EWORKSPACE, "mask_bytes smaller than lstm_sd_mask_bytes()");
+    if (reserve_bytes < P.r_total) return fail(LSTM_SD_EWORKSPACE, "reserve_bytes smaller than lstm_sd_reserve_bytes()");
+    void* ws = nullptr;
+    if ((rc = scratch_ptr(&ws))) return rc;
+    if (setup_kernel_attributes()) return fail(LSTM_SD_EHIP, "hipFuncSetAttribute failed");
+    hipStream_t st = (hipStream_t)stream;
+    if (P.dtype == LSTM_SD_DTYPE_BF16)
+        return forward_impl<bf16>(P, w, x, lengths, h0, c0, mask_buf, y, hT, cT, reserve, ws, st);
+    return forward_impl<float>(P, w, x, lengths, h0, c0, mask_buf, y, hT, cT, reserve, ws, st);
 }
 
 int lstm_sd_status(const lstm_sd_dims* dims, const void* workspace, size_t workspace_bytes, void* stream) {
