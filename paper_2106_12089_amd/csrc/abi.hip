@@ -8,6 +8,7 @@
 #include <string.h>
 
 #include <atomic>
+#include <type_traits>
 #include <mutex>
 #include <string>
 
@@ -47,6 +48,8 @@ constexpr int KID_FWDP_ = 7;
 constexpr int KID_BWDP_ = 8;
 template <typename T>
 hipError_t launch_bwd_persist(PBwdArgs& a, hipStream_t st, int timer_on, hipEvent_t e0, hipEvent_t e1);
+hipError_t launch_fwd_big(PFwdArgs& a, hipStream_t st, int timer_on, hipEvent_t e0, hipEvent_t e1);
+hipError_t launch_bwd_big(PBwdArgs& a, hipStream_t st, int timer_on, hipEvent_t e0, hipEvent_t e1);
 int kernel_timer_start(const char* name);
 int kernel_timer_stop(double* total_ms, int64_t* launches);
 
@@ -150,6 +153,7 @@ int make_plan(const lstm_sd_dims* d, Plan* p, const char** why) {
     q.w_dc = off;     off = align_up(off + D * B * H * 4, A);
     q.w_dhc = off;    off = align_up(off + D * B * H * 4, A);
     q.w_dxc = off;    off = align_up(off + 2 * T * B * (size_t)q.kin_max * 4, A);
+    q.w_part = off;   off = align_up(off + (size_t)((4 * q.H + 511) / 512) * B * H * 4, A);
     const size_t bwd = off;
     q.w_sync = align_up(fwd > bwd ? fwd : bwd, A);
     q.w_loss = q.w_sync + align_up(SYNC_BYTES, A);   // barrier counters and error flag
@@ -170,6 +174,16 @@ static bool use_fwd_workers() {
     const char* v = getenv("LSTM_SD_FWD_WORKERS");
     return !(v && v[0] == '0');
 }
+
+// The large-batch persistent kernels (bf16) run where the row-group tiling
+// does not fit.  LSTM_SD_BIG=0: never (per-step kernels there instead);
+// LSTM_SD_BIG=2: wherever they apply, one launch per layer (tests of their
+// tiling on ragged shapes).
+static int big_mode() {
+    const char* v = getenv("LSTM_SD_BIG");
+    return (v && v[0] == '0') ? 0 : (v && v[0] == '2') ? 2 : 1;
+}
+static bool use_big() { return big_mode() != 0; }
 
 static bool use_persistent() {
     const char* v = getenv("LSTM_SD_PERSIST");
@@ -379,7 +393,8 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
         if (timed) timer_unpair();
         return false;
     };
-    if (use_persistent() && use_stacked() && D == 1 && L > 1 && L <= 4) {
+    const bool big_first = std::is_same<E, bf16>::value && big_mode() == 2;
+    if (use_persistent() && use_stacked() && !big_first && D == 1 && L > 1 && L <= 4) {
         launch_fx_layer(0);
         if ((use_fwd_workers() && stacked(true)) || stacked(false)) return hip_check("forward launch");
         // neither fits: one layer at a time below (layer 0's input product is done)
@@ -409,8 +424,13 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
             }
             hipEvent_t e0 = nullptr, e1 = nullptr;
             const bool timed = timer_pair(KID_FWDP_, &e0, &e1);
+            if (big_first && launch_fwd_big(pa, st, timed, e0, e1) == hipSuccess) continue;
+            (void)hipGetLastError();
             if (launch_fwd_persist<E>(pa, st, timed, e0, e1) == hipSuccess) continue;
-            (void)hipGetLastError();          // does not fit: per-step kernels below
+            (void)hipGetLastError();          // does not fit: the large-batch kernel (bf16), else per step
+            if (std::is_same<E, bf16>::value && use_big() && launch_fwd_big(pa, st, timed, e0, e1) == hipSuccess)
+                continue;
+            (void)hipGetLastError();
             if (timed) timer_unpair();
         }
         for (int s = 0; s < T; ++s) {
@@ -563,7 +583,8 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
 
     // Unidirectional stack: every layer's BPTT in one persistent launch, with
     // a worker between layers l+1 and l forming dx of layer l+1 per step.
-    if (use_persistent() && use_stacked() && D == 1 && L > 1 && 2 * L - 1 <= 8) {
+    const bool big_first = std::is_same<E, bf16>::value && big_mode() == 2;
+    if (use_persistent() && use_stacked() && !big_first && D == 1 && L > 1 && 2 * L - 1 <= 8) {
         launch_bwd_init(nullptr, nullptr, nullptr, nullptr, 0, W + P.w_da, (int)es, G, P.mtiles, (long)L * T,
                         (long)P.das, sync_bar, sync_err, st);
         PBwdArgs pa;
@@ -611,7 +632,33 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
         float* dxc_above = (float*)(W + P.w_dxc) + (size_t)((l + 1) & 1) * T * B * P.kin_max;
         float* dxc_here = (float*)(W + P.w_dxc) + (size_t)(l & 1) * T * B * P.kin_max;
         bool persistent_done = false;
-        if (use_persistent()) {
+        // the large-batch kernel, one launch per direction
+        auto big = [&]() -> bool {
+            if (!std::is_same<E, bf16>::value || !use_big()) return false;
+            for (int d = 0; d < D; ++d) {
+                PBwdArgs pa;
+                common_args(pa);
+                pa.nslots = 1;
+                pa.lddx = l + 1 < L ? P.kin(l + 1) : 0;
+                pa.part = (float*)(W + P.w_part);
+                PBwdDir& pd = pa.d[0];
+                fill_layer(pd, l, d, d);
+                if (l < L - 1) {
+                    pd.dxc = dxc_above;
+                    pd.dxpos = site_view(P, mbuf, P.site_nr(l + 1)).pos + d * H;
+                }
+                hipEvent_t e0 = nullptr, e1 = nullptr;
+                const bool timed = timer_pair(KID_BWDP_, &e0, &e1);
+                if (launch_bwd_big(pa, st, timed, e0, e1) != hipSuccess) {
+                    (void)hipGetLastError();
+                    if (timed) timer_unpair();
+                    return false;             // (the first direction: nothing was launched)
+                }
+            }
+            return true;
+        };
+        if (use_persistent() && big_first) persistent_done = big();
+        if (use_persistent() && !persistent_done) {
             PBwdArgs pa;
             common_args(pa);
             pa.nslots = D;
@@ -629,8 +676,9 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
             if (launch_bwd_persist<E>(pa, st, timed, e0, e1) == hipSuccess) {
                 persistent_done = true;
             } else {
-                (void)hipGetLastError();      // does not fit: per-step kernels below
+                (void)hipGetLastError();      // does not fit: the large-batch kernel, else per step
                 if (timed) timer_unpair();
+                persistent_done = big();
             }
         }
         // T pointwise steps plus one final pass (recurrent gradient of h0)

@@ -286,6 +286,8 @@ struct PBwdArgs {
     int* err;
     long long timeout;                  // wall-clock ticks (<= 0: every wait fails at once)
     int B, H, T, BP, ldy, lddx, kmax, dense, ntiles, mgroups, mtiles, nslots;
+    float* part;                        // large-batch kernel: [ngk][B][H] partial recurrent gradients
+    int ngu, ngk;                       // large-batch kernel: unit groups and gate-column groups
 };
 
 }  // namespace lsd

@@ -16,211 +16,10 @@
 
 #include "device.h"
 #include "kernels.h"
+#include "sync.h"
 #include "../../include/lstm_sd.h"
 
 namespace lsd {
-
-// ---------------------------------------------------------------------------
-// Cross-workgroup exchange and grid barrier.
-//
-// Values that other workgroups read during the same launch (the compacted
-// h_t, x_t and gx_t of the forward stack, the backward DA_t and dx_t) are
-// written with relaxed agent-scope atomic stores (ordinary stores carrying
-// the device-coherence bit, written through to the coherent level), so a
-// producer never writes back its L2, and read with device-coherent loads
-// (16-byte buffer loads with the SC1 bit, the form of an agent-scope atomic
-// load), so a consumer needs no cache invalidation.  A workgroup signals the
-// end of a step by waiting for its own stores to complete, synchronising its
-// threads and adding 1 to its slot's counter; a waiting workgroup spins (one
-// wave) until the counter shows the step complete.  The spin is bounded by
-// wall-clock time; on time-out, or when another workgroup has timed out, it
-// reports failure and the kernel ends (outputs are then poisoned with NaN).
-// A slot's counter is split over BAR_LINES cache lines (workgroup j adds to
-// line j % BAR_LINES, lanes of the waiting wave poll one line each): the
-// atomic adds of one line are serialised, and with one line per slot a step
-// of 82 workgroups spent about 0.5 us more in the barrier.  Waits are on
-// step counts: line k of slot d reaches s * (the number of the slot's
-// workgroups on line k) once step s is complete.
-
-// workgroups of slot `slot` (blocks [slot*nslot, (slot+1)*nslot)) that add
-// to line i
-__device__ __forceinline__ unsigned bar_count(int nslot, int slot, int i) {
-    auto upto = [&](int n) { return n > i ? (n - i + BAR_LINES - 1) / BAR_LINES : 0; };
-    return (unsigned)(upto((slot + 1) * nslot) - upto(slot * nslot));
-}
-__device__ __forceinline__ unsigned* slot_bar(unsigned* bar, int slot) { return bar + BAR_PITCH * BAR_LINES * slot; }
-// the sticky status word of the step, beside the error flag
-__device__ __forceinline__ int* sync_status(int* err) { return (int*)((char*)err + (SYNC_STATUS_OFS - SYNC_ERR_OFS)); }
-
-__device__ __forceinline__ void grid_arrive(unsigned* sbar) {
-    __builtin_amdgcn_s_waitcnt(0);      // this thread's stores have completed
-    __syncthreads();
-    if (threadIdx.x == 0)
-        __hip_atomic_fetch_add(sbar + BAR_PITCH * (blockIdx.x % BAR_LINES), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// Wait until slot `slot` (counter lines at sbar) has completed `steps`
-// steps, and, with sbar2, slot `slot2` has completed `steps2` (lanes 0-15
-// poll the first slot's lines, lanes 16-31 the second's, in the same loop:
-// no extra round trip).  Returns false on time-out or when another workgroup
-// has timed out (err set).  With seen / seen2 (LDS), also records the number
-// of steps the lines read last show as complete.
-__device__ __forceinline__ bool grid_wait(unsigned* sbar, int slot, int nslot, unsigned steps, int* err,
-                                          long long timeout, int fail_bit, unsigned* seen = nullptr,
-                                          unsigned* sbar2 = nullptr, int slot2 = 0, unsigned steps2 = 0,
-                                          unsigned* seen2 = nullptr) {
-    __shared__ int ok;
-    if (timeout <= 0) {
-        // a zero time-out (set from the host, for tests of the failure
-        // path): every wait fails at once, so every workgroup leaves through
-        // the time-out path without spinning.  The flags are set before the
-        // workgroup barrier, so every thread reads them set afterwards.
-        if (threadIdx.x == 0) {
-            __hip_atomic_fetch_or(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_fetch_or(sync_status(err), fail_bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __builtin_amdgcn_s_waitcnt(0);      // both have completed
-        }
-        __syncthreads();
-        return false;
-    }
-    if (threadIdx.x < 64) {
-        const int i = threadIdx.x;
-        const bool second = i >= BAR_LINES;
-        const int li = i & (BAR_LINES - 1);
-        const unsigned n = i < BAR_LINES ? bar_count(nslot, slot, li)
-                         : (i < 2 * BAR_LINES && sbar2) ? bar_count(nslot, slot2, li) : 0u;
-        const unsigned* line = (second && sbar2 ? sbar2 : sbar) + BAR_PITCH * li;
-        const unsigned want = (second ? steps2 : steps) * n;
-        int good = 1;
-        const long long t0 = wall_clock64();
-        unsigned v = 0;
-        // (the error flag is read only once a wait has taken a while: a load
-        // of it in every poll made the barrier 0.2 us slower)
-        for (;;) {
-            v = n ? __hip_atomic_load(line, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
-            if (__builtin_amdgcn_ballot_w64(n != 0 && v < want) == 0) break;
-            const long long el = wall_clock64() - t0;
-            if (el > timeout) {
-                if (i == 0) {
-                    __hip_atomic_fetch_or(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    __hip_atomic_fetch_or(sync_status(err), fail_bit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    __builtin_amdgcn_s_waitcnt(0);
-                }
-                good = 0;
-                break;
-            }
-            if (el > (timeout >> 12)) {
-                const int e = i == 0 ? __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0;
-                if (__builtin_amdgcn_ballot_w64(e != 0) != 0) { good = 0; break; }
-            }
-        }
-        if (seen || seen2) {
-            // steps complete per lane; the minimum over each half of the wave
-            unsigned c = n ? v / n : 0xffffffffu;
-#pragma unroll
-            for (int o = 8; o; o >>= 1) c = min(c, (unsigned)__shfl_xor((int)c, o));
-            if (seen && i == 0) *seen = c;
-            if (seen2 && i == BAR_LINES) *seen2 = c;
-        }
-        if (i == 0) ok = good;
-    }
-    // every read of what other workgroups of this launch published is a
-    // device-coherent load (SC1), issued after this point: no cache needs
-    // invalidating (an agent-scope acquire would invalidate the XCD's L2 from
-    // every workgroup, which cost up to 0.9 us per barrier at 123 workgroups)
-    __syncthreads();
-    return ok != 0;
-}
-
-// Every workgroup ends here, past its last barrier wait; the last one to
-// arrive returns the step counters, the error flag and the exit counter to
-// zero, so the next launch starts clear without a clearing kernel.  (The
-// outputs' time-out check comes before: the flag is read by then.  A
-// time-out stays recorded in the sticky status word, which this does not
-// clear.)
-__device__ __forceinline__ void grid_exit(unsigned* bar, int nslots, int* err) {
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        unsigned* ex = slot_bar(bar, BAR_EXIT);
-        const unsigned tk = __hip_atomic_fetch_add(ex, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-        if (tk == gridDim.x - 1) {
-            for (int i = 0; i < nslots * BAR_LINES; ++i)
-                __hip_atomic_store(bar + BAR_PITCH * i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_store(err, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_store(ex, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-    }
-}
-
-// coherent (agent-scope) element store and 8-element load of exchange data
-__device__ __forceinline__ void xstore(bf16* p, bf16 v) {
-    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void xstore(float* p, float v) {
-    __hip_atomic_store((uint32_t*)p, __float_as_uint(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void xload8(const bf16* p, bf16* o) {
-    const unsigned long long* q = (const unsigned long long*)p;
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-        const unsigned long long v = __hip_atomic_load(q + h, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) o[4 * h + e] = (bf16)((v >> (16 * e)) & 0xffffu);
-    }
-}
-__device__ __forceinline__ void xload8(const float* p, float* o) {
-    const unsigned long long* q = (const unsigned long long*)p;
-#pragma unroll
-    for (int h = 0; h < 4; ++h) {
-        const unsigned long long v = __hip_atomic_load(q + h, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        o[2 * h] = __uint_as_float((uint32_t)v);
-        o[2 * h + 1] = __uint_as_float((uint32_t)(v >> 32));
-    }
-}
-
-// coherent load of one float
-__device__ __forceinline__ float xload1(const float* p) {
-    return __uint_as_float(__hip_atomic_load((const uint32_t*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-}
-
-// coherent load of 4 consecutive elements (8-byte aligned bf16 / 16-byte f32)
-__device__ __forceinline__ void xload4(const bf16* p, bf16* o) {
-    const unsigned long long v = __hip_atomic_load((const unsigned long long*)p, __ATOMIC_RELAXED,
-                                                   __HIP_MEMORY_SCOPE_AGENT);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) o[e] = (bf16)((v >> (16 * e)) & 0xffffu);
-}
-__device__ __forceinline__ void xload4(const float* p, float* o) {
-    const unsigned long long* q = (const unsigned long long*)p;
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-        const unsigned long long v = __hip_atomic_load(q + h, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        o[2 * h] = __uint_as_float((uint32_t)v);
-        o[2 * h + 1] = __uint_as_float((uint32_t)(v >> 32));
-    }
-}
-// 4 consecutive elements, plain load (8-byte aligned bf16 / 16-byte f32)
-__device__ __forceinline__ void ld4g(const bf16* p, bf16* o) {
-    const uint2 v = *(const uint2*)p;
-    o[0] = (bf16)(v.x & 0xffffu); o[1] = (bf16)(v.x >> 16);
-    o[2] = (bf16)(v.y & 0xffffu); o[3] = (bf16)(v.y >> 16);
-}
-__device__ __forceinline__ void ld4g(const float* p, float* o) {
-    const float4 v = *(const float4*)p;
-    o[0] = v.x; o[1] = v.y; o[2] = v.z; o[3] = v.w;
-}
-// 8 consecutive elements (LDS or global, 16-byte aligned)
-__device__ __forceinline__ void lds8(const bf16* p, bf16* o) {
-    const uint4 v = *(const uint4*)p;
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-    for (int e = 0; e < 8; ++e) o[e] = (bf16)((w[e >> 1] >> (16 * (e & 1))) & 0xffffu);
-}
-__device__ __forceinline__ void lds8(const float* p, float* o) {
-    const float4 v0 = *(const float4*)p, v1 = *(const float4*)(p + 4);
-    o[0] = v0.x; o[1] = v0.y; o[2] = v0.z; o[3] = v0.w;
-    o[4] = v1.x; o[5] = v1.y; o[6] = v1.z; o[7] = v1.w;
-}
 
 // ---------------------------------------------------------------------------
 // Persistent forward recurrence (Eq. 1-6).  A launch runs every step of its
@@ -1003,6 +802,499 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Persistent forward recurrence for large batches (Eq. 1-6), one layer (its
+// directions as slots).  At a batch where the row-group tiling of
+// k_fwd_persist does not fit the device at once (each of its workgroups
+// holds a U slice in LDS for every 64 rows), this kernel holds the U slice
+// in registers instead and gives LDS to the reduction:
+//   workgroup = (slot, 16 hidden units = 64 gate columns, 64 batch rows),
+//   512 threads = 8 waves.  Wave w owns the recurrent neurons
+//   [32*KC*w, 32*KC*(w+1)) of the contraction: its B fragments (U rows of
+//   those neurons, the 64 columns of the tile: KC chunks x 4 column tiles)
+//   are loaded once and stay in registers for the whole sequence.  Per step
+//   each wave loads the A fragments of its neuron range for the 64 rows
+//   (every element of h_{t-1} the workgroup needs is loaded by exactly one
+//   wave), forms a 64 x 64 partial product, and the eight partials are
+//   summed through LDS by the threads of the gate pointwise (two
+//   (row, unit) pairs each).
+// h_{t-1} is exchanged uncompacted and multiplied by the step's RH mask at
+// the producer (a dropped neuron contributes an exact zero), so the same
+// kernel serves both modes; rows and neurons past the shape read as zero.
+constexpr int BG_NW = 8, BG_MG = 64, BG_UT = 16, BG_NC = 4 * BG_UT, BG_RP = BG_NC + 4;
+
+template <int KC>
+__global__ void __launch_bounds__(512) k_fwd_big(PFwdArgs a) {
+    constexpr int MT = BG_MG / 16, NTL = BG_NC / 16, NTH = 64 * BG_NW;
+    constexpr int PPT = BG_MG * BG_UT / NTH;   // (row, unit) pairs per thread
+    extern __shared__ __align__(16) char smem[];
+    float* red = (float*)smem;                 // [8 waves][64 rows][BG_RP]
+    const int H = a.H, G = 4 * H, B = a.B, T_ = a.T;
+    const int nslot = a.ntiles * a.mgroups;
+    const int d = blockIdx.x / nslot, rem = blockIdx.x % nslot;
+    const int tile = rem / a.mgroups, mg = rem % a.mgroups;
+    const PFwdDir& D = a.d[d];
+    const int u0 = tile * BG_UT, m0 = mg * BG_MG;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g8 = 8 * (lane >> 4);
+    unsigned* bar = slot_bar(a.bar, d);
+    const int nch = (H + 31) / 32;             // 32-neuron chunks of the contraction
+
+    // B fragments: U rows of this wave's neurons, the tile's 64 columns
+    // (column c of tile j is gate (c&15)>>2 of unit u0 + 4j + (c&3))
+    bf16x8_t ub[KC][NTL];
+    {
+        const bf16* U = (const bf16*)D.U;
+#pragma unroll
+        for (int j = 0; j < NTL; ++j) {
+            const int cl = lane & 15;
+            const int unit = u0 + 4 * j + (cl & 3);
+            const int gcol = (cl >> 2) * H + min(unit, H - 1);
+#pragma unroll
+            for (int c = 0; c < KC; ++c) {
+                const int kb = 32 * (w * KC + c) + g8;
+                s16x8_t f;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const int k = kb + e;
+                    const bf16 v = U[(size_t)min(k, H - 1) * G + gcol];
+                    f[e] = (short)((k < H && unit < H) ? v : (bf16)0);
+                }
+                ub[c][j] = __builtin_bit_cast(bf16x8_t, f);
+            }
+        }
+    }
+    // this thread's (row, unit) pairs, their state and per-step inputs
+    float creg[PPT], hreg[PPT], gxr[PPT][4];
+    int pb[PPT], pu[PPT], lenr[PPT], mnx[PPT];
+#pragma unroll
+    for (int q = 0; q < PPT; ++q) {
+        const int p = tid + NTH * q;
+        pb[q] = m0 + p / BG_UT;
+        pu[q] = u0 + p % BG_UT;
+        const bool ok = pb[q] < B && pu[q] < H;
+        creg[q] = ok ? D.c0[(size_t)pb[q] * H + pu[q]] : 0.f;
+        hreg[q] = ok ? bf2f(((const bf16*)D.h0)[(size_t)pb[q] * H + pu[q]]) : 0.f;
+        lenr[q] = a.lengths ? a.lengths[min(pb[q], B - 1)] : T_;
+    }
+    auto step_t = [&](int s) { return D.dir == 0 ? s : T_ - 1 - s; };
+    // inputs of step s (clamped, valid addresses): the input product and the
+    // RH mask of the step that consumes h_t
+    auto prefetch = [&](int s) {
+        const int sc = min(s, T_ - 1);
+        const int t = step_t(sc);
+        const int tn = step_t(min(sc + 1, T_ - 1));
+#pragma unroll
+        for (int q = 0; q < PPT; ++q) {
+            const int bc = min(pb[q], B - 1), uc = min(pu[q], H - 1);
+            const float* gp = D.gx + ((size_t)t * B + bc) * G + uc;
+#pragma unroll
+            for (int g = 0; g < 4; ++g) gxr[q][g] = gp[g * H];
+            mnx[q] = D.rh.mask[(size_t)tn * D.rh.kmax + uc];
+        }
+    };
+    const size_t hxs = (size_t)nch * a.mtiles * 512;       // elements per h slot
+    // this lane's A offset in chunk 0 of the wave and row tile 0 of the group
+    const uint32_t a_base = (uint32_t)(frag_lane_off(w * KC, m0 / 16, lane, a.mtiles) * sizeof(bf16));
+    // Rows past the batch inside its last 16-row tile are never written and
+    // only reach outputs of rows past the batch (not stored).  Neurons past H
+    // in the last chunk are never written either and meet zero U rows, so
+    // they are cleared here, in both slots, before the first barrier (a
+    // stale NaN times zero would not vanish): the last unit tile's
+    // workgroups clear them for their rows.
+    if (tile == a.ntiles - 1 && H % 32) {
+        const int npad = 32 * nch - H;
+        for (int i = tid; i < 2 * BG_MG * npad; i += NTH) {
+            const int sl = i / (BG_MG * npad), r = (i / npad) % BG_MG, k = H + i % npad;
+            if (m0 + r < 16 * a.mtiles)
+                xstore((bf16*)D.hx + (size_t)sl * hxs + frag_off(m0 + r, k, a.mtiles), (bf16)0);
+        }
+    }
+    // prologue: h0 times the first step's RH mask into slot 0
+    {
+        const int t0 = step_t(0);
+        bf16* hx0 = (bf16*)D.hx;
+#pragma unroll
+        for (int q = 0; q < PPT; ++q)
+            if (pb[q] < B && pu[q] < H)
+                xstore(hx0 + frag_off(pb[q], pu[q], a.mtiles),
+                       D.rh.mask[(size_t)t0 * D.rh.kmax + pu[q]] ? f2bf(hreg[q]) : (bf16)0);
+    }
+    prefetch(0);
+    grid_arrive(bar);
+
+    for (int s = 0; s < T_; ++s) {
+        const int t = step_t(s);
+        if (!grid_wait(bar, d, nslot, (unsigned)(s + 1), a.err, a.timeout, STATUS_FWD)) break;
+        // ---- h~_{t-1} (this wave's neurons, the tile's rows) times the U slice
+        // A fragments two chunks deep (registers): chunk c+2 is issued as
+        // soon as chunk c has been multiplied.  Offsets: one base register
+        // (copied inside the loop, so the compiler keeps one register rather
+        // than hoisting a register per fragment) plus the chunk; the row tile
+        // is the instruction's immediate (tiles are 1 KB apart).  Chunks past
+        // the last one and row tiles past the last one of the batch read
+        // past the slot (zero) or rows past the batch (whose outputs are not
+        // stored).
+        const __amdgpu_buffer_rsrc_t hr = buf_rsrc((const bf16*)D.hx + (size_t)(s & 1) * hxs,
+                                                   (uint32_t)(hxs * sizeof(bf16)));
+        uint32_t vb;
+        asm volatile("v_mov_b32 %0, %1" : "=v"(vb) : "v"(a_base));
+        auto issue = [&](int c, u32x4_t (&f)[MT]) {
+            const uint32_t vo = vb + (uint32_t)(c * a.mtiles * 1024);
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) f[mt] = __builtin_amdgcn_raw_buffer_load_b128(hr, vo + mt * 1024, 0, CPOL_SC1);
+        };
+        u32x4_t fa[2][MT];
+        issue(0, fa[0]);
+        if (KC > 1) issue(1, fa[1]);
+        f32x4_t acc[MT][NTL];
+#pragma unroll
+        for (int i = 0; i < MT; ++i)
+#pragma unroll
+            for (int j = 0; j < NTL; ++j) acc[i][j] = f32x4_t{0, 0, 0, 0};
+#pragma unroll
+        for (int c = 0; c < KC; ++c) {
+            u32x4_t (&f)[MT] = fa[c & 1];
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+                const bf16x8_t av = __builtin_bit_cast(bf16x8_t, f[mt]);
+#pragma unroll
+                for (int j = 0; j < NTL; ++j)
+                    acc[mt][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, ub[c][j], acc[mt][j], 0, 0, 0);
+            }
+            if (c + 2 < KC) issue(c + 2, f);
+        }
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int j = 0; j < NTL; ++j)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    red[(w * BG_MG + mt * 16 + acc_row(lane, r)) * BG_RP + j * 16 + (lane & 15)] = acc[mt][j][r];
+        __syncthreads();
+        // ---- pointwise (Eq. 1-6); h_t goes out first, masked for the next step
+        bf16* hxn = (bf16*)D.hx + (size_t)((s + 1) & 1) * hxs;
+        float og4[PPT][4], cnv[PPT], hnv[PPT];
+#pragma unroll
+        for (int q = 0; q < PPT; ++q) {
+            const int p = tid + NTH * q;
+            const int rr = p / BG_UT, uu = p % BG_UT;
+            const int cb = (uu >> 2) * 16 + (uu & 3);
+            float pre[4];
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                float v = 0.f;
+#pragma unroll
+                for (int i = 0; i < BG_NW; ++i) v += red[(i * BG_MG + rr) * BG_RP + cb + 4 * g];
+                pre[g] = D.s_rh * v + gxr[q][g];
+            }
+            og4[q][0] = sigmoid_fast(pre[0]);
+            og4[q][1] = sigmoid_fast(pre[1]);
+            og4[q][2] = tanh_fast(pre[2]);
+            og4[q][3] = sigmoid_fast(pre[3]);
+            cnv[q] = og4[q][1] * creg[q] + og4[q][0] * og4[q][2];
+            hnv[q] = og4[q][3] * tanh_fast(cnv[q]);
+            if (pb[q] < B && pu[q] < H && s + 1 < T_) {
+                const bool vq = t < lenr[q];
+                xstore(hxn + frag_off(pb[q], pu[q], a.mtiles), mnx[q] ? f2bf(vq ? hnv[q] : hreg[q]) : (bf16)0);
+            }
+        }
+        grid_arrive(bar);
+        // outputs only later kernels read, and the next step's inputs
+#pragma unroll
+        for (int q = 0; q < PPT; ++q) {
+            const int b = pb[q], u = pu[q];
+            if (b >= B || u >= H) continue;
+            const bool vq = t < lenr[q];
+            const float cn = vq ? cnv[q] : creg[q], hn = hnv[q];
+            const bf16 hv = f2bf(vq ? hn : hreg[q]);
+            float* gt = D.gates + ((size_t)t * B + b) * G;
+            gt[u] = og4[q][0]; gt[H + u] = og4[q][1]; gt[2 * H + u] = og4[q][2]; gt[3 * H + u] = og4[q][3];
+            D.cres[((size_t)t * B + b) * H + u] = cn;
+            if (vq) { creg[q] = cnv[q]; hreg[q] = hn; }
+            ((bf16*)D.hrecT)[((size_t)t * H + u) * a.BP + b] = hv;
+            if (D.y) D.y[((size_t)t * B + b) * a.ldy + u] = vq ? hn : 0.0f;
+            if (D.ybuf) {
+                const bf16 yv = vq ? f2bf(hn) : (bf16)0;
+                ((bf16*)D.ybuf)[((size_t)t * B + b) * a.ldy + u] = yv;
+                ((bf16*)D.ybufT)[((size_t)t * a.ldy + u) * a.BP + b] = yv;
+            }
+        }
+        prefetch(s + 1);
+    }
+    // ---- final state (NaN if a barrier wait timed out, and then every step of y)
+    const bool failed = __hip_atomic_load(a.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0;
+#pragma unroll
+    for (int q = 0; q < PPT; ++q) {
+        if (pb[q] < B && pu[q] < H) {
+            D.hT[(size_t)pb[q] * H + pu[q]] = failed ? __builtin_nanf("") : hreg[q];
+            D.cT[(size_t)pb[q] * H + pu[q]] = failed ? __builtin_nanf("") : creg[q];
+            if (failed && D.y)
+                for (int t = 0; t < T_; ++t) D.y[((size_t)t * B + pb[q]) * a.ldy + pu[q]] = __builtin_nanf("");
+        }
+    }
+    grid_exit(a.bar, a.nslots, a.err);
+}
+
+// ---------------------------------------------------------------------------
+// Persistent BPTT for large batches (Eq. 7-10), one layer.  The recurrent
+// gradient of a step, dh_{t-1} = (DA_t U^T) * m * s, is a product over the
+// 4H gate columns; at a large batch it runs split over the gate columns so
+// that every workgroup keeps a 128-unit x 512-column block of U in
+// registers:
+//   phase A (pointwise, Eq. 7-9): workgroup = (16 units, 64 rows); sums the
+//     partial gradients of the step before over the column groups, forms
+//     DA_t of its tile and publishes it;
+//   phase B (product, Eq. 10): workgroup = (64 rows, unit group of 128,
+//     column group of 512); each wave multiplies 4 of the group's 16
+//     column chunks for 64 of its units, the four column quarters are
+//     summed through LDS and the group's partial [B][H] is published.
+// Two grid barriers per step; partial sums are added in a fixed order.
+constexpr int BB_NW = 8, BB_MG = 64, BB_UT = 16, BB_UG = 128, BB_KG = 512, BB_RP = BB_UG + 4;
+
+__global__ void __launch_bounds__(512) k_bwd_big(PBwdArgs a) {
+    constexpr int MT = BB_MG / 16, NTH = 64 * BB_NW, KC = 4, NTL = 4;
+    constexpr int PPT = BB_MG * BB_UT / NTH;   // (row, unit) pairs per thread in phase A
+    extern __shared__ __align__(16) char smem[];
+    float* red = (float*)smem;                 // phase B: [4 column quarters][64 rows][BB_RP]
+    const int H = a.H, G = 4 * H, B = a.B, T_ = a.T;
+    const int nslot = gridDim.x;               // one slot (one direction per launch)
+    const PBwdDir& D = a.d[0];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g8 = 8 * (lane >> 4);
+    unsigned* bar = slot_bar(a.bar, 0);
+    const size_t das = (size_t)((G + 31) / 32) * a.mtiles * 512;   // fragment-major DA block per step
+    const int nchG = (G + 31) / 32;
+
+    // ---- phase A role: (unit tile, row group)
+    const int nA = a.ntiles * a.mgroups;
+    const bool roleA = (int)blockIdx.x < nA;
+    const int tA = blockIdx.x / a.mgroups, mA = blockIdx.x % a.mgroups;
+    const int u0 = tA * BB_UT, mA0 = mA * BB_MG;
+    // ---- phase B role: (row group, unit group, column group)
+    const int nB = a.mgroups * a.ngu * a.ngk;
+    const bool roleB = (int)blockIdx.x < nB;
+    const int rgB = blockIdx.x % a.mgroups, ugB = (blockIdx.x / a.mgroups) % a.ngu,
+              kgB = blockIdx.x / (a.mgroups * a.ngu);
+    const int mB0 = rgB * BB_MG;
+    const int kq = w >> 1, ch = w & 1;         // this wave's column quarter and unit half
+
+    // U block in registers: B fragment (chunk c, unit tile j) of this wave:
+    // contraction = gate columns, output columns = units
+    bf16x8_t ub[KC][NTL];
+    {
+        const bf16* U = (const bf16*)D.U;
+#pragma unroll
+        for (int j = 0; j < NTL; ++j) {
+            const int u = BB_UG * ugB + 16 * (NTL * ch + j) + (lane & 15);
+#pragma unroll
+            for (int c = 0; c < KC; ++c) {
+                const int n0 = BB_KG * kgB + 32 * (KC * kq + c) + g8;
+                s16x8_t f;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const int n = n0 + e;
+                    const bf16 v = U[(size_t)min(u, H - 1) * G + min(n, G - 1)];
+                    f[e] = (short)((roleB && u < H && n < G) ? v : (bf16)0);
+                }
+                ub[c][j] = __builtin_bit_cast(bf16x8_t, f);
+            }
+        }
+    }
+    // phase A pairs and their carries
+    float dcs[PPT], dhc[PPT];
+    int pb[PPT], pu[PPT], lenr[PPT];
+#pragma unroll
+    for (int q = 0; q < PPT; ++q) {
+        const int p = tid + NTH * q;
+        pb[q] = roleA ? mA0 + p / BB_UT : B;
+        pu[q] = u0 + p % BB_UT;
+        const bool ok = pb[q] < B && pu[q] < H;
+        dhc[q] = (ok && D.dhT) ? D.dhT[(size_t)pb[q] * H + pu[q]] : 0.f;
+        dcs[q] = (ok && D.dcT) ? D.dcT[(size_t)pb[q] * H + pu[q]] : 0.f;
+        lenr[q] = a.lengths ? a.lengths[min(pb[q], B - 1)] : T_;
+    }
+    auto step_t = [&](int s) { return D.dir == 0 ? T_ - 1 - s : s; };
+    // per-step inputs of phase A (clamped addresses), one step ahead
+    float gt4[PPT][4], ctv[PPT], cpv[PPT], dyv[PPT];
+    int mkr[PPT];
+    auto prefetch = [&](int s) {
+        const int t = step_t(min(s, T_ - 1));
+        const int tp = D.dir == 0 ? t - 1 : t + 1;        // forward predecessor of t
+        const int tn = step_t(max(s - 1, 0));              // the step processed before
+#pragma unroll
+        for (int q = 0; q < PPT; ++q) {
+            const int bc = min(pb[q], B - 1), uc = min(pu[q], H - 1);
+            const float* gr = D.gates + ((size_t)t * B + bc) * G;
+#pragma unroll
+            for (int g = 0; g < 4; ++g) gt4[q][g] = gr[g * H + uc];
+            ctv[q] = D.cres[((size_t)t * B + bc) * H + uc];
+            cpv[q] = *(s >= T_ - 1 ? D.c0 + (size_t)bc * H + uc : D.cres + ((size_t)tp * B + bc) * H + uc);
+            if (D.dy) {
+                dyv[q] = D.dy[((size_t)t * B + bc) * a.ldy + uc];
+            } else if (D.dxc) {
+                const int dp = D.dxpos[(size_t)t * a.kmax + uc];
+                dyv[q] = dp >= 0 ? D.dxc[((size_t)t * B + bc) * a.lddx + dp] : 0.0f;
+            } else {
+                dyv[q] = 0.0f;
+            }
+            mkr[q] = D.rh.mask[(size_t)tn * a.kmax + uc];
+        }
+    };
+    // this lane's A offset in the wave's first chunk and the group's first
+    // row tile (chunks past 4H read past the block: zero)
+    const uint32_t a_base = (uint32_t)(frag_lane_off((BB_KG / 32) * kgB + KC * kq, mB0 / 16, lane, a.mtiles) *
+                                       sizeof(bf16));
+
+    prefetch(0);
+    bool ok = true;
+    for (int s = 0; s <= T_; ++s) {
+        const bool final_pass = s == T_;
+        const int t = final_pass ? -1 : step_t(s);
+        // ---- phase A: the partial recurrent gradients of the step before
+        // (phase B of iteration s-1) are complete after 2s arrivals
+        if (s > 0 && !(ok = grid_wait(bar, 0, nslot, (unsigned)(2 * s), a.err, a.timeout, STATUS_BWD))) break;
+        float da4[PPT][4];
+#pragma unroll
+        for (int q = 0; q < PPT; ++q) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g) da4[q][g] = 0.f;
+            // (copies the compiler cannot hoist: the addresses derived from
+            // them are recomputed per step instead of occupying registers)
+            int b = pb[q], u = pu[q];
+            asm volatile("" : "+v"(b), "+v"(u));
+            if (b >= B || u >= H) continue;
+            float dh = dhc[q];
+            if (s > 0 && mkr[q]) {
+                // units dropped at the step before get no recurrent gradient (Eq. 10)
+                float v = 0.f;
+                for (int k = 0; k < a.ngk; ++k) v += xload1(a.part + ((size_t)k * B + b) * H + u);
+                dh += D.s_rh * v;
+            }
+            if (final_pass) {
+                D.dh0[(size_t)b * H + u] = dh;
+                D.dc0[(size_t)b * H + u] = dcs[q];
+                continue;
+            }
+            if (t < lenr[q]) {
+                dh += dyv[q];
+                const float ig = gt4[q][0], fg = gt4[q][1], gg = gt4[q][2], og = gt4[q][3];
+                const float tc = tanh_fast(ctv[q]);
+                const float dout = dh * tc;                            // Eq. 7
+                const float dc = dh * og * (1.0f - tc * tc) + dcs[q];  // Eq. 7
+                da4[q][0] = dc * gg * ig * (1.0f - ig);                // Eq. 9, sigmoid'
+                da4[q][1] = dc * cpv[q] * fg * (1.0f - fg);            // Eq. 8, sigmoid'
+                da4[q][2] = dc * ig * (1.0f - gg * gg);                // Eq. 9, tanh'
+                da4[q][3] = dout * og * (1.0f - og);                   // Eq. 7, sigmoid'
+                dcs[q] = dc * fg;                                      // Eq. 8
+                dhc[q] = 0.0f;
+            } else {
+                dhc[q] = dh;                                           // frozen row: pass through
+            }
+            bf16* dar = (bf16*)D.da + (size_t)t * das;
+#pragma unroll
+            for (int g = 0; g < 4; ++g) xstore(dar + frag_off(b, g * H + u, a.mtiles), f2bf(da4[q][g]));
+        }
+        if (final_pass) break;
+        grid_arrive(bar);                                  // DA_t is published (arrival 2s+1)
+        // DA^T (the weight gradients' operand) through LDS: the tile's
+        // [4 gates x 16 units][64 rows] block, written as 16-byte row pieces
+        if (roleA) {
+            bf16* st = (bf16*)red;
+#pragma unroll
+            for (int q = 0; q < PPT; ++q) {
+                const int p = tid + NTH * q;
+                const bool okp = pb[q] < B && pu[q] < H;
+#pragma unroll
+                for (int g = 0; g < 4; ++g) st[(g * BB_UT + p % BB_UT) * BB_MG + p / BB_UT] = f2bf(okp ? da4[q][g] : 0.f);
+            }
+            __syncthreads();
+            constexpr int PPR = BB_MG * 2 / 16;            // 16-byte pieces of a staged row
+            bf16* dat = (bf16*)D.daT + (size_t)t * G * a.BP;
+            for (int i = tid; i < 4 * BB_UT * PPR; i += NTH) {
+                const int r = i / PPR, pc = i % PPR;
+                const int u = u0 + r % BB_UT, col = mA0 + pc * 8;
+                if (u < H && col < a.BP)
+                    *(uint4*)(dat + (size_t)((r / BB_UT) * H + u) * a.BP + col) = *(const uint4*)(st + r * BB_MG + pc * 8);
+            }
+        }
+        // ---- phase B: every DA_t tile is published after 2s+1 arrivals
+        if (!(ok = grid_wait(bar, 0, nslot, (unsigned)(2 * s + 1), a.err, a.timeout, STATUS_BWD))) break;
+        if (roleB) {
+            // A fragments (DA_t rows of the group, this wave's column quarter)
+            // two chunks deep; offsets as in the large-batch forward
+            const __amdgpu_buffer_rsrc_t dr = buf_rsrc((const bf16*)D.da + (size_t)t * das,
+                                                       (uint32_t)(das * sizeof(bf16)));
+            uint32_t vb;
+            asm volatile("v_mov_b32 %0, %1" : "=v"(vb) : "v"(a_base));
+            auto issue = [&](int c, u32x4_t (&f)[MT]) {
+                const uint32_t vo = vb + (uint32_t)(c * a.mtiles * 1024);
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+                    f[mt] = __builtin_amdgcn_raw_buffer_load_b128(dr, vo + mt * 1024, 0, CPOL_SC1);
+            };
+            u32x4_t fa[2][MT];
+            issue(0, fa[0]);
+            issue(1, fa[1]);
+            f32x4_t acc[MT][NTL];
+#pragma unroll
+            for (int i = 0; i < MT; ++i)
+#pragma unroll
+                for (int j = 0; j < NTL; ++j) acc[i][j] = f32x4_t{0, 0, 0, 0};
+#pragma unroll
+            for (int c = 0; c < KC; ++c) {
+                u32x4_t (&f)[MT] = fa[c & 1];
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) {
+                    const bf16x8_t av = __builtin_bit_cast(bf16x8_t, f[mt]);
+#pragma unroll
+                    for (int j = 0; j < NTL; ++j)
+                        acc[mt][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, ub[c][j], acc[mt][j], 0, 0, 0);
+                }
+                if (c + 2 < KC) issue(c + 2, f);
+            }
+            // (the DA^T staging of phase A is done with the LDS area: every
+            // thread passed the barrier wait above after its stores)
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int j = 0; j < NTL; ++j)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        red[(kq * BB_MG + mt * 16 + acc_row(lane, r)) * BB_RP + 64 * ch + 16 * j + (lane & 15)] =
+                            acc[mt][j][r];
+            __syncthreads();
+            float* pk = a.part + (size_t)kgB * B * H;
+            for (int i = tid; i < BB_MG * BB_UG; i += NTH) {
+                const int rr = i / BB_UG, uu = i % BB_UG;
+                const int b = mB0 + rr, u = BB_UG * ugB + uu;
+                if (b < B && u < H) {
+                    float v = 0.f;
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) v += red[(k * BB_MG + rr) * BB_RP + uu];
+                    xstore(pk + (size_t)b * H + u, v);
+                }
+            }
+        }
+        grid_arrive(bar);                                  // the partials are published (arrival 2s+2)
+        prefetch(s + 1);                                   // (in flight during the next wait)
+    }
+    // a timed-out barrier, here or in the forward pass of the step, poisons
+    // the input-state gradients
+    if (!ok || __hip_atomic_load(a.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0 ||
+        __hip_atomic_load(sync_status(a.err), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
+#pragma unroll
+        for (int q = 0; q < PPT; ++q)
+            if (pb[q] < B && pu[q] < H) {
+                D.dh0[(size_t)pb[q] * H + pu[q]] = __builtin_nanf("");
+                D.dc0[(size_t)pb[q] * H + pu[q]] = __builtin_nanf("");
+            }
+    }
+    grid_exit(a.bar, 1, a.err);
+}
+
+// ---------------------------------------------------------------------------
 // Host side.
 
 // Checks (once per device, kernel and LDS size) that nwg workgroups of the
@@ -1077,6 +1369,26 @@ hipError_t launch_fwd_persist(PFwdArgs& a, hipStream_t st, int kid_timer_on, hip
 template hipError_t launch_fwd_persist<float>(PFwdArgs&, hipStream_t, int, hipEvent_t, hipEvent_t);
 template hipError_t launch_fwd_persist<bf16>(PFwdArgs&, hipStream_t, int, hipEvent_t, hipEvent_t);
 
+// The large-batch forward (bf16): returns an error before anything is
+// enqueued when the shape is outside its register budget or the grid does
+// not fit the device at once.
+hipError_t launch_fwd_big(PFwdArgs& a, hipStream_t st, int timer_on, hipEvent_t e0, hipEvent_t e1) {
+    const int KC = a.H <= 512 ? 2 : a.H <= 1024 ? 4 : 0;
+    if (!KC || a.nslots > 2) return hipErrorInvalidValue;
+    a.ntiles = (a.H + BG_UT - 1) / BG_UT;
+    a.mgroups = (a.B + BG_MG - 1) / BG_MG;
+    const int nwg = a.nslots * a.ntiles * a.mgroups;
+    const size_t lds = (size_t)BG_NW * BG_MG * BG_RP * sizeof(float);
+    void (*fn)(PFwdArgs) = KC == 2 ? k_fwd_big<2> : k_fwd_big<4>;
+    hipError_t e = resident_limit((const void*)fn, 64 * BG_NW, lds, nwg);
+    if (e != hipSuccess) return e;
+    if (timer_on) (void)hipEventRecord(e0, st);
+    hipLaunchKernelGGL(fn, dim3(nwg), dim3(64 * BG_NW), lds, st, a);
+    e = hipGetLastError();
+    if (timer_on && e == hipSuccess) (void)hipEventRecord(e1, st);
+    return e;
+}
+
 size_t bwd_persist_lds(int H, int UB, int MG, int esize) {
     const size_t G = 4 * (size_t)H, GP = (G + 31) / 32 * 32 + 8;
     return (((size_t)UB * GP * esize + 15) & ~(size_t)15) + (size_t)PB_NW * MG * 16 * 4;
@@ -1116,5 +1428,25 @@ hipError_t launch_bwd_persist(PBwdArgs& a, hipStream_t st, int timer_on, hipEven
 
 template hipError_t launch_bwd_persist<float>(PBwdArgs&, hipStream_t, int, hipEvent_t, hipEvent_t);
 template hipError_t launch_bwd_persist<bf16>(PBwdArgs&, hipStream_t, int, hipEvent_t, hipEvent_t);
+
+// The large-batch backward (bf16, one direction per launch): returns an
+// error before anything is enqueued when the grid does not fit the device.
+hipError_t launch_bwd_big(PBwdArgs& a, hipStream_t st, int timer_on, hipEvent_t e0, hipEvent_t e1) {
+    if (a.nslots != 1) return hipErrorInvalidValue;
+    a.ntiles = (a.H + BB_UT - 1) / BB_UT;
+    a.mgroups = (a.B + BB_MG - 1) / BB_MG;
+    a.ngu = (a.H + BB_UG - 1) / BB_UG;
+    a.ngk = (4 * a.H + BB_KG - 1) / BB_KG;
+    const int nA = a.ntiles * a.mgroups, nB = a.mgroups * a.ngu * a.ngk;
+    const int nwg = nA > nB ? nA : nB;
+    const size_t lds = (size_t)4 * BB_MG * BB_RP * sizeof(float);
+    hipError_t e = resident_limit((const void*)k_bwd_big, 64 * BB_NW, lds, nwg);
+    if (e != hipSuccess) return e;
+    if (timer_on) (void)hipEventRecord(e0, st);
+    hipLaunchKernelGGL(k_bwd_big, dim3(nwg), dim3(64 * BB_NW), lds, st, a);
+    e = hipGetLastError();
+    if (timer_on && e == hipSuccess) (void)hipEventRecord(e1, st);
+    return e;
+}
 
 }  // namespace lsd

@@ -37,6 +37,7 @@ struct Plan {
     // workspace
     size_t w_gx, w_hrec, w_hx, w_xx, w_gxs;     // forward (w_gxs: input products of the stacked layers above the first)
     size_t w_da, w_daT, w_dxw, w_dc, w_dhc, w_dxc;  // backward
+    size_t w_part;                              // backward, large batch: [ceil(4H/512)][B][H] partial sums
     size_t w_sync;                              // barrier counters and error flag
     size_t w_loss, w_total;
 

@@ -1,0 +1,55 @@
+"""The large-batch persistent forward (U slice held in registers, the
+contraction split over the waves and summed through LDS) on ragged shapes,
+forced with LSTM_SD_BIG=2 (it otherwise runs only where the row-group
+tiling of the other persistent forward does not fit, as at the stress
+shape): hidden sizes that are not multiples of the 32-neuron chunk or of the
+16-unit tile, batches that are not multiples of the 64-row group or of the
+16-row MFMA tile, both directions, per-row lengths, and both modes."""
+import dataclasses
+
+import numpy as np
+import pytest
+
+import workloads
+from tests._parity import TOL, compare, oracle_step, say, summary
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+def _run(cfg, wl, p_nr, p_rh, compact):
+    from oracle import masks as om
+    from paper_2106_12089_amd.session import Session
+    s = Session(wl, p_nr, p_rh, compact)
+    s.masks(cfg.mask_seed, 0)
+    s.forward()
+    s.loss_grad()
+    s.backward()
+    torch.cuda.synchronize()
+    m_nr, m_rh = om.all_masks(cfg.mask_seed, 0, cfg.num_layers, cfg.num_dirs, cfg.seq_len, cfg.k_in,
+                              cfg.hidden, p_nr, p_rh)
+    return s.outputs(), oracle_step(wl, p_nr, p_rh, m_nr, m_rh)
+
+
+@pytest.mark.parametrize("shape", [
+    dict(num_layers=2, num_dirs=1, input_dim=70, hidden=45, batch=70, seq_len=5),
+    dict(num_layers=1, num_dirs=2, input_dim=129, hidden=100, batch=19, seq_len=4),
+    dict(num_layers=2, num_dirs=1, input_dim=64, hidden=1000, batch=130, seq_len=3),
+    dict(num_layers=1, num_dirs=1, input_dim=33, hidden=512, batch=64, seq_len=6, min_len=0),
+])
+@pytest.mark.parametrize("mode", [(0.5, 0.5, 1), (0.5, 0.5, 0), (0.3, 0.0, 1)])
+def test_big_forward_ragged(shape, mode, monkeypatch):
+    monkeypatch.setenv("LSTM_SD_BIG", "2")
+    base = workloads.get_config("tiny")
+    cfg = dataclasses.replace(base, name="big", dtype="bf16", loss="mse", **shape)
+    wl = workloads.make_workload(cfg)
+    p_nr, p_rh, compact = mode
+    say(f"[gpu] big forward {shape} p_nr={p_nr} p_rh={p_rh} compact={compact}")
+    gpu, ref = _run(cfg, wl, p_nr, p_rh, compact)
+    errs = compare(gpu, ref)
+    say("   errs", summary(errs))
+    bad = {k: v for k, v in errs.items() if not v <= TOL["bf16"]}
+    assert not bad, bad
+    if cfg.min_len is not None:
+        valid = np.arange(cfg.seq_len)[:, None] < wl.lengths[None, :]
+        assert np.all(gpu["y"][~valid] == 0.0)
