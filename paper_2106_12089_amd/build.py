@@ -13,7 +13,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIBDIR = os.path.join(PKG, "_lib")
 LIB = os.path.join(LIBDIR, "liblstm_sd.so")
-SOURCES = ["kernels.hip", "persist.hip", "abi.hip"]
+SOURCES = ["kernels.hip", "persist.hip", "big.hip", "abi.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

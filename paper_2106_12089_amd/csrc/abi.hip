@@ -50,6 +50,7 @@ template <typename T>
 hipError_t launch_bwd_persist(PBwdArgs& a, hipStream_t st, int timer_on, hipEvent_t e0, hipEvent_t e1);
 hipError_t launch_fwd_big(PFwdArgs& a, hipStream_t st, int timer_on, hipEvent_t e0, hipEvent_t e1);
 hipError_t launch_bwd_big(PBwdArgs& a, hipStream_t st, int timer_on, hipEvent_t e0, hipEvent_t e1);
+bool wgrad_big_fits(int B);
 int kernel_timer_start(const char* name);
 int kernel_timer_stop(double* total_ms, int64_t* launches);
 
@@ -184,6 +185,12 @@ static int big_mode() {
     return (v && v[0] == '0') ? 0 : (v && v[0] == '2') ? 2 : 1;
 }
 static bool use_big() { return big_mode() != 0; }
+// LSTM_SD_WGRAD_BIG=0: the weight gradients of a large batch on the
+// small-batch kernel
+static bool use_wgrad_big() {
+    const char* v = getenv("LSTM_SD_WGRAD_BIG");
+    return !(v && v[0] == '0');
+}
 
 static bool use_persistent() {
     const char* v = getenv("LSTM_SD_PERSIST");
@@ -538,6 +545,8 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
     WgBatch b;
     b.np = 0;
     b.status = sync_status;
+    b.big = std::is_same<E, bf16>::value && wgrad_big_fits(B) && use_big() && (B >= 128 || big_mode() == 2) &&
+            use_wgrad_big();
     auto add_wgrad = [&](const WgArgs& a) {
         if (b.np == WG_MAXP) {                 // full: launch it (its DA is complete)
             launch_wgrad<E>(b, st);

@@ -174,6 +174,7 @@ constexpr int WG_MAXP = 8;
 struct WgBatch {
     WgArgs p[WG_MAXP];
     int np;
+    int big;                            // bf16 at a large batch: the register-accumulated kernel
     const int* status;                  // sticky barrier status of the step, or null: when set, NaN is written
 };
 

@@ -1688,9 +1688,18 @@ void launch_dx(const DxArgs& a, int K, hipStream_t st) {
     else if (a.B <= 32) launch_k(KID_DX, k_dx<T, 2>, grid, dim3(256), 0, st, a);
     else launch_k(KID_DX, k_dx<T, 4>, grid, dim3(256), 0, st, a);
 }
+void launch_wgrad_big(const WgBatch& b, hipStream_t st, hipEvent_t e0, hipEvent_t e1);
+int setup_big_attributes();
+
 template <typename T>
 void launch_wgrad(const WgBatch& b, hipStream_t st) {
     if (b.np == 0) return;
+    if (b.big && sizeof(T) == 2) {             // large batch (bf16): the register-accumulated kernel
+        hipEvent_t e0 = nullptr, e1 = nullptr;
+        if (g_timer_kid == KID_WGRAD) { e0 = timer_event(); e1 = timer_event(); }
+        launch_wgrad_big(b, st, e0, e1);
+        return;
+    }
     const WgArgs& a = b.p[0];                  // the problems share G, B and the mode
     const dim3 grid(NXCD * ((a.G + WG_NB - 1) / WG_NB), 1, b.np);
     size_t lds = 0;
@@ -1782,6 +1791,7 @@ int setup_kernel_attributes() {
                           (const void*)k_wgrad<float, true, true>, (const void*)k_wgrad<bf16, true, true>};
     for (const void* f : fns)
         if (hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, lds) != hipSuccess) return LSTM_SD_EHIP;
+    if (setup_big_attributes()) return LSTM_SD_EHIP;
     g_attr_done = 1;
     return 0;
 }
