@@ -3,17 +3,26 @@
 A step is one pass of the whole path over one batch of synthetic input that
 is already resident in HBM: draw the Case-III masks and build the keep lists
 (fresh masks every step), forward unroll, MSE loss gradient, BPTT with the
-weight gradients.  The workload is the 2-layer, 650-unit language-model
-shape (batch 20, 35 steps, bf16 storage with fp32 accumulation, structured
-dropout p = 0.5 on the non-recurrent inputs).  Prints one JSON line.
+weight gradients.  The headline workload is the 2-layer, 650-unit
+language-model shape (batch 20, 35 steps, bf16 storage with fp32
+accumulation, structured dropout p = 0.5 on the non-recurrent inputs).
+Every other workload (LM-large, the Luong encoder, the BiLSTM tagger, the
+2-layer 1024-unit batch-256 stress shape, the AWD-LSTM shape) is measured in
+the same run under "configs".  Prints one JSON line.
 
   value      effective TFLOP/s: algorithmic FLOPs of the step (products over
              the rows actually kept, three products per gate GEMM) / step time
   speedup    the same kernels run dense (compact = 0) / the method
-  roofline   the kernel with the largest share of the step, its algorithmic
-             bytes (or FLOPs) per launch over its average launch duration,
-             measured with HIP events on its own stream in a second timed
-             pass of the same workload
+  phases     per-step time of each kernel class (FP-x input product, FP-rec
+             recurrence, BP-rec recurrence backward, BP-dx input gradient,
+             WG weight gradients, mask draw), from HIP events around every
+             launch of that class on its launch stream, in a separate pass
+  roofline   the kernel class with the largest share of the step.  The
+             recurrent classes at batch <= 64 are priced on the bytes of the
+             kept rows of U they stream every time step (K'_h * 4H * element
+             size per (layer, direction, t)) against HBM; every other class on
+             its algorithmic MFMA FLOPs against the dense matrix peak of its
+             data type
 """
 from __future__ import annotations
 
@@ -33,7 +42,13 @@ WORKLOAD = "lm_medium"
 METRIC = "LSTM fwd+BPTT step time & eff. TFLOP/s; speedup vs dense at p=0.5"
 PEAK_HBM_GBS = 8000.0
 PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
-KERNELS = ("fwd_persist", "step", "bwd_persist", "bwd", "wgrad", "fx", "dx")
+KERNELS = ("mask_build", "transpose", "fx", "fwd_persist", "step", "bwd_persist", "bwd", "dx", "wgrad")
+GEMM_KERNELS = ("fx", "fwd_persist", "step", "bwd_persist", "bwd", "dx", "wgrad")
+RECURRENT = ("fwd_persist", "step", "bwd_persist", "bwd")
+# kernel classes of each phase of the step (the paper's FP / BP / WG split)
+PHASES = {"mask": ("mask_build",), "fp_x": ("fx",), "fp_rec": ("fwd_persist", "step"),
+          "bp_rec": ("bwd_persist", "bwd"), "bp_dx": ("dx",), "wg": ("wgrad",), "other": ("transpose",)}
+CONFIG_RUNS = ("lm_large", "seq2seq_enc", "tagger", "stress", "awd_lstm")
 KERNEL_SRC_DIR = os.path.join(ROOT, "paper_2106_12089_amd", "csrc")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
@@ -158,7 +173,7 @@ def kernel_work(kind, counts, cfg, stacked=False):
 
 # ---------------------------------------------------------------------------
 
-def run_mode(wl, p_nr, p_rh, compact, steps, warmup, timed_kernels=(), fixed=False):
+def run_mode(wl, p_nr, p_rh, compact, steps, warmup, timed_kernels=(), fixed=False, kernel_steps=None):
     import torch
     from paper_2106_12089_amd import binding as B_
     from paper_2106_12089_amd.session import Session
@@ -208,13 +223,14 @@ def run_mode(wl, p_nr, p_rh, compact, steps, warmup, timed_kernels=(), fixed=Fal
     counts = np.mean(counts_all, axis=0)
     # per-kernel timing: a second timed pass per kernel class, events on the launch stream
     ktime = {}
+    ks = steps if kernel_steps is None else kernel_steps
     for kname in timed_kernels:
         B_.lstm_sd_kernel_timer_start(kname)
-        for i in range(steps):
+        for i in range(ks):
             s.step(cfg.mask_seed, i)
         ms, n = B_.lstm_sd_kernel_timer_stop()
         torch.cuda.synchronize()
-        ktime[kname] = dict(total_ms=ms / steps, launches=n / steps, avg_us=1e3 * ms / max(n, 1))
+        ktime[kname] = dict(total_ms=ms / ks, launches=n / ks, avg_us=1e3 * ms / max(n, 1))
     return dict(ms=total_ms / steps, wall_ms=wall * 1e3 / steps, counts=counts,
                 flops=float(np.mean([algorithmic_flops(c, cfg, wl.lengths) for c in counts_all])),
                 phases=dict(mask=phases[0], forward=phases[1], loss=phases[2], backward=phases[3]),
@@ -386,18 +402,65 @@ def embedding_cpu_baseline(wl, p):
                 sample="one embedding-gradient call of the same workload, float64 NumPy loop")
 
 
-def roofline(res, cfg):
+def recurrent_u_bytes(counts, cfg):
+    """Bytes of U a recurrence streams per step of work: the kept rows
+    U[K'_h, :] of every (layer, direction, t), K'_h * 4H * element size."""
+    L, D, H = cfg.num_layers, cfg.num_dirs, cfg.hidden
+    e = 2 if cfg.dtype == "bf16" else 4
+    return float(sum(np.sum(np.asarray(counts[L + l * D + d], np.float64)) * 4 * H * e
+                     for l in range(L) for d in range(D)))
+
+
+def is_stacked(res, cfg):
+    """One persistent launch per pass over a unidirectional stack."""
     kt = res["ktime"]
-    name = max(kt, key=lambda k: kt[k]["total_ms"])
-    # one persistent launch per pass: the stacked layout ran
-    stacked = cfg.num_layers > 1 and all(kt.get(k, {}).get("launches", 0) == 1 for k in ("fwd_persist", "bwd_persist"))
-    fl, by, nl = kernel_work(name, res["counts"], cfg, stacked)
+    return cfg.num_layers > 1 and all(kt.get(k, {}).get("launches", 0) == 1 for k in ("fwd_persist", "bwd_persist"))
+
+
+def kernel_table(res, cfg):
+    """Per kernel class: time per step, launches, algorithmic FLOPs and the
+    MFMA fraction (FLOPs / summed launch time / dense peak of the data type);
+    for the recurrences also the U-row bytes per launch and their HBM
+    fraction."""
+    kt = res["ktime"]
+    stacked = is_stacked(res, cfg)
+    peak_f = PEAK_TFLOPS["bf16" if cfg.dtype == "bf16" else "f32"]
+    out = {}
+    for k, v in kt.items():
+        if v["total_ms"] <= 0:
+            continue
+        ent = {"ms_per_step": round(v["total_ms"], 4), "launches_per_step": v["launches"],
+               "avg_us": round(v["avg_us"], 3)}
+        if k in GEMM_KERNELS:
+            fl, by, _ = kernel_work(k, res["counts"], cfg, stacked)
+            tf = fl / (v["total_ms"] * 1e-3) / 1e12
+            ent.update(gflop_per_step=round(fl / 1e9, 4), tflops=round(tf, 3), mfma_frac=round(tf / peak_f, 5),
+                       min_bytes_per_launch=int(by / max(v["launches"], 1)))
+            if k in RECURRENT:
+                ub = recurrent_u_bytes(res["counts"], cfg) / max(v["launches"], 1)
+                gbs = ub / (v["avg_us"] * 1e-6) / 1e9
+                ent.update(u_bytes_per_launch=int(ub), u_gbs=round(gbs, 1), hbm_frac=round(gbs / PEAK_HBM_GBS, 5))
+        out[k] = ent
+    return out
+
+
+def phase_times(res):
+    """Per-step ms of each phase (sum of its kernel classes)."""
+    kt = res["ktime"]
+    return {ph: round(sum(kt.get(k, {}).get("total_ms", 0.0) for k in ks), 4) for ph, ks in PHASES.items()}
+
+
+def roofline(res, cfg):
+    """Roofline of the dominant kernel class (largest time per step)."""
+    kt = res["ktime"]
+    cand = [k for k in GEMM_KERNELS if kt.get(k, {}).get("total_ms", 0) > 0]
+    name = max(cand, key=lambda k: kt[k]["total_ms"])
+    stacked = is_stacked(res, cfg)
+    fl, by, _ = kernel_work(name, res["counts"], cfg, stacked)
     launches = kt[name]["launches"]
     fl_l, by_l = fl / launches, by / launches
     dur = kt[name]["avg_us"] * 1e-6
     peak_f = PEAK_TFLOPS["bf16" if cfg.dtype == "bf16" else "f32"]
-    ai = fl_l / by_l
-    ridge = peak_f * 1e12 / (PEAK_HBM_GBS * 1e9)
     traffic = None
     try:
         with open(TRAFFIC_FILE) as f:
@@ -407,26 +470,105 @@ def roofline(res, cfg):
             traffic = ent["bytes_per_launch"]
     except (OSError, ValueError):
         pass
-    if ai < ridge:
-        out = dict(bound="hbm", achieved=by_l / dur / 1e9, peak=PEAK_HBM_GBS, unit="GB/s")
+    if name in RECURRENT and cfg.batch <= 64:
+        ub = recurrent_u_bytes(res["counts"], cfg) / launches
+        out = dict(bound="hbm", achieved=ub / dur / 1e9, peak=PEAK_HBM_GBS, unit="GB/s",
+                   formula="sum over (layer, direction, t) of K'_h * 4H * element bytes, per launch / launch time")
+        out["algorithmic_bytes_per_launch"] = ub
     else:
-        out = dict(bound="mfma", achieved=fl_l / dur / 1e12, peak=peak_f, unit="TFLOP/s")
+        out = dict(bound="mfma", achieved=fl_l / dur / 1e12, peak=peak_f, unit="TFLOP/s",
+                   formula="algorithmic FLOPs (2 * B * 4H * K' per product over kept rows) per launch / launch time")
+        out["algorithmic_bytes_per_launch"] = by_l
     out["frac"] = out["achieved"] / out["peak"]
     out["traffic"] = traffic
+    out["mfma_frac"] = fl_l / dur / 1e12 / peak_f
     out.update(kernel=name, launch_avg_us=kt[name]["avg_us"], launches_per_step=launches,
-               algorithmic_bytes_per_launch=by_l, algorithmic_flops_per_launch=fl_l,
-               share_of_step=kt[name]["total_ms"] / res["ms"],
-               kernels_ms_per_step={k: round(v["total_ms"], 4) for k, v in kt.items()})
-    for k in ("achieved", "frac"):
+               min_bytes_per_launch=by_l, algorithmic_flops_per_launch=fl_l,
+               share_of_step=kt[name]["total_ms"] / res["ms"])
+    for k in ("achieved", "frac", "mfma_frac", "share_of_step"):
         out[k] = round(out[k], 5)
     return out
 
 
-def cpu_baseline(wl, p_nr, p_rh, budget_s=12.0):
+def rates(cfg, p, rh):
+    """(p_nr, p_rh) of a mode: p on every site, or the config's per-layer
+    rate vectors when it has them."""
+    if cfg.p_nr_layers is not None:
+        return list(cfg.p_nr_layers), (list(cfg.p_rh_layers) if rh else 0.0)
+    return p, (p if rh else 0.0)
+
+
+def mode_summary(r, rd, cfg, wl):
+    """One mode (compact r, dense rd) of a config."""
+    out = {"ms_per_step": round(r["ms"], 4),
+           "tflops": round(r["flops"] / (r["ms"] * 1e-3) / 1e12, 4),
+           "gflop_per_step": round(r["flops"] / 1e9, 4),
+           "step_ms_p10_p50_p90": [round(v, 4) for v in r["pct"]]}
+    if rd is not None:
+        out.update(dense_ms_per_step=round(rd["ms"], 4), speedup_vs_dense=round(rd["ms"] / r["ms"], 4),
+                   dense_equiv_tflops=round(algorithmic_flops(dense_counts(cfg), cfg, wl.lengths)
+                                            / (r["ms"] * 1e-3) / 1e12, 4))
+    if r["ktime"]:
+        ph = phase_times(r)
+        out["phases_ms"] = ph
+        out["kernels"] = kernel_table(r, cfg)
+        if rd is not None and rd["ktime"]:
+            phd = phase_times(rd)
+            out["phases_ms_dense"] = phd
+            out["phase_speedup"] = {k: round(phd[k] / ph[k], 4) for k in ph if ph[k] > 0 and phd[k] > 0}
+    return out
+
+
+def config_block(name, steps, warmup, cpu, no_dense=False, sweep=True):
+    """Every mode of one config: NR+ST and NR+RH+ST, each against the same
+    kernels run dense, with kernel-class times; the p sweep of configs that
+    have one (speedups only); the oracle on the host."""
+    import workloads
+    cfg = workloads.get_config(name)
+    wl = workloads.make_workload(cfg)
+    p = 0.5 if 0.5 in cfg.p_values else cfg.p_values[0]
+    kst = max(5, min(steps, 20))            # steps of each per-kernel-class pass
+    out = {"layers": cfg.num_layers, "dirs": cfg.num_dirs, "input_dim": cfg.input_dim, "hidden": cfg.hidden,
+           "batch": cfg.batch, "seq_len": cfg.seq_len, "dtype": cfg.dtype}
+    for mode, rh in (("nr_st", False), ("nr_rh_st", True)):
+        pn, pr = rates(cfg, p, rh)
+        r = run_mode(wl, pn, pr, 1, steps, warmup, timed_kernels=KERNELS, kernel_steps=kst)
+        rd = None if no_dense else run_mode(wl, pn, pr, 0, steps, warmup, timed_kernels=KERNELS, kernel_steps=kst)
+        out[mode] = dict(p_nr=pn, p_rh=pr, **mode_summary(r, rd, cfg, wl))
+        if mode == "nr_st":
+            out["roofline"] = roofline(r, cfg)
+    if sweep and len(cfg.p_values) > 1 and not no_dense:
+        sw = {}
+        for q in cfg.p_values:
+            if q == p:
+                continue
+            ent = {}
+            for mode, rh in (("nr_st", False), ("nr_rh_st", True)):
+                pn, pr = rates(cfg, q, rh)
+                r = run_mode(wl, pn, pr, 1, steps, warmup)
+                rd = run_mode(wl, pn, pr, 0, steps, warmup)
+                ent[mode] = {"ms_per_step": round(r["ms"], 4), "dense_ms_per_step": round(rd["ms"], 4),
+                             "speedup_vs_dense": round(rd["ms"] / r["ms"], 4),
+                             "tflops": round(r["flops"] / (r["ms"] * 1e-3) / 1e12, 4)}
+            sw[str(q)] = ent
+        out["p_sweep"] = sw
+    if cpu:
+        rows = None if cfg.batch <= 64 else np.arange(32)
+        out["cpu_baseline"] = cpu_baseline(wl, *rates(cfg, p, False), budget_s=2.0, max_steps=3, rows=rows)
+    return out
+
+
+def cpu_baseline(wl, p_nr, p_rh, budget_s=12.0, max_steps=50, rows=None):
     """The float64 oracle as it stands, timed on the host on whole training
-    steps of the same workload until about budget_s seconds of CPU work."""
+    steps of the same workload until about budget_s seconds of CPU work (at
+    most max_steps steps).  rows: time the oracle on these batch rows only
+    (the same workload's first rows; FLOPs counted for those rows)."""
+    import workloads
     from oracle import lstm, masks
     cfg = wl.cfg
+    B = cfg.batch
+    if rows is not None:
+        wl = workloads.slice_rows(wl, rows)
     try:
         from threadpoolctl import threadpool_info
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
@@ -434,7 +576,7 @@ def cpu_baseline(wl, p_nr, p_rh, budget_s=12.0):
         threads = os.cpu_count() or 1
     P = lstm.params_from(wl.W, wl.U, wl.b, cfg.num_layers, cfg.num_dirs)
     n, t_tot, flops = 0, 0.0, 0.0
-    while t_tot < budget_s and n < 50:
+    while t_tot < budget_s and n < max_steps:
         t0 = time.perf_counter()
         m_nr, m_rh = masks.all_masks(cfg.mask_seed, n, cfg.num_layers, cfg.num_dirs, cfg.seq_len,
                                      cfg.k_in, cfg.hidden, p_nr, p_rh)
@@ -442,7 +584,7 @@ def cpu_baseline(wl, p_nr, p_rh, budget_s=12.0):
         t_tot += time.perf_counter() - t0
         counts = [m.sum(1) for m in m_nr] + [m_rh[l][d].sum(1) for l in range(cfg.num_layers)
                                               for d in range(cfg.num_dirs)]
-        flops += algorithmic_flops(counts, cfg, wl.lengths)
+        flops += algorithmic_flops(counts, cfg, wl.lengths) * (wl.x.shape[1] / B)
         n += 1
     model = ""
     try:
@@ -454,15 +596,16 @@ def cpu_baseline(wl, p_nr, p_rh, budget_s=12.0):
         pass
     return dict(value=round(flops / t_tot / 1e12, 6), unit="TFLOP/s", cores=int(threads), kind="oracle",
                 cpu_count=os.cpu_count(), cpu_model=model,
-                sample=f"{n} whole training steps of the {cfg.name} workload (NR+ST, masks of steps "
-                       f"0..{n - 1}), float64 NumPy oracle, {t_tot / n * 1e3:.0f} ms/step",
+                sample=f"{n} whole training steps of the {cfg.name} workload"
+                       + ("" if rows is None else f" on its first {len(rows)} of {B} batch rows")
+                       + f" (NR+ST, masks of steps 0..{n - 1}), float64 NumPy oracle, {t_tot / n * 1e3:.0f} ms/step",
                 ms_per_step=round(t_tot / n * 1e3, 3))
 
 
-KERNEL_SYMBOLS = {"fwd_persist": "lsd::k_fwd_persist<", "step": "lsd::k_step<", "bwd_persist": "lsd::k_bwd_persist<",
-                  "bwd": "lsd::k_bwd<",
-                  "wgrad": "lsd::k_wgrad",            # the row-sparse and the full kernel
-                  "fx": "lsd::k_fx<", "dx": "lsd::k_dx<"}
+KERNEL_SYMBOLS = {"fwd_persist": ("lsd::k_fwd_persist<", "lsd::k_fwd_big<"), "step": ("lsd::k_step<",),
+                  "bwd_persist": ("lsd::k_bwd_persist<", "lsd::k_bwd_big"), "bwd": ("lsd::k_bwd<",),
+                  "wgrad": ("lsd::k_wgrad",),            # the row-sparse, the full and the large-batch kernel
+                  "fx": ("lsd::k_fx<",), "dx": ("lsd::k_dx<",), "mask_build": ("lsd::k_mask_build",)}
 
 
 def summarize_counters(fetch_csv, write_csv, copy_bytes, workload, command):
@@ -481,8 +624,8 @@ def summarize_counters(fetch_csv, write_csv, copy_bytes, workload, command):
             name = r["Kernel_Name"]
             if "copyBuffer" in name or "copy_kernel" in name:
                 copy = max(copy, v)
-            for k, sym in KERNEL_SYMBOLS.items():
-                if sym in name:
+            for k, syms in KERNEL_SYMBOLS.items():
+                if any(sym in name for sym in syms):
                     agg[k].append(v)
         return agg, copy
 
@@ -517,6 +660,9 @@ def main(argv=None):
     ap.add_argument("--no-head", action="store_true", help="skip the language-model output head runs")
     ap.add_argument("--no-case4", action="store_true", help="skip the Case-IV (fixed-in-time mask) runs")
     ap.add_argument("--no-case1", action="store_true", help="skip the Case-I (NR+Random) comparator run")
+    ap.add_argument("--configs", default="all",
+                    help="other workloads to measure in the same run: 'all', 'none' or a comma list")
+    ap.add_argument("--no-sweep", action="store_true", help="skip the p sweep of the tagger and stress workloads")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="also run a plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -540,8 +686,11 @@ def main(argv=None):
     cfg = workloads.get_config(args.workload)
     wl = workloads.make_workload(cfg)
     p = 0.5 if 0.5 in cfg.p_values else cfg.p_values[0]
-    head = run_mode(wl, p, 0.0, 1, args.steps, args.warmup, timed_kernels=KERNELS)
-    dense = None if args.no_dense else run_mode(wl, p, 0.0, 0, args.steps, args.warmup, timed_kernels=KERNELS)
+    kst = max(5, min(args.steps, 20))
+    head = run_mode(wl, p, 0.0, 1, args.steps, args.warmup, timed_kernels=KERNELS, kernel_steps=kst)
+    dense = None if args.no_dense else run_mode(wl, p, 0.0, 0, args.steps, args.warmup, timed_kernels=KERNELS,
+                                                kernel_steps=kst)
+    ms = mode_summary(head, dense, cfg, wl)
     out = {
         "metric": METRIC,
         "value": round(head["flops"] / (head["ms"] * 1e-3) / 1e12, 4),
@@ -554,27 +703,24 @@ def main(argv=None):
                    "input_dim": cfg.input_dim, "hidden": cfg.hidden, "batch": cfg.batch,
                    "seq_len": cfg.seq_len, "p_nr": p, "p_rh": 0.0, "mode": "NR+ST"},
         "value_kind": "effective TFLOP/s over kept-row FLOPs",
-        "speedup_vs_dense": round(dense["ms"] / head["ms"], 4) if dense else None,
-        "dense_ms_per_step": round(dense["ms"], 4) if dense else None,
-        "gflop_per_step": round(head["flops"] / 1e9, 4),
-        "dense_equiv_tflops": round(algorithmic_flops(dense_counts(cfg), cfg, wl.lengths)
-                                    / (head["ms"] * 1e-3) / 1e12, 4),
-        "phases_ms": {k: round(v, 4) for k, v in head["phases"].items()},
-        "phases_ms_dense": {k: round(v, 4) for k, v in dense["phases"].items()} if dense else None,
-        "step_ms_p10_p50_p90": [round(v, 4) for v in head["pct"]],
+        "speedup_vs_dense": ms.get("speedup_vs_dense"),
+        "dense_ms_per_step": ms.get("dense_ms_per_step"),
+        "gflop_per_step": ms["gflop_per_step"],
+        "dense_equiv_tflops": ms.get("dense_equiv_tflops"),
+        "step_ms_p10_p50_p90": ms["step_ms_p10_p50_p90"],
         "step_ms_p10_p50_p90_note": "per-step times of the pass with phase events (about 19 us above the clean pass)",
-        "speedup_per_kernel": {k: round(dense["ktime"][k]["total_ms"] / head["ktime"][k]["total_ms"], 4)
-                               for k in head["ktime"] if dense and head["ktime"][k]["total_ms"] > 0
-                               and dense["ktime"][k]["total_ms"] > 0} if dense else None,
+        "host_phases_ms": {k: round(v, 4) for k, v in head["phases"].items()},
+        "phases_ms": ms.get("phases_ms"),
+        "phases_ms_dense": ms.get("phases_ms_dense"),
+        "phase_speedup": ms.get("phase_speedup"),
+        "kernels": ms.get("kernels"),
         "roofline": roofline(head, cfg),
     }
     if not args.no_nrrh:
-        r = run_mode(wl, p, p, 1, args.steps, args.warmup)
-        rd = None if args.no_dense else run_mode(wl, p, p, 0, args.steps, args.warmup)
-        out["nrrh"] = {"ms_per_step": round(r["ms"], 4), "dense_ms_per_step": round(rd["ms"], 4) if rd else None,
-                       "speedup_vs_dense": round(rd["ms"] / r["ms"], 4) if rd else None,
-                       "tflops": round(r["flops"] / (r["ms"] * 1e-3) / 1e12, 4),
-                       "phases_ms": {k: round(v, 4) for k, v in r["phases"].items()}}
+        r = run_mode(wl, p, p, 1, args.steps, args.warmup, timed_kernels=KERNELS, kernel_steps=kst)
+        rd = None if args.no_dense else run_mode(wl, p, p, 0, args.steps, args.warmup, timed_kernels=KERNELS,
+                                                 kernel_steps=kst)
+        out["nrrh"] = dict(p_nr=p, p_rh=p, **mode_summary(r, rd, cfg, wl))
     if not args.no_case1:
         c1 = run_case1(wl, p, args.steps, args.warmup)
         out["case1"] = {"what": "Case-I (NR+Random) comparator: per-element input dropout, every layer dense",
@@ -614,6 +760,14 @@ def main(argv=None):
         out["calibration_copy_bytes"] = n * 4
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(wl, p, 0.0)
+    names = [] if args.configs in ("", "none") else \
+        [c for c in (CONFIG_RUNS if args.configs == "all" else args.configs.split(",")) if c != cfg.name]
+    if names:
+        out["configs"] = {}
+        for name in names:
+            print(f"[bench] config {name}", file=sys.stderr, flush=True)
+            out["configs"][name] = config_block(name, args.steps, args.warmup, not args.no_cpu, args.no_dense,
+                                                not args.no_sweep)
     print(json.dumps(out), flush=True)
     return 0
 

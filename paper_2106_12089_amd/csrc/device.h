@@ -149,6 +149,17 @@ __device__ __forceinline__ void raw_lds(Raw8<T>& f, const T* p) {
         f.w[4 * q] = v.x; f.w[4 * q + 1] = v.y; f.w[4 * q + 2] = v.z; f.w[4 * q + 3] = v.w;
     }
 }
+// Four consecutive 16-bit elements through the transposing LDS read of
+// gfx950 (ds_read_b64_tr_b16).  Within each 16-lane group, lane i receives
+// element i % 4 of the 8 bytes addressed by lanes 4e + i / 4, e = 0..3, as
+// its element e: when lanes 4e..4e+3 address columns 0, 4, 8, 12 of one row
+// of a K-major [K][N] tile, lane i receives column i of the four rows e.
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint2 lds_tr4(const bf16* p) {
+    const s16x4_t r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((s16x4_t __attribute__((address_space(3)))*)p);
+    return __builtin_bit_cast(uint2, r);
+}
+
 // pack an element-wise fragment
 __device__ __forceinline__ void raw_from(Raw8<bf16>& f, const Frag<bf16>& x) {
 #pragma unroll

@@ -34,13 +34,17 @@ namespace lsd {
 // group is MG batch rows.  512 threads = 8 waves; each contraction over kept
 // neurons is split over the waves (each wave issues all of its exchange
 // loads before its first MFMA) and reduced in LDS.
-// Dynamic LDS: the weight slice transposed, U [16*NT][HP] for a layer, W
-// [16*NT][KP] for a worker (dtype; pitch = rows rounded up to 32, plus 8,
-// zero past the end), keep lists [H+32] and [kin_max+32] (int16), reduction
-// [8][MG][16*NT] (float).  With every neuron of a contraction kept (its keep
-// list is the identity) a B fragment is one 16-byte LDS read per column
-// tile; otherwise its 8 rows are gathered through the keep list.
+// Dynamic LDS: the weight slice, U for a layer, W for a worker, with HP =
+// fwd_hp(H) (or KP) rows: rows of the weight rounded up to 32, plus 8, zero
+// past the end.  bf16 slices are K-major, [HP][16*NT + 4]: the B fragment of
+// a 16-column tile over 32 kept neurons is two transposing 8-byte LDS reads
+// per lane, whose addresses are the kept rows of the keep list, so a
+// gathered fragment costs what a contiguous one does.  f32 slices are
+// column-major, [16*NT][HP], a fragment one 32-byte read (identity keep
+// list) or 8 gathered elements.  Then keep lists [H+32] and [kin_max+32]
+// (int16) and the reduction area [8][MG][16*NT] (float).
 constexpr int PF_NW = 8;
+__host__ __device__ constexpr int fwd_ncp(int NT) { return 16 * NT + 4; }
 
 template <typename T, int NT, int MG>
 __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
@@ -48,6 +52,8 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
     constexpr int NTH = 64 * NW;
     constexpr int PPT = (MG * UPW + NTH - 1) / NTH;
     constexpr int MAXC = MT <= 2 ? 3 : 2;       // chunks per wave per round (registers)
+    constexpr bool KM = sizeof(T) == 2;          // K-major weight slices (transposing reads)
+    constexpr int NCP = fwd_ncp(NT);             // their row pitch (elements)
     extern __shared__ __align__(16) char smem[];
     const int H = a.H, G = 4 * H, B = a.B, T_ = a.T;
     const int HP = fwd_hp(H), KP = a.KP;
@@ -77,8 +83,10 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
     const bool fed = !has_x && D.dep >= 0;        // a layer reading its worker's input product
     const int kin = D.kin;
 
-    // U slice (or W slice) -> LDS, transposed: row c = nt*16 + g*4 + cu holds
-    // column g*H + u0 + 4nt + cu of the weight.  Each thread issues its loads
+    // U slice (or W slice) -> LDS: column c = nt*16 + cu*4 + g of the slice
+    // is column g*H + u0 + 4nt + cu of the weight (the four gates of a unit
+    // side by side, so the reduction reads them as one 16-byte piece).
+    // Each thread issues its loads
     // in batches of LB from clamped (valid) addresses before storing any: a
     // loop of load-then-store waits a full memory latency per element.
     {
@@ -91,22 +99,27 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
                 for (int j = 0; j < LB; ++j) {
                     const int i = min(i0 + NTH * j, total - 1);
                     const int k = i / NC, c = i % NC;
-                    const int u = u0 + 4 * (c >> 4) + (c & 3);
-                    v[j] = Wm[(size_t)min(k, krows - 1) * G + ((c & 15) >> 2) * H + min(u, H - 1)];
+                    const int u = u0 + 4 * (c >> 4) + ((c & 15) >> 2);
+                    v[j] = Wm[(size_t)min(k, krows - 1) * G + (c & 3) * H + min(u, H - 1)];
                 }
 #pragma unroll
                 for (int j = 0; j < LB; ++j) {
                     const int i = i0 + NTH * j;
                     if (i < total) {
                         const int k = i / NC, c = i % NC;
-                        const int u = u0 + 4 * (c >> 4) + (c & 3);
-                        dst[c * pitch + k] = (u < H && k < rows) ? v[j] : zero_val<T>();
+                        const int u = u0 + 4 * (c >> 4) + ((c & 15) >> 2);
+                        dst[KM ? k * NCP + c : c * pitch + k] = (u < H && k < rows) ? v[j] : zero_val<T>();
                     }
                 }
             }
         };
         if (!worker) load_slice((const T*)D.U, H, H, Ut, HP);
         if (has_x) load_slice((const T*)D.Win, kin, kin, Wt, KP);
+        // keep-list entries past a step's count are read as rows (their A
+        // side is zero): they always hold a valid row index
+        for (int i = tid; i < H + 32; i += NTH) kidx[i] = 0;
+        if (KP)
+            for (int i = tid; i < a.kin_max + 32; i += NTH) kidx_x[i] = 0;
     }
     // register state of this thread's (row, unit) pairs
     float creg[PPT], hreg[PPT], biasr[PPT][4];
@@ -199,8 +212,11 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
     // compute() multiplies every chunk slot of the
     // round (slots past the keep count have a zeroed A side and read B rows at
     // offset 0: no branch lets the compiler sink the loads into the products).
-    auto issue = [&](const T* src, size_t slot_elems, int c0, Raw8<T> (&fa)[MAXC][MT]) {
-        const __amdgpu_buffer_rsrc_t hr = buf_rsrc(src, (uint32_t)(slot_elems * sizeof(T)));
+    auto issue = [&](const T* src, size_t slot_elems, int n, int c0, Raw8<T> (&fa)[MAXC][MT]) {
+        // the resource ends after the chunks the count uses: loads of the
+        // chunk slots past it return 0 and move no data
+        const size_t used = (size_t)((n + 31) / 32) * a.mtiles * 512;
+        const __amdgpu_buffer_rsrc_t hr = buf_rsrc(src, (uint32_t)((used < slot_elems ? used : slot_elems) * sizeof(T)));
 #pragma unroll
         for (int i = 0; i < MAXC; ++i) {
             const int c = c0 + w + NW * i;
@@ -209,34 +225,49 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
                 raw_load<T, CPOL_SC1>(fa[i][mt], hr, m0 + 16 * mt + (lane & 15) < B ? (uint32_t)(frag_lane_off(c, m0 / 16 + mt, lane, a.mtiles) * sizeof(T)) : OOB_OFF);
         }
     };
-    // B fragments (weight-slice rows of the keep list) of round c0, from LDS
-    auto gather_b = [&](int c0, int n, const int16_t* kid, const T* Bt, int bp, int kfull, Raw8<T> (&fbr)[MAXC][NT]) {
+    // B fragments of the 32-neuron chunk at kc: rows kid[kc..kc+31] of the
+    // weight slice Bt (count n; kfull = the contraction length with nothing
+    // dropped; bp = the f32 slice's pitch).  Slots past the count read rows
+    // of the first chunk (their A side is zero).
+    auto load_b = [&](int kc, int n, const int16_t* kid, const T* Bt, int bp, int kfull, Raw8<T> (&fb)[NT]) {
+        const int kb = kc < n ? kc : 0;
+        if constexpr (KM) {
+            // lanes 4e..4e+3 of group g address kept row kb + 8g + e (read 0)
+            // and kb + 8g + 4 + e (read 1), at columns 0, 4, 8, 12 of a tile
+            const int j = kb + g8 + ((lane & 15) >> 2);
+            const T* p0 = Bt + (int)kid[j] * NCP + 4 * (lane & 3);
+            const T* p1 = Bt + (int)kid[j + 4] * NCP + 4 * (lane & 3);
 #pragma unroll
-        for (int i = 0; i < MAXC; ++i) {
-            const int kc = 32 * (c0 + w + NW * i);
-            if (n == kfull) {                   // identity keep list: contiguous rows
-                const int kb = kc < n ? kc : 0;
+            for (int nt = 0; nt < NT; ++nt) {
+                const uint2 lo = lds_tr4((const bf16*)(p0 + 16 * nt)), hi = lds_tr4((const bf16*)(p1 + 16 * nt));
+                fb[nt].w[0] = lo.x; fb[nt].w[1] = lo.y; fb[nt].w[2] = hi.x; fb[nt].w[3] = hi.y;
+            }
+        } else if (n == kfull) {                // identity keep list: contiguous rows
 #pragma unroll
-                for (int nt = 0; nt < NT; ++nt) raw_lds(fbr[i][nt], Bt + (size_t)(nt * 16 + (lane & 15)) * bp + kb + g8);
-            } else {
-                const int4 k8 = *(const int4*)(kid + kc + g8);          // 8 int16 keep indices
-                const int kw[4] = {k8.x, k8.y, k8.z, k8.w};
-                int kk[8];
+            for (int nt = 0; nt < NT; ++nt) raw_lds(fb[nt], Bt + (size_t)(nt * 16 + (lane & 15)) * bp + kb + g8);
+        } else {
+            const int4 k8 = *(const int4*)(kid + kc + g8);          // 8 int16 keep indices
+            const int kw[4] = {k8.x, k8.y, k8.z, k8.w};
+            int kk[8];
 #pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const int j = kc + g8 + e;
-                    kk[e] = j < n ? (int)(int16_t)(kw[e >> 1] >> (16 * (e & 1))) : 0;
-                }
+            for (int e = 0; e < 8; ++e) {
+                const int j = kc + g8 + e;
+                kk[e] = j < n ? (int)(int16_t)(kw[e >> 1] >> (16 * (e & 1))) : 0;
+            }
 #pragma unroll
-                for (int nt = 0; nt < NT; ++nt) {
-                    const T* row = Bt + (size_t)(nt * 16 + (lane & 15)) * bp;
-                    Frag<T> fb;
+            for (int nt = 0; nt < NT; ++nt) {
+                const T* row = Bt + (size_t)(nt * 16 + (lane & 15)) * bp;
+                Frag<T> f;
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) fb.v[e] = row[kk[e]];
-                    raw_from(fbr[i][nt], fb);
-                }
+                for (int e = 0; e < 8; ++e) f.v[e] = row[kk[e]];
+                raw_from(fb[nt], f);
             }
         }
+    };
+    // B fragments of round c0
+    auto gather_b = [&](int c0, int n, const int16_t* kid, const T* Bt, int bp, int kfull, Raw8<T> (&fbr)[MAXC][NT]) {
+#pragma unroll
+        for (int i = 0; i < MAXC; ++i) load_b(32 * (c0 + w + NW * i), n, kid, Bt, bp, kfull, fbr[i]);
     };
     // acc += A fragments of round c0 times the B fragments gathered for it
     auto compute_b = [&](Raw8<T> (&fa)[MAXC][MT], const Raw8<T> (&fbr)[MAXC][NT], int c0, int n,
@@ -262,28 +293,7 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
         for (int i = 0; i < MAXC; ++i) {
             const int kc = 32 * (c0 + w + NW * i);
             Raw8<T> fbr[NT];
-            if (n == kfull) {                   // identity keep list: contiguous rows
-                const int kb = kc < n ? kc : 0;
-#pragma unroll
-                for (int nt = 0; nt < NT; ++nt) raw_lds(fbr[nt], Bt + (size_t)(nt * 16 + (lane & 15)) * bp + kb + g8);
-            } else {
-                const int4 k8 = *(const int4*)(kid + kc + g8);          // 8 int16 keep indices
-                const int kw[4] = {k8.x, k8.y, k8.z, k8.w};
-                int kk[8];
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const int j = kc + g8 + e;
-                    kk[e] = j < n ? (int)(int16_t)(kw[e >> 1] >> (16 * (e & 1))) : 0;
-                }
-#pragma unroll
-                for (int nt = 0; nt < NT; ++nt) {
-                    const T* row = Bt + (size_t)(nt * 16 + (lane & 15)) * bp;
-                    Frag<T> fb;
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) fb.v[e] = row[kk[e]];
-                    raw_from(fbr[nt], fb);
-                }
-            }
+            load_b(kc, n, kid, Bt, bp, kfull, fbr);
             if (kc + 32 > n) {                  // last chunk: slots past the keep count hold stale values
                 uint32_t m[Raw8<T>::NW];
                 pad_mask<T>(kc + g8, n, m);
@@ -300,7 +310,8 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
                         f32x4_t (&acc)[MT][NT]) {
         for (int c0 = 0; c0 < (n + 31) / 32; c0 += NW * MAXC) {
             Raw8<T> fa[MAXC][MT];
-            issue(src, slot_elems, c0, fa);
+            issue(src, slot_elems, n, c0, fa);
+            __builtin_amdgcn_sched_barrier(0);  // every load before the first product
             compute(fa, c0, n, kid, Bt, bp, kfull, acc);
         }
     };
@@ -330,15 +341,15 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
     // this thread's sums over the waves' partial products (in red) of the
     // four gates of pair q
     auto red_sum = [&](int q, float* pre) {
-        const int rr = pb[q] - m0, uu = pu[q] - u0, nt = uu >> 2, cu = uu & 3;
+        const int rr = pb[q] - m0, uu = pu[q] - u0;
+        const float* r = red + rr * NC + (uu >> 2) * 16 + (uu & 3) * 4;
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-            const int cc = nt * 16 + g * 4 + cu;
-            float v = 0.f;
-#pragma unroll
-            for (int i = 0; i < NW; ++i) v += red[(i * MG + rr) * NC + cc];
-            pre[g] = v;
+        for (int i = 0; i < NW; ++i) {
+            const float4 x = *(const float4*)(r + i * MG * NC);
+            v.x += x.x; v.y += x.y; v.z += x.z; v.w += x.w;
         }
+        pre[0] = v.x; pre[1] = v.y; pre[2] = v.z; pre[3] = v.w;
     };
     auto red_store = [&](f32x4_t (&acc)[MT][NT]) {
 #pragma unroll
@@ -423,7 +434,8 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
         const T* hsrc = (const T*)D.hx + (size_t)(s & 1) * hxs;
         if (one_round) {
             Raw8<T> fh[MAXC][MT];
-            issue(hsrc, hxs, 0, fh);
+            issue(hsrc, hxs, cnt, 0, fh);
+            __builtin_amdgcn_sched_barrier(0);  // every load before the first product
             compute_b(fh, bh, 0, cnt, acc);
         } else {
             contract(hsrc, hxs, cnt, kidx, Ut, HP, H, acc);
@@ -514,14 +526,16 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
 // split over the waves; skipped when every unit of the tile was dropped),
 // then the pointwise backward (Eq. 7-9) with the dc and pass-through
 // carries held in registers.  Dynamic LDS: U rows [UB][GP] (dtype),
-// reduction [16][MG][16] (float).
+// reduction [16][MG][16] (float).  MC: chunks per wave per round, the
+// fewest that cover 4H in one round within the register budget (the loads
+// of a round are all in flight at once).
 constexpr int PB_NW = 16;
 
-template <typename T, int UB, int MG>
+template <typename T, int UB, int MG, int MC>
 __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
     constexpr int MT = MG / 16, NW = PB_NW, NTH = 64 * NW;
     constexpr int PPT = (MG * UB + NTH - 1) / NTH;
-    constexpr int MAXC = (MT <= 2 ? 6 : 2) / (sizeof(T) == 4 ? 2 : 1);   // 128 VGPRs at 1024 threads
+    constexpr int MAXC = MC;
     extern __shared__ __align__(16) char smem[];
     const int H = a.H, G = 4 * H, B = a.B, T_ = a.T;
     const int GP = (G + 31) / 32 * 32 + 8;       // row pitch; zero past 4H up to the last chunk
@@ -650,6 +664,10 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) raw_load<T, CPOL_SC1>(fa[i][mt], dr, lofs[mt] + (uint32_t)(c0 + w + NW * i) * cbytes);
             }
+            // every load of the round is issued before the first product
+            // (the scheduler would otherwise interleave them and pay the
+            // memory latency several times)
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int i = 0; i < MAXC; ++i) {
                 const int n = 32 * (c0 + w + NW * i);
@@ -1332,8 +1350,9 @@ static hipError_t resident_limit(const void* fn, int threads, size_t lds, int nw
 // products); keep lists at kofs; then the reduction area.  Returns the size.
 size_t fwd_persist_lds(int H, int NT, int MG, int esize, int KP, int kin_max, bool w_beside_u, size_t* wofs,
                        size_t* kofs) {
-    const size_t us = ((size_t)16 * NT * fwd_hp(H) * esize + 15) & ~(size_t)15;
-    const size_t ws = ((size_t)16 * NT * KP * esize + 15) & ~(size_t)15;
+    const size_t cols = esize == 2 ? (size_t)fwd_ncp(NT) : (size_t)16 * NT;   // bf16: K-major, padded rows
+    const size_t us = (cols * fwd_hp(H) * esize + 15) & ~(size_t)15;
+    const size_t ws = (cols * KP * esize + 15) & ~(size_t)15;
     *wofs = w_beside_u ? us : 0;
     *kofs = w_beside_u ? us + ws : (us > ws ? us : ws);
     const size_t kx = (size_t)(((H + 32) + 7) & ~7) * 2;
@@ -1394,9 +1413,9 @@ size_t bwd_persist_lds(int H, int UB, int MG, int esize) {
     return (((size_t)UB * GP * esize + 15) & ~(size_t)15) + (size_t)PB_NW * MG * 16 * 4;
 }
 
-template <typename T, int UB, int MG>
+template <typename T, int UB, int MG, int MC>
 static hipError_t launch_bwd_persist_t(const PBwdArgs& a, int nwg, size_t lds, hipStream_t st) {
-    auto fn = k_bwd_persist<T, UB, MG>;
+    auto fn = k_bwd_persist<T, UB, MG, MC>;
     const hipError_t e = resident_limit((const void*)fn, 64 * PB_NW, lds, nwg);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(fn, dim3(nwg), dim3(64 * PB_NW), lds, st, a);
@@ -1417,11 +1436,28 @@ hipError_t launch_bwd_persist(PBwdArgs& a, hipStream_t st, int timer_on, hipEven
     const int nwg = a.nslots * a.ntiles * a.mgroups;
     if (a.nslots > 8) return hipErrorInvalidValue;
     if (timer_on) (void)hipEventRecord(e0, st);
+    // chunks per wave per round: 128 VGPRs at 1024 threads hold 6 bf16
+    // rounds of 32-row fragments (3 f32), 2 of 64-row ones (1 f32)
+    const int nch = (4 * a.H + 31) / 32, per_wave = (nch + PB_NW - 1) / PB_NW;
     hipError_t e;
-    if (UB == 16 && MG == 32) e = launch_bwd_persist_t<T, 16, 32>(a, nwg, lds, st);
-    else if (UB == 16) e = launch_bwd_persist_t<T, 16, 64>(a, nwg, lds, st);
-    else if (MG == 32) e = launch_bwd_persist_t<T, 8, 32>(a, nwg, lds, st);
-    else e = launch_bwd_persist_t<T, 8, 64>(a, nwg, lds, st);
+    if constexpr (sizeof(T) == 4) {
+        if (UB == 16) e = MG == 32 ? launch_bwd_persist_t<T, 16, 32, 3>(a, nwg, lds, st)
+                                   : launch_bwd_persist_t<T, 16, 64, 1>(a, nwg, lds, st);
+        else e = MG == 32 ? launch_bwd_persist_t<T, 8, 32, 3>(a, nwg, lds, st)
+                          : launch_bwd_persist_t<T, 8, 64, 1>(a, nwg, lds, st);
+    } else if (MG == 64) {
+        e = UB == 16 ? launch_bwd_persist_t<T, 16, 64, 2>(a, nwg, lds, st)
+                     : launch_bwd_persist_t<T, 8, 64, 2>(a, nwg, lds, st);
+    } else if (per_wave <= 2) {
+        e = UB == 16 ? launch_bwd_persist_t<T, 16, 32, 2>(a, nwg, lds, st)
+                     : launch_bwd_persist_t<T, 8, 32, 2>(a, nwg, lds, st);
+    } else if (per_wave <= 4) {
+        e = UB == 16 ? launch_bwd_persist_t<T, 16, 32, 4>(a, nwg, lds, st)
+                     : launch_bwd_persist_t<T, 8, 32, 4>(a, nwg, lds, st);
+    } else {
+        e = UB == 16 ? launch_bwd_persist_t<T, 16, 32, 6>(a, nwg, lds, st)
+                     : launch_bwd_persist_t<T, 8, 32, 6>(a, nwg, lds, st);
+    }
     if (timer_on && e == hipSuccess) (void)hipEventRecord(e1, st);
     return e;
 }
