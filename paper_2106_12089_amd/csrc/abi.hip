@@ -192,6 +192,13 @@ static bool use_wgrad_big() {
     return !(v && v[0] == '0');
 }
 
+// LSTM_SD_GEMM_BIG=0: the input products and input gradients of a large
+// batch on the small-batch kernels
+static bool use_gemm_big() {
+    const char* v = getenv("LSTM_SD_GEMM_BIG");
+    return !(v && v[0] == '0');
+}
+
 static bool use_persistent() {
     const char* v = getenv("LSTM_SD_PERSIST");
     return !(v && v[0] == '0');
@@ -294,6 +301,8 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
     tr.h0 = h0; tr.c0 = c0; tr.hT = hT; tr.cT = cT; tr.n_init = (long)L * D * B * H;
     tr.bar = (unsigned*)(W + P.w_sync); tr.err = (int*)(W + P.w_sync + SYNC_ERR_OFS);
     bool tr_pending = true;
+    // large batches (bf16): the input products read the transposed inputs
+    const bool gemm_big = std::is_same<E, bf16>::value && B >= 64 && use_gemm_big();
     auto attach_tr = [&](FxArgs& f) {
         if (!tr_pending) return;
         f.tr = tr;
@@ -353,6 +362,11 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
             f.site = site_view(P, mbuf, P.site_nr(l));
             f.Gx = (float*)(W + P.w_gx) + (size_t)d * T * B * G;
             f.K = kin; f.B = B; f.G = G; f.T = T; f.dense = !P.compact; f.s = P.s_nr[l];
+            if (gemm_big) {
+                f.XT = l == 0 ? (const void*)(R + P.r_xT) : (const void*)(R + P.rybufT(l - 1));
+                f.xt_tstride = (long)kin * BP;
+                f.xt_ld = BP;
+            }
             attach_tr(f);
             launch_fx<E>(f, st);
         }
@@ -401,15 +415,16 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
         return false;
     };
     const bool big_first = std::is_same<E, bf16>::value && big_mode() == 2;
+    bool fx0_done = false;
     if (use_persistent() && use_stacked() && !big_first && D == 1 && L > 1 && L <= 4) {
         launch_fx_layer(0);
         if ((use_fwd_workers() && stacked(true)) || stacked(false)) return hip_check("forward launch");
-        // neither fits: one layer at a time below (layer 0's input product is done)
+        fx0_done = true;                      // neither fits: one layer at a time below
     }
     for (int l = 0; l < L; ++l) {
         const int kin = P.kin(l);
         const void* X = l == 0 ? x : (const void*)(R + P.rybuf(l - 1));
-        for (int d = 0; d < D; ++d) {
+        for (int d = 0; d < D && !(l == 0 && fx0_done); ++d) {
             FxArgs f;
             memset(&f, 0, sizeof(f));
             f.X = X; f.ldx = kin;
@@ -418,6 +433,11 @@ static int forward_impl(const Plan& P, const lstm_sd_weights* w, const void* x, 
             f.site = site_view(P, mbuf, P.site_nr(l));
             f.Gx = (float*)(W + P.w_gx) + (size_t)d * T * B * G;
             f.K = kin; f.B = B; f.G = G; f.T = T; f.dense = !P.compact; f.s = P.s_nr[l];
+            if (gemm_big) {
+                f.XT = l == 0 ? (const void*)(R + P.r_xT) : (const void*)(R + P.rybufT(l - 1));
+                f.xt_tstride = (long)kin * BP;
+                f.xt_ld = BP;
+            }
             attach_tr(f);
             launch_fx<E>(f, st);
         }
@@ -538,6 +558,7 @@ static int backward_impl(const Plan& P, const lstm_sd_weights* w, const int32_t*
         a.T = T; a.K = kin; a.tps = ((kin + 7) / 8 + 15) / 16; a.mtiles = P.mtiles;
         a.dense = !P.compact; a.s = P.s_nr[l];
         a.status = sync_status;
+        a.big = std::is_same<E, bf16>::value && B >= 64 && use_gemm_big();
         launch_dx<E>(a, kin, st);
     };
     // weight and bias gradients (Eq. 11) of layer l: its problems join one

@@ -236,6 +236,301 @@ __global__ void __launch_bounds__(512) k_wgrad_big(WgBatch bt) {
     }
 }
 
+// ---------------------------------------------------------------------------
+// Forward input product for large batches (Eq. 1-4 input term; Sec. 3.2 FP
+// input sparsity):
+//   Gx_t = s * X_t[:, keep_t] W[keep_t, :] + bias
+// grid (ceil(G/128), T, ceil(B/256)), 512 threads (8 waves).  A workgroup
+// computes a 256-row x 128-column tile of Gx_t; wave w owns rows
+// 64*(w/2) .. +63 and columns 64*(w%2) .. +63 (4 x 4 tiles of
+// 16x16x32 MFMA).  The contraction runs over the keep list of t in chunks
+// of 64 kept neurons: the gathered rows of the transposed input X_t^T
+// ([K][ld], 256 batch columns) and of W (128 columns) are staged in LDS as
+// K-major tiles (whole 16-byte pieces of each row, coalesced), double
+// buffered so that chunk i+1 is in flight while chunk i is multiplied, and
+// both operands' fragments are read with ds_read_b64_tr_b16 (lanes 4e..4e+3
+// of a 16-lane group address row e of the group's four at columns 0, 4, 8,
+// 12: lane i receives column i of the four rows).  Dropped rows of the
+// dense mode and rows past the count read as zero (an offset past the
+// buffer).  Rows past B and columns past G are computed and not stored.
+constexpr int FB_M = 256, FB_N = 128, FB_KC = 64, FB_AP = FB_M + 16, FB_BP = FB_N + 16;
+constexpr size_t FB_LDS = (size_t)2 * FB_KC * (FB_AP + FB_BP) * 2 + (size_t)(LSTM_SD_MAX_K + 2 * FB_KC) * 4;
+
+__global__ void __launch_bounds__(512) k_fx_big(FxArgs a) {
+    extern __shared__ __align__(16) char smem[];
+    bf16* As = (bf16*)smem;                                  // [2][FB_KC][FB_AP]
+    bf16* Bs = As + 2 * FB_KC * FB_AP;                       // [2][FB_KC][FB_BP]
+    int* kidx = (int*)(Bs + 2 * FB_KC * FB_BP);              // [count]
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int t = blockIdx.y, n0 = blockIdx.x * FB_N, m0 = blockIdx.z * FB_M;
+    const int K = a.K, G = a.G, B = a.B;
+    const int32_t* krow = a.site.keep + (size_t)t * a.site.kmax;
+    const uint8_t* mrow = a.site.mask + (size_t)t * a.site.kmax;
+    const int cnt = a.site.count[t];
+    // the keep list, then -1 through two chunks past the last (rows read as
+    // zero: the loop fetches two chunks ahead without a condition)
+    const int cpad = ((cnt + FB_KC - 1) / FB_KC + 2) * FB_KC;
+    for (int j = tid; j < cpad; j += 512) kidx[j] = j >= cnt || (a.dense && !mrow[j]) ? -1 : krow[j];
+    __syncthreads();
+    const __amdgpu_buffer_rsrc_t xr = buf_rsrc((const bf16*)a.XT + (size_t)t * a.xt_tstride,
+                                               (uint32_t)((size_t)K * a.xt_ld * 2));
+    const __amdgpu_buffer_rsrc_t wr = buf_rsrc(a.W, (uint32_t)((size_t)K * G * 2));
+    // staging: A rows (512 bytes of X^T) as 32 pieces, 4 per thread; B rows
+    // (256 bytes of W) as 16 pieces, 2 per thread.  Chunk j goes through
+    // register set j % 2: its loads are issued two chunks ahead, so each
+    // has two chunks' products to arrive in
+    u32x4_t ra[2][4], rb[2][2];
+    // (every row index of a chunk is read first, then its six loads go out
+    // back to back; absent rows take an offset past the buffer: no branch)
+    const uint32_t aoff = (uint32_t)(m0 + 8 * (tid & 31)) * 2, boff = (uint32_t)(n0 + 8 * (tid & 15)) * 2;
+    auto fetch = [&](int set, int kc) {
+        int ka[4], kb[2];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) ka[i] = kidx[kc + (tid >> 5) + 16 * i];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) kb[i] = kidx[kc + (tid >> 4) + 32 * i];
+        uint32_t oa[4], ob[2];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) oa[i] = ka[i] < 0 ? OOB_OFF : (uint32_t)ka[i] * (uint32_t)(a.xt_ld * 2) + aoff;
+#pragma unroll
+        for (int i = 0; i < 2; ++i) ob[i] = kb[i] < 0 ? OOB_OFF : (uint32_t)kb[i] * (uint32_t)(G * 2) + boff;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) ra[set][i] = __builtin_amdgcn_raw_buffer_load_b128(xr, oa[i], 0, 0);
+#pragma unroll
+        for (int i = 0; i < 2; ++i) rb[set][i] = __builtin_amdgcn_raw_buffer_load_b128(wr, ob[i], 0, 0);
+    };
+    auto commit = [&](int set, int buf) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int q = tid + 512 * i, r = q >> 5, c = q & 31;
+            *(u32x4_t*)(As + ((size_t)buf * FB_KC + r) * FB_AP + 8 * c) = ra[set][i];
+        }
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int q = tid + 512 * i, r = q >> 4, c = q & 15;
+            *(u32x4_t*)(Bs + ((size_t)buf * FB_KC + r) * FB_BP + 8 * c) = rb[set][i];
+        }
+    };
+    f32x4_t acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0, 0, 0, 0};
+    const int wr0 = 64 * (w >> 1), wc0 = 64 * (w & 1);
+    const int trow = 8 * (lane >> 4) + ((lane & 15) >> 2), tcol = 4 * (lane & 3);
+    const int nch = (cnt + FB_KC - 1) / FB_KC;
+    fetch(0, 0);
+    fetch(1, FB_KC);
+    commit(0, 0);
+    __syncthreads();
+    // chunk ch (in LDS buffer ch % 2): the loads of ch+2 go out, the
+    // products of ch, then ch+1 (loaded during ch-1) into the other buffer
+    // (fetch and commit run unconditionally, past the end on zero rows: a
+    // conditional load leaves the compiler unsure which loads are still in
+    // flight, and it then waits for all of them before the next fetch)
+    auto chunk = [&](int ch, int cur) {
+        fetch(cur, (ch + 2) * FB_KC);
+        __builtin_amdgcn_sched_barrier(0);     // (the loads go out before anything waits)
+        const int buf = cur;
+        const bf16* Ab = As + (size_t)buf * FB_KC * FB_AP;
+        const bf16* Bb = Bs + (size_t)buf * FB_KC * FB_BP;
+#pragma unroll
+        for (int ks = 0; ks < FB_KC / 32; ++ks) {
+            Raw8<bf16> fa[4], fb[4];
+            const bf16* a0 = Ab + (size_t)(32 * ks + trow) * FB_AP + wr0 + tcol;
+            const bf16* b0 = Bb + (size_t)(32 * ks + trow) * FB_BP + wc0 + tcol;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const uint2 lo = lds_tr4(a0 + 16 * i), hi = lds_tr4(a0 + 4 * FB_AP + 16 * i);
+                fa[i].w[0] = lo.x; fa[i].w[1] = lo.y; fa[i].w[2] = hi.x; fa[i].w[3] = hi.y;
+                const uint2 lb = lds_tr4(b0 + 16 * i), hb = lds_tr4(b0 + 4 * FB_BP + 16 * i);
+                fb[i].w[0] = lb.x; fb[i].w[1] = lb.y; fb[i].w[2] = hb.x; fb[i].w[3] = hb.y;
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) raw_mma(fa[i], fb[j], acc[i][j]);
+        }
+        commit(cur ^ 1, cur ^ 1);
+        __syncthreads();
+    };
+    // (pairs with both calls unconditional: the register sets' states agree
+    // at the top of every iteration)
+    int ch = 0;
+    for (; ch + 1 < nch; ch += 2) {
+        chunk(ch, 0);
+        chunk(ch + 1, 1);
+    }
+    if (ch < nch) chunk(ch, 0);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int n = n0 + wc0 + 16 * j + (lane & 15);
+        if (n >= G) continue;
+        const float bn = a.bias[n];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int row = m0 + wr0 + 16 * i + acc_row(lane, r);
+                if (row < B) a.Gx[((size_t)t * B + row) * G + n] = a.s * acc[i][j][r] + bn;
+            }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Output-sparse input gradient for large batches (Eq. 10), summed over the
+// directions:
+//   dX_t[:, keep_t[j]] = s * sum_d DA_{d,t} W_d[keep_t[j], :]^T
+// grid (8 * ceil(T/8) * ceil(K/128), 1, ceil(B/256)), 512 threads: workgroup i
+// runs on XCD i % 8, which takes the steps t = i % 8 + 8j with all their
+// column tiles, so DA_t is fetched into one XCD's L2 once.  A workgroup
+// computes 256 rows x the 128 kept columns at keep-list positions 128*x ..
+// (and, with
+// scatter, writes the zeros of the dropped columns at drop-list positions
+// 128*x ..); wave w owns rows 64*(w/2) and columns 64*(w%2) (4 x 4 tiles of
+// 16x16x32 MFMA).  The contraction over 4H runs in chunks of 64: the DA
+// chunk (fragment-major in memory: the MFMA operand layout) is copied to LDS
+// as 1 KB blocks, the 128 gathered W rows' 64-column pieces are staged as
+// [128][64+8] rows, double buffered, with the loads issued two chunks
+// ahead; every fragment is one 16-byte LDS read.
+constexpr int DB_M = 256, DB_N = 128, DB_KC = 64, DB_BP = DB_KC + 8;
+constexpr size_t DB_LDS = (size_t)2 * (DB_M * DB_KC + DB_N * DB_BP) * 2 + (size_t)DB_N * 4;
+
+__global__ void __launch_bounds__(512) k_dx_big(DxArgs a) {
+    extern __shared__ __align__(16) char smem[];
+    bf16* As = (bf16*)smem;                                  // [2][2 chunks][16 tiles][64 lanes][8]
+    bf16* Bs = As + 2 * DB_M * DB_KC;                        // [2][DB_N][DB_BP]
+    int* kcol = (int*)(Bs + 2 * DB_N * DB_BP);               // [DB_N] W rows of the tile's columns
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int ntile = (a.K + DB_N - 1) / DB_N;
+    const int xcd = blockIdx.x % 8, idx = blockIdx.x / 8;
+    const int t = xcd + 8 * (idx / ntile), j0 = (idx % ntile) * DB_N, m0 = blockIdx.z * DB_M;
+    if (t >= a.T) return;
+    const int B = a.B, G = a.G;
+    const bool failed = a.status && *a.status != 0;
+    const int cnt = a.site.count[t];
+    const int32_t* krow = a.site.keep + (size_t)t * a.site.kmax;
+    const uint8_t* mrow = a.site.mask + (size_t)t * a.site.kmax;
+    float* out = a.out + (size_t)t * B * a.ldo;
+    if (a.scatter) {                           // the dropped columns of this tile's drop-list range
+        const int dn = a.site.dcount[t];
+        const int32_t* drow = a.site.drop + (size_t)t * a.site.kmax;
+        for (int i = tid; i < DB_N * DB_M; i += 512) {
+            const int jj = j0 + (i % DB_N), row = m0 + i / DB_N;
+            if (jj < dn && row < B) out[(size_t)row * a.ldo + drow[jj]] = failed ? __builtin_nanf("") : 0.0f;
+        }
+    }
+    if (j0 >= cnt) return;
+    if (tid < DB_N) kcol[tid] = j0 + tid < cnt ? krow[j0 + tid] : -1;
+    __syncthreads();
+    const int mt0 = m0 / 16;                   // first 16-row tile of the workgroup
+    const size_t das = (size_t)((G + 31) / 32) * a.mtiles * 512;
+    const int wr0 = 64 * (w >> 1), wc0 = 64 * (w & 1);
+    const int g8 = 8 * (lane >> 4), cl = lane & 15;
+    f32x4_t acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0, 0, 0, 0};
+    const int nch = (G + DB_KC - 1) / DB_KC;
+    for (int d = 0; d < a.D; ++d) {
+        const __amdgpu_buffer_rsrc_t dr = buf_rsrc((const bf16*)a.da[d] + (size_t)t * das, (uint32_t)(das * 2));
+        const __amdgpu_buffer_rsrc_t wr = buf_rsrc(a.W[d], (uint32_t)((size_t)a.K * G * 2));
+        // staging: A = 2 chunks x 16 tiles of 1 KB (4 pieces per thread),
+        // B = 128 rows x 8 pieces of 16 bytes (2 per thread); chunk c goes
+        // through register set c % 2, its loads issued two chunks ahead
+        u32x4_t ra[2][4], rb[2][2];
+        auto fetch = [&](int set, int c) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int q = tid + 512 * i, blk = q >> 6, l = q & 63;   // blk = chunk half * 16 + tile
+                const int ck = 2 * c + (blk >> 4), mt = mt0 + (blk & 15);
+                const bool ok = mt < a.mtiles && 32 * ck < G;
+                ra[set][i] = __builtin_amdgcn_raw_buffer_load_b128(
+                    dr, ok ? (uint32_t)(frag_lane_off(ck, mt, l, a.mtiles) * 2) : OOB_OFF, 0, 0);
+            }
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const int q = tid + 512 * i, r = q >> 3, pc = q & 7;
+                const int k = kcol[r], g = DB_KC * c + 8 * pc;
+                rb[set][i] = __builtin_amdgcn_raw_buffer_load_b128(
+                    wr, (k >= 0 && g < G) ? (uint32_t)(((size_t)k * G + g) * 2) : OOB_OFF, 0, 0);
+            }
+        };
+        auto commit = [&](int set, int buf) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int q = tid + 512 * i;
+                *(u32x4_t*)(As + (size_t)buf * DB_M * DB_KC + (size_t)q * 8) = ra[set][i];
+            }
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const int q = tid + 512 * i, r = q >> 3, pc = q & 7;
+                *(u32x4_t*)(Bs + ((size_t)buf * DB_N + r) * DB_BP + 8 * pc) = rb[set][i];
+            }
+        };
+        fetch(0, 0);
+        fetch(1, 1);
+        __syncthreads();                       // (the previous direction's last chunk is read)
+        commit(0, 0);
+        __syncthreads();
+        auto chunk = [&](int c, int cur) {
+            fetch(cur, c + 2);                 // (past the end: zeros, unconditionally)
+            __builtin_amdgcn_sched_barrier(0);
+            const int buf = cur;
+            const bf16* Ab = As + (size_t)buf * DB_M * DB_KC;
+            const bf16* Bb = Bs + (size_t)buf * DB_N * DB_BP;
+#pragma unroll
+            for (int ks = 0; ks < DB_KC / 32; ++ks) {
+                Raw8<bf16> fa[4], fb[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    raw_lds(fa[i], Ab + ((size_t)(ks * 16 + (wr0 >> 4) + i) * 64 + lane) * 8);
+                    raw_lds(fb[i], Bb + (size_t)(wc0 + 16 * i + cl) * DB_BP + 32 * ks + g8);
+                }
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) raw_mma(fa[i], fb[j], acc[i][j]);
+            }
+            commit(cur ^ 1, cur ^ 1);
+            __syncthreads();
+        };
+        int c = 0;
+        for (; c + 1 < nch; c += 2) {
+            chunk(c, 0);
+            chunk(c + 1, 1);
+        }
+        if (c < nch) chunk(c, 0);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int jl = wc0 + 16 * j + cl, jj = j0 + jl;
+        if (jj >= cnt) continue;
+        const int kk = kcol[jl];                 // (a kept column: a valid row)
+        const float sc = (a.dense && !mrow[kk]) ? 0.0f : a.s;
+        const int oc = a.scatter ? kk : jj;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int row = m0 + wr0 + 16 * i + acc_row(lane, r);
+                if (row < B) out[(size_t)row * a.ldo + oc] = failed ? __builtin_nanf("") : sc * acc[i][j][r];
+            }
+    }
+}
+
+void launch_fx_big(const FxArgs& a, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
+    const dim3 grid((a.G + FB_N - 1) / FB_N, a.T, (a.B + FB_M - 1) / FB_M), blk(512);
+    if (e0 && e1) hipExtLaunchKernelGGL(k_fx_big, grid, blk, (uint32_t)FB_LDS, st, e0, e1, 0, a);
+    else k_fx_big<<<grid, blk, FB_LDS, st>>>(a);
+}
+void launch_dx_big(const DxArgs& a, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
+    const dim3 grid(8 * ((a.T + 7) / 8) * ((a.K + DB_N - 1) / DB_N), 1, (a.B + DB_M - 1) / DB_M), blk(512);
+    if (e0 && e1) hipExtLaunchKernelGGL(k_dx_big, grid, blk, (uint32_t)DB_LDS, st, e0, e1, 0, a);
+    else k_dx_big<<<grid, blk, DB_LDS, st>>>(a);
+}
+
 size_t wgrad_big_lds() { return (size_t)(WB_R + 1) * WB_LDC * 4 + (size_t)8 * 2 * WB_R * 4; }
 
 // The large-batch weight gradient takes any batch (its loads run two
@@ -252,8 +547,13 @@ void launch_wgrad_big(const WgBatch& b, hipStream_t st, hipEvent_t e0, hipEvent_
 }
 
 int setup_big_attributes() {
-    return hipFuncSetAttribute((const void*)k_wgrad_big, hipFuncAttributeMaxDynamicSharedMemorySize,
-                               (int)wgrad_big_lds()) == hipSuccess ? 0 : -1;
+    bool ok = hipFuncSetAttribute((const void*)k_wgrad_big, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                  (int)wgrad_big_lds()) == hipSuccess;
+    ok = hipFuncSetAttribute((const void*)k_fx_big, hipFuncAttributeMaxDynamicSharedMemorySize, (int)FB_LDS) ==
+             hipSuccess && ok;
+    ok = hipFuncSetAttribute((const void*)k_dx_big, hipFuncAttributeMaxDynamicSharedMemorySize, (int)DB_LDS) ==
+             hipSuccess && ok;
+    return ok ? 0 : -1;
 }
 
 }  // namespace lsd

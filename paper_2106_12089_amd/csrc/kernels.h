@@ -69,6 +69,9 @@ struct FxArgs {
     float* Gx;                          // [T][B][G]
     int B, G, T, dense;
     float s;
+    // the input transposed, XT + t*xt_tstride + k*xt_ld + b, bf16: when set
+    // (batch >= 64), the large-batch kernel runs (after the transposes)
+    const void* XT; long xt_tstride; int xt_ld;
     // with tr_gz > 0, the launch also runs the transposes (and the pass
     // initialisation) of tr, as a virtual (tr_gx, tr_gy, tr_gz) grid of
     // workgroups past y = T; trN = its matrix count
@@ -150,6 +153,7 @@ struct DxArgs {
     int D, B, G, ldo, T, K, tps, dense, mtiles;
     float s;
     const int* status;                  // sticky barrier status of the step, or null: when set, NaN is written
+    int big;                            // bf16, batch >= 64: the large-batch kernel
 };
 
 // Weight gradient of one (layer, direction, site), summed over every step:

@@ -1659,8 +1659,25 @@ static inline int nblk(long n, int bs, int cap = 4096) {
 void launch_mask_build(const MaskArgs& a, int sites, hipStream_t st) {
     launch_k(KID_MASK, k_mask_build, dim3(a.T, sites), dim3(256), 0, st, a);
 }
+void launch_fx_big(const FxArgs& a, hipStream_t st, hipEvent_t e0, hipEvent_t e1);
+void launch_dx_big(const DxArgs& a, hipStream_t st, hipEvent_t e0, hipEvent_t e1);
+
+// the transposes (and the pass initialisation) of FxArgs::tr on their own
+template <typename T>
+__global__ void __launch_bounds__(256) k_trans(FxArgs a) {
+    __shared__ T tile[32][33];
+    transpose_block<T>(a.tr, a.trN, blockIdx.x, blockIdx.y, blockIdx.z, a.tr_gx, a.tr_gy, tile);
+}
+
 template <typename T>
 void launch_fx(const FxArgs& a, hipStream_t st) {
+    if (sizeof(T) == 2 && a.XT) {              // large batch: the transposed input feeds the product
+        if (a.tr_gz > 0) launch_k(KID_TRANS, k_trans<T>, dim3(a.tr_gx, a.tr_gy, a.tr_gz), dim3(256), 0, st, a);
+        hipEvent_t e0 = nullptr, e1 = nullptr;
+        if (g_timer_kid == KID_FX) { e0 = timer_event(); e1 = timer_event(); }
+        launch_fx_big(a, st, e0, e1);
+        return;
+    }
     dim3 grid(xcd_grid((a.G + FX_NB - 1) / FX_NB), a.T, (a.B + FX_MB - 1) / FX_MB);
     if (a.tr_gz > 0) {                         // room for the transposes past y = T
         const long ntr = (long)a.tr_gx * a.tr_gy * a.tr_gz, per_y = (long)grid.x * grid.z;
@@ -1683,6 +1700,12 @@ void launch_bwd(const BwdArgs& a, int D, hipStream_t st) {
 }
 template <typename T>
 void launch_dx(const DxArgs& a, int K, hipStream_t st) {
+    if (sizeof(T) == 2 && a.big) {
+        hipEvent_t e0 = nullptr, e1 = nullptr;
+        if (g_timer_kid == KID_DX) { e0 = timer_event(); e1 = timer_event(); }
+        launch_dx_big(a, st, e0, e1);
+        return;
+    }
     const dim3 grid(NXCD * a.tps, a.T, (a.B + 63) / 64);
     if (a.B <= 16) launch_k(KID_DX, k_dx<T, 1>, grid, dim3(256), 0, st, a);
     else if (a.B <= 32) launch_k(KID_DX, k_dx<T, 2>, grid, dim3(256), 0, st, a);

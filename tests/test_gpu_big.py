@@ -1,5 +1,7 @@
-"""The large-batch persistent forward (U slice held in registers, the
-contraction split over the waves and summed through LDS) on ragged shapes,
+"""The large-batch kernels (the persistent forward with its U slice held in
+registers, the contraction split over the waves and summed through LDS; the
+input products, input gradients and weight gradients on 256-row tiles) on
+ragged shapes,
 forced with LSTM_SD_BIG=2 (it otherwise runs only where the row-group
 tiling of the other persistent forward does not fit, as at the stress
 shape): hidden sizes that are not multiples of the 32-neuron chunk or of the
@@ -36,6 +38,7 @@ def _run(cfg, wl, p_nr, p_rh, compact):
     dict(num_layers=1, num_dirs=2, input_dim=129, hidden=100, batch=19, seq_len=4),
     dict(num_layers=2, num_dirs=1, input_dim=64, hidden=1000, batch=130, seq_len=3),
     dict(num_layers=1, num_dirs=1, input_dim=33, hidden=512, batch=64, seq_len=6, min_len=0),
+    dict(num_layers=2, num_dirs=2, input_dim=200, hidden=72, batch=300, seq_len=3),
 ])
 @pytest.mark.parametrize("mode", [(0.5, 0.5, 1), (0.5, 0.5, 0), (0.3, 0.0, 1)])
 def test_big_forward_ragged(shape, mode, monkeypatch):
