@@ -1,10 +1,10 @@
-// Products of the step at large batches (gfx950, bf16): the weight
-// gradients (Eq. 11) as a contraction over the batch on 32x32x16 MFMA tiles.
-// At a batch of a few hundred rows the contraction is long enough for the
-// products to be bound by MFMA and cache bandwidth, so these kernels keep
-// their accumulators in registers over the batch and feed the MFMAs from
-// loads issued several contraction steps ahead, where the small-batch
-// kernels (one contraction chunk per step) are bound by per-step latency.
+// Products of the step at large batches (gfx950, bf16, 64 rows or more): the
+// weight gradients (Eq. 11), the input products (Eq. 1-4) and the input
+// gradients (Eq. 10).  At a batch of a few hundred rows every product is a
+// large GEMM over gathered rows, so these kernels stage operand chunks in LDS
+// for a whole workgroup (8 waves on a 128- or 256-row tile), with the loads
+// issued two chunks ahead, where the small-batch kernels (one contraction
+// chunk per step, operands straight from the cache) are bound by latency.
 #include <hip/hip_runtime.h>
 #include <hip/hip_ext.h>
 
@@ -16,223 +16,232 @@
 
 namespace lsd {
 
-typedef float f32x16_t __attribute__((ext_vector_type(16)));
-
-// Operand fragment of v_mfma_f32_32x32x16_bf16: lane l holds row (A) or
-// column (B) l % 32 and contraction elements 8*(l/32) .. 8*(l/32)+7 of a
-// 16-long step; result element i of lane l is row 8*(i/4) + 4*(l/32) + i%4,
-// column l % 32.
-__device__ __forceinline__ int acc32_row(int lane, int i) { return 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3); }
 
 // ---------------------------------------------------------------------------
 // Weight gradient for large batches, Eq. 11:
-//   dW[k][n] = s * sum_t sum_{b} act_t[b][k] da_t[b][n]   over the steps t
-// at which row k is kept (row-sparse), or every step with the mask as a
-// multiplier (the dense comparison mode); rows never kept are 0.
-// grid (row slices of 128 x column blocks of 128, 1, problems), 512 threads.
-// Per step the workgroup lists the kept rows of its slice (a ballot over the
-// mask bytes), wave w multiplies the kept-row tiles rp, rp+2 (rp = w/4) of
-// 32 rows with column tile w%4 of 32 columns over the batch (16-long MFMA
-// steps, operands loaded two 64-row groups ahead across step boundaries), and adds
-// the tiles into the slice's rows of an LDS accumulator (kept rows of one
-// step are distinct; absent tile rows go to a spare row).  Slice 0 also sums
-// the bias gradient.  One launch covers every problem of a pass.
-constexpr int WB_R = 128, WB_C = 128, WB_LDC = WB_C + 4;
+//   dW[k][n] = s * sum_t sum_{b} act_t[b][k] da_t[b][n]
+// over the steps t at which row k is kept (row-sparse), or every step with
+// the mask as a multiplier (the dense comparison mode); rows never kept are
+// 0.  grid (row slices of 128 x column blocks of 128, 1, problems), 512
+// threads (8 waves); workgroup i runs on XCD i % 8, which takes the column
+// blocks x, x+8, ... with every row slice, so one XCD's L2 holds its
+// columns' DA^T of a step once for all of its slices.
+// At each step the kept rows of the slice are listed in ascending order (a
+// ballot over the mask bytes), and the contraction over the batch runs in
+// chunks of 64 batch rows: the chunk of the listed rows of act_t^T ([K][BP])
+// and of the block's 128 columns of DA_t^T ([G][BP]) are staged in LDS as
+// [row][64+8] tiles (whole 16-byte pieces of each row), double buffered,
+// with the loads issued two chunks ahead across step boundaries.  The
+// step's product (listed rows x 128 columns) is tiled in 16x16 MFMA tiles:
+// wave w takes the columns 32*(w%4) .. +31 and the row tiles w/4, w/4+2,
+// .. (those past the listed count are skipped), and at the end of the step
+// adds its tiles into the slice's rows of an LDS accumulator (the rows of
+// one step are distinct; the positions past the count go to a spare row).
+// Slice 0 also sums the bias gradient.  One launch covers every problem of
+// a pass.
+constexpr int WL_R = 128, WL_C = 128, WL_KC = 64, WL_P = WL_KC + 8, WL_LDC = WL_C + 4;
+constexpr size_t WL_LDS = (size_t)(WL_R + 1) * WL_LDC * 4 + (size_t)2 * (WL_R + WL_C) * WL_P * 2 +
+                          (size_t)4 * 2 * WL_R * 4 + 64;
 
 __global__ void __launch_bounds__(512) k_wgrad_big(WgBatch bt) {
     extern __shared__ __align__(16) char smem[];
     const WgArgs& a = bt.p[blockIdx.z];
-    const int nrs = (a.K + WB_R - 1) / WB_R, ncb = (a.G + WB_C - 1) / WB_C;
-    // workgroup i runs on XCD i % 8: each XCD takes the column blocks
-    // x, x+8, ... with every row slice, so one XCD's L2 holds its columns'
-    // DA^T of a step once for all of its slices (column blocks across XCDs
-    // would make every XCD read all of DA^T)
+    const int nrs = (a.K + WL_R - 1) / WL_R, ncb = (a.G + WL_C - 1) / WL_C;
     const int xcd = blockIdx.x % 8, k8 = blockIdx.x / 8;
     const int rs = k8 % nrs, cb = xcd + 8 * (k8 / nrs);
     if (cb >= ncb) return;
-    const int r0 = rs * WB_R, nrow = min(WB_R, a.K - r0), n0 = cb * WB_C;
-    float* acc_lds = (float*)smem;                                // [WB_R + 1][WB_LDC]
-    const int tid = threadIdx.x, lane = tid & 63;
-    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-    int* rowlist = (int*)(smem + (size_t)(WB_R + 1) * WB_LDC * 4) + w * 2 * WB_R;   // [2][WB_R] per wave
-    const int rp = w >> 2, ct = w & 3;
+    const int r0 = rs * WL_R, nrow = min(WL_R, a.K - r0), n0 = cb * WL_C;
+    float* acc_lds = (float*)smem;                                        // [WL_R + 1][WL_LDC]
+    bf16* As = (bf16*)(smem + (size_t)(WL_R + 1) * WL_LDC * 4);           // [2][WL_R][WL_P]
+    bf16* Bs = As + 2 * WL_R * WL_P;                                      // [2][WL_C][WL_P]
+    int* lrow = (int*)(Bs + 2 * WL_C * WL_P);                             // [4][WL_R] rows to load (-1: zero)
+    int* trow = lrow + 4 * WL_R;                                          // [4][WL_R] accumulator rows
+    int* lcount = trow + 4 * WL_R;                                        // [4]
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int B = a.B, G = a.G, T_ = a.T;
+    const int nb = (B + WL_KC - 1) / WL_KC, nq = T_ * nb;               // chunks per step, in all
     const bool failed = bt.status && *bt.status != 0;
-    for (int i = tid; i < (WB_R + 1) * WB_LDC; i += 512) acc_lds[i] = 0.0f;
-    __syncthreads();
+    for (int i = tid; i < (WL_R + 1) * WL_LDC; i += 512) acc_lds[i] = 0.0f;
 
-    const int ncol = n0 + 32 * ct + (lane & 31);                  // this lane's B column
-    const uint32_t boff = (uint32_t)(min(ncol, G - 1) * a.BP + 32 * (lane >> 5)) * 2;   // this lane's DA^T row and half
-    const bool dbw = a.db && rs == 0 && rp == 0;                  // sums the bias gradient
-    float dbacc = 0.0f;
-
-    // mask bytes of the slice's rows r0 + lane and r0 + 64 + lane at step t
-    // (clamped, valid addresses; loaded a step before they are used)
-    auto mask_load = [&](int t, uint32_t& k0, uint32_t& k1) {
+    // the row list of step t into ring slot t % 4 (wave 0; mask bytes of
+    // the step in mk0 / mk1): compact mode lists the kept rows of the slice
+    // in ascending order, then -1 (loaded as zero, added into the spare
+    // row); dense mode lists every row, a dropped one loaded as zero
+    auto mask_load = [&](int t, uint32_t& mk0, uint32_t& mk1) {
         const uint8_t* mrow = a.site.mask + (size_t)min(t, T_ - 1) * a.site.kmax + r0;
-        k0 = mrow[min(lane, nrow - 1)];
-        k1 = mrow[min(lane + 64, nrow - 1)];
+        mk0 = mrow[min(lane, nrow - 1)];
+        mk1 = mrow[min(lane + 64, nrow - 1)];
     };
-    // the rows of a step from its mask bytes: kept rows of the slice in
-    // ascending order (compact mode) or every row (dense mode); returns the
-    // count
-    auto build = [&](uint32_t mk0, uint32_t mk1, int* rl) -> int {
-        const bool k0 = lane < nrow && mk0 != 0;
-        const bool k1 = lane + 64 < nrow && mk1 != 0;
+    auto build = [&](int t, uint32_t mk0, uint32_t mk1) {
+        int* lr = lrow + (t & 3) * WL_R;
+        int* tr = trow + (t & 3) * WL_R;
+        const bool k0 = t < T_ && lane < nrow && mk0 != 0;
+        const bool k1 = t < T_ && lane + 64 < nrow && mk1 != 0;
         if (a.dense) {
-            rl[lane] = r0 + min(lane, nrow - 1);
-            rl[lane + 64] = r0 + min(lane + 64, nrow - 1);
-            return nrow;
+            lr[lane] = k0 ? r0 + lane : -1;
+            lr[lane + 64] = k1 ? r0 + 64 + lane : -1;
+            tr[lane] = lane < nrow ? lane : WL_R;
+            tr[lane + 64] = lane + 64 < nrow ? lane + 64 : WL_R;
+            if (lane == 0) lcount[t & 3] = t < T_ ? nrow : 0;
+            return;
         }
         const uint64_t b0 = __builtin_amdgcn_ballot_w64(k0), b1 = __builtin_amdgcn_ballot_w64(k1);
-        const int c0 = __popcll(b0);
+        const int c0 = __popcll(b0), n = c0 + __popcll(b1);
         const int i0 = __builtin_amdgcn_mbcnt_hi((uint32_t)(b0 >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)b0, 0));
         const int i1 = c0 + __builtin_amdgcn_mbcnt_hi((uint32_t)(b1 >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)b1, 0));
-        if (k0) rl[i0] = r0 + lane;
-        if (k1) rl[i1] = r0 + 64 + lane;
-        return c0 + __popcll(b1);
+        if (k0) { lr[i0] = r0 + lane; tr[i0] = lane; }
+        if (k1) { lr[i1] = r0 + 64 + lane; tr[i1] = 64 + lane; }
+        if (n + lane < WL_R) { lr[n + lane] = -1; tr[n + lane] = WL_R; }
+        if (n + 64 + lane < WL_R) { lr[n + 64 + lane] = -1; tr[n + 64 + lane] = WL_R; }
+        if (lane == 0) lcount[t & 3] = n;
     };
     auto act_ptr = [&](int t) {
         return (a.actT_first && t == a.t_first) ? (const bf16*)a.actT_first
                                                 : (const bf16*)a.actT + (long)(t + a.shift) * a.tstride;
     };
-
-    // The contraction over the batch runs in groups of 64 batch rows (one
-    // 128-byte line of an operand row): MFMA step j (0..3) of group g takes,
-    // on lane half h, the 8 batch rows 64g + 32h + 8j (the order inside a
-    // group only has to agree between the two operands), so the four steps'
-    // loads of a lane read 64 contiguous bytes and a row's line is used up
-    // by one group.  Flattened pipeline over q = t * ng + g, two groups of
-    // operands in flight: slot q & 1 holds group q, and receives q + 2 (of
-    // step t or t+1) once q is multiplied.  Loads are unconditional (clamped
-    // q; rows of absent tiles point at one row), so the compiler keeps exact
-    // wait counts.  The row lists of two steps are kept: cur (step t) and nxt
-    // (t+1); the list of t+2 is built once t is done.
-    struct Rows { int n; uint32_t ao[2]; uint32_t dm[2]; };     // ao: A row and lane-half byte offsets
-    auto prep = [&](int t, uint32_t mk0, uint32_t mk1, Rows& R) {
-        int* rl = rowlist + (t & 1) * WB_R;
-        R.n = __builtin_amdgcn_readfirstlane(build(mk0, mk1, rl));
-        // (wave-local LDS: the writes above come before the reads below in program order)
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int j = 32 * (rp + 2 * i) + (lane & 31);
-            const int r = j < R.n ? rl[j] : r0;
-            R.ao[i] = (uint32_t)r * a.BP * 2 + (uint32_t)(32 * (lane >> 5)) * 2;
-            // dense mode: the mask byte of row r0 + j sits in lane j % 64
-            const uint32_t mj = (uint32_t)__shfl((int)(j < 64 ? mk0 : mk1), j & 63);
-            R.dm[i] = a.dense ? (uint32_t)(mj != 0) : 1u;
+    // lists are built three steps ahead: with one chunk per step the loads
+    // of step t+2 go out during step t, before its list would otherwise be
+    // built
+    uint32_t mk0 = 0, mk1 = 0;
+    if (w == 0) {
+        for (int t = 0; t < 3; ++t) {
+            mask_load(t, mk0, mk1);
+            build(t, mk0, mk1);
         }
-    };
-    const int ng = (B + 63) / 64;                                 // 64-row groups of the batch
-    u32x4_t fa[2][4][2], fb[2][4];
-    auto issue = [&](int q, const Rows& R, u32x4_t (&fa_)[4][2], u32x4_t (&fb_)[4]) {
-        const int t = min(q / ng, T_ - 1), g = q % ng;
-        const __amdgpu_buffer_rsrc_t ar = buf_rsrc(act_ptr(t), (uint32_t)a.K * a.BP * 2);
-        const __amdgpu_buffer_rsrc_t br = buf_rsrc((const bf16*)a.daT + (size_t)t * G * a.BP, (uint32_t)G * a.BP * 2);
-        const uint32_t gb = (uint32_t)(128 * g);                  // the group's bytes within a row
-        const uint32_t bo = boff + gb, ao0 = R.ao[0] + gb, ao1 = R.ao[1] + gb;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            fa_[j][0] = __builtin_amdgcn_raw_buffer_load_b128(ar, ao0 + 16 * j, 0, 0);
-            fa_[j][1] = __builtin_amdgcn_raw_buffer_load_b128(ar, ao1 + 16 * j, 0, 0);
-            fb_[j] = __builtin_amdgcn_raw_buffer_load_b128(br, bo + 16 * j, 0, 0);
-        }
-    };
-
-    f32x16_t acc[2];
-    Rows cur, nxt;
-    uint32_t mk0, mk1;                                            // mask bytes of step t+2, in flight
-    mask_load(0, mk0, mk1);
-    prep(0, mk0, mk1, cur);
-    mask_load(1, mk0, mk1);
-    prep(min(1, T_ - 1), mk0, mk1, nxt);
-    mask_load(2, mk0, mk1);
-    issue(0, cur, fa[0], fb[0]);
-    issue(1, ng > 1 ? cur : nxt, fa[1], fb[1]);
-    for (int q0 = 0; q0 < T_ * ng; q0 += 2) {
-#pragma unroll
-        for (int sl = 0; sl < 2; ++sl) {
-            const int q = q0 + sl;
-            if (q >= T_ * ng) break;
-            const int t = q / ng, g = q % ng;
-            if (g == 0) {
-#pragma unroll
-                for (int i = 0; i < 2; ++i) acc[i] = f32x16_t{};
-            }
-            const bool act0 = 32 * rp < cur.n, act1 = 32 * (rp + 2) < cur.n;   // (uniform) tiles with kept rows
-            const bool pad = 64 * (g + 1) > B;                    // batch rows past B in this group
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                u32x4_t b = fb[sl][j];
-                u32x4_t av0 = fa[sl][j][0], av1 = fa[sl][j][1];
-                if (pad) {
-                    uint32_t m[4];
-                    pad_mask<bf16>(64 * g + 32 * (lane >> 5) + 8 * j, B, m);
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) { b[e] &= m[e]; av0[e] &= m[e]; av1[e] &= m[e]; }
-                }
-                if (dbw && ncol < G) {
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) dbacc += __uint_as_float(b[e] << 16) + __uint_as_float(b[e] & 0xffff0000u);
-                }
-                const bf16x8_t bv = __builtin_bit_cast(bf16x8_t, b);
-                if (act0) {
-                    const u32x4_t x = cur.dm[0] ? av0 : u32x4_t{0, 0, 0, 0};   // dense mode: a dropped row
-                    acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, x), bv, acc[0], 0, 0, 0);
-                }
-                if (act1) {
-                    const u32x4_t x = cur.dm[1] ? av1 : u32x4_t{0, 0, 0, 0};
-                    acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, x), bv, acc[1], 0, 0, 0);
-                }
-            }
-            const bool last = g == ng - 1;
-            // group q + 2 belongs to step t (cur) or t+1 (nxt); q + 2 of step
-            // t+2 only when ng == 1, in which case it is issued after the
-            // lists advance below
-            if (ng > 1) issue(q + 2, (q + 2) / ng == t ? cur : nxt, fa[sl], fb[sl]);
-            if (last) {
-                // the tiles of step t into their rows of the accumulator.  A
-                // row's compacted position, and so the wave that adds it,
-                // changes from step to step: every wave's additions of step
-                // t-1 are complete before any of step t begins.  Within a
-                // step the rows of the tiles are distinct (absent ones go to
-                // the spare row), so all old values are read before any is
-                // written.
-                __syncthreads();
-                const int* rl = rowlist + (t & 1) * WB_R;
-#pragma unroll
-                for (int i = 0; i < 2; ++i) {
-                    if (!(i == 0 ? act0 : act1)) continue;
-                    const int tb = 32 * (rp + 2 * i);
-                    float* dst[16];
-                    float old[16];
-#pragma unroll
-                    for (int e = 0; e < 16; ++e) {
-                        const int jj = tb + acc32_row(lane, e);
-                        const int r = jj < cur.n ? rl[min(jj, WB_R - 1)] - r0 : WB_R;
-                        dst[e] = acc_lds + r * WB_LDC + 32 * ct + (lane & 31);
-                    }
-#pragma unroll
-                    for (int e = 0; e < 16; ++e) old[e] = *dst[e];
-#pragma unroll
-                    for (int e = 0; e < 16; ++e) *dst[e] = old[e] + a.s * acc[i][e];
-                }
-                cur = nxt;
-                if (t + 2 < T_) prep(t + 2, mk0, mk1, nxt);       // (the list of t is no longer read)
-                mask_load(t + 3, mk0, mk1);
-            }
-            if (ng == 1) issue(q + 2, nxt, fa[sl], fb[sl]);       // (step t+2: nxt after the advance)
-        }
+        mask_load(3, mk0, mk1);                                           // (step 3's, built at step 0)
     }
     __syncthreads();
+
+    // staging of chunk q = t * nb + c: thread -> (row slot tid/8 + 64i,
+    // 16-byte piece tid%8) of A and of B; batch entries past B are zeroed
+    const int sr = tid >> 3, sp = tid & 7;
+    u32x4_t ra[2][2], rb[2][2];
+    float dbacc[2] = {0.0f, 0.0f};
+    const bool dbw = a.db && rs == 0;
+    auto fetch = [&](int set, int q) {
+        const bool live = q < nq;
+        const int t = live ? q / nb : T_ - 1, c = live ? q % nb : 0;
+        const int bq = WL_KC * c + 8 * sp;                                // first batch entry of the piece
+        const __amdgpu_buffer_rsrc_t ar = buf_rsrc(act_ptr(t), (uint32_t)((size_t)a.K * a.BP * 2));
+        const __amdgpu_buffer_rsrc_t br = buf_rsrc((const bf16*)a.daT + (size_t)t * G * a.BP,
+                                                   (uint32_t)((size_t)G * a.BP * 2));
+        const int* lr = lrow + (t & 3) * WL_R;
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int r = lr[sr + 64 * i];
+            const uint32_t oa = (live && r >= 0 && bq < B) ? (uint32_t)((size_t)r * a.BP + bq) * 2 : OOB_OFF;
+            ra[set][i] = __builtin_amdgcn_raw_buffer_load_b128(ar, oa, 0, 0);
+            const int n = n0 + sr + 64 * i;
+            const uint32_t ob = (live && n < G && bq < B) ? (uint32_t)((size_t)n * a.BP + bq) * 2 : OOB_OFF;
+            rb[set][i] = __builtin_amdgcn_raw_buffer_load_b128(br, ob, 0, 0);
+        }
+    };
+    auto commit = [&](int set, int buf, int q) {
+        const int c = q % nb;
+        const int bq = WL_KC * c + 8 * sp;
+        uint32_t m[4];
+        pad_mask<bf16>(bq, B, m);                                         // (batch entries past B)
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            u32x4_t x = ra[set][i], y = rb[set][i];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) { x[e] &= m[e]; y[e] &= m[e]; }
+            *(u32x4_t*)(As + ((size_t)buf * WL_R + sr + 64 * i) * WL_P + 8 * sp) = x;
+            *(u32x4_t*)(Bs + ((size_t)buf * WL_C + sr + 64 * i) * WL_P + 8 * sp) = y;
+            if (dbw && q < nq) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) dbacc[i] += __uint_as_float(y[e] << 16) + __uint_as_float(y[e] & 0xffff0000u);
+            }
+        }
+    };
+
+    f32x4_t acc[4][2];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = f32x4_t{0, 0, 0, 0};
+    const int mw = w >> 2, cw = 32 * (w & 3);
+    const int cl = lane & 15, g8 = 8 * (lane >> 4);
+    int cnt = lcount[0];                                                  // rows of the current step
+    fetch(0, 0);
+    fetch(1, 1);
+    commit(0, 0, 0);
+    __syncthreads();
+    // chunk q (LDS buffer cur = q % 2): the loads of q+2 go out, then the
+    // products; at the first chunk of a step wave 0 lists the rows of step
+    // t+3 (ring slot (t+3) % 4, whose step t-1 is done), at the last the
+    // step's tiles go into the accumulator
+    auto chunk = [&](int q, int cur) {
+        fetch(cur, q + 2);
+        __builtin_amdgcn_sched_barrier(0);     // (the loads go out before anything waits)
+        const int t = q / nb, c = q % nb;
+        if (c == 0 && w == 0) {
+            build(t + 3, mk0, mk1);
+            mask_load(t + 4, mk0, mk1);
+        }
+        const bf16* Ab = As + (size_t)cur * WL_R * WL_P;
+        const bf16* Bb = Bs + (size_t)cur * WL_C * WL_P;
+#pragma unroll
+        for (int ks = 0; ks < WL_KC / 32; ++ks) {
+            Raw8<bf16> fb[2];
+#pragma unroll
+            for (int j = 0; j < 2; ++j) raw_lds(fb[j], Bb + (size_t)(cw + 16 * j + cl) * WL_P + 32 * ks + g8);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int mt = mw + 2 * i;
+                if (16 * mt >= cnt) break;                                // (uniform) row tiles past the list
+                Raw8<bf16> fa;
+                raw_lds(fa, Ab + (size_t)(16 * mt + cl) * WL_P + 32 * ks + g8);
+#pragma unroll
+                for (int j = 0; j < 2; ++j) raw_mma(fa, fb[j], acc[i][j]);
+            }
+        }
+        if (c == nb - 1) {
+            // the step's tiles into their rows: every wave's additions of
+            // the step before are complete (a barrier ends every chunk)
+            const int* tr = trow + (t & 3) * WL_R;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int mt = mw + 2 * i;
+                if (16 * mt >= cnt) break;
+#pragma unroll
+                for (int j = 0; j < 2; ++j) {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        float* d = acc_lds + (size_t)tr[16 * mt + acc_row(lane, r)] * WL_LDC + cw + 16 * j + cl;
+                        *d += a.s * acc[i][j][r];
+                    }
+                    acc[i][j] = f32x4_t{0, 0, 0, 0};
+                }
+            }
+        }
+        commit(cur ^ 1, cur ^ 1, q + 1);
+        __syncthreads();
+        if (c == nb - 1) cnt = lcount[(t + 1) & 3];
+    };
+    int q = 0;
+    for (; q + 1 < nq; q += 2) {
+        chunk(q, 0);
+        chunk(q + 1, 1);
+    }
+    if (q < nq) chunk(q, 0);
+    __syncthreads();
     const float nan = __builtin_nanf("");
-    for (int i = tid; i < nrow * WB_C; i += 512) {
-        const int r = i / WB_C, c = i % WB_C;
-        if (n0 + c < G) a.out[(size_t)(r0 + r) * G + n0 + c] = failed ? nan : acc_lds[r * WB_LDC + c];
+    for (int i = tid; i < nrow * WL_C; i += 512) {
+        const int r = i / WL_C, c = i % WL_C;
+        if (n0 + c < G) a.out[(size_t)(r0 + r) * G + n0 + c] = failed ? nan : acc_lds[r * WL_LDC + c];
     }
     if (dbw) {
-        dbacc += __shfl_xor(dbacc, 32);
-        if (lane < 32 && ncol < G) a.db[ncol] = failed ? nan : dbacc;
+        // the 8 threads of a column slot hold its partial sums over their pieces
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            float v = dbacc[i];
+            v += __shfl_xor(v, 1);
+            v += __shfl_xor(v, 2);
+            v += __shfl_xor(v, 4);
+            const int n = n0 + sr + 64 * i;
+            if (sp == 0 && n < G) a.db[n] = failed ? nan : v;
+        }
     }
 }
 
@@ -531,7 +540,7 @@ void launch_dx_big(const DxArgs& a, hipStream_t st, hipEvent_t e0, hipEvent_t e1
     else k_dx_big<<<grid, blk, DB_LDS, st>>>(a);
 }
 
-size_t wgrad_big_lds() { return (size_t)(WB_R + 1) * WB_LDC * 4 + (size_t)8 * 2 * WB_R * 4; }
+size_t wgrad_big_lds() { return WL_LDS; }
 
 // The large-batch weight gradient takes any batch (its loads run two
 // 64-row groups ahead); it pays off from a few groups per step on.
@@ -540,7 +549,7 @@ bool wgrad_big_fits(int B) { return B >= 64; }
 void launch_wgrad_big(const WgBatch& b, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
     int nx = 0;                                // 8 x (row slices) x ceil(column blocks / 8)
     for (int i = 0; i < b.np; ++i)
-        nx = std::max(nx, 8 * ((b.p[i].K + WB_R - 1) / WB_R) * (((b.p[i].G + WB_C - 1) / WB_C + 7) / 8));
+        nx = std::max(nx, 8 * ((b.p[i].K + WL_R - 1) / WL_R) * (((b.p[i].G + WL_C - 1) / WL_C + 7) / 8));
     const dim3 grid(nx, 1, b.np), blk(512);
     if (e0 && e1) hipExtLaunchKernelGGL(k_wgrad_big, grid, blk, (uint32_t)wgrad_big_lds(), st, e0, e1, 0, b);
     else k_wgrad_big<<<grid, blk, wgrad_big_lds(), st>>>(b);
