@@ -1120,7 +1120,8 @@ __global__ void __launch_bounds__(512) k_bwd_big(PBwdArgs a) {
             }
         }
     }
-    // phase A pairs and their carries
+    // phase A pairs and their carries: pair p = tid + 512q is row p/16 of
+    // the group, unit p%16 of the tile (16 lanes on 16 adjacent units)
     float dcs[PPT], dhc[PPT];
     int pb[PPT], pu[PPT], lenr[PPT];
 #pragma unroll
@@ -1167,12 +1168,37 @@ __global__ void __launch_bounds__(512) k_bwd_big(PBwdArgs a) {
 
     prefetch(0);
     bool ok = true;
+    // hidden sizes in multiples of 8: DA goes out as whole 16-byte pieces
+    const bool wide = (H & 7) == 0;
     for (int s = 0; s <= T_; ++s) {
         const bool final_pass = s == T_;
         const int t = final_pass ? -1 : step_t(s);
         // ---- phase A: the partial recurrent gradients of the step before
         // (phase B of iteration s-1) are complete after 2s arrivals
         if (s > 0 && !(ok = grid_wait(bar, 0, nslot, (unsigned)(2 * s), a.err, a.timeout, STATUS_BWD))) break;
+        // the recurrent gradients of the thread's pairs: the partial sums of
+        // the column groups, 8 groups' loads of both pairs in flight at once
+        // (absent groups read group 0; clamped addresses: the results of
+        // pairs outside the batch or the layer are not used), added in group
+        // order
+        float rg[PPT] = {0.f, 0.f};
+        if (s > 0) {
+            for (int k0 = 0; k0 < a.ngk; k0 += 8) {
+                float pv[PPT][8];
+#pragma unroll
+                for (int k = 0; k < 8; ++k) {
+                    const float* pk = a.part + (size_t)(k0 + k < a.ngk ? k0 + k : 0) * B * H;
+#pragma unroll
+                    for (int q = 0; q < PPT; ++q)
+                        pv[q][k] = xload1(pk + (size_t)min(pb[q], B - 1) * H + min(pu[q], H - 1));
+                }
+#pragma unroll
+                for (int k = 0; k < 8; ++k)
+#pragma unroll
+                    for (int q = 0; q < PPT; ++q)
+                        if (k0 + k < a.ngk) rg[q] += pv[q][k];
+            }
+        }
         float da4[PPT][4];
 #pragma unroll
         for (int q = 0; q < PPT; ++q) {
@@ -1184,12 +1210,8 @@ __global__ void __launch_bounds__(512) k_bwd_big(PBwdArgs a) {
             asm volatile("" : "+v"(b), "+v"(u));
             if (b >= B || u >= H) continue;
             float dh = dhc[q];
-            if (s > 0 && mkr[q]) {
-                // units dropped at the step before get no recurrent gradient (Eq. 10)
-                float v = 0.f;
-                for (int k = 0; k < a.ngk; ++k) v += xload1(a.part + ((size_t)k * B + b) * H + u);
-                dh += D.s_rh * v;
-            }
+            // units dropped at the step before get no recurrent gradient (Eq. 10)
+            if (s > 0 && mkr[q]) dh += D.s_rh * rg[q];
             if (final_pass) {
                 D.dh0[(size_t)b * H + u] = dh;
                 D.dc0[(size_t)b * H + u] = dcs[q];
@@ -1210,11 +1232,33 @@ __global__ void __launch_bounds__(512) k_bwd_big(PBwdArgs a) {
             } else {
                 dhc[q] = dh;                                           // frozen row: pass through
             }
-            bf16* dar = (bf16*)D.da + (size_t)t * das;
+            if (!wide) {
+                bf16* dar = (bf16*)D.da + (size_t)t * das;
 #pragma unroll
-            for (int g = 0; g < 4; ++g) xstore(dar + frag_off(b, g * H + u, a.mtiles), f2bf(da4[q][g]));
+                for (int g = 0; g < 4; ++g) xstore(dar + frag_off(b, g * H + u, a.mtiles), f2bf(da4[q][g]));
+            }
         }
         if (final_pass) break;
+        if (wide && roleA) {
+            // DA_t of the tile through LDS ([64 rows][4 gates x 16 units]),
+            // published as 16-byte pieces: 8 adjacent units of one gate and
+            // row are one piece of the fragment-major block
+            bf16* st = (bf16*)red;
+#pragma unroll
+            for (int q = 0; q < PPT; ++q) {
+                const int p = tid + NTH * q;
+#pragma unroll
+                for (int g = 0; g < 4; ++g) st[(p / BB_UT) * 64 + g * BB_UT + p % BB_UT] = f2bf(da4[q][g]);
+            }
+            __syncthreads();
+            const int rr = tid >> 3, g = (tid >> 1) & 3, h = tid & 1;
+            const int b = mA0 + rr, uh = u0 + 8 * h;
+            if (b < B && uh < H) {
+                const __amdgpu_buffer_rsrc_t dw = buf_rsrc((const bf16*)D.da + (size_t)t * das, (uint32_t)(das * 2));
+                const u32x4_t v = *(const u32x4_t*)(st + rr * 64 + g * BB_UT + 8 * h);
+                __builtin_amdgcn_raw_buffer_store_b128(v, dw, (uint32_t)(frag_off(b, g * H + uh, a.mtiles) * 2), 0, CPOL_SC1);
+            }
+        }
         grid_arrive(bar);                                  // DA_t is published (arrival 2s+1)
         // DA^T (the weight gradients' operand) through LDS: the tile's
         // [4 gates x 16 units][64 rows] block, written as 16-byte row pieces
@@ -1284,14 +1328,33 @@ __global__ void __launch_bounds__(512) k_bwd_big(PBwdArgs a) {
                             acc[mt][j][r];
             __syncthreads();
             float* pk = a.part + (size_t)kgB * B * H;
-            for (int i = tid; i < BB_MG * BB_UG; i += NTH) {
-                const int rr = i / BB_UG, uu = i % BB_UG;
-                const int b = mB0 + rr, u = BB_UG * ugB + uu;
-                if (b < B && u < H) {
-                    float v = 0.f;
+            if ((H & 3) == 0) {                // four adjacent units, one 16-byte coherent store
+                const __amdgpu_buffer_rsrc_t pr = buf_rsrc(pk, (uint32_t)((size_t)B * H * 4));
+                for (int i = tid; i < BB_MG * BB_UG / 4; i += NTH) {
+                    const int rr = i / (BB_UG / 4), uu = 4 * (i % (BB_UG / 4));
+                    const int b = mB0 + rr, u = BB_UG * ugB + uu;
+                    if (b < B && u < H) {
+                        float4 v = *(const float4*)(red + (size_t)rr * BB_RP + uu);
 #pragma unroll
-                    for (int k = 0; k < 4; ++k) v += red[(k * BB_MG + rr) * BB_RP + uu];
-                    xstore(pk + (size_t)b * H + u, v);
+                        for (int k = 1; k < 4; ++k) {
+                            const float4 x = *(const float4*)(red + (size_t)(k * BB_MG + rr) * BB_RP + uu);
+                            v.x += x.x; v.y += x.y; v.z += x.z; v.w += x.w;
+                        }
+                        const u32x4_t o = {__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z),
+                                           __float_as_uint(v.w)};
+                        __builtin_amdgcn_raw_buffer_store_b128(o, pr, (uint32_t)(((size_t)b * H + u) * 4), 0, CPOL_SC1);
+                    }
+                }
+            } else {
+                for (int i = tid; i < BB_MG * BB_UG; i += NTH) {
+                    const int rr = i / BB_UG, uu = i % BB_UG;
+                    const int b = mB0 + rr, u = BB_UG * ugB + uu;
+                    if (b < B && u < H) {
+                        float v = 0.f;
+#pragma unroll
+                        for (int k = 0; k < 4; ++k) v += red[(k * BB_MG + rr) * BB_RP + uu];
+                        xstore(pk + (size_t)b * H + u, v);
+                    }
                 }
             }
         }
