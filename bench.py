@@ -605,7 +605,70 @@ def cpu_baseline(wl, p_nr, p_rh, budget_s=12.0, max_steps=50, rows=None):
 KERNEL_SYMBOLS = {"fwd_persist": ("lsd::k_fwd_persist<", "lsd::k_fwd_big<"), "step": ("lsd::k_step<",),
                   "bwd_persist": ("lsd::k_bwd_persist<", "lsd::k_bwd_big"), "bwd": ("lsd::k_bwd<",),
                   "wgrad": ("lsd::k_wgrad",),            # the row-sparse, the full and the large-batch kernel
-                  "fx": ("lsd::k_fx<",), "dx": ("lsd::k_dx<",), "mask_build": ("lsd::k_mask_build",)}
+                  "fx": ("lsd::k_fx<", "lsd::k_fx_big"), "dx": ("lsd::k_dx<", "lsd::k_dx_big"),
+                  "mask_build": ("lsd::k_mask_build",), "transpose": ("lsd::k_trans",)}
+SIMDS = 256 * 4             # MI355X: 256 compute units of 4 SIMDs
+XCDS = 8                    # GRBM_GUI_ACTIVE is counted once per XCD
+MFMA_BF16_FLOP_PER_MOP = 512
+
+
+def kernel_class(name):
+    for k, syms in KERNEL_SYMBOLS.items():
+        if any(sym in name for sym in syms):
+            return k
+    return None
+
+
+def summarize_pmc(paths, command):
+    """Markdown summary of rocprofv3 --pmc counter runs (one CSV per pass)
+    per kernel class: dispatches, average duration, MFMA busy fraction
+    (SQ_VALU_MFMA_BUSY_CYCLES over GRBM_GUI_ACTIVE per XCD times the SIMD
+    count), MFMA rate from the bf16 MOPS count, and every other counter's
+    mean per dispatch."""
+    import csv
+    import collections
+    vals = collections.defaultdict(lambda: collections.defaultdict(list))
+    dur = collections.defaultdict(dict)
+    names = collections.defaultdict(set)
+    for path in paths:
+        for r in csv.DictReader(open(path)):
+            k = kernel_class(r["Kernel_Name"])
+            if k is None:
+                continue
+            names[k].add(r["Kernel_Name"].split("(")[0].replace("void ", ""))
+            vals[k][r["Counter_Name"]].append(float(r["Counter_Value"]))
+            dur[k][(path, r["Dispatch_Id"])] = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-3
+    lines = ["| class | kernels | dispatches | avg us | MFMA busy | MFMA TFLOP/s (bf16 MOPS) | counters (mean per dispatch) |",
+             "|---|---|---|---|---|---|---|"]
+    for k in KERNEL_SYMBOLS:
+        if k not in vals:
+            continue
+        v = {c: float(np.mean(x)) for c, x in vals[k].items()}
+        us = float(np.mean(list(dur[k].values())))
+        busy = ""
+        if "SQ_VALU_MFMA_BUSY_CYCLES" in v and "GRBM_GUI_ACTIVE" in v and v["GRBM_GUI_ACTIVE"] > 0:
+            busy = f"{100.0 * v['SQ_VALU_MFMA_BUSY_CYCLES'] / (v['GRBM_GUI_ACTIVE'] / XCDS * SIMDS):.1f}%"
+        rate = ""
+        if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in v and us > 0:
+            rate = f"{v['SQ_INSTS_VALU_MFMA_MOPS_BF16'] * MFMA_BF16_FLOP_PER_MOP / (us * 1e-6) / 1e12:.1f}"
+        others = ", ".join(f"{c} {x:.4g}" for c, x in sorted(v.items()))
+        lines.append(f"| {k} | {' '.join(sorted(names[k]))} | {len(dur[k])} | {us:.1f} | {busy} | {rate} | {others} |")
+    return "\n".join([f"Command: `{command}`", ""] + lines)
+
+
+def summarize_stats(path, command):
+    """Markdown table of a rocprofv3 --stats kernel summary (library kernels
+    first, by total time)."""
+    import csv
+    rows = list(csv.DictReader(open(path)))
+    lines = [f"Command: `{command}`", "", "| kernel | class | calls | total ms | avg us | min us | max us | % |",
+             "|---|---|---|---|---|---|---|---|"]
+    for r in rows:
+        k = kernel_class(r["Name"])
+        lines.append(f"| {r['Name'].split('(')[0].replace('void ', '')[:70]} | {k or ''} | {r['Calls']} | "
+                     f"{float(r['TotalDurationNs']) / 1e6:.3f} | {float(r['AverageNs']) / 1e3:.2f} | "
+                     f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.2f} |")
+    return "\n".join(lines)
 
 
 def summarize_counters(fetch_csv, write_csv, copy_bytes, workload, command):
@@ -624,9 +687,9 @@ def summarize_counters(fetch_csv, write_csv, copy_bytes, workload, command):
             name = r["Kernel_Name"]
             if "copyBuffer" in name or "copy_kernel" in name:
                 copy = max(copy, v)
-            for k, syms in KERNEL_SYMBOLS.items():
-                if any(sym in name for sym in syms):
-                    agg[k].append(v)
+            k = kernel_class(name)
+            if k is not None:
+                agg[k].append(v)
         return agg, copy
 
     fetch, fcopy = per_kernel(fetch_csv)
@@ -667,8 +730,18 @@ def main(argv=None):
                     help="also run a plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--summarize-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write profiles/traffic.json from two rocprofv3 --pmc runs and exit (no GPU)")
-    ap.add_argument("--counter-command", default="", help="command recorded with --summarize-counters")
+    ap.add_argument("--counter-command", default="", help="command recorded with the summaries")
+    ap.add_argument("--summarize-pmc", nargs="+", metavar="CSV",
+                    help="print a markdown summary of rocprofv3 --pmc counter CSVs per kernel class and exit (no GPU)")
+    ap.add_argument("--summarize-stats", metavar="CSV",
+                    help="print a markdown table of a rocprofv3 --stats kernel summary and exit (no GPU)")
     args = ap.parse_args(argv)
+    if args.summarize_pmc:
+        print(summarize_pmc(args.summarize_pmc, args.counter_command))
+        return 0
+    if args.summarize_stats:
+        print(summarize_stats(args.summarize_stats, args.counter_command))
+        return 0
     if args.summarize_counters:
         out = summarize_counters(*args.summarize_counters, copy_bytes=args.calibrate_copy * (1 << 20),
                                  workload=args.workload, command=args.counter_command)
