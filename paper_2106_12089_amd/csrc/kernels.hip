@@ -776,8 +776,9 @@ __device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
     float dbacc[WG_CT] = {};
     // multiply the tiles (chunk-0 fragments already loaded) with both column
     // tiles, finish the other batch chunks, and add the tiles into their LDS
-    // rows.  Tiles past nt are multiplied too (their rows are absent):
-    // unconditional products keep the loads out of branches.  The products
+    // rows.  Tiles past nt hold no kept row and are skipped (a wave-uniform
+    // branch: their loads went out a step earlier, in another iteration,
+    // so no load is moved into it).  The products
     // are taken transposed (DA^T fragment as the left operand): the output
     // column of a lane is then its own A-fragment row, and its four values
     // are four adjacent gradient columns, so each lane adds one 16-byte piece
@@ -787,11 +788,12 @@ __device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
         f32x4_t acc[MAXT][WG_CT];
 #pragma unroll
         for (int i = 0; i < MAXT; ++i) {
-            raw_and(fa[i], pm0);
 #pragma unroll
-            for (int h = 0; h < WG_CT; ++h) {
-                acc[i][h] = f32x4_t{0, 0, 0, 0};
-                raw_mma(fb0[h], fa[i], acc[i][h]);
+            for (int h = 0; h < WG_CT; ++h) acc[i][h] = f32x4_t{0, 0, 0, 0};
+            if (i < nt) {
+                raw_and(fa[i], pm0);
+#pragma unroll
+                for (int h = 0; h < WG_CT; ++h) raw_mma(fb0[h], fa[i], acc[i][h]);
             }
         }
         for (int bc = 32; MULTI && bc < a.B; bc += 32) {
@@ -809,9 +811,11 @@ __device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
             }
 #pragma unroll
             for (int i = 0; i < MAXT; ++i) {
-                raw_and(fa[i], pm);
+                if (i < nt) {
+                    raw_and(fa[i], pm);
 #pragma unroll
-                for (int h = 0; h < WG_CT; ++h) raw_mma(fb[h], fa[i], acc[i][h]);
+                    for (int h = 0; h < WG_CT; ++h) raw_mma(fb[h], fa[i], acc[i][h]);
+                }
             }
         }
         // output r of this lane is gradient column 4*(lane/16)+r of the

@@ -107,7 +107,7 @@ __device__ __forceinline__ bool grid_wait(unsigned* sbar, int slot, int nslot, u
             // steps complete per lane; the minimum over each half of the wave
             unsigned c = n ? v / n : 0xffffffffu;
 #pragma unroll
-            for (int o = 8; o; o >>= 1) c = min(c, (unsigned)__shfl_xor((int)c, o));
+            for (int o = BAR_LINES / 2; o; o >>= 1) c = min(c, (unsigned)__shfl_xor((int)c, o));
             if (seen && i == 0) *seen = c;
             if (seen2 && i == BAR_LINES) *seen2 = c;
         }
