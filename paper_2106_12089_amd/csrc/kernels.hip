@@ -548,8 +548,11 @@ __global__ void __launch_bounds__(1024) k_bwd(BwdArgs a) {
 
 // ---------------------------------------------------------------------------
 // Output-sparse input gradient, all t (Eq. 10), summed over directions.
-// grid (ceil(K/16), T, ceil(B/64)), block 256: 16 kept columns per
-// workgroup, the contraction over 4H split over the 4 waves.  With scatter,
+// grid (32 * tps * ceil(T/4), 1, ceil(B/64)), block 256: 16 kept columns per
+// workgroup, the contraction over 4H split over the 4 waves.  Workgroup i
+// runs on XCD c = i % 8, which takes the steps t = c/2 (mod 4) and the W
+// slices 4(c%2) .. 4(c%2)+3: a step's DA is read by 2 XCDs and a slice of W
+// by 4 (DA of all steps and W are of about the same size).  With scatter,
 // the output is the full-width gradient: kept columns go to their own
 // positions, and the workgroup of (slice, tile) also writes the zeros of
 // the same tile of the slice's dropped columns.
@@ -559,9 +562,11 @@ __global__ void __launch_bounds__(256) k_dx(DxArgs a) {
     constexpr uint32_t ES = sizeof(T);
     __shared__ float red[4][64][17];
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int t = blockIdx.y;
-    // slot -> (XCD slice x, tile ti): kept rows of t inside slice x of W
-    const int x = blockIdx.x % NXCD, ti = blockIdx.x / NXCD;
+    // slot -> (step t, slice x, tile ti): kept rows of t inside slice x of W
+    const int c = blockIdx.x % NXCD, jw = blockIdx.x / NXCD;
+    const int t = (c >> 1) + 4 * (jw / (4 * a.tps));
+    const int x = 4 * (c & 1) + (jw / a.tps) % 4, ti = jw % a.tps;
+    if (t >= a.T) return;
     const int32_t* ks = a.site.kseg + (size_t)t * (NSEG + 1);
     const int hi = ks[2 * x + 2];
     const int j0 = ks[2 * x] + 16 * ti;
@@ -651,12 +656,12 @@ __device__ __forceinline__ void db_add_raw(const Raw8<T>& f, float& acc) {
 }
 
 // ---------------------------------------------------------------------------
-// Row-sparse weight gradient (Eq. 11; Sec. 3.2 WG).  grid (8 * ceil(G/128),
-// 1, problems), block 512 (8 waves), dynamic LDS (rows of a slice + 1) *
-// WG_LDC floats.  Workgroup (i, z) owns, for problem z, neuron slice
-// x = i % 8, the rows [floor(xK/8), floor((x+1)K/8)) (workgroup i runs on
-// XCD i % 8, so a slice's activation rows stay in one XCD's L2), and the 128
-// gradient columns of block i / 8, over every time step (no partial sums).
+// Row-sparse weight gradient (Eq. 11; Sec. 3.2 WG).  grid (64 *
+// ceil(G/1024), 1, problems), block 512 (8 waves), dynamic LDS (rows of a
+// slice + 1) * WG_LDC floats.  Workgroup (i, z) owns, for problem z, a
+// neuron slice x, the rows [floor(xK/8), floor((x+1)K/8)), and the 128
+// gradient columns of a block cb (wg_slot: the column blocks of an XCD share
+// their DA^T through its L2), over every time step (no partial sums).
 // At each t the kept rows of the slice (keep-list entries kseg[t][x] ..
 // kseg[t][x+1]) are taken in 16-row tiles; wave w multiplies them with its
 // 16 DA^T columns and adds each tile into its columns of the LDS
@@ -695,13 +700,25 @@ inline size_t wgrad_lds_bytes(int K) {
     return (size_t)(wgrad_tsplit<T>(K) ? 2 : 1) * ((K + NXCD - 1) / NXCD + 1) * WG_LDC * sizeof(float);
 }
 
+// workgroup i -> (row slice x, column block cb).  Workgroup i runs on XCD
+// i % 8, which takes the column blocks i % 8 + 8j with every row slice: one
+// XCD's L2 then holds its columns' DA^T (4H x B per step, the larger operand)
+// for all of the slices, and each XCD reads 1/8 of it.  The grid has
+// 64 * ceil(column blocks / 8) workgroups; those past the last block return.
+__device__ __forceinline__ void wg_slot(int& x, int& cb) {
+    const int i = blockIdx.x, j = i / NXCD;
+    x = j % NXCD;
+    cb = i % NXCD + NXCD * (j / NXCD);
+}
+
 template <typename T, bool MULTI>
 __device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
     constexpr int MAXT = WgTiles<T>::N / 2;     // 16-row tiles of a round
     constexpr int NW = Raw8<T>::NW;
     constexpr uint32_t ES = sizeof(T);
     // acc_lds: [rows of the slice + 1][WG_LDC], one per half when the halves split the t-range
-    const int x = blockIdx.x % NXCD, cb = blockIdx.x / NXCD;
+    int x, cb;
+    wg_slot(x, cb);
     if (cb * WG_NB >= a.G) return;
     const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // (wave-uniform)
     const int col = lane & 15, g8 = 8 * (lane >> 4);
@@ -938,7 +955,7 @@ __device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
 // or the dense comparison mode, where the mask zeroes the dropped rows):
 // every row takes part at every t, so the accumulators stay in registers
 // over the whole t-range; no gather, no scatter.  Same grid as the
-// row-sparse kernel: workgroup i owns slice x = i % 8 and 128 columns; wave
+// row-sparse kernel: workgroup i owns a slice x and 128 columns; wave
 // w owns 32 columns (two tiles: each A fragment feeds two products) and
 // the rows of the slice in passes of 16-row tiles.  The two halves of the
 // workgroup (w / 4) split each pass's tiles, NTW each; a slice that one
@@ -951,7 +968,8 @@ template <typename T, bool MASKED, int NTW, bool MULTI, int RING = 2>
 __device__ __forceinline__ void wgrad_full(const WgArgs& a, float* red) {
     constexpr int NW = Raw8<T>::NW;
     constexpr uint32_t ES = sizeof(T);
-    const int x = blockIdx.x % NXCD, cb = blockIdx.x / NXCD;
+    int x, cb;
+    wg_slot(x, cb);
     if (cb * WG_NB >= a.G) return;
     const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // (wave-uniform)
     const int col = lane & 15, g8 = 8 * (lane >> 4);
@@ -1113,10 +1131,12 @@ __device__ __forceinline__ void wgrad_full(const WgArgs& a, float* red) {
     }
 }
 
-// NaN into the part of a problem's outputs this workgroup owns (slice x =
-// i % 8 of the rows, 128 columns of block i / 8; slice 0 also the bias)
+// NaN into the part of a problem's outputs this workgroup owns (its row
+// slice and column block; slice 0 also the bias)
 __device__ __forceinline__ void wgrad_poison(const WgArgs& a) {
-    const int x = blockIdx.x % NXCD, n0 = (blockIdx.x / NXCD) * WG_NB;
+    int x, cb;
+    wg_slot(x, cb);
+    const int n0 = cb * WG_NB;
     const int r0 = slice_start(x, a.K), r1 = slice_start(x + 1, a.K);
     const float nan = __builtin_nanf("");
     for (int i = threadIdx.x; i < (r1 - r0) * WG_NB; i += blockDim.x) {
@@ -1710,7 +1730,7 @@ void launch_dx(const DxArgs& a, int K, hipStream_t st) {
         launch_dx_big(a, st, e0, e1);
         return;
     }
-    const dim3 grid(NXCD * a.tps, a.T, (a.B + 63) / 64);
+    const dim3 grid(NXCD * a.tps * 4 * ((a.T + 3) / 4), 1, (a.B + 63) / 64);
     if (a.B <= 16) launch_k(KID_DX, k_dx<T, 1>, grid, dim3(256), 0, st, a);
     else if (a.B <= 32) launch_k(KID_DX, k_dx<T, 2>, grid, dim3(256), 0, st, a);
     else launch_k(KID_DX, k_dx<T, 4>, grid, dim3(256), 0, st, a);
@@ -1728,7 +1748,8 @@ void launch_wgrad(const WgBatch& b, hipStream_t st) {
         return;
     }
     const WgArgs& a = b.p[0];                  // the problems share G, B and the mode
-    const dim3 grid(NXCD * ((a.G + WG_NB - 1) / WG_NB), 1, b.np);
+    const int ncb = (a.G + WG_NB - 1) / WG_NB;  // column blocks (wg_slot: 8 XCDs x 8 slices each)
+    const dim3 grid(NXCD * NXCD * ((ncb + NXCD - 1) / NXCD), 1, b.np);
     size_t lds = 0;
     bool multi = a.B > 32;                     // builds with the extra loops (batch chunks, tile rounds)
     for (int i = 0; i < b.np; ++i) {
