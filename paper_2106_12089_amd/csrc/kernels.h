@@ -171,6 +171,8 @@ struct WgArgs {
     float* db;                          // non-null: also the bias gradient (Eq. 11), the sum of DA^T
     int K, B, BP, G, T, dense;
     int full;                           // every keep list of the site is the identity (p = 0, or dense mode)
+    int staged;                         // (set at launch) a kernel with LDS-staged operands
+    int fullmask;                       // (set at launch) a row-sparse problem on the full kernel, rows times the mask
     float s;
 };
 // Weight gradients of a pass (row-sparse and full problems) in one launch

@@ -14,6 +14,7 @@
 #include <hip/hip_runtime.h>
 #include <hip/hip_ext.h>
 
+#include <stdlib.h>
 #include <string.h>
 
 #include <vector>
@@ -700,6 +701,19 @@ inline size_t wgrad_lds_bytes(int K) {
     return (size_t)(wgrad_tsplit<T>(K) ? 2 : 1) * ((K + NXCD - 1) / NXCD + 1) * WG_LDC * sizeof(float);
 }
 
+// Layout of the staged row-sparse kernel's LDS: the accumulator rows of the
+// largest slice (+ a spare row), two stage buffers (DA^T: 8 fragment tiles;
+// the kept rows: up to wgs_tiles tiles; their accumulator row offsets), and
+// the keep-list ranges of every step
+__host__ __device__ inline int wgs_rows(int K) { return (K + NXCD - 1) / NXCD; }
+__host__ __device__ inline int wgs_tiles(int K) { return (wgs_rows(K) + 15) / 16; }
+__host__ __device__ inline int wgs_stage_bytes(int K) { return (8 + wgs_tiles(K)) * 1024 + 16 * wgs_tiles(K) * 4; }
+inline size_t wgs_lds_bytes(int K, int T) {
+    return (size_t)(wgs_rows(K) + 1) * WG_LDC * 4 + 2 * (size_t)wgs_stage_bytes(K) + (size_t)T * 8;
+}
+constexpr int WGS_MAX_ROWS = 128;          // a stage buffer row per thread piece: 512 / 4
+constexpr size_t WGS_MAX_LDS = 80 * 1024;  // two workgroups per CU
+
 // workgroup i -> (row slice x, column block cb).  Workgroup i runs on XCD
 // i % 8, which takes the column blocks i % 8 + 8j with every row slice: one
 // XCD's L2 then holds its columns' DA^T (4H x B per step, the larger operand)
@@ -951,6 +965,298 @@ __device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
     }
 }
 
+// Row-sparse weight gradient with LDS-staged operands (bf16, batch <= 32,
+// slices of at most 128 rows).  Same grid, slots and result as the kernel
+// above; what differs is how a step's operands reach the waves.  There,
+// every wave loaded its own fragments from memory: the four waves of a half
+// the same gathered rows, the two halves the same DA^T columns, so the
+// vector memory pipe moved about three times the step's data and set the
+// step time.  Here the 512 threads load a step's operands once, one 16-byte
+// piece each: thread i takes piece i % 4 (8 batch entries) of DA^T column
+// i / 4 of the block (8 KB, one piece per thread) and of the step's kept row
+// i / 4 of the slice (gathered through the keep list; absent rows read past
+// the resource, i.e. zeros), and stores them fragment-major in LDS, with
+// the accumulator row offset of each kept row beside them.  Wave w then
+// multiplies DA^T column tile w with every kept-row tile of the step and
+// adds the tiles into its 16 columns of the LDS accumulator.  Loads run two
+// steps ahead of the store into LDS (register ring), keep-list entries two
+// steps ahead of those; the stage buffers alternate, one barrier per step.
+// The slice's keep-list ranges for every step sit in LDS ([T][2] ints).
+template <typename T>
+__device__ __forceinline__ void wgrad_staged(const WgArgs& a, float* lds) {
+    static_assert(sizeof(T) == 2, "bf16 only");
+    int x, cb;
+    wg_slot(x, cb);
+    if (cb * WG_NB >= a.G) return;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);     // (wave-uniform)
+    const int n0 = cb * WG_NB;
+    const int r0 = slice_start(x, a.K), nrow = slice_start(x + 1, a.K) - r0;
+    const int ntmax = wgs_tiles(a.K);
+    float* acc = lds;                                              // [rows of the slice + 1][WG_LDC]
+    char* stg = (char*)(lds + (size_t)(wgs_rows(a.K) + 1) * WG_LDC);
+    const int sbytes = wgs_stage_bytes(a.K);                       // one stage buffer
+    int* seg = (int*)(stg + 2 * sbytes);                           // [T][2]: keep-list range of the slice
+    for (int i = tid; i < (nrow + 1) * WG_NB; i += blockDim.x) acc[(i / WG_NB) * WG_LDC + i % WG_NB] = 0.0f;
+    for (int t = tid; t < a.T; t += blockDim.x) {
+        const int32_t* ks = a.site.kseg + (size_t)t * (NSEG + 1) + 2 * x;
+        seg[2 * t] = ks[0];
+        seg[2 * t + 1] = ks[2];
+    }
+    __syncthreads();
+
+    // this thread's piece: row / column j of the step, batch entries 8q .. 8q+7
+    const int j = tid >> 2, q = tid & 3;
+    uint32_t pm[4];
+    pad_mask<T>(8 * q, a.B, pm);
+    const uint32_t abytes = (uint32_t)a.K * a.BP * 2, bbytes = (uint32_t)a.G * a.BP * 2;
+    const uint32_t boff = n0 + j < a.G ? (uint32_t)((n0 + j) * a.BP + 8 * q) * 2 : OOB_OFF;
+    const int frag = ((j & 15) + 16 * q) * 16 + (j >> 4) * 1024;   // fragment-major LDS offset of the piece
+    const bool arow = j < 16 * ntmax;                              // a row of the stage buffer
+    const int spare = nrow * WG_LDC;
+    const uint32_t kbytes = (uint32_t)a.site.kmax * 4;
+    auto clampt = [&](int t) { return t < a.T ? t : a.T - 1; };
+    auto act_rsrc = [&](int t) {
+        const T* act = (a.actT_first && t == a.t_first) ? (const T*)a.actT_first
+                                                        : (const T*)a.actT + (long)(t + a.shift) * a.tstride;
+        return buf_rsrc(act, abytes);
+    };
+    // ring slots: keep-list entry, staged pieces and accumulator row offset of a step
+    int kv[2], la[2];
+    uint4 ra[2], rb[2];
+    auto issue_kv = [&](int t, int sl) {
+        t = clampt(t);
+        const int jb = seg[2 * t], n = seg[2 * t + 1] - jb;
+        const __amdgpu_buffer_rsrc_t kr = buf_rsrc(a.site.keep + (size_t)t * a.site.kmax, kbytes);
+        kv[sl] = (int)__builtin_amdgcn_raw_buffer_load_b32(kr, j < n ? (uint32_t)(jb + j) * 4 : OOB_OFF, 0, 0);
+    };
+    auto issue_ab = [&](int t, int sl) {
+        t = clampt(t);
+        const int n = seg[2 * t + 1] - seg[2 * t];
+        const bool ok = j < n;
+        const u32x4_t va = __builtin_amdgcn_raw_buffer_load_b128(
+            act_rsrc(t), ok ? ((uint32_t)kv[sl] * a.BP + 8 * q) * 2 : OOB_OFF, 0, 0);
+        const u32x4_t vb = __builtin_amdgcn_raw_buffer_load_b128(
+            buf_rsrc((const T*)a.daT + (size_t)t * a.G * a.BP, bbytes), boff, 0, 0);
+        ra[sl] = make_uint4(va[0], va[1], va[2], va[3]);
+        rb[sl] = make_uint4(vb[0], vb[1], vb[2], vb[3]);
+        la[sl] = ok ? (kv[sl] - r0) * WG_LDC : spare;
+    };
+    auto stage = [&](int buf, int sl) {
+        char* sb = stg + buf * sbytes;
+        const uint4 b4 = make_uint4(rb[sl].x & pm[0], rb[sl].y & pm[1], rb[sl].z & pm[2], rb[sl].w & pm[3]);
+        *(uint4*)(sb + frag) = b4;
+        if (arow) {
+            const uint4 a4 = make_uint4(ra[sl].x & pm[0], ra[sl].y & pm[1], ra[sl].z & pm[2], ra[sl].w & pm[3]);
+            *(uint4*)(sb + 8 * 1024 + frag) = a4;
+            if (q == 0) ((int*)(sb + (8 + ntmax) * 1024))[j] = la[sl];
+        }
+    };
+    const bool dbw = a.db && x == 0;
+    float dbacc = 0.0f;
+    const int cq = 16 * w + 4 * (lane >> 4);                       // this lane's 4 accumulator columns
+    auto compute = [&](int t, int buf) {
+        const char* sb = stg + buf * sbytes;
+        const int n = __builtin_amdgcn_readfirstlane(seg[2 * t + 1] - seg[2 * t]);
+        const int ntile = (n + 15) >> 4;
+        Raw8<T> fb;
+        raw_lds(fb, (const T*)(sb + w * 1024 + lane * 16));
+        if (dbw) db_add_raw(fb, dbacc);
+        const int* lab = (const int*)(sb + (8 + ntmax) * 1024);
+        for (int rt0 = 0; rt0 < ntile; rt0 += 4) {
+            Raw8<T> fa[4];
+            int lr[4];
+            f32x4_t d[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                if (rt0 + i < ntile) {
+                    raw_lds(fa[i], (const T*)(sb + 8 * 1024 + (rt0 + i) * 1024 + lane * 16));
+                    lr[i] = lab[(rt0 + i) * 16 + (lane & 15)];
+                }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                if (rt0 + i < ntile) {
+                    d[i] = f32x4_t{0, 0, 0, 0};
+                    raw_mma(fb, fa[i], d[i]);
+                }
+            float4 old[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                if (rt0 + i < ntile) old[i] = *(const float4*)(acc + lr[i] + cq);
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                if (rt0 + i < ntile) {
+                    float4 v = old[i];
+                    v.x += a.s * d[i][0];
+                    v.y += a.s * d[i][1];
+                    v.z += a.s * d[i][2];
+                    v.w += a.s * d[i][3];
+                    *(float4*)(acc + lr[i] + cq) = v;
+                }
+        }
+    };
+    // step t: stage t+1 (its loads went out two steps earlier), issue the
+    // operand loads of t+3 and the keep-list entries of t+5, multiply t
+    auto iter = [&](int t, int sl) {
+        stage((t + 1) & 1, sl ^ 1);
+        issue_ab(t + 3, sl ^ 1);
+        issue_kv(t + 5, sl ^ 1);
+        if (t < a.T) compute(t, t & 1);
+        __syncthreads();
+    };
+    issue_kv(0, 0);
+    issue_kv(1, 1);
+    issue_ab(0, 0);
+    issue_kv(2, 0);
+    issue_ab(1, 1);
+    issue_kv(3, 1);
+    stage(0, 0);
+    issue_ab(2, 0);
+    issue_kv(4, 0);
+    __syncthreads();
+    for (int t = 0; t < a.T; t += 2) {
+        iter(t, 0);
+        iter(t + 1, 1);
+    }
+    if (dbw) {                                                     // lanes l, l+16, l+32, l+48 hold column l
+        dbacc += __shfl_xor(dbacc, 16);
+        dbacc += __shfl_xor(dbacc, 32);
+        if (lane < 16 && n0 + 16 * w + lane < a.G) a.db[n0 + 16 * w + lane] = dbacc;
+    }
+    for (int i = tid; i < nrow * WG_NB; i += blockDim.x) {
+        const int rr = i / WG_NB, cc = i % WG_NB;
+        if (n0 + cc < a.G) a.out[(size_t)(r0 + rr) * a.G + n0 + cc] = acc[rr * WG_LDC + cc];
+    }
+}
+
+// Weight gradient of a full problem (identity keep lists, the dense
+// comparison mode, or a row-sparse problem routed here: in the last two the
+// mask byte zeroes the dropped rows) with LDS-staged rows (bf16, batch <=
+// 32).  Same grid and slots as the kernels above.
+// Wave w owns DA^T column tile w of the block (16 columns, its fragment
+// loaded straight into registers: no other wave reads it) and every row of
+// the slice, in passes of up to 6 row tiles whose accumulators stay in
+// registers over all steps.  The rows are the operand every wave shares: the
+// 512 threads load a step's rows once (one 16-byte piece each: row i / 4,
+// batch entries 8(i % 4) .. +7, zeroed when the row is dropped) and store
+// them fragment-major in LDS, where each wave reads its fragments.  Loads
+// run three steps ahead (register ring), the two stage buffers alternate,
+// one barrier per step.
+constexpr int WFS_TILES = 6;               // 16-row tiles of a pass
+constexpr int WFS_RING = 3;                // steps whose loads are in flight
+constexpr size_t WFS_LDS = 2 * WFS_TILES * 1024;
+
+template <typename T, bool MASKED>
+__device__ __forceinline__ void wgrad_full_staged(const WgArgs& a, float* lds) {
+    static_assert(sizeof(T) == 2, "bf16 only");
+    int x, cb;
+    wg_slot(x, cb);
+    if (cb * WG_NB >= a.G) return;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);     // (wave-uniform)
+    const int n0 = cb * WG_NB, nc = n0 + 16 * w + (lane & 15), g8 = 8 * (lane >> 4);
+    const int r0 = slice_start(x, a.K), r1 = slice_start(x + 1, a.K);
+    char* stg = (char*)lds;
+    const int j = tid >> 2, q = tid & 3;                           // staging: row j of the pass, piece q
+    const bool srow = j < 16 * WFS_TILES;
+    const int frag = ((j & 15) + 16 * q) * 16 + (j >> 4) * 1024;   // fragment-major LDS offset of the piece
+    uint32_t pm[4], pmb[4];
+    pad_mask<T>(8 * q, a.B, pm);
+    pad_mask<T>(g8, a.B, pmb);
+    if (nc >= a.G) pmb[0] = pmb[1] = pmb[2] = pmb[3] = 0u;
+    const uint32_t boff = (uint32_t)(min(nc, a.G - 1) * a.BP + g8) * 2;
+    const uint32_t abytes = (uint32_t)a.K * a.BP * 2, bbytes = (uint32_t)a.G * a.BP * 2;
+    const bool dbw = a.db && x == NXCD - 1;                        // (the last slice is never empty)
+    const bool masked = MASKED || a.fullmask;                      // dropped rows zeroed by the mask byte
+    float dbacc = 0.0f;
+    auto act_rsrc = [&](int t) {
+        const T* act = (a.actT_first && t == a.t_first) ? (const T*)a.actT_first
+                                                        : (const T*)a.actT + (long)(t + a.shift) * a.tstride;
+        return buf_rsrc(act, abytes);
+    };
+    for (int rp = r0; rp < r1; rp += 16 * WFS_TILES) {            // passes over the slice's rows
+        const int nt = min(WFS_TILES, (r1 - rp + 15) >> 4);        // row tiles of the pass
+        const bool first = rp == r0 && dbw;                        // (the bias gradient: first pass)
+        const int row = rp + j;
+        const bool rok = srow && row < r1;
+        uint4 ra[WFS_RING];
+        Raw8<T> rb[WFS_RING];
+        int mk[WFS_RING];
+        auto issue = [&](int t, int sl) {
+            t = t < a.T ? t : a.T - 1;
+            const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(
+                act_rsrc(t), rok ? (uint32_t)(row * a.BP + 8 * q) * 2 : OOB_OFF, 0, 0);
+            ra[sl] = make_uint4(v[0], v[1], v[2], v[3]);
+            raw_load(rb[sl], buf_rsrc((const T*)a.daT + (size_t)t * a.G * a.BP, bbytes), boff);
+            // (always issued, past the resource when unmasked: a load under a
+            // branch would make the compiler wait for every load on its own)
+            const __amdgpu_buffer_rsrc_t mr = buf_rsrc(a.site.mask + (size_t)t * a.site.kmax, (uint32_t)a.site.kmax);
+            mk[sl] = (int)__builtin_amdgcn_raw_buffer_load_b8(mr, masked && rok ? (uint32_t)row : OOB_OFF, 0, 0);
+        };
+        auto stage = [&](int buf, int sl) {
+            if (srow) {
+                uint4 v = make_uint4(ra[sl].x & pm[0], ra[sl].y & pm[1], ra[sl].z & pm[2], ra[sl].w & pm[3]);
+                if (masked && !mk[sl]) v = make_uint4(0u, 0u, 0u, 0u);
+                *(uint4*)(stg + buf * (WFS_TILES * 1024) + frag) = v;
+            }
+        };
+        f32x4_t acc[WFS_TILES];
+#pragma unroll
+        for (int i = 0; i < WFS_TILES; ++i) acc[i] = f32x4_t{0, 0, 0, 0};
+        auto compute = [&](int buf, int sl) {
+            Raw8<T> fb = rb[sl];
+            raw_and(fb, pmb);
+            if (first) db_add_raw(fb, dbacc);
+            const char* sb = stg + buf * (WFS_TILES * 1024);
+#pragma unroll
+            for (int i = 0; i < WFS_TILES; ++i)
+                if (i < nt) {
+                    Raw8<T> fa;
+                    raw_lds(fa, (const T*)(sb + i * 1024 + lane * 16));
+                    raw_mma(fb, fa, acc[i]);
+                }
+        };
+        // step t: stage t+1 (its loads went out two steps earlier), multiply
+        // t, then its slot takes the loads of t+3
+        auto iter = [&](int t, int sl) {
+            stage((t + 1) & 1, (sl + 1) % WFS_RING);
+            if (t < a.T) compute(t & 1, sl);
+            issue(t + WFS_RING, sl);
+            __syncthreads();
+        };
+#pragma unroll
+        for (int i = 0; i < WFS_RING; ++i) issue(i, i);
+        stage(0, 0);
+        __syncthreads();
+        for (int t = 0; t < a.T; t += WFS_RING) {
+#pragma unroll
+            for (int i = 0; i < WFS_RING; ++i) iter(t + i, i);
+        }
+        // (transposed products) output r of this lane is gradient column
+        // 4*(lane/16)+r of the wave's tile, in the lane's own row
+        const int nq = n0 + 16 * w + 4 * (lane >> 4);
+#pragma unroll
+        for (int i = 0; i < WFS_TILES; ++i) {
+            const int orow = rp + 16 * i + (lane & 15);
+            if (i < nt && orow < r1) {
+                float* o = a.out + (size_t)orow * a.G + nq;
+                if (nq + 3 < a.G) {
+                    *(float4*)o = make_float4(a.s * acc[i][0], a.s * acc[i][1], a.s * acc[i][2], a.s * acc[i][3]);
+                } else {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        if (nq + r < a.G) o[r] = a.s * acc[i][r];
+                }
+            }
+        }
+    }
+    if (dbw) {                                                     // lanes l, l+16, l+32, l+48 hold column l
+        dbacc += __shfl_xor(dbacc, 16);
+        dbacc += __shfl_xor(dbacc, 32);
+        if (lane < 16 && nc < a.G) a.db[nc] = dbacc;
+    }
+}
+
 // Weight gradient of a site whose keep lists are all the identity (p = 0,
 // or the dense comparison mode, where the mask zeroes the dropped rows):
 // every row takes part at every t, so the accumulators stay in registers
@@ -1164,8 +1470,30 @@ __global__ void __launch_bounds__(128 * WG_NWV) __attribute__((amdgpu_waves_per_
         wgrad_poison(a);
         return;
     }
-    if (a.full) wgrad_full<T, MASKED, WgTiles<T>::N / 2, MULTI>(a, acc_lds);
-    else wgrad_gather<T, MULTI>(a, acc_lds);
+    if (a.full) {
+        if constexpr (sizeof(T) == 2) {
+            if (a.staged) wgrad_full_staged<T, MASKED>(a, acc_lds);
+            else wgrad_full<T, MASKED, WgTiles<T>::N / 2, MULTI>(a, acc_lds);
+        } else wgrad_full<T, MASKED, WgTiles<T>::N / 2, MULTI>(a, acc_lds);
+    } else if constexpr (sizeof(T) == 2) {
+        if (a.staged) wgrad_staged<T>(a, acc_lds);
+        else wgrad_gather<T, MULTI>(a, acc_lds);
+    } else wgrad_gather<T, MULTI>(a, acc_lds);
+}
+
+// The same pass when every problem runs on the staged full kernel (bf16,
+// batch <= 32): built on its own for six waves per SIMD (80 registers), i.e.
+// three workgroups per CU, so that a pass's workgroups (the grid is 64 per
+// 1024 gradient columns and problem) mostly run in one round.
+template <bool MASKED>
+__global__ void __launch_bounds__(128 * WG_NWV) __attribute__((amdgpu_waves_per_eu(6))) k_wgrad_fs(WgBatch bt) {
+    extern __shared__ float stage_lds[];
+    const WgArgs& a = bt.p[blockIdx.z];
+    if (bt.status && *bt.status != 0) {
+        wgrad_poison(a);
+        return;
+    }
+    wgrad_full_staged<bf16, MASKED>(a, stage_lds);
 }
 
 // ---------------------------------------------------------------------------
@@ -1738,6 +2066,24 @@ void launch_dx(const DxArgs& a, int K, hipStream_t st) {
 void launch_wgrad_big(const WgBatch& b, hipStream_t st, hipEvent_t e0, hipEvent_t e1);
 int setup_big_attributes();
 
+// LSTM_SD_WGRAD_STAGED=0 keeps row-sparse problems on the unstaged kernel
+static bool use_wgrad_staged() {
+    const char* v = getenv("LSTM_SD_WGRAD_STAGED");
+    return !(v && v[0] == '0');
+}
+// Whether a row-sparse problem (bf16, batch <= 32) runs on the full kernel
+// with its rows times the mask byte instead of the row-sparse scatter.  At a
+// batch this small a step's products are nearly free, while the scatter
+// pays, at every step, a chain of dependent reads (keep-list range, entries,
+// rows) and an LDS read-modify-write of every kept row; measured at hidden
+// 650 and 256 (batch 20 and 32) and at the AWD-LSTM shape, the full kernel
+// is faster at every rate from 0.3 to 0.9, so it is the default there.
+// LSTM_SD_WGRAD_ROWSPARSE=1 takes the scatter.
+static bool wgrad_as_full() {
+    const char* v = getenv("LSTM_SD_WGRAD_ROWSPARSE");
+    return !(v && v[0] == '1');
+}
+
 template <typename T>
 void launch_wgrad(const WgBatch& b, hipStream_t st) {
     if (b.np == 0) return;
@@ -1747,26 +2093,50 @@ void launch_wgrad(const WgBatch& b, hipStream_t st) {
         launch_wgrad_big(b, st, e0, e1);
         return;
     }
-    const WgArgs& a = b.p[0];                  // the problems share G, B and the mode
+    WgBatch bs = b;
+    const WgArgs& a = bs.p[0];                 // the problems share G, B and the mode
     const int ncb = (a.G + WG_NB - 1) / WG_NB;  // column blocks (wg_slot: 8 XCDs x 8 slices each)
-    const dim3 grid(NXCD * NXCD * ((ncb + NXCD - 1) / NXCD), 1, b.np);
+    const dim3 grid(NXCD * NXCD * ((ncb + NXCD - 1) / NXCD), 1, bs.np);
     size_t lds = 0;
     bool multi = a.B > 32;                     // builds with the extra loops (batch chunks, tile rounds)
-    for (int i = 0; i < b.np; ++i) {
-        if (b.p[i].full) {
-            lds = std::max(lds, wgrad_full_lds_bytes<T>());
+    for (int i = 0; i < bs.np; ++i) {
+        WgArgs& p = bs.p[i];
+        p.staged = p.fullmask = 0;
+        if (p.full) {
+            if (sizeof(T) == 2 && p.B <= 32 && use_wgrad_staged()) {
+                p.staged = 1;
+                lds = std::max(lds, WFS_LDS);
+            } else lds = std::max(lds, wgrad_full_lds_bytes<T>());
             continue;
         }
-        lds = std::max(lds, wgrad_lds_bytes<T>(b.p[i].K));
-        multi = multi || (b.p[i].K + NSEG - 1) / NSEG > 16 * (WgTiles<T>::N / 2);
+        if (sizeof(T) == 2 && p.B <= 32 && use_wgrad_staged() && wgrad_as_full()) {
+            p.full = p.staged = p.fullmask = 1;
+            lds = std::max(lds, WFS_LDS);
+            continue;
+        }
+        if (sizeof(T) == 2 && p.B <= 32 && wgs_rows(p.K) <= WGS_MAX_ROWS && wgs_lds_bytes(p.K, p.T) <= WGS_MAX_LDS &&
+            use_wgrad_staged()) {
+            p.staged = 1;
+            lds = std::max(lds, wgs_lds_bytes(p.K, p.T));
+            continue;
+        }
+        lds = std::max(lds, wgrad_lds_bytes<T>(p.K));
+        multi = multi || (p.K + NSEG - 1) / NSEG > 16 * (WgTiles<T>::N / 2);
     }
     const dim3 blk(128 * WG_NWV);
+    bool all_fs = sizeof(T) == 2;
+    for (int i = 0; i < bs.np; ++i) all_fs = all_fs && bs.p[i].full && bs.p[i].staged;
+    if (all_fs) {
+        if (a.dense) launch_k(KID_WGRAD, k_wgrad_fs<true>, grid, blk, WFS_LDS, st, bs);
+        else launch_k(KID_WGRAD, k_wgrad_fs<false>, grid, blk, WFS_LDS, st, bs);
+        return;
+    }
     if (a.dense) {
-        if (multi) launch_k(KID_WGRAD, k_wgrad<T, true, true>, grid, blk, lds, st, b);
-        else launch_k(KID_WGRAD, k_wgrad<T, true, false>, grid, blk, lds, st, b);
+        if (multi) launch_k(KID_WGRAD, k_wgrad<T, true, true>, grid, blk, lds, st, bs);
+        else launch_k(KID_WGRAD, k_wgrad<T, true, false>, grid, blk, lds, st, bs);
     } else {
-        if (multi) launch_k(KID_WGRAD, k_wgrad<T, false, true>, grid, blk, lds, st, b);
-        else launch_k(KID_WGRAD, k_wgrad<T, false, false>, grid, blk, lds, st, b);
+        if (multi) launch_k(KID_WGRAD, k_wgrad<T, false, true>, grid, blk, lds, st, bs);
+        else launch_k(KID_WGRAD, k_wgrad<T, false, false>, grid, blk, lds, st, bs);
     }
 }
 void launch_bwd_init(const float* dhT, const float* dcT, float* dhc, float* dcs, long n, void* da, int es, int G,
