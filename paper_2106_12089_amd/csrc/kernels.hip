@@ -268,19 +268,40 @@ __global__ void __launch_bounds__(256) k_fx(FxArgs a) {
     for (int ch = 0; ch < nchunk; ++ch) {
         const int buf = ch & 1;
         if (ch + 1 < nchunk) fetch((ch + 1) * FX_KC);
-        Frag<T> fa[2], fb[2];
+        if constexpr (sizeof(T) == 2) {
+            // A: 8 consecutive kept columns of the lane's row, one 16-byte
+            // read; B: column n of the K-major W chunk over 8 rows, two
+            // transposing reads (lanes 4e..4e+3 of a 16-lane group address
+            // columns 0, 4, 8, 12 of row e; lane i receives column i)
+            Raw8<T> fa[2], fb[2];
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+            for (int i = 0; i < 2; ++i) raw_lds(fa[i], &xs[buf][16 * i + cl][g8]);
+            const int e4 = (lane & 15) >> 2, j4 = lane & 3;
 #pragma unroll
-            for (int e = 0; e < 8; ++e) fa[i].v[e] = xs[buf][16 * i + cl][g8 + e];
+            for (int c = 0; c < 2; ++c) {
+                const int nb = 32 * w + 16 * c + 4 * j4;
+                const uint2 lo = lds_tr4(&ws[buf][g8 + e4][nb]), hi = lds_tr4(&ws[buf][g8 + 4 + e4][nb]);
+                fb[c].w[0] = lo.x; fb[c].w[1] = lo.y; fb[c].w[2] = hi.x; fb[c].w[3] = hi.y;
+            }
 #pragma unroll
-        for (int c = 0; c < 2; ++c)
+            for (int i = 0; i < 2; ++i)
 #pragma unroll
-            for (int e = 0; e < 8; ++e) fb[c].v[e] = ws[buf][g8 + e][32 * w + 16 * c + cl];
+                for (int c = 0; c < 2; ++c) raw_mma(fa[i], fb[c], acc[i][c]);
+        } else {
+            Frag<T> fa[2], fb[2];
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+            for (int i = 0; i < 2; ++i)
 #pragma unroll
-            for (int c = 0; c < 2; ++c) mma_16x16x32(fa[i], fb[c], acc[i][c]);
+                for (int e = 0; e < 8; ++e) fa[i].v[e] = xs[buf][16 * i + cl][g8 + e];
+#pragma unroll
+            for (int c = 0; c < 2; ++c)
+#pragma unroll
+                for (int e = 0; e < 8; ++e) fb[c].v[e] = ws[buf][g8 + e][32 * w + 16 * c + cl];
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int c = 0; c < 2; ++c) mma_16x16x32(fa[i], fb[c], acc[i][c]);
+        }
         if (ch + 1 < nchunk) commit(buf ^ 1);
         __syncthreads();
     }
