@@ -546,6 +546,173 @@ size_t wgrad_big_lds() { return WL_LDS; }
 // 64-row groups ahead); it pays off from a few groups per step on.
 bool wgrad_big_fits(int B) { return B >= 64; }
 
+// Weight gradient for large batches as one GEMM per problem, Eq. 11 with
+// every row multiplied by its mask byte (a dropped row contributes an exact
+// zero; identity keep lists need no mask):
+//   dW[k][n] = s * sum over (t, b) of m_t[k] act_t[b][k] da_t[b][n]
+// The contraction runs over all T*B (step, batch) pairs, so each
+// workgroup's accumulators stay in registers for the whole pass: no per-step
+// read-modify-write of an LDS accumulator (the row-sparse kernel above pays
+// one for every kept row at every step, and at 256 rows per step that,
+// with its per-step chain, holds it to about 10% of MFMA peak).
+// grid (8 x row blocks x ceil(column blocks / 8), 1, problems), 512 threads;
+// workgroup = 128 rows x 256 columns; workgroup i runs on XCD i % 8, which
+// takes the column blocks i % 8 + 8j with every row block, so an XCD's L2
+// holds its columns' DA^T for all of its row blocks.  Wave w owns rows
+// 64 (w / 4) .. +63 and columns 64 (w % 4) .. +63 of the tile (4 x 4 MFMA
+// tiles).  The contraction goes in chunks of 32 batch rows of one step: the
+// chunk's 128 activation rows and 256 DA^T columns are loaded once (one or
+// two 16-byte pieces per thread), stored fragment-major in LDS and read by
+// the waves that need them; loads run three chunks ahead (register ring),
+// two stage buffers alternate, one barrier per chunk.  The workgroups of the
+// last row block also sum the bias gradient.
+constexpr int WM_R = 128, WM_C = 256, WM_KC = 32, WM_RING = 3;
+constexpr size_t WM_STAGE = (size_t)(WM_R + WM_C) * WM_KC * 2;    // one stage buffer: 24 KB
+constexpr size_t WM_LDS = 2 * WM_STAGE;
+
+__global__ void __launch_bounds__(512) k_wgrad_gemm(WgBatch bt) {
+    extern __shared__ __align__(16) char smem[];
+    const WgArgs& a = bt.p[blockIdx.z];
+    const int nrb = (a.K + WM_R - 1) / WM_R, ncb = (a.G + WM_C - 1) / WM_C;
+    const int xcd = blockIdx.x % 8, k8 = blockIdx.x / 8;
+    const int rb = k8 % nrb, cb = xcd + 8 * (k8 / nrb);
+    if (cb >= ncb) return;
+    const int r0 = rb * WM_R, n0 = cb * WM_C;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wr = w >> 2, wc = w & 3;
+    const bool dbw = a.db && rb == nrb - 1;
+    if (bt.status && *bt.status != 0) {        // the step's recurrence timed out: NaN in every output
+        const float nan = __builtin_nanf("");
+        for (int i = tid; i < WM_R * WM_C; i += 512) {
+            const int r = r0 + i / WM_C, n = n0 + i % WM_C;
+            if (r < a.K && n < a.G) a.out[(size_t)r * a.G + n] = nan;
+        }
+        if (dbw)
+            for (int n = n0 + tid; n < min(n0 + WM_C, a.G); n += 512) a.db[n] = nan;
+        return;
+    }
+    const bool masked = a.dense || !a.full;    // rows times the mask byte
+    const int nb = (a.B + WM_KC - 1) / WM_KC, nq = a.T * nb;
+    const uint32_t abytes = (uint32_t)a.K * a.BP * 2, bbytes = (uint32_t)a.G * a.BP * 2;
+    // staging pieces of this thread: activation row j, DA^T columns j and
+    // j + 128, batch entries 8 q4 .. +7 of the chunk
+    // (lane l of a wave takes fragment position l of a 16-row tile, so a
+    // wave's LDS stores are one contiguous 1 KB block: no bank conflicts)
+    const int j = (tid & 15) + 16 * (tid >> 6), q4 = (tid >> 4) & 3;
+    const int frag = ((j & 15) + 16 * q4) * 16 + (j >> 4) * 1024;   // fragment-major offset in a 16-row tile
+    const bool rok = r0 + j < a.K;
+    auto act_rsrc = [&](int t) {
+        const bf16* act = (a.actT_first && t == a.t_first) ? (const bf16*)a.actT_first
+                                                           : (const bf16*)a.actT + (long)(t + a.shift) * a.tstride;
+        return buf_rsrc(act, abytes);
+    };
+    u32x4_t ra[WM_RING], rb0[WM_RING], rb1[WM_RING];
+    int mk[WM_RING], bq[WM_RING];
+    auto issue = [&](int q, int sl) {
+        q = q < nq ? q : nq - 1;
+        const int t = q / nb, bc = WM_KC * (q % nb) + 8 * q4;
+        bq[sl] = bc;
+        ra[sl] = __builtin_amdgcn_raw_buffer_load_b128(act_rsrc(t), rok ? (uint32_t)((r0 + j) * a.BP + bc) * 2 : OOB_OFF, 0, 0);
+        const __amdgpu_buffer_rsrc_t br = buf_rsrc((const bf16*)a.daT + (size_t)t * a.G * a.BP, bbytes);
+        rb0[sl] = __builtin_amdgcn_raw_buffer_load_b128(br, n0 + j < a.G ? (uint32_t)((n0 + j) * a.BP + bc) * 2 : OOB_OFF, 0, 0);
+        rb1[sl] = __builtin_amdgcn_raw_buffer_load_b128(
+            br, n0 + 128 + j < a.G ? (uint32_t)((n0 + 128 + j) * a.BP + bc) * 2 : OOB_OFF, 0, 0);
+        // (always issued, past the resource when not masked or past the rows)
+        const __amdgpu_buffer_rsrc_t mr = buf_rsrc(a.site.mask + (size_t)t * a.site.kmax, (uint32_t)a.site.kmax);
+        mk[sl] = (int)__builtin_amdgcn_raw_buffer_load_b8(mr, masked && rok ? (uint32_t)(r0 + j) : OOB_OFF, 0, 0);
+    };
+    auto stage = [&](int buf, int sl) {
+        uint32_t pm[4];
+        pad_mask<bf16>(bq[sl], a.B, pm);
+        char* sb = smem + buf * WM_STAGE;
+        const bool keep = !masked || mk[sl] != 0;
+        const uint4 va = keep ? make_uint4(ra[sl][0] & pm[0], ra[sl][1] & pm[1], ra[sl][2] & pm[2], ra[sl][3] & pm[3])
+                              : make_uint4(0u, 0u, 0u, 0u);
+        *(uint4*)(sb + frag) = va;
+        *(uint4*)(sb + WM_R * WM_KC * 2 + frag) =
+            make_uint4(rb0[sl][0] & pm[0], rb0[sl][1] & pm[1], rb0[sl][2] & pm[2], rb0[sl][3] & pm[3]);
+        *(uint4*)(sb + WM_R * WM_KC * 2 + 8 * 1024 + frag) =
+            make_uint4(rb1[sl][0] & pm[0], rb1[sl][1] & pm[1], rb1[sl][2] & pm[2], rb1[sl][3] & pm[3]);
+    };
+    f32x4_t acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc[i][c] = f32x4_t{0, 0, 0, 0};
+    float dbacc[4] = {0.f, 0.f, 0.f, 0.f};
+    auto multiply = [&](int buf) {
+        const char* sb = smem + buf * WM_STAGE;
+        Raw8<bf16> fb[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            raw_lds(fb[c], (const bf16*)(sb + WM_R * WM_KC * 2 + (4 * wc + c) * 1024 + lane * 16));
+            if (dbw && wr == 0) db_add_raw(fb[c], dbacc[c]);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            Raw8<bf16> fa;
+            raw_lds(fa, (const bf16*)(sb + (4 * wr + i) * 1024 + lane * 16));
+#pragma unroll
+            for (int c = 0; c < 4; ++c) raw_mma(fb[c], fa, acc[i][c]);
+        }
+    };
+    // chunk q: stage q+1 (its loads went out two chunks earlier) into the
+    // other buffer, multiply q, then its slot takes the loads of q+3
+    auto iter = [&](int q, int sl) {
+        stage((q + 1) & 1, (sl + 1) % WM_RING);
+        if (q < nq) multiply(q & 1);
+        issue(q + WM_RING, sl);
+        __syncthreads();
+    };
+#pragma unroll
+    for (int i = 0; i < WM_RING; ++i) issue(i, i);
+    stage(0, 0);
+    __syncthreads();
+    for (int q = 0; q < nq; q += WM_RING) {
+#pragma unroll
+        for (int i = 0; i < WM_RING; ++i) iter(q + i, i);
+    }
+    // (transposed products) output r of this lane is gradient column
+    // 4*(lane/16)+r of the column tile, in the lane's own row
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int row = r0 + 64 * wr + 16 * i + (lane & 15);
+        if (row >= a.K) continue;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const int nq4 = n0 + 64 * wc + 16 * c + 4 * (lane >> 4);
+            float* o = a.out + (size_t)row * a.G + nq4;
+            if (nq4 + 3 < a.G) {
+                *(float4*)o = make_float4(a.s * acc[i][c][0], a.s * acc[i][c][1], a.s * acc[i][c][2], a.s * acc[i][c][3]);
+            } else {
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    if (nq4 + r < a.G) o[r] = a.s * acc[i][c][r];
+            }
+        }
+    }
+    if (dbw && wr == 0) {                      // lanes l, l+16, l+32, l+48 hold column l of each tile
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            float v = dbacc[c];
+            v += __shfl_xor(v, 16);
+            v += __shfl_xor(v, 32);
+            const int n = n0 + 64 * wc + 16 * c + (lane & 15);
+            if (lane < 16 && n < a.G) a.db[n] = v;
+        }
+    }
+}
+
+void launch_wgrad_gemm(const WgBatch& b, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
+    int nx = 0;                                // 8 x (row blocks) x ceil(column blocks / 8)
+    for (int i = 0; i < b.np; ++i)
+        nx = std::max(nx, 8 * ((b.p[i].K + WM_R - 1) / WM_R) * (((b.p[i].G + WM_C - 1) / WM_C + 7) / 8));
+    const dim3 grid(nx, 1, b.np), blk(512);
+    if (e0 && e1) hipExtLaunchKernelGGL(k_wgrad_gemm, grid, blk, (uint32_t)WM_LDS, st, e0, e1, 0, b);
+    else k_wgrad_gemm<<<grid, blk, WM_LDS, st>>>(b);
+}
+
 void launch_wgrad_big(const WgBatch& b, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
     int nx = 0;                                // 8 x (row slices) x ceil(column blocks / 8)
     for (int i = 0; i < b.np; ++i)

@@ -140,6 +140,18 @@ __device__ __forceinline__ void raw_mma(const Raw8<float>& a, const Raw8<float>&
         c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w[e]), __uint_as_float(b.w[e]), c, 0, 0, 0);
 }
 
+// column sums of a packed fragment (bias gradient)
+template <typename T>
+__device__ __forceinline__ void db_add_raw(const Raw8<T>& f, float& acc) {
+    if (sizeof(T) == 2) {
+#pragma unroll
+        for (int q = 0; q < Raw8<T>::NW; ++q) acc += __uint_as_float(f.w[q] << 16) + __uint_as_float(f.w[q] & 0xffff0000u);
+    } else {
+#pragma unroll
+        for (int q = 0; q < Raw8<T>::NW; ++q) acc += __uint_as_float(f.w[q]);
+    }
+}
+
 // 8 elements from LDS (16-byte aligned)
 template <typename T>
 __device__ __forceinline__ void raw_lds(Raw8<T>& f, const T* p) {

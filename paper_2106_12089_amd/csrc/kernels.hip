@@ -665,18 +665,6 @@ __global__ void __launch_bounds__(256) k_dx(DxArgs a) {
     }
 }
 
-// column sums of a packed fragment (bias gradient)
-template <typename T>
-__device__ __forceinline__ void db_add_raw(const Raw8<T>& f, float& acc) {
-    if (sizeof(T) == 2) {
-#pragma unroll
-        for (int q = 0; q < Raw8<T>::NW; ++q) acc += __uint_as_float(f.w[q] << 16) + __uint_as_float(f.w[q] & 0xffff0000u);
-    } else {
-#pragma unroll
-        for (int q = 0; q < Raw8<T>::NW; ++q) acc += __uint_as_float(f.w[q]);
-    }
-}
-
 // ---------------------------------------------------------------------------
 // Row-sparse weight gradient (Eq. 11; Sec. 3.2 WG).  grid (64 *
 // ceil(G/1024), 1, problems), block 512 (8 waves), dynamic LDS (rows of a
@@ -993,10 +981,10 @@ __device__ __forceinline__ void wgrad_gather(const WgArgs& a, float* acc_lds) {
 // the same gathered rows, the two halves the same DA^T columns, so the
 // vector memory pipe moved about three times the step's data and set the
 // step time.  Here the 512 threads load a step's operands once, one 16-byte
-// piece each: thread i takes piece i % 4 (8 batch entries) of DA^T column
-// i / 4 of the block (8 KB, one piece per thread) and of the step's kept row
-// i / 4 of the slice (gathered through the keep list; absent rows read past
-// the resource, i.e. zeros), and stores them fragment-major in LDS, with
+// piece each: a piece is 8 batch entries of a DA^T column of the block (8
+// KB, one piece per thread) and of a kept row of the step in the slice
+// (gathered through the keep list; absent rows read past the resource,
+// i.e. zeros), and the threads store them fragment-major in LDS, with
 // the accumulator row offset of each kept row beside them.  Wave w then
 // multiplies DA^T column tile w with every kept-row tile of the step and
 // adds the tiles into its 16 columns of the LDS accumulator.  Loads run two
@@ -1027,7 +1015,9 @@ __device__ __forceinline__ void wgrad_staged(const WgArgs& a, float* lds) {
     __syncthreads();
 
     // this thread's piece: row / column j of the step, batch entries 8q .. 8q+7
-    const int j = tid >> 2, q = tid & 3;
+    // (lane l of a wave takes fragment position l of a 16-row tile: a wave's
+    // LDS stores are one contiguous 1 KB block, free of bank conflicts)
+    const int j = (tid & 15) + 16 * (tid >> 6), q = (tid >> 4) & 3;
     uint32_t pm[4];
     pad_mask<T>(8 * q, a.B, pm);
     const uint32_t abytes = (uint32_t)a.K * a.BP * 2, bbytes = (uint32_t)a.G * a.BP * 2;
@@ -1158,8 +1148,8 @@ __device__ __forceinline__ void wgrad_staged(const WgArgs& a, float* lds) {
 // loaded straight into registers: no other wave reads it) and every row of
 // the slice, in passes of up to 6 row tiles whose accumulators stay in
 // registers over all steps.  The rows are the operand every wave shares: the
-// 512 threads load a step's rows once (one 16-byte piece each: row i / 4,
-// batch entries 8(i % 4) .. +7, zeroed when the row is dropped) and store
+// 512 threads load a step's rows once (one 16-byte piece each: 8 batch
+// entries of one row, zeroed when the row is dropped) and store
 // them fragment-major in LDS, where each wave reads its fragments.  Loads
 // run three steps ahead (register ring), the two stage buffers alternate,
 // one barrier per step.
@@ -1178,7 +1168,9 @@ __device__ __forceinline__ void wgrad_full_staged(const WgArgs& a, float* lds) {
     const int n0 = cb * WG_NB, nc = n0 + 16 * w + (lane & 15), g8 = 8 * (lane >> 4);
     const int r0 = slice_start(x, a.K), r1 = slice_start(x + 1, a.K);
     char* stg = (char*)lds;
-    const int j = tid >> 2, q = tid & 3;                           // staging: row j of the pass, piece q
+    // staging: row j of the pass, piece q (lane l of a wave takes fragment
+    // position l of a 16-row tile: its LDS stores are free of bank conflicts)
+    const int j = (tid & 15) + 16 * (tid >> 6), q = (tid >> 4) & 3;
     const bool srow = j < 16 * WFS_TILES;
     const int frag = ((j & 15) + 16 * q) * 16 + (j >> 4) * 1024;   // fragment-major LDS offset of the piece
     uint32_t pm[4], pmb[4];
@@ -2085,7 +2077,14 @@ void launch_dx(const DxArgs& a, int K, hipStream_t st) {
     else launch_k(KID_DX, k_dx<T, 4>, grid, dim3(256), 0, st, a);
 }
 void launch_wgrad_big(const WgBatch& b, hipStream_t st, hipEvent_t e0, hipEvent_t e1);
+void launch_wgrad_gemm(const WgBatch& b, hipStream_t st, hipEvent_t e0, hipEvent_t e1);
 int setup_big_attributes();
+// LSTM_SD_WGRAD_GEMM=0: the large-batch weight gradients on the row-sparse
+// kernel (per-step gathered rows) instead of the mask-multiplied GEMM
+static bool use_wgrad_gemm() {
+    const char* v = getenv("LSTM_SD_WGRAD_GEMM");
+    return !(v && v[0] == '0');
+}
 
 // LSTM_SD_WGRAD_STAGED=0 keeps row-sparse problems on the unstaged kernel
 static bool use_wgrad_staged() {
@@ -2108,10 +2107,14 @@ static bool wgrad_as_full() {
 template <typename T>
 void launch_wgrad(const WgBatch& b, hipStream_t st) {
     if (b.np == 0) return;
-    if (b.big && sizeof(T) == 2) {             // large batch (bf16): the register-accumulated kernel
+    // bf16 past 32 batch rows: one GEMM per problem over every (step, batch
+    // row) pair, rows times the mask byte; or (LSTM_SD_WGRAD_GEMM=0) the
+    // large-batch row-sparse kernel where it applies
+    if (sizeof(T) == 2 && (b.big || b.p[0].B > 32) && (use_wgrad_gemm() || b.big)) {
         hipEvent_t e0 = nullptr, e1 = nullptr;
         if (g_timer_kid == KID_WGRAD) { e0 = timer_event(); e1 = timer_event(); }
-        launch_wgrad_big(b, st, e0, e1);
+        if (use_wgrad_gemm()) launch_wgrad_gemm(b, st, e0, e1);
+        else launch_wgrad_big(b, st, e0, e1);
         return;
     }
     WgBatch bs = b;

@@ -6,7 +6,8 @@ forced with LSTM_SD_BIG=2 (it otherwise runs only where the row-group
 tiling of the other persistent forward does not fit, as at the stress
 shape): hidden sizes that are not multiples of the 32-neuron chunk or of the
 16-unit tile, batches that are not multiples of the 64-row group or of the
-16-row MFMA tile, both directions, per-row lengths, and both modes."""
+16-row MFMA tile, both directions, per-row lengths, and both modes; the
+weight gradients on the default GEMM and on the row-sparse kernel."""
 import dataclasses
 
 import numpy as np
@@ -56,6 +57,29 @@ def test_big_forward_ragged(shape, mode, monkeypatch):
     if cfg.min_len is not None:
         valid = np.arange(cfg.seq_len)[:, None] < wl.lengths[None, :]
         assert np.all(gpu["y"][~valid] == 0.0)
+
+
+@pytest.mark.parametrize("shape", [
+    dict(num_layers=2, num_dirs=1, input_dim=70, hidden=45, batch=70, seq_len=5),
+    dict(num_layers=2, num_dirs=2, input_dim=200, hidden=72, batch=300, seq_len=3),
+])
+@pytest.mark.parametrize("mode", [(0.5, 0.5, 1), (0.5, 0.5, 0)])
+def test_big_wgrad_rowsparse_kernel(shape, mode, monkeypatch):
+    """The large-batch row-sparse weight-gradient kernel (per-step gathered
+    rows; LSTM_SD_WGRAD_GEMM=0) in place of the default mask-multiplied
+    GEMM."""
+    monkeypatch.setenv("LSTM_SD_BIG", "2")
+    monkeypatch.setenv("LSTM_SD_WGRAD_GEMM", "0")
+    base = workloads.get_config("tiny")
+    cfg = dataclasses.replace(base, name="big", dtype="bf16", loss="mse", **shape)
+    wl = workloads.make_workload(cfg)
+    p_nr, p_rh, compact = mode
+    say(f"[gpu] big row-sparse wgrad {shape} p_nr={p_nr} p_rh={p_rh} compact={compact}")
+    gpu, ref = _run(cfg, wl, p_nr, p_rh, compact)
+    errs = compare(gpu, ref)
+    say("   errs", summary(errs))
+    bad = {k: v for k, v in errs.items() if not v <= TOL["bf16"]}
+    assert not bad, bad
 
 
 @pytest.mark.parametrize("mode", [(0.3, 0.0, 1), (0.5, 0.5, 1), (0.5, 0.5, 0)])
