@@ -563,12 +563,14 @@ bool wgrad_big_fits(int B) { return B >= 64; }
 // tiles).  The contraction goes in chunks of 32 batch rows of one step: the
 // chunk's 128 activation rows and 256 DA^T columns are loaded once (one or
 // two 16-byte pieces per thread), stored fragment-major in LDS and read by
-// the waves that need them; loads run three chunks ahead (register ring),
-// two stage buffers alternate, one barrier per chunk.  The workgroups of the
+// the waves that need them.  Loads run up to five chunks ahead (register
+// ring), three stage buffers rotate (a chunk is staged two chunks before it
+// is multiplied), and each wave reads the fragments of the next chunk from
+// LDS while it multiplies the current one; one barrier per chunk.  The workgroups of the
 // last row block also sum the bias gradient.
 constexpr int WM_R = 128, WM_C = 256, WM_KC = 32, WM_RING = 3;
 constexpr size_t WM_STAGE = (size_t)(WM_R + WM_C) * WM_KC * 2;    // one stage buffer: 24 KB
-constexpr size_t WM_LDS = 2 * WM_STAGE;
+constexpr size_t WM_LDS = 3 * WM_STAGE;
 
 __global__ void __launch_bounds__(512) k_wgrad_gemm(WgBatch bt) {
     extern __shared__ __align__(16) char smem[];
@@ -641,37 +643,47 @@ __global__ void __launch_bounds__(512) k_wgrad_gemm(WgBatch bt) {
 #pragma unroll
         for (int c = 0; c < 4; ++c) acc[i][c] = f32x4_t{0, 0, 0, 0};
     float dbacc[4] = {0.f, 0.f, 0.f, 0.f};
-    auto multiply = [&](int buf) {
+    // fragments of two chunks in registers: those of chunk q+1 are read
+    // from LDS while chunk q is multiplied
+    Raw8<bf16> fa[2][4], fb[2][4];
+    auto frags = [&](int buf, int fs) {
         const char* sb = smem + buf * WM_STAGE;
-        Raw8<bf16> fb[4];
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            raw_lds(fb[c], (const bf16*)(sb + WM_R * WM_KC * 2 + (4 * wc + c) * 1024 + lane * 16));
-            if (dbw && wr == 0) db_add_raw(fb[c], dbacc[c]);
-        }
+        for (int c = 0; c < 4; ++c) raw_lds(fb[fs][c], (const bf16*)(sb + WM_R * WM_KC * 2 + (4 * wc + c) * 1024 + lane * 16));
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            Raw8<bf16> fa;
-            raw_lds(fa, (const bf16*)(sb + (4 * wr + i) * 1024 + lane * 16));
-#pragma unroll
-            for (int c = 0; c < 4; ++c) raw_mma(fb[c], fa, acc[i][c]);
-        }
+        for (int i = 0; i < 4; ++i) raw_lds(fa[fs][i], (const bf16*)(sb + (4 * wr + i) * 1024 + lane * 16));
     };
-    // chunk q: stage q+1 (its loads went out two chunks earlier) into the
-    // other buffer, multiply q, then its slot takes the loads of q+3
-    auto iter = [&](int q, int sl) {
-        stage((q + 1) & 1, (sl + 1) % WM_RING);
-        if (q < nq) multiply(q & 1);
-        issue(q + WM_RING, sl);
+    auto multiply = [&](int fs) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+            if (dbw && wr == 0) db_add_raw(fb[fs][c], dbacc[c]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int c = 0; c < 4; ++c) raw_mma(fb[fs][c], fa[fs][i], acc[i][c]);
+    };
+    // chunk q: stage q+2 (its loads went out two chunks earlier) into the
+    // third buffer, read the fragments of q+1, multiply q, then the slot of
+    // q+2 takes the loads of q+2+WM_RING
+    // (sl = q % WM_RING and fs = q % 2, passed as constants of the unrolled loop)
+    auto iter = [&](int q, int sl, int fs) {
+        stage((q + 2) % 3, (sl + 2) % WM_RING);
+        frags((q + 1) % 3, fs ^ 1);
+        if (q < nq) multiply(fs);
+        issue(q + 2 + WM_RING, (sl + 2) % WM_RING);
         __syncthreads();
     };
 #pragma unroll
     for (int i = 0; i < WM_RING; ++i) issue(i, i);
     stage(0, 0);
+    stage(1, 1);
+    issue(WM_RING, 0);
+    issue(WM_RING + 1, 1);
     __syncthreads();
-    for (int q = 0; q < nq; q += WM_RING) {
+    frags(0, 0);
+    for (int q = 0; q < nq; q += 2 * WM_RING) {
 #pragma unroll
-        for (int i = 0; i < WM_RING; ++i) iter(q + i, i);
+        for (int i = 0; i < 2 * WM_RING; ++i) iter(q + i, i % WM_RING, i & 1);
     }
     // (transposed products) output r of this lane is gradient column
     // 4*(lane/16)+r of the column tile, in the lane's own row
@@ -728,6 +740,8 @@ int setup_big_attributes() {
     ok = hipFuncSetAttribute((const void*)k_fx_big, hipFuncAttributeMaxDynamicSharedMemorySize, (int)FB_LDS) ==
              hipSuccess && ok;
     ok = hipFuncSetAttribute((const void*)k_dx_big, hipFuncAttributeMaxDynamicSharedMemorySize, (int)DB_LDS) ==
+             hipSuccess && ok;
+    ok = hipFuncSetAttribute((const void*)k_wgrad_gemm, hipFuncAttributeMaxDynamicSharedMemorySize, (int)WM_LDS) ==
              hipSuccess && ok;
     return ok ? 0 : -1;
 }
