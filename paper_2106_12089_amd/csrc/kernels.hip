@@ -1900,15 +1900,31 @@ __global__ void __launch_bounds__(256) k_mse(const float* y, const float* tg, co
     __shared__ float red[256];
     const float N = nvalid_rows(lengths, B, T) * (float)F;
     const float inv = N > 0.f ? 2.0f / N : 0.0f;
-    const long n = (long)T * B * F;
+    // a row (t, b) per workgroup at a time, its features over the threads
+    // (16 bytes each when the rows allow it): no per-element division
+    const int nrows = T * B;
+    const bool vec = (F & 3) == 0 && ((reinterpret_cast<uintptr_t>(y) | reinterpret_cast<uintptr_t>(tg) |
+                                       reinterpret_cast<uintptr_t>(dy)) & 15) == 0;
     float acc = 0.f;
-    for (long i = blockIdx.x * (long)blockDim.x + threadIdx.x; i < n; i += (long)gridDim.x * blockDim.x) {
-        const long tb = i / F;
-        const int t = (int)(tb / B), b = (int)(tb % B);
+    for (int r = blockIdx.x; r < nrows; r += gridDim.x) {
+        const int t = r / B, b = r - t * B;
         const bool valid = !lengths || t < lengths[b];
-        const float d = valid ? y[i] - tg[i] : 0.0f;
-        dy[i] = inv * d;
-        acc += d * d;
+        const size_t o = (size_t)r * F;
+        if (vec) {
+            for (int f = 4 * threadIdx.x; f < F; f += 4 * blockDim.x) {
+                const float4 yv = *(const float4*)(y + o + f), tv = *(const float4*)(tg + o + f);
+                const float4 d = valid ? make_float4(yv.x - tv.x, yv.y - tv.y, yv.z - tv.z, yv.w - tv.w)
+                                       : make_float4(0.f, 0.f, 0.f, 0.f);
+                *(float4*)(dy + o + f) = make_float4(inv * d.x, inv * d.y, inv * d.z, inv * d.w);
+                acc += d.x * d.x + d.y * d.y + d.z * d.z + d.w * d.w;
+            }
+        } else {
+            for (int f = threadIdx.x; f < F; f += blockDim.x) {
+                const float d = valid ? y[o + f] - tg[o + f] : 0.0f;
+                dy[o + f] = inv * d;
+                acc += d * d;
+            }
+        }
     }
     red[threadIdx.x] = acc;
     __syncthreads();
