@@ -671,6 +671,27 @@ def summarize_stats(path, command):
     return "\n".join(lines)
 
 
+def summarize_trace(path, command):
+    """Markdown table of a rocprofv3 --kernel-trace CSV grouped by kernel and
+    grid (workgroups x, y, z), so that launches of one kernel on different
+    problems (the LSTM's and the output head's) stand apart.  Microseconds."""
+    import csv
+    import collections
+    agg = collections.defaultdict(list)
+    for r in csv.DictReader(open(path)):
+        name = r["Kernel_Name"].split("(")[0].replace("void ", "")
+        if not name.startswith("lsd::"):
+            continue
+        grid = tuple(int(r[f"Grid_Size_{a}"]) // max(1, int(r[f"Workgroup_Size_{a}"])) for a in "XYZ")
+        agg[(name, grid)].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    lines = [f"Command: `{command}`", "", "| Kernel | Grid (workgroups) | Calls | Average | Min | Max |",
+             "|---|---|---:|---:|---:|---:|"]
+    for (name, grid), v in sorted(agg.items(), key=lambda kv: -sum(kv[1])):
+        lines.append(f"| `{name[:70]}` | {grid[0]} x {grid[1]} x {grid[2]} | {len(v)} | {sum(v) / len(v):.2f} | "
+                     f"{min(v):.2f} | {max(v):.2f} |")
+    return "\n".join(lines)
+
+
 def summarize_counters(fetch_csv, write_csv, copy_bytes, workload, command):
     """Turn two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE; KiB per
     dispatch) into HBM bytes per launch of each kernel class.  Each counter is
@@ -733,6 +754,8 @@ def main(argv=None):
     ap.add_argument("--counter-command", default="", help="command recorded with the summaries")
     ap.add_argument("--summarize-pmc", nargs="+", metavar="CSV",
                     help="print a markdown summary of rocprofv3 --pmc counter CSVs per kernel class and exit (no GPU)")
+    ap.add_argument("--summarize-trace", metavar="CSV",
+                    help="print a markdown table of a rocprofv3 kernel-trace CSV by kernel and grid, and exit")
     ap.add_argument("--summarize-stats", metavar="CSV",
                     help="print a markdown table of a rocprofv3 --stats kernel summary and exit (no GPU)")
     args = ap.parse_args(argv)
@@ -741,6 +764,9 @@ def main(argv=None):
         return 0
     if args.summarize_stats:
         print(summarize_stats(args.summarize_stats, args.counter_command))
+        return 0
+    if args.summarize_trace:
+        print(summarize_trace(args.summarize_trace, args.counter_command))
         return 0
     if args.summarize_counters:
         out = summarize_counters(*args.summarize_counters, copy_bytes=args.calibrate_copy * (1 << 20),
