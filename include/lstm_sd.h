@@ -31,7 +31,11 @@
  *   - compact = 1 skips dropped rows/columns (the method); compact = 0 runs
  *     the same kernels over every row with the mask applied as a
  *     multiplier (the dense baseline).  Both give the same result up to
- *     floating-point summation order.
+ *     floating-point summation order.  The weight gradients (bf16) sum every
+ *     step with each row multiplied by its mask byte in both modes: on this
+ *     device that is faster than the row-sparse form of Eq. 11, which the
+ *     environment selects with LSTM_SD_WGRAD_ROWSPARSE=1 (batch <= 32) or
+ *     LSTM_SD_WGRAD_GEMM=0 (batch >= 128); the result is the same.
  *   - Optional per-row lengths [B] (int32, device): rows freeze h and c and
  *     output 0 from t = lengths[b] on; lengths outside [0, T] are clamped.
  *
