@@ -35,7 +35,7 @@
  *     step with each row multiplied by its mask byte in both modes: on this
  *     device that is faster than the row-sparse form of Eq. 11, which the
  *     environment selects with LSTM_SD_WGRAD_ROWSPARSE=1 (batch <= 32) or
- *     LSTM_SD_WGRAD_GEMM=0 (batch >= 128); the result is the same.
+ *     LSTM_SD_WGRAD_GEMM=0 (batch > 32); the result is the same.
  *   - Optional per-row lengths [B] (int32, device): rows freeze h and c and
  *     output 0 from t = lengths[b] on; lengths outside [0, T] are clamped.
  *
