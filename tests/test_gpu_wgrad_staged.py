@@ -108,3 +108,26 @@ def test_wgrad_staged_repeats_bit_identical():
             continue
         diff = [k for k in ref if not np.array_equal(ref[k], cur[k])]
         assert not diff, (it, diff)
+
+
+@pytest.mark.parametrize("mode", [(0.5, 0.5, 1), (0.5, 0.5, 0), (0.3, 0.0, 1)])
+def test_wgrad_batch_above_32_both_kernels(mode, monkeypatch):
+    """A batch of 48 (bf16): the default mask-multiplied GEMM, and with
+    LSTM_SD_WGRAD_GEMM=0 the unstaged kernels (the row-sparse scatter and the
+    full kernel, two 32-row batch chunks)."""
+    from oracle import masks as om
+    base = workloads.get_config("tiny")
+    cfg = dataclasses.replace(base, name="wgs", dtype="bf16", loss="mse", num_layers=2, num_dirs=1,
+                              input_dim=150, hidden=60, batch=48, seq_len=6)
+    wl = workloads.make_workload(cfg)
+    p_nr, p_rh, compact = mode
+    m_nr, m_rh = om.all_masks(cfg.mask_seed, 0, cfg.num_layers, cfg.num_dirs, cfg.seq_len, cfg.k_in,
+                              cfg.hidden, p_nr, p_rh)
+    ref = oracle_step(wl, p_nr, p_rh, m_nr, m_rh)
+    for gemm in ("1", "0"):
+        monkeypatch.setenv("LSTM_SD_WGRAD_GEMM", gemm)
+        say(f"[gpu] batch 48 weight gradient gemm={gemm} p_nr={p_nr} p_rh={p_rh} compact={compact}")
+        errs = compare(_gpu(cfg, wl, p_nr, p_rh, compact), ref)
+        say("   errs", summary(errs))
+        bad = {k: v for k, v in errs.items() if not v <= TOL["bf16"]}
+        assert not bad, (gemm, bad)
