@@ -609,24 +609,44 @@ __global__ void __launch_bounds__(512) k_wgrad_gemm(WgBatch bt) {
                                                            : (const bf16*)a.actT + (long)(t + a.shift) * a.tstride;
         return buf_rsrc(act, abytes);
     };
+    // per-thread byte offsets of the pieces within a step's blocks (chunk 0);
+    // chunk c of the step adds 64 c bytes (out-of-range offsets stay so)
+    const uint32_t aoff = rok ? (uint32_t)((r0 + j) * a.BP + 8 * q4) * 2 : OOB_OFF;
+    const uint32_t boff0 = n0 + j < a.G ? (uint32_t)((n0 + j) * a.BP + 8 * q4) * 2 : OOB_OFF;
+    const uint32_t boff1 = n0 + 128 + j < a.G ? (uint32_t)((n0 + 128 + j) * a.BP + 8 * q4) * 2 : OOB_OFF;
+    const uint32_t moff = masked && rok ? (uint32_t)(r0 + j) : OOB_OFF;
+    const bool padb = (a.B & (WM_KC - 1)) != 0;   // the last chunk of a step holds padding rows
+    auto dat_rsrc = [&](int t) { return buf_rsrc((const bf16*)a.daT + (size_t)t * a.G * a.BP, bbytes); };
+    auto msk_rsrc = [&](int t) { return buf_rsrc(a.site.mask + (size_t)t * a.site.kmax, (uint32_t)a.site.kmax); };
+    // the next chunk to load (chunks go out in order): its step, its index
+    // in the step, its index, and the step's resources; past the last chunk
+    // the last one is loaded again
+    int it = 0, ic = 0, iq = 0;
+    __amdgpu_buffer_rsrc_t ar = act_rsrc(0), br = dat_rsrc(0), mr = msk_rsrc(0);
     u32x4_t ra[WM_RING], rb0[WM_RING], rb1[WM_RING];
     int mk[WM_RING], bq[WM_RING];
-    auto issue = [&](int q, int sl) {
-        q = q < nq ? q : nq - 1;
-        const int t = q / nb, bc = WM_KC * (q % nb) + 8 * q4;
-        bq[sl] = bc;
-        ra[sl] = __builtin_amdgcn_raw_buffer_load_b128(act_rsrc(t), rok ? (uint32_t)((r0 + j) * a.BP + bc) * 2 : OOB_OFF, 0, 0);
-        const __amdgpu_buffer_rsrc_t br = buf_rsrc((const bf16*)a.daT + (size_t)t * a.G * a.BP, bbytes);
-        rb0[sl] = __builtin_amdgcn_raw_buffer_load_b128(br, n0 + j < a.G ? (uint32_t)((n0 + j) * a.BP + bc) * 2 : OOB_OFF, 0, 0);
-        rb1[sl] = __builtin_amdgcn_raw_buffer_load_b128(
-            br, n0 + 128 + j < a.G ? (uint32_t)((n0 + 128 + j) * a.BP + bc) * 2 : OOB_OFF, 0, 0);
+    auto issue = [&](int sl) {
+        const uint32_t co = 64u * ic;
+        bq[sl] = WM_KC * ic + 8 * q4;
+        ra[sl] = __builtin_amdgcn_raw_buffer_load_b128(ar, aoff + co, 0, 0);
+        rb0[sl] = __builtin_amdgcn_raw_buffer_load_b128(br, boff0 + co, 0, 0);
+        rb1[sl] = __builtin_amdgcn_raw_buffer_load_b128(br, boff1 + co, 0, 0);
         // (always issued, past the resource when not masked or past the rows)
-        const __amdgpu_buffer_rsrc_t mr = buf_rsrc(a.site.mask + (size_t)t * a.site.kmax, (uint32_t)a.site.kmax);
-        mk[sl] = (int)__builtin_amdgcn_raw_buffer_load_b8(mr, masked && rok ? (uint32_t)(r0 + j) : OOB_OFF, 0, 0);
+        mk[sl] = (int)__builtin_amdgcn_raw_buffer_load_b8(mr, moff, 0, 0);
+        if (iq + 1 < nq) {
+            ++iq;
+            if (++ic == nb) {
+                ic = 0;
+                ++it;
+                ar = act_rsrc(it);
+                br = dat_rsrc(it);
+                mr = msk_rsrc(it);
+            }
+        }
     };
     auto stage = [&](int buf, int sl) {
-        uint32_t pm[4];
-        pad_mask<bf16>(bq[sl], a.B, pm);
+        uint32_t pm[4] = {~0u, ~0u, ~0u, ~0u};
+        if (padb) pad_mask<bf16>(bq[sl], a.B, pm);
         char* sb = smem + buf * WM_STAGE;
         const bool keep = !masked || mk[sl] != 0;
         const uint4 va = keep ? make_uint4(ra[sl][0] & pm[0], ra[sl][1] & pm[1], ra[sl][2] & pm[2], ra[sl][3] & pm[3])
@@ -670,15 +690,15 @@ __global__ void __launch_bounds__(512) k_wgrad_gemm(WgBatch bt) {
         stage((q + 2) % 3, (sl + 2) % WM_RING);
         frags((q + 1) % 3, fs ^ 1);
         if (q < nq) multiply(fs);
-        issue(q + 2 + WM_RING, (sl + 2) % WM_RING);
+        issue((sl + 2) % WM_RING);               // (chunk q + 2 + WM_RING)
         __syncthreads();
     };
 #pragma unroll
-    for (int i = 0; i < WM_RING; ++i) issue(i, i);
+    for (int i = 0; i < WM_RING; ++i) issue(i);
     stage(0, 0);
     stage(1, 1);
-    issue(WM_RING, 0);
-    issue(WM_RING + 1, 1);
+    issue(0);
+    issue(1);
     __syncthreads();
     frags(0, 0);
     for (int q = 0; q < nq; q += 2 * WM_RING) {
