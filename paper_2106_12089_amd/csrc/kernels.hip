@@ -1144,44 +1144,60 @@ __device__ __forceinline__ void wgrad_staged(const WgArgs& a, float* lds) {
 // comparison mode, or a row-sparse problem routed here: in the last two the
 // mask byte zeroes the dropped rows) with LDS-staged rows (bf16, batch <=
 // 32).  Same grid and slots as the kernels above.
-// Wave w owns DA^T column tile w of the block (16 columns, its fragment
-// loaded straight into registers: no other wave reads it) and every row of
-// the slice, in passes of up to 6 row tiles whose accumulators stay in
-// registers over all steps.  The rows are the operand every wave shares: the
-// 512 threads load a step's rows once (one 16-byte piece each: 8 batch
-// entries of one row, zeroed when the row is dropped) and store
-// them fragment-major in LDS, where each wave reads its fragments.  Loads
-// run three steps ahead (register ring), the two stage buffers alternate,
-// one barrier per step.
+// Wave w owns CT DA^T column tiles of the block (16 columns each, their
+// fragments loaded straight into registers: no other wave reads them) and
+// every row of the slice, in passes of up to 6 row tiles whose accumulators
+// stay in registers over all steps.  The rows are the operand every wave
+// shares: the workgroup loads a step's rows once (16-byte pieces: 8 batch
+// entries of one row, zeroed when the row is dropped) and stores them
+// fragment-major in LDS, where each wave reads its fragments; each fragment
+// read feeds CT products.  Loads run three steps ahead (register ring), the
+// two stage buffers alternate, one barrier per step.  8/CT waves.
 constexpr int WFS_TILES = 6;               // 16-row tiles of a pass
 constexpr int WFS_RING = 3;                // steps whose loads are in flight
 constexpr size_t WFS_LDS = 2 * WFS_TILES * 1024;
 
-template <typename T, bool MASKED>
+template <typename T, bool MASKED, int CT = 1>
 __device__ __forceinline__ void wgrad_full_staged(const WgArgs& a, float* lds) {
     static_assert(sizeof(T) == 2, "bf16 only");
+    constexpr int NTH = 512 / CT;                               // threads
+    constexpr int PP = (64 * WFS_TILES + NTH - 1) / NTH;        // staged pieces per thread and step
     int x, cb;
     wg_slot(x, cb);
     if (cb * WG_NB >= a.G) return;
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);     // (wave-uniform)
-    const int n0 = cb * WG_NB, nc = n0 + 16 * w + (lane & 15), g8 = 8 * (lane >> 4);
+    const int n0 = cb * WG_NB, g8 = 8 * (lane >> 4);
+    int nc[CT];
+#pragma unroll
+    for (int h = 0; h < CT; ++h) nc[h] = n0 + 16 * (CT * w + h) + (lane & 15);
     const int r0 = slice_start(x, a.K), r1 = slice_start(x + 1, a.K);
     char* stg = (char*)lds;
-    // staging: row j of the pass, piece q (lane l of a wave takes fragment
-    // position l of a 16-row tile: its LDS stores are free of bank conflicts)
-    const int j = (tid & 15) + 16 * (tid >> 6), q = (tid >> 4) & 3;
-    const bool srow = j < 16 * WFS_TILES;
-    const int frag = ((j & 15) + 16 * q) * 16 + (j >> 4) * 1024;   // fragment-major LDS offset of the piece
-    uint32_t pm[4], pmb[4];
-    pad_mask<T>(8 * q, a.B, pm);
-    pad_mask<T>(g8, a.B, pmb);
-    if (nc >= a.G) pmb[0] = pmb[1] = pmb[2] = pmb[3] = 0u;
-    const uint32_t boff = (uint32_t)(min(nc, a.G - 1) * a.BP + g8) * 2;
+    // staging: piece i = tid + NTH*p is row j of the pass, 8-entry part q
+    // (lane l of a wave takes fragment position l of a 16-row tile: its LDS
+    // stores are free of bank conflicts)
+    int sj[PP], sfrag[PP];
+    uint32_t pm[PP][4];
+#pragma unroll
+    for (int p = 0; p < PP; ++p) {
+        const int i = tid + NTH * p, j = (i & 15) + 16 * (i >> 6), q = (i >> 4) & 3;
+        sj[p] = j < 16 * WFS_TILES ? j : -1;
+        sfrag[p] = ((j & 15) + 16 * q) * 16 + (j >> 4) * 1024;   // fragment-major LDS offset of the piece
+        pad_mask<T>(8 * q, a.B, pm[p]);
+    }
+    uint32_t pmb[CT][4], boff[CT];
+#pragma unroll
+    for (int h = 0; h < CT; ++h) {
+        pad_mask<T>(g8, a.B, pmb[h]);
+        if (nc[h] >= a.G) pmb[h][0] = pmb[h][1] = pmb[h][2] = pmb[h][3] = 0u;
+        boff[h] = (uint32_t)(min(nc[h], a.G - 1) * a.BP + g8) * 2;
+    }
     const uint32_t abytes = (uint32_t)a.K * a.BP * 2, bbytes = (uint32_t)a.G * a.BP * 2;
     const bool dbw = a.db && x == NXCD - 1;                        // (the last slice is never empty)
     const bool masked = MASKED || a.fullmask;                      // dropped rows zeroed by the mask byte
-    float dbacc = 0.0f;
+    float dbacc[CT];
+#pragma unroll
+    for (int h = 0; h < CT; ++h) dbacc[h] = 0.0f;
     auto act_rsrc = [&](int t) {
         const T* act = (a.actT_first && t == a.t_first) ? (const T*)a.actT_first
                                                         : (const T*)a.actT + (long)(t + a.shift) * a.tstride;
@@ -1190,44 +1206,65 @@ __device__ __forceinline__ void wgrad_full_staged(const WgArgs& a, float* lds) {
     for (int rp = r0; rp < r1; rp += 16 * WFS_TILES) {            // passes over the slice's rows
         const int nt = min(WFS_TILES, (r1 - rp + 15) >> 4);        // row tiles of the pass
         const bool first = rp == r0 && dbw;                        // (the bias gradient: first pass)
-        const int row = rp + j;
-        const bool rok = srow && row < r1;
-        uint4 ra[WFS_RING];
-        Raw8<T> rb[WFS_RING];
-        int mk[WFS_RING];
+        bool rok[PP];
+#pragma unroll
+        for (int p = 0; p < PP; ++p) rok[p] = sj[p] >= 0 && rp + sj[p] < r1;
+        uint4 ra[WFS_RING][PP];
+        Raw8<T> rb[WFS_RING][CT];
+        int mk[WFS_RING][PP];
         auto issue = [&](int t, int sl) {
             t = t < a.T ? t : a.T - 1;
-            const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(
-                act_rsrc(t), rok ? (uint32_t)(row * a.BP + 8 * q) * 2 : OOB_OFF, 0, 0);
-            ra[sl] = make_uint4(v[0], v[1], v[2], v[3]);
-            raw_load(rb[sl], buf_rsrc((const T*)a.daT + (size_t)t * a.G * a.BP, bbytes), boff);
-            // (always issued, past the resource when unmasked: a load under a
-            // branch would make the compiler wait for every load on its own)
+            const __amdgpu_buffer_rsrc_t ar = act_rsrc(t);
+            // (the mask load is always issued, past the resource when
+            // unmasked: a load under a branch would make the compiler wait
+            // for every load on its own)
             const __amdgpu_buffer_rsrc_t mr = buf_rsrc(a.site.mask + (size_t)t * a.site.kmax, (uint32_t)a.site.kmax);
-            mk[sl] = (int)__builtin_amdgcn_raw_buffer_load_b8(mr, masked && rok ? (uint32_t)row : OOB_OFF, 0, 0);
+#pragma unroll
+            for (int p = 0; p < PP; ++p) {
+                const int row = rp + sj[p], q = ((tid + NTH * p) >> 4) & 3;
+                const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(
+                    ar, rok[p] ? (uint32_t)(row * a.BP + 8 * q) * 2 : OOB_OFF, 0, 0);
+                ra[sl][p] = make_uint4(v[0], v[1], v[2], v[3]);
+                mk[sl][p] = (int)__builtin_amdgcn_raw_buffer_load_b8(mr, masked && rok[p] ? (uint32_t)row : OOB_OFF, 0, 0);
+            }
+            const __amdgpu_buffer_rsrc_t br = buf_rsrc((const T*)a.daT + (size_t)t * a.G * a.BP, bbytes);
+#pragma unroll
+            for (int h = 0; h < CT; ++h) raw_load(rb[sl][h], br, boff[h]);
         };
         auto stage = [&](int buf, int sl) {
-            if (srow) {
-                uint4 v = make_uint4(ra[sl].x & pm[0], ra[sl].y & pm[1], ra[sl].z & pm[2], ra[sl].w & pm[3]);
-                if (masked && !mk[sl]) v = make_uint4(0u, 0u, 0u, 0u);
-                *(uint4*)(stg + buf * (WFS_TILES * 1024) + frag) = v;
-            }
-        };
-        f32x4_t acc[WFS_TILES];
 #pragma unroll
-        for (int i = 0; i < WFS_TILES; ++i) acc[i] = f32x4_t{0, 0, 0, 0};
+            for (int p = 0; p < PP; ++p)
+                if (sj[p] >= 0) {
+                    uint4 v = make_uint4(ra[sl][p].x & pm[p][0], ra[sl][p].y & pm[p][1], ra[sl][p].z & pm[p][2],
+                                         ra[sl][p].w & pm[p][3]);
+                    if (masked && !mk[sl][p]) v = make_uint4(0u, 0u, 0u, 0u);
+                    *(uint4*)(stg + buf * (WFS_TILES * 1024) + sfrag[p]) = v;
+                }
+        };
+        f32x4_t acc[WFS_TILES][CT];
+#pragma unroll
+        for (int i = 0; i < WFS_TILES; ++i)
+#pragma unroll
+            for (int h = 0; h < CT; ++h) acc[i][h] = f32x4_t{0, 0, 0, 0};
         auto compute = [&](int buf, int sl) {
-            Raw8<T> fb = rb[sl];
-            raw_and(fb, pmb);
-            if (first) db_add_raw(fb, dbacc);
+            Raw8<T> fb[CT];
+#pragma unroll
+            for (int h = 0; h < CT; ++h) {
+                fb[h] = rb[sl][h];
+                raw_and(fb[h], pmb[h]);
+                if (first) db_add_raw(fb[h], dbacc[h]);
+            }
             const char* sb = stg + buf * (WFS_TILES * 1024);
+            // every tile, also past nt (their accumulators are never written
+            // out): the LDS reads then go out together instead of one read,
+            // wait and product at a time behind a branch
+            Raw8<T> fa[WFS_TILES];
+#pragma unroll
+            for (int i = 0; i < WFS_TILES; ++i) raw_lds(fa[i], (const T*)(sb + i * 1024 + lane * 16));
 #pragma unroll
             for (int i = 0; i < WFS_TILES; ++i)
-                if (i < nt) {
-                    Raw8<T> fa;
-                    raw_lds(fa, (const T*)(sb + i * 1024 + lane * 16));
-                    raw_mma(fb, fa, acc[i]);
-                }
+#pragma unroll
+                for (int h = 0; h < CT; ++h) raw_mma(fb[h], fa[i], acc[i][h]);
         };
         // step t: stage t+1 (its loads went out two steps earlier), multiply
         // t, then its slot takes the loads of t+3
@@ -1246,27 +1283,35 @@ __device__ __forceinline__ void wgrad_full_staged(const WgArgs& a, float* lds) {
             for (int i = 0; i < WFS_RING; ++i) iter(t + i, i);
         }
         // (transposed products) output r of this lane is gradient column
-        // 4*(lane/16)+r of the wave's tile, in the lane's own row
-        const int nq = n0 + 16 * w + 4 * (lane >> 4);
+        // 4*(lane/16)+r of tile h, in the lane's own row
 #pragma unroll
-        for (int i = 0; i < WFS_TILES; ++i) {
-            const int orow = rp + 16 * i + (lane & 15);
-            if (i < nt && orow < r1) {
-                float* o = a.out + (size_t)orow * a.G + nq;
-                if (nq + 3 < a.G) {
-                    *(float4*)o = make_float4(a.s * acc[i][0], a.s * acc[i][1], a.s * acc[i][2], a.s * acc[i][3]);
-                } else {
+        for (int h = 0; h < CT; ++h) {
+            const int nq = n0 + 16 * (CT * w + h) + 4 * (lane >> 4);
 #pragma unroll
-                    for (int r = 0; r < 4; ++r)
-                        if (nq + r < a.G) o[r] = a.s * acc[i][r];
+            for (int i = 0; i < WFS_TILES; ++i) {
+                const int orow = rp + 16 * i + (lane & 15);
+                if (i < nt && orow < r1) {
+                    float* o = a.out + (size_t)orow * a.G + nq;
+                    if (nq + 3 < a.G) {
+                        *(float4*)o = make_float4(a.s * acc[i][h][0], a.s * acc[i][h][1], a.s * acc[i][h][2],
+                                                  a.s * acc[i][h][3]);
+                    } else {
+#pragma unroll
+                        for (int r = 0; r < 4; ++r)
+                            if (nq + r < a.G) o[r] = a.s * acc[i][h][r];
+                    }
                 }
             }
         }
     }
     if (dbw) {                                                     // lanes l, l+16, l+32, l+48 hold column l
-        dbacc += __shfl_xor(dbacc, 16);
-        dbacc += __shfl_xor(dbacc, 32);
-        if (lane < 16 && nc < a.G) a.db[nc] = dbacc;
+#pragma unroll
+        for (int h = 0; h < CT; ++h) {
+            float v = dbacc[h];
+            v += __shfl_xor(v, 16);
+            v += __shfl_xor(v, 32);
+            if (lane < 16 && nc[h] < a.G) a.db[nc[h]] = v;
+        }
     }
 }
 
@@ -1494,19 +1539,26 @@ __global__ void __launch_bounds__(128 * WG_NWV) __attribute__((amdgpu_waves_per_
     } else wgrad_gather<T, MULTI>(a, acc_lds);
 }
 
+// 4 waves of 2 column tiles: each row fragment read from LDS feeds two
+// products (8 waves of one tile: 43 us at LM-medium against 41), 145
+// registers, 3 waves per SIMD, 3 workgroups per CU
+constexpr int WFS_FS_CT = 2;
+constexpr int WFS_FS_THREADS = 512 / WFS_FS_CT;
+constexpr int WFS_FS_WPE = 3;
+
 // The same pass when every problem runs on the staged full kernel (bf16,
-// batch <= 32): built on its own for six waves per SIMD (80 registers), i.e.
-// three workgroups per CU, so that a pass's workgroups (the grid is 64 per
-// 1024 gradient columns and problem) mostly run in one round.
+// batch <= 32): built on its own for three workgroups per CU, so that a
+// pass's workgroups (the grid is 64 per 1024 gradient columns and problem)
+// mostly run in one round.
 template <bool MASKED>
-__global__ void __launch_bounds__(128 * WG_NWV) __attribute__((amdgpu_waves_per_eu(6))) k_wgrad_fs(WgBatch bt) {
+__global__ void __launch_bounds__(WFS_FS_THREADS) __attribute__((amdgpu_waves_per_eu(WFS_FS_WPE))) k_wgrad_fs(WgBatch bt) {
     extern __shared__ float stage_lds[];
     const WgArgs& a = bt.p[blockIdx.z];
     if (bt.status && *bt.status != 0) {
         wgrad_poison(a);
         return;
     }
-    wgrad_full_staged<bf16, MASKED>(a, stage_lds);
+    wgrad_full_staged<bf16, MASKED, WFS_FS_CT>(a, stage_lds);
 }
 
 // ---------------------------------------------------------------------------
@@ -2167,8 +2219,9 @@ void launch_wgrad(const WgBatch& b, hipStream_t st) {
     bool all_fs = sizeof(T) == 2;
     for (int i = 0; i < bs.np; ++i) all_fs = all_fs && bs.p[i].full && bs.p[i].staged;
     if (all_fs) {
-        if (a.dense) launch_k(KID_WGRAD, k_wgrad_fs<true>, grid, blk, WFS_LDS, st, bs);
-        else launch_k(KID_WGRAD, k_wgrad_fs<false>, grid, blk, WFS_LDS, st, bs);
+        const dim3 bfs(WFS_FS_THREADS);
+        if (a.dense) launch_k(KID_WGRAD, k_wgrad_fs<true>, grid, bfs, WFS_LDS, st, bs);
+        else launch_k(KID_WGRAD, k_wgrad_fs<false>, grid, bfs, WFS_LDS, st, bs);
         return;
     }
     if (a.dense) {
