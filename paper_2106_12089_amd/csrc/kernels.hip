@@ -1190,7 +1190,7 @@ __device__ __forceinline__ void wgrad_full_staged(const WgArgs& a, float* lds) {
     for (int h = 0; h < CT; ++h) {
         pad_mask<T>(g8, a.B, pmb[h]);
         if (nc[h] >= a.G) pmb[h][0] = pmb[h][1] = pmb[h][2] = pmb[h][3] = 0u;
-        boff[h] = (uint32_t)(min(nc[h], a.G - 1) * a.BP + g8) * 2;
+        boff[h] = g8 < a.B ? (uint32_t)(min(nc[h], a.G - 1) * a.BP + g8) * 2 : OOB_OFF;   // (as the row pieces)
     }
     const uint32_t abytes = (uint32_t)a.K * a.BP * 2, bbytes = (uint32_t)a.G * a.BP * 2;
     const bool dbw = a.db && x == NXCD - 1;                        // (the last slice is never empty)
@@ -1209,6 +1209,11 @@ __device__ __forceinline__ void wgrad_full_staged(const WgArgs& a, float* lds) {
         bool rok[PP];
 #pragma unroll
         for (int p = 0; p < PP; ++p) rok[p] = sj[p] >= 0 && rp + sj[p] < r1;
+        // pieces wholly past the batch (entries 24-31 at B <= 24) read 0
+        // without moving data, like rows past the slice
+        bool aok[PP];
+#pragma unroll
+        for (int p = 0; p < PP; ++p) aok[p] = rok[p] && 8 * (((tid + NTH * p) >> 4) & 3) < a.B;
         uint4 ra[WFS_RING][PP];
         Raw8<T> rb[WFS_RING][CT];
         int mk[WFS_RING][PP];
@@ -1223,7 +1228,7 @@ __device__ __forceinline__ void wgrad_full_staged(const WgArgs& a, float* lds) {
             for (int p = 0; p < PP; ++p) {
                 const int row = rp + sj[p], q = ((tid + NTH * p) >> 4) & 3;
                 const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(
-                    ar, rok[p] ? (uint32_t)(row * a.BP + 8 * q) * 2 : OOB_OFF, 0, 0);
+                    ar, aok[p] ? (uint32_t)(row * a.BP + 8 * q) * 2 : OOB_OFF, 0, 0);
                 ra[sl][p] = make_uint4(v[0], v[1], v[2], v[3]);
                 mk[sl][p] = (int)__builtin_amdgcn_raw_buffer_load_b8(mr, masked && rok[p] ? (uint32_t)row : OOB_OFF, 0, 0);
             }
