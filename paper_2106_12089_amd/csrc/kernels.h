@@ -87,7 +87,7 @@ struct StepDir {
     const uint8_t* mask;                // RH site row at t
     const int32_t* keep;
     const int32_t* count;               // -> count_t
-    float* gates;                       // [B][4H]
+    float* gates;                       // [B][H][4] (the four gates of a unit together)
     float* cres;                        // [B][H]
     void* hrec;                         // [B][H] row-major h_t (dtype)
     void* hrecT;                        // [H][BP] h_t transposed (dtype)
@@ -120,7 +120,7 @@ struct BwdDir {
     const int32_t* ndseg;               // [17] segment offsets of ndrop
     const void* U;                      // [H][G]
     // pointwise at t
-    const float* gates;                 // [B][G]
+    const float* gates;                 // [B][H][4]
     const float* cres;                  // c_t [B][H]
     const float* cprev;                 // c_prev [B][H]
     const float* dy;                    // top layer: rows + d*H (ld ldy), or null
@@ -192,7 +192,7 @@ struct PFwdDir {
     const float* gx;                    // [T][B][4H] input product incl. bias
     const float* c0;                    // [B][H]
     SiteView rh;                        // RH site of (l, d)
-    float* gates;                       // [T][B][4H]
+    float* gates;                       // [T][B][H][4] (the four gates of a unit together)
     float* cres;                        // [T][B][H]
     void* hrecT;                        // [T][H][BP]
     void* hx;                           // [2] fragment-major slots: h_t compacted by the next step's keep list
@@ -261,7 +261,7 @@ struct PFwdArgs {
 struct PBwdDir {
     const void* U;                      // [H][4H]
     SiteView rh;                        // RH site of (l, d)
-    const float* gates;                 // [T][B][4H]
+    const float* gates;                 // [T][B][H][4]
     const float* cres;                  // [T][B][H]
     const float* c0;                    // [B][H]
     const float* dy;                    // top layer: dy + d*H (rows ld ldy, t stride B*ldy), or null

@@ -414,8 +414,7 @@ __global__ void __launch_bounds__(1024) k_step(StepArgs a) {
             const float cn = fg * cp + ig * gg;
             const float hn = og * tanh_fast(cn);
             const bool valid = (a.lengths == nullptr) || (D.t < a.lengths[b]);
-            float* gt = D.gates + (size_t)b * G;
-            gt[u] = ig; gt[H + u] = fg; gt[2 * H + u] = gg; gt[3 * H + u] = og;
+            *(float4*)(D.gates + (size_t)b * G + 4 * u) = make_float4(ig, fg, gg, og);
             D.cres[(size_t)b * H + u] = valid ? cn : cp;
             const T hv = valid ? from_f32<T>(hn) : hp[(size_t)b * H + u];
             ((T*)D.hrec)[(size_t)b * H + u] = hv;
@@ -541,8 +540,8 @@ __global__ void __launch_bounds__(1024) k_bwd(BwdArgs a) {
             }
             const float dcin = D.dcs[(size_t)b * H + u];
             if (valid) {
-                const float* gt = D.gates + (size_t)b * G;
-                const float ig = gt[u], fg = gt[H + u], gg = gt[2 * H + u], og = gt[3 * H + u];
+                const float4 gt = *(const float4*)(D.gates + (size_t)b * G + 4 * u);
+                const float ig = gt.x, fg = gt.y, gg = gt.z, og = gt.w;
                 const float ct = D.cres[(size_t)b * H + u];
                 const float cp = D.cprev[(size_t)b * H + u];
                 const float tc = tanh_fast(ct);

@@ -484,8 +484,7 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
             const bool vq = is_valid(q, t);
             const float cp = creg[q], cn = vq ? cnv[q] : cp, hn = hnv[q];
             const T hv = from_f32<T>(vq ? hn : hreg[q]);
-            float* gt = D.gates + ((size_t)t * B + b) * G;
-            gt[u] = og4[q][0]; gt[H + u] = og4[q][1]; gt[2 * H + u] = og4[q][2]; gt[3 * H + u] = og4[q][3];
+            *(float4*)(D.gates + ((size_t)t * B + b) * G + 4 * u) = make_float4(og4[q][0], og4[q][1], og4[q][2], og4[q][3]);
             D.cres[((size_t)t * B + b) * H + u] = cn;
             if (vq) { creg[q] = cnv[q]; hreg[q] = hn; }
             ((T*)D.hrecT)[((size_t)t * H + u) * a.BP + b] = hv;
@@ -607,9 +606,8 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
         for (int q = 0; q < PPT; ++q) {
             const int bc = min(pb[q], B - 1), uc = min(pu[q], H - 1);
             lenr[q] = a.lengths ? a.lengths[bc] : T_;
-            const float* gr = D.gates + ((size_t)t * B + bc) * G;
-#pragma unroll
-            for (int g = 0; g < 4; ++g) gt4[q][g] = gr[g * H + uc];
+            const float4 gr = *(const float4*)(D.gates + ((size_t)t * B + bc) * G + 4 * uc);
+            gt4[q][0] = gr.x; gt4[q][1] = gr.y; gt4[q][2] = gr.z; gt4[q][3] = gr.w;
             ctv[q] = D.cres[((size_t)t * B + bc) * H + uc];
             cpv[q] = *(s >= T_ - 1 ? D.c0 + (size_t)bc * H + uc : D.cres + ((size_t)tp * B + bc) * H + uc);
             if (D.dy) dyr[q] = D.dy[((size_t)t * B + bc) * a.ldy + uc];
@@ -1026,8 +1024,7 @@ __global__ void __launch_bounds__(512) k_fwd_big(PFwdArgs a) {
             const bool vq = t < lenr[q];
             const float cn = vq ? cnv[q] : creg[q], hn = hnv[q];
             const bf16 hv = f2bf(vq ? hn : hreg[q]);
-            float* gt = D.gates + ((size_t)t * B + b) * G;
-            gt[u] = og4[q][0]; gt[H + u] = og4[q][1]; gt[2 * H + u] = og4[q][2]; gt[3 * H + u] = og4[q][3];
+            *(float4*)(D.gates + ((size_t)t * B + b) * G + 4 * u) = make_float4(og4[q][0], og4[q][1], og4[q][2], og4[q][3]);
             D.cres[((size_t)t * B + b) * H + u] = cn;
             if (vq) { creg[q] = cnv[q]; hreg[q] = hn; }
             ((bf16*)D.hrecT)[((size_t)t * H + u) * a.BP + b] = hv;
@@ -1145,9 +1142,8 @@ __global__ void __launch_bounds__(512) k_bwd_big(PBwdArgs a) {
 #pragma unroll
         for (int q = 0; q < PPT; ++q) {
             const int bc = min(pb[q], B - 1), uc = min(pu[q], H - 1);
-            const float* gr = D.gates + ((size_t)t * B + bc) * G;
-#pragma unroll
-            for (int g = 0; g < 4; ++g) gt4[q][g] = gr[g * H + uc];
+            const float4 gr = *(const float4*)(D.gates + ((size_t)t * B + bc) * G + 4 * uc);
+            gt4[q][0] = gr.x; gt4[q][1] = gr.y; gt4[q][2] = gr.z; gt4[q][3] = gr.w;
             ctv[q] = D.cres[((size_t)t * B + bc) * H + uc];
             cpv[q] = *(s >= T_ - 1 ? D.c0 + (size_t)bc * H + uc : D.cres + ((size_t)tp * B + bc) * H + uc);
             if (D.dy) {
