@@ -4,7 +4,8 @@ kernel for identity keep lists, the dense mode and row-sparse problems
 whose kept fraction is high; the default wherever they apply) on ragged
 shapes: weight heights whose slices are 1, 16-17 or 95 rows, gate
 widths that end inside a 128-column block, batches below the 32-entry
-chunk, sequences shorter than its two-step lookahead, both directions, and
+chunk (27: the last 8-entry piece of a row partly valid, 17 and 20: past
+the batch and never loaded), sequences shorter than its two-step lookahead, both directions, and
 rates that leave steps with no kept row (an 8-wide input at p = 0.9).  Each
 case runs a whole step against the oracle, with each row-sparse problem
 on either kernel (LSTM_SD_WGRAD_ROWSPARSE=1, 0) and on the unstaged ones
@@ -43,6 +44,7 @@ SHAPES = [
     dict(num_layers=2, num_dirs=1, input_dim=760, hidden=40, batch=20, seq_len=7),
     dict(num_layers=1, num_dirs=1, input_dim=8, hidden=250, batch=17, seq_len=70),
     dict(num_layers=1, num_dirs=2, input_dim=64, hidden=20, batch=3, seq_len=6, min_len=0),
+    dict(num_layers=2, num_dirs=1, input_dim=97, hidden=70, batch=27, seq_len=5),
 ]
 
 
