@@ -160,12 +160,15 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
         const int t = step_t(sc);
         const bool has_next = sc + 1 < T_;
         const int tn = has_next ? step_t(sc + 1) : t;
-        cnt_next = D.rh.count[t];
+        // (counts made wave-uniform: the buffer resources sized by them are
+        // then scalar; a count from a vector load wrapped every exchange
+        // load in a loop over the resource's distinct values)
+        cnt_next = __builtin_amdgcn_readfirstlane(D.rh.count[t]);
         const int32_t* krow = D.rh.keep + (size_t)t * D.rh.kmax;
 #pragma unroll
         for (int i = 0; i < KPT; ++i) kreg[i] = krow[min(tid + NTH * i, D.rh.kmax - 1)];
         if (has_x) {
-            cnt_x_next = D.nr.count[t];
+            cnt_x_next = __builtin_amdgcn_readfirstlane(D.nr.count[t]);
             const int32_t* kx = D.nr.keep + (size_t)t * D.nr.kmax;
 #pragma unroll
             for (int i = 0; i < KPT; ++i) kreg_x[i] = kx[min(tid + NTH * i, D.nr.kmax - 1)];
