@@ -773,9 +773,19 @@ __global__ void __launch_bounds__(1024) k_bwd_persist(PBwdArgs a) {
             } else {
                 dhc[q] = dh;                                           // frozen row: pass through
             }
-            T* dar = (T*)D.da + (size_t)t * das;
+            // coherent stores (SC1, as xstore) through the step's block with
+            // 32-bit offsets: a 64-bit element address kept across the step
+            // had been spilled to scratch and reloaded here, on the path to
+            // the arrival
+            const __amdgpu_buffer_rsrc_t dw = buf_rsrc((const T*)D.da + (size_t)t * das, (uint32_t)(das * sizeof(T)));
 #pragma unroll
-            for (int g = 0; g < 4; ++g) xstore(dar + frag_off(b, g * H + u, a.mtiles), from_f32<T>(da4[q][g]));
+            for (int g = 0; g < 4; ++g) {
+                const uint32_t o = (uint32_t)frag_off(b, g * H + u, a.mtiles) * (uint32_t)sizeof(T);
+                if constexpr (sizeof(T) == 2)
+                    __builtin_amdgcn_raw_buffer_store_b16(from_f32<T>(da4[q][g]), dw, o, 0, CPOL_SC1);
+                else
+                    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(da4[q][g]), dw, o, 0, CPOL_SC1);
+            }
         }
         if (final_pass) break;
         grid_arrive(bar);                                  // DA_t is published
