@@ -471,10 +471,12 @@ __global__ void __launch_bounds__(512) k_fwd_persist(PFwdArgs a) {
             hnv[q] = og4[q][3] * tanh_fast(cnv[q]);
             const bool vq = is_valid(q, t);
             const T hv = from_f32<T>(vq ? hnv[q] : hreg[q]);
-            if (pn[q] >= 0) xstore(hxn + frag_off(b, pn[q], a.mtiles), (a.dense && !mnr[q]) ? zero_val<T>() : hv);
+            // (coherent buffer stores at 32-bit offsets, as xstore)
+            if (pn[q] >= 0)
+                store_coherent(hxn, hxs, (uint32_t)frag_off(b, pn[q], a.mtiles), (a.dense && !mnr[q]) ? zero_val<T>() : hv);
             if (D.xout && pup[q] >= 0) {
                 const T yv = (vq && !(a.dense && !mup[q])) ? from_f32<T>(hnv[q]) : zero_val<T>();
-                xstore((T*)D.xout + (size_t)t * a.xxs + frag_off(b, pup[q], a.mtiles), yv);
+                store_coherent((T*)D.xout + (size_t)t * a.xxs, a.xxs, (uint32_t)frag_off(b, pup[q], a.mtiles), yv);
             }
         }
         grid_arrive(bar);

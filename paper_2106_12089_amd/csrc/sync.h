@@ -141,6 +141,15 @@ __device__ __forceinline__ void grid_exit(unsigned* bar, int nslots, int* err) {
     }
 }
 
+// coherent store of element i of a buffer of n elements: a buffer store with
+// the device-coherence bit (as xstore) at a 32-bit offset
+__device__ __forceinline__ void store_coherent(bf16* base, size_t n, uint32_t i, bf16 v) {
+    __builtin_amdgcn_raw_buffer_store_b16(v, buf_rsrc(base, (uint32_t)(n * 2)), i * 2u, 0, CPOL_SC1);
+}
+__device__ __forceinline__ void store_coherent(float* base, size_t n, uint32_t i, float v) {
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), buf_rsrc(base, (uint32_t)(n * 4)), i * 4u, 0, CPOL_SC1);
+}
+
 // coherent (agent-scope) element store and 8-element load of exchange data
 __device__ __forceinline__ void xstore(bf16* p, bf16 v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
