@@ -662,7 +662,17 @@ __global__ void __launch_bounds__(512) k_wgrad_gemm(WgBatch bt) {
     for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int c = 0; c < 4; ++c) acc[i][c] = f32x4_t{0, 0, 0, 0};
-    float dbacc[4] = {0.f, 0.f, 0.f, 0.f};
+    // the bias gradient (the last row block's waves 0-3): each DA^T fragment
+    // times a fragment of ones, i.e. its column sums over the chunk's batch
+    // entries, on the matrix cores (unpacking and adding the bf16 pairs took
+    // 64 vector instructions per chunk, and those workgroups set the
+    // kernel's time)
+    f32x4_t dbacc[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) dbacc[c] = f32x4_t{0, 0, 0, 0};
+    Raw8<bf16> ones;
+#pragma unroll
+    for (int q = 0; q < Raw8<bf16>::NW; ++q) ones.w[q] = 0x3f803f80u;     // bf16 1.0, twice
     // fragments of two chunks in registers: those of chunk q+1 are read
     // from LDS while chunk q is multiplied
     Raw8<bf16> fa[2][4], fb[2][4];
@@ -674,9 +684,9 @@ __global__ void __launch_bounds__(512) k_wgrad_gemm(WgBatch bt) {
         for (int i = 0; i < 4; ++i) raw_lds(fa[fs][i], (const bf16*)(sb + (4 * wr + i) * 1024 + lane * 16));
     };
     auto multiply = [&](int fs) {
+        if (dbw && wr == 0)
 #pragma unroll
-        for (int c = 0; c < 4; ++c)
-            if (dbw && wr == 0) db_add_raw(fb[fs][c], dbacc[c]);
+            for (int c = 0; c < 4; ++c) raw_mma(fb[fs][c], ones, dbacc[c]);
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -724,15 +734,14 @@ __global__ void __launch_bounds__(512) k_wgrad_gemm(WgBatch bt) {
             }
         }
     }
-    if (dbw && wr == 0) {                      // lanes l, l+16, l+32, l+48 hold column l of each tile
+    if (dbw && wr == 0 && (lane & 15) == 0) {  // (every output column holds the same sums) output r of
+#pragma unroll                                 // lane 16j is the sum of tile column 4j+r
+        for (int c = 0; c < 4; ++c)
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            float v = dbacc[c];
-            v += __shfl_xor(v, 16);
-            v += __shfl_xor(v, 32);
-            const int n = n0 + 64 * wc + 16 * c + (lane & 15);
-            if (lane < 16 && n < a.G) a.db[n] = v;
-        }
+            for (int r = 0; r < 4; ++r) {
+                const int n = n0 + 64 * wc + 16 * c + 4 * (lane >> 4) + r;
+                if (n < a.G) a.db[n] = dbacc[c][r];
+            }
     }
 }
 
