@@ -1194,9 +1194,14 @@ __device__ __forceinline__ void wgrad_full_staged(const WgArgs& a, float* lds) {
     const uint32_t abytes = (uint32_t)a.K * a.BP * 2, bbytes = (uint32_t)a.G * a.BP * 2;
     const bool dbw = a.db && x == NXCD - 1;                        // (the last slice is never empty)
     const bool masked = MASKED || a.fullmask;                      // dropped rows zeroed by the mask byte
-    float dbacc[CT];
+    // the bias gradient (the last slice's workgroups): each DA^T fragment
+    // times a fragment of ones, i.e. its column sums, on the matrix cores
+    f32x4_t dbacc[CT];
 #pragma unroll
-    for (int h = 0; h < CT; ++h) dbacc[h] = 0.0f;
+    for (int h = 0; h < CT; ++h) dbacc[h] = f32x4_t{0, 0, 0, 0};
+    Raw8<T> ones;
+#pragma unroll
+    for (int q = 0; q < Raw8<T>::NW; ++q) ones.w[q] = 0x3f803f80u;       // bf16 1.0, twice
     auto act_rsrc = [&](int t) {
         const T* act = (a.actT_first && t == a.t_first) ? (const T*)a.actT_first
                                                         : (const T*)a.actT + (long)(t + a.shift) * a.tstride;
@@ -1256,7 +1261,7 @@ __device__ __forceinline__ void wgrad_full_staged(const WgArgs& a, float* lds) {
             for (int h = 0; h < CT; ++h) {
                 fb[h] = rb[sl][h];
                 raw_and(fb[h], pmb[h]);
-                if (first) db_add_raw(fb[h], dbacc[h]);
+                if (first) raw_mma(fb[h], ones, dbacc[h]);
             }
             const char* sb = stg + buf * (WFS_TILES * 1024);
             // every tile, also past nt (their accumulators are never written
@@ -1308,14 +1313,14 @@ __device__ __forceinline__ void wgrad_full_staged(const WgArgs& a, float* lds) {
             }
         }
     }
-    if (dbw) {                                                     // lanes l, l+16, l+32, l+48 hold column l
+    if (dbw && (lane & 15) == 0) {                                 // output r of lane 16j: column 4j+r's sum
 #pragma unroll
-        for (int h = 0; h < CT; ++h) {
-            float v = dbacc[h];
-            v += __shfl_xor(v, 16);
-            v += __shfl_xor(v, 32);
-            if (lane < 16 && nc[h] < a.G) a.db[nc[h]] = v;
-        }
+        for (int h = 0; h < CT; ++h)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int n = n0 + 16 * (CT * w + h) + 4 * (lane >> 4) + r;
+                if (n < a.G) a.db[n] = dbacc[h][r];
+            }
     }
 }
 
