@@ -113,14 +113,17 @@ def test_wgrad_staged_repeats_bit_identical():
 
 
 @pytest.mark.parametrize("mode", [(0.5, 0.5, 1), (0.5, 0.5, 0), (0.3, 0.0, 1)])
-def test_wgrad_batch_above_32_both_kernels(mode, monkeypatch):
+@pytest.mark.parametrize("hidden", [60, 33])
+def test_wgrad_batch_above_32_both_kernels(mode, hidden, monkeypatch):
     """A batch of 48 (bf16): the default mask-multiplied GEMM, and with
     LSTM_SD_WGRAD_GEMM=0 the unstaged kernels (the row-sparse scatter and the
-    full kernel, two 32-row batch chunks)."""
+    full kernel, two 32-row batch chunks); 4H = 240 or 132 gradient columns
+    (the last 16-column tile ragged: the bias gradient's columns past 4H are
+    not written)."""
     from oracle import masks as om
     base = workloads.get_config("tiny")
     cfg = dataclasses.replace(base, name="wgs", dtype="bf16", loss="mse", num_layers=2, num_dirs=1,
-                              input_dim=150, hidden=60, batch=48, seq_len=6)
+                              input_dim=150, hidden=hidden, batch=48, seq_len=6)
     wl = workloads.make_workload(cfg)
     p_nr, p_rh, compact = mode
     m_nr, m_rh = om.all_masks(cfg.mask_seed, 0, cfg.num_layers, cfg.num_dirs, cfg.seq_len, cfg.k_in,
