@@ -63,6 +63,7 @@ __global__ void __launch_bounds__(256) k_mask_build(MaskArgs a) {
     const int t = blockIdx.x, s = blockIdx.y, tid = threadIdx.x;
     const int K = a.K[s];
     __shared__ uint8_t sm[LSTM_SD_MAX_K];
+    __shared__ int kpre[LSTM_SD_MAX_K];        // kept entries before k (compact mode)
     __shared__ int wsum[4], wdrop[4];
     const size_t row = ((size_t)s * a.T + t) * a.kmax;
     uint8_t* mrow = a.mask + row;
@@ -125,12 +126,19 @@ __global__ void __launch_bounds__(256) k_mask_build(MaskArgs a) {
         if (k < K) {
             if (f) { krow[off + pre] = k; prow[k] = off + pre; }
             else { drow[doff + dpre] = k; prow[k] = -1; }
-            for (int x = 0; x < NSEG; ++x)
-                if (k == seg_start(x, K)) { ksrow[x] = off + pre; dsrow[x] = doff + dpre; }
+            kpre[k] = off + pre;
         }
         base += tot;
         dbase += dtot;
         __syncthreads();
+    }
+    // segment x starts at entry seg_start(x, K): its keep-list range starts
+    // at the number of kept entries before it, its drop-list range at the
+    // number dropped before it
+    if (tid < NSEG) {
+        const int sx = seg_start(tid, K);
+        ksrow[tid] = kpre[sx];
+        dsrow[tid] = sx - kpre[sx];
     }
     if (tid == 0) {
         a.count[(size_t)s * a.T + t] = base;
