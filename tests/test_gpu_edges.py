@@ -1,5 +1,5 @@
 """Edge cases of the HIP path against the oracle: ragged sizes that are not
-multiples of any tile, a single row and step, zero-length rows, rates of 0,
+multiples of any tile, contractions at the size limit, a single row and step, zero-length rows, rates of 0,
 forced mask patterns (a neuron never kept, a step with everything dropped,
 everything kept) and the dense/compact equivalence."""
 import dataclasses
@@ -56,6 +56,25 @@ def test_ragged_shapes(shape, dtype, mode):
     compact = 0 if mode.endswith("dense") else 1
     say(f"[gpu] ragged {shape} {dtype} {mode}")
     gpu, ref, _, _ = run_both(cfg, wl, 0.5, 0.5, compact)
+    errs = compare(gpu, ref)
+    assert max(errs.values()) <= TOL[dtype], errs
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("shape", [
+    dict(num_layers=2, num_dirs=2, input_dim=2048, hidden=1024, batch=5, seq_len=2),
+    dict(num_layers=1, num_dirs=1, input_dim=40, hidden=2048, batch=3, seq_len=2),
+    dict(num_layers=2, num_dirs=2, input_dim=2048, hidden=1024, batch=64, seq_len=2),
+    dict(num_layers=1, num_dirs=1, input_dim=64, hidden=2048, batch=64, seq_len=2),
+])
+def test_contractions_at_the_size_limit(shape, dtype):
+    """Every contraction length at the library's limit of 2048: the input
+    width and the stacked layer's input D*H, the recurrent H; at a small
+    batch and at 64 rows (the large-batch kernels, and for H = 2048 the
+    per-step recurrence that serves shapes past their register budget)."""
+    cfg, wl = make("kmax", dtype=dtype, loss="mse", **shape)
+    say(f"[gpu] size limit {shape} {dtype}")
+    gpu, ref, _, _ = run_both(cfg, wl, 0.5, 0.5, 1)
     errs = compare(gpu, ref)
     assert max(errs.values()) <= TOL[dtype], errs
 
