@@ -80,6 +80,19 @@ def test_contractions_at_the_size_limit(shape, dtype):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_long_sequence(dtype):
+    """257 steps, two stacked bidirectional layers: many barrier generations
+    of the persistent recurrences, and rounding carried through a long
+    forward and BPTT."""
+    cfg, wl = make("long", dtype=dtype, loss="mse", num_layers=2, num_dirs=2, input_dim=80, hidden=96,
+                   batch=21, seq_len=257)
+    say(f"[gpu] long sequence {dtype}")
+    gpu, ref, _, _ = run_both(cfg, wl, 0.5, 0.5, 1)
+    errs = compare(gpu, ref)
+    assert max(errs.values()) <= TOL[dtype], errs
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_lengths_with_zero_rows(dtype):
     cfg, wl = make("lens", dtype=dtype, loss="mse", num_layers=2, num_dirs=2, input_dim=24, hidden=20,
                    batch=6, seq_len=7, min_len=0)
