@@ -40,6 +40,7 @@ def _run(cfg, wl, p_nr, p_rh, compact):
     dict(num_layers=2, num_dirs=1, input_dim=64, hidden=1000, batch=130, seq_len=3),
     dict(num_layers=1, num_dirs=1, input_dim=33, hidden=512, batch=64, seq_len=6, min_len=0),
     dict(num_layers=2, num_dirs=2, input_dim=200, hidden=72, batch=300, seq_len=3),
+    dict(num_layers=1, num_dirs=2, input_dim=48, hidden=40, batch=1030, seq_len=3),
 ])
 @pytest.mark.parametrize("mode", [(0.5, 0.5, 1), (0.5, 0.5, 0), (0.3, 0.0, 1)])
 def test_big_forward_ragged(shape, mode, monkeypatch):
